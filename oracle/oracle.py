@@ -1,0 +1,159 @@
+"""Python front end of the fp64 CPU oracle (test infrastructure only).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this module.  It compiles ``fate_oracle.c`` with gcc
+on first use (or when the source is newer than the library), marshals a
+:class:`~paper_2605_07238_amd.synth.Workload`'s flat arrays into the C input
+record and returns plain numpy arrays.  It never touches the HIP library.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+import threading
+from typing import Dict, Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "fate_oracle.c")
+LIB = os.path.join(HERE, "libfate_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = False, src: str = SRC, out: str = LIB) -> str:
+    """Compile the oracle (plain C, fp64, OpenMP over instances)."""
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(src):
+        tmp = out + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-shared", "-fPIC", "-Wall", "-Wextra",
+               "-Wno-unused-parameter", src, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, out)
+    return out
+
+
+class _In(C.Structure):
+    _fields_ = [
+        ("D", C.c_int), ("M", C.c_int), ("K", C.c_int), ("H", C.c_int), ("max_shard", C.c_int),
+        ("exec", C.c_void_p), ("switch_s", C.c_void_p), ("beta", C.c_void_p),
+        ("weight", C.c_void_p), ("cap", C.c_void_p),
+        ("stage_off", C.c_void_p), ("par_off", C.c_void_p),
+        ("par_idx", C.c_void_p), ("model", C.c_void_p), ("shard", C.c_void_p),
+        ("elig", C.c_void_p), ("hash", C.c_void_p),
+        ("tokens", C.c_void_p), ("sigma", C.c_void_p),
+        ("resident", C.c_void_p), ("cache", C.c_void_p),
+        ("holders", C.c_void_p), ("status", C.c_void_p),
+        ("tau", C.c_void_p), ("t_now", C.c_void_p),
+        ("lam_q", C.c_double), ("lam_s", C.c_double), ("lam_tr", C.c_double),
+        ("lam_c", C.c_double), ("lam_p", C.c_double), ("kappa_prefix", C.c_double),
+        ("gamma", C.c_double),
+    ]
+
+
+def load(path: Optional[str] = None):
+    """Load (building if needed) the oracle library; ``path`` loads another
+    build of the same source (used by tests that plant mistakes)."""
+    global _lib
+    if path is not None:
+        lib = C.CDLL(path)
+        _bind(lib)
+        return lib
+    with _lock:
+        if _lib is None:
+            build()
+            _lib = C.CDLL(LIB)
+            _bind(_lib)
+    return _lib
+
+
+def _bind(lib):
+    lib.oracle_count.argtypes = [C.POINTER(_In), C.c_int, C.c_void_p, C.c_void_p]
+    lib.oracle_count.restype = C.c_int
+    lib.oracle_score.argtypes = [C.POINTER(_In), C.c_int, C.c_void_p, C.c_void_p, C.c_void_p,
+                                 C.c_void_p, C.c_void_p, C.c_void_p, C.c_int]
+    lib.oracle_score.restype = C.c_int
+    lib.oracle_topk.argtypes = [C.c_void_p, C.c_int64, C.c_int, C.c_void_p, C.c_void_p]
+    lib.oracle_topk.restype = C.c_int
+
+
+def f32(x: float) -> float:
+    """Round a parameter to float32, the precision the GPU receives it in."""
+    return float(np.float32(x))
+
+
+def _c(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+def score(w, params: Optional[Dict[str, float]] = None, H: Optional[int] = None,
+          max_shard: Optional[int] = None, threads: Optional[int] = None, lib=None) -> dict:
+    """Score every candidate of every frontier stage of workload ``w``.
+
+    Returns a dict with ``front_b``, ``front_v`` (instance-local ids),
+    ``cand_off`` ([n_frontier+1], global candidate offsets), ``psi`` and
+    ``mag`` (fp64, per candidate) and ``nf`` (frontier size per instance).
+    Parameters are rounded to float32 first, as the GPU path sees them.
+    """
+    lib = lib or load()
+    p = dict(w.params)
+    if params:
+        p.update(params)
+    keep = dict(
+        exec=_c(w.exec, np.float32), switch_s=_c(w.switch_s, np.float32), beta=_c(w.beta, np.float32),
+        weight=_c(w.weight_bytes, np.int64), cap=_c(w.cap_bytes, np.int64),
+        stage_off=_c(w.stage_off, np.int64), par_off=_c(w.par_off, np.int64),
+        par_idx=_c(w.par_idx, np.int32), model=_c(w.model, np.int32), shard=_c(w.shard_max, np.int32),
+        elig=_c(w.elig, np.uint64), hash=_c(w.prefix_hash, np.uint64),
+        tokens=_c(w.prefix_tokens, np.float32), sigma=_c(w.out_bytes, np.float32),
+        resident=_c(w.resident, np.uint64), cache=_c(w.prefix_cache, np.uint64),
+        holders=_c(w.holders, np.uint64), status=_c(w.status, np.uint8),
+        tau=_c(w.tau_free, np.float32), t_now=_c(w.t_now, np.float32),
+    )
+    rec = _In()
+    rec.D, rec.M, rec.K = int(w.D), int(w.M), int(w.K)
+    rec.H = int(w.H if H is None else H)
+    rec.max_shard = int(w.max_shard if max_shard is None else max_shard)
+    for k, a in keep.items():
+        setattr(rec, k, a.ctypes.data)
+    for k in ("lam_q", "lam_s", "lam_tr", "lam_c", "lam_p", "kappa_prefix", "gamma"):
+        setattr(rec, k, f32(p[k]))
+    B = w.B
+    nf = np.zeros(B, np.int64)
+    nc = np.zeros(B, np.int64)
+    lib.oracle_count(C.byref(rec), B, nf.ctypes.data, nc.ctypes.data)
+    f_off = np.zeros(B + 1, np.int64)
+    c_off = np.zeros(B + 1, np.int64)
+    f_off[1:] = np.cumsum(nf)
+    c_off[1:] = np.cumsum(nc)
+    F, NC = int(f_off[-1]), int(c_off[-1])
+    front_v = np.zeros(F, np.int32)
+    cand_off = np.zeros(F + 1, np.int64)
+    psi = np.zeros(NC, np.float64)
+    mag = np.zeros(NC, np.float64)
+    if threads is None:
+        threads = min(16, os.cpu_count() or 1)
+    rc = lib.oracle_score(C.byref(rec), B, f_off.ctypes.data, c_off.ctypes.data, front_v.ctypes.data,
+                          cand_off.ctypes.data, psi.ctypes.data, mag.ctypes.data, int(threads))
+    if rc != 0:
+        raise ValueError("oracle rejected the input (code %d)" % rc)
+    cand_off[F] = NC
+    front_b = np.repeat(np.arange(B, dtype=np.int32), nf)
+    return dict(front_b=front_b, front_v=front_v, cand_off=cand_off, psi=psi, mag=mag, nf=nf)
+
+
+def topk(res: dict, k: int, lib=None):
+    """Per-frontier-stage top-k of an oracle result: (idx [F,k], val [F,k])."""
+    lib = lib or load()
+    F = len(res["front_v"])
+    idx = np.full((F, k), -1, np.int32)
+    val = np.full((F, k), -np.inf, np.float64)
+    psi = res["psi"]
+    co = res["cand_off"]
+    for f in range(F):
+        seg = np.ascontiguousarray(psi[co[f]:co[f + 1]])
+        lib.oracle_topk(seg.ctypes.data, int(co[f + 1] - co[f]), int(k),
+                        idx[f].ctypes.data, val[f].ctypes.data)
+    return idx, val

@@ -1,0 +1,310 @@
+"""Checks that pin the fp64 oracle to the paper and to mathematics.
+
+Each ``check_*`` function raises AssertionError on a mismatch and takes an
+optional oracle library handle, so the same checks run against the real
+oracle (tests/test_oracle_pins.py) and against copies of it with a planted
+mistake (tests/test_oracle_mutants.py), which they must reject.
+
+Kinds of pins used here:
+* hand-derived values for small scenarios (tests/scenarios.py) and for the
+  worked example in tests/golden/worked_example.json;
+* closed-form reductions computed with numpy and scipy's breadth-first
+  shortest paths (only base runtimes, or only waiting costs, switched on);
+* invariants: device relabelling, H = 0 equals gamma = 0, stages outside the
+  horizon do not matter, an added isolated stage changes nothing else.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import json
+import os
+
+import numpy as np
+import scipy.sparse as sp
+from scipy.sparse.csgraph import shortest_path
+
+import builders
+import scenarios
+from oracle import oracle
+from paper_2605_07238_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _close(a, b, rtol=1e-12, atol=1e-12):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    assert a.shape == b.shape, (a.shape, b.shape)
+    inf_a, inf_b = np.isinf(a), np.isinf(b)
+    assert np.array_equal(inf_a, inf_b) and np.array_equal(a[inf_a], b[inf_b]), (a, b)
+    fa, fb = a[~inf_a], b[~inf_b]
+    assert np.allclose(fa, fb, rtol=rtol, atol=atol), (fa, fb, np.abs(fa - fb).max() if fa.size else 0)
+
+
+def check_scenario(name: str, lib=None):
+    sc = scenarios.ALL[name]
+    w = builders.from_spec(sc["spec"], H=sc["H"], params=sc["params"])
+    r = oracle.score(w, lib=lib)
+    assert list(r["front_v"]) == sc["front_v"], (list(r["front_v"]), sc["front_v"])
+    _close(r["psi"], sc["psi"], rtol=1e-12)
+    if "topk3" in sc:
+        idx, _ = oracle.topk(r, 3, lib=lib)
+        assert idx[0].tolist() == sc["topk3"], idx
+    if "topk4" in sc:
+        idx, val = oracle.topk(r, 4, lib=lib)
+        assert idx.tolist() == sc["topk4"], idx
+
+
+def check_worked_example(lib=None):
+    spec = json.load(open(os.path.join(GOLDEN, "worked_example.json")))
+    for key, H in (("H1", 1), ("H0", 0)):
+        exp = spec["expected"][key]
+        w = builders.from_spec(spec, H=H)
+        r = oracle.score(w, lib=lib)
+        assert list(r["front_v"]) == exp["front_v"]
+        # inputs such as 1.1 s are float32-rounded, hence 1e-6
+        _close(r["psi"], exp["psi"], rtol=1e-6, atol=0)
+        idx, _ = oracle.topk(r, 3, lib=lib)
+        assert idx[0].tolist() == exp["topk3"], idx
+
+
+# ---------------------------------------------------------------------------
+# closed-form reductions
+# ---------------------------------------------------------------------------
+
+def _frontier(w, b):
+    lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+    out = []
+    for v in range(hi - lo):
+        g = lo + v
+        ps = w.par_idx[w.par_off[g]:w.par_off[g + 1]]
+        if w.status[g] == 0 and all(w.status[lo + p] == 1 for p in ps):
+            out.append(v)
+    return out
+
+
+def _windows(D, r):
+    c = [(i, 1) for i in range(D)]
+    for k in range(2, r + 1):
+        c += [(i, k) for i in range(D - k + 1)]
+    return c
+
+
+def _feasible(w, g, d):
+    m = int(w.model[g])
+    return bool((int(w.elig[g]) >> d) & 1) and w.weight_bytes[m] <= w.cap_bytes[d]
+
+
+def check_exec_only_reduction(seed: int, lib=None, H: int = 3):
+    """With every weight but the base runtime at zero, the score is
+    -(max_{d in S} c(v,d)/|S| + sum_h gamma^h sum_{dist(v,w)=h} min_feasible c(w,.)).
+    Hop distances come from scipy's unweighted shortest paths."""
+    w = synth.make_random_small(seed, B=2, n=14, D=4, M=3, K=2, H=H, max_shard=3)
+    zero = dict(lam_q=0.0, lam_s=0.0, lam_tr=0.0, lam_c=0.0, lam_p=0.0, gamma=0.5)
+    r = oracle.score(w, params=zero, lib=lib)
+    gam = oracle.f32(0.5)
+    exp, fronts = [], []
+    for b in range(w.B):
+        lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+        n = hi - lo
+        rows, cols = [], []
+        for x in range(n):
+            g = lo + x
+            for p in w.par_idx[w.par_off[g]:w.par_off[g + 1]]:
+                rows.append(int(p))
+                cols.append(x)
+        adj = sp.csr_matrix((np.ones(len(rows)), (rows, cols)), shape=(n, n))
+        dist = shortest_path(adj, directed=True, unweighted=True)
+        for v in _frontier(w, b):
+            fronts.append(v)
+            g = lo + v
+            tail = 0.0
+            for x in range(n):
+                h = dist[v, x]
+                if 1 <= h <= H:
+                    gx = lo + x
+                    best = min(float(w.exec[w.model[gx], d]) for d in range(w.D) if _feasible(w, gx, d))
+                    tail += gam ** int(h) * best
+            r_v = min(int(w.shard_max[g]), w.max_shard, w.D)
+            for (i, k) in _windows(w.D, r_v):
+                S = range(i, i + k)
+                if not all(_feasible(w, g, d) for d in S):
+                    exp.append(-np.inf)
+                    continue
+                j0 = max(float(w.exec[w.model[g], d]) / k for d in S)
+                exp.append(-(j0 + tail))
+    assert list(r["front_v"]) == fronts
+    _close(r["psi"], exp, rtol=1e-12)
+
+
+def check_wait_only_reduction(seed: int, lib=None):
+    """Only the waiting cost switched on and H = 0: Psi = -max_{d in S} max(0, tau_d - t)."""
+    w = synth.make_random_small(seed, B=3, n=10, D=5, M=2, K=2, H=0, max_shard=4)
+    w.exec[:] = 0.0
+    only = dict(lam_q=1.0, lam_s=0.0, lam_tr=0.0, lam_c=0.0, lam_p=0.0)
+    r = oracle.score(w, params=only, lib=lib)
+    exp = []
+    for b in range(w.B):
+        lo = int(w.stage_off[b])
+        for v in _frontier(w, b):
+            g = lo + v
+            r_v = min(int(w.shard_max[g]), w.max_shard, w.D)
+            for (i, k) in _windows(w.D, r_v):
+                S = range(i, i + k)
+                if not all(_feasible(w, g, d) for d in S):
+                    exp.append(-np.inf)
+                    continue
+                exp.append(-max(max(0.0, float(w.tau_free[b, d]) - float(w.t_now[b])) for d in S))
+    _close(r["psi"], exp, rtol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# invariants
+# ---------------------------------------------------------------------------
+
+def _permute_bits(x: int, perm) -> int:
+    out = 0
+    for d, pd in enumerate(perm):
+        if (x >> d) & 1:
+            out |= 1 << int(pd)
+    return out
+
+
+def relabel(w, perm):
+    """Apply device relabelling d -> perm[d] to every device-indexed input."""
+    perm = np.asarray(perm)
+    D = w.D
+    inv = np.argsort(perm)  # new index -> old index
+    beta = w.beta[np.ix_(inv, inv)]
+    return dataclasses.replace(
+        w,
+        exec=w.exec[:, inv].copy(), switch_s=w.switch_s[:, inv].copy(), beta=beta.copy(),
+        cap_bytes=w.cap_bytes[inv].copy(),
+        elig=np.array([_permute_bits(int(e), perm) for e in w.elig], np.uint64),
+        holders=np.array([_permute_bits(int(e), perm) for e in w.holders], np.uint64),
+        resident=w.resident[:, inv].copy(), prefix_cache=w.prefix_cache[:, inv, :].copy(),
+        tau_free=w.tau_free[:, inv].copy(), params=dict(w.params),
+    )
+
+
+def check_relabel_singletons(seed: int, lib=None):
+    w = synth.make_random_small(seed, B=2, n=12, D=5, M=3, K=3, H=2, max_shard=1)
+    perm = np.random.default_rng(seed).permutation(w.D)
+    r0 = oracle.score(w, lib=lib)
+    r1 = oracle.score(relabel(w, perm), lib=lib)
+    assert np.array_equal(r0["front_v"], r1["front_v"])
+    co = r0["cand_off"]
+    for f in range(len(r0["front_v"])):
+        a = r0["psi"][co[f]:co[f] + w.D]
+        b = r1["psi"][co[f]:co[f] + w.D]
+        _close(b[perm], a, rtol=1e-13, atol=0)
+
+
+def check_reversal_windows(seed: int, lib=None):
+    w = synth.make_random_small(seed, B=2, n=12, D=5, M=3, K=3, H=2, max_shard=4, shard_frac=0.8)
+    D = w.D
+    perm = np.arange(D)[::-1]
+    r0 = oracle.score(w, lib=lib)
+    r1 = oracle.score(relabel(w, perm), lib=lib)
+    co = r0["cand_off"]
+    for f in range(len(r0["front_v"])):
+        nc = int(co[f + 1] - co[f])
+        r_v = 1
+        while D + sum(D - k + 1 for k in range(2, r_v + 1)) < nc:
+            r_v += 1
+        cands = _windows(D, r_v)
+        pos = {c: j for j, c in enumerate(cands)}
+        a = r0["psi"][co[f]:co[f + 1]]
+        b = r1["psi"][co[f]:co[f + 1]]
+        mapped = np.array([b[pos[(D - i - k, k)]] for (i, k) in cands])
+        _close(mapped, a, rtol=1e-12, atol=0)
+
+
+def check_h0_equals_gamma0(seed: int, lib=None):
+    w = synth.make_random_small(seed, B=2, n=12, D=4, M=3, K=2, H=3)
+    a = oracle.score(w, H=0, lib=lib)["psi"]
+    b = oracle.score(w, params=dict(gamma=0.0), lib=lib)["psi"]
+    assert np.array_equal(a, b)
+
+
+def _reach(w, b, v, H):
+    """Stages whose attributes may enter v's scores: v, its parents, the
+    stages within H hops below v and their parents."""
+    lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+    n = hi - lo
+    ch = [[] for _ in range(n)]
+    for x in range(n):
+        for p in w.par_idx[w.par_off[lo + x]:w.par_off[lo + x + 1]]:
+            ch[int(p)].append(x)
+    seen = {v: 0}
+    fr = [v]
+    for h in range(1, H + 1):
+        nxt = []
+        for x in fr:
+            for c in ch[x]:
+                if c not in seen:
+                    seen[c] = h
+                    nxt.append(c)
+        fr = nxt
+    keep = set(seen)
+    for x in list(seen):
+        keep.update(int(p) for p in w.par_idx[w.par_off[lo + x]:w.par_off[lo + x + 1]])
+    return keep
+
+
+def check_truncation(seed: int, lib=None):
+    """Changing stages outside every frontier stage's horizon (and their
+    parents) leaves every score unchanged."""
+    w = synth.make_random_small(seed, B=1, n=16, D=4, M=3, K=2, H=1, p_edge=0.25, tight_caps=False)
+    r0 = oracle.score(w, lib=lib)
+    keep = set()
+    for v in _frontier(w, 0):
+        keep |= _reach(w, 0, v, w.H)
+    w2 = dataclasses.replace(w, model=w.model.copy(), out_bytes=w.out_bytes.copy(),
+                             prefix_hash=w.prefix_hash.copy(), prefix_tokens=w.prefix_tokens.copy())
+    rng = np.random.default_rng(seed)
+    far = [x for x in range(w.N) if x not in keep]
+    for x in far:
+        w2.model[x] = (w2.model[x] + 1) % w.M
+        w2.out_bytes[x] *= 3.0
+        w2.prefix_hash[x] = np.uint64(int(rng.integers(1, 1 << 60)))
+        w2.prefix_tokens[x] += 100.0
+    r1 = oracle.score(w2, lib=lib)
+    assert np.array_equal(r0["psi"], r1["psi"])
+
+
+def check_isolated_stage(seed: int, lib=None):
+    """Appending an isolated pending root adds one frontier stage and changes
+    no other score."""
+    w = synth.make_random_small(seed, B=1, n=12, D=4, M=3, K=2, H=2)
+    r0 = oracle.score(w, lib=lib)
+    n = w.N
+    par_off = np.append(w.par_off, w.par_off[-1])
+    w2 = dataclasses.replace(
+        w, stage_off=np.array([0, n + 1], np.int64), par_off=par_off,
+        model=np.append(w.model, 0).astype(np.int32),
+        elig=np.append(w.elig, np.uint64((1 << w.D) - 1)).astype(np.uint64),
+        shard_max=np.append(w.shard_max, 1).astype(np.int32),
+        prefix_hash=np.append(w.prefix_hash, np.uint64(5)).astype(np.uint64),
+        prefix_tokens=np.append(w.prefix_tokens, 10.0).astype(np.float32),
+        out_bytes=np.append(w.out_bytes, 1e6).astype(np.float32),
+        holders=np.append(w.holders, np.uint64(0)).astype(np.uint64),
+        status=np.append(w.status, 0).astype(np.uint8))
+    r1 = oracle.score(w2, lib=lib)
+    F = len(r0["front_v"])
+    assert list(r1["front_v"][:F]) == list(r0["front_v"]) and r1["front_v"][F] == n
+    assert np.array_equal(r1["psi"][:len(r0["psi"])], r0["psi"])
+
+
+ALL_CHECKS = (
+    [("scenario:" + k, (lambda k: lambda lib: check_scenario(k, lib))(k)) for k in scenarios.ALL]
+    + [("worked_example", check_worked_example)]
+    + [("exec_only:%d" % s, (lambda s: lambda lib: check_exec_only_reduction(s, lib))(s)) for s in range(3)]
+    + [("wait_only:%d" % s, (lambda s: lambda lib: check_wait_only_reduction(s, lib))(s)) for s in range(2)]
+    + [("relabel:%d" % s, (lambda s: lambda lib: check_relabel_singletons(s, lib))(s)) for s in range(2)]
+    + [("reversal:%d" % s, (lambda s: lambda lib: check_reversal_windows(s, lib))(s)) for s in range(2)]
+    + [("h0_gamma0:%d" % s, (lambda s: lambda lib: check_h0_equals_gamma0(s, lib))(s)) for s in range(2)]
+    + [("truncation:%d" % s, (lambda s: lambda lib: check_truncation(s, lib))(s)) for s in range(3)]
+    + [("isolated:%d" % s, (lambda s: lambda lib: check_isolated_stage(s, lib))(s)) for s in range(2)]
+)

@@ -1,0 +1,144 @@
+"""Hand-derived micro scenarios that pin each term of the score.
+
+Every expected value below was worked out by hand from the definitions the
+paper gives (App. A.3 term definitions, App. A.1/A.4 additive estimator,
+Sec. 3.3 horizon) under the readings recorded in the design notes.  Inputs are
+exact binary fractions (powers of two for transfer coefficients and sizes,
+lam_c = 1/8, kappa_prefix = 2^-10) so every expected value is exact in fp64
+(the only exception is k = 3 windows, which divide by 3).
+
+Each scenario is chosen so that a plausible slip (dropped term, wrong sign,
+transposed transfer coefficient, wrong divisor, wrong eviction order, wrong
+depth weight, missing de-duplication, ...) changes at least one number.
+"""
+
+from __future__ import annotations
+
+INF = float("inf")
+P = dict(lam_c=0.125, kappa_prefix=2.0 ** -10)
+
+# A: waiting cost is clamped at zero; switch only when the model is absent.
+#   d0: wait max(0, 0.25-1) = 0, exec 1.0, m0 resident            -> 1.0
+#   d1: wait 2-1 = 1, exec 0.5, switch 0.75                         -> 2.25
+WAIT_SWITCH = dict(
+    spec=dict(D=2, M=1, K=1, exec=[[1.0, 0.5]], switch_s=[[0.75, 0.75]], weight_gb=[10], cap_gb=[20, 20],
+              beta=[[0, 0], [0, 0]],
+              instances=[dict(parents=[[]], model=[0], elig=[3], out_bytes=[1.0], status=[0], holders=[0],
+                              resident=[1, 0], tau_free=[0.25, 2.0], t_now=1.0)]),
+    H=0, params=P, front_v=[0], psi=[-1.0, -2.25])
+
+# B: transfer uses beta[from][to], the cheapest of several holders, and
+#    colocation counts the fraction of parents held on the device.
+#   u0 on {d0}, sigma 2^32; u1 on {d1,d2}, sigma 2^30; lam_c = 1/8.
+#   d0: u1 -> 2^30 * min(beta[1][0]=2^-30, beta[2][0]=2^-31) = 0.5; colo 1/2
+#       J0 = 1 + 0.5 - 1/16 = 1.4375
+#   d1: u0 -> 2^32 * beta[0][1] (2^-32) = 1.0; colo 1/2  -> 1.9375
+#   d2: u0 -> 2^32 * beta[0][2] (2^-31) = 2.0; colo 1/2  -> 2.9375
+_B_BETA = [[0.0, 2.0 ** -32, 2.0 ** -31],
+           [2.0 ** -30, 0.0, 2.0 ** -33],
+           [2.0 ** -31, 2.0 ** -34, 0.0]]
+TRANSFER_COLO = dict(
+    spec=dict(D=3, M=1, K=1, exec=[[1.0, 1.0, 1.0]], switch_s=[[0.0, 0.0, 0.0]], weight_gb=[10],
+              cap_gb=[20, 20, 20], beta=_B_BETA,
+              instances=[dict(parents=[[], [], [0, 1]], model=[0, 0, 0], elig=[7, 7, 7],
+                              out_bytes=[2.0 ** 32, 2.0 ** 30, 1.0], status=[1, 1, 0], holders=[1, 6, 0],
+                              resident=[1, 1, 1], tau_free=[0.0, 0.0, 0.0], t_now=0.0)]),
+    H=0, params=P, front_v=[2], psi=[-1.4375, -1.9375, -2.9375])
+
+# C: shard windows.  Per device (wait, exec, switch, transfer, colo, prefix):
+#   d0: (2.0, 1.0, 0,   0,   1, 0)    d1: (0, 2.0, 0.5, 0.5, 0, 0)
+#   d2: (0,   4.0, 0.5, 1.0, 0, 0.5)  with sigma(v) = 3*2^31.
+#   T(d,k) = wait + exec/k + switch + (transfer - prefix)/k - colo/8.
+#   k=1: T = 2.875, 3.0, 5.0
+#   {0,1}: max(2.375, 1.75) + G; G = min(beta[1][0], beta[0][1])*sigma/2 = 0.375 -> 2.75
+#   {1,2}: max(1.75, 2.75) + G; G = min(beta[2][1], beta[1][2])*sigma/2 = 0.1875 -> 2.9375
+#   {0,1,2}: max(2 + 1/3 - 1/8, 2/3 + 1/2 + 1/6, 4/3 + 1/2 + 1/6) + G
+#            G = min over p of the column sum into p times sigma/3
+#              = min(1.25, 0.75, 0.625) = 0.625               -> 2.833333...
+_C_BETA = [[0.0, 2.0 ** -33, 2.0 ** -32],
+           [2.0 ** -31, 0.0, 2.0 ** -34],
+           [2.0 ** -33, 2.0 ** -32, 0.0]]
+WINDOWS = dict(
+    spec=dict(D=3, M=1, K=1, exec=[[1.0, 2.0, 4.0]], switch_s=[[0.5, 0.5, 0.5]], weight_gb=[10],
+              cap_gb=[20, 20, 20], beta=_C_BETA,
+              instances=[dict(parents=[[], [0]], model=[0, 0], elig=[7, 7], shard_max=[1, 3],
+                              prefix_hash=[0, 7], prefix_tokens=[0.0, 512.0],
+                              out_bytes=[2.0 ** 32, 3.0 * 2.0 ** 31], status=[1, 0], holders=[1, 0],
+                              resident=[1, 0, 0], prefix_cache=[[0], [0], [7]],
+                              tau_free=[3.0, 1.0, 1.0], t_now=1.0)]),
+    H=0, params=P, front_v=[1],
+    psi=[-2.875, -3.0, -5.0, -2.75, -2.9375, -(2.0 + 1.0 / 3.0 - 0.125 + 0.625)],
+    topk3=[3, 5, 0])
+
+# D: post-state seen by the descendants.
+#   Models W = 10 GB each, capacity 25 GB; switch m0 0.25, m1 0.5, m2 1.0.
+#   p (m0) completed on d1; v (m1, group 99, sigma 2^32) is the frontier stage;
+#   q is running; w1 (m0, group 99, L 512, parents v and q); w2 (m2, parent v,
+#   no prefix group, so its 256 tokens never count).
+#   Immediate: d0 = 1 + 0.5 (switch) + 0.5 (p's output, 2^31*2^-32) = 2.0;
+#              d1 = 1 + 0.5 - 1/8 (p colocated) = 1.375.
+#   v on d0: loading m1 onto {m0,m2} overflows (30 > 25) and evicts m0.
+#     w1: d0 = 1 + 0.25 - 1/16 - 0.5 = 0.6875; d1 = 1 + 0.25 + 1.0 = 2.25
+#     w2: d0 = 1 - 1/8 = 0.875;              d1 = 1 + 1.0 = 2.0
+#     J = 2.0 + 0.5 (0.6875 + 0.875) = 2.78125
+#   v on d1: {m2} + m1 fits, nothing evicted.
+#     w1: d0 = 1 + 1.0 = 2.0; d1 = 1 + 0.25 - 1/16 - 0.5 = 0.6875
+#     w2: d0 = 1 + 1.0 = 2.0; d1 = 1 - 1/8 = 0.875
+#     J = 1.375 + 0.78125 = 2.15625
+_UNI = [[0.0, 2.0 ** -32], [2.0 ** -32, 0.0]]
+POST_STATE = dict(
+    spec=dict(D=2, M=3, K=1, exec=[[1.0, 1.0]] * 3, switch_s=[[0.25, 0.25], [0.5, 0.5], [1.0, 1.0]],
+              weight_gb=[10, 10, 10], cap_gb=[25, 25], beta=_UNI,
+              instances=[dict(parents=[[], [0], [], [1, 2], [1]], model=[0, 1, 0, 0, 2], elig=[3] * 5,
+                              prefix_hash=[0, 99, 0, 99, 0], prefix_tokens=[0.0, 256.0, 0.0, 512.0, 256.0],
+                              out_bytes=[2.0 ** 31, 2.0 ** 32, 1.0, 1.0, 1.0],
+                              status=[1, 0, 2, 0, 0], holders=[2, 0, 0, 0, 0],
+                              resident=[5, 4], prefix_cache=[[0], [0]],
+                              tau_free=[1.0, 1.0], t_now=1.0)]),
+    H=1, params=P, front_v=[1], psi=[-2.78125, -2.15625])
+POST_STATE_H0 = dict(POST_STATE, H=0, psi=[-2.0, -1.375])
+
+# E: horizon set = breadth-first levels 1..H, each stage once at its minimum
+#    distance; descendants use only their feasible devices.  Only base
+#    runtimes are non-zero (exec d0 = 1, d1 = 2; c is eligible on d1 only).
+#    Levels from v: {a, b, f} at 1, {c} at 2, {e} at 3 (f is also a child of c).
+#    H=2: J(d0) = 1 + 0.5*3 + 0.25*2 = 3.0; J(d1) = 4.0
+#    H=3: plus 0.125*1 for e.
+_E_P = dict(lam_c=0.0, kappa_prefix=0.0)
+HORIZON_SET = dict(
+    spec=dict(D=2, M=1, K=1, exec=[[1.0, 2.0]], switch_s=[[0.0, 0.0]], weight_gb=[10], cap_gb=[20, 20],
+              beta=[[0, 0], [0, 0]],
+              instances=[dict(parents=[[], [0], [1], [1], [2, 3], [4], [1, 4]], model=[0] * 7,
+                              elig=[3, 3, 3, 3, 2, 3, 3], out_bytes=[1.0] * 7,
+                              status=[1, 0, 0, 0, 0, 0, 0], holders=[1, 0, 0, 0, 0, 0, 0],
+                              resident=[1, 1], tau_free=[0.0, 0.0], t_now=0.0)]),
+    H=2, params=_E_P, front_v=[1], psi=[-3.0, -4.0])
+HORIZON_SET_H3 = dict(HORIZON_SET, H=3, psi=[-3.125, -4.125])
+
+# F: feasibility needs eligibility and capacity; top-k skips -inf, breaks
+#    ties by candidate index and pads with (-1, -inf).
+#    v0 (m1, 30 GB) does not fit d0 (20 GB); v1 (m0) is eligible on d0, d2.
+FEASIBILITY = dict(
+    spec=dict(D=3, M=2, K=1, exec=[[1.0, 1.0, 1.0], [1.0, 1.0, 1.0]], switch_s=[[0.0] * 3, [0.0] * 3],
+              weight_gb=[10, 30], cap_gb=[20, 40, 40], beta=[[0.0] * 3] * 3,
+              instances=[dict(parents=[[], []], model=[1, 0], elig=[7, 5], shard_max=[1, 2],
+                              out_bytes=[1.0, 1.0], status=[0, 0], holders=[0, 0],
+                              resident=[1, 3, 3], tau_free=[0.0] * 3, t_now=0.0)]),
+    H=0, params=P, front_v=[0, 1],
+    psi=[-INF, -1.0, -1.0, -1.0, -INF, -1.0, -INF, -INF],
+    topk4=[[1, 2, -1, -1], [0, 2, -1, -1]])
+
+# G: the frontier holds pending stages whose parents are all completed;
+#    running and committed stages are not in it.
+FRONTIER = dict(
+    spec=dict(D=2, M=1, K=1, exec=[[1.0, 1.0]], switch_s=[[0.0, 0.0]], weight_gb=[10], cap_gb=[20, 20],
+              beta=[[0, 0], [0, 0]],
+              instances=[dict(parents=[[], [], [], [0], [1], [], [0, 3]], model=[0] * 7, elig=[3] * 7,
+                              out_bytes=[1.0] * 7, status=[1, 2, 3, 0, 0, 0, 0],
+                              holders=[1, 0, 0, 0, 0, 0, 0], resident=[1, 1],
+                              tau_free=[0.0, 0.0], t_now=0.0)]),
+    H=0, params=P, front_v=[3, 5], psi=[-(1.0 - 0.125), -1.0, -1.0, -1.0])
+
+ALL = dict(WAIT_SWITCH=WAIT_SWITCH, TRANSFER_COLO=TRANSFER_COLO, WINDOWS=WINDOWS, POST_STATE=POST_STATE,
+           POST_STATE_H0=POST_STATE_H0, HORIZON_SET=HORIZON_SET, HORIZON_SET_H3=HORIZON_SET_H3,
+           FEASIBILITY=FEASIBILITY, FRONTIER=FRONTIER)

@@ -1,0 +1,80 @@
+"""Plant plausible mistakes in copies of the oracle source and check that the
+pin suite rejects every one of them (no GPU).
+
+Each mutant is a list of exact text replacements applied to
+oracle/fate_oracle.c; the mutated copy is compiled into a temporary
+directory, loaded, and run through every check in tests/pins.py.  A mutant
+that passes every check would mean the pins cannot see that mistake.
+"""
+
+import os
+import subprocess
+
+import pytest
+
+import pins
+from oracle import oracle
+
+MUTANTS = {
+    "wait_not_clamped": [("return w > 0.0 ? w : 0.0;", "return w;")],
+    "switch_even_if_resident": [("if (has_bit(s->res[d], m)) return 0.0;", "if (0) return 0.0;")],
+    "transfer_beta_transposed": [("(double)in->beta[i * in->D + d] < bmin)\n                bmin = (double)in->beta[i * in->D + d];",
+                                  "(double)in->beta[d * in->D + i] < bmin)\n                bmin = (double)in->beta[d * in->D + i];")],
+    "transfer_first_holder": [("if (has_bit(hu, i) && (double)in->beta[i * in->D + d] < bmin)",
+                               "if (has_bit(hu, i) && bmin == INFINITY)")],
+    "transfer_child_size": [("tr += (double)in->sigma[s->base + u] * bmin;", "tr += (double)in->sigma[g] * bmin;")],
+    "colo_sign": [("return c + t_sw + t_tr - t_co - t_pf;", "return c + t_sw + t_tr + t_co - t_pf;")],
+    "colo_not_normalised": [("return (double)cnt / (double)np;", "return (double)cnt;")],
+    "prefix_group_zero_counts": [("if (h == 0) return 0.0;", "if (0) return 0.0;")],
+    "post_state_no_prefix": [("post.extra_hash[d] = in->hash[g];", "post.extra_hash[d] = 0;")],
+    "post_state_no_holders": [("post.over_stage = v;", "post.over_stage = -1;")],
+    "load_evicts_largest_id": [("for (int i = 0; i < in->M && total > in->cap[d]; ++i) {",
+                                "for (int i = in->M - 1; i >= 0 && total > in->cap[d]; --i) {")],
+    "load_never_evicts": [("res &= ~((uint64_t)1 << i);\n        total -= in->weight[i];",
+                           "total -= in->weight[i];")],
+    "depth_weight_off_by_one": [("pow(in->gamma, (double)sc.depth[w])", "pow(in->gamma, (double)(sc.depth[w] - 1))")],
+    "horizon_one_level_too_deep": [("if (sc->depth[x] >= H) continue;", "if (sc->depth[x] > H) continue;")],
+    "window_exec_not_split": [("double a_c = exec_c(in, mv, d) / k;", "double a_c = exec_c(in, mv, d);")],
+    "window_transfer_not_split": [("transfer_cost(&cur, v, d) / k;", "transfer_cost(&cur, v, d);")],
+    "window_switch_split": [("double a_s = in->lam_s * switch_cost(&cur, v, d);",
+                             "double a_s = in->lam_s * switch_cost(&cur, v, d) / k;")],
+    "window_wait_split": [("double a_q = in->lam_q * wait_cost(&cur, d);",
+                           "double a_q = in->lam_q * wait_cost(&cur, d) / k;")],
+    "gather_beta_transposed": [("in->beta[d * D + p]", "in->beta[p * D + d]")],
+    "gather_max_over_target": [("gsum = INFINITY;", "gsum = -INFINITY;"), ("if (s < gsum) gsum = s;", "if (s > gsum) gsum = s;")],
+    "feasible_ignores_capacity": [("return has_bit(in->elig[g], d) && fits(in, in->model[g], d);",
+                                   "return has_bit(in->elig[g], d);")],
+    "feasible_ignores_eligibility": [("return has_bit(in->elig[g], d) && fits(in, in->model[g], d);",
+                                      "return fits(in, in->model[g], d);")],
+    "frontier_includes_running": [("if (in->status[g] != ST_PENDING) return 0;",
+                                   "if (in->status[g] == ST_COMPLETED) return 0;")],
+    "descendant_max_device": [("if (val < vbest) { vbest = val; vmag = m_; }",
+                               "if (vbest == INFINITY || val > vbest) { vbest = val; vmag = m_; }")],
+    "prefix_sign": [("return c + t_sw + t_tr - t_co - t_pf;", "return c + t_sw + t_tr - t_co + t_pf;")],
+}
+
+
+def _build_mutant(name, tmp_path):
+    src = open(oracle.SRC).read()
+    for old, new in MUTANTS[name]:
+        assert src.count(old) == 1, (name, old)
+        src = src.replace(old, new)
+    cpath = os.path.join(tmp_path, name + ".c")
+    with open(cpath, "w") as fh:
+        fh.write(src)
+    so = os.path.join(tmp_path, "lib" + name + ".so")
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fopenmp", "-shared", "-fPIC", cpath, "-o", so, "-lm"], check=True)
+    return oracle.load(so)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_reject_mutant(name, tmp_path):
+    lib = _build_mutant(name, str(tmp_path))
+    caught = []
+    for check_name, check in pins.ALL_CHECKS:
+        try:
+            check(lib)
+        except AssertionError:
+            caught.append(check_name)
+            break
+    assert caught, "no pin rejects the planted mistake '%s'" % name
