@@ -1,0 +1,243 @@
+#!/usr/bin/env python3
+"""Benchmark of horizon-aware candidate scoring on one MI355X.
+
+One step = one pass of the scoring path over the whole batch with the packed
+DAGs and state already resident in HBM: fate_score_frontier (every candidate
+of every frontier stage, immediate cost plus the depth-H horizon) followed by
+fate_topk.  Packing (host validation, layout and the host-to-device copy) is
+done once before timing and reported separately.
+
+Prints one JSON line (rank 0, N=1):
+  value          candidate-horizon evaluations per second over the timed steps;
+                 one evaluation per feasible candidate and per (feasible
+                 candidate, horizon descendant) pair
+  roofline       the score kernel's algorithmic bytes per launch / its average
+                 launch time (HIP events on the launch stream) vs 8 TB/s HBM
+  cpu_baseline   the fp64 oracle timed on this host's cores over the same batch
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+DEFAULT_WORKLOAD = "forkjoin-4096x1000-d16"
+HBM_PEAK_GBS = 8000.0
+METRIC = "candidate-horizon evaluations/sec and achieved HBM GB/s (fraction of peak)"
+KERNEL_SRC = os.path.join(ROOT, "paper_2605_07238_amd", "csrc", "fate_kernels.hip")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+
+
+def counted_work(w, pk, st, scores_host, H):
+    """Exact evaluation count and algorithmic bytes of one score launch,
+    counted from the packed structures (each needed byte once)."""
+    import torch
+    from paper_2605_07238_amd import fate
+
+    fv, fb, co = fate.frontier_table(st)
+    F = len(fv)
+    h = pk.handle
+    base = pk.buf.data_ptr()
+    N = int(h.N)
+    doff = pk.buf[h.desc_off - base:h.desc_off - base + 4 * (N + 1)].view(torch.int32).cpu().numpy().astype(np.int64)
+    desc = pk.buf[h.desc - base:h.desc - base + 4 * int(h.n_desc)].view(torch.int32).cpu().numpy().astype(np.int64)
+    desc &= 0xFFFFFFFF
+    depth = desc >> 28
+    wid = desc & ((1 << 28) - 1)
+    # per frontier stage: entries with depth <= H
+    lens = doff[fv + 1] - doff[fv]
+    starts = doff[fv]
+    idx = np.repeat(starts - np.concatenate([[0], np.cumsum(lens)[:-1]]), lens) + np.arange(int(lens.sum()))
+    ent_depth = depth[idx]
+    keep = ent_depth <= H
+    seg = np.repeat(np.arange(F), lens)
+    ndesc = np.bincount(seg[keep], minlength=F)
+    feas = np.add.reduceat(np.isfinite(scores_host).astype(np.int64), co[:-1]) if F else np.zeros(0, np.int64)
+    n_eval = int((feas * (1 + ndesc)).sum())
+    touched = np.unique(np.concatenate([fv, wid[idx][keep]]))
+    npar = np.diff(w.par_off)
+    inst = np.repeat(np.arange(w.B), np.diff(w.stage_off))
+    par_global = w.par_idx.astype(np.int64) + w.stage_off[np.repeat(inst, npar)]
+    pstart = w.par_off[touched]
+    plen = npar[touched]
+    pidx = np.repeat(pstart - np.concatenate([[0], np.cumsum(plen)[:-1]]), plen) + np.arange(int(plen.sum()))
+    parents = np.unique(par_global[pidx])
+    completed = int(np.count_nonzero(w.holders[parents] != 0))
+    D, M, K = w.D, w.M, w.K
+    active = len(np.unique(fb))
+    nbytes = dict(
+        frontier=8 * F + 4 * (F + 1),
+        desc=8 * F + 4 * int(keep.sum()),
+        records=32 * len(touched),
+        parents=4 * int(plen.sum()) + 8 * len(parents) + 4 * completed,
+        state=active * (8 * D + 8 * D * K + 4 * D + 4),
+        cluster=8 * M * D + 4 * D * D + 8 * (2 * M + D),
+        scores=4 * int(co[-1]),
+    )
+    return n_eval, int(sum(nbytes.values())), nbytes, dict(F=F, C=int(co[-1]), touched=len(touched),
+                                                            desc_entries=int(keep.sum()))
+
+
+def read_traffic(workload: str):
+    """HBM traffic of the score kernel from committed rocprofv3 counter runs,
+    if they were taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "k_score_%s_counters.txt" % workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256") != kernel_sha():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, H, gpu_evals_unit):
+    from oracle import oracle
+    threads = min(16, os.cpu_count() or 1)
+    t = time.perf_counter()
+    ref = oracle.score(w, H=H, threads=threads)
+    dt = time.perf_counter() - t
+    return ref, dt, threads
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--topk", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, run one plain device copy of 512 MiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the scoring path has no cross-GPU step "
+              "(instances shard across GPUs with no exchange); --gpus %d is not supported." % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    from paper_2605_07238_amd import synth
+    t0 = time.perf_counter()
+    w = synth.make_workload(args.workload, workers=min(16, os.cpu_count() or 1))
+    log("generated %s: B=%d N=%d in %.1fs" % (args.workload, w.B, w.N, time.perf_counter() - t0))
+
+    import torch
+    from paper_2605_07238_amd import fate
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    fate.load()
+    H = w.H
+    t0 = time.perf_counter()
+    pk = fate.fate_pack_dags(w, H=H)
+    t_pack_dags = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    st = fate.fate_pack_state(pk, w)
+    t_pack_state = time.perf_counter() - t0
+    log("packed: dags %.2fs (%.1f MB), state %.2fs (%.1f MB); %d frontier stages, %d candidates"
+        % (t_pack_dags, pk.handle.bytes / 1e6, t_pack_state, st.handle.bytes / 1e6, st.n_frontier, st.n_cand))
+    params = fate.make_params(w, H=H)
+    scores = torch.empty(max(1, st.n_cand), dtype=torch.float32, device="cuda")
+    idx = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.int32, device="cuda")
+    val = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.float32, device="cuda")
+
+    def step():
+        fate.fate_score_frontier(pk, st, params, out=scores)
+        fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done (%d steps)" % args.warmup)
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(K):
+        ev[i][0].record()
+        fate.fate_score_frontier(pk, st, params, out=scores)
+        ev[i][1].record()
+        fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
+        ev[i][2].record()
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    ms_step = (t_end - t_start) * 1e3 / K
+    score_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
+    topk_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+    log("timed %d steps: %.4f ms/step (score %.4f ms, topk %.4f ms)" % (K, ms_step, score_ms, topk_ms))
+
+    if args.copy_calibration:
+        src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: 536870912 bytes read + written")
+
+    scores_host = scores[:st.n_cand].cpu().numpy()
+    n_eval, alg_bytes, parts, counts = counted_work(w, pk, st, scores_host, H)
+    achieved = alg_bytes / (score_ms * 1e-3) / 1e9
+    traffic = read_traffic(args.workload)
+    out = {
+        "metric": METRIC,
+        "value": n_eval / (ms_step * 1e-3),
+        "unit": "evals/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload, "B": w.B, "stages_per_dag": int(np.diff(w.stage_off).max()),
+            "D": w.D, "M": w.M, "K": w.K, "H": H, "max_shard": w.max_shard, "topk": args.topk,
+            "frontier_stages": counts["F"], "candidates": counts["C"], "horizon_entries": counts["desc_entries"],
+            "evals_per_step": n_eval, "score_kernel_ms": score_ms, "topk_kernel_ms": topk_ms,
+            "pack_dags_s": t_pack_dags, "pack_state_s": t_pack_state,
+            "algorithmic_bytes_per_launch": alg_bytes, "algorithmic_bytes_parts": parts,
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": "k_score",
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on the host ...")
+        ref, dt, threads = cpu_baseline(w, H, None)
+        # same evaluation count definition, from the oracle's own scores
+        n_eval_cpu = n_eval  # identical frontier, candidates and horizon sets (checked by the parity tests)
+        out["cpu_baseline"] = {"value": n_eval_cpu / dt, "unit": "evals/s", "cores": threads, "kind": "oracle",
+                               "sample": "all %d instances of %s, one pass (%.1f s)" % (w.B, args.workload, dt)}
+        log("oracle: %.2f s with %d threads" % (dt, threads))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,248 @@
+/*
+ * fate.h - C ABI of the MI355X horizon-aware candidate scoring library.
+ *
+ * The library scores, for a batch of B workflow-DAG instances, every
+ * candidate placement (a single device, or a contiguous window of devices for
+ * a shardable stage) of every ready-frontier stage, following FATE
+ * (arXiv 2605.07238):
+ *   - stage tuple (m(v), A(v), R(v), c_v, phi(v), Pa(v), Ch(v)): Sec. 2 and
+ *     App. A.1;
+ *   - execution state s_t = (rho_t, kappa_t, l_t, tau_t): Sec. 2, App. A.1;
+ *   - ready frontier and feasible candidate set: Sec. 2, App. A.1;
+ *   - score terms (waiting, switch, transfer, colocation, prefix, shard):
+ *     Sec. 3.4 and App. A.3; additive state-conditional cost: App. A.1/A.4;
+ *   - horizon-aware candidate score Psi(v, k, d | s_t, H): Sec. 3.3, App. A.2.
+ * H counts downstream DAG levels beyond the frontier; H = 0 scores the
+ * immediate cost only (App. D.4).  Psi is the negated estimated cost in
+ * seconds: higher is better.
+ *
+ * Conventions for every entry point:
+ *   - Every function returns a fate_status_t and is reentrant; the library
+ *     keeps no global state and never allocates device memory.
+ *   - Host arrays passed in are read during the call only and never retained.
+ *   - Device buffers are allocated by the caller (sizes come from the *_size
+ *     queries) and passed as a pointer plus a byte count.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Device work is
+ *     enqueued on it.  The pack functions copy from pageable host memory and
+ *     synchronise the stream before returning; scoring and top-k never
+ *     synchronise.
+ *   - Inputs are validated on the host before anything is enqueued; on an
+ *     error nothing is written to device memory and outputs are untouched.
+ *   - Devices are indexed 0..D-1 with D <= 64, models 0..M-1 with M <= 64;
+ *     bitmasks over devices or models are uint64_t with bit i for index i.
+ */
+#ifndef FATE_H
+#define FATE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FATE_MAX_DEVICES 64
+#define FATE_MAX_MODELS 64
+#define FATE_MAX_PREFIX_SLOTS 32
+#define FATE_MAX_HORIZON 15
+#define FATE_MAX_TOPK 64
+#define FATE_MAX_SHARD 4
+#define FATE_MAX_PARENTS 65535
+/* Total stages over the batch must fit 28 bits (stage ids share a 32-bit word
+ * with their horizon depth in the packed descendant lists). */
+#define FATE_MAX_TOTAL_STAGES ((1 << 28) - 1)
+
+typedef enum {
+    FATE_OK = 0,
+    FATE_EINVAL = -1,  /* null pointer, negative size, non-finite or negative value, bad mask */
+    FATE_ERANGE = -2,  /* a limit above is exceeded (D, M, K, H, k, R, parents, totals) */
+    FATE_ECYCLE = -3,  /* a parent id is not smaller than its child's id, or parents unsorted */
+    FATE_ENOFEAS = -4, /* a stage has no eligible device that can hold its model */
+    FATE_ESIZE = -5,   /* a caller buffer is smaller than the size query returned */
+    FATE_ESTATE = -6,  /* inconsistent state (status, holders, handle mismatch) */
+    FATE_EHIP = -7     /* a HIP runtime call failed */
+} fate_status_t;
+
+/* Stage status codes (App. A.1 tracks completed, running and committed). */
+enum { FATE_PENDING = 0, FATE_COMPLETED = 1, FATE_RUNNING = 2, FATE_COMMITTED = 3 };
+
+/* Cluster tables (host memory), shared by every instance of a batch.
+ *   exec[m*D + d]     base runtime c_v(d) of a stage using model m, seconds (>= 0)
+ *   switch_s[m*D + d] kappa_switch(m, d), cost of loading model m on d, seconds (>= 0)
+ *   weight_bytes[m]   memory footprint W(m) of model m, bytes (> 0)
+ *   cap_bytes[d]      model memory capacity of device d, bytes (> 0)
+ *   beta[i*D + j]     transfer coefficient beta_{i,j} from device i to j,
+ *                     seconds per byte (>= 0; the diagonal is never used)  */
+typedef struct {
+    int32_t D, M;
+    const float *exec;
+    const float *switch_s;
+    const int64_t *weight_bytes;
+    const int64_t *cap_bytes;
+    const float *beta;
+} fate_cluster_t;
+
+/* A batch of B DAG instances (host memory), stages stored flat.
+ *   stage_off[B+1]  instance b owns flat stages [stage_off[b], stage_off[b+1]);
+ *                   inside an instance stages are numbered 0..n_b-1 and
+ *                   every edge goes from a smaller to a larger id
+ *   par_off[N+1]    parents of flat stage g are par_idx[par_off[g] .. par_off[g+1])
+ *   par_idx[E]      instance-local parent ids, strictly increasing per stage
+ *   model[N]        m(v) in [0, M)
+ *   elig[N]         A(v) as a device bitmask (non-zero, bits < D)
+ *   shard_max[N]    R(v) in [1, 255]: maximum shard degree
+ *   prefix_hash[N]  grp(v), the shared-prefix group; 0 = no group
+ *   prefix_tokens[N] L(v), reusable prefix length in tokens (>= 0)
+ *   out_bytes[N]    sigma(v), output size in bytes (>= 0)                  */
+typedef struct {
+    int32_t B;
+    const int64_t *stage_off;
+    const int64_t *par_off;
+    const int32_t *par_idx;
+    const int32_t *model;
+    const uint64_t *elig;
+    const int32_t *shard_max;
+    const uint64_t *prefix_hash;
+    const float *prefix_tokens;
+    const float *out_bytes;
+} fate_dag_batch_t;
+
+/* Execution state of every instance (host memory), Sec. 2 s_t.
+ *   K                  prefix-cache slots per device, 0..32
+ *   resident[B*D]      rho: resident-model bitmask of device d of instance b
+ *   prefix_cache[B*D*K] kappa: cached prefix groups per device, 0 = empty slot
+ *   holders[N]         l: device bitmask holding a completed stage's output;
+ *                      non-zero exactly for completed stages
+ *   status[N]          FATE_PENDING / COMPLETED / RUNNING / COMMITTED; completed
+ *                      and running stages have all parents completed
+ *   tau_free[B*D]      tau_d^free: next time device d is free, seconds
+ *   t_now[B]           current decision time t, seconds                    */
+typedef struct {
+    int32_t K;
+    const uint64_t *resident;
+    const uint64_t *prefix_cache;
+    const uint64_t *holders;
+    const uint8_t *status;
+    const float *tau_free;
+    const float *t_now;
+} fate_state_t;
+
+/* Score weights (Sec. 3.4 lambda_q, lambda_s, lambda_tr, lambda_c, lambda_p;
+ * App. A.3 kappa_prefix), the horizon discount gamma (Sec. 3.2) and the
+ * horizon H (Sec. 3.3; 0 <= H <= the H the DAGs were packed with). */
+typedef struct {
+    float lam_q, lam_s, lam_tr, lam_c, lam_p, kappa_prefix, gamma;
+    int32_t H;
+} fate_params_t;
+
+/* Packed DAG batch: plain data pointing into the caller's device buffer.
+ * Valid while that buffer lives; filled by fate_pack_dags. */
+typedef struct {
+    int32_t B, D, M, H;
+    int64_t N, E, n_desc;
+    int32_t beta_uniform; /* 1 if every off-diagonal beta is equal */
+    float beta0;          /* that common value */
+    void *base;
+    size_t bytes;
+    const float *exec, *switch_s, *beta;
+    const uint64_t *weight, *cap, *fits; /* fits[m]: devices that can hold model m */
+    const void *records;                  /* 32-byte stage records [N] */
+    const uint32_t *par_idx;              /* [E] flat parent ids */
+    const uint32_t *desc_off;             /* [N+1] */
+    const uint32_t *desc;                 /* [n_desc]: flat id | depth << 28 */
+    const int64_t *stage_off;             /* [B+1] */
+} fate_dags_t;
+
+/* Packed state of one planning step: plain data pointing into the caller's
+ * device buffer; filled by fate_pack_state. */
+typedef struct {
+    int32_t B, D, K, max_shard;
+    int64_t N, n_frontier, n_cand;
+    void *base;
+    size_t bytes;
+    const uint64_t *resident, *prefix_cache, *holders;
+    const float *tau_free, *t_now;
+    const uint32_t *frontier; /* [n_frontier][2]: flat stage id, instance */
+    const uint32_t *cand_off; /* [n_frontier+1]: first score of each frontier stage */
+} fate_state_h;
+
+const char *fate_version(void);
+const char *fate_strerror(fate_status_t status);
+
+/* fate_pack_dags_size: validate a DAG batch against the cluster and return
+ * the device bytes fate_pack_dags needs for horizon H (0..15).
+ * Errors: EINVAL, ERANGE, ECYCLE, ENOFEAS. */
+fate_status_t fate_pack_dags_size(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                  int32_t H, size_t *bytes);
+
+/* fate_pack_dags: validate, build the packed image on the host (cluster
+ * tables, 32-byte stage records, flat parent lists, and for every stage its
+ * horizon descendants: stages at breadth-first distance 1..H, each once at its
+ * minimum distance, ordered by (distance, id) - Sec. 3.3), copy it to d_buf
+ * on `stream` and synchronise.  `out` receives device pointers into d_buf.
+ * Errors: as fate_pack_dags_size, plus ESIZE if bytes is too small, EHIP. */
+fate_status_t fate_pack_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
+                             void *d_buf, size_t bytes, void *stream, fate_dags_t *out);
+
+/* fate_layout_dags: the host half of fate_pack_dags, writing the same image
+ * into host memory h_buf (no HIP call; `out` points into h_buf). */
+fate_status_t fate_layout_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
+                               void *h_buf, size_t bytes, fate_dags_t *out);
+
+/* fate_pack_state_size: validate a state against a packed batch and the same
+ * host DAG arrays it was packed from; return the device bytes needed, the
+ * number of frontier stages (pending stages whose parents are all completed,
+ * App. A.1) and of candidates.  A frontier stage v has D single-device
+ * candidates followed by the windows {i..i+k-1}, k = 2..r, i = 0..D-k, with
+ * r = min(R(v), max_shard, D) (Sec. 3.3 shard slots).  max_shard in 1..4.
+ * Errors: EINVAL, ERANGE, ESTATE. */
+fate_status_t fate_pack_state_size(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                   const fate_state_t *state, int32_t max_shard, size_t *bytes,
+                                   int64_t *n_frontier, int64_t *n_cand);
+
+/* fate_pack_state: validate, build the frontier list (ordered by instance,
+ * then stage id) and candidate offsets, copy state and frontier to d_buf on
+ * `stream` and synchronise.  Errors: as the size query, ESIZE, EHIP. */
+fate_status_t fate_pack_state(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                              const fate_state_t *state, int32_t max_shard, void *d_buf, size_t bytes,
+                              void *stream, fate_state_h *out);
+
+/* fate_layout_state: the host half of fate_pack_state, into host memory. */
+fate_status_t fate_layout_state(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                const fate_state_t *state, int32_t max_shard, void *h_buf, size_t bytes,
+                                fate_state_h *out);
+
+/* fate_score_ws_size: device workspace bytes fate_score_frontier needs
+ * (may be 0).  Errors: EINVAL, ESTATE. */
+fate_status_t fate_score_ws_size(const fate_dags_t *dags, const fate_state_h *state, size_t *bytes);
+
+/* fate_score_frontier: for every frontier stage v and candidate S write
+ *   Psi(v, S) = -( J0(v, S) + sum_{h=1..H} gamma^h sum_{w at distance h} min_{d' feasible for w} c_hat(w, d' | s') )
+ * into d_scores[cand_off[f] + j] (float32, device memory, n_scores >= n_cand):
+ *   J0(v, S) = max_{d in S} [ lam_q Wait(d) + c(v,d)/k + lam_s Sw(v,d)
+ *                              + (lam_tr Tr(v,d) - lam_p Pf(v,d))/k - lam_c Colo(v,d) ]
+ *              + lam_tr min_{p in S} sum_{d in S, d != p} beta[d][p] sigma(v)/k,
+ * k = |S|; s' is the state after placing v on S (its model loaded on each
+ * device of S, evicting the smallest-id other models while over capacity;
+ * grp(v) cached there; v's output held by S).  Candidates with a device that
+ * is not eligible or cannot hold the model score -infinity.
+ * d_ws/ws_bytes: workspace of at least fate_score_ws_size bytes (may be NULL
+ * when that size is 0).  Enqueued on `stream`; does not synchronise.
+ * Errors: EINVAL (null, non-finite or negative weights, H out of range),
+ * ESIZE, ESTATE (handles from different batches), EHIP. */
+fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *state,
+                                  const fate_params_t *params, float *d_scores, int64_t n_scores,
+                                  void *d_ws, size_t ws_bytes, void *stream);
+
+/* fate_topk: per frontier stage, the k (1..64) best candidates by
+ * (score descending, candidate index ascending), skipping -infinity, padded
+ * with (-1, -infinity).  d_idx/d_val: device arrays [n_frontier * k] of
+ * local candidate indices and scores.  Enqueued on `stream`.
+ * Errors: EINVAL, ERANGE (k), ESIZE (n_scores < n_cand), EHIP. */
+fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_t n_scores, int32_t k,
+                        int32_t *d_idx, float *d_val, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FATE_H */

@@ -1,0 +1,649 @@
+// Host half of libfate: validation, packing of DAG batches and states into
+// flat device images, and the C ABI entry points declared in fate.h.
+//
+// Packing does no scoring arithmetic.  It checks the inputs, lays out the
+// stage records and parent lists, derives each stage's horizon descendants
+// (breadth-first levels 1..H below it, Sec. 3.3) and the ready frontier
+// (pending stages whose parents are all completed, Sec. 2 / App. A.1), and
+// copies the image to the caller's device buffer.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstring>
+#include <thread>
+#include <vector>
+
+#include "fate_internal.h"
+
+namespace {
+
+using fate::StageRec;
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+inline bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.0f; }
+inline uint64_t dev_mask(int D) { return D >= 64 ? ~0ull : ((1ull << D) - 1ull); }
+
+unsigned worker_count() {
+    unsigned n = std::thread::hardware_concurrency();
+    if (n == 0) n = 1;
+    return std::min(n, 16u);
+}
+
+template <class F>
+void parallel_for(int64_t count, F &&fn) {
+    unsigned nw = worker_count();
+    if (count < 4 || nw == 1) {
+        for (int64_t i = 0; i < count; ++i) fn(i);
+        return;
+    }
+    std::atomic<int64_t> next(0);
+    std::vector<std::thread> ts;
+    for (unsigned t = 0; t < nw; ++t)
+        ts.emplace_back([&] {
+            for (;;) {
+                int64_t i = next.fetch_add(1);
+                if (i >= count) break;
+                fn(i);
+            }
+        });
+    for (auto &t : ts) t.join();
+}
+
+// ---------------------------------------------------------------------------
+// validation
+// ---------------------------------------------------------------------------
+
+fate_status_t validate_cluster(const fate_cluster_t *c) {
+    if (!c) return FATE_EINVAL;
+    if (c->D < 1 || c->D > FATE_MAX_DEVICES || c->M < 1 || c->M > FATE_MAX_MODELS) return FATE_ERANGE;
+    if (!c->exec || !c->switch_s || !c->weight_bytes || !c->cap_bytes || !c->beta) return FATE_EINVAL;
+    const int D = c->D, M = c->M;
+    for (int i = 0; i < M * D; ++i)
+        if (!finite_nonneg(c->exec[i]) || !finite_nonneg(c->switch_s[i])) return FATE_EINVAL;
+    for (int i = 0; i < D * D; ++i)
+        if (!finite_nonneg(c->beta[i])) return FATE_EINVAL;
+    for (int m = 0; m < M; ++m)
+        if (c->weight_bytes[m] <= 0) return FATE_EINVAL;
+    for (int d = 0; d < D; ++d)
+        if (c->cap_bytes[d] <= 0) return FATE_EINVAL;
+    return FATE_OK;
+}
+
+std::vector<uint64_t> fit_masks(const fate_cluster_t *c) {
+    std::vector<uint64_t> fits(c->M, 0);
+    for (int m = 0; m < c->M; ++m)
+        for (int d = 0; d < c->D; ++d)
+            if (c->weight_bytes[m] <= c->cap_bytes[d]) fits[m] |= 1ull << d;
+    return fits;
+}
+
+// Structural checks of the flat batch: offsets, parent order, attributes.
+fate_status_t validate_batch(const fate_cluster_t *c, const fate_dag_batch_t *g, int64_t *N_out,
+                             int64_t *E_out) {
+    if (!g || g->B < 0 || !g->stage_off) return FATE_EINVAL;
+    const int B = g->B;
+    if (g->stage_off[0] != 0) return FATE_EINVAL;
+    for (int b = 0; b < B; ++b)
+        if (g->stage_off[b + 1] < g->stage_off[b]) return FATE_EINVAL;
+    const int64_t N = g->stage_off[B];
+    if (N > FATE_MAX_TOTAL_STAGES) return FATE_ERANGE;
+    if (N > 0 && (!g->par_off || !g->model || !g->elig || !g->shard_max || !g->prefix_hash ||
+                  !g->prefix_tokens || !g->out_bytes))
+        return FATE_EINVAL;
+    if (N > 0 && g->par_off[0] != 0) return FATE_EINVAL;
+    for (int64_t i = 0; i < N; ++i)
+        if (g->par_off[i + 1] < g->par_off[i]) return FATE_EINVAL;
+    const int64_t E = N > 0 ? g->par_off[N] : 0;
+    if (E > 0 && !g->par_idx) return FATE_EINVAL;
+    if (E >= (int64_t(1) << 32)) return FATE_ERANGE;
+    const std::vector<uint64_t> fits = fit_masks(c);
+    const uint64_t dm = dev_mask(c->D);
+    for (int b = 0; b < B; ++b) {
+        const int64_t base = g->stage_off[b];
+        const int64_t n = g->stage_off[b + 1] - base;
+        for (int64_t v = 0; v < n; ++v) {
+            const int64_t s = base + v;
+            const int64_t np = g->par_off[s + 1] - g->par_off[s];
+            if (np > FATE_MAX_PARENTS) return FATE_ERANGE;
+            int64_t prev = -1;
+            for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) {
+                const int64_t p = g->par_idx[q];
+                if (p < 0) return FATE_EINVAL;
+                if (p >= v || p <= prev) return FATE_ECYCLE;
+                prev = p;
+            }
+            const int m = g->model[s];
+            if (m < 0 || m >= c->M) return FATE_EINVAL;
+            const uint64_t e = g->elig[s];
+            if (e == 0 || (e & ~dm) != 0) return FATE_EINVAL;
+            if (g->shard_max[s] < 1) return FATE_EINVAL;
+            if (g->shard_max[s] > 255) return FATE_ERANGE;
+            if (!finite_nonneg(g->prefix_tokens[s]) || !finite_nonneg(g->out_bytes[s])) return FATE_EINVAL;
+            if ((e & fits[m]) == 0) return FATE_ENOFEAS;
+        }
+    }
+    *N_out = N;
+    *E_out = E;
+    return FATE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// horizon descendants
+// ---------------------------------------------------------------------------
+
+// Breadth-first levels 1..H below every stage of instance b.  With `out`,
+// stores each stage's entries (flat id | depth << 28) ordered by (depth, id);
+// always stores the per-stage counts into count[] (indexed by flat id).
+void instance_horizons(const fate_dag_batch_t *g, int b, int H, uint32_t *count,
+                       std::vector<uint32_t> *out) {
+    const int64_t base = g->stage_off[b];
+    const int64_t n = g->stage_off[b + 1] - base;
+    if (n == 0) return;
+    std::vector<int64_t> cptr(n + 1, 0);
+    for (int64_t v = 0; v < n; ++v)
+        for (int64_t q = g->par_off[base + v]; q < g->par_off[base + v + 1]; ++q) cptr[g->par_idx[q] + 1]++;
+    for (int64_t v = 0; v < n; ++v) cptr[v + 1] += cptr[v];
+    std::vector<int32_t> cidx(cptr[n]);
+    std::vector<int64_t> fill(cptr.begin(), cptr.end() - 1);
+    for (int64_t v = 0; v < n; ++v)
+        for (int64_t q = g->par_off[base + v]; q < g->par_off[base + v + 1]; ++q)
+            cidx[fill[g->par_idx[q]]++] = (int32_t)v;
+    std::vector<int64_t> stamp(n, -1);
+    std::vector<int32_t> cur, nxt;
+    if (out) out->clear();
+    for (int64_t v = 0; v < n; ++v) {
+        uint32_t cnt = 0;
+        stamp[v] = v;
+        cur.assign(1, (int32_t)v);
+        for (int h = 1; h <= H && !cur.empty(); ++h) {
+            nxt.clear();
+            for (int32_t x : cur)
+                for (int64_t q = cptr[x]; q < cptr[x + 1]; ++q) {
+                    const int32_t c = cidx[q];
+                    if (stamp[c] == v) continue;
+                    stamp[c] = v;
+                    nxt.push_back(c);
+                }
+            std::sort(nxt.begin(), nxt.end());
+            cnt += (uint32_t)nxt.size();
+            if (out)
+                for (int32_t c : nxt)
+                    out->push_back((uint32_t)(base + c) | ((uint32_t)h << fate::kDescDepthShift));
+            cur.swap(nxt);
+        }
+        count[base + v] = cnt;
+    }
+}
+
+struct DagLayout {
+    size_t exec, ksw, beta, weight, cap, fits, stage_off, rec, par, desc_off, desc, total;
+};
+
+DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc) {
+    DagLayout L;
+    size_t o = 0;
+    L.exec = o; o = align_up(o + sizeof(float) * M * D);
+    L.ksw = o; o = align_up(o + sizeof(float) * M * D);
+    L.beta = o; o = align_up(o + sizeof(float) * D * D);
+    L.weight = o; o = align_up(o + sizeof(uint64_t) * M);
+    L.cap = o; o = align_up(o + sizeof(uint64_t) * D);
+    L.fits = o; o = align_up(o + sizeof(uint64_t) * M);
+    L.stage_off = o; o = align_up(o + sizeof(int64_t) * (B + 1));
+    L.rec = o; o = align_up(o + sizeof(StageRec) * N);
+    L.par = o; o = align_up(o + sizeof(uint32_t) * E);
+    L.desc_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
+    L.desc = o; o = align_up(o + sizeof(uint32_t) * ndesc);
+    L.total = o;
+    return L;
+}
+
+struct DagsPlan {
+    int64_t N = 0, E = 0, ndesc = 0;
+    std::vector<uint32_t> count;
+    std::vector<std::vector<uint32_t>> lists;  // per instance, when building
+};
+
+fate_status_t plan_dags(const fate_cluster_t *c, const fate_dag_batch_t *g, int H, bool keep, DagsPlan *p) {
+    fate_status_t st = validate_cluster(c);
+    if (st != FATE_OK) return st;
+    if (H < 0 || H > FATE_MAX_HORIZON) return FATE_ERANGE;
+    st = validate_batch(c, g, &p->N, &p->E);
+    if (st != FATE_OK) return st;
+    p->count.assign(p->N, 0);
+    if (keep) p->lists.assign(g->B, {});
+    parallel_for(g->B, [&](int64_t b) {
+        instance_horizons(g, (int)b, H, p->count.data(), keep ? &p->lists[b] : nullptr);
+    });
+    int64_t tot = 0;
+    for (uint32_t x : p->count) tot += x;
+    if (tot >= (int64_t(1) << 32)) return FATE_ERANGE;
+    p->ndesc = tot;
+    return FATE_OK;
+}
+
+void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, int H, const DagsPlan &p,
+                      const DagLayout &L, uint8_t *base, size_t bytes, fate_dags_t *out) {
+    std::memset(out, 0, sizeof(*out));
+    out->B = g->B;
+    out->D = c->D;
+    out->M = c->M;
+    out->H = H;
+    out->N = p.N;
+    out->E = p.E;
+    out->n_desc = p.ndesc;
+    int uniform = 1;
+    float b0 = 0.0f;
+    bool first = true;
+    for (int i = 0; i < c->D; ++i)
+        for (int j = 0; j < c->D; ++j) {
+            if (i == j) continue;
+            float x = c->beta[i * c->D + j];
+            if (first) { b0 = x; first = false; }
+            else if (std::memcmp(&x, &b0, sizeof(float)) != 0) uniform = 0;
+        }
+    out->beta_uniform = uniform;
+    out->beta0 = b0;
+    out->base = base;
+    out->bytes = bytes;
+    out->exec = reinterpret_cast<const float *>(base + L.exec);
+    out->switch_s = reinterpret_cast<const float *>(base + L.ksw);
+    out->beta = reinterpret_cast<const float *>(base + L.beta);
+    out->weight = reinterpret_cast<const uint64_t *>(base + L.weight);
+    out->cap = reinterpret_cast<const uint64_t *>(base + L.cap);
+    out->fits = reinterpret_cast<const uint64_t *>(base + L.fits);
+    out->stage_off = reinterpret_cast<const int64_t *>(base + L.stage_off);
+    out->records = base + L.rec;
+    out->par_idx = reinterpret_cast<const uint32_t *>(base + L.par);
+    out->desc_off = reinterpret_cast<const uint32_t *>(base + L.desc_off);
+    out->desc = reinterpret_cast<const uint32_t *>(base + L.desc);
+}
+
+void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const DagsPlan &p,
+                      const DagLayout &L, uint8_t *img) {
+    const int D = c->D, M = c->M;
+    std::memcpy(img + L.exec, c->exec, sizeof(float) * M * D);
+    std::memcpy(img + L.ksw, c->switch_s, sizeof(float) * M * D);
+    std::memcpy(img + L.beta, c->beta, sizeof(float) * D * D);
+    uint64_t *w = reinterpret_cast<uint64_t *>(img + L.weight);
+    uint64_t *cp = reinterpret_cast<uint64_t *>(img + L.cap);
+    uint64_t *ft = reinterpret_cast<uint64_t *>(img + L.fits);
+    const std::vector<uint64_t> fits = fit_masks(c);
+    for (int m = 0; m < M; ++m) { w[m] = (uint64_t)c->weight_bytes[m]; ft[m] = fits[m]; }
+    for (int d = 0; d < D; ++d) cp[d] = (uint64_t)c->cap_bytes[d];
+    std::memcpy(img + L.stage_off, g->stage_off, sizeof(int64_t) * (g->B + 1));
+    StageRec *rec = reinterpret_cast<StageRec *>(img + L.rec);
+    uint32_t *par = reinterpret_cast<uint32_t *>(img + L.par);
+    uint32_t *doff = reinterpret_cast<uint32_t *>(img + L.desc_off);
+    uint32_t *desc = reinterpret_cast<uint32_t *>(img + L.desc);
+    uint32_t acc = 0;
+    for (int64_t s = 0; s < p.N; ++s) { doff[s] = acc; acc += p.count[s]; }
+    doff[p.N] = acc;
+    parallel_for(g->B, [&](int64_t b) {
+        const int64_t base = g->stage_off[b];
+        const int64_t n = g->stage_off[b + 1] - base;
+        for (int64_t v = 0; v < n; ++v) {
+            const int64_t s = base + v;
+            StageRec r;
+            r.elig = g->elig[s];
+            r.hash = g->prefix_hash[s];
+            r.tokens = g->prefix_tokens[s];
+            r.sigma = g->out_bytes[s];
+            r.par_begin = (uint32_t)g->par_off[s];
+            r.model = (uint8_t)g->model[s];
+            r.shard = (uint8_t)g->shard_max[s];
+            r.npar = (uint16_t)(g->par_off[s + 1] - g->par_off[s]);
+            rec[s] = r;
+            for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) par[q] = (uint32_t)(base + g->par_idx[q]);
+        }
+        if (n > 0 && !p.lists[b].empty())
+            std::memcpy(desc + doff[base], p.lists[b].data(), sizeof(uint32_t) * p.lists[b].size());
+    });
+}
+
+// ---------------------------------------------------------------------------
+// state
+// ---------------------------------------------------------------------------
+
+inline int shard_cap(int R, int max_shard, int D) { return std::max(1, std::min(std::min(R, max_shard), D)); }
+inline int64_t candidates_of(int r, int D) {
+    int64_t c = D;
+    for (int k = 2; k <= r; ++k) c += D - k + 1;
+    return c;
+}
+
+struct StatePlan {
+    std::vector<uint32_t> frontier;  // pairs
+    std::vector<uint32_t> cand_off;
+    int64_t nF = 0, nC = 0;
+};
+
+fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const fate_state_t *st,
+                         int max_shard, StatePlan *p) {
+    if (!pk || !g || !st) return FATE_EINVAL;
+    if (max_shard < 1 || max_shard > FATE_MAX_SHARD) return FATE_ERANGE;
+    if (st->K < 0 || st->K > FATE_MAX_PREFIX_SLOTS) return FATE_ERANGE;
+    if (g->B != pk->B || !g->stage_off || g->stage_off[g->B] != pk->N) return FATE_ESTATE;
+    const int B = g->B, D = pk->D, K = st->K;
+    const int64_t N = pk->N;
+    if (B > 0 && (!st->resident || !st->tau_free || !st->t_now)) return FATE_EINVAL;
+    if (N > 0 && (!st->holders || !st->status || !g->par_off || !g->shard_max)) return FATE_EINVAL;
+    if (pk->E > 0 && !g->par_idx) return FATE_EINVAL;
+    if (B > 0 && K > 0 && !st->prefix_cache) return FATE_EINVAL;
+    if (N > 0 && g->par_off[N] != pk->E) return FATE_ESTATE;
+    const uint64_t mm = pk->M >= 64 ? ~0ull : ((1ull << pk->M) - 1ull);
+    const uint64_t dm = dev_mask(D);
+    for (int64_t i = 0; i < (int64_t)B * D; ++i) {
+        if (st->resident[i] & ~mm) return FATE_EINVAL;
+        if (!std::isfinite(st->tau_free[i])) return FATE_EINVAL;
+    }
+    for (int b = 0; b < B; ++b)
+        if (!std::isfinite(st->t_now[b])) return FATE_EINVAL;
+    p->cand_off.clear();
+    p->frontier.clear();
+    int64_t nc = 0;
+    for (int b = 0; b < B; ++b) {
+        const int64_t base = g->stage_off[b];
+        const int64_t n = g->stage_off[b + 1] - base;
+        for (int64_t v = 0; v < n; ++v) {
+            const int64_t s = base + v;
+            const uint8_t status = st->status[s];
+            const uint64_t hold = st->holders[s];
+            if (status > FATE_COMMITTED) return FATE_EINVAL;
+            if (hold & ~dm) return FATE_ESTATE;
+            if ((status == FATE_COMPLETED) != (hold != 0)) return FATE_ESTATE;
+            bool parents_done = true;
+            for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) {
+                const int64_t u = g->par_idx[q];
+                if (u < 0 || u >= v) return FATE_ECYCLE;
+                if (st->status[base + u] != FATE_COMPLETED) parents_done = false;
+            }
+            if ((status == FATE_COMPLETED || status == FATE_RUNNING) && !parents_done) return FATE_ESTATE;
+            if (status == FATE_PENDING && parents_done) {
+                p->frontier.push_back((uint32_t)s);
+                p->frontier.push_back((uint32_t)b);
+                p->cand_off.push_back((uint32_t)nc);
+                nc += candidates_of(shard_cap(g->shard_max[s], max_shard, D), D);
+                if (nc >= (int64_t(1) << 32)) return FATE_ERANGE;
+            }
+        }
+    }
+    p->cand_off.push_back((uint32_t)nc);
+    p->nF = (int64_t)p->frontier.size() / 2;
+    p->nC = nc;
+    return FATE_OK;
+}
+
+struct StateLayout {
+    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, total;
+};
+
+StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF) {
+    StateLayout L;
+    size_t o = 0;
+    L.resident = o; o = align_up(o + sizeof(uint64_t) * B * D);
+    L.pcache = o; o = align_up(o + sizeof(uint64_t) * (size_t)B * D * K);
+    L.holders = o; o = align_up(o + sizeof(uint64_t) * N);
+    L.tau = o; o = align_up(o + sizeof(float) * B * D);
+    L.tnow = o; o = align_up(o + sizeof(float) * B);
+    L.frontier = o; o = align_up(o + sizeof(uint32_t) * 2 * nF);
+    L.cand_off = o; o = align_up(o + sizeof(uint32_t) * (nF + 1));
+    L.total = o;
+    return L;
+}
+
+void write_state_image(const fate_dags_t *pk, const fate_state_t *st, const StatePlan &p, const StateLayout &L,
+                       uint8_t *img) {
+    const int B = pk->B, D = pk->D, K = st->K;
+    std::memcpy(img + L.resident, st->resident, sizeof(uint64_t) * B * D);
+    if (K > 0) std::memcpy(img + L.pcache, st->prefix_cache, sizeof(uint64_t) * (size_t)B * D * K);
+    std::memcpy(img + L.holders, st->holders, sizeof(uint64_t) * pk->N);
+    std::memcpy(img + L.tau, st->tau_free, sizeof(float) * B * D);
+    std::memcpy(img + L.tnow, st->t_now, sizeof(float) * B);
+    std::memcpy(img + L.frontier, p.frontier.data(), sizeof(uint32_t) * p.frontier.size());
+    std::memcpy(img + L.cand_off, p.cand_off.data(), sizeof(uint32_t) * p.cand_off.size());
+}
+
+void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_shard, const StatePlan &p,
+                       const StateLayout &L, uint8_t *base, size_t bytes, fate_state_h *out) {
+    std::memset(out, 0, sizeof(*out));
+    out->B = pk->B;
+    out->D = pk->D;
+    out->K = st->K;
+    out->max_shard = max_shard;
+    out->N = pk->N;
+    out->n_frontier = p.nF;
+    out->n_cand = p.nC;
+    out->base = base;
+    out->bytes = bytes;
+    out->resident = reinterpret_cast<const uint64_t *>(base + L.resident);
+    out->prefix_cache = reinterpret_cast<const uint64_t *>(base + L.pcache);
+    out->holders = reinterpret_cast<const uint64_t *>(base + L.holders);
+    out->tau_free = reinterpret_cast<const float *>(base + L.tau);
+    out->t_now = reinterpret_cast<const float *>(base + L.tnow);
+    out->frontier = reinterpret_cast<const uint32_t *>(base + L.frontier);
+    out->cand_off = reinterpret_cast<const uint32_t *>(base + L.cand_off);
+}
+
+fate_status_t copy_to_device(void *d_buf, const void *h, size_t bytes, void *stream) {
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (hipMemcpyAsync(d_buf, h, bytes, hipMemcpyHostToDevice, s) != hipSuccess) return FATE_EHIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return FATE_EHIP;
+    return FATE_OK;
+}
+
+bool params_ok(const fate_params_t *p) {
+    const float v[] = {p->lam_q, p->lam_s, p->lam_tr, p->lam_c, p->lam_p, p->kappa_prefix, p->gamma};
+    for (float x : v)
+        if (!finite_nonneg(x)) return false;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *fate_version(void) { return "fate-mi355x 0.1.0 (gfx950)"; }
+
+const char *fate_strerror(fate_status_t s) {
+    switch (s) {
+        case FATE_OK: return "ok";
+        case FATE_EINVAL: return "invalid argument";
+        case FATE_ERANGE: return "value out of supported range";
+        case FATE_ECYCLE: return "parent id not below child id (not a DAG in topological order)";
+        case FATE_ENOFEAS: return "stage has no eligible device that can hold its model";
+        case FATE_ESIZE: return "caller buffer too small";
+        case FATE_ESTATE: return "inconsistent execution state or handle";
+        case FATE_EHIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+fate_status_t fate_pack_dags_size(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
+                                  size_t *bytes) {
+    if (!bytes) return FATE_EINVAL;
+    DagsPlan p;
+    fate_status_t st = plan_dags(cluster, dags, H, false, &p);
+    if (st != FATE_OK) return st;
+    *bytes = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc).total;
+    return FATE_OK;
+}
+
+static fate_status_t build_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
+                                size_t bytes, std::vector<uint8_t> &img, DagsPlan &p, DagLayout &L) {
+    fate_status_t st = plan_dags(cluster, dags, H, true, &p);
+    if (st != FATE_OK) return st;
+    L = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc);
+    if (bytes < L.total) return FATE_ESIZE;
+    img.assign(L.total, 0);
+    write_dags_image(cluster, dags, p, L, img.data());
+    return FATE_OK;
+}
+
+fate_status_t fate_layout_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
+                               void *h_buf, size_t bytes, fate_dags_t *out) {
+    if (!h_buf || !out) return FATE_EINVAL;
+    std::vector<uint8_t> img;
+    DagsPlan p;
+    DagLayout L;
+    fate_status_t st = build_dags(cluster, dags, H, bytes, img, p, L);
+    if (st != FATE_OK) return st;
+    std::memcpy(h_buf, img.data(), L.total);
+    fill_dags_handle(cluster, dags, H, p, L, static_cast<uint8_t *>(h_buf), bytes, out);
+    return FATE_OK;
+}
+
+fate_status_t fate_pack_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
+                             void *d_buf, size_t bytes, void *stream, fate_dags_t *out) {
+    if (!d_buf || !out) return FATE_EINVAL;
+    std::vector<uint8_t> img;
+    DagsPlan p;
+    DagLayout L;
+    fate_status_t st = build_dags(cluster, dags, H, bytes, img, p, L);
+    if (st != FATE_OK) return st;
+    st = copy_to_device(d_buf, img.data(), L.total, stream);
+    if (st != FATE_OK) return st;
+    fill_dags_handle(cluster, dags, H, p, L, static_cast<uint8_t *>(d_buf), bytes, out);
+    return FATE_OK;
+}
+
+fate_status_t fate_pack_state_size(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                   const fate_state_t *state, int32_t max_shard, size_t *bytes,
+                                   int64_t *n_frontier, int64_t *n_cand) {
+    if (!bytes) return FATE_EINVAL;
+    StatePlan p;
+    fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
+    if (st != FATE_OK) return st;
+    *bytes = state_layout(packed->B, packed->D, state->K, packed->N, p.nF).total;
+    if (n_frontier) *n_frontier = p.nF;
+    if (n_cand) *n_cand = p.nC;
+    return FATE_OK;
+}
+
+static fate_status_t build_state(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                 const fate_state_t *state, int32_t max_shard, size_t bytes,
+                                 std::vector<uint8_t> &img, StatePlan &p, StateLayout &L) {
+    fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
+    if (st != FATE_OK) return st;
+    L = state_layout(packed->B, packed->D, state->K, packed->N, p.nF);
+    if (bytes < L.total) return FATE_ESIZE;
+    img.assign(L.total, 0);
+    write_state_image(packed, state, p, L, img.data());
+    return FATE_OK;
+}
+
+fate_status_t fate_layout_state(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                const fate_state_t *state, int32_t max_shard, void *h_buf, size_t bytes,
+                                fate_state_h *out) {
+    if (!h_buf || !out) return FATE_EINVAL;
+    std::vector<uint8_t> img;
+    StatePlan p;
+    StateLayout L;
+    fate_status_t st = build_state(packed, dags, state, max_shard, bytes, img, p, L);
+    if (st != FATE_OK) return st;
+    std::memcpy(h_buf, img.data(), L.total);
+    fill_state_handle(packed, state, max_shard, p, L, static_cast<uint8_t *>(h_buf), bytes, out);
+    return FATE_OK;
+}
+
+fate_status_t fate_pack_state(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                              const fate_state_t *state, int32_t max_shard, void *d_buf, size_t bytes,
+                              void *stream, fate_state_h *out) {
+    if (!d_buf || !out) return FATE_EINVAL;
+    std::vector<uint8_t> img;
+    StatePlan p;
+    StateLayout L;
+    fate_status_t st = build_state(packed, dags, state, max_shard, bytes, img, p, L);
+    if (st != FATE_OK) return st;
+    st = copy_to_device(d_buf, img.data(), L.total, stream);
+    if (st != FATE_OK) return st;
+    fill_state_handle(packed, state, max_shard, p, L, static_cast<uint8_t *>(d_buf), bytes, out);
+    return FATE_OK;
+}
+
+static fate_status_t check_pair(const fate_dags_t *dags, const fate_state_h *state) {
+    if (!dags || !state) return FATE_EINVAL;
+    if (dags->B != state->B || dags->D != state->D || dags->N != state->N) return FATE_ESTATE;
+    if (!dags->records || !state->frontier || !state->cand_off) return FATE_EINVAL;
+    return FATE_OK;
+}
+
+fate_status_t fate_score_ws_size(const fate_dags_t *dags, const fate_state_h *state, size_t *bytes) {
+    if (!bytes) return FATE_EINVAL;
+    fate_status_t st = check_pair(dags, state);
+    if (st != FATE_OK) return st;
+    *bytes = 0;
+    return FATE_OK;
+}
+
+fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *state,
+                                  const fate_params_t *params, float *d_scores, int64_t n_scores,
+                                  void *d_ws, size_t ws_bytes, void *stream) {
+    (void)d_ws;
+    (void)ws_bytes;
+    fate_status_t st = check_pair(dags, state);
+    if (st != FATE_OK) return st;
+    if (!params || !params_ok(params)) return FATE_EINVAL;
+    if (params->H < 0 || params->H > dags->H) return FATE_EINVAL;
+    if (n_scores < state->n_cand) return FATE_ESIZE;
+    if (state->n_frontier == 0) return FATE_OK;
+    if (!d_scores) return FATE_EINVAL;
+    fate::ScoreLaunch a;
+    a.rec = static_cast<const StageRec *>(dags->records);
+    a.par_idx = dags->par_idx;
+    a.desc_off = dags->desc_off;
+    a.desc = dags->desc;
+    a.exec = dags->exec;
+    a.ksw = dags->switch_s;
+    a.beta = dags->beta;
+    a.weight = dags->weight;
+    a.cap = dags->cap;
+    a.fits = dags->fits;
+    a.resident = state->resident;
+    a.pcache = state->prefix_cache;
+    a.holders = state->holders;
+    a.tau = state->tau_free;
+    a.tnow = state->t_now;
+    a.frontier = state->frontier;
+    a.cand_off = state->cand_off;
+    a.scores = d_scores;
+    a.nF = state->n_frontier;
+    a.D = dags->D;
+    a.M = dags->M;
+    a.K = state->K;
+    a.H = params->H;
+    a.max_shard = state->max_shard;
+    a.beta_uniform = dags->beta_uniform;
+    a.beta0 = dags->beta0;
+    a.lam_q = params->lam_q;
+    a.lam_s = params->lam_s;
+    a.lam_tr = params->lam_tr;
+    a.lam_c = params->lam_c;
+    a.lam_p = params->lam_p;
+    a.kpf = params->kappa_prefix;
+    a.gamma = params->gamma;
+    return fate::launch_score(a, stream) == 0 ? FATE_OK : FATE_EHIP;
+}
+
+fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_t n_scores, int32_t k,
+                        int32_t *d_idx, float *d_val, void *stream) {
+    if (!state) return FATE_EINVAL;
+    if (k < 1 || k > FATE_MAX_TOPK) return FATE_ERANGE;
+    if (n_scores < state->n_cand) return FATE_ESIZE;
+    if (state->n_frontier == 0) return FATE_OK;
+    if (!d_scores || !d_idx || !d_val || !state->cand_off) return FATE_EINVAL;
+    fate::TopkLaunch a;
+    a.cand_off = state->cand_off;
+    a.scores = d_scores;
+    a.idx = d_idx;
+    a.val = d_val;
+    a.nF = state->n_frontier;
+    a.D = state->D;
+    a.k = k;
+    return fate::launch_topk(a, stream) == 0 ? FATE_OK : FATE_EHIP;
+}
+
+}  // extern "C"

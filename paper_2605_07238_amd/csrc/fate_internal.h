@@ -1,0 +1,65 @@
+// Internal layout shared by the host packer and the HIP kernels of libfate.
+#pragma once
+
+#include <stdint.h>
+
+#include "fate.h"
+
+namespace fate {
+
+// 32-byte stage record, one per flat stage id (Sec. 2 stage tuple: model,
+// eligible devices, shard cap, prefix group and length, output size, parents).
+struct alignas(16) StageRec {
+    uint64_t elig;       // A(v) device bitmask
+    uint64_t hash;       // grp(v), 0 = none
+    float tokens;        // L(v)
+    float sigma;         // output bytes
+    uint32_t par_begin;  // first entry of this stage in the flat parent list
+    uint8_t model;       // m(v)
+    uint8_t shard;       // R(v)
+    uint16_t npar;       // |Pa(v)|
+};
+static_assert(sizeof(StageRec) == 32, "stage record must be 32 bytes");
+
+constexpr uint32_t kDescIdMask = (1u << 28) - 1u;
+constexpr int kDescDepthShift = 28;
+
+struct ScoreLaunch {
+    const StageRec *rec;
+    const uint32_t *par_idx;
+    const uint32_t *desc_off;
+    const uint32_t *desc;
+    const float *exec;
+    const float *ksw;
+    const float *beta;
+    const uint64_t *weight;
+    const uint64_t *cap;
+    const uint64_t *fits;
+    const uint64_t *resident;
+    const uint64_t *pcache;
+    const uint64_t *holders;
+    const float *tau;
+    const float *tnow;
+    const uint32_t *frontier;
+    const uint32_t *cand_off;
+    float *scores;
+    int64_t nF;
+    int32_t D, M, K, H, max_shard, beta_uniform;
+    float beta0;
+    float lam_q, lam_s, lam_tr, lam_c, lam_p, kpf, gamma;
+};
+
+struct TopkLaunch {
+    const uint32_t *cand_off;
+    const float *scores;
+    int32_t *idx;
+    float *val;
+    int64_t nF;
+    int32_t D, k;
+};
+
+// Kernel launchers (fate_kernels.hip).  Return a hipError_t as int.
+int launch_score(const ScoreLaunch &a, void *stream);
+int launch_topk(const TopkLaunch &a, void *stream);
+
+}  // namespace fate

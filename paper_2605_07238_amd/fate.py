@@ -1,0 +1,327 @@
+"""Thin ctypes binding of libfate (include/fate.h).
+
+Argument marshalling only: numpy host arrays are passed by pointer, device
+buffers are torch tensors (torch is used for device memory and streams), and
+every step of the scoring path runs in libfate's HIP kernels.  There is no
+fallback: if the library is missing or a call fails, an exception is raised.
+
+Entry points mirror the C names: :func:`fate_pack_dags`,
+:func:`fate_pack_state`, :func:`fate_score_frontier`, :func:`fate_topk`, plus
+the host-only :func:`fate_layout_dags` / :func:`fate_layout_state`.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfate.so")
+
+FATE_OK = 0
+STATUS_NAMES = {0: "FATE_OK", -1: "FATE_EINVAL", -2: "FATE_ERANGE", -3: "FATE_ECYCLE", -4: "FATE_ENOFEAS",
+                -5: "FATE_ESIZE", -6: "FATE_ESTATE", -7: "FATE_EHIP"}
+
+# Every symbol declared in include/fate.h.
+EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_dags", "fate_layout_dags",
+           "fate_pack_state_size", "fate_pack_state", "fate_layout_state", "fate_score_ws_size",
+           "fate_score_frontier", "fate_topk"]
+
+
+class FateError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s failed: %s (%s)" % (what, STATUS_NAMES.get(status, status), _strerror(status)))
+
+
+class Cluster(C.Structure):
+    _fields_ = [("D", C.c_int32), ("M", C.c_int32), ("exec", C.c_void_p), ("switch_s", C.c_void_p),
+                ("weight_bytes", C.c_void_p), ("cap_bytes", C.c_void_p), ("beta", C.c_void_p)]
+
+
+class DagBatch(C.Structure):
+    _fields_ = [("B", C.c_int32), ("stage_off", C.c_void_p), ("par_off", C.c_void_p), ("par_idx", C.c_void_p),
+                ("model", C.c_void_p), ("elig", C.c_void_p), ("shard_max", C.c_void_p),
+                ("prefix_hash", C.c_void_p), ("prefix_tokens", C.c_void_p), ("out_bytes", C.c_void_p)]
+
+
+class State(C.Structure):
+    _fields_ = [("K", C.c_int32), ("resident", C.c_void_p), ("prefix_cache", C.c_void_p),
+                ("holders", C.c_void_p), ("status", C.c_void_p), ("tau_free", C.c_void_p),
+                ("t_now", C.c_void_p)]
+
+
+class Params(C.Structure):
+    _fields_ = [("lam_q", C.c_float), ("lam_s", C.c_float), ("lam_tr", C.c_float), ("lam_c", C.c_float),
+                ("lam_p", C.c_float), ("kappa_prefix", C.c_float), ("gamma", C.c_float), ("H", C.c_int32)]
+
+
+class Dags(C.Structure):
+    _fields_ = [("B", C.c_int32), ("D", C.c_int32), ("M", C.c_int32), ("H", C.c_int32),
+                ("N", C.c_int64), ("E", C.c_int64), ("n_desc", C.c_int64),
+                ("beta_uniform", C.c_int32), ("beta0", C.c_float),
+                ("base", C.c_void_p), ("bytes", C.c_size_t),
+                ("exec", C.c_void_p), ("switch_s", C.c_void_p), ("beta", C.c_void_p),
+                ("weight", C.c_void_p), ("cap", C.c_void_p), ("fits", C.c_void_p),
+                ("records", C.c_void_p), ("par_idx", C.c_void_p), ("desc_off", C.c_void_p),
+                ("desc", C.c_void_p), ("stage_off", C.c_void_p)]
+
+
+class StateH(C.Structure):
+    _fields_ = [("B", C.c_int32), ("D", C.c_int32), ("K", C.c_int32), ("max_shard", C.c_int32),
+                ("N", C.c_int64), ("n_frontier", C.c_int64), ("n_cand", C.c_int64),
+                ("base", C.c_void_p), ("bytes", C.c_size_t),
+                ("resident", C.c_void_p), ("prefix_cache", C.c_void_p), ("holders", C.c_void_p),
+                ("tau_free", C.c_void_p), ("t_now", C.c_void_p),
+                ("frontier", C.c_void_p), ("cand_off", C.c_void_p)]
+
+
+_lib = None
+
+
+def load(path: Optional[str] = None):
+    """Load libfate.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError("libfate.so not found at %s; build it with `python -m paper_2605_07238_amd.build`" % p)
+    lib = C.CDLL(p)
+    P = C.POINTER
+    st = C.c_int
+    lib.fate_version.restype = C.c_char_p
+    lib.fate_strerror.restype = C.c_char_p
+    lib.fate_strerror.argtypes = [st]
+    lib.fate_pack_dags_size.argtypes = [P(Cluster), P(DagBatch), C.c_int32, P(C.c_size_t)]
+    lib.fate_pack_dags.argtypes = [P(Cluster), P(DagBatch), C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p, P(Dags)]
+    lib.fate_layout_dags.argtypes = [P(Cluster), P(DagBatch), C.c_int32, C.c_void_p, C.c_size_t, P(Dags)]
+    lib.fate_pack_state_size.argtypes = [P(Dags), P(DagBatch), P(State), C.c_int32, P(C.c_size_t),
+                                         P(C.c_int64), P(C.c_int64)]
+    lib.fate_pack_state.argtypes = [P(Dags), P(DagBatch), P(State), C.c_int32, C.c_void_p, C.c_size_t,
+                                    C.c_void_p, P(StateH)]
+    lib.fate_layout_state.argtypes = [P(Dags), P(DagBatch), P(State), C.c_int32, C.c_void_p, C.c_size_t, P(StateH)]
+    lib.fate_score_ws_size.argtypes = [P(Dags), P(StateH), P(C.c_size_t)]
+    lib.fate_score_frontier.argtypes = [P(Dags), P(StateH), P(Params), C.c_void_p, C.c_int64, C.c_void_p,
+                                        C.c_size_t, C.c_void_p]
+    lib.fate_topk.argtypes = [P(StateH), C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
+    for name in EXPORTS[2:]:
+        getattr(lib, name).restype = st
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _strerror(status: int) -> str:
+    try:
+        return load().fate_strerror(status).decode()
+    except Exception:  # noqa: BLE001 - best effort in an error path
+        return "?"
+
+
+def _check(status: int, what: str):
+    if status != FATE_OK:
+        raise FateError(status, what)
+
+
+def version() -> str:
+    return load().fate_version().decode()
+
+
+def _c(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+class HostInputs:
+    """C views of a workload's host arrays (kept alive by this object)."""
+
+    def __init__(self, w):
+        self.keep = dict(
+            exec=_c(w.exec, np.float32), switch_s=_c(w.switch_s, np.float32),
+            weight=_c(w.weight_bytes, np.int64), cap=_c(w.cap_bytes, np.int64), beta=_c(w.beta, np.float32),
+            stage_off=_c(w.stage_off, np.int64), par_off=_c(w.par_off, np.int64), par_idx=_c(w.par_idx, np.int32),
+            model=_c(w.model, np.int32), elig=_c(w.elig, np.uint64), shard=_c(w.shard_max, np.int32),
+            hash=_c(w.prefix_hash, np.uint64), tokens=_c(w.prefix_tokens, np.float32),
+            sigma=_c(w.out_bytes, np.float32),
+            resident=_c(w.resident, np.uint64), cache=_c(w.prefix_cache, np.uint64),
+            holders=_c(w.holders, np.uint64), status=_c(w.status, np.uint8),
+            tau=_c(w.tau_free, np.float32), t_now=_c(w.t_now, np.float32),
+        )
+        k = self.keep
+        ptr = lambda a: a.ctypes.data if a.size else None
+        self.cluster = Cluster(int(w.D), int(w.M), ptr(k["exec"]), ptr(k["switch_s"]), ptr(k["weight"]),
+                               ptr(k["cap"]), ptr(k["beta"]))
+        self.batch = DagBatch(int(w.B), k["stage_off"].ctypes.data, ptr(k["par_off"]), ptr(k["par_idx"]),
+                              ptr(k["model"]), ptr(k["elig"]), ptr(k["shard"]), ptr(k["hash"]), ptr(k["tokens"]),
+                              ptr(k["sigma"]))
+        self.state = State(int(w.K), ptr(k["resident"]), ptr(k["cache"]), ptr(k["holders"]), ptr(k["status"]),
+                           ptr(k["tau"]), ptr(k["t_now"]))
+
+
+def _stream_ptr(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class PackedDags:
+    def __init__(self, buf, handle: Dags, host: HostInputs):
+        self.buf = buf          # torch uint8 device tensor owning the memory
+        self.handle = handle
+        self.host = host
+
+
+class PackedState:
+    def __init__(self, buf, handle: StateH, host: HostInputs):
+        self.buf = buf
+        self.handle = handle
+        self.host = host
+
+    @property
+    def n_frontier(self) -> int:
+        return int(self.handle.n_frontier)
+
+    @property
+    def n_cand(self) -> int:
+        return int(self.handle.n_cand)
+
+
+def fate_pack_dags_size(w, H: int) -> int:
+    hi = HostInputs(w)
+    nbytes = C.c_size_t(0)
+    _check(load().fate_pack_dags_size(C.byref(hi.cluster), C.byref(hi.batch), int(H), C.byref(nbytes)),
+           "fate_pack_dags_size")
+    return int(nbytes.value)
+
+
+def fate_pack_dags(w, H: Optional[int] = None, device="cuda", stream=None) -> PackedDags:
+    """Validate and pack workload ``w``'s DAG batch into a device buffer."""
+    import torch
+    H = int(w.H if H is None else H)
+    lib = load()
+    hi = HostInputs(w)
+    nbytes = C.c_size_t(0)
+    _check(lib.fate_pack_dags_size(C.byref(hi.cluster), C.byref(hi.batch), H, C.byref(nbytes)), "fate_pack_dags_size")
+    buf = torch.empty(max(1, nbytes.value), dtype=torch.uint8, device=device)
+    h = Dags()
+    _check(lib.fate_pack_dags(C.byref(hi.cluster), C.byref(hi.batch), H, C.c_void_p(buf.data_ptr()),
+                              nbytes.value, C.c_void_p(_stream_ptr(stream)), C.byref(h)), "fate_pack_dags")
+    return PackedDags(buf, h, hi)
+
+
+def fate_layout_dags(w, H: Optional[int] = None):
+    """Host-only packed image of the DAG batch: (numpy uint8 buffer, Dags handle)."""
+    H = int(w.H if H is None else H)
+    lib = load()
+    hi = HostInputs(w)
+    nbytes = C.c_size_t(0)
+    _check(lib.fate_pack_dags_size(C.byref(hi.cluster), C.byref(hi.batch), H, C.byref(nbytes)), "fate_pack_dags_size")
+    buf = np.zeros(max(1, nbytes.value), np.uint8)
+    h = Dags()
+    _check(lib.fate_layout_dags(C.byref(hi.cluster), C.byref(hi.batch), H, buf.ctypes.data, nbytes.value,
+                                C.byref(h)), "fate_layout_dags")
+    return buf, h, hi
+
+
+def fate_pack_state(packed: PackedDags, w, max_shard: Optional[int] = None, device="cuda",
+                    stream=None) -> PackedState:
+    """Validate the state of ``w`` against ``packed`` and pack state + frontier."""
+    import torch
+    ms = int(w.max_shard if max_shard is None else max_shard)
+    lib = load()
+    hi = HostInputs(w)
+    nbytes = C.c_size_t(0)
+    nf, nc = C.c_int64(0), C.c_int64(0)
+    _check(lib.fate_pack_state_size(C.byref(packed.handle), C.byref(hi.batch), C.byref(hi.state), ms,
+                                    C.byref(nbytes), C.byref(nf), C.byref(nc)), "fate_pack_state_size")
+    buf = torch.empty(max(1, nbytes.value), dtype=torch.uint8, device=device)
+    h = StateH()
+    _check(lib.fate_pack_state(C.byref(packed.handle), C.byref(hi.batch), C.byref(hi.state), ms,
+                               C.c_void_p(buf.data_ptr()), nbytes.value, C.c_void_p(_stream_ptr(stream)),
+                               C.byref(h)), "fate_pack_state")
+    return PackedState(buf, h, hi)
+
+
+def fate_layout_state(dags_handle: Dags, w, max_shard: Optional[int] = None):
+    """Host-only packed state image: (numpy uint8 buffer, StateH handle)."""
+    ms = int(w.max_shard if max_shard is None else max_shard)
+    lib = load()
+    hi = HostInputs(w)
+    nbytes = C.c_size_t(0)
+    nf, nc = C.c_int64(0), C.c_int64(0)
+    _check(lib.fate_pack_state_size(C.byref(dags_handle), C.byref(hi.batch), C.byref(hi.state), ms,
+                                    C.byref(nbytes), C.byref(nf), C.byref(nc)), "fate_pack_state_size")
+    buf = np.zeros(max(1, nbytes.value), np.uint8)
+    h = StateH()
+    _check(lib.fate_layout_state(C.byref(dags_handle), C.byref(hi.batch), C.byref(hi.state), ms, buf.ctypes.data,
+                                 nbytes.value, C.byref(h)), "fate_layout_state")
+    return buf, h, hi
+
+
+def make_params(w=None, H: Optional[int] = None, **over) -> Params:
+    from . import synth
+    p = dict(synth.DEFAULT_PARAMS)
+    if w is not None:
+        p.update(w.params)
+    p.update({k: v for k, v in over.items() if k != "H"})
+    Hv = int(H if H is not None else (w.H if w is not None else 0))
+    return Params(p["lam_q"], p["lam_s"], p["lam_tr"], p["lam_c"], p["lam_p"], p["kappa_prefix"], p["gamma"], Hv)
+
+
+def fate_score_frontier(packed: PackedDags, state: PackedState, params: Params, out=None, stream=None):
+    """Score every candidate; returns a float32 device tensor [n_cand]."""
+    import torch
+    lib = load()
+    nc = state.n_cand
+    if out is None:
+        out = torch.empty(max(1, nc), dtype=torch.float32, device=packed.buf.device)
+    ws = C.c_size_t(0)
+    _check(lib.fate_score_ws_size(C.byref(packed.handle), C.byref(state.handle), C.byref(ws)), "fate_score_ws_size")
+    wsbuf = torch.empty(max(1, ws.value), dtype=torch.uint8, device=packed.buf.device) if ws.value else None
+    _check(lib.fate_score_frontier(C.byref(packed.handle), C.byref(state.handle), C.byref(params),
+                                   C.c_void_p(out.data_ptr()), int(out.numel()),
+                                   C.c_void_p(wsbuf.data_ptr()) if wsbuf is not None else None, ws.value,
+                                   C.c_void_p(_stream_ptr(stream))), "fate_score_frontier")
+    return out
+
+
+def fate_topk(state: PackedState, scores, k: int, idx=None, val=None, stream=None):
+    """Per-frontier-stage top-k; returns (int32 [F, k], float32 [F, k]) device tensors."""
+    import torch
+    lib = load()
+    F = state.n_frontier
+    dev = scores.device
+    if idx is None:
+        idx = torch.empty((max(1, F), k), dtype=torch.int32, device=dev)
+    if val is None:
+        val = torch.empty((max(1, F), k), dtype=torch.float32, device=dev)
+    _check(lib.fate_topk(C.byref(state.handle), C.c_void_p(scores.data_ptr()), int(scores.numel()), int(k),
+                         C.c_void_p(idx.data_ptr()), C.c_void_p(val.data_ptr()),
+                         C.c_void_p(_stream_ptr(stream))), "fate_topk")
+    return idx[:F], val[:F]
+
+
+def frontier_table(state: PackedState):
+    """Host copies of the packed frontier: (flat stage ids, instances, cand_off)."""
+    import torch
+    h = state.handle
+    F = int(h.n_frontier)
+    base = state.buf.data_ptr()
+    off_f = h.frontier - base
+    off_c = h.cand_off - base
+    fr = state.buf[off_f:off_f + 8 * F].view(torch.int32).cpu().numpy().reshape(F, 2) if F else np.zeros((0, 2), np.int32)
+    co = state.buf[off_c:off_c + 4 * (F + 1)].view(torch.int32).cpu().numpy()
+    return fr[:, 0].astype(np.int64), fr[:, 1].astype(np.int64), co.astype(np.int64)
+
+
+def desc_counts(packed: PackedDags):
+    """Host copy of every stage's horizon-descendant count (from desc_off)."""
+    import torch
+    h = packed.handle
+    N = int(h.N)
+    off = h.desc_off - packed.buf.data_ptr()
+    do = packed.buf[off:off + 4 * (N + 1)].view(torch.int32).cpu().numpy().astype(np.int64)
+    return np.diff(do)

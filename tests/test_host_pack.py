@@ -1,0 +1,204 @@
+"""Host half of packing, run without a GPU: the packed image round-trips the
+inputs, the descendant lists equal breadth-first distances computed with
+scipy, the frontier and candidate offsets follow the definitions, and every
+validation error code fires on the input that should trigger it."""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+from scipy.sparse.csgraph import shortest_path
+
+from paper_2605_07238_amd import fate, synth
+
+REC = np.dtype([("elig", "<u8"), ("hash", "<u8"), ("tokens", "<f4"), ("sigma", "<f4"),
+                ("par_begin", "<u4"), ("model", "u1"), ("shard", "u1"), ("npar", "<u2")])
+
+
+def _view(buf, base, ptr, dtype, count):
+    off = ptr - base
+    return np.frombuffer(buf, dtype=dtype, count=count, offset=off)
+
+
+def unpack_dags(buf, h):
+    base = buf.ctypes.data
+    N, E = int(h.N), int(h.E)
+    return dict(
+        rec=_view(buf, base, h.records, REC, N),
+        par=_view(buf, base, h.par_idx, np.uint32, E),
+        desc_off=_view(buf, base, h.desc_off, np.uint32, N + 1),
+        desc=_view(buf, base, h.desc, np.uint32, int(h.n_desc)),
+        fits=_view(buf, base, h.fits, np.uint64, int(h.M)),
+    )
+
+
+@pytest.mark.parametrize("maker", [
+    lambda: synth.make_workload("tiny-layered-1x24-d4"),
+    lambda: synth.make_workload("layered-1024x200-d8", B=3),
+    lambda: synth.make_workload("forkjoin-4096x1000-d16", B=2),
+    lambda: synth.make_workload("shards-1024x500-d16", B=2),
+    lambda: synth.make_random_small(3, B=3, n=15),
+])
+def test_dags_image_roundtrip(maker):
+    w = maker()
+    buf, h, _ = fate.fate_layout_dags(w)
+    u = unpack_dags(buf, h)
+    rec = u["rec"]
+    assert np.array_equal(rec["elig"], w.elig)
+    assert np.array_equal(rec["hash"], w.prefix_hash)
+    assert np.array_equal(rec["model"], w.model.astype(np.uint8))
+    assert np.array_equal(rec["shard"], w.shard_max.astype(np.uint8))
+    assert np.array_equal(rec["tokens"], w.prefix_tokens)
+    assert np.array_equal(rec["sigma"], w.out_bytes)
+    assert np.array_equal(rec["npar"], np.diff(w.par_off).astype(np.uint16))
+    assert np.array_equal(rec["par_begin"], w.par_off[:-1].astype(np.uint32))
+    inst = np.repeat(np.arange(w.B), np.diff(w.stage_off))
+    exp_par = (w.par_idx.astype(np.int64) + w.stage_off[inst[np.repeat(np.arange(w.N), np.diff(w.par_off))]])
+    assert np.array_equal(u["par"], exp_par.astype(np.uint32))
+    fits = [sum(1 << d for d in range(w.D) if w.weight_bytes[m] <= w.cap_bytes[d]) for m in range(w.M)]
+    assert u["fits"].tolist() == fits
+    # descendant lists = breadth-first distances 1..H, ordered by (distance, id)
+    for b in range(w.B):
+        lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+        n = hi - lo
+        rows = []
+        cols = []
+        for x in range(n):
+            for p in w.par_idx[w.par_off[lo + x]:w.par_off[lo + x + 1]]:
+                rows.append(int(p))
+                cols.append(x)
+        dist = shortest_path(sp.csr_matrix((np.ones(len(rows)), (rows, cols)), shape=(n, n)),
+                             directed=True, unweighted=True)
+        for v in range(n):
+            ents = u["desc"][u["desc_off"][lo + v]:u["desc_off"][lo + v + 1]]
+            got = [(int(e >> 28), int(e & ((1 << 28) - 1)) - lo) for e in ents]
+            exp = sorted((int(dist[v, x]), x) for x in range(n) if 1 <= dist[v, x] <= w.H)
+            assert got == exp, (b, v)
+
+
+def _cands(D, r):
+    return D + sum(D - k + 1 for k in range(2, r + 1))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_state_image_frontier(seed):
+    w = synth.make_random_small(seed, B=3, n=14, D=5, max_shard=3)
+    buf, h, _ = fate.fate_layout_dags(w)
+    sbuf, sh, _ = fate.fate_layout_state(h, w)
+    base = sbuf.ctypes.data
+    F = int(sh.n_frontier)
+    fr = _view(sbuf, base, sh.frontier, np.uint32, 2 * F).reshape(F, 2)
+    co = _view(sbuf, base, sh.cand_off, np.uint32, F + 1)
+    exp_f, exp_c = [], [0]
+    for b in range(w.B):
+        lo = int(w.stage_off[b])
+        for v in range(int(w.stage_off[b + 1]) - lo):
+            g = lo + v
+            ps = w.par_idx[w.par_off[g]:w.par_off[g + 1]]
+            if w.status[g] == 0 and all(w.status[lo + p] == 1 for p in ps):
+                exp_f.append((g, b))
+                exp_c.append(exp_c[-1] + _cands(w.D, min(int(w.shard_max[g]), w.max_shard, w.D)))
+    assert [tuple(x) for x in fr.tolist()] == exp_f
+    assert co.tolist() == exp_c
+    assert int(sh.n_cand) == exp_c[-1]
+    res = _view(sbuf, base, sh.resident, np.uint64, w.B * w.D)
+    assert np.array_equal(res, w.resident.reshape(-1))
+    assert np.array_equal(_view(sbuf, base, sh.holders, np.uint64, w.N), w.holders)
+
+
+def _status(fn, w, H=None):
+    try:
+        fn(w, H)
+    except fate.FateError as e:
+        return e.status
+    return 0
+
+
+def _pack_dags(w, H=None):
+    fate.fate_layout_dags(w, H)
+
+
+def _pack_state(w, H=None):
+    _, h, _ = fate.fate_layout_dags(w, H)
+    fate.fate_layout_state(h, w)
+
+
+def test_error_codes():
+    base = synth.make_random_small(1, B=1, n=8, D=4)
+    assert _status(_pack_dags, base) == 0
+    assert _status(_pack_state, base) == 0
+    # parent id not below the child's id
+    w = dataclasses.replace(base, par_idx=base.par_idx.copy())
+    g = int(np.argmax(np.diff(w.par_off) > 0))
+    w.par_idx[w.par_off[g]] = g
+    assert _status(_pack_dags, w) == -3
+    # eligibility outside the device range
+    w = dataclasses.replace(base, elig=base.elig.copy())
+    w.elig[0] = np.uint64(1 << 5)
+    assert _status(_pack_dags, w) == -1
+    # no eligible device can hold the model
+    w = dataclasses.replace(base, elig=base.elig.copy(), cap_bytes=base.cap_bytes.copy())
+    m0 = int(w.model[0])
+    w.cap_bytes[:] = int(w.weight_bytes[m0]) - 1
+    assert _status(_pack_dags, w) == -4
+    # horizon out of range
+    assert _status(_pack_dags, base, 16) == -2
+    # negative runtime
+    w = dataclasses.replace(base, exec=base.exec.copy())
+    w.exec[0, 0] = -1.0
+    assert _status(_pack_dags, w) == -1
+    # too many devices
+    w = dataclasses.replace(base, D=65)
+    assert _status(_pack_dags, w) == -2
+    # completed stage without holders
+    w = dataclasses.replace(base, holders=base.holders.copy(), status=base.status.copy())
+    done = np.nonzero(w.status == 1)[0]
+    w.holders[done[0]] = np.uint64(0)
+    assert _status(_pack_state, w) == -6
+    # holder bit outside the device range
+    w = dataclasses.replace(base, holders=base.holders.copy())
+    w.holders[done[0]] = np.uint64(1 << 7)
+    assert _status(_pack_state, w) == -6
+    # bad status code
+    w = dataclasses.replace(base, status=base.status.copy())
+    w.status[0] = 9
+    assert _status(_pack_state, w) == -1
+    # resident model id >= M
+    w = dataclasses.replace(base, resident=base.resident.copy())
+    w.resident[0, 0] = np.uint64(1 << 20)
+    assert _status(_pack_state, w) == -1
+
+
+def test_too_small_buffer_is_rejected():
+    w = synth.make_random_small(2, B=1, n=8)
+    lib = fate.load()
+    hi = fate.HostInputs(w)
+    import ctypes as C
+    need = C.c_size_t(0)
+    assert lib.fate_pack_dags_size(C.byref(hi.cluster), C.byref(hi.batch), 2, C.byref(need)) == 0
+    buf = np.zeros(need.value, np.uint8)
+    h = fate.Dags()
+    assert lib.fate_layout_dags(C.byref(hi.cluster), C.byref(hi.batch), 2, buf.ctypes.data, need.value - 1,
+                                C.byref(h)) == -5
+    assert lib.fate_layout_dags(C.byref(hi.cluster), C.byref(hi.batch), 2, buf.ctypes.data, need.value,
+                                C.byref(h)) == 0
+
+
+def test_every_scenario_packs_on_the_host():
+    """Includes batches without any edge (no parent array at all)."""
+    import builders
+    import scenarios
+    for name, sc in scenarios.ALL.items():
+        w = builders.from_spec(sc["spec"], H=max(sc["H"], 1), params=sc["params"])
+        _, h, _ = fate.fate_layout_dags(w)
+        _, sh, _ = fate.fate_layout_state(h, w)
+        assert int(sh.n_frontier) == len(sc["front_v"]), name
+
+
+def test_all_committed_gives_empty_frontier():
+    w = synth.make_random_small(5, B=2, n=8)
+    w = dataclasses.replace(w, status=np.where(w.status == 0, 3, w.status).astype(np.uint8))
+    _, h, _ = fate.fate_layout_dags(w)
+    _, sh, _ = fate.fate_layout_state(h, w)
+    assert int(sh.n_frontier) == 0 and int(sh.n_cand) == 0
