@@ -164,6 +164,13 @@ typedef struct {
     const float *tau_free, *t_now;
     const uint32_t *frontier; /* [n_frontier][2]: flat stage id, instance */
     const uint32_t *cand_off; /* [n_frontier+1]: first score of each frontier stage */
+    int64_t n_slices;
+    const uint32_t *slices;   /* [n_slices][3]: instance, first and end frontier slot; the
+                                 scoring kernel runs one workgroup per slice */
+    int64_t n_done_edges;
+    const uint32_t *done_off; /* [N+1]: completed parents of flat stage g are
+                                 done[done_off[g] .. done_off[g+1]) */
+    const void *done;         /* 16-byte entries {uint64 holders; float out_bytes; pad} */
 } fate_state_h;
 
 const char *fate_version(void);

@@ -318,7 +318,10 @@ inline int64_t candidates_of(int r, int D) {
 struct StatePlan {
     std::vector<uint32_t> frontier;  // pairs
     std::vector<uint32_t> cand_off;
-    int64_t nF = 0, nC = 0;
+    std::vector<uint32_t> slices;    // triples
+    std::vector<uint32_t> done_off;  // [N+1]
+    std::vector<fate::DoneParent> done;
+    int64_t nF = 0, nC = 0, nS = 0;
 };
 
 fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const fate_state_t *st,
@@ -344,10 +347,13 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
         if (!std::isfinite(st->t_now[b])) return FATE_EINVAL;
     p->cand_off.clear();
     p->frontier.clear();
+    p->slices.clear();
+    const int64_t slice = fate::slice_len(D);
     int64_t nc = 0;
     for (int b = 0; b < B; ++b) {
         const int64_t base = g->stage_off[b];
         const int64_t n = g->stage_off[b + 1] - base;
+        const int64_t first = (int64_t)p->frontier.size() / 2;
         for (int64_t v = 0; v < n; ++v) {
             const int64_t s = base + v;
             const uint8_t status = st->status[s];
@@ -370,6 +376,38 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
                 if (nc >= (int64_t(1) << 32)) return FATE_ERANGE;
             }
         }
+        const int64_t last = (int64_t)p->frontier.size() / 2;
+        for (int64_t f = first; f < last; f += slice) {
+            p->slices.push_back((uint32_t)b);
+            p->slices.push_back((uint32_t)f);
+            p->slices.push_back((uint32_t)std::min(last, f + slice));
+        }
+    }
+    p->nS = (int64_t)p->slices.size() / 3;
+    // completed parents of every stage, with the state's holders and sizes
+    p->done_off.assign(N + 1, 0);
+    p->done.clear();
+    {
+        int64_t acc = 0;
+        for (int b = 0; b < B; ++b) {
+            const int64_t base = g->stage_off[b];
+            const int64_t n = g->stage_off[b + 1] - base;
+            for (int64_t v = 0; v < n; ++v) {
+                const int64_t s = base + v;
+                p->done_off[s] = (uint32_t)acc;
+                for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) {
+                    const int64_t u = base + g->par_idx[q];
+                    if (st->holders[u] == 0) continue;
+                    fate::DoneParent e;
+                    e.holders = st->holders[u];
+                    e.sigma = g->out_bytes[u];
+                    e.pad = 0;
+                    p->done.push_back(e);
+                    ++acc;
+                }
+            }
+        }
+        p->done_off[N] = (uint32_t)acc;
     }
     p->cand_off.push_back((uint32_t)nc);
     p->nF = (int64_t)p->frontier.size() / 2;
@@ -378,10 +416,10 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
 }
 
 struct StateLayout {
-    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, total;
+    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_off, done, total;
 };
 
-StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF) {
+StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS, int64_t nDone) {
     StateLayout L;
     size_t o = 0;
     L.resident = o; o = align_up(o + sizeof(uint64_t) * B * D);
@@ -391,6 +429,9 @@ StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF) {
     L.tnow = o; o = align_up(o + sizeof(float) * B);
     L.frontier = o; o = align_up(o + sizeof(uint32_t) * 2 * nF);
     L.cand_off = o; o = align_up(o + sizeof(uint32_t) * (nF + 1));
+    L.slices = o; o = align_up(o + sizeof(uint32_t) * 3 * nS);
+    L.done_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
+    L.done = o; o = align_up(o + sizeof(fate::DoneParent) * nDone);
     L.total = o;
     return L;
 }
@@ -405,6 +446,9 @@ void write_state_image(const fate_dags_t *pk, const fate_state_t *st, const Stat
     std::memcpy(img + L.tnow, st->t_now, sizeof(float) * B);
     std::memcpy(img + L.frontier, p.frontier.data(), sizeof(uint32_t) * p.frontier.size());
     std::memcpy(img + L.cand_off, p.cand_off.data(), sizeof(uint32_t) * p.cand_off.size());
+    if (!p.slices.empty()) std::memcpy(img + L.slices, p.slices.data(), sizeof(uint32_t) * p.slices.size());
+    std::memcpy(img + L.done_off, p.done_off.data(), sizeof(uint32_t) * p.done_off.size());
+    if (!p.done.empty()) std::memcpy(img + L.done, p.done.data(), sizeof(fate::DoneParent) * p.done.size());
 }
 
 void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_shard, const StatePlan &p,
@@ -426,6 +470,11 @@ void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_sh
     out->t_now = reinterpret_cast<const float *>(base + L.tnow);
     out->frontier = reinterpret_cast<const uint32_t *>(base + L.frontier);
     out->cand_off = reinterpret_cast<const uint32_t *>(base + L.cand_off);
+    out->n_slices = p.nS;
+    out->slices = reinterpret_cast<const uint32_t *>(base + L.slices);
+    out->n_done_edges = (int64_t)p.done.size();
+    out->done_off = reinterpret_cast<const uint32_t *>(base + L.done_off);
+    out->done = base + L.done;
 }
 
 fate_status_t copy_to_device(void *d_buf, const void *h, size_t bytes, void *stream) {
@@ -517,7 +566,7 @@ fate_status_t fate_pack_state_size(const fate_dags_t *packed, const fate_dag_bat
     StatePlan p;
     fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
     if (st != FATE_OK) return st;
-    *bytes = state_layout(packed->B, packed->D, state->K, packed->N, p.nF).total;
+    *bytes = state_layout(packed->B, packed->D, state->K, packed->N, p.nF, p.nS, (int64_t)p.done.size()).total;
     if (n_frontier) *n_frontier = p.nF;
     if (n_cand) *n_cand = p.nC;
     return FATE_OK;
@@ -528,7 +577,7 @@ static fate_status_t build_state(const fate_dags_t *packed, const fate_dag_batch
                                  std::vector<uint8_t> &img, StatePlan &p, StateLayout &L) {
     fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
     if (st != FATE_OK) return st;
-    L = state_layout(packed->B, packed->D, state->K, packed->N, p.nF);
+    L = state_layout(packed->B, packed->D, state->K, packed->N, p.nF, p.nS, (int64_t)p.done.size());
     if (bytes < L.total) return FATE_ESIZE;
     img.assign(L.total, 0);
     write_state_image(packed, state, p, L, img.data());
@@ -567,7 +616,8 @@ fate_status_t fate_pack_state(const fate_dags_t *packed, const fate_dag_batch_t 
 static fate_status_t check_pair(const fate_dags_t *dags, const fate_state_h *state) {
     if (!dags || !state) return FATE_EINVAL;
     if (dags->B != state->B || dags->D != state->D || dags->N != state->N) return FATE_ESTATE;
-    if (!dags->records || !state->frontier || !state->cand_off) return FATE_EINVAL;
+    if (!dags->records || !state->frontier || !state->cand_off || !state->slices || !state->done_off)
+        return FATE_EINVAL;
     return FATE_OK;
 }
 
@@ -609,14 +659,19 @@ fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *s
     a.tnow = state->t_now;
     a.frontier = state->frontier;
     a.cand_off = state->cand_off;
+    a.slices = state->slices;
+    a.done_off = state->done_off;
+    a.done = static_cast<const fate::DoneParent *>(state->done);
     a.scores = d_scores;
     a.nF = state->n_frontier;
+    a.n_slices = state->n_slices;
     a.D = dags->D;
     a.M = dags->M;
     a.K = state->K;
     a.H = params->H;
     a.max_shard = state->max_shard;
     a.beta_uniform = dags->beta_uniform;
+    a.slice = fate::slice_len(dags->D);
     a.beta0 = dags->beta0;
     a.lam_q = params->lam_q;
     a.lam_s = params->lam_s;

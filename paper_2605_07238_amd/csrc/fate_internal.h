@@ -21,6 +21,15 @@ struct alignas(16) StageRec {
 };
 static_assert(sizeof(StageRec) == 32, "stage record must be 32 bytes");
 
+// A completed parent of a stage as packed per planning step: the devices
+// holding its output and its output size.
+struct alignas(16) DoneParent {
+    uint64_t holders;
+    float sigma;
+    uint32_t pad;
+};
+static_assert(sizeof(DoneParent) == 16, "completed-parent entry must be 16 bytes");
+
 constexpr uint32_t kDescIdMask = (1u << 28) - 1u;
 constexpr int kDescDepthShift = 28;
 
@@ -42,9 +51,12 @@ struct ScoreLaunch {
     const float *tnow;
     const uint32_t *frontier;
     const uint32_t *cand_off;
+    const uint32_t *slices;
+    const uint32_t *done_off;
+    const DoneParent *done;
     float *scores;
-    int64_t nF;
-    int32_t D, M, K, H, max_shard, beta_uniform;
+    int64_t nF, n_slices;
+    int32_t D, M, K, H, max_shard, beta_uniform, slice;
     float beta0;
     float lam_q, lam_s, lam_tr, lam_c, lam_p, kpf, gamma;
 };
@@ -57,6 +69,19 @@ struct TopkLaunch {
     int64_t nF;
     int32_t D, k;
 };
+
+// Lane-group width for D devices (power of two, 4..64) and the number of
+// frontier stages per scoring workgroup slice (eight rounds of its groups).
+constexpr int kScoreBlock = 256;
+inline int group_width(int D) {
+    int g = 4;
+    while (g < D) g <<= 1;
+    return g;
+}
+inline int slice_len(int D) {
+    const int groups = kScoreBlock / group_width(D);
+    return groups * 8 > 256 ? 256 : groups * 8;
+}
 
 // Kernel launchers (fate_kernels.hip).  Return a hipError_t as int.
 int launch_score(const ScoreLaunch &a, void *stream);

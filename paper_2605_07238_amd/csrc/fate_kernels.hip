@@ -1,31 +1,35 @@
 // HIP kernels of libfate for gfx950 (CDNA4, wave64).
 //
-// k_score: one lane group of G lanes (G = next power of two >= D, 4..64) per
-// frontier stage v; lane d stands for device d.
+// k_score: one workgroup per (instance, slice of its frontier).  The
+// prologue stages the instance's state in LDS: a hash table from prefix group
+// to the devices caching it, per-model residency masks, per-device waits and
+// capacity fits, and a work-sorted order of the slice's frontier stages (most
+// horizon descendants first, so the lane groups of a wave stay balanced).
+// Each frontier stage v is then handled by one lane group of G lanes (G =
+// next power of two >= D, 4..64); lane d stands for device d.
 //   1. Lane d evaluates the immediate terms of v on device d (App. A.3):
 //      waiting, switch, transfer from completed parents, colocation, prefix
 //      reuse, and the post-state of d after loading m(v) (Load with eviction
 //      of the smallest-id other models while over capacity).
-//   2. Lane d owns the candidates j = d, d+G, d+2G, d+3G (singletons first,
-//      then contiguous windows).  For a window S of k devices the immediate
-//      cost is the maximum over S of the per-device time with runtime,
-//      transfer and prefix split k ways, plus the output gather term (the
-//      cheapest gather target in S).
+//   2. Slot 0 of lane d is the single-device candidate {d}; slots 1..3 hold
+//      contiguous windows.  A window's immediate cost is the maximum over its
+//      devices of the per-device time with runtime, transfer and prefix split
+//      k ways, plus the output gather term (cheapest gather target).
 //   3. For each horizon descendant w of v (breadth-first levels 1..H, packed
 //      by the host) lane d' computes B(d') = c_hat(w, d' | s) and the value it
 //      takes once v sits on d' (model loaded, prefix group cached, v's output
-//      local).  A group prefix/suffix minimum over B gives, for every window
-//      S, the best device outside S in O(1); the best device inside S is a
-//      minimum over at most four lanes.  min(outside, inside) is w's value
-//      under candidate S, weighted by gamma^depth and added with compensated
-//      summation.
+//      local).  Group prefix/suffix minimum scans over B (DPP row shifts for
+//      G <= 16) give the best device outside any window in O(1); the best
+//      device inside a window is a minimum over at most four lanes.
+//      min(outside, inside) is w's value under the candidate; it is weighted
+//      by gamma^depth and accumulated in fp64.
 //   This is an exact rearrangement of evaluating c_hat from scratch in the
 //   post-state: only v's own output, the model loaded for v and v's prefix
 //   group differ between s and s', and they only touch devices of S (plus
 //   the transfer of v's output to devices outside S when w is a child of v).
 //
-// k_topk: same group layout; k rounds of a group-wide maximum over 64-bit
-// keys (order-preserving score bits, then inverted candidate index).
+// k_topk: one lane group per frontier stage; k rounds of a group-wide maximum
+// over 64-bit keys (order-preserving score bits, then inverted candidate index).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -34,7 +38,7 @@
 namespace fate {
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = kScoreBlock;
 
 __device__ __forceinline__ bool bit(uint64_t m, int i) { return (m >> i) & 1ull; }
 
@@ -61,21 +65,6 @@ __device__ __forceinline__ float min_beta_into(const float *beta, uint64_t holde
     return m;
 }
 
-__device__ __forceinline__ bool cached_on(const uint64_t *slots, int K, uint64_t h) {
-    bool hit = false;
-    for (int q = 0; q < K; ++q) hit |= (slots[q] == h);
-    return hit;
-}
-
-// Candidate j of a stage -> window start i and size k (singletons first).
-__device__ __forceinline__ void decode_candidate(int j, int D, int &i, int &k) {
-    if (j < D) { i = j; k = 1; return; }
-    j -= D;
-    k = 2;
-    while (j >= D - k + 1) { j -= D - k + 1; ++k; }
-    i = j;
-}
-
 template <int G>
 __device__ __forceinline__ float group_prefix_min(float x, int lane) {
 #pragma unroll
@@ -96,181 +85,476 @@ __device__ __forceinline__ float group_suffix_min(float x, int lane) {
     return x;
 }
 
-__device__ __forceinline__ void kahan_add(float &sum, float &comp, float x) {
-    const float t = sum + x;
-    if (fabsf(sum) >= fabsf(x)) comp += (sum - t) + x;
-    else comp += (x - t) + sum;
-    sum = t;
+// ---- per-workgroup LDS layout ----------------------------------------------
+// Frontier stage of the slice, staged once per workgroup.
+struct StageL {
+    uint64_t elig, hash;
+    float tokens, sigma;
+    uint32_t v, e0, e1, dbeg;
+    uint16_t dn, npar;
+    uint8_t model, shard, pad0, pad1;
+};
+static_assert(sizeof(StageL) == 48, "StageL");
+
+// Horizon descendant staged by one lane of a group for the whole group.
+constexpr int kCap = 4;  // completed parents staged per descendant
+struct EntryL {
+    uint64_t elig, hash, pfdevs;
+    float tokens;
+    uint32_t dbeg;
+    uint16_t dn, npar;
+    uint8_t model, depth, pad0, pad1;
+    uint64_t ph[kCap];
+    float ps[kCap];
+    uint32_t pad2[2];
+};
+static_assert(sizeof(EntryL) == 96, "EntryL");
+
+struct Lds {
+    uint64_t *pkey, *pmask, *rm, *rho, *fits, *order;
+    float *wait, *exec, *ksw;
+    StageL *stages;
+    EntryL *entries;
+    int logT;
+};
+
+__host__ __device__ inline int table_log2(int D, int K) {
+    int lt = 4;
+    while ((1 << lt) < 2 * D * K) ++lt;
+    return lt;
 }
 
-// Transfer and colocation of stage x onto device d from its completed parents.
-__device__ __forceinline__ void parent_terms(const ScoreLaunch &a, const StageRec &rx, int d, float &tr, int &cnt) {
-    tr = 0.0f;
-    cnt = 0;
-    for (int q = 0; q < rx.npar; ++q) {
-        const uint32_t u = a.par_idx[rx.par_begin + q];
-        const uint64_t hu = a.holders[u];
-        if (hu == 0) continue;
-        if (bit(hu, d)) { ++cnt; continue; }
-        tr += a.rec[u].sigma * min_beta_into(a.beta, hu, d, a.D);
+__host__ __device__ inline int pow2_at_least(int x) {
+    int p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+// Byte offsets of every LDS array (shared by the launcher and the kernel).
+struct LdsPlan {
+    uint32_t pkey, pmask, rm, rho, fits, order, wait, exec, ksw, stages, entries, total;
+};
+
+__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice) {
+    LdsPlan q;
+    const uint32_t T = 1u << table_log2(D, K);
+    uint32_t o = 0;
+    q.pkey = o; o += 8 * T;
+    q.pmask = o; o += 8 * T;
+    q.rm = o; o += 8 * 64;
+    q.rho = o; o += 8 * 64;
+    q.fits = o; o += 8 * 64;
+    q.order = o; o += 8 * (uint32_t)pow2_at_least(slice);
+    q.stages = o; o += (uint32_t)sizeof(StageL) * (uint32_t)slice;
+    q.entries = o; o += (uint32_t)sizeof(EntryL) * kScoreBlock;
+    q.wait = o; o += 4 * 64;
+    q.exec = o; o += 4 * (uint32_t)(M * D);
+    q.ksw = o; o += 4 * (uint32_t)(M * D);
+    q.total = (o + 15u) & ~15u;
+    return q;
+}
+
+__device__ __forceinline__ uint32_t table_slot(uint64_t h, int logT) {
+    h ^= h >> 31;
+    h *= 0x9E3779B97F4A7C15ull;
+    return (uint32_t)(h >> (64 - logT));
+}
+
+__device__ __forceinline__ void table_insert(const Lds &L, uint64_t h, int d) {
+    const uint32_t m = (1u << L.logT) - 1u;
+    uint32_t s = table_slot(h, L.logT);
+    for (;;) {
+        const unsigned long long old = atomicCAS((unsigned long long *)&L.pkey[s], 0ull, (unsigned long long)h);
+        if (old == 0ull || old == h) {
+            atomicOr((unsigned long long *)&L.pmask[s], 1ull << d);
+            return;
+        }
+        s = (s + 1u) & m;
     }
+}
+
+// Devices whose prefix cache holds group h (0 for h == 0).  The table has
+// more slots than distinct keys, so every probe sequence reaches an empty slot.
+__device__ __forceinline__ uint64_t table_find(const Lds &L, uint64_t h) {
+    if (h == 0) return 0;
+    const uint32_t m = (1u << L.logT) - 1u;
+    uint32_t s = table_slot(h, L.logT);
+    for (;;) {
+        const uint64_t k = L.pkey[s];
+        if (k == h) return L.pmask[s];
+        if (k == 0) return 0;
+        s = (s + 1u) & m;
+    }
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float old, float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Inclusive minimum over lanes 0..lane of the group.
+template <int G>
+__device__ __forceinline__ float scan_min_up(float x, int lane) {
+    if constexpr (G <= 16) {  // groups sit inside one 16-lane DPP row
+        float y = dpp_move<0x111>(inf_f(), x);
+        if (lane >= 1) x = fminf(x, y);
+        if constexpr (G > 2) { y = dpp_move<0x112>(inf_f(), x); if (lane >= 2) x = fminf(x, y); }
+        if constexpr (G > 4) { y = dpp_move<0x114>(inf_f(), x); if (lane >= 4) x = fminf(x, y); }
+        if constexpr (G > 8) { y = dpp_move<0x118>(inf_f(), x); if (lane >= 8) x = fminf(x, y); }
+        return x;
+    } else {
+        return group_prefix_min<G>(x, lane);
+    }
+}
+
+// Inclusive minimum over lanes lane..G-1 of the group.
+template <int G>
+__device__ __forceinline__ float scan_min_down(float x, int lane) {
+    if constexpr (G <= 16) {
+        float y = dpp_move<0x101>(inf_f(), x);
+        if (lane + 1 < G) x = fminf(x, y);
+        if constexpr (G > 2) { y = dpp_move<0x102>(inf_f(), x); if (lane + 2 < G) x = fminf(x, y); }
+        if constexpr (G > 4) { y = dpp_move<0x104>(inf_f(), x); if (lane + 4 < G) x = fminf(x, y); }
+        if constexpr (G > 8) { y = dpp_move<0x108>(inf_f(), x); if (lane + 8 < G) x = fminf(x, y); }
+        return x;
+    } else {
+        return group_suffix_min<G>(x, lane);
+    }
+}
+
+// Value of lane-1 (lane 0 gets +inf) and of lane+1 (last lane gets +inf).
+template <int G>
+__device__ __forceinline__ float from_left(float x, int lane) {
+    float y;
+    if constexpr (G <= 16) y = dpp_move<0x111>(inf_f(), x);
+    else y = __shfl_up(x, 1, G);
+    return lane >= 1 ? y : inf_f();
+}
+
+template <int G>
+__device__ __forceinline__ float from_right(float x, int lane) {
+    float y;
+    if constexpr (G <= 16) y = dpp_move<0x101>(inf_f(), x);
+    else y = __shfl_down(x, 1, G);
+    return lane + 1 < G ? y : inf_f();
+}
+
+// Window t (0-based among a stage's windows) -> start i and size k >= 2.
+__device__ __forceinline__ void decode_window(int t, int D, int &i, int &k) {
+    k = 2;
+    while (t >= D - k + 1) { t -= D - k + 1; ++k; }
+    i = t;
+}
+
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// Make the group's LDS writes visible to the other lanes of the same wave.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Transfer into device d of one completed parent's output, and whether d
+// already holds it.
+__device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, float su, int d, float &tr, int &cnt) {
+    if (bit(hu, d)) { ++cnt; return; }
+    tr += su * (a.beta_uniform ? a.beta0 : min_beta_into(a.beta, hu, d, a.D));
 }
 
 template <int G>
 __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
-    constexpr int kSlots = 4;
+    extern __shared__ uint64_t smem[];
+    uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
     const int tid = threadIdx.x;
-    const int lane = tid & (G - 1);
-    const int64_t f = (int64_t)blockIdx.x * (kBlock / G) + tid / G;
-    if (f >= a.nF) return;  // uniform within the group
-    const int D = a.D;
-    const bool live = lane < D;
-    const uint32_t v = a.frontier[2 * f];
-    const uint32_t b = a.frontier[2 * f + 1];
-    const StageRec rv = a.rec[v];
-    const int mv = rv.model;
-    const int64_t sd = (int64_t)b * D + (live ? lane : 0);
+    const int D = a.D, K = a.K, M = a.M;
+    const uint32_t b = a.slices[3 * blockIdx.x];
+    const uint32_t f0 = a.slices[3 * blockIdx.x + 1];
+    const int nF = (int)(a.slices[3 * blockIdx.x + 2] - f0);
+    const int P = pow2_at_least(nF);
+    const LdsPlan plan = lds_plan(D, K, M, a.slice);
 
-    // ---- 1. per-device immediate terms and post-state of v on device lane
-    uint64_t rho = 0, rho_new = 0;
-    bool hv_cached = false, feas_v = false;
-    float a_imm = 0.0f, b_imm = 0.0f;
-    if (live) {
-        rho = a.resident[sd];
-        const float wait = fmaxf(0.0f, a.tau[sd] - a.tnow[b]);
-        if (rv.hash != 0) hv_cached = cached_on(a.pcache + sd * a.K, a.K, rv.hash);
-        feas_v = bit(rv.elig, lane) && bit(a.fits[mv], lane);
-        const float c = a.exec[mv * D + lane];
-        const float sw = bit(rho, mv) ? 0.0f : a.ksw[mv * D + lane];
-        float tr;
-        int cnt;
-        parent_terms(a, rv, lane, tr, cnt);
-        const float colo = rv.npar ? (float)cnt / (float)rv.npar : 0.0f;
-        const float pf = hv_cached ? a.kpf * rv.tokens : 0.0f;
-        a_imm = a.lam_q * wait + a.lam_s * sw - a.lam_c * colo;
-        b_imm = c + a.lam_tr * tr - a.lam_p * pf;
-        rho_new = load_model(rho, mv, a.cap[lane], a.weight);
+    Lds L;
+    L.logT = table_log2(D, K);
+    const int T = 1 << L.logT;
+    L.pkey = reinterpret_cast<uint64_t *>(sb + plan.pkey);
+    L.pmask = reinterpret_cast<uint64_t *>(sb + plan.pmask);
+    L.rm = reinterpret_cast<uint64_t *>(sb + plan.rm);
+    L.rho = reinterpret_cast<uint64_t *>(sb + plan.rho);
+    L.fits = reinterpret_cast<uint64_t *>(sb + plan.fits);
+    L.order = reinterpret_cast<uint64_t *>(sb + plan.order);
+    L.stages = reinterpret_cast<StageL *>(sb + plan.stages);
+    L.entries = reinterpret_cast<EntryL *>(sb + plan.entries);
+    L.wait = reinterpret_cast<float *>(sb + plan.wait);
+    L.exec = reinterpret_cast<float *>(sb + plan.exec);
+    L.ksw = reinterpret_cast<float *>(sb + plan.ksw);
+
+    // ---- prologue: instance tables, cluster tables, the slice's stages
+    for (int i = tid; i < T; i += kBlock) { L.pkey[i] = 0; L.pmask[i] = 0; }
+    if (tid < D) {
+        L.rho[tid] = a.resident[(int64_t)b * D + tid];
+        L.wait[tid] = fmaxf(0.0f, a.tau[(int64_t)b * D + tid] - a.tnow[b]);
     }
-    const bool prefix_added = live && rv.hash != 0 && !hv_cached;
-    const int gbase = (tid & 63) & ~(G - 1);
-    const uint64_t gmask = (G == 64) ? ~0ull : ((1ull << G) - 1ull);
-    const uint64_t feas_mask = (__ballot(feas_v) >> gbase) & gmask;
-
-    // ---- 2. candidates owned by this lane and their immediate cost
-    const uint32_t c0 = a.cand_off[f];
-    const int C = (int)(a.cand_off[f + 1] - c0);
-    const int nslots = (C + G - 1) / G;
-    int s_i[kSlots], s_k[kSlots];
-    float j0[kSlots], acc[kSlots], comp[kSlots];
-    bool ok[kSlots];
-#pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-        s_i[s] = 0; s_k[s] = 1; j0[s] = 0.0f; acc[s] = 0.0f; comp[s] = 0.0f; ok[s] = false;
-        if (s >= nslots) continue;  // uniform
-        const int j = lane + s * G;
-        int i = 0, k = 1;
-        if (j < C) decode_candidate(j, D, i, k);
-        float tmax = -inf_f();
-#pragma unroll
-        for (int q = 0; q < kSlots; ++q) {
-            const int src = min(i + q, G - 1);
-            const float aq = __shfl(a_imm, src, G);
-            const float bq = __shfl(b_imm, src, G);
-            if (q < k) tmax = fmaxf(tmax, aq + bq / (float)k);
+    if (tid < M) L.fits[tid] = a.fits[tid];
+    for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = a.ksw[i]; }
+    for (int i = tid; i < P; i += kBlock) {
+        uint64_t key = ~0ull;
+        if (i < nF) {
+            const uint32_t v = a.frontier[2 * (f0 + i)];
+            const StageRec r = a.rec[v];
+            StageL st;
+            st.elig = r.elig;
+            st.hash = r.hash;
+            st.tokens = r.tokens;
+            st.sigma = r.sigma;
+            st.v = v;
+            st.e0 = a.desc_off[v];
+            st.e1 = a.desc_off[v + 1];
+            st.dbeg = a.done_off[v];
+            st.dn = (uint16_t)(a.done_off[v + 1] - st.dbeg);
+            st.npar = r.npar;
+            st.model = r.model;
+            st.shard = r.shard;
+            st.pad0 = st.pad1 = 0;
+            L.stages[i] = st;
+            key = ((uint64_t)(0xffffffffu - (st.e1 - st.e0)) << 32) | (uint32_t)i;
         }
-        const uint64_t wmask = (k >= 64 ? ~0ull : ((1ull << k) - 1ull)) << i;
-        const bool feasible = (j < C) && ((feas_mask & wmask) == wmask);
-        float gat = 0.0f;
-        if (feasible && k > 1) {
-            gat = inf_f();
-            for (int p = i; p < i + k; ++p) {
-                float sum = 0.0f;
-                for (int d = i; d < i + k; ++d)
-                    if (d != p) sum += a.beta[d * D + p] * rv.sigma / (float)k;
-                gat = fminf(gat, sum);
-            }
-        }
-        s_i[s] = i;
-        s_k[s] = k;
-        ok[s] = feasible;
-        j0[s] = tmax + a.lam_tr * gat;
+        L.order[i] = key;
     }
-
-    // ---- 3. horizon descendants
-    const uint32_t e0 = a.desc_off[v], e1 = a.desc_off[v + 1];
-    const float t0 = a.lam_tr * rv.sigma * a.beta0;  // uniform-beta transfer of v's output
-    const uint64_t *my_slots = a.pcache + sd * a.K;
-    int cur_h = 0;
-    float gh = 1.0f;
-    for (uint32_t e = e0; e < e1; ++e) {
-        const uint32_t ent = a.desc[e];
-        const int h = (int)(ent >> kDescDepthShift);
-        if (h > a.H) break;
-        while (cur_h < h) { gh *= a.gamma; ++cur_h; }
-        const uint32_t w = ent & kDescIdMask;
-        const StageRec rw = a.rec[w];
-        const int mw = rw.model;
-        const bool child = (h == 1);
-        float Bd = inf_f(), inval = inf_f();
-        if (live && bit(rw.elig, lane) && bit(a.fits[mw], lane)) {
-            const float c = a.exec[mw * D + lane];
-            const float kswd = a.ksw[mw * D + lane];
-            const bool in_old = bit(rho, mw);
-            const bool in_new = bit(rho_new, mw);
-            float tr;
-            int cnt;
-            parent_terms(a, rw, lane, tr, cnt);
-            const float colo = rw.npar ? (float)cnt / (float)rw.npar : 0.0f;
-            const bool pfw = rw.hash != 0 && cached_on(my_slots, a.K, rw.hash);
-            const float pfv = a.kpf * rw.tokens;
-            Bd = c + a.lam_s * (in_old ? 0.0f : kswd) + a.lam_tr * tr - a.lam_c * colo - (pfw ? a.lam_p * pfv : 0.0f);
-            float dl = 0.0f;
-            if (in_new && !in_old) dl -= a.lam_s * kswd;
-            else if (!in_new && in_old) dl += a.lam_s * kswd;
-            if (prefix_added && rw.hash == rv.hash) dl -= a.lam_p * pfv;
-            if (child) dl -= a.lam_c / (float)rw.npar;
-            inval = Bd + dl;
-        }
-        const float P = group_prefix_min<G>(Bd, lane);
-        const float Q = group_suffix_min<G>(Bd, lane);
-#pragma unroll
-        for (int s = 0; s < kSlots; ++s) {
-            if (s >= nslots) continue;  // uniform
-            const int i = s_i[s], k = s_k[s];
-            const float left = __shfl(P, max(i - 1, 0), G);
-            const float right = __shfl(Q, min(i + k, G - 1), G);
-            float excl = fminf(i > 0 ? left : inf_f(), i + k < G ? right : inf_f());
-            if (child) {
-                if (a.beta_uniform) {
-                    excl += t0;
-                } else {
-                    excl = inf_f();
-                    for (int dd = 0; dd < D; ++dd) {  // uniform trip count
-                        const float bdd = __shfl(Bd, dd, G);
-                        if (dd >= i && dd < i + k) continue;
-                        float bmin = inf_f();
-                        for (int q = 0; q < k; ++q) bmin = fminf(bmin, a.beta[(i + q) * D + dd]);
-                        excl = fminf(excl, bdd + a.lam_tr * rv.sigma * bmin);
-                    }
+    __syncthreads();
+    for (int i = tid; i < D * K; i += kBlock) {
+        const uint64_t h = a.pcache[(int64_t)b * D * K + i];
+        if (h != 0) table_insert(L, h, i / K);
+    }
+    if (tid < M) {
+        uint64_t m = 0;
+        for (int d = 0; d < D; ++d)
+            if (bit(L.rho[d], tid)) m |= 1ull << d;
+        L.rm[tid] = m;
+    }
+    for (int k = 2; k <= P; k <<= 1)  // bitonic sort, ascending keys: most work first
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < P; i += kBlock) {
+                const int ixj = i ^ j;
+                if (ixj > i) {
+                    const uint64_t x = L.order[i], y = L.order[ixj];
+                    if ((x > y) == ((i & k) == 0)) { L.order[i] = y; L.order[ixj] = x; }
                 }
             }
-            float inside = inf_f();
-#pragma unroll
-            for (int q = 0; q < kSlots; ++q) {
-                const float x = __shfl(inval, min(i + q, G - 1), G);
-                if (q < k) inside = fminf(inside, x);
-            }
-            if (ok[s]) kahan_add(acc[s], comp[s], gh * fminf(excl, inside));
+            __syncthreads();
         }
-    }
+    __syncthreads();
 
-    // ---- 4. emit
+    constexpr int kGroups = kBlock / G;
+    const int lane = tid & (G - 1);
+    const bool live = lane < D;
+    const int gbase = (tid & 63) & ~(G - 1);
+    const uint64_t gmask = (G >= 64) ? ~0ull : ((1ull << (G & 63)) - 1ull);
+    const uint64_t rho = live ? L.rho[lane] : 0;
+    EntryL *area = L.entries + (tid & ~(G - 1));  // this group's G staging slots
+
+    for (int pos = tid / G; pos < nF; pos += kGroups) {  // uniform within the group
+        const int si = (int)(L.order[pos] & 0xffffffffu);
+        const StageL sv = L.stages[si];
+        const int64_t f = f0 + si;
+        const int mv = sv.model;
+        const bool hv_cached = bit(table_find(L, sv.hash), lane);
+
+        // ---- immediate terms of v on device `lane` and the post-state there
+        float a_imm = 0.0f, b_imm = 0.0f;
+        uint64_t rho_new = 0;
+        const bool feas_v = live && bit(sv.elig, lane) && bit(L.fits[mv], lane);
+        {
+            float tr = 0.0f;
+            int cnt = 0;
+            for (int q = 0; q < sv.dn; ++q) {  // uniform trip count
+                const DoneParent pu = a.done[sv.dbeg + q];
+                if (live) add_parent(a, pu.holders, pu.sigma, lane, tr, cnt);
+            }
+            if (live) {
+                const float c = L.exec[mv * D + lane];
+                const float sw = bit(L.rm[mv], lane) ? 0.0f : L.ksw[mv * D + lane];
+                const float colo = sv.npar ? (float)cnt / (float)sv.npar : 0.0f;
+                const float pf = hv_cached ? a.kpf * sv.tokens : 0.0f;
+                a_imm = a.lam_q * L.wait[lane] + a.lam_s * sw - a.lam_c * colo;
+                b_imm = c + a.lam_tr * tr - a.lam_p * pf;
+                rho_new = load_model(rho, mv, a.cap[lane], a.weight);
+            }
+        }
+        const bool prefix_added = live && sv.hash != 0 && !hv_cached;
+        const uint64_t feas_mask = (__ballot(feas_v) >> gbase) & gmask;
+
+        // ---- candidates: slot 0 = single device `lane`; slots 1..3 = windows
+        const uint32_t c0 = a.cand_off[f];
+        const int nwin = (int)(a.cand_off[f + 1] - c0) - D;
+        const int wslots = (nwin + G - 1) / G;
+        const float j0_single = a_imm + b_imm;
+        double acc0 = 0.0;
+        int w_i[3], w_k[3];
+        float w_j0[3];
+        bool w_ok[3];
+        double w_acc[3];
 #pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-        if (s >= nslots) continue;
-        const int j = lane + s * G;
-        if (j >= C) continue;
-        a.scores[c0 + j] = ok[s] ? -(j0[s] + (acc[s] + comp[s])) : -inf_f();
+        for (int s = 0; s < 3; ++s) {
+            w_i[s] = 0; w_k[s] = 2; w_j0[s] = 0.0f; w_ok[s] = false; w_acc[s] = 0.0;
+            if (s >= wslots) continue;  // uniform
+            const int t = lane + s * G;
+            int i = 0, k = 2;
+            if (t < nwin) decode_window(t, D, i, k);
+            float tmax = -inf_f();
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int src = min(i + q, G - 1);
+                const float aq = __shfl(a_imm, src, G);
+                const float bq = __shfl(b_imm, src, G);
+                if (q < k) tmax = fmaxf(tmax, aq + bq / (float)k);
+            }
+            const uint64_t wm = ((1ull << k) - 1ull) << i;
+            const bool feasible = (t < nwin) && ((feas_mask & wm) == wm);
+            float gat = inf_f();
+            if (feasible) {
+                for (int p = i; p < i + k; ++p) {
+                    float sum = 0.0f;
+                    for (int d = i; d < i + k; ++d)
+                        if (d != p) sum += a.beta[d * D + p] * sv.sigma / (float)k;
+                    gat = fminf(gat, sum);
+                }
+            }
+            w_i[s] = i;
+            w_k[s] = k;
+            w_ok[s] = feasible;
+            w_j0[s] = tmax + a.lam_tr * gat;
+        }
+
+        // ---- horizon descendants, G at a time: lane j stages entry j in LDS
+        const float t0 = a.lam_tr * sv.sigma * a.beta0;
+        int cur_h = 0;
+        float gh = 1.0f;
+        for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
+            {
+                const uint32_t e = base + lane;
+                bool valid = e < sv.e1;
+                uint32_t ent = 0;
+                if (valid) {
+                    ent = a.desc[e];
+                    valid = (int)(ent >> kDescDepthShift) <= a.H;
+                }
+                if (valid) {
+                    const uint32_t w = ent & kDescIdMask;
+                    const StageRec rw = a.rec[w];
+                    const uint32_t db = a.done_off[w];
+                    const uint32_t dn = a.done_off[w + 1] - db;
+                    EntryL &E = area[lane];
+                    E.elig = rw.elig;
+                    E.hash = rw.hash;
+                    E.pfdevs = table_find(L, rw.hash);
+                    E.tokens = rw.tokens;
+                    E.dbeg = db;
+                    E.dn = (uint16_t)dn;
+                    E.npar = rw.npar;
+                    E.model = rw.model;
+                    E.depth = (uint8_t)(ent >> kDescDepthShift);
+                    for (uint32_t q = 0; q < dn && q < (uint32_t)kCap; ++q) {
+                        const DoneParent pu = a.done[db + q];
+                        E.ph[q] = pu.holders;
+                        E.ps[q] = pu.sigma;
+                    }
+                }
+                const int nb = __popcll((__ballot(valid) >> gbase) & gmask);  // valid entries form a prefix
+                wave_sync();
+                for (int jj = 0; jj < nb; ++jj) {  // uniform
+                    const EntryL &E = area[jj];
+                    const int h = E.depth;
+                    while (cur_h < h) { gh *= a.gamma; ++cur_h; }
+                    const int mw = E.model;
+                    const bool child = (h == 1);
+                    float tr = 0.0f;
+                    int cnt = 0;
+                    for (int q = 0; q < E.dn; ++q) {  // uniform trip count
+                        uint64_t hu;
+                        float su;
+                        if (q < kCap) { hu = E.ph[q]; su = E.ps[q]; }
+                        else { const DoneParent pu = a.done[E.dbeg + q]; hu = pu.holders; su = pu.sigma; }
+                        if (live) add_parent(a, hu, su, lane, tr, cnt);
+                    }
+                    float Bd = inf_f(), inval = inf_f();
+                    if (live && bit(E.elig, lane) && bit(L.fits[mw], lane)) {
+                        const float c = L.exec[mw * D + lane];
+                        const float kswd = L.ksw[mw * D + lane];
+                        const bool in_old = bit(L.rm[mw], lane);
+                        const bool in_new = bit(rho_new, mw);
+                        const float inv_np = E.npar ? fast_rcp((float)E.npar) : 0.0f;
+                        const float pfv = a.kpf * E.tokens;
+                        Bd = c + a.lam_s * (in_old ? 0.0f : kswd) + a.lam_tr * tr - a.lam_c * ((float)cnt * inv_np) -
+                             (bit(E.pfdevs, lane) ? a.lam_p * pfv : 0.0f);
+                        float dl = 0.0f;
+                        if (in_new && !in_old) dl -= a.lam_s * kswd;
+                        else if (!in_new && in_old) dl += a.lam_s * kswd;
+                        if (prefix_added && E.hash == sv.hash) dl -= a.lam_p * pfv;
+                        if (child) dl -= a.lam_c * inv_np;
+                        inval = Bd + dl;
+                    }
+                    const float Pm = scan_min_up<G>(Bd, lane);
+                    const float Qm = scan_min_down<G>(Bd, lane);
+                    {  // single device `lane`
+                        float excl = fminf(from_left<G>(Pm, lane), from_right<G>(Qm, lane));
+                        if (child) {
+                            if (a.beta_uniform) {
+                                excl += t0;
+                            } else {
+                                excl = inf_f();
+                                for (int dd = 0; dd < D; ++dd) {  // uniform trip count
+                                    const float bdd = __shfl(Bd, dd, G);
+                                    if (dd != lane && live)
+                                        excl = fminf(excl, bdd + a.lam_tr * sv.sigma * a.beta[lane * D + dd]);
+                                }
+                            }
+                        }
+                        if (feas_v) acc0 += (double)(gh * fminf(excl, inval));
+                    }
+#pragma unroll
+                    for (int s = 0; s < 3; ++s) {  // windows
+                        if (s >= wslots) continue;  // uniform
+                        const int i = w_i[s], k = w_k[s];
+                        const float left = __shfl(Pm, max(i - 1, 0), G);
+                        const float right = __shfl(Qm, min(i + k, G - 1), G);
+                        float excl = fminf(i > 0 ? left : inf_f(), i + k < G ? right : inf_f());
+                        if (child) {
+                            if (a.beta_uniform) {
+                                excl += t0;
+                            } else {
+                                excl = inf_f();
+                                for (int dd = 0; dd < D; ++dd) {  // uniform trip count
+                                    const float bdd = __shfl(Bd, dd, G);
+                                    if (dd >= i && dd < i + k) continue;
+                                    float bmin = inf_f();
+                                    for (int q = 0; q < k; ++q) bmin = fminf(bmin, a.beta[(i + q) * D + dd]);
+                                    excl = fminf(excl, bdd + a.lam_tr * sv.sigma * bmin);
+                                }
+                            }
+                        }
+                        float inside = inf_f();
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const float x = __shfl(inval, min(i + q, G - 1), G);
+                            if (q < k) inside = fminf(inside, x);
+                        }
+                        if (w_ok[s]) w_acc[s] += (double)(gh * fminf(excl, inside));
+                    }
+                }
+                wave_sync();  // the next batch overwrites the staging slots
+                if (nb < G) break;  // past the horizon depth or the list end
+            }
+        }
+
+        // ---- emit
+        if (live) a.scores[c0 + lane] = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
+#pragma unroll
+        for (int s = 0; s < 3; ++s) {
+            if (s >= wslots) continue;
+            const int t = lane + s * G;
+            if (t < nwin) a.scores[c0 + D + t] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
+        }
     }
 }
 
@@ -327,25 +611,19 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
     }
 }
 
-int group_width(int D) {
-    int g = 4;
-    while (g < D) g <<= 1;
-    return g;
-}
-
 }  // namespace
 
 int launch_score(const ScoreLaunch &a, void *stream) {
     const int G = group_width(a.D);
-    const int64_t groups = kBlock / G;
-    const int64_t blocks = (a.nF + groups - 1) / groups;
+    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice).total;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const dim3 grid((unsigned)a.n_slices), block(kBlock);
     switch (G) {
-        case 4: hipLaunchKernelGGL(k_score<4>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        case 8: hipLaunchKernelGGL(k_score<8>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        case 16: hipLaunchKernelGGL(k_score<16>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        case 32: hipLaunchKernelGGL(k_score<32>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        default: hipLaunchKernelGGL(k_score<64>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_score<4>, grid, block, lds, s, a); break;
+        case 8: hipLaunchKernelGGL(k_score<8>, grid, block, lds, s, a); break;
+        case 16: hipLaunchKernelGGL(k_score<16>, grid, block, lds, s, a); break;
+        case 32: hipLaunchKernelGGL(k_score<32>, grid, block, lds, s, a); break;
+        default: hipLaunchKernelGGL(k_score<64>, grid, block, lds, s, a); break;
     }
     return (int)hipGetLastError();
 }

@@ -76,7 +76,9 @@ class StateH(C.Structure):
                 ("base", C.c_void_p), ("bytes", C.c_size_t),
                 ("resident", C.c_void_p), ("prefix_cache", C.c_void_p), ("holders", C.c_void_p),
                 ("tau_free", C.c_void_p), ("t_now", C.c_void_p),
-                ("frontier", C.c_void_p), ("cand_off", C.c_void_p)]
+                ("frontier", C.c_void_p), ("cand_off", C.c_void_p),
+                ("n_slices", C.c_int64), ("slices", C.c_void_p),
+                ("n_done_edges", C.c_int64), ("done_off", C.c_void_p), ("done", C.c_void_p)]
 
 
 _lib = None
