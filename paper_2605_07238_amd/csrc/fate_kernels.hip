@@ -33,6 +33,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "fate_internal.h"
 
 namespace fate {
@@ -96,23 +98,34 @@ struct StageL {
 };
 static_assert(sizeof(StageL) == 48, "StageL");
 
-// Horizon descendant staged by one lane of a group for the whole group.
-constexpr int kCap = 4;  // completed parents staged per descendant
+// Horizon descendant staged by one lane of a group for the whole group, with
+// the per-descendant values every device lane needs precomputed.  For a
+// uniform transfer coefficient the completed parents are folded into a base
+// transfer term (every parent remote) and, per staged parent, the amount a
+// device holding that parent's output saves (its transfer plus the
+// colocation benefit).
+constexpr int kCap = 3;  // completed parents staged per descendant
 struct EntryL {
-    uint64_t elig, hash, pfdevs;
-    float tokens;
-    uint32_t dbeg;
-    uint16_t dn, npar;
-    uint8_t model, depth, pad0, pad1;
-    uint64_t ph[kCap];
-    float ps[kCap];
-    uint32_t pad2[2];
+    uint64_t feas;     // devices feasible for w: eligible and able to hold its model
+    uint64_t pfdevs;   // devices whose prefix cache holds grp(w)
+    uint64_t ph[kCap]; // holder masks of the first completed parents
+    float gh;          // gamma^depth
+    float base_tr;     // lam_tr * beta0 * sum of completed parents' sizes (uniform beta)
+    float pfp;         // lam_p * kappa_prefix * L(w)
+    float cw;          // lam_c / |Pa(w)|
+    uint32_t moff;     // m(w) * D
+    uint8_t model;
+    uint8_t flags;     // bit 0: child of v; bit 1: same prefix group as v
+    uint16_t dn;       // completed parents
+    uint32_t dbeg;     // first completed parent
+    float pw[kCap];    // uniform beta: lam_tr*beta0*sigma_u + cw; otherwise sigma_u
 };
-static_assert(sizeof(EntryL) == 96, "EntryL");
+static_assert(sizeof(EntryL) == 80, "EntryL");
 
 struct Lds {
-    uint64_t *pkey, *pmask, *rm, *rho, *fits, *order;
-    float *wait, *exec, *ksw;
+    uint64_t *pkey, *pmask, *rm, *rho, *fits, *keys;
+    uint8_t *order;
+    float *wait, *exec, *ksw, *gpow;
     StageL *stages;
     EntryL *entries;
     int logT;
@@ -132,7 +145,7 @@ __host__ __device__ inline int pow2_at_least(int x) {
 
 // Byte offsets of every LDS array (shared by the launcher and the kernel).
 struct LdsPlan {
-    uint32_t pkey, pmask, rm, rho, fits, order, wait, exec, ksw, stages, entries, total;
+    uint32_t pkey, pmask, rm, rho, fits, order, wait, gpow, exec, ksw, stages, entries, total;
 };
 
 __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice) {
@@ -144,10 +157,11 @@ __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice) {
     q.rm = o; o += 8 * 64;
     q.rho = o; o += 8 * 64;
     q.fits = o; o += 8 * 64;
-    q.order = o; o += 8 * (uint32_t)pow2_at_least(slice);
     q.stages = o; o += (uint32_t)sizeof(StageL) * (uint32_t)slice;
-    q.entries = o; o += (uint32_t)sizeof(EntryL) * kScoreBlock;
+    q.entries = o; o += (uint32_t)sizeof(EntryL) * kScoreBlock;  // also holds the prologue's sort keys
+    q.order = o; o += ((uint32_t)slice + 15u) & ~15u;
     q.wait = o; o += 4 * 64;
+    q.gpow = o; o += 4 * 16;
     q.exec = o; o += 4 * (uint32_t)(M * D);
     q.ksw = o; o += 4 * (uint32_t)(M * D);
     q.total = (o + 15u) & ~15u;
@@ -195,7 +209,13 @@ __device__ __forceinline__ float dpp_move(float old, float x) {
 // Inclusive minimum over lanes 0..lane of the group.
 template <int G>
 __device__ __forceinline__ float scan_min_up(float x, int lane) {
-    if constexpr (G <= 16) {  // groups sit inside one 16-lane DPP row
+    if constexpr (G == 16) {  // the group is one DPP row; lanes without a source keep x
+        x = fminf(x, dpp_move<0x111>(x, x));
+        x = fminf(x, dpp_move<0x112>(x, x));
+        x = fminf(x, dpp_move<0x114>(x, x));
+        x = fminf(x, dpp_move<0x118>(x, x));
+        return x;
+    } else if constexpr (G < 16) {  // groups sit inside one 16-lane DPP row
         float y = dpp_move<0x111>(inf_f(), x);
         if (lane >= 1) x = fminf(x, y);
         if constexpr (G > 2) { y = dpp_move<0x112>(inf_f(), x); if (lane >= 2) x = fminf(x, y); }
@@ -210,7 +230,13 @@ __device__ __forceinline__ float scan_min_up(float x, int lane) {
 // Inclusive minimum over lanes lane..G-1 of the group.
 template <int G>
 __device__ __forceinline__ float scan_min_down(float x, int lane) {
-    if constexpr (G <= 16) {
+    if constexpr (G == 16) {
+        x = fminf(x, dpp_move<0x101>(x, x));
+        x = fminf(x, dpp_move<0x102>(x, x));
+        x = fminf(x, dpp_move<0x104>(x, x));
+        x = fminf(x, dpp_move<0x108>(x, x));
+        return x;
+    } else if constexpr (G < 16) {
         float y = dpp_move<0x101>(inf_f(), x);
         if (lane + 1 < G) x = fminf(x, y);
         if constexpr (G > 2) { y = dpp_move<0x102>(inf_f(), x); if (lane + 2 < G) x = fminf(x, y); }
@@ -225,16 +251,18 @@ __device__ __forceinline__ float scan_min_down(float x, int lane) {
 // Value of lane-1 (lane 0 gets +inf) and of lane+1 (last lane gets +inf).
 template <int G>
 __device__ __forceinline__ float from_left(float x, int lane) {
+    if constexpr (G == 16) return dpp_move<0x111>(inf_f(), x);
     float y;
-    if constexpr (G <= 16) y = dpp_move<0x111>(inf_f(), x);
+    if constexpr (G < 16) y = dpp_move<0x111>(inf_f(), x);
     else y = __shfl_up(x, 1, G);
     return lane >= 1 ? y : inf_f();
 }
 
 template <int G>
 __device__ __forceinline__ float from_right(float x, int lane) {
+    if constexpr (G == 16) return dpp_move<0x101>(inf_f(), x);
     float y;
-    if constexpr (G <= 16) y = dpp_move<0x101>(inf_f(), x);
+    if constexpr (G < 16) y = dpp_move<0x101>(inf_f(), x);
     else y = __shfl_down(x, 1, G);
     return lane + 1 < G ? y : inf_f();
 }
@@ -255,14 +283,17 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Transfer into device d of one completed parent's output, and whether d
-// already holds it.
-__device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, float su, int d, float &tr, int &cnt) {
-    if (bit(hu, d)) { ++cnt; return; }
-    tr += su * (a.beta_uniform ? a.beta0 : min_beta_into(a.beta, hu, d, a.D));
+// One completed parent's contribution on device d: its output is local
+// (colocation count) or has to be transferred from the cheapest holder.
+template <bool UNI>
+__device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, float su, int d, float &tr, float &cnt) {
+    const bool local = bit(hu, d);
+    const float bm = UNI ? a.beta0 : min_beta_into(a.beta, hu, d, a.D);
+    cnt += local ? 1.0f : 0.0f;
+    tr += local ? 0.0f : su * bm;
 }
 
-template <int G>
+template <int G, bool UNI>
 __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     extern __shared__ uint64_t smem[];
     uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
@@ -282,12 +313,14 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     L.rm = reinterpret_cast<uint64_t *>(sb + plan.rm);
     L.rho = reinterpret_cast<uint64_t *>(sb + plan.rho);
     L.fits = reinterpret_cast<uint64_t *>(sb + plan.fits);
-    L.order = reinterpret_cast<uint64_t *>(sb + plan.order);
+    L.order = sb + plan.order;
+    L.keys = reinterpret_cast<uint64_t *>(sb + plan.entries);
     L.stages = reinterpret_cast<StageL *>(sb + plan.stages);
     L.entries = reinterpret_cast<EntryL *>(sb + plan.entries);
     L.wait = reinterpret_cast<float *>(sb + plan.wait);
     L.exec = reinterpret_cast<float *>(sb + plan.exec);
     L.ksw = reinterpret_cast<float *>(sb + plan.ksw);
+    L.gpow = reinterpret_cast<float *>(sb + plan.gpow);
 
     // ---- prologue: instance tables, cluster tables, the slice's stages
     for (int i = tid; i < T; i += kBlock) { L.pkey[i] = 0; L.pmask[i] = 0; }
@@ -296,6 +329,10 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         L.wait[tid] = fmaxf(0.0f, a.tau[(int64_t)b * D + tid] - a.tnow[b]);
     }
     if (tid < M) L.fits[tid] = a.fits[tid];
+    if (tid == 0) {
+        float g = 1.0f;
+        for (int h = 0; h < 16; ++h) { L.gpow[h] = g; g *= a.gamma; }
+    }
     for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = a.ksw[i]; }
     for (int i = tid; i < P; i += kBlock) {
         uint64_t key = ~0ull;
@@ -319,7 +356,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             L.stages[i] = st;
             key = ((uint64_t)(0xffffffffu - (st.e1 - st.e0)) << 32) | (uint32_t)i;
         }
-        L.order[i] = key;
+        L.keys[i] = key;
     }
     __syncthreads();
     for (int i = tid; i < D * K; i += kBlock) {
@@ -337,51 +374,52 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             for (int i = tid; i < P; i += kBlock) {
                 const int ixj = i ^ j;
                 if (ixj > i) {
-                    const uint64_t x = L.order[i], y = L.order[ixj];
-                    if ((x > y) == ((i & k) == 0)) { L.order[i] = y; L.order[ixj] = x; }
+                    const uint64_t x = L.keys[i], y = L.keys[ixj];
+                    if ((x > y) == ((i & k) == 0)) { L.keys[i] = y; L.keys[ixj] = x; }
                 }
             }
             __syncthreads();
         }
     __syncthreads();
+    for (int i = tid; i < nF; i += kBlock) L.order[i] = (uint8_t)(L.keys[i] & 0xffu);
+    __syncthreads();  // the sort keys' space becomes staging slots
 
     constexpr int kGroups = kBlock / G;
     const int lane = tid & (G - 1);
     const bool live = lane < D;
+    const int dl = live ? lane : D - 1;  // clamped device index for table reads
     const int gbase = (tid & 63) & ~(G - 1);
     const uint64_t gmask = (G >= 64) ? ~0ull : ((1ull << (G & 63)) - 1ull);
-    const uint64_t rho = live ? L.rho[lane] : 0;
+    const uint64_t rho = L.rho[dl];
+    using Mask = typename std::conditional<(G <= 32), uint32_t, uint64_t>::type;  // device bitmask
+    const Mask mybit = live ? (Mask(1) << lane) : Mask(0);
+    const float *exec_col = L.exec + dl;
+    const float *ksw_col = L.ksw + dl;
     EntryL *area = L.entries + (tid & ~(G - 1));  // this group's G staging slots
+    const float lam_s = a.lam_s, lam_tr = a.lam_tr, lam_c = a.lam_c, lam_p = a.lam_p;
 
     for (int pos = tid / G; pos < nF; pos += kGroups) {  // uniform within the group
-        const int si = (int)(L.order[pos] & 0xffffffffu);
+        const int si = (int)L.order[pos];
         const StageL sv = L.stages[si];
         const int64_t f = f0 + si;
         const int mv = sv.model;
         const bool hv_cached = bit(table_find(L, sv.hash), lane);
 
         // ---- immediate terms of v on device `lane` and the post-state there
-        float a_imm = 0.0f, b_imm = 0.0f;
-        uint64_t rho_new = 0;
-        const bool feas_v = live && bit(sv.elig, lane) && bit(L.fits[mv], lane);
-        {
-            float tr = 0.0f;
-            int cnt = 0;
-            for (int q = 0; q < sv.dn; ++q) {  // uniform trip count
-                const DoneParent pu = a.done[sv.dbeg + q];
-                if (live) add_parent(a, pu.holders, pu.sigma, lane, tr, cnt);
-            }
-            if (live) {
-                const float c = L.exec[mv * D + lane];
-                const float sw = bit(L.rm[mv], lane) ? 0.0f : L.ksw[mv * D + lane];
-                const float colo = sv.npar ? (float)cnt / (float)sv.npar : 0.0f;
-                const float pf = hv_cached ? a.kpf * sv.tokens : 0.0f;
-                a_imm = a.lam_q * L.wait[lane] + a.lam_s * sw - a.lam_c * colo;
-                b_imm = c + a.lam_tr * tr - a.lam_p * pf;
-                rho_new = load_model(rho, mv, a.cap[lane], a.weight);
-            }
+        float tr = 0.0f, cnt = 0.0f;
+        for (int q = 0; q < sv.dn; ++q) {  // uniform trip count
+            const DoneParent pu = a.done[sv.dbeg + q];
+            add_parent<UNI>(a, pu.holders, pu.sigma, dl, tr, cnt);
         }
-        const bool prefix_added = live && sv.hash != 0 && !hv_cached;
+        const bool feas_v = live && bit(sv.elig, lane) && bit(L.fits[mv], lane);
+        const float c_v = L.exec[mv * D + dl];
+        const float sw_v = bit(rho, mv) ? 0.0f : L.ksw[mv * D + dl];
+        const float colo_v = sv.npar ? cnt / (float)sv.npar : 0.0f;
+        const float pf_v = hv_cached ? a.kpf * sv.tokens : 0.0f;
+        const float a_imm = a.lam_q * L.wait[dl] + lam_s * sw_v - lam_c * colo_v;
+        const float b_imm = c_v + lam_tr * tr - lam_p * pf_v;
+        const uint64_t rho_new = load_model(rho, mv, a.cap[dl], a.weight);
+        const bool prefix_added = sv.hash != 0 && !hv_cached;
         const uint64_t feas_mask = (__ballot(feas_v) >> gbase) & gmask;
 
         // ---- candidates: slot 0 = single device `lane`; slots 1..3 = windows
@@ -423,128 +461,135 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             w_i[s] = i;
             w_k[s] = k;
             w_ok[s] = feasible;
-            w_j0[s] = tmax + a.lam_tr * gat;
+            w_j0[s] = tmax + lam_tr * gat;
         }
 
         // ---- horizon descendants, G at a time: lane j stages entry j in LDS
-        const float t0 = a.lam_tr * sv.sigma * a.beta0;
-        int cur_h = 0;
-        float gh = 1.0f;
+        const float t0 = lam_tr * sv.sigma * a.beta0;
         for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
-            {
-                const uint32_t e = base + lane;
-                bool valid = e < sv.e1;
-                uint32_t ent = 0;
-                if (valid) {
-                    ent = a.desc[e];
-                    valid = (int)(ent >> kDescDepthShift) <= a.H;
-                }
-                if (valid) {
-                    const uint32_t w = ent & kDescIdMask;
-                    const StageRec rw = a.rec[w];
-                    const uint32_t db = a.done_off[w];
-                    const uint32_t dn = a.done_off[w + 1] - db;
-                    EntryL &E = area[lane];
-                    E.elig = rw.elig;
-                    E.hash = rw.hash;
-                    E.pfdevs = table_find(L, rw.hash);
-                    E.tokens = rw.tokens;
-                    E.dbeg = db;
-                    E.dn = (uint16_t)dn;
-                    E.npar = rw.npar;
-                    E.model = rw.model;
-                    E.depth = (uint8_t)(ent >> kDescDepthShift);
-                    for (uint32_t q = 0; q < dn && q < (uint32_t)kCap; ++q) {
-                        const DoneParent pu = a.done[db + q];
-                        E.ph[q] = pu.holders;
-                        E.ps[q] = pu.sigma;
-                    }
-                }
-                const int nb = __popcll((__ballot(valid) >> gbase) & gmask);  // valid entries form a prefix
-                wave_sync();
-                for (int jj = 0; jj < nb; ++jj) {  // uniform
-                    const EntryL &E = area[jj];
-                    const int h = E.depth;
-                    while (cur_h < h) { gh *= a.gamma; ++cur_h; }
-                    const int mw = E.model;
-                    const bool child = (h == 1);
-                    float tr = 0.0f;
-                    int cnt = 0;
-                    for (int q = 0; q < E.dn; ++q) {  // uniform trip count
-                        uint64_t hu;
-                        float su;
-                        if (q < kCap) { hu = E.ph[q]; su = E.ps[q]; }
-                        else { const DoneParent pu = a.done[E.dbeg + q]; hu = pu.holders; su = pu.sigma; }
-                        if (live) add_parent(a, hu, su, lane, tr, cnt);
-                    }
-                    float Bd = inf_f(), inval = inf_f();
-                    if (live && bit(E.elig, lane) && bit(L.fits[mw], lane)) {
-                        const float c = L.exec[mw * D + lane];
-                        const float kswd = L.ksw[mw * D + lane];
-                        const bool in_old = bit(L.rm[mw], lane);
-                        const bool in_new = bit(rho_new, mw);
-                        const float inv_np = E.npar ? fast_rcp((float)E.npar) : 0.0f;
-                        const float pfv = a.kpf * E.tokens;
-                        Bd = c + a.lam_s * (in_old ? 0.0f : kswd) + a.lam_tr * tr - a.lam_c * ((float)cnt * inv_np) -
-                             (bit(E.pfdevs, lane) ? a.lam_p * pfv : 0.0f);
-                        float dl = 0.0f;
-                        if (in_new && !in_old) dl -= a.lam_s * kswd;
-                        else if (!in_new && in_old) dl += a.lam_s * kswd;
-                        if (prefix_added && E.hash == sv.hash) dl -= a.lam_p * pfv;
-                        if (child) dl -= a.lam_c * inv_np;
-                        inval = Bd + dl;
-                    }
-                    const float Pm = scan_min_up<G>(Bd, lane);
-                    const float Qm = scan_min_down<G>(Bd, lane);
-                    {  // single device `lane`
-                        float excl = fminf(from_left<G>(Pm, lane), from_right<G>(Qm, lane));
-                        if (child) {
-                            if (a.beta_uniform) {
-                                excl += t0;
-                            } else {
-                                excl = inf_f();
-                                for (int dd = 0; dd < D; ++dd) {  // uniform trip count
-                                    const float bdd = __shfl(Bd, dd, G);
-                                    if (dd != lane && live)
-                                        excl = fminf(excl, bdd + a.lam_tr * sv.sigma * a.beta[lane * D + dd]);
-                                }
-                            }
-                        }
-                        if (feas_v) acc0 += (double)(gh * fminf(excl, inval));
-                    }
-#pragma unroll
-                    for (int s = 0; s < 3; ++s) {  // windows
-                        if (s >= wslots) continue;  // uniform
-                        const int i = w_i[s], k = w_k[s];
-                        const float left = __shfl(Pm, max(i - 1, 0), G);
-                        const float right = __shfl(Qm, min(i + k, G - 1), G);
-                        float excl = fminf(i > 0 ? left : inf_f(), i + k < G ? right : inf_f());
-                        if (child) {
-                            if (a.beta_uniform) {
-                                excl += t0;
-                            } else {
-                                excl = inf_f();
-                                for (int dd = 0; dd < D; ++dd) {  // uniform trip count
-                                    const float bdd = __shfl(Bd, dd, G);
-                                    if (dd >= i && dd < i + k) continue;
-                                    float bmin = inf_f();
-                                    for (int q = 0; q < k; ++q) bmin = fminf(bmin, a.beta[(i + q) * D + dd]);
-                                    excl = fminf(excl, bdd + a.lam_tr * sv.sigma * bmin);
-                                }
-                            }
-                        }
-                        float inside = inf_f();
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const float x = __shfl(inval, min(i + q, G - 1), G);
-                            if (q < k) inside = fminf(inside, x);
-                        }
-                        if (w_ok[s]) w_acc[s] += (double)(gh * fminf(excl, inside));
-                    }
-                }
-                wave_sync();  // the next batch overwrites the staging slots
-                if (nb < G) break;  // past the horizon depth or the list end
+            const uint32_t e = base + lane;
+            bool valid = e < sv.e1;
+            uint32_t ent = 0;
+            if (valid) {
+                ent = a.desc[e];
+                valid = (int)(ent >> kDescDepthShift) <= a.H;
             }
+            if (valid) {
+                const uint32_t w = ent & kDescIdMask;
+                const int depth = (int)(ent >> kDescDepthShift);
+                const StageRec rw = a.rec[w];
+                const uint32_t db = a.done_off[w];
+                const uint32_t dn = a.done_off[w + 1] - db;
+                EntryL &E = area[lane];
+                E.feas = rw.elig & L.fits[rw.model];
+                E.pfdevs = table_find(L, rw.hash);
+                E.gh = L.gpow[depth];
+                const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
+                E.cw = cw;
+                E.pfp = lam_p * a.kpf * rw.tokens;
+                E.moff = (uint32_t)rw.model * (uint32_t)D;
+                E.model = rw.model;
+                E.flags = (uint8_t)((depth == 1 ? 1 : 0) | (rw.hash != 0 && rw.hash == sv.hash ? 2 : 0));
+                E.dn = (uint16_t)dn;
+                E.dbeg = db;
+                float base_tr = 0.0f;
+                for (uint32_t q = 0; q < dn; ++q) {
+                    const DoneParent pu = a.done[db + q];
+                    const float t = lam_tr * a.beta0 * pu.sigma;
+                    if (UNI) base_tr += t;
+                    if (q < (uint32_t)kCap) {
+                        E.ph[q] = pu.holders;
+                        E.pw[q] = UNI ? t + cw : pu.sigma;
+                    }
+                }
+                E.base_tr = base_tr;
+            }
+            const int nb = __popcll((__ballot(valid) >> gbase) & gmask);  // valid entries form a prefix
+            wave_sync();
+            for (int jj = 0; jj < nb; ++jj) {  // uniform
+                const EntryL &E = area[jj];
+                const Mask feas = (Mask)E.feas, pfd = (Mask)E.pfdevs;
+                const float gh = E.gh, pfp = E.pfp, cw = E.cw;
+                const int mw = E.model, dn = E.dn, flags = E.flags;
+                const bool child = (flags & 1) != 0;
+                float X = exec_col[E.moff] + E.base_tr;
+                const int ns = dn < kCap ? dn : kCap;
+                if (UNI) {
+                    for (int q = 0; q < ns; ++q)  // uniform trip count
+                        X -= ((Mask)E.ph[q] & mybit) != 0 ? E.pw[q] : 0.0f;
+                    for (int q = kCap; q < dn; ++q) {  // rare: more completed parents than staged
+                        const DoneParent pu = a.done[E.dbeg + q];
+                        X -= ((Mask)pu.holders & mybit) != 0 ? lam_tr * a.beta0 * pu.sigma + cw : 0.0f;
+                    }
+                } else {
+                    float trw = 0.0f, cntw = 0.0f;
+                    for (int q = 0; q < ns; ++q) add_parent<false>(a, E.ph[q], E.pw[q], dl, trw, cntw);
+                    for (int q = kCap; q < dn; ++q) {
+                        const DoneParent pu = a.done[E.dbeg + q];
+                        add_parent<false>(a, pu.holders, pu.sigma, dl, trw, cntw);
+                    }
+                    X += lam_tr * trw - cntw * cw;
+                }
+                const float sw = lam_s * ksw_col[E.moff];
+                const bool in_old = ((rho >> mw) & 1ull) != 0;
+                const bool in_new = ((rho_new >> mw) & 1ull) != 0;
+                const bool pf_old = (pfd & mybit) != 0;
+                const bool pf_new = pf_old || ((flags & 2) && prefix_added);
+                const float Braw = X + (in_old ? 0.0f : sw) - (pf_old ? pfp : 0.0f);
+                const float Bnew = X + (in_new ? 0.0f : sw) - (pf_new ? pfp : 0.0f) - (child ? cw : 0.0f);
+                const bool fw = (feas & mybit) != 0;
+                const float Bd = fw ? Braw : inf_f();
+                const float inval = fw ? Bnew : inf_f();
+                const float Pm = scan_min_up<G>(Bd, lane);
+                const float Qm = scan_min_down<G>(Bd, lane);
+                {  // single device `lane`
+                    float excl = fminf(from_left<G>(Pm, lane), from_right<G>(Qm, lane));
+                    if (UNI) {
+                        excl += child ? t0 : 0.0f;
+                    } else if (child) {
+                        {
+                            excl = inf_f();
+                            for (int dd = 0; dd < D; ++dd) {  // uniform trip count
+                                const float bdd = __shfl(Bd, dd, G);
+                                if (dd != lane)
+                                    excl = fminf(excl, bdd + lam_tr * sv.sigma * a.beta[dl * D + dd]);
+                            }
+                        }
+                    }
+                    acc0 += (double)(gh * fminf(excl, inval));
+                }
+#pragma unroll
+                for (int s = 0; s < 3; ++s) {  // windows
+                    if (s >= wslots) continue;  // uniform
+                    const int i = w_i[s], k = w_k[s];
+                    const float left = __shfl(Pm, max(i - 1, 0), G);
+                    const float right = __shfl(Qm, min(i + k, G - 1), G);
+                    float excl = fminf(i > 0 ? left : inf_f(), i + k < G ? right : inf_f());
+                    if (child) {
+                        if (UNI) {
+                            excl += t0;
+                        } else {
+                            excl = inf_f();
+                            for (int dd = 0; dd < D; ++dd) {  // uniform trip count
+                                const float bdd = __shfl(Bd, dd, G);
+                                if (dd >= i && dd < i + k) continue;
+                                float bmin = inf_f();
+                                for (int q = 0; q < k; ++q) bmin = fminf(bmin, a.beta[(i + q) * D + dd]);
+                                excl = fminf(excl, bdd + lam_tr * sv.sigma * bmin);
+                            }
+                        }
+                    }
+                    float inside = inf_f();
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float x = __shfl(inval, min(i + q, G - 1), G);
+                        if (q < k) inside = fminf(inside, x);
+                    }
+                    w_acc[s] += (double)(gh * fminf(excl, inside));
+                }
+            }
+            wave_sync();  // the next batch overwrites the staging slots
+            if (nb < G) break;  // past the horizon depth or the list end
         }
 
         // ---- emit
@@ -613,18 +658,24 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
 
 }  // namespace
 
-int launch_score(const ScoreLaunch &a, void *stream) {
+template <bool UNI>
+static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int G = group_width(a.D);
     const size_t lds = lds_plan(a.D, a.K, a.M, a.slice).total;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const dim3 grid((unsigned)a.n_slices), block(kBlock);
     switch (G) {
-        case 4: hipLaunchKernelGGL(k_score<4>, grid, block, lds, s, a); break;
-        case 8: hipLaunchKernelGGL(k_score<8>, grid, block, lds, s, a); break;
-        case 16: hipLaunchKernelGGL(k_score<16>, grid, block, lds, s, a); break;
-        case 32: hipLaunchKernelGGL(k_score<32>, grid, block, lds, s, a); break;
-        default: hipLaunchKernelGGL(k_score<64>, grid, block, lds, s, a); break;
+        case 4: hipLaunchKernelGGL((k_score<4, UNI>), grid, block, lds, s, a); break;
+        case 8: hipLaunchKernelGGL((k_score<8, UNI>), grid, block, lds, s, a); break;
+        case 16: hipLaunchKernelGGL((k_score<16, UNI>), grid, block, lds, s, a); break;
+        case 32: hipLaunchKernelGGL((k_score<32, UNI>), grid, block, lds, s, a); break;
+        default: hipLaunchKernelGGL((k_score<64, UNI>), grid, block, lds, s, a); break;
     }
+}
+
+int launch_score(const ScoreLaunch &a, void *stream) {
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (a.beta_uniform) launch_score_g<true>(a, s);
+    else launch_score_g<false>(a, s);
     return (int)hipGetLastError();
 }
 

@@ -148,6 +148,16 @@ def test_error_codes():
     w = dataclasses.replace(base, exec=base.exec.copy())
     w.exec[0, 0] = -1.0
     assert _status(_pack_dags, w) == -1
+    # NaN inputs are rejected (host validation is compiled with NaN semantics)
+    w = dataclasses.replace(base, exec=base.exec.copy())
+    w.exec[0, 1] = np.nan
+    assert _status(_pack_dags, w) == -1
+    w = dataclasses.replace(base, out_bytes=base.out_bytes.copy())
+    w.out_bytes[2] = np.nan
+    assert _status(_pack_dags, w) == -1
+    w = dataclasses.replace(base, tau_free=base.tau_free.copy())
+    w.tau_free[0, 0] = np.inf
+    assert _status(_pack_state, w) == -1
     # too many devices
     w = dataclasses.replace(base, D=65)
     assert _status(_pack_dags, w) == -2
