@@ -248,6 +248,27 @@ __device__ __forceinline__ float scan_min_down(float x, int lane) {
     }
 }
 
+// Prefix and suffix minima of two independent rows, steps interleaved so the
+// four dependency chains overlap.
+template <int G>
+__device__ __forceinline__ void scan_min_pair(float &p0, float &q0, float &p1, float &q1, int lane) {
+    if constexpr (G == 16) {
+        p0 = fminf(p0, dpp_move<0x111>(p0, p0)); q0 = fminf(q0, dpp_move<0x101>(q0, q0));
+        p1 = fminf(p1, dpp_move<0x111>(p1, p1)); q1 = fminf(q1, dpp_move<0x101>(q1, q1));
+        p0 = fminf(p0, dpp_move<0x112>(p0, p0)); q0 = fminf(q0, dpp_move<0x102>(q0, q0));
+        p1 = fminf(p1, dpp_move<0x112>(p1, p1)); q1 = fminf(q1, dpp_move<0x102>(q1, q1));
+        p0 = fminf(p0, dpp_move<0x114>(p0, p0)); q0 = fminf(q0, dpp_move<0x104>(q0, q0));
+        p1 = fminf(p1, dpp_move<0x114>(p1, p1)); q1 = fminf(q1, dpp_move<0x104>(q1, q1));
+        p0 = fminf(p0, dpp_move<0x118>(p0, p0)); q0 = fminf(q0, dpp_move<0x108>(q0, q0));
+        p1 = fminf(p1, dpp_move<0x118>(p1, p1)); q1 = fminf(q1, dpp_move<0x108>(q1, q1));
+    } else {
+        p0 = scan_min_up<G>(p0, lane);
+        q0 = scan_min_down<G>(q0, lane);
+        p1 = scan_min_up<G>(p1, lane);
+        q1 = scan_min_down<G>(q1, lane);
+    }
+}
+
 // Value of lane-1 (lane 0 gets +inf) and of lane+1 (last lane gets +inf).
 template <int G>
 __device__ __forceinline__ float from_left(float x, int lane) {
@@ -506,8 +527,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             }
             const int nb = __popcll((__ballot(valid) >> gbase) & gmask);  // valid entries form a prefix
             wave_sync();
-            for (int jj = 0; jj < nb; ++jj) {  // uniform
-                const EntryL &E = area[jj];
+            // Row of descendant E: B(d') = c_hat(w, d' | s) and its value once v
+            // sits on d' (both +inf where w is infeasible).
+            auto entry_row = [&](const EntryL &E, float &Bd_out, float &inval_out, float &gh_out, bool &child_out) {
                 const Mask feas = (Mask)E.feas, pfd = (Mask)E.pfdevs;
                 const float gh = E.gh, pfp = E.pfp, cw = E.cw;
                 const int mw = E.model, dn = E.dn, flags = E.flags;
@@ -540,6 +562,30 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 const bool fw = (feas & mybit) != 0;
                 const float Bd = fw ? Braw : inf_f();
                 const float inval = fw ? Bnew : inf_f();
+                Bd_out = Bd;
+                inval_out = inval;
+                gh_out = gh;
+                child_out = child;
+            };
+            int jj = 0;
+            if (UNI && wslots == 0) {  // singletons only: two descendants per iteration
+                for (; jj + 1 < nb; jj += 2) {
+                    float B0, N0, g0, B1, N1, g1;
+                    bool c0c, c1c;
+                    entry_row(area[jj], B0, N0, g0, c0c);
+                    entry_row(area[jj + 1], B1, N1, g1, c1c);
+                    float p0 = B0, q0 = B0, p1 = B1, q1 = B1;
+                    scan_min_pair<G>(p0, q0, p1, q1, lane);
+                    const float e0 = fminf(from_left<G>(p0, lane), from_right<G>(q0, lane)) + (c0c ? t0 : 0.0f);
+                    const float e1 = fminf(from_left<G>(p1, lane), from_right<G>(q1, lane)) + (c1c ? t0 : 0.0f);
+                    acc0 += (double)(g0 * fminf(e0, N0));
+                    acc0 += (double)(g1 * fminf(e1, N1));
+                }
+            }
+            for (; jj < nb; ++jj) {  // uniform
+                float Bd, inval, gh;
+                bool child;
+                entry_row(area[jj], Bd, inval, gh, child);
                 const float Pm = scan_min_up<G>(Bd, lane);
                 const float Qm = scan_min_down<G>(Bd, lane);
                 {  // single device `lane`
