@@ -88,15 +88,17 @@ __device__ __forceinline__ float group_suffix_min(float x, int lane) {
 }
 
 // ---- per-workgroup LDS layout ----------------------------------------------
-// Frontier stage of the slice, staged once per workgroup.
+// Frontier stage of the slice, staged once per workgroup with its candidate
+// offsets.
 struct StageL {
     uint64_t elig, hash;
     float tokens, sigma;
     uint32_t v, e0, e1, dbeg;
+    uint32_t c0, nc;      // first score and number of candidates
     uint16_t dn, npar;
     uint8_t model, shard, pad0, pad1;
 };
-static_assert(sizeof(StageL) == 48, "StageL");
+static_assert(sizeof(StageL) == 56, "StageL");
 
 // Horizon descendant staged by one lane of a group for the whole group, with
 // the per-descendant values every device lane needs precomputed.  For a
@@ -105,10 +107,11 @@ static_assert(sizeof(StageL) == 48, "StageL");
 // device holding that parent's output saves (its transfer plus the
 // colocation benefit).
 constexpr int kCap = 3;  // completed parents staged per descendant
+template <class Mask>
 struct EntryL {
-    uint64_t feas;     // devices feasible for w: eligible and able to hold its model
-    uint64_t pfdevs;   // devices whose prefix cache holds grp(w)
-    uint64_t ph[kCap]; // holder masks of the first completed parents
+    Mask feas;         // devices feasible for w: eligible and able to hold its model
+    Mask pfdevs;       // devices whose prefix cache holds grp(w)
+    Mask ph[kCap];     // holder masks of the first completed parents
     float gh;          // gamma^depth
     float base_tr;     // lam_tr * beta0 * sum of completed parents' sizes (uniform beta)
     float pfp;         // lam_p * kappa_prefix * L(w)
@@ -120,14 +123,19 @@ struct EntryL {
     uint32_t dbeg;     // first completed parent
     float pw[kCap];    // uniform beta: lam_tr*beta0*sigma_u + cw; otherwise sigma_u
 };
-static_assert(sizeof(EntryL) == 80, "EntryL");
+static_assert(sizeof(EntryL<uint32_t>) == 60, "EntryL<u32>");
+static_assert(sizeof(EntryL<uint64_t>) == 80, "EntryL<u64>");
+
+template <int G>
+using MaskFor = typename std::conditional<(G <= 32), uint32_t, uint64_t>::type;
 
 struct Lds {
-    uint64_t *pkey, *pmask, *rm, *rho, *fits, *keys;
+    uint64_t *pkey, *rm, *rho, *fits, *wt, *cap, *keys;
+    void *pmask;  // device masks of the prefix table: uint32_t when D <= 32, else uint64_t
     uint8_t *order;
     float *wait, *exec, *ksw, *gpow;
     StageL *stages;
-    EntryL *entries;
+    void *entries;
     int logT;
 };
 
@@ -145,22 +153,28 @@ __host__ __device__ inline int pow2_at_least(int x) {
 
 // Byte offsets of every LDS array (shared by the launcher and the kernel).
 struct LdsPlan {
-    uint32_t pkey, pmask, rm, rho, fits, order, wait, gpow, exec, ksw, stages, entries, total;
+    uint32_t pkey, pmask, rm, rho, fits, wt, cap, order, wait, gpow, exec, ksw, stages, entries, total;
 };
 
-__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice) {
+__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int entry_bytes) {
     LdsPlan q;
     const uint32_t T = 1u << table_log2(D, K);
+    const uint32_t mask_bytes = D <= 32 ? 4u : 8u;
     uint32_t o = 0;
     q.pkey = o; o += 8 * T;
-    q.pmask = o; o += 8 * T;
-    q.rm = o; o += 8 * 64;
-    q.rho = o; o += 8 * 64;
-    q.fits = o; o += 8 * 64;
+    q.pmask = o; o += mask_bytes * T;
+    o = (o + 7u) & ~7u;
+    q.rm = o; o += 8 * (uint32_t)M;
+    q.rho = o; o += 8 * (uint32_t)D;
+    q.fits = o; o += 8 * (uint32_t)M;
+    q.wt = o; o += 8 * (uint32_t)M;
+    q.cap = o; o += 8 * (uint32_t)D;
+    o = (o + 15u) & ~15u;
     q.stages = o; o += (uint32_t)sizeof(StageL) * (uint32_t)slice;
-    q.entries = o; o += (uint32_t)sizeof(EntryL) * kScoreBlock;  // also holds the prologue's sort keys
+    q.entries = o; o += (uint32_t)entry_bytes * kScoreBlock;  // also holds the prologue's sort keys
+    o = (o + 15u) & ~15u;
     q.order = o; o += ((uint32_t)slice + 15u) & ~15u;
-    q.wait = o; o += 4 * 64;
+    q.wait = o; o += 4 * (uint32_t)D;
     q.gpow = o; o += 4 * 16;
     q.exec = o; o += 4 * (uint32_t)(M * D);
     q.ksw = o; o += 4 * (uint32_t)(M * D);
@@ -174,13 +188,15 @@ __device__ __forceinline__ uint32_t table_slot(uint64_t h, int logT) {
     return (uint32_t)(h >> (64 - logT));
 }
 
+template <class Mask>
 __device__ __forceinline__ void table_insert(const Lds &L, uint64_t h, int d) {
     const uint32_t m = (1u << L.logT) - 1u;
     uint32_t s = table_slot(h, L.logT);
+    Mask *pm = static_cast<Mask *>(L.pmask);
     for (;;) {
         const unsigned long long old = atomicCAS((unsigned long long *)&L.pkey[s], 0ull, (unsigned long long)h);
         if (old == 0ull || old == h) {
-            atomicOr((unsigned long long *)&L.pmask[s], 1ull << d);
+            atomicOr(&pm[s], (Mask)((Mask)1 << d));
             return;
         }
         s = (s + 1u) & m;
@@ -189,13 +205,15 @@ __device__ __forceinline__ void table_insert(const Lds &L, uint64_t h, int d) {
 
 // Devices whose prefix cache holds group h (0 for h == 0).  The table has
 // more slots than distinct keys, so every probe sequence reaches an empty slot.
-__device__ __forceinline__ uint64_t table_find(const Lds &L, uint64_t h) {
+template <class Mask>
+__device__ __forceinline__ Mask table_find(const Lds &L, uint64_t h) {
     if (h == 0) return 0;
     const uint32_t m = (1u << L.logT) - 1u;
     uint32_t s = table_slot(h, L.logT);
+    const Mask *pm = static_cast<const Mask *>(L.pmask);
     for (;;) {
         const uint64_t k = L.pkey[s];
-        if (k == h) return L.pmask[s];
+        if (k == h) return pm[s];
         if (k == 0) return 0;
         s = (s + 1u) & m;
     }
@@ -324,32 +342,37 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     const uint32_t f0 = a.slices[3 * blockIdx.x + 1];
     const int nF = (int)(a.slices[3 * blockIdx.x + 2] - f0);
     const int P = pow2_at_least(nF);
-    const LdsPlan plan = lds_plan(D, K, M, a.slice);
+    using Mask = MaskFor<G>;  // device bitmask
+    using Entry = EntryL<Mask>;
+    const LdsPlan plan = lds_plan(D, K, M, a.slice, (int)sizeof(Entry));
 
     Lds L;
     L.logT = table_log2(D, K);
     const int T = 1 << L.logT;
     L.pkey = reinterpret_cast<uint64_t *>(sb + plan.pkey);
-    L.pmask = reinterpret_cast<uint64_t *>(sb + plan.pmask);
+    L.pmask = sb + plan.pmask;
     L.rm = reinterpret_cast<uint64_t *>(sb + plan.rm);
     L.rho = reinterpret_cast<uint64_t *>(sb + plan.rho);
     L.fits = reinterpret_cast<uint64_t *>(sb + plan.fits);
     L.order = sb + plan.order;
     L.keys = reinterpret_cast<uint64_t *>(sb + plan.entries);
     L.stages = reinterpret_cast<StageL *>(sb + plan.stages);
-    L.entries = reinterpret_cast<EntryL *>(sb + plan.entries);
+    L.entries = sb + plan.entries;
+    L.wt = reinterpret_cast<uint64_t *>(sb + plan.wt);
+    L.cap = reinterpret_cast<uint64_t *>(sb + plan.cap);
     L.wait = reinterpret_cast<float *>(sb + plan.wait);
     L.exec = reinterpret_cast<float *>(sb + plan.exec);
     L.ksw = reinterpret_cast<float *>(sb + plan.ksw);
     L.gpow = reinterpret_cast<float *>(sb + plan.gpow);
 
     // ---- prologue: instance tables, cluster tables, the slice's stages
-    for (int i = tid; i < T; i += kBlock) { L.pkey[i] = 0; L.pmask[i] = 0; }
+    for (int i = tid; i < T; i += kBlock) { L.pkey[i] = 0; static_cast<Mask *>(L.pmask)[i] = 0; }
     if (tid < D) {
         L.rho[tid] = a.resident[(int64_t)b * D + tid];
         L.wait[tid] = fmaxf(0.0f, a.tau[(int64_t)b * D + tid] - a.tnow[b]);
+        L.cap[tid] = a.cap[tid];
     }
-    if (tid < M) L.fits[tid] = a.fits[tid];
+    if (tid < M) { L.fits[tid] = a.fits[tid]; L.wt[tid] = a.weight[tid]; }
     if (tid == 0) {
         float g = 1.0f;
         for (int h = 0; h < 16; ++h) { L.gpow[h] = g; g *= a.gamma; }
@@ -370,6 +393,8 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             st.e1 = a.desc_off[v + 1];
             st.dbeg = a.done_off[v];
             st.dn = (uint16_t)(a.done_off[v + 1] - st.dbeg);
+            st.c0 = a.cand_off[f0 + i];
+            st.nc = a.cand_off[f0 + i + 1] - st.c0;
             st.npar = r.npar;
             st.model = r.model;
             st.shard = r.shard;
@@ -382,7 +407,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     __syncthreads();
     for (int i = tid; i < D * K; i += kBlock) {
         const uint64_t h = a.pcache[(int64_t)b * D * K + i];
-        if (h != 0) table_insert(L, h, i / K);
+        if (h != 0) table_insert<Mask>(L, h, i / K);
     }
     if (tid < M) {
         uint64_t m = 0;
@@ -412,19 +437,17 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     const int gbase = (tid & 63) & ~(G - 1);
     const uint64_t gmask = (G >= 64) ? ~0ull : ((1ull << (G & 63)) - 1ull);
     const uint64_t rho = L.rho[dl];
-    using Mask = typename std::conditional<(G <= 32), uint32_t, uint64_t>::type;  // device bitmask
     const Mask mybit = live ? (Mask(1) << lane) : Mask(0);
     const float *exec_col = L.exec + dl;
     const float *ksw_col = L.ksw + dl;
-    EntryL *area = L.entries + (tid & ~(G - 1));  // this group's G staging slots
+    Entry *area = reinterpret_cast<Entry *>(L.entries) + (tid & ~(G - 1));  // this group's G staging slots
     const float lam_s = a.lam_s, lam_tr = a.lam_tr, lam_c = a.lam_c, lam_p = a.lam_p;
 
     for (int pos = tid / G; pos < nF; pos += kGroups) {  // uniform within the group
         const int si = (int)L.order[pos];
         const StageL sv = L.stages[si];
-        const int64_t f = f0 + si;
         const int mv = sv.model;
-        const bool hv_cached = bit(table_find(L, sv.hash), lane);
+        const bool hv_cached = bit((uint64_t)table_find<Mask>(L, sv.hash), lane);
 
         // ---- immediate terms of v on device `lane` and the post-state there
         float tr = 0.0f, cnt = 0.0f;
@@ -439,13 +462,13 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         const float pf_v = hv_cached ? a.kpf * sv.tokens : 0.0f;
         const float a_imm = a.lam_q * L.wait[dl] + lam_s * sw_v - lam_c * colo_v;
         const float b_imm = c_v + lam_tr * tr - lam_p * pf_v;
-        const uint64_t rho_new = load_model(rho, mv, a.cap[dl], a.weight);
+        const uint64_t rho_new = load_model(rho, mv, L.cap[dl], L.wt);
         const bool prefix_added = sv.hash != 0 && !hv_cached;
         const uint64_t feas_mask = (__ballot(feas_v) >> gbase) & gmask;
 
         // ---- candidates: slot 0 = single device `lane`; slots 1..3 = windows
-        const uint32_t c0 = a.cand_off[f];
-        const int nwin = (int)(a.cand_off[f + 1] - c0) - D;
+        const uint32_t c0 = sv.c0;
+        const int nwin = (int)sv.nc - D;
         const int wslots = (nwin + G - 1) / G;
         const float j0_single = a_imm + b_imm;
         double acc0 = 0.0;
@@ -501,9 +524,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 const StageRec rw = a.rec[w];
                 const uint32_t db = a.done_off[w];
                 const uint32_t dn = a.done_off[w + 1] - db;
-                EntryL &E = area[lane];
-                E.feas = rw.elig & L.fits[rw.model];
-                E.pfdevs = table_find(L, rw.hash);
+                Entry &E = area[lane];
+                E.feas = (Mask)(rw.elig & L.fits[rw.model]);
+                E.pfdevs = table_find<Mask>(L, rw.hash);
                 E.gh = L.gpow[depth];
                 const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
                 E.cw = cw;
@@ -519,7 +542,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     const float t = lam_tr * a.beta0 * pu.sigma;
                     if (UNI) base_tr += t;
                     if (q < (uint32_t)kCap) {
-                        E.ph[q] = pu.holders;
+                        E.ph[q] = (Mask)pu.holders;
                         E.pw[q] = UNI ? t + cw : pu.sigma;
                     }
                 }
@@ -529,7 +552,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             wave_sync();
             // Row of descendant E: B(d') = c_hat(w, d' | s) and its value once v
             // sits on d' (both +inf where w is infeasible).
-            auto entry_row = [&](const EntryL &E, float &Bd_out, float &inval_out, float &gh_out, bool &child_out) {
+            auto entry_row = [&](const Entry &E, float &Bd_out, float &inval_out, float &gh_out, bool &child_out) {
                 const Mask feas = (Mask)E.feas, pfd = (Mask)E.pfdevs;
                 const float gh = E.gh, pfp = E.pfp, cw = E.cw;
                 const int mw = E.model, dn = E.dn, flags = E.flags;
@@ -707,7 +730,8 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
 template <bool UNI>
 static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int G = group_width(a.D);
-    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice).total;
+    const int entry_bytes = G <= 32 ? (int)sizeof(EntryL<uint32_t>) : (int)sizeof(EntryL<uint64_t>);
+    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, entry_bytes).total;
     const dim3 grid((unsigned)a.n_slices), block(kBlock);
     switch (G) {
         case 4: hipLaunchKernelGGL((k_score<4, UNI>), grid, block, lds, s, a); break;
