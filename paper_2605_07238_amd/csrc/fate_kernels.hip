@@ -404,8 +404,19 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         }
         L.keys[i] = key;
     }
+    // prefix-cache entries are fetched before the barrier and inserted after it
+    constexpr int kPre = 4;
+    uint64_t pre[kPre];
+#pragma unroll
+    for (int r = 0; r < kPre; ++r) {
+        const int i = tid + r * kBlock;
+        pre[r] = i < D * K ? a.pcache[(int64_t)b * D * K + i] : 0ull;
+    }
     __syncthreads();
-    for (int i = tid; i < D * K; i += kBlock) {
+#pragma unroll
+    for (int r = 0; r < kPre; ++r)
+        if (pre[r] != 0) table_insert<Mask>(L, pre[r], (tid + r * kBlock) / K);
+    for (int i = tid + kPre * kBlock; i < D * K; i += kBlock) {  // D*K > 1024 only
         const uint64_t h = a.pcache[(int64_t)b * D * K + i];
         if (h != 0) table_insert<Mask>(L, h, i / K);
     }
@@ -415,19 +426,14 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             if (bit(L.rho[d], tid)) m |= 1ull << d;
         L.rm[tid] = m;
     }
-    for (int k = 2; k <= P; k <<= 1)  // bitonic sort, ascending keys: most work first
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < P; i += kBlock) {
-                const int ixj = i ^ j;
-                if (ixj > i) {
-                    const uint64_t x = L.keys[i], y = L.keys[ixj];
-                    if ((x > y) == ((i & k) == 0)) { L.keys[i] = y; L.keys[ixj] = x; }
-                }
-            }
-            __syncthreads();
-        }
-    __syncthreads();
-    for (int i = tid; i < nF; i += kBlock) L.order[i] = (uint8_t)(L.keys[i] & 0xffu);
+    // work order: stage i goes to position = number of keys smaller than its
+    // own (keys are distinct), so the most descendants come first
+    for (int i = tid; i < nF; i += kBlock) {
+        const uint64_t ki = L.keys[i];
+        int rank = 0;
+        for (int j = 0; j < nF; ++j) rank += L.keys[j] < ki ? 1 : 0;
+        L.order[rank] = (uint8_t)i;
+    }
     __syncthreads();  // the sort keys' space becomes staging slots
 
     constexpr int kGroups = kBlock / G;
