@@ -2,17 +2,17 @@
 """Benchmark of horizon-aware candidate scoring on one MI355X.
 
 One step = one pass of the scoring path over the whole batch with the packed
-DAGs and state already resident in HBM: fate_score_frontier (every candidate
-of every frontier stage, immediate cost plus the depth-H horizon) followed by
-fate_topk.  Packing (host validation, layout and the host-to-device copy) is
+DAGs and state already resident in HBM: fate_score_topk, which scores every
+candidate of every frontier stage (immediate cost plus the depth-H horizon)
+and writes each stage's top-k in the same kernel.  Packing (host validation, layout and the host-to-device copy) is
 done once before timing and reported separately.
 
 Prints one JSON line (rank 0, N=1):
   value          candidate-horizon evaluations per second over the timed steps;
                  one evaluation per feasible candidate and per (feasible
                  candidate, horizon descendant) pair
-  roofline       the score kernel's algorithmic bytes per launch / its average
-                 launch time (HIP events on the launch stream) vs 8 TB/s HBM
+  roofline       the kernel's algorithmic bytes per launch / its average launch
+                 time (HIP events on the launch stream) vs 8 TB/s HBM
   cpu_baseline   the fp64 oracle timed on this host's cores over the same batch
 """
 
@@ -165,8 +165,7 @@ def main():
     val = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.float32, device="cuda")
 
     def step():
-        fate.fate_score_frontier(pk, st, params, out=scores)
-        fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
+        fate.fate_score_topk(pk, st, params, args.topk, out=scores, idx=idx, val=val)
 
     for _ in range(args.warmup):
         step()
@@ -174,22 +173,18 @@ def main():
     log("warmup done (%d steps)" % args.warmup)
 
     K = args.steps
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(K):
         ev[i][0].record()
-        fate.fate_score_frontier(pk, st, params, out=scores)
+        step()
         ev[i][1].record()
-        fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
-        ev[i][2].record()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     ms_step = (t_end - t_start) * 1e3 / K
-    score_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
-    topk_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
-    log("timed %d steps: %.4f ms/step (score %.4f ms, topk %.4f ms)" % (K, ms_step, score_ms, topk_ms))
+    score_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    log("timed %d steps: %.4f ms/step (fused score + top-k kernel %.4f ms)" % (K, ms_step, score_ms))
 
     if args.copy_calibration:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -200,6 +195,8 @@ def main():
 
     scores_host = scores[:st.n_cand].cpu().numpy()
     n_eval, alg_bytes, parts, counts = counted_work(w, pk, st, scores_host, H)
+    parts["topk"] = 8 * args.topk * counts["F"]
+    alg_bytes += parts["topk"]
     achieved = alg_bytes / (score_ms * 1e-3) / 1e9
     traffic = read_traffic(args.workload)
     out = {
@@ -219,7 +216,7 @@ def main():
             "workload": args.workload, "B": w.B, "stages_per_dag": int(np.diff(w.stage_off).max()),
             "D": w.D, "M": w.M, "K": w.K, "H": H, "max_shard": w.max_shard, "topk": args.topk,
             "frontier_stages": counts["F"], "candidates": counts["C"], "horizon_entries": counts["desc_entries"],
-            "evals_per_step": n_eval, "score_kernel_ms": score_ms, "topk_kernel_ms": topk_ms,
+            "evals_per_step": n_eval, "score_topk_kernel_ms": score_ms,
             "pack_dags_s": t_pack_dags, "pack_state_s": t_pack_state,
             "algorithmic_bytes_per_launch": alg_bytes, "algorithmic_bytes_parts": parts,
         },

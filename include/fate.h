@@ -241,6 +241,14 @@ fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *s
                                   const fate_params_t *params, float *d_scores, int64_t n_scores,
                                   void *d_ws, size_t ws_bytes, void *stream);
 
+/* fate_score_topk: fate_score_frontier and fate_topk in one launch.  Writes
+ * the same scores to d_scores and the same per-stage top-k to d_idx / d_val
+ * ([n_frontier * k]) as the two calls in sequence would.
+ * Errors: those of fate_score_frontier, plus ERANGE (k outside 1..64). */
+fate_status_t fate_score_topk(const fate_dags_t *dags, const fate_state_h *state, const fate_params_t *params,
+                              float *d_scores, int64_t n_scores, int32_t k, int32_t *d_idx, float *d_val,
+                              void *d_ws, size_t ws_bytes, void *stream);
+
 /* fate_topk: per frontier stage, the k (1..64) best candidates by
  * (score descending, candidate index ascending), skipping -infinity, padded
  * with (-1, -infinity).  d_idx/d_val: device arrays [n_frontier * k] of

@@ -629,11 +629,9 @@ fate_status_t fate_score_ws_size(const fate_dags_t *dags, const fate_state_h *st
     return FATE_OK;
 }
 
-fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *state,
-                                  const fate_params_t *params, float *d_scores, int64_t n_scores,
-                                  void *d_ws, size_t ws_bytes, void *stream) {
-    (void)d_ws;
-    (void)ws_bytes;
+static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *state, const fate_params_t *params,
+                                float *d_scores, int64_t n_scores, int32_t k, int32_t *d_idx, float *d_val,
+                                void *stream) {
     fate_status_t st = check_pair(dags, state);
     if (st != FATE_OK) return st;
     if (!params || !params_ok(params)) return FATE_EINVAL;
@@ -663,6 +661,9 @@ fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *s
     a.done_off = state->done_off;
     a.done = static_cast<const fate::DoneParent *>(state->done);
     a.scores = d_scores;
+    a.topk = k;
+    a.tk_idx = d_idx;
+    a.tk_val = d_val;
     a.nF = state->n_frontier;
     a.n_slices = state->n_slices;
     a.D = dags->D;
@@ -681,6 +682,24 @@ fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *s
     a.kpf = params->kappa_prefix;
     a.gamma = params->gamma;
     return fate::launch_score(a, stream) == 0 ? FATE_OK : FATE_EHIP;
+}
+
+fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *state,
+                                  const fate_params_t *params, float *d_scores, int64_t n_scores,
+                                  void *d_ws, size_t ws_bytes, void *stream) {
+    (void)d_ws;
+    (void)ws_bytes;
+    return score_impl(dags, state, params, d_scores, n_scores, 0, nullptr, nullptr, stream);
+}
+
+fate_status_t fate_score_topk(const fate_dags_t *dags, const fate_state_h *state, const fate_params_t *params,
+                              float *d_scores, int64_t n_scores, int32_t k, int32_t *d_idx, float *d_val,
+                              void *d_ws, size_t ws_bytes, void *stream) {
+    (void)d_ws;
+    (void)ws_bytes;
+    if (k < 1 || k > FATE_MAX_TOPK) return FATE_ERANGE;
+    if (state && state->n_frontier > 0 && (!d_idx || !d_val)) return FATE_EINVAL;
+    return score_impl(dags, state, params, d_scores, n_scores, k, d_idx, d_val, stream);
 }
 
 fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_t n_scores, int32_t k,

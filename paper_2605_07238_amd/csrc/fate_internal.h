@@ -55,6 +55,9 @@ struct ScoreLaunch {
     const uint32_t *done_off;
     const DoneParent *done;
     float *scores;
+    int32_t *tk_idx;  // fused top-k outputs (topk > 0), [nF][topk]
+    float *tk_val;
+    int32_t topk;
     int64_t nF, n_slices;
     int32_t D, M, K, H, max_shard, beta_uniform, slice;
     float beta0;

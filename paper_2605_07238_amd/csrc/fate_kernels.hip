@@ -29,7 +29,7 @@
 //   the transfer of v's output to devices outside S when w is a child of v).
 //
 // k_topk: one lane group per frontier stage; k rounds of a group-wide maximum
-// over 64-bit keys (order-preserving score bits, then inverted candidate index).
+// of order-preserving score bits, then of the lowest candidate index holding it.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -324,6 +324,82 @@ __device__ __forceinline__ void wave_sync() {
 
 // One completed parent's contribution on device d: its output is local
 // (colocation count) or has to be transferred from the cheapest holder.
+__device__ __forceinline__ uint32_t order_bits(float x) {
+    const uint32_t u = __float_as_uint(x + 0.0f);  // -0 -> +0
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float order_bits_inv(uint32_t o) {
+    const uint32_t u = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
+    return __uint_as_float(u);
+}
+
+// Group-wide maximum / minimum of a 32-bit unsigned value.  Inside a 16-lane
+// row: DPP steps (rotate by 8, mirror within halves, two quad swaps), each a
+// single VALU op with its operand taken from another lane; wider groups finish
+// across rows with shuffles.  The identity goes in as the DPP "old" value so
+// the move folds into the min/max.
+template <int G, bool MAX>
+__device__ __forceinline__ uint32_t group_reduce_u32(uint32_t x) {
+    constexpr int kId = MAX ? 0 : -1;
+    auto op = [](uint32_t p, uint32_t q) { return MAX ? (p > q ? p : q) : (p < q ? p : q); };
+    if constexpr (G >= 16) x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)x, 0x128, 0xF, 0xF, false));
+    if constexpr (G >= 8) x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)x, 0x141, 0xF, 0xF, false));
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)x, 0xB1, 0xF, 0xF, false));
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)x, 0x4E, 0xF, 0xF, false));
+#pragma unroll
+    for (int off = 16; off < G; off <<= 1) x = op(x, (uint32_t)__shfl_xor((int)x, off, G));
+    return x;
+}
+
+// Top-k of one stage held by a lane group: lane l owns candidates l + s*G
+// (s < 4) as order-preserving score bits, 0 for none or -inf.  Each of k
+// rounds takes the group maximum of the bits, then the smallest candidate
+// index holding it (ties go to the lower index), and clears that slot; lane
+// 0 writes (index, score), or (-1, -inf) once the group runs out.
+template <int G>
+__device__ __forceinline__ void group_topk(uint32_t (&sb)[4], int lane, int k, int32_t *out_i, float *out_v) {
+    for (int r = 0; r < k; ++r) {
+        uint32_t m = sb[0];
+#pragma unroll
+        for (int s = 1; s < 4; ++s) m = sb[s] > m ? sb[s] : m;
+        m = group_reduce_u32<G, true>(m);
+        uint32_t jm = 0xffffffffu;
+#pragma unroll
+        for (int s = 3; s >= 0; --s) jm = sb[s] == m ? (uint32_t)(lane + s * G) : jm;
+        jm = group_reduce_u32<G, false>(jm);
+        if (lane == 0) {
+            out_i[r] = m != 0 ? (int32_t)jm : -1;
+            out_v[r] = m != 0 ? order_bits_inv(m) : -inf_f();
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s) sb[s] = (uint32_t)(lane + s * G) == jm ? 0u : sb[s];
+    }
+}
+
+__device__ __forceinline__ uint32_t topk_bits(float x) { return x > -inf_f() ? order_bits(x) : 0u; }
+
+template <int G, int R>
+__device__ __forceinline__ void rank_stages(const float *scores, const uint32_t (&c0)[R], const int (&C)[R],
+                                            const int64_t (&f)[R], int lane, int k, int32_t *idx, float *val) {
+    float x[R][4];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const int j = lane + s * G;
+            x[r][s] = (f[r] >= 0 && j < C[r]) ? scores[c0[r] + j] : -inf_f();
+        }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (f[r] < 0) continue;  // uniform within the group
+        uint32_t sb[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) sb[s] = topk_bits(x[r][s]);
+        group_topk<G>(sb, lane, k, idx + f[r] * k, val + f[r] * k);
+    }
+}
+
 template <bool UNI>
 __device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, float su, int d, float &tr, float &cnt) {
     const bool local = bit(hu, d);
@@ -667,68 +743,64 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             if (nb < G) break;  // past the horizon depth or the list end
         }
 
-        // ---- emit
-        if (live) a.scores[c0 + lane] = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
+        // ---- emit scores
+        const float psi0 = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
+        if (live) a.scores[c0 + lane] = psi0;
 #pragma unroll
         for (int s = 0; s < 3; ++s) {
-            if (s >= wslots) continue;
+            if (s >= wslots) continue;  // uniform
             const int t = lane + s * G;
             if (t < nwin) a.scores[c0 + D + t] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
         }
     }
+
+    // ---- fused top-k: each group ranks the stages it scored, re-reading the
+    // scores its own lanes just wrote (outside the scoring loop, so it adds
+    // no register pressure there)
+    if (a.topk > 0) {  // uniform
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        constexpr int kRounds = 8;  // a slice holds at most eight rounds of groups
+        uint32_t c0[kRounds];
+        int C[kRounds];
+        int64_t f[kRounds];
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r) {
+            const int pos = tid / G + r * kGroups;
+            c0[r] = 0; C[r] = 0; f[r] = -1;
+            if (pos < nF) {
+                const int si = (int)L.order[pos];
+                c0[r] = L.stages[si].c0;
+                C[r] = (int)L.stages[si].nc;
+                f[r] = (int64_t)f0 + si;
+            }
+        }
+        rank_stages<G, kRounds>(a.scores, c0, C, f, lane, a.topk, a.tk_idx, a.tk_val);
+    }
 }
 
-__device__ __forceinline__ uint32_t order_bits(float x) {
-    const uint32_t u = __float_as_uint(x + 0.0f);  // -0 -> +0
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ float order_bits_inv(uint32_t o) {
-    const uint32_t u = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
-    return __uint_as_float(u);
-}
+constexpr int kTopkRounds = 4;  // stages per lane group in k_topk
 
 template <int G>
 __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
-    constexpr int kSlots = 4;
+    constexpr int kGroups = kBlock / G;
     const int tid = threadIdx.x;
     const int lane = tid & (G - 1);
-    const int64_t f = (int64_t)blockIdx.x * (kBlock / G) + tid / G;
-    if (f >= a.nF) return;
-    const uint32_t c0 = a.cand_off[f];
-    const int C = (int)(a.cand_off[f + 1] - c0);
-    uint64_t key[kSlots];
+    uint32_t c0[kTopkRounds];
+    int C[kTopkRounds];
+    int64_t f[kTopkRounds];
 #pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-        key[s] = 0;
-        const int j = lane + s * G;
-        if (j < C) {
-            const float x = a.scores[c0 + j];
-            if (x > -inf_f()) key[s] = ((uint64_t)order_bits(x) << 32) | (uint64_t)(0xffffffffu - (uint32_t)j);
+    for (int r = 0; r < kTopkRounds; ++r) {  // round r: the block's groups take consecutive stages
+        const int64_t fr = ((int64_t)blockIdx.x * kTopkRounds + r) * kGroups + tid / G;
+        c0[r] = 0; C[r] = 0; f[r] = -1;
+        if (fr < a.nF) {
+            c0[r] = a.cand_off[fr];
+            C[r] = (int)(a.cand_off[fr + 1] - c0[r]);
+            f[r] = fr;
         }
     }
-    int32_t *out_i = a.idx + f * a.k;
-    float *out_v = a.val + f * a.k;
-    for (int r = 0; r < a.k; ++r) {
-        uint64_t best = key[0];
-#pragma unroll
-        for (int s = 1; s < kSlots; ++s) best = key[s] > best ? key[s] : best;
-#pragma unroll
-        for (int off = G / 2; off >= 1; off >>= 1) {
-            const uint64_t o = __shfl_xor(best, off, G);
-            best = o > best ? o : best;
-        }
-        if (lane == 0) {
-            if (best == 0) { out_i[r] = -1; out_v[r] = -inf_f(); }
-            else {
-                out_i[r] = (int32_t)(0xffffffffu - (uint32_t)(best & 0xffffffffu));
-                out_v[r] = order_bits_inv((uint32_t)(best >> 32));
-            }
-        }
-#pragma unroll
-        for (int s = 0; s < kSlots; ++s)
-            if (best != 0 && key[s] == best) key[s] = 0;
-    }
+    rank_stages<G, kTopkRounds>(a.scores, c0, C, f, lane, a.k, a.idx, a.val);
 }
 
 }  // namespace
@@ -757,8 +829,8 @@ int launch_score(const ScoreLaunch &a, void *stream) {
 
 int launch_topk(const TopkLaunch &a, void *stream) {
     const int G = group_width(a.D);
-    const int64_t groups = kBlock / G;
-    const int64_t blocks = (a.nF + groups - 1) / groups;
+    const int64_t per_block = (int64_t)(kBlock / G) * kTopkRounds;
+    const int64_t blocks = (a.nF + per_block - 1) / per_block;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     switch (G) {
         case 4: hipLaunchKernelGGL(k_topk<4>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;

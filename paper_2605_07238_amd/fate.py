@@ -28,7 +28,7 @@ STATUS_NAMES = {0: "FATE_OK", -1: "FATE_EINVAL", -2: "FATE_ERANGE", -3: "FATE_EC
 # Every symbol declared in include/fate.h.
 EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_dags", "fate_layout_dags",
            "fate_pack_state_size", "fate_pack_state", "fate_layout_state", "fate_score_ws_size",
-           "fate_score_frontier", "fate_topk"]
+           "fate_score_frontier", "fate_score_topk", "fate_topk"]
 
 
 class FateError(RuntimeError):
@@ -109,6 +109,8 @@ def load(path: Optional[str] = None):
     lib.fate_score_ws_size.argtypes = [P(Dags), P(StateH), P(C.c_size_t)]
     lib.fate_score_frontier.argtypes = [P(Dags), P(StateH), P(Params), C.c_void_p, C.c_int64, C.c_void_p,
                                         C.c_size_t, C.c_void_p]
+    lib.fate_score_topk.argtypes = [P(Dags), P(StateH), P(Params), C.c_void_p, C.c_int64, C.c_int32, C.c_void_p,
+                                    C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
     lib.fate_topk.argtypes = [P(StateH), C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
     for name in EXPORTS[2:]:
         getattr(lib, name).restype = st
@@ -288,6 +290,30 @@ def fate_score_frontier(packed: PackedDags, state: PackedState, params: Params, 
                                    C.c_void_p(wsbuf.data_ptr()) if wsbuf is not None else None, ws.value,
                                    C.c_void_p(_stream_ptr(stream))), "fate_score_frontier")
     return out
+
+
+def fate_score_topk(packed: PackedDags, state: PackedState, params: Params, k: int, out=None, idx=None, val=None,
+                    stream=None):
+    """Scores and per-stage top-k in one launch; returns (scores, idx [F,k], val [F,k])."""
+    import torch
+    lib = load()
+    nc, F = state.n_cand, state.n_frontier
+    dev = packed.buf.device
+    if out is None:
+        out = torch.empty(max(1, nc), dtype=torch.float32, device=dev)
+    if idx is None:
+        idx = torch.empty((max(1, F), k), dtype=torch.int32, device=dev)
+    if val is None:
+        val = torch.empty((max(1, F), k), dtype=torch.float32, device=dev)
+    ws = C.c_size_t(0)
+    _check(lib.fate_score_ws_size(C.byref(packed.handle), C.byref(state.handle), C.byref(ws)), "fate_score_ws_size")
+    wsbuf = torch.empty(max(1, ws.value), dtype=torch.uint8, device=dev) if ws.value else None
+    _check(lib.fate_score_topk(C.byref(packed.handle), C.byref(state.handle), C.byref(params),
+                               C.c_void_p(out.data_ptr()), int(out.numel()), int(k), C.c_void_p(idx.data_ptr()),
+                               C.c_void_p(val.data_ptr()),
+                               C.c_void_p(wsbuf.data_ptr()) if wsbuf is not None else None, ws.value,
+                               C.c_void_p(_stream_ptr(stream))), "fate_score_topk")
+    return out, idx[:F], val[:F]
 
 
 def fate_topk(state: PackedState, scores, k: int, idx=None, val=None, stream=None):

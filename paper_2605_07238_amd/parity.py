@@ -51,3 +51,26 @@ def topk_mismatches(idx_gpu, psi_ref, mag_ref, cand_off, k, rtol=1e-5):
             if abs(seg[p] - seg[order[rnk]]) > 2 * tol:
                 bad += 1
     return bad
+
+
+def topk_of_scores(psi, cand_off, k):
+    """Per-stage top-k of given scores by (score descending, index ascending),
+    -inf excluded, padded with -1: the selection rule the top-k kernels
+    implement, applied on the host to the same float32 scores."""
+    psi = np.asarray(psi, np.float32)
+    co = np.asarray(cand_off, np.int64)
+    nF = len(co) - 1
+    out = np.full((nF, k), -1, np.int32)
+    if nF == 0 or k == 0 or co[-1] == 0:
+        return out
+    C = np.diff(co)
+    stage = np.repeat(np.arange(nF), C)
+    j = np.arange(co[-1]) - np.repeat(co[:-1], C)
+    order = np.lexsort((j, -psi.astype(np.float64), stage))
+    order = order[np.isfinite(psi[order])]
+    st = stage[order]
+    first = np.searchsorted(st, st, side="left")
+    rank = np.arange(len(order)) - first
+    keep = rank < k
+    out[st[keep], rank[keep]] = j[order[keep]]
+    return out

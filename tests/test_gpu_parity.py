@@ -162,3 +162,68 @@ def test_relabel_singletons_bitwise():
         x = a["psi"][co[f]:co[f] + w.D]
         y = b["psi"][co[f]:co[f] + w.D]
         assert np.allclose(y[perm], x, rtol=RTOL, atol=0)
+
+
+@pytest.mark.parametrize("case", [
+    ("random", dict(seed=4, D=8, n=20, shard_frac=0.8), 3, 4),
+    ("random", dict(seed=9, D=64, n=14, M=8, K=4), 2, 4),
+    ("random", dict(seed=2, D=7, K=0), 2, 2),
+    ("recipe", "shards-1024x500-d16", None, None),
+    ("recipe", "forkjoin-4096x1000-d16", None, None),
+], ids=["windows-d8", "d64", "d7-k0", "shards", "forkjoin"])
+@pytest.mark.parametrize("k", [1, 4, 9])
+def test_fused_score_topk_matches_two_calls(case, k):
+    """fate_score_topk writes bit-identical scores and top-k to
+    fate_score_frontier followed by fate_topk."""
+    import torch
+    from paper_2605_07238_amd import fate
+    kind, spec, H, ms = case
+    if kind == "random":
+        spec = dict(spec)
+        w = synth.make_random_small(spec.pop("seed"), B=3, H=H, max_shard=ms, **spec)
+    else:
+        w = synth.make_workload(spec, B=16)
+    pk = fate.fate_pack_dags(w)
+    st = fate.fate_pack_state(pk, w)
+    p = fate.make_params(w)
+    s1 = fate.fate_score_frontier(pk, st, p)
+    i1, v1 = fate.fate_topk(st, s1, k)
+    s2, i2, v2 = fate.fate_score_topk(pk, st, p, k)
+    torch.cuda.synchronize()
+    n = st.n_cand
+    assert np.array_equal(s1[:n].cpu().numpy().view(np.uint32), s2[:n].cpu().numpy().view(np.uint32))
+    assert np.array_equal(i1.cpu().numpy(), i2.cpu().numpy())
+    assert np.array_equal(v1.cpu().numpy().view(np.uint32), v2.cpu().numpy().view(np.uint32))
+
+
+@pytest.mark.parametrize("D", [4, 8, 16, 40])
+def test_topk_exact_ties_go_to_lower_index(D):
+    """Identical devices make every single-device candidate of a stage tie
+    exactly; the top-k must list the tied candidates by ascending index."""
+    w = synth.make_random_small(31, B=3, n=16, D=D, H=2, max_shard=2)
+    full = np.uint64((1 << D) - 1) if D < 64 else np.uint64(0xFFFFFFFFFFFFFFFF)
+    w.exec[:] = w.exec[:, :1]
+    w.switch_s[:] = w.switch_s[:, :1]
+    off = float(w.beta[0, 1])
+    w.beta[:] = off
+    np.fill_diagonal(w.beta, 0.0)
+    w.cap_bytes[:] = w.cap_bytes.max()
+    w.elig[:] = full
+    w.resident[:] = 0
+    w.prefix_cache[:] = 0
+    w.tau_free[:] = w.tau_free[:, :1]
+    w.holders[w.holders != 0] = full
+    print("[gpu] ties D", D, flush=True)
+    k = 6
+    g = run_gpu(w, H=2, max_shard=2, k=k)
+    check_against_oracle(w, g, H=2, max_shard=2, k=k)
+    co = g["cand_off"]
+    n_tied = 0
+    for f in range(g["nF"]):
+        single = g["psi"][co[f]:co[f] + D]
+        if np.all(single.view(np.uint32) == single[:1].view(np.uint32)) and np.isfinite(single[0]) \
+                and single[0] >= g["psi"][co[f]:co[f + 1]].max():
+            n_tied += 1
+            m = min(k, D)
+            assert g["idx"][f, :m].tolist() == list(range(m))
+    assert n_tied > 0

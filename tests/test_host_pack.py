@@ -212,3 +212,15 @@ def test_all_committed_gives_empty_frontier():
     _, h, _ = fate.fate_layout_dags(w)
     _, sh, _ = fate.fate_layout_state(h, w)
     assert int(sh.n_frontier) == 0 and int(sh.n_cand) == 0
+
+
+def test_topk_of_scores_rule():
+    """Host top-k rule used to check the kernels: score descending, ties to
+    the lower index, -inf skipped, -1 padding."""
+    from paper_2605_07238_amd import parity
+    inf = np.inf
+    psi = np.array([1.0, 3.0, 3.0, -inf, 2.0,   -inf, -inf,   0.0, -0.0], np.float32)
+    co = np.array([0, 5, 7, 9])
+    got = parity.topk_of_scores(psi, co, 4)
+    assert got.tolist() == [[1, 2, 4, 0], [-1, -1, -1, -1], [0, 1, -1, -1]]
+    assert parity.topk_of_scores(psi, np.array([0]), 3).shape == (0, 3)
