@@ -131,6 +131,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--topk", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload-file", default=None,
+                    help="load the batch from this .npz if it exists, else generate it and save it there "
+                         "(lets profiled runs skip the forked generator)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one plain device copy of 512 MiB (counter calibration)")
     args = ap.parse_args()
@@ -142,8 +145,17 @@ def main():
 
     from paper_2605_07238_amd import synth
     t0 = time.perf_counter()
-    w = synth.make_workload(args.workload, workers=min(16, os.cpu_count() or 1))
-    log("generated %s: B=%d N=%d in %.1fs" % (args.workload, w.B, w.N, time.perf_counter() - t0))
+    if args.workload_file and os.path.exists(args.workload_file):
+        w = synth.load_workload(args.workload_file)
+        if w.name != args.workload:
+            raise SystemExit("%s holds %s, not %s" % (args.workload_file, w.name, args.workload))
+        log("loaded %s from %s: B=%d N=%d in %.1fs" % (w.name, args.workload_file, w.B, w.N, time.perf_counter() - t0))
+    else:
+        w = synth.make_workload(args.workload, workers=min(16, os.cpu_count() or 1))
+        log("generated %s: B=%d N=%d in %.1fs" % (args.workload, w.B, w.N, time.perf_counter() - t0))
+        if args.workload_file:
+            synth.save_workload(w, args.workload_file)
+            log("saved to %s" % args.workload_file)
 
     import torch
     from paper_2605_07238_amd import fate

@@ -126,6 +126,40 @@ struct EntryL {
 static_assert(sizeof(EntryL<uint32_t>) == 60, "EntryL<u32>");
 static_assert(sizeof(EntryL<uint64_t>) == 80, "EntryL<u64>");
 
+// Staging entry of the slot layout (16-lane groups, so D <= 16 and device
+// masks fit in 16 bits; at most 32 models): four 16-byte words, read with
+// wide LDS loads.  The parent words are read only when w has completed parents.
+struct alignas(16) EntryS {
+    uint32_t moff;  // m(w) * D: column of w's model in the exec / switch tables
+    uint32_t m1;    // devices feasible for w | devices caching grp(w) << 16
+    uint32_t m2;    // devices caching grp(w) once v runs there | holders of parent 2 << 16
+    uint32_t mdn;   // m(w) | completed parents << 8
+    float gh;       // gamma^depth
+    float xbase;    // lam_tr * beta0 * sum of completed parents' sizes (every parent remote)
+    float pfp;      // lam_p * kappa_prefix * L(w)
+    float ccw;      // -lam_c / |Pa(w)| for a child of v (sign bit = child), else +0
+    uint32_t dbeg;  // first completed parent
+    uint32_t ph01;  // holders of parent 0 | holders of parent 1 << 16
+    float pw0;      // what a device holding parent q saves: its transfer plus lam_c / |Pa(w)|
+    float pw1;
+    float pw2;
+    float cw;       // lam_c / |Pa(w)|
+    uint32_t pad0, pad1;
+};
+static_assert(sizeof(EntryS) == 64, "EntryS");
+
+// The slot layout gives each 16-lane group G staging entries plus 16 bytes,
+// so the four groups of a wave start on different LDS banks and their wide
+// row reads do not conflict.
+constexpr int kSlotGroupBytes = 16 * (int)sizeof(EntryS) + 16;
+
+// Bytes of the staging area for lane-group width G (host and device agree).
+template <int G>
+constexpr int staging_bytes() {
+    return G == 16 ? (kScoreBlock / 16) * kSlotGroupBytes
+                   : kScoreBlock * (G <= 32 ? (int)sizeof(EntryL<uint32_t>) : (int)sizeof(EntryL<uint64_t>));
+}
+
 template <int G>
 using MaskFor = typename std::conditional<(G <= 32), uint32_t, uint64_t>::type;
 
@@ -134,6 +168,7 @@ struct Lds {
     void *pmask;  // device masks of the prefix table: uint32_t when D <= 32, else uint64_t
     uint8_t *order;
     float *wait, *exec, *ksw, *gpow;
+    uint32_t *next;  // next chunk of work positions to hand out
     StageL *stages;
     void *entries;
     int logT;
@@ -153,10 +188,10 @@ __host__ __device__ inline int pow2_at_least(int x) {
 
 // Byte offsets of every LDS array (shared by the launcher and the kernel).
 struct LdsPlan {
-    uint32_t pkey, pmask, rm, rho, fits, wt, cap, order, wait, gpow, exec, ksw, stages, entries, total;
+    uint32_t pkey, pmask, rm, rho, fits, wt, cap, order, wait, gpow, next, exec, ksw, stages, entries, total;
 };
 
-__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int entry_bytes) {
+__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int staging) {
     LdsPlan q;
     const uint32_t T = 1u << table_log2(D, K);
     const uint32_t mask_bytes = D <= 32 ? 4u : 8u;
@@ -171,11 +206,12 @@ __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int 
     q.cap = o; o += 8 * (uint32_t)D;
     o = (o + 15u) & ~15u;
     q.stages = o; o += (uint32_t)sizeof(StageL) * (uint32_t)slice;
-    q.entries = o; o += (uint32_t)entry_bytes * kScoreBlock;  // also holds the prologue's sort keys
+    q.entries = o; o += (uint32_t)staging;  // also holds the prologue's sort keys
     o = (o + 15u) & ~15u;
     q.order = o; o += ((uint32_t)slice + 15u) & ~15u;
     q.wait = o; o += 4 * (uint32_t)D;
     q.gpow = o; o += 4 * 16;
+    q.next = o; o += 16;
     q.exec = o; o += 4 * (uint32_t)(M * D);
     q.ksw = o; o += 4 * (uint32_t)(M * D);
     q.total = (o + 15u) & ~15u;
@@ -222,6 +258,53 @@ __device__ __forceinline__ Mask table_find(const Lds &L, uint64_t h) {
 template <int CTRL>
 __device__ __forceinline__ float dpp_move(float old, float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Order-preserving float <-> int32 map (an involution): the signed order of
+// the keys is the order of the floats (no NaNs); +inf maps to 0x7f800000.
+__device__ __forceinline__ int fkey(float x) {
+    const int b = __float_as_int(x);
+    return b ^ (int)((uint32_t)(b >> 31) >> 1);
+}
+__device__ __forceinline__ float unkey(int k) { return __int_as_float(k ^ (int)((uint32_t)(k >> 31) >> 1)); }
+
+constexpr int kKeyInf = 0x7f800000;  // key of +inf
+constexpr int kKeyId = 0x7fffffff;   // identity of the key minimum
+
+// min(x, x of the lane CTRL names); a lane without a source keeps x.  With
+// the identity as the DPP "old" value the move folds into one v_min_i32.
+template <int CTRL>
+__device__ __forceinline__ int kmin_dpp(int x) {
+    return min(x, __builtin_amdgcn_update_dpp(kKeyId, x, CTRL, 0xF, 0xF, false));
+}
+// min(a, x of the lane CTRL names); a lane without a source gets a.
+template <int CTRL>
+__device__ __forceinline__ int kmin_from(int a, int x) {
+    return min(a, __builtin_amdgcn_update_dpp(kKeyId, x, CTRL, 0xF, 0xF, false));
+}
+// x of the lane CTRL names; the key of +inf where there is none.
+template <int CTRL>
+__device__ __forceinline__ int kshift_in(int x) {
+    return __builtin_amdgcn_update_dpp(kKeyInf, x, CTRL, 0xF, 0xF, false);
+}
+// Inclusive prefix / suffix minimum of keys over a 16-lane DPP row.
+__device__ __forceinline__ int kscan_up16(int x) {
+    x = kmin_dpp<0x111>(x);
+    x = kmin_dpp<0x112>(x);
+    x = kmin_dpp<0x114>(x);
+    return kmin_dpp<0x118>(x);
+}
+__device__ __forceinline__ int kscan_down16(int x) {
+    x = kmin_dpp<0x101>(x);
+    x = kmin_dpp<0x102>(x);
+    x = kmin_dpp<0x104>(x);
+    return kmin_dpp<0x108>(x);
+}
+// x of the lane CTRL names, 0 where there is none: only for lanes whose
+// result is discarded (lets a following min/max fold the move).
+template <int CTRL>
+__device__ __forceinline__ float dpp_b0(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
 }
 
 // Inclusive minimum over lanes 0..lane of the group.
@@ -408,8 +491,9 @@ __device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, fl
     tr += local ? 0.0f : su * bm;
 }
 
-template <int G, bool UNI>
+template <int G, bool UNI, bool SLOTS>
 __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
+    static_assert(!SLOTS || (UNI && G == 16), "the slot layout needs 16-lane groups and uniform beta");
     extern __shared__ uint64_t smem[];
     uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
     const int tid = threadIdx.x;
@@ -419,8 +503,10 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     const int nF = (int)(a.slices[3 * blockIdx.x + 2] - f0);
     const int P = pow2_at_least(nF);
     using Mask = MaskFor<G>;  // device bitmask
+    // slot layout: 16-lane groups, uniform beta, at most 32 models (chosen by the launcher)
+    constexpr bool kSlots = SLOTS;
     using Entry = EntryL<Mask>;
-    const LdsPlan plan = lds_plan(D, K, M, a.slice, (int)sizeof(Entry));
+    const LdsPlan plan = lds_plan(D, K, M, a.slice, staging_bytes<G>());
 
     Lds L;
     L.logT = table_log2(D, K);
@@ -440,6 +526,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     L.exec = reinterpret_cast<float *>(sb + plan.exec);
     L.ksw = reinterpret_cast<float *>(sb + plan.ksw);
     L.gpow = reinterpret_cast<float *>(sb + plan.gpow);
+    L.next = reinterpret_cast<uint32_t *>(sb + plan.next);
 
     // ---- prologue: instance tables, cluster tables, the slice's stages
     for (int i = tid; i < T; i += kBlock) { L.pkey[i] = 0; static_cast<Mask *>(L.pmask)[i] = 0; }
@@ -452,8 +539,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     if (tid == 0) {
         float g = 1.0f;
         for (int h = 0; h < 16; ++h) { L.gpow[h] = g; g *= a.gamma; }
+        *L.next = 0u;
     }
-    for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = a.ksw[i]; }
+    for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = a.lam_s * a.ksw[i]; }
     for (int i = tid; i < P; i += kBlock) {
         uint64_t key = ~0ull;
         if (i < nF) {
@@ -523,9 +611,21 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     const float *exec_col = L.exec + dl;
     const float *ksw_col = L.ksw + dl;
     Entry *area = reinterpret_cast<Entry *>(L.entries) + (tid & ~(G - 1));  // this group's G staging slots
-    const float lam_s = a.lam_s, lam_tr = a.lam_tr, lam_c = a.lam_c, lam_p = a.lam_p;
+    const float lam_tr = a.lam_tr, lam_c = a.lam_c, lam_p = a.lam_p;
 
-    for (int pos = tid / G; pos < nF; pos += kGroups) {  // uniform within the group
+    // Waves claim chunks of consecutive work positions (one per group of the
+    // wave) from a shared counter: the largest stages go first and a wave
+    // that finishes early takes the next chunk (list scheduling).
+    constexpr int kGpw = 64 / G;  // lane groups per wave
+    const int gw = (tid & 63) / G;
+    const int nchunks = (nF + kGpw - 1) / kGpw;
+    for (;;) {
+        uint32_t chunk = 0;
+        if ((tid & 63) == 0) chunk = atomicAdd(L.next, 1u);
+        chunk = __builtin_amdgcn_readfirstlane(chunk);
+        if ((int)chunk >= nchunks) break;  // uniform within the wave
+        const int pos = (int)chunk * kGpw + gw;
+        if (pos >= nF) continue;  // the last chunk may be partial
         const int si = (int)L.order[pos];
         const StageL sv = L.stages[si];
         const int mv = sv.model;
@@ -542,12 +642,261 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         const float sw_v = bit(rho, mv) ? 0.0f : L.ksw[mv * D + dl];
         const float colo_v = sv.npar ? cnt / (float)sv.npar : 0.0f;
         const float pf_v = hv_cached ? a.kpf * sv.tokens : 0.0f;
-        const float a_imm = a.lam_q * L.wait[dl] + lam_s * sw_v - lam_c * colo_v;
+        const float a_imm = a.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
         const float b_imm = c_v + lam_tr * tr - lam_p * pf_v;
         const uint64_t rho_new = load_model(rho, mv, L.cap[dl], L.wt);
         const bool prefix_added = sv.hash != 0 && !hv_cached;
         const uint64_t feas_mask = (__ballot(feas_v) >> gbase) & gmask;
 
+        // ---- horizon descendants: shared staging and row evaluation
+        const float t0 = lam_tr * sv.sigma * a.beta0;  // v's output to one more device (uniform beta)
+        // Lane j stages entry base + j of v's descendant list into the group's
+        // LDS slots; returns how many entries the batch holds (they form a prefix).
+        auto stage_batch = [&](uint32_t base) -> int {
+            const uint32_t e = base + lane;
+            bool valid = e < sv.e1;
+            uint32_t ent = 0;
+            if (valid) {
+                ent = a.desc[e];
+                valid = (int)(ent >> kDescDepthShift) <= a.H;
+            }
+            if (valid) {
+                const uint32_t w = ent & kDescIdMask;
+                const int depth = (int)(ent >> kDescDepthShift);
+                const StageRec rw = a.rec[w];
+                const uint32_t db = a.done_off[w];
+                const uint32_t dn = a.done_off[w + 1] - db;
+                Entry &E = area[lane];
+                E.feas = (Mask)(rw.elig & L.fits[rw.model]);
+                E.pfdevs = table_find<Mask>(L, rw.hash);
+                E.gh = L.gpow[depth];
+                const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
+                E.cw = cw;
+                E.pfp = lam_p * a.kpf * rw.tokens;
+                E.moff = (uint32_t)rw.model * (uint32_t)D;
+                E.model = rw.model;
+                E.flags = (uint8_t)((depth == 1 ? 1 : 0) | (rw.hash != 0 && rw.hash == sv.hash ? 2 : 0));
+                E.dn = (uint16_t)dn;
+                E.dbeg = db;
+                float base_tr = 0.0f;
+                for (uint32_t q = 0; q < dn; ++q) {
+                    const DoneParent pu = a.done[db + q];
+                    const float t = lam_tr * a.beta0 * pu.sigma;
+                    if (UNI) base_tr += t;
+                    if (q < (uint32_t)kCap) {
+                        E.ph[q] = (Mask)pu.holders;
+                        E.pw[q] = UNI ? t + cw : pu.sigma;
+                    }
+                }
+                E.base_tr = base_tr;
+            }
+            const int nb = __popcll((__ballot(valid) >> gbase) & gmask);
+            wave_sync();
+            return nb;
+        };
+        // Row of descendant E: B(d') = c_hat(w, d' | s) and its value once v
+        // sits on d' (both +inf where w is infeasible).
+        auto entry_row = [&](const Entry &E, float &Bd_out, float &inval_out, float &gh_out, bool &child_out) {
+            const Mask feas = (Mask)E.feas, pfd = (Mask)E.pfdevs;
+            const float gh = E.gh, pfp = E.pfp, cw = E.cw;
+            const int mw = E.model, dn = E.dn, flags = E.flags;
+            const bool child = (flags & 1) != 0;
+            float X = exec_col[E.moff] + E.base_tr;
+            const int ns = dn < kCap ? dn : kCap;
+            if (UNI) {
+                for (int q = 0; q < ns; ++q)  // uniform trip count
+                    X -= ((Mask)E.ph[q] & mybit) != 0 ? E.pw[q] : 0.0f;
+                for (int q = kCap; q < dn; ++q) {  // rare: more completed parents than staged
+                    const DoneParent pu = a.done[E.dbeg + q];
+                    X -= ((Mask)pu.holders & mybit) != 0 ? lam_tr * a.beta0 * pu.sigma + cw : 0.0f;
+                }
+            } else {
+                float trw = 0.0f, cntw = 0.0f;
+                for (int q = 0; q < ns; ++q) add_parent<false>(a, E.ph[q], E.pw[q], dl, trw, cntw);
+                for (int q = kCap; q < dn; ++q) {
+                    const DoneParent pu = a.done[E.dbeg + q];
+                    add_parent<false>(a, pu.holders, pu.sigma, dl, trw, cntw);
+                }
+                X += lam_tr * trw - cntw * cw;
+            }
+            const float sw = ksw_col[E.moff];
+            const bool in_old = ((rho >> mw) & 1ull) != 0;
+            const bool in_new = ((rho_new >> mw) & 1ull) != 0;
+            const bool pf_old = (pfd & mybit) != 0;
+            const bool pf_new = pf_old || ((flags & 2) && prefix_added);
+            const float Braw = X + (in_old ? 0.0f : sw) - (pf_old ? pfp : 0.0f);
+            const float Bnew = X + (in_new ? 0.0f : sw) - (pf_new ? pfp : 0.0f) - (child ? cw : 0.0f);
+            const bool fw = (feas & mybit) != 0;
+            const float Bd = fw ? Braw : inf_f();
+            const float inval = fw ? Bnew : inf_f();
+            Bd_out = Bd;
+            inval_out = inval;
+            gh_out = gh;
+            child_out = child;
+        };
+
+        if constexpr (kSlots) {
+          {
+            // ---- candidates: the single {lane} on its own lane; the window of
+            // size k = s + 2 starting at device i on lane i of slot s (windows
+            // are ordered by size, then start: slot s writes one contiguous run)
+            const uint32_t c0 = sv.c0;
+            int nk = 0;  // window sizes present: 2 .. nk + 1
+            for (int rem = (int)sv.nc - D; rem > 0; rem -= D - nk) ++nk;
+            const float j0_single = a_imm + b_imm;
+            const uint32_t fm = (uint32_t)feas_mask;
+            float w_j0[3];
+            bool w_ok[3];
+#pragma unroll
+            for (int s = 0; s < 3; ++s) {
+                const int k = s + 2;
+                const float y = a_imm + b_imm / (float)k;
+                // maximum over devices i..i+k-1 (a lane whose source is past the row holds no window)
+                float m = fmaxf(y, dpp_b0<0x101>(y));
+                if (k >= 3) m = fmaxf(m, dpp_b0<0x102>(y));
+                if (k >= 4) m = fmaxf(m, dpp_b0<0x103>(y));
+                const uint32_t wm = (1u << k) - 1u;
+                w_ok[s] = s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
+                // gather with uniform beta: each of the k-1 other devices sends sigma/k
+                w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma / (float)k);
+            }
+
+            // ---- horizon rows, G at a time: lane j stages row j (EntryS)
+            EntryS *areaS = reinterpret_cast<EntryS *>(static_cast<uint8_t *>(L.entries) + (tid / G) * kSlotGroupBytes);
+            const uint32_t rho32 = (uint32_t)rho, rhon32 = (uint32_t)rho_new;
+            const uint32_t bit_lo = (uint32_t)mybit, bit_hi = bit_lo << 16;
+            auto stage_rows = [&](uint32_t base) -> int {
+                const uint32_t e = base + lane;
+                bool valid = e < sv.e1;
+                uint32_t ent = 0;
+                if (valid) {
+                    ent = a.desc[e];
+                    valid = (int)(ent >> kDescDepthShift) <= a.H;
+                }
+                if (valid) {
+                    const uint32_t w = ent & kDescIdMask;
+                    const int depth = (int)(ent >> kDescDepthShift);
+                    const StageRec rw = a.rec[w];
+                    const uint32_t db = a.done_off[w];
+                    const uint32_t dn = a.done_off[w + 1] - db;
+                    const uint32_t feas = (uint32_t)(rw.elig & L.fits[rw.model]);
+                    const uint32_t pfo = table_find<uint32_t>(L, rw.hash);
+                    const bool same = rw.hash != 0 && rw.hash == sv.hash;
+                    const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
+                    float base_tr = 0.0f;
+                    uint32_t ph[kCap] = {0u, 0u, 0u};
+                    float pw[kCap] = {0.0f, 0.0f, 0.0f};
+                    for (uint32_t q = 0; q < dn; ++q) {
+                        const DoneParent pu = a.done[db + q];
+                        const float t = lam_tr * a.beta0 * pu.sigma;
+                        base_tr += t;
+                        if (q < (uint32_t)kCap) {
+                            ph[q] = (uint32_t)pu.holders;
+                            pw[q] = t + cw;
+                        }
+                    }
+                    EntryS S;
+                    S.moff = (uint32_t)rw.model * (uint32_t)D;
+                    S.m1 = feas | (pfo << 16);
+                    // once v runs on a device, that device also caches grp(v)
+                    S.m2 = (same ? 0xffffu : pfo) | (ph[2] << 16);
+                    S.mdn = (uint32_t)rw.model | (dn << 8);
+                    S.gh = L.gpow[depth];
+                    S.xbase = base_tr;
+                    S.pfp = lam_p * a.kpf * rw.tokens;
+                    S.ccw = depth == 1 ? -cw : 0.0f;
+                    S.dbeg = db;
+                    S.ph01 = ph[0] | (ph[1] << 16);
+                    S.pw0 = pw[0];
+                    S.pw1 = pw[1];
+                    S.pw2 = pw[2];
+                    S.cw = cw;
+                    areaS[lane] = S;
+                }
+                const int nb = __popcll((__ballot(valid) >> gbase) & gmask);
+                wave_sync();
+                return nb;
+            };
+
+            // ---- horizon rows.  Outside S the row is scanned as order-preserving
+            // integer keys (prefix and suffix minima, one DPP op per step); the
+            // minimum outside a window {i..i+k-1} is min(prefix(i-1), suffix(i+k)).
+            // Inside S the window minimum of the post-state values slides by one
+            // lane per size.  A batch's terms are summed in fp32, batches in fp64.
+            double acc0 = 0.0, w_acc[3] = {0.0, 0.0, 0.0};
+            for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
+                const int nb = stage_rows(base);
+                float f0 = 0.0f, f1 = 0.0f, f2 = 0.0f, f3 = 0.0f;
+                for (int jj = 0; jj < nb; ++jj) {  // uniform
+                    const EntryS *E = areaS + jj;
+                    const uint4 q0 = *reinterpret_cast<const uint4 *>(E);
+                    const float4 q1 = *reinterpret_cast<const float4 *>(&E->gh);
+                    // q0: moff, m1, m2, mdn; q1: gh, xbase, pfp, ccw
+                    const float ex = exec_col[q0.x];
+                    const float sw = ksw_col[q0.x];
+                    float X = ex + q1.y;  // every completed parent remote
+                    if (q0.w > 255u) {  // completed parents: holding one's output saves its transfer and adds colocation
+                        const uint4 q2 = *reinterpret_cast<const uint4 *>(&E->dbeg);
+                        const float4 q3 = *reinterpret_cast<const float4 *>(&E->pw1);
+                        X -= (q2.y & bit_lo) ? __uint_as_float(q2.z) : 0.0f;
+                        X -= (q2.y & bit_hi) ? q3.x : 0.0f;
+                        X -= (q0.z & bit_hi) ? q3.y : 0.0f;
+                        const uint32_t dn = q0.w >> 8;
+                        for (uint32_t q = kCap; q < dn; ++q) {  // rare: more completed parents than staged
+                            const DoneParent pu = a.done[q2.x + q];
+                            X -= ((uint32_t)pu.holders & bit_lo) ? lam_tr * a.beta0 * pu.sigma + q3.z : 0.0f;
+                        }
+                    }
+                    const bool in_old = ((rho32 >> (q0.w & 31u)) & 1u) != 0;
+                    const bool in_new = ((rhon32 >> (q0.w & 31u)) & 1u) != 0;
+                    const bool fw = (q0.y & bit_lo) != 0;
+                    const bool pf_old = (q0.y & bit_hi) != 0;
+                    const bool pf_new = (q0.z & bit_lo) != 0;
+                    const float Braw = X + (in_old ? 0.0f : sw) - (pf_old ? q1.z : 0.0f);
+                    const float Bnew = X + (in_new ? 0.0f : sw) - (pf_new ? q1.z : 0.0f) + q1.w;
+                    const bool child = __float_as_int(q1.w) < 0;
+                    const float inval = fw ? Bnew : inf_f();
+                    // outside S: a child also receives v's output there
+                    const int key = fw ? fkey(Braw + (child ? t0 : 0.0f)) : kKeyInf;
+                    const int P = kscan_up16(key), Q = kscan_down16(key);
+                    const int Pl = kshift_in<0x111>(P);  // prefix up to lane-1; +inf at lane 0
+                    const float gh = q1.x;
+                    f0 += gh * fminf(unkey(kmin_from<0x101>(Pl, Q)), inval);
+                    if (nk >= 1) {  // uniform
+                        float inside = fminf(inval, dpp_b0<0x101>(inval));
+                        f1 += gh * fminf(unkey(kmin_from<0x102>(Pl, Q)), inside);
+                        if (nk >= 2) {
+                            inside = fminf(inside, dpp_b0<0x101>(inside));
+                            f2 += gh * fminf(unkey(kmin_from<0x103>(Pl, Q)), inside);
+                            if (nk >= 3) {
+                                inside = fminf(inside, dpp_b0<0x101>(inside));
+                                f3 += gh * fminf(unkey(kmin_from<0x104>(Pl, Q)), inside);
+                            }
+                        }
+                    }
+                }
+                acc0 += (double)f0;
+                w_acc[0] += (double)f1;
+                w_acc[1] += (double)f2;
+                w_acc[2] += (double)f3;
+                wave_sync();  // the next batch overwrites the staging slots
+                if (nb < G) break;  // past the horizon depth or the list end
+            }
+
+            // ---- emit scores
+            const float psi0 = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
+            if (live) a.scores[c0 + lane] = psi0;
+            uint32_t off = c0 + (uint32_t)D;
+#pragma unroll
+            for (int s = 0; s < 3; ++s) {
+                if (s >= nk) break;  // uniform
+                const int k = s + 2;
+                if (lane <= D - k) a.scores[off + lane] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
+                off += (uint32_t)(D - k + 1);
+            }
+            continue;
+          }
+        }
         // ---- candidates: slot 0 = single device `lane`; slots 1..3 = windows
         const uint32_t c0 = sv.c0;
         const int nwin = (int)sv.nc - D;
@@ -590,88 +939,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             w_j0[s] = tmax + lam_tr * gat;
         }
 
-        // ---- horizon descendants, G at a time: lane j stages entry j in LDS
-        const float t0 = lam_tr * sv.sigma * a.beta0;
+        // ---- horizon descendants, G at a time
         for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
-            const uint32_t e = base + lane;
-            bool valid = e < sv.e1;
-            uint32_t ent = 0;
-            if (valid) {
-                ent = a.desc[e];
-                valid = (int)(ent >> kDescDepthShift) <= a.H;
-            }
-            if (valid) {
-                const uint32_t w = ent & kDescIdMask;
-                const int depth = (int)(ent >> kDescDepthShift);
-                const StageRec rw = a.rec[w];
-                const uint32_t db = a.done_off[w];
-                const uint32_t dn = a.done_off[w + 1] - db;
-                Entry &E = area[lane];
-                E.feas = (Mask)(rw.elig & L.fits[rw.model]);
-                E.pfdevs = table_find<Mask>(L, rw.hash);
-                E.gh = L.gpow[depth];
-                const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
-                E.cw = cw;
-                E.pfp = lam_p * a.kpf * rw.tokens;
-                E.moff = (uint32_t)rw.model * (uint32_t)D;
-                E.model = rw.model;
-                E.flags = (uint8_t)((depth == 1 ? 1 : 0) | (rw.hash != 0 && rw.hash == sv.hash ? 2 : 0));
-                E.dn = (uint16_t)dn;
-                E.dbeg = db;
-                float base_tr = 0.0f;
-                for (uint32_t q = 0; q < dn; ++q) {
-                    const DoneParent pu = a.done[db + q];
-                    const float t = lam_tr * a.beta0 * pu.sigma;
-                    if (UNI) base_tr += t;
-                    if (q < (uint32_t)kCap) {
-                        E.ph[q] = (Mask)pu.holders;
-                        E.pw[q] = UNI ? t + cw : pu.sigma;
-                    }
-                }
-                E.base_tr = base_tr;
-            }
-            const int nb = __popcll((__ballot(valid) >> gbase) & gmask);  // valid entries form a prefix
-            wave_sync();
-            // Row of descendant E: B(d') = c_hat(w, d' | s) and its value once v
-            // sits on d' (both +inf where w is infeasible).
-            auto entry_row = [&](const Entry &E, float &Bd_out, float &inval_out, float &gh_out, bool &child_out) {
-                const Mask feas = (Mask)E.feas, pfd = (Mask)E.pfdevs;
-                const float gh = E.gh, pfp = E.pfp, cw = E.cw;
-                const int mw = E.model, dn = E.dn, flags = E.flags;
-                const bool child = (flags & 1) != 0;
-                float X = exec_col[E.moff] + E.base_tr;
-                const int ns = dn < kCap ? dn : kCap;
-                if (UNI) {
-                    for (int q = 0; q < ns; ++q)  // uniform trip count
-                        X -= ((Mask)E.ph[q] & mybit) != 0 ? E.pw[q] : 0.0f;
-                    for (int q = kCap; q < dn; ++q) {  // rare: more completed parents than staged
-                        const DoneParent pu = a.done[E.dbeg + q];
-                        X -= ((Mask)pu.holders & mybit) != 0 ? lam_tr * a.beta0 * pu.sigma + cw : 0.0f;
-                    }
-                } else {
-                    float trw = 0.0f, cntw = 0.0f;
-                    for (int q = 0; q < ns; ++q) add_parent<false>(a, E.ph[q], E.pw[q], dl, trw, cntw);
-                    for (int q = kCap; q < dn; ++q) {
-                        const DoneParent pu = a.done[E.dbeg + q];
-                        add_parent<false>(a, pu.holders, pu.sigma, dl, trw, cntw);
-                    }
-                    X += lam_tr * trw - cntw * cw;
-                }
-                const float sw = lam_s * ksw_col[E.moff];
-                const bool in_old = ((rho >> mw) & 1ull) != 0;
-                const bool in_new = ((rho_new >> mw) & 1ull) != 0;
-                const bool pf_old = (pfd & mybit) != 0;
-                const bool pf_new = pf_old || ((flags & 2) && prefix_added);
-                const float Braw = X + (in_old ? 0.0f : sw) - (pf_old ? pfp : 0.0f);
-                const float Bnew = X + (in_new ? 0.0f : sw) - (pf_new ? pfp : 0.0f) - (child ? cw : 0.0f);
-                const bool fw = (feas & mybit) != 0;
-                const float Bd = fw ? Braw : inf_f();
-                const float inval = fw ? Bnew : inf_f();
-                Bd_out = Bd;
-                inval_out = inval;
-                gh_out = gh;
-                child_out = child;
-            };
+            const int nb = stage_batch(base);
             int jj = 0;
             if (UNI && wslots == 0) {  // singletons only: two descendants per iteration
                 for (; jj + 1 < nb; jj += 2) {
@@ -743,6 +1013,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             if (nb < G) break;  // past the horizon depth or the list end
         }
 
+
         // ---- emit scores
         const float psi0 = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
         if (live) a.scores[c0 + lane] = psi0;
@@ -754,13 +1025,11 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         }
     }
 
-    // ---- fused top-k: each group ranks the stages it scored, re-reading the
-    // scores its own lanes just wrote (outside the scoring loop, so it adds
-    // no register pressure there)
-    if (a.topk > 0) {  // uniform
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    // ---- fused top-k: after the block's scoring, each group ranks a fixed
+    // share of its stages, re-reading the scores just written (outside the
+    // scoring loop, so it adds no register pressure there)
+    if (a.topk > 0) {  // uniform over the block
+        __syncthreads();  // stages were scored by whichever wave claimed them
         constexpr int kRounds = 8;  // a slice holds at most eight rounds of groups
         uint32_t c0[kRounds];
         int C[kRounds];
@@ -808,15 +1077,18 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
 template <bool UNI>
 static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int G = group_width(a.D);
-    const int entry_bytes = G <= 32 ? (int)sizeof(EntryL<uint32_t>) : (int)sizeof(EntryL<uint64_t>);
-    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, entry_bytes).total;
+    const int sb = G == 16 ? staging_bytes<16>() : G <= 32 ? staging_bytes<8>() : staging_bytes<64>();
+    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb).total;
     const dim3 grid((unsigned)a.n_slices), block(kBlock);
     switch (G) {
-        case 4: hipLaunchKernelGGL((k_score<4, UNI>), grid, block, lds, s, a); break;
-        case 8: hipLaunchKernelGGL((k_score<8, UNI>), grid, block, lds, s, a); break;
-        case 16: hipLaunchKernelGGL((k_score<16, UNI>), grid, block, lds, s, a); break;
-        case 32: hipLaunchKernelGGL((k_score<32, UNI>), grid, block, lds, s, a); break;
-        default: hipLaunchKernelGGL((k_score<64, UNI>), grid, block, lds, s, a); break;
+        case 4: hipLaunchKernelGGL((k_score<4, UNI, false>), grid, block, lds, s, a); break;
+        case 8: hipLaunchKernelGGL((k_score<8, UNI, false>), grid, block, lds, s, a); break;
+        case 16:
+            if (UNI && a.M <= 32) hipLaunchKernelGGL((k_score<16, UNI, UNI>), grid, block, lds, s, a);
+            else hipLaunchKernelGGL((k_score<16, UNI, false>), grid, block, lds, s, a);
+            break;
+        case 32: hipLaunchKernelGGL((k_score<32, UNI, false>), grid, block, lds, s, a); break;
+        default: hipLaunchKernelGGL((k_score<64, UNI, false>), grid, block, lds, s, a); break;
     }
 }
 

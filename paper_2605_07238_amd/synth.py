@@ -618,3 +618,28 @@ def make_random_small(seed: int, B: int = 2, n: int = 12, D: int = 4, M: int = 3
     rc = dict(D=D, M=M, H=H)
     w = _assemble(f"random-small-{seed}", rc, (exec_, switch, weight, cap, beta), insts, K, max_shard)
     return w
+
+
+# ---------------------------------------------------------------------------
+# Saving a generated batch (so a process that must not fork can reuse one)
+# ---------------------------------------------------------------------------
+
+_ARRAY_FIELDS = [f.name for f in dataclasses.fields(Workload)
+                 if f.name not in ("name", "D", "M", "K", "H", "max_shard", "params")]
+
+
+def save_workload(w: Workload, path: str) -> None:
+    """Write ``w`` as an uncompressed .npz (plain arrays plus a JSON header)."""
+    import json
+    meta = dict(name=w.name, D=w.D, M=w.M, K=w.K, H=w.H, max_shard=w.max_shard, params=w.params)
+    np.savez(path, _meta=np.array(json.dumps(meta)), **{k: getattr(w, k) for k in _ARRAY_FIELDS})
+
+
+def load_workload(path: str) -> Workload:
+    """Read a batch written by :func:`save_workload` (no pickled objects)."""
+    import json
+    with np.load(path, allow_pickle=False) as z:
+        meta = json.loads(str(z["_meta"]))
+        arrays = {k: z[k] for k in _ARRAY_FIELDS}
+    return Workload(name=meta["name"], D=int(meta["D"]), M=int(meta["M"]), K=int(meta["K"]), H=int(meta["H"]),
+                    max_shard=int(meta["max_shard"]), params=dict(meta["params"]), **arrays)

@@ -67,6 +67,11 @@ RANDOM_CASES = [
     (9, dict(D=64, n=14, M=8, K=4), 2, 4),
     (10, dict(D=64, n=14, M=8, K=4, uniform_beta=True), 3, 1),
     (11, dict(D=2, n=30, p_edge=0.5), 5, 2),
+    # 16-lane groups with uniform beta: more than 32 models (general layout), then the
+    # slot layout with dense edges (more completed parents than a staging slot holds)
+    (12, dict(D=16, n=24, M=40, K=4, uniform_beta=True), 3, 4),
+    (13, dict(D=12, n=30, M=6, p_edge=0.5, uniform_beta=True), 4, 3),
+    (14, dict(D=16, n=40, M=8, p_edge=0.35, uniform_beta=True, shard_frac=0.7), 3, 4),
 ]
 
 
@@ -227,3 +232,41 @@ def test_topk_exact_ties_go_to_lower_index(D):
             m = min(k, D)
             assert g["idx"][f, :m].tolist() == list(range(m))
     assert n_tied > 0
+
+
+def _many_parents_spec(seed, D=16, n_roots=6):
+    """Completed roots feed a pending stage w together with the frontier stage
+    v, so w's row carries more completed parents than a staging slot holds;
+    a grandchild of v adds a second such row at depth 2."""
+    rng = np.random.default_rng(seed)
+    M = 4
+    full = (1 << D) - 1
+    insts = []
+    for _ in range(3):
+        roots = list(range(n_roots))
+        v, w, x, y = n_roots, n_roots + 1, n_roots + 2, n_roots + 3
+        parents = [[] for _ in roots] + [[0], roots + [v], [1, 2, 3, 4, w], [1]]
+        n = len(parents)
+        holders = [int(rng.integers(1, full + 1)) for _ in roots] + [0] * 4
+        insts.append(dict(
+            parents=parents, model=[int(rng.integers(M)) for _ in range(n)], elig=[full] * n,
+            shard_max=[1] * n_roots + [3, 2, 1, 4],
+            prefix_hash=[0] * n_roots + [77, 77, 0, 78], prefix_tokens=[0.0] * n_roots + [512.0, 256.0, 0.0, 128.0],
+            out_bytes=[float(rng.uniform(1e8, 2e9)) for _ in range(n)],
+            status=[1] * n_roots + [0, 0, 0, 0], holders=holders,
+            resident=[int(rng.integers(0, 1 << M)) for _ in range(D)],
+            prefix_cache=[[77 if rng.random() < 0.3 else 0] for _ in range(D)],
+            tau_free=[float(rng.uniform(0, 2)) for _ in range(D)], t_now=0.5))
+    beta = [[0.0 if i == j else 3e-10 for j in range(D)] for i in range(D)]
+    return dict(D=D, M=M, K=1, exec=rng.uniform(0.2, 2.0, size=(M, D)).tolist(),
+                switch_s=rng.uniform(0.0, 1.0, size=(M, D)).tolist(), weight_gb=[10] * M, cap_gb=[40] * D,
+                beta=beta, max_shard=4, instances=insts)
+
+
+@pytest.mark.parametrize("D", [16, 12])
+def test_rows_with_many_completed_parents(D):
+    from builders import from_spec
+    w = from_spec(_many_parents_spec(5 + D, D=D), H=3)
+    print("[gpu] many completed parents D", D, flush=True)
+    g = run_gpu(w, H=3)
+    check_against_oracle(w, g, H=3)

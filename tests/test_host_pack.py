@@ -224,3 +224,14 @@ def test_topk_of_scores_rule():
     got = parity.topk_of_scores(psi, co, 4)
     assert got.tolist() == [[1, 2, 4, 0], [-1, -1, -1, -1], [0, 1, -1, -1]]
     assert parity.topk_of_scores(psi, np.array([0]), 3).shape == (0, 3)
+
+
+def test_workload_save_load_roundtrip(tmp_path):
+    w = synth.make_random_small(3, B=3, n=20, D=8)
+    p = str(tmp_path / "w.npz")
+    synth.save_workload(w, p)
+    v = synth.load_workload(p)
+    for f in synth._ARRAY_FIELDS:
+        a, b = getattr(w, f), getattr(v, f)
+        assert a.dtype == b.dtype and np.array_equal(a, b), f
+    assert (w.name, w.D, w.M, w.K, w.H, w.max_shard, w.params) == (v.name, v.D, v.M, v.K, v.H, v.max_shard, v.params)
