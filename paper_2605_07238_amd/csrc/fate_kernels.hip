@@ -436,27 +436,41 @@ __device__ __forceinline__ uint32_t group_reduce_u32(uint32_t x) {
 }
 
 // Top-k of one stage held by a lane group: lane l owns candidates l + s*G
-// (s < 4) as order-preserving score bits, 0 for none or -inf.  Each of k
+// (s < S) as order-preserving score bits, 0 for none or -inf.  Each of k
 // rounds takes the group maximum of the bits, then the smallest candidate
-// index holding it (ties go to the lower index), and clears that slot; lane
-// 0 writes (index, score), or (-1, -inf) once the group runs out.
-template <int G>
-__device__ __forceinline__ void group_topk(uint32_t (&sb)[4], int lane, int k, int32_t *out_i, float *out_v) {
+// index holding it (ties go to the lower index), and clears that slot.  The
+// pick is (index, score), or (-1, -inf) once the group runs out.  For k <= G
+// lane r keeps round r's pick and lanes 0..k-1 store them together;
+// otherwise lane 0 stores each round's pick.
+template <int G, int S>
+__device__ __forceinline__ void group_topk(uint32_t (&sb)[S], int lane, int k, int32_t *out_i, float *out_v) {
+    int32_t my_i = -1;
+    uint32_t my_m = 0u;
     for (int r = 0; r < k; ++r) {
         uint32_t m = sb[0];
 #pragma unroll
-        for (int s = 1; s < 4; ++s) m = sb[s] > m ? sb[s] : m;
+        for (int s = 1; s < S; ++s) m = sb[s] > m ? sb[s] : m;
         m = group_reduce_u32<G, true>(m);
         uint32_t jm = 0xffffffffu;
 #pragma unroll
-        for (int s = 3; s >= 0; --s) jm = sb[s] == m ? (uint32_t)(lane + s * G) : jm;
+        for (int s = S - 1; s >= 0; --s) jm = sb[s] == m ? (uint32_t)(lane + s * G) : jm;
         jm = group_reduce_u32<G, false>(jm);
-        if (lane == 0) {
-            out_i[r] = m != 0 ? (int32_t)jm : -1;
+        const int32_t pick = m != 0 ? (int32_t)jm : -1;
+        if (k <= G) {  // uniform
+            if (lane == r) {
+                my_i = pick;
+                my_m = m;
+            }
+        } else if (lane == 0) {
+            out_i[r] = pick;
             out_v[r] = m != 0 ? order_bits_inv(m) : -inf_f();
         }
 #pragma unroll
-        for (int s = 0; s < 4; ++s) sb[s] = (uint32_t)(lane + s * G) == jm ? 0u : sb[s];
+        for (int s = 0; s < S; ++s) sb[s] = (uint32_t)(lane + s * G) == jm ? 0u : sb[s];
+    }
+    if (k <= G && lane < k) {
+        out_i[lane] = my_i;
+        out_v[lane] = my_m != 0 ? order_bits_inv(my_m) : -inf_f();
     }
 }
 
@@ -476,10 +490,15 @@ __device__ __forceinline__ void rank_stages(const float *scores, const uint32_t 
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         if (f[r] < 0) continue;  // uniform within the group
-        uint32_t sb[4];
+        if (C[r] <= G) {  // one candidate per lane
+            uint32_t sb[1] = {topk_bits(x[r][0])};
+            group_topk<G, 1>(sb, lane, k, idx + f[r] * k, val + f[r] * k);
+        } else {
+            uint32_t sb[4];
 #pragma unroll
-        for (int s = 0; s < 4; ++s) sb[s] = topk_bits(x[r][s]);
-        group_topk<G>(sb, lane, k, idx + f[r] * k, val + f[r] * k);
+            for (int s = 0; s < 4; ++s) sb[s] = topk_bits(x[r][s]);
+            group_topk<G, 4>(sb, lane, k, idx + f[r] * k, val + f[r] * k);
+        }
     }
 }
 
