@@ -2,17 +2,18 @@
 """Benchmark of horizon-aware candidate scoring on one MI355X.
 
 One step = one pass of the scoring path over the whole batch with the packed
-DAGs and state already resident in HBM: fate_score_topk, which scores every
-candidate of every frontier stage (immediate cost plus the depth-H horizon)
-and writes each stage's top-k in the same kernel.  Packing (host validation, layout and the host-to-device copy) is
-done once before timing and reported separately.
+DAGs and state already resident in HBM: fate_score_frontier, which scores
+every candidate of every frontier stage (immediate cost plus the depth-H
+horizon), then fate_topk (each stage's top-k); --fused times the one-launch
+fate_score_topk instead.  Packing (host validation, layout and the
+host-to-device copy) is done once before timing and reported separately.
 
 Prints one JSON line (rank 0, N=1):
   value          candidate-horizon evaluations per second over the timed steps;
                  one evaluation per feasible candidate and per (feasible
                  candidate, horizon descendant) pair
-  roofline       the kernel's algorithmic bytes per launch / its average launch
-                 time (HIP events on the launch stream) vs 8 TB/s HBM
+  roofline       the score kernel's algorithmic bytes per launch / its average
+                 launch time (HIP events on the launch stream) vs 8 TB/s HBM
   cpu_baseline   the fp64 oracle timed on this host's cores over the same batch
 """
 
@@ -70,7 +71,8 @@ def counted_work(w, pk, st, scores_host, H):
     seg = np.repeat(np.arange(F), lens)
     ndesc = np.bincount(seg[keep], minlength=F)
     feas = np.add.reduceat(np.isfinite(scores_host).astype(np.int64), co[:-1]) if F else np.zeros(0, np.int64)
-    n_eval = int((feas * (1 + ndesc)).sum())
+    per_stage = feas * (1 + ndesc)
+    n_eval = int(per_stage.sum())
     touched = np.unique(np.concatenate([fv, wid[idx][keep]]))
     npar = np.diff(w.par_off)
     inst = np.repeat(np.arange(w.B), np.diff(w.stage_off))
@@ -92,7 +94,8 @@ def counted_work(w, pk, st, scores_host, H):
         scores=4 * int(co[-1]),
     )
     return n_eval, int(sum(nbytes.values())), nbytes, dict(F=F, C=int(co[-1]), touched=len(touched),
-                                                            desc_entries=int(keep.sum()))
+                                                            desc_entries=int(keep.sum()),
+                                                            per_stage=per_stage, stage_inst=fb)
 
 
 def read_traffic(workload: str):
@@ -114,6 +117,29 @@ def read_traffic(workload: str):
         return None
 
 
+def host_info():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return dict(cpu_model=model, nproc=os.cpu_count(), omp_num_threads=os.environ.get("OMP_NUM_THREADS"))
+
+
+def cpu_per_core(w, H, counts, n_inst=64):
+    """One oracle thread on the first ``n_inst`` instances (evaluations/s)."""
+    from oracle import oracle
+    n_inst = min(n_inst, w.B)
+    sub = w.subset(list(range(n_inst)))
+    evals = int(counts["per_stage"][counts["stage_inst"] < n_inst].sum())
+    t = time.perf_counter()
+    oracle.score(sub, H=H, threads=1)
+    return evals / (time.perf_counter() - t), n_inst
+
+
 def cpu_baseline(w, H, min_seconds=10.0, max_passes=50):
     """Time the fp64 oracle over the whole batch, repeating passes until at
     least ``min_seconds`` of host work; returns (seconds per pass, passes, threads)."""
@@ -128,6 +154,34 @@ def cpu_baseline(w, H, min_seconds=10.0, max_passes=50):
     return total / passes, passes, threads
 
 
+def describe(k):
+    """Per-recipe sizes of one planning step (one JSON line each)."""
+    import torch
+    from paper_2605_07238_amd import fate, synth
+    assert torch.cuda.is_available(), "--describe needs a GPU (evaluations count feasible candidates)"
+    torch.cuda.set_device(0)
+    fate.load()
+    for name in synth.RECIPE_ORDER:
+        w = synth.make_workload(name, workers=min(16, os.cpu_count() or 1))
+        pk = fate.fate_pack_dags(w, H=w.H)
+        st = fate.fate_pack_state(pk, w)
+        params = fate.make_params(w, H=w.H)
+        scores, idx, val = fate.fate_score_topk(pk, st, params, k)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
+        for e0, e1 in evs:
+            e0.record()
+            fate.fate_score_topk(pk, st, params, k, out=scores, idx=idx, val=val)
+            e1.record()
+        torch.cuda.synchronize()
+        ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in evs]))
+        n_eval, alg, parts, counts = counted_work(w, pk, st, scores[:st.n_cand].cpu().numpy(), w.H)
+        alg += 8 * k * counts["F"]
+        print(json.dumps(dict(workload=name, B=w.B, N=w.N, D=w.D, H=w.H, frontier_stages=counts["F"],
+                              candidates=counts["C"], horizon_entries=counts["desc_entries"], evals=n_eval,
+                              algorithmic_bytes=alg, fused_median_ms=ms, evals_per_s=n_eval / (ms * 1e-3),
+                              achieved_gbs=alg / (ms * 1e-3) / 1e9, input_sha256=synth.fingerprint(w))), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,7 +189,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--topk", type=int, default=4)
+    ap.add_argument("--fused", action="store_true",
+                    help="time fate_score_topk (one launch) instead of fate_score_frontier + fate_topk")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-medians", action="store_true",
+                    help="skip the extra median timings of the three launch variants (profiling runs)")
+    ap.add_argument("--describe", action="store_true",
+                    help="print |F|, candidates, horizon entries, evaluations, algorithmic bytes and the fused "
+                         "kernel's median time for every recipe, then exit")
     ap.add_argument("--workload-file", default=None,
                     help="load the batch from this .npz if it exists, else generate it and save it there "
                          "(lets profiled runs skip the forked generator)")
@@ -149,6 +210,9 @@ def main():
         sys.exit(2)
 
     from paper_2605_07238_amd import synth
+    if args.describe:
+        describe(args.topk)
+        return
     t0 = time.perf_counter()
     if args.workload_file and os.path.exists(args.workload_file):
         w = synth.load_workload(args.workload_file)
@@ -181,27 +245,67 @@ def main():
     idx = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.int32, device="cuda")
     val = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.float32, device="cuda")
 
-    def step():
-        fate.fate_score_topk(pk, st, params, args.topk, out=scores, idx=idx, val=val)
+    if args.fused:
+        def step():
+            fate.fate_score_topk(pk, st, params, args.topk, out=scores, idx=idx, val=val)
+    else:
+        def step():
+            fate.fate_score_frontier(pk, st, params, out=scores)
+            fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     log("warmup done (%d steps)" % args.warmup)
 
+    # Timed region: K steps.  Events on the launch stream bracket the score
+    # kernel (the dominant one) and the whole step.
     K = args.steps
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    ev = [(mk(), mk(), mk()) for _ in range(K)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(K):
         ev[i][0].record()
-        step()
-        ev[i][1].record()
+        if args.fused:
+            step()
+            ev[i][1].record()
+        else:
+            fate.fate_score_frontier(pk, st, params, out=scores)
+            ev[i][1].record()
+            fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
+        ev[i][2].record()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     ms_step = (t_end - t_start) * 1e3 / K
-    score_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    log("timed %d steps: %.4f ms/step (fused score + top-k kernel %.4f ms)" % (K, ms_step, score_ms))
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))  # score kernel (fused: score + top-k)
+    step_kern_ms = float(np.mean([a.elapsed_time(c) for a, _, c in ev]))
+    log("timed %d steps: %.4f ms/step; %s kernel %.4f ms, all kernels %.4f ms"
+        % (K, ms_step, "fused score + top-k" if args.fused else "score", kern_ms, step_kern_ms))
+
+    def median_ms(fn, n=20):
+        for _ in range(3):
+            fn()
+        evs = [(mk(), mk()) for _ in range(n)]
+        for e0, e1 in evs:
+            e0.record()
+            fn()
+            e1.record()
+        torch.cuda.synchronize()
+        return float(np.median([e0.elapsed_time(e1) for e0, e1 in evs]))
+
+    medians = None
+    if not args.no_medians:
+        medians = {
+            "fused_score_topk": median_ms(
+                lambda: fate.fate_score_topk(pk, st, params, args.topk, out=scores, idx=idx, val=val)),
+            "score_only": median_ms(lambda: fate.fate_score_frontier(pk, st, params, out=scores)),
+            "score_then_topk_two_calls": median_ms(lambda: (fate.fate_score_frontier(pk, st, params, out=scores),
+                                                            fate.fate_topk(st, scores, args.topk, idx=idx, val=val))),
+        }
+        step()  # leave this step's results in place for the counts below
+        torch.cuda.synchronize()
+        log("medians (ms): %s" % json.dumps(medians))
 
     if args.copy_calibration:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -212,9 +316,10 @@ def main():
 
     scores_host = scores[:st.n_cand].cpu().numpy()
     n_eval, alg_bytes, parts, counts = counted_work(w, pk, st, scores_host, H)
-    parts["topk"] = 8 * args.topk * counts["F"]
-    alg_bytes += parts["topk"]
-    achieved = alg_bytes / (score_ms * 1e-3) / 1e9
+    if args.fused:  # the top-k output belongs to the timed kernel
+        parts["topk"] = 8 * args.topk * counts["F"]
+        alg_bytes += parts["topk"]
+    achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
     traffic = read_traffic(args.workload)
     out = {
         "metric": METRIC,
@@ -233,13 +338,17 @@ def main():
             "workload": args.workload, "B": w.B, "stages_per_dag": int(np.diff(w.stage_off).max()),
             "D": w.D, "M": w.M, "K": w.K, "H": H, "max_shard": w.max_shard, "topk": args.topk,
             "frontier_stages": counts["F"], "candidates": counts["C"], "horizon_entries": counts["desc_entries"],
-            "evals_per_step": n_eval, "score_topk_kernel_ms": score_ms,
+            "evals_per_step": n_eval, "step": "fused score + top-k" if args.fused else "score, then top-k",
+            "kernel_ms": kern_ms, "step_kernels_ms": step_kern_ms,
+            "median_ms": medians,
+            "input_sha256": synth.fingerprint(w),
             "pack_dags_s": t_pack_dags, "pack_state_s": t_pack_state,
             "algorithmic_bytes_per_launch": alg_bytes, "algorithmic_bytes_parts": parts,
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": "k_score",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+            "kernel": "k_score (with top-k epilogue)" if args.fused else "k_score",
         },
     }
     if not args.no_cpu_baseline:
@@ -249,7 +358,11 @@ def main():
         # (checked by the parity tests), so the evaluation count is shared
         out["cpu_baseline"] = {"value": n_eval / dt, "unit": "evals/s", "cores": threads, "kind": "oracle",
                                "sample": "all %d instances of %s, %d passes of %.2f s" % (w.B, args.workload, passes, dt)}
-        log("oracle: %d passes, %.2f s each, %d threads" % (passes, dt, threads))
+        per_core, n_inst = cpu_per_core(w, H, counts)
+        out["cpu_baseline"].update(host_info())
+        out["cpu_baseline"]["per_core_value"] = per_core
+        out["cpu_baseline"]["per_core_sample"] = "1 thread, first %d instances" % n_inst
+        log("oracle: %d passes, %.2f s each, %d threads; %.3g evals/s on one thread" % (passes, dt, threads, per_core))
     print(json.dumps(out), flush=True)
 
 

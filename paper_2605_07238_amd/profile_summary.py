@@ -41,6 +41,8 @@ def main():
     ap.add_argument("--kernel", default="k_score")
     ap.add_argument("--copy-bytes", type=int, default=512 << 20)
     ap.add_argument("--kernel-source")
+    ap.add_argument("--cus", type=int, default=256)
+    ap.add_argument("--xcds", type=int, default=8)
     args = ap.parse_args()
     out = []
     if args.trace_db:
@@ -50,11 +52,13 @@ def main():
             out.append("%-70s %7d %10.2f %10.2f %10.2f %12.1f" % (name[:70], n, avg, mn, mx, tot))
     fetch = write = None
     copy_fetch = copy_write = None
+    kavg = {}
     for path in args.pmc:
         for kname, cs in counters(path).items():
             for cname, v in cs.items():
                 if args.kernel in kname:
                     avg = sum(v) / len(v)
+                    kavg[cname] = avg
                     out.append("counter %-20s %-60s avg over %d dispatches: %.1f" % (cname, kname[:60], len(v), avg))
                     if cname == "FETCH_SIZE":
                         fetch = avg
@@ -77,6 +81,13 @@ def main():
         out.append("fetch_kib_per_dispatch: %.1f" % fetch)
         out.append("write_kib_per_dispatch: %.1f" % write)
         out.append("hbm_bytes_per_launch: %.0f" % hbm)
+    if "SQ_INSTS_VALU" in kavg and "GRBM_GUI_ACTIVE" in kavg:
+        # GRBM_GUI_ACTIVE is summed over the XCDs; a wave64 VALU instruction
+        # occupies a 16-lane SIMD for 4 cycles
+        cycles = kavg["GRBM_GUI_ACTIVE"] / args.xcds
+        busy = kavg["SQ_INSTS_VALU"] * 4.0 / (args.cus * 4 * cycles)
+        out.append("gpu_cycles_per_dispatch: %.0f" % cycles)
+        out.append("valu_issue_busy_frac: %.3f  (SQ_INSTS_VALU x 4 / (%d CUs x 4 SIMDs x cycles))" % (busy, args.cus))
     if args.kernel_source:
         out.append("kernel_source_sha256: %s" % hashlib.sha256(open(args.kernel_source, "rb").read()).hexdigest())
     print("\n".join(out))

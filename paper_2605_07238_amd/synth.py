@@ -643,3 +643,18 @@ def load_workload(path: str) -> Workload:
         arrays = {k: z[k] for k in _ARRAY_FIELDS}
     return Workload(name=meta["name"], D=int(meta["D"]), M=int(meta["M"]), K=int(meta["K"]), H=int(meta["H"]),
                     max_shard=int(meta["max_shard"]), params=dict(meta["params"]), **arrays)
+
+
+def fingerprint(w: Workload) -> str:
+    """SHA-256 over a batch's arrays and header (identifies the generated input)."""
+    import hashlib
+    import json
+    h = hashlib.sha256()
+    h.update(json.dumps(dict(name=w.name, D=w.D, M=w.M, K=w.K, H=w.H, max_shard=w.max_shard,
+                             params=w.params), sort_keys=True).encode())
+    for k in _ARRAY_FIELDS:
+        a = np.ascontiguousarray(getattr(w, k))
+        h.update(k.encode())
+        h.update(str(a.dtype).encode())
+        h.update(memoryview(a).cast("B"))
+    return h.hexdigest()
