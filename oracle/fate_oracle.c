@@ -53,6 +53,23 @@
  * 10. Top-k per frontier stage: candidates ordered by (Psi descending,
  *     candidate index ascending), infeasible ones skipped, padded with
  *     (-1, -infinity).
+ * 11. Commit-and-advance of the planning state (Alg. 1: materialise the
+ *     selected placements, then advance the frontier and update the
+ *     planning state; Alg. 2: commit into the action pool and update the
+ *     state as the stages complete) [reading: one planning-state update per
+ *     planning step].  Per instance, the selected frontier stages are applied
+ *     in ascending stage id; for each device d of the chosen candidate S
+ *     (k = |S|), in ascending device id:
+ *       start  = max(tau_d, t)
+ *       switch = kappa_switch(m(v), d) if m(v) is not resident on d, else 0
+ *       rho_d  = Load(rho_d, m(v))                      (as in step 6)
+ *       grp(v) joins the prefix slots of d if it is nonzero and absent: the
+ *         first empty slot takes it, or, when all K slots are full, the slots
+ *         move down by one (slot 0, the oldest, is dropped) and slot K-1
+ *         takes it  [reading: the slots are kept oldest first]
+ *       tau_d  = start + c(v,d)/k + switch
+ *     then v is completed with its output held by exactly S.  The next
+ *     frontier follows from step 1 on the updated state.
  *
  * Alongside Psi the oracle reports A, the sum of the absolute values of every
  * weighted term it added (for the maximising device of step 5 and the
@@ -254,6 +271,17 @@ int oracle_count(const oracle_in_t *in, int B, int64_t *nf, int64_t *nc) {
     return 0;
 }
 
+/* Frontier stages of every instance (instance-local ids), slots as in
+ * oracle_score: f_off[b] is the first slot of instance b. */
+int oracle_frontier(const oracle_in_t *in, int B, const int64_t *f_off, int32_t *front_v) {
+    for (int b = 0; b < B; ++b) {
+        int64_t base = in->stage_off[b], n = in->stage_off[b + 1] - base, f = f_off[b];
+        for (int v = 0; v < n; ++v)
+            if (is_frontier(in, base, v)) front_v[f++] = v;
+    }
+    return 0;
+}
+
 typedef struct { int *depth; int *queue; int *list; int *cptr; int *cidx; } scratch_t;
 
 /* Breadth-first horizon set of v: fills list[0..count) with stages at hop
@@ -410,4 +438,63 @@ int oracle_topk(const double *psi, int64_t nc, int k, int32_t *idx, double *val)
     }
     free(taken);
     return 0;
+}
+
+/* Step 11: commit the selected candidates of the current frontier and
+ * advance the planning state.  sel[f] is the chosen candidate of frontier
+ * slot f (slots as oracle_score lists them, f_off[b] the first slot of
+ * instance b), or -1 to leave the stage pending.  The output arrays start as
+ * copies of the current state and are updated in place; tau_out is fp64.
+ * Returns the number of selections rejected (candidate index out of range,
+ * or a device of the candidate infeasible for the stage); those stages stay
+ * pending. */
+int oracle_commit(const oracle_in_t *in, int B, const int64_t *f_off, const int32_t *front_v,
+                  const int32_t *sel, uint64_t *res_out, uint64_t *cache_out, uint64_t *holders_out,
+                  uint8_t *status_out, double *tau_out) {
+    const int D = in->D, K = in->K;
+    int rejected = 0;
+    for (int b = 0; b < B; ++b) {
+        int64_t base = in->stage_off[b];
+        for (int64_t f = f_off[b]; f < f_off[b + 1]; ++f) {
+            if (sel[f] < 0) continue;
+            int64_t g = base + front_v[f];
+            if (sel[f] >= n_candidates(in, g)) { ++rejected; continue; }
+            int i0, k;
+            candidate(in, sel[f], &i0, &k);
+            int ok = 1;
+            for (int d = i0; d < i0 + k; ++d)
+                if (!feasible(in, g, d)) ok = 0;
+            if (!ok) { ++rejected; continue; }
+            int m = in->model[g];
+            uint64_t h = in->hash[g];
+            uint64_t held = 0;
+            for (int d = i0; d < i0 + k; ++d) {
+                int64_t bd = (int64_t)b * D + d;
+                double start = tau_out[bd] > (double)in->t_now[b] ? tau_out[bd] : (double)in->t_now[b];
+                double sw = has_bit(res_out[bd], m) ? 0.0 : (double)in->switch_s[m * D + d];
+                res_out[bd] = load_model(in, res_out[bd], m, d);
+                if (h != 0 && K > 0) {
+                    uint64_t *slots = cache_out + bd * K;
+                    int present = 0, empty = -1;
+                    for (int q = 0; q < K; ++q) {
+                        if (slots[q] == h) present = 1;
+                        if (slots[q] == 0 && empty < 0) empty = q;
+                    }
+                    if (!present) {
+                        if (empty >= 0) {
+                            slots[empty] = h;
+                        } else {
+                            for (int q = 0; q + 1 < K; ++q) slots[q] = slots[q + 1];
+                            slots[K - 1] = h;
+                        }
+                    }
+                }
+                tau_out[bd] = start + exec_c(in, m, d) / (double)k + sw;
+                held |= (uint64_t)1 << d;
+            }
+            holders_out[g] = held;
+            status_out[g] = ST_COMPLETED;
+        }
+    }
+    return rejected;
 }

@@ -77,6 +77,11 @@ def _bind(lib):
     lib.oracle_score.restype = C.c_int
     lib.oracle_topk.argtypes = [C.c_void_p, C.c_int64, C.c_int, C.c_void_p, C.c_void_p]
     lib.oracle_topk.restype = C.c_int
+    lib.oracle_frontier.argtypes = [C.POINTER(_In), C.c_int, C.c_void_p, C.c_void_p]
+    lib.oracle_frontier.restype = C.c_int
+    lib.oracle_commit.argtypes = [C.POINTER(_In), C.c_int, C.c_void_p, C.c_void_p, C.c_void_p,
+                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    lib.oracle_commit.restype = C.c_int
 
 
 def f32(x: float) -> float:
@@ -88,16 +93,8 @@ def _c(a, dt):
     return np.ascontiguousarray(a, dtype=dt)
 
 
-def score(w, params: Optional[Dict[str, float]] = None, H: Optional[int] = None,
-          max_shard: Optional[int] = None, threads: Optional[int] = None, lib=None) -> dict:
-    """Score every candidate of every frontier stage of workload ``w``.
-
-    Returns a dict with ``front_b``, ``front_v`` (instance-local ids),
-    ``cand_off`` ([n_frontier+1], global candidate offsets), ``psi`` and
-    ``mag`` (fp64, per candidate) and ``nf`` (frontier size per instance).
-    Parameters are rounded to float32 first, as the GPU path sees them.
-    """
-    lib = lib or load()
+def _record(w, params=None, H=None, max_shard=None):
+    """The C input record for workload ``w`` (and the arrays it points into)."""
     p = dict(w.params)
     if params:
         p.update(params)
@@ -120,6 +117,20 @@ def score(w, params: Optional[Dict[str, float]] = None, H: Optional[int] = None,
         setattr(rec, k, a.ctypes.data)
     for k in ("lam_q", "lam_s", "lam_tr", "lam_c", "lam_p", "kappa_prefix", "gamma"):
         setattr(rec, k, f32(p[k]))
+    return rec, keep
+
+
+def score(w, params: Optional[Dict[str, float]] = None, H: Optional[int] = None,
+          max_shard: Optional[int] = None, threads: Optional[int] = None, lib=None) -> dict:
+    """Score every candidate of every frontier stage of workload ``w``.
+
+    Returns a dict with ``front_b``, ``front_v`` (instance-local ids),
+    ``cand_off`` ([n_frontier+1], global candidate offsets), ``psi`` and
+    ``mag`` (fp64, per candidate) and ``nf`` (frontier size per instance).
+    Parameters are rounded to float32 first, as the GPU path sees them.
+    """
+    lib = lib or load()
+    rec, keep = _record(w, params, H, max_shard)
     B = w.B
     nf = np.zeros(B, np.int64)
     nc = np.zeros(B, np.int64)
@@ -157,3 +168,47 @@ def topk(res: dict, k: int, lib=None):
         lib.oracle_topk(seg.ctypes.data, int(co[f + 1] - co[f]), int(k),
                         idx[f].ctypes.data, val[f].ctypes.data)
     return idx, val
+
+
+def frontier(w, max_shard: Optional[int] = None, lib=None):
+    """Frontier of ``w``: (front_b, front_v instance-local, f_off [B+1], cand_off [F+1])."""
+    lib = lib or load()
+    rec, keep = _record(w, None, None, max_shard)
+    B = w.B
+    nf = np.zeros(B, np.int64)
+    nc = np.zeros(B, np.int64)
+    lib.oracle_count(C.byref(rec), B, nf.ctypes.data, nc.ctypes.data)
+    f_off = np.zeros(B + 1, np.int64)
+    f_off[1:] = np.cumsum(nf)
+    front_v = np.zeros(int(f_off[-1]), np.int32)
+    lib.oracle_frontier(C.byref(rec), B, f_off.ctypes.data, front_v.ctypes.data)
+    front_b = np.repeat(np.arange(B, dtype=np.int32), nf)
+    return front_b, front_v, f_off
+
+
+def commit(w, sel, max_shard: Optional[int] = None, lib=None):
+    """Commit-and-advance (oracle step 11): apply the candidate ``sel[f]``
+    chosen for each frontier slot f of ``w`` (-1 = leave pending).
+
+    Returns (new workload, tau in fp64 [B, D], number of rejected
+    selections).  The new workload is a copy of ``w`` whose resident models,
+    prefix slots, holders, statuses and free times (rounded to float32, the
+    state's format) are the committed state."""
+    import dataclasses
+    lib = lib or load()
+    front_b, front_v, f_off = frontier(w, max_shard, lib)
+    sel = np.ascontiguousarray(sel, dtype=np.int32)
+    if sel.shape != (len(front_v),):
+        raise ValueError("one selection per frontier slot expected (%d), got %s" % (len(front_v), sel.shape))
+    rec, keep = _record(w, None, None, max_shard)
+    res = np.array(w.resident, dtype=np.uint64, copy=True)
+    cache = np.array(w.prefix_cache, dtype=np.uint64, copy=True)
+    holders = np.array(w.holders, dtype=np.uint64, copy=True)
+    status = np.array(w.status, dtype=np.uint8, copy=True)
+    tau = np.array(w.tau_free, dtype=np.float64, copy=True)
+    rejected = lib.oracle_commit(C.byref(rec), w.B, f_off.ctypes.data, front_v.ctypes.data, sel.ctypes.data,
+                                 res.ctypes.data, cache.ctypes.data, holders.ctypes.data, status.ctypes.data,
+                                 tau.ctypes.data)
+    new = dataclasses.replace(w, resident=res, prefix_cache=cache, holders=holders, status=status,
+                              tau_free=tau.astype(np.float32))
+    return new, tau, int(rejected)

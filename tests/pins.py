@@ -297,6 +297,98 @@ def check_isolated_stage(seed: int, lib=None):
     assert np.array_equal(r1["psi"][:len(r0["psi"])], r0["psi"])
 
 
+def check_commit_scenario(name: str, lib=None):
+    """Commit-and-advance against the hand-derived state of a scenario."""
+    sc = scenarios.COMMITS[name]
+    w = builders.from_spec(sc["spec"], H=1)
+    _, fv, _ = oracle.frontier(w, lib=lib)
+    assert fv.tolist() == sc["front_v"], fv
+    new, tau, rejected = oracle.commit(w, sc["sel"], lib=lib)
+    assert rejected == sc["rejected"], rejected
+    assert new.resident.reshape(-1).tolist() == sc["resident"], new.resident
+    assert new.prefix_cache.reshape(w.D, w.K).tolist() == sc["prefix_cache"], new.prefix_cache
+    assert new.holders.tolist() == sc["holders"], new.holders
+    assert new.status.tolist() == sc["status"], new.status
+    _close(tau.reshape(-1), sc["tau"], rtol=0, atol=0)
+    _, fv2, _ = oracle.frontier(new, lib=lib)
+    assert fv2.tolist() == sc["next_front_v"], fv2
+
+
+def check_commit_invariants(seed: int, lib=None):
+    """Committing each frontier stage's best candidate: every such stage is
+    completed on exactly its candidate's devices, each touched device then
+    holds the stage's model within its capacity after dropping the
+    smallest-id other models, caches the stage's prefix group, and never
+    frees up earlier than before; the next frontier is the set of pending
+    stages whose parents are all completed (recomputed here with numpy).
+    Committing nothing changes nothing."""
+    w = synth.make_random_small(seed, B=3, n=24, D=6, M=5, K=3, max_shard=3, shard_frac=0.6, tight_caps=True)
+    r = oracle.score(w, lib=lib)
+    idx, _ = oracle.topk(r, 1, lib=lib)
+    none, _, rej0 = oracle.commit(w, np.full(len(r["front_v"]), -1, np.int32), lib=lib)
+    assert rej0 == 0
+    for f in ("resident", "prefix_cache", "holders", "status", "tau_free"):
+        assert np.array_equal(getattr(none, f), getattr(w, f)), f
+    new, tau, rej = oracle.commit(w, idx[:, 0], lib=lib)
+    assert rej == 0
+    D, K = w.D, w.K
+
+    def devices(j):
+        k, i = 1, int(j)
+        if j >= D:  # windows by size, then start
+            t = int(j) - D
+            k = 2
+            while t >= D - k + 1:
+                t -= D - k + 1
+                k += 1
+            i = t
+        return list(range(i, i + k))
+
+    # a device that takes several stages in one commit sees them in turn; the
+    # per-device checks below are for devices that take exactly one
+    uses = np.zeros((w.B, D), np.int64)
+    for f, j in enumerate(idx[:, 0]):
+        if j >= 0:
+            for d in devices(j):
+                uses[int(r["front_b"][f]), d] += 1
+    for f, j in enumerate(idx[:, 0]):
+        b, v = int(r["front_b"][f]), int(r["front_v"][f])
+        g = int(w.stage_off[b]) + v
+        if j < 0:
+            assert new.status[g] == w.status[g]
+            continue
+        S = devices(j)
+        assert new.status[g] == 1 and int(new.holders[g]) == sum(1 << d for d in S)
+        m = int(w.model[g])
+        for d in S:
+            assert tau[b, d] >= float(w.tau_free[b, d])
+            if uses[b, d] != 1:
+                continue
+            old = int(w.resident[b, d])
+            res = int(new.resident[b, d])
+            assert (res >> m) & 1
+            used = sum(int(w.weight_bytes[x]) for x in range(w.M) if (res >> x) & 1)
+            assert used <= int(w.cap_bytes[d])
+            if not (old >> m) & 1:
+                # models dropped from d are the smallest ids other than m
+                dropped = [x for x in range(w.M) if (old >> x) & 1 and not (res >> x) & 1]
+                kept = [x for x in range(w.M) if (old >> x) & 1 and (res >> x) & 1 and x != m]
+                assert not dropped or not kept or max(dropped) < min(kept), (old, res, m)
+            h = int(w.prefix_hash[g])
+            if h and K:
+                assert h in [int(x) for x in new.prefix_cache[b, d]]
+    # next frontier, recomputed from the parent lists
+    npar = np.diff(w.par_off)
+    inst = np.repeat(np.arange(w.B), np.diff(w.stage_off))
+    pg = w.par_idx.astype(np.int64) + w.stage_off[np.repeat(inst, npar)]
+    done = np.zeros(len(npar), np.int64)
+    np.add.at(done, np.repeat(np.arange(len(npar)), npar), (new.status[pg] == 1).astype(np.int64))
+    ready = np.nonzero((new.status == 0) & (done == npar))[0]
+    fb2, fv2, _ = oracle.frontier(new, lib=lib)
+    got = (w.stage_off[fb2] + fv2).astype(np.int64)
+    assert np.array_equal(got, ready), (got, ready)
+
+
 ALL_CHECKS = (
     [("scenario:" + k, (lambda k: lambda lib: check_scenario(k, lib))(k)) for k in scenarios.ALL]
     + [("worked_example", check_worked_example)]
@@ -307,4 +399,6 @@ ALL_CHECKS = (
     + [("h0_gamma0:%d" % s, (lambda s: lambda lib: check_h0_equals_gamma0(s, lib))(s)) for s in range(2)]
     + [("truncation:%d" % s, (lambda s: lambda lib: check_truncation(s, lib))(s)) for s in range(3)]
     + [("isolated:%d" % s, (lambda s: lambda lib: check_isolated_stage(s, lib))(s)) for s in range(2)]
+    + [("commit:" + k, (lambda k: lambda lib: check_commit_scenario(k, lib))(k)) for k in scenarios.COMMITS]
+    + [("commit_invariants:%d" % s, (lambda s: lambda lib: check_commit_invariants(s, lib))(s)) for s in range(3)]
 )

@@ -142,3 +142,62 @@ FRONTIER = dict(
 ALL = dict(WAIT_SWITCH=WAIT_SWITCH, TRANSFER_COLO=TRANSFER_COLO, WINDOWS=WINDOWS, POST_STATE=POST_STATE,
            POST_STATE_H0=POST_STATE_H0, HORIZON_SET=HORIZON_SET, HORIZON_SET_H3=HORIZON_SET_H3,
            FEASIBILITY=FEASIBILITY, FRONTIER=FRONTIER)
+
+
+# ---------------------------------------------------------------------------
+# Commit-and-advance (oracle step 11).  Each scenario lists the selection per
+# frontier slot and the hand-derived state after the commit.
+# ---------------------------------------------------------------------------
+
+# C1: one device each.  v1 (model 2) on d0: start = max(1.0, t=1.5) = 1.5;
+#     model 2 absent -> switch 0.5; Load adds 2 (30 GB > 25 GB) and evicts
+#     the smallest other id, model 0; grp 99 takes the empty slot 1;
+#     tau0 = 1.5 + 0.75 + 0.5 = 2.75.  v4 (model 1) on d1: start 1.5, switch
+#     0.5, Load adds 1 (20 GB fits); grp 7 already cached; tau1 = 1.5 + 1.0 +
+#     0.5 = 3.0.  Next frontier: v2 (parent v1) and v3 (parents v0, v1).
+COMMIT_SINGLE = dict(
+    spec=dict(D=2, M=3, K=2, exec=[[0.5, 0.5], [1.0, 1.0], [0.75, 1.25]],
+              switch_s=[[0.25, 0.25], [0.5, 0.5], [0.5, 1.0]], weight_gb=[10, 10, 10], cap_gb=[25, 25],
+              beta=_UNI,
+              instances=[dict(parents=[[], [0], [1], [0, 1], []], model=[0, 2, 1, 0, 1], elig=[3] * 5,
+                              prefix_hash=[0, 99, 99, 0, 7], prefix_tokens=[0.0] * 5, out_bytes=[1.0] * 5,
+                              status=[1, 0, 0, 0, 0], holders=[1, 0, 0, 0, 0],
+                              resident=[3, 4], prefix_cache=[[5, 0], [7, 8]],
+                              tau_free=[1.0, 0.5], t_now=1.5)]),
+    front_v=[1, 4], sel=[0, 1],
+    resident=[6, 6], prefix_cache=[[5, 99], [7, 8]], tau=[2.75, 3.0],
+    holders=[1, 1, 0, 0, 2], status=[1, 1, 0, 0, 1], next_front_v=[2, 3], rejected=0)
+
+# C2: a window and a second stage on a shared device.  v0 (model 0, R = 2)
+#     on the window {d0, d1} (candidate D + 0): d0 start 2.0, model resident,
+#     full prefix slots [3, 4] drop the oldest -> [4, 99], tau0 = 2.0 + 1/2;
+#     d1 start max(0, 1) = 1.0, switch 0.25, empty slots -> [99, 0],
+#     tau1 = 1.0 + 3/2 + 0.25 = 2.75; holders 0b11.  Then v1 (model 1) on d0:
+#     start 2.5, switch 1.0, Load adds 1 (fits), grp 0 inserts nothing,
+#     tau0 = 2.5 + 0.5 + 1.0 = 4.0.  Next frontier: v2.
+COMMIT_WINDOW = dict(
+    spec=dict(D=2, M=2, K=2, exec=[[1.0, 3.0], [0.5, 0.5]], switch_s=[[0.25, 0.25], [1.0, 1.0]],
+              weight_gb=[10, 10], cap_gb=[25, 25], beta=_UNI, max_shard=2,
+              instances=[dict(parents=[[], [], [0]], model=[0, 1, 0], elig=[3] * 3, shard_max=[2, 1, 1],
+                              prefix_hash=[99, 0, 0], prefix_tokens=[0.0] * 3, out_bytes=[1.0] * 3,
+                              status=[0, 0, 0], holders=[0, 0, 0],
+                              resident=[1, 0], prefix_cache=[[3, 4], [0, 0]],
+                              tau_free=[2.0, 0.0], t_now=1.0)]),
+    front_v=[0, 1], sel=[2, 0],
+    resident=[3, 1], prefix_cache=[[4, 99], [99, 0]], tau=[4.0, 2.75],
+    holders=[3, 1, 0], status=[1, 1, 0], next_front_v=[2], rejected=0)
+
+# C3: rejected selections leave the state unchanged: an index past the
+#     candidates, and a window over a device where v is not eligible.
+COMMIT_REJECT = dict(
+    spec=dict(D=2, M=1, K=1, exec=[[1.0, 1.0]], switch_s=[[0.5, 0.5]], weight_gb=[10], cap_gb=[20, 20],
+              beta=_UNI, max_shard=2,
+              instances=[dict(parents=[[], []], model=[0, 0], elig=[3, 1], shard_max=[1, 2],
+                              prefix_hash=[11, 12], prefix_tokens=[0.0, 0.0], out_bytes=[1.0, 1.0],
+                              status=[0, 0], holders=[0, 0], resident=[0, 0], prefix_cache=[[0], [0]],
+                              tau_free=[0.0, 0.0], t_now=0.0)]),
+    front_v=[0, 1], sel=[5, 2],
+    resident=[0, 0], prefix_cache=[[0], [0]], tau=[0.0, 0.0],
+    holders=[0, 0], status=[0, 0], next_front_v=[0, 1], rejected=2)
+
+COMMITS = dict(COMMIT_SINGLE=COMMIT_SINGLE, COMMIT_WINDOW=COMMIT_WINDOW, COMMIT_REJECT=COMMIT_REJECT)

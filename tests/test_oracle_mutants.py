@@ -51,6 +51,18 @@ MUTANTS = {
     "descendant_max_device": [("if (val < vbest) { vbest = val; vmag = m_; }",
                                "if (vbest == INFINITY || val > vbest) { vbest = val; vmag = m_; }")],
     "prefix_sign": [("return c + t_sw + t_tr - t_co - t_pf;", "return c + t_sw + t_tr - t_co + t_pf;")],
+    # commit-and-advance
+    "commit_start_ignores_now": [("double start = tau_out[bd] > (double)in->t_now[b] ? tau_out[bd] : (double)in->t_now[b];",
+                                  "double start = tau_out[bd];")],
+    "commit_switch_always": [("double sw = has_bit(res_out[bd], m) ? 0.0 : (double)in->switch_s[m * D + d];",
+                              "double sw = (double)in->switch_s[m * D + d];")],
+    "commit_exec_not_split": [("tau_out[bd] = start + exec_c(in, m, d) / (double)k + sw;",
+                               "tau_out[bd] = start + exec_c(in, m, d) + sw;")],
+    "commit_full_ring_overwrites_newest": [("for (int q = 0; q + 1 < K; ++q) slots[q] = slots[q + 1];\n", "")],
+    "commit_holders_last_device": [("held |= (uint64_t)1 << d;", "held = (uint64_t)1 << d;")],
+    "commit_no_load": [("res_out[bd] = load_model(in, res_out[bd], m, d);", "res_out[bd] = res_out[bd];")],
+    "commit_ignores_feasibility": [("if (!ok) { ++rejected; continue; }", "if (0) { ++rejected; continue; }")],
+    "commit_not_completed": [("status_out[g] = ST_COMPLETED;", "status_out[g] = status_out[g];")],
 }
 
 
