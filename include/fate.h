@@ -171,6 +171,15 @@ typedef struct {
     const uint32_t *done_off; /* [N+1]: completed parents of flat stage g are
                                  done[done_off[g] .. done_off[g+1]) */
     const void *done;         /* 16-byte entries {uint64 holders; float out_bytes; pad} */
+    /* Planning state (fate_pack_state_advance; all zero otherwise).  Its
+     * sections are sized for any later planning step, so n_frontier,
+     * n_cand and n_slices above hold those capacities, and the current
+     * counts live in device memory: counts[0] frontier stages, counts[1]
+     * candidates, counts[2] slices, counts[3] selections rejected by the
+     * last fate_commit_advance. */
+    int32_t advance;
+    const uint8_t *status;    /* [N] stage status: FATE_PENDING .. FATE_COMMITTED */
+    const uint32_t *counts;   /* [4] device counters, see above */
 } fate_state_h;
 
 const char *fate_version(void);
@@ -218,6 +227,58 @@ fate_status_t fate_pack_state(const fate_dags_t *packed, const fate_dag_batch_t 
 fate_status_t fate_layout_state(const fate_dags_t *packed, const fate_dag_batch_t *dags,
                                 const fate_state_t *state, int32_t max_shard, void *h_buf, size_t bytes,
                                 fate_state_h *out);
+
+/* fate_pack_state_advance_size / fate_pack_state_advance: as
+ * fate_pack_state_size / fate_pack_state, but the packed state is a planning
+ * state that fate_commit_advance can update on the device, step after step:
+ * it carries the stage statuses, and its frontier, candidate, slice and
+ * completed-parent sections are sized for the largest possible frontier
+ * (every stage of the batch).  The handle's n_frontier, n_cand and n_slices
+ * are those capacities; the current counts are in the device array
+ * `counts` (see fate_state_h).  Scoring and top-k accept such a handle:
+ * their outputs are sized by the capacities, and slots past the current
+ * counts are left untouched.
+ * Errors: as fate_pack_state, plus ERANGE if the candidate capacity
+ * reaches 2^32. */
+fate_status_t fate_pack_state_advance_size(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                           const fate_state_t *state, int32_t max_shard, size_t *bytes);
+fate_status_t fate_pack_state_advance(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                      const fate_state_t *state, int32_t max_shard, void *d_buf, size_t bytes,
+                                      void *stream, fate_state_h *out);
+
+/* fate_commit_ws_size: device workspace bytes fate_commit_advance needs
+ * (about 16 bytes per stage).  Errors: EINVAL, ESTATE. */
+fate_status_t fate_commit_ws_size(const fate_dags_t *dags, const fate_state_h *state, size_t *bytes);
+
+/* fate_commit_advance: commit one planning step on the device and advance
+ * the planning state (Alg. 1: materialise the selected placements, then
+ * advance the frontier and update the planning state; Alg. 2: commit into
+ * the action pool and update the state as the stages complete).
+ *   d_sel[f * sel_stride], f < counts[0]: the candidate chosen for frontier
+ *     slot f (the local index fate_topk reports, so a top-k array with
+ *     sel_stride = k selects each stage's best candidate), or -1 to leave
+ *     the stage pending.  Device memory, read only.
+ * Per instance the selected stages are applied in ascending stage id, and on
+ * each device d of the chosen candidate S (k = |S|):
+ *   start = max(tau_d, t); the switch time kappa_switch(m(v), d) counts if
+ *   m(v) was not resident; m(v) is loaded (the smallest-id other models are
+ *   evicted while the weights exceed the capacity, as in the post-state of
+ *   fate_score_frontier); grp(v), if nonzero and absent, takes the first
+ *   empty prefix slot of d or, with all slots full, is appended after
+ *   dropping slot 0 (slots are kept oldest first); tau_d = start + c(v,d)/k
+ *   + switch.  Then v is completed and its output is held by exactly S.
+ * A selection past the stage's candidates, or whose candidate has a device
+ * that is not eligible or cannot hold the model, is skipped and counted in
+ * counts[3].  Afterwards the frontier (pending stages whose parents are all
+ * completed), candidate offsets, workgroup slices and completed-parent lists
+ * are rebuilt on the device.  t_now is unchanged.
+ * `state` must come from fate_pack_state_advance; its buffer is updated in
+ * place.  d_ws: at least fate_commit_ws_size bytes.  Enqueued on `stream`;
+ * does not synchronise.
+ * Errors: EINVAL (null pointers, sel_stride < 1, not a planning state),
+ * ESIZE (workspace), ESTATE, EHIP. */
+fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
+                                  int32_t sel_stride, void *d_ws, size_t ws_bytes, void *stream);
 
 /* fate_score_ws_size: device workspace bytes fate_score_frontier needs
  * (may be 0).  Errors: EINVAL, ESTATE. */

@@ -1,0 +1,60 @@
+// Device helpers shared by the scoring kernels and the commit-and-advance
+// kernels of libfate: bit tests, +infinity, the Load rule and the candidate
+// numbering of a frontier stage.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fate {
+
+__device__ __forceinline__ bool bit(uint64_t m, int i) { return (m >> i) & 1ull; }
+
+__device__ __forceinline__ float inf_f() { return __builtin_huge_valf(); }
+
+// Load of model m on a device of capacity `cap` (Sec. 3.2 future state, with
+// the eviction rule: add m, then drop the smallest-id other resident models
+// while the resident weights exceed the capacity).
+__device__ __forceinline__ uint64_t load_model(uint64_t res, int m, uint64_t cap, const uint64_t *weight) {
+    if (bit(res, m)) return res;
+    res |= 1ull << m;
+    uint64_t total = 0;
+    for (uint64_t t = res; t; t &= t - 1) total += weight[__builtin_ctzll(t)];
+    for (uint64_t t = res & ~(1ull << m); t && total > cap; t &= t - 1) {
+        const int i = __builtin_ctzll(t);
+        res &= ~(1ull << i);
+        total -= weight[i];
+    }
+    return res;
+}
+
+// Candidates of a stage with shard cap R (Sec. 3.3 shard slots): the D
+// single devices, then the windows {i..i+k-1}, k = 2..r, i = 0..D-k, with
+// r = min(R, max_shard, D).
+__device__ __forceinline__ int shard_cap_of(int R, int max_shard, int D) {
+    int r = R < max_shard ? R : max_shard;
+    r = r < D ? r : D;
+    return r < 1 ? 1 : r;
+}
+__device__ __forceinline__ int candidates_of(int r, int D) {
+    int c = D;
+    for (int k = 2; k <= r; ++k) c += D - k + 1;
+    return c;
+}
+// Candidate j -> first device i and size k.
+__device__ __forceinline__ void candidate_window(int j, int D, int &i, int &k) {
+    if (j < D) {
+        i = j;
+        k = 1;
+        return;
+    }
+    j -= D;
+    k = 2;
+    while (j >= D - k + 1) {
+        j -= D - k + 1;
+        ++k;
+    }
+    i = j;
+}
+
+}  // namespace fate

@@ -416,10 +416,14 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
 }
 
 struct StateLayout {
-    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_off, done, total;
+    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_off, done, status, counts, total;
 };
 
-StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS, int64_t nDone) {
+// Section sizes: nF frontier slots, nS slices, nDone completed-parent entries
+// (the exact counts, or the capacities of a planning state, which also
+// carries the stage statuses and the device counters).
+StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS, int64_t nDone,
+                         bool advance = false) {
     StateLayout L;
     size_t o = 0;
     L.resident = o; o = align_up(o + sizeof(uint64_t) * B * D);
@@ -432,8 +436,35 @@ StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS,
     L.slices = o; o = align_up(o + sizeof(uint32_t) * 3 * nS);
     L.done_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
     L.done = o; o = align_up(o + sizeof(fate::DoneParent) * nDone);
+    L.status = o;
+    if (advance) o = align_up(o + (size_t)N);
+    L.counts = o;
+    if (advance) o = align_up(o + 4 * sizeof(uint32_t));
     L.total = o;
     return L;
+}
+
+// Capacities of a planning state: every pending stage may join the frontier
+// later, every parent may complete.
+struct AdvanceCaps {
+    int64_t nF = 0, nC = 0, nS = 0, nDone = 0;
+};
+fate_status_t advance_caps(const fate_dags_t *pk, const fate_dag_batch_t *g, const fate_state_t *st,
+                           int max_shard, AdvanceCaps *c) {
+    const int64_t slice = fate::slice_len(pk->D);
+    for (int b = 0; b < pk->B; ++b) {
+        int64_t pend = 0;
+        for (int64_t s = g->stage_off[b]; s < g->stage_off[b + 1]; ++s) {
+            if (st->status[s] != FATE_PENDING) continue;
+            ++pend;
+            c->nC += candidates_of(shard_cap(g->shard_max[s], max_shard, pk->D), pk->D);
+        }
+        c->nF += pend;
+        c->nS += (pend + slice - 1) / slice;
+    }
+    c->nDone = pk->E;
+    if (c->nC >= (int64_t(1) << 32)) return FATE_ERANGE;
+    return FATE_OK;
 }
 
 void write_state_image(const fate_dags_t *pk, const fate_state_t *st, const StatePlan &p, const StateLayout &L,
@@ -449,6 +480,11 @@ void write_state_image(const fate_dags_t *pk, const fate_state_t *st, const Stat
     if (!p.slices.empty()) std::memcpy(img + L.slices, p.slices.data(), sizeof(uint32_t) * p.slices.size());
     std::memcpy(img + L.done_off, p.done_off.data(), sizeof(uint32_t) * p.done_off.size());
     if (!p.done.empty()) std::memcpy(img + L.done, p.done.data(), sizeof(fate::DoneParent) * p.done.size());
+    if (L.counts > L.status) {  // planning state
+        std::memcpy(img + L.status, st->status, (size_t)pk->N);
+        const uint32_t counts[4] = {(uint32_t)p.nF, (uint32_t)p.nC, (uint32_t)p.nS, 0u};
+        std::memcpy(img + L.counts, counts, sizeof(counts));
+    }
 }
 
 void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_shard, const StatePlan &p,
@@ -475,6 +511,16 @@ void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_sh
     out->n_done_edges = (int64_t)p.done.size();
     out->done_off = reinterpret_cast<const uint32_t *>(base + L.done_off);
     out->done = base + L.done;
+}
+
+void fill_advance_handle(const AdvanceCaps &c, const StateLayout &L, uint8_t *base, fate_state_h *out) {
+    out->n_frontier = c.nF;
+    out->n_cand = c.nC;
+    out->n_slices = c.nS;
+    out->n_done_edges = c.nDone;
+    out->advance = 1;
+    out->status = base + L.status;
+    out->counts = reinterpret_cast<const uint32_t *>(base + L.counts);
 }
 
 fate_status_t copy_to_device(void *d_buf, const void *h, size_t bytes, void *stream) {
@@ -613,12 +659,105 @@ fate_status_t fate_pack_state(const fate_dags_t *packed, const fate_dag_batch_t 
     return FATE_OK;
 }
 
+fate_status_t fate_pack_state_advance_size(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                           const fate_state_t *state, int32_t max_shard, size_t *bytes) {
+    if (!bytes) return FATE_EINVAL;
+    StatePlan p;
+    fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
+    if (st != FATE_OK) return st;
+    AdvanceCaps c;
+    st = advance_caps(packed, dags, state, max_shard, &c);
+    if (st != FATE_OK) return st;
+    *bytes = state_layout(packed->B, packed->D, state->K, packed->N, c.nF, c.nS, c.nDone, true).total;
+    return FATE_OK;
+}
+
+fate_status_t fate_pack_state_advance(const fate_dags_t *packed, const fate_dag_batch_t *dags,
+                                      const fate_state_t *state, int32_t max_shard, void *d_buf, size_t bytes,
+                                      void *stream, fate_state_h *out) {
+    if (!d_buf || !out) return FATE_EINVAL;
+    StatePlan p;
+    fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
+    if (st != FATE_OK) return st;
+    AdvanceCaps c;
+    st = advance_caps(packed, dags, state, max_shard, &c);
+    if (st != FATE_OK) return st;
+    const StateLayout L = state_layout(packed->B, packed->D, state->K, packed->N, c.nF, c.nS, c.nDone, true);
+    if (bytes < L.total) return FATE_ESIZE;
+    std::vector<uint8_t> img(L.total, 0);
+    write_state_image(packed, state, p, L, img.data());
+    st = copy_to_device(d_buf, img.data(), L.total, stream);
+    if (st != FATE_OK) return st;
+    fill_state_handle(packed, state, max_shard, p, L, static_cast<uint8_t *>(d_buf), bytes, out);
+    fill_advance_handle(c, L, static_cast<uint8_t *>(d_buf), out);
+    return FATE_OK;
+}
+
 static fate_status_t check_pair(const fate_dags_t *dags, const fate_state_h *state) {
     if (!dags || !state) return FATE_EINVAL;
     if (dags->B != state->B || dags->D != state->D || dags->N != state->N) return FATE_ESTATE;
     if (!dags->records || !state->frontier || !state->cand_off || !state->slices || !state->done_off)
         return FATE_EINVAL;
     return FATE_OK;
+}
+
+fate_status_t fate_commit_ws_size(const fate_dags_t *dags, const fate_state_h *state, size_t *bytes) {
+    if (!bytes) return FATE_EINVAL;
+    fate_status_t st = check_pair(dags, state);
+    if (st != FATE_OK) return st;
+    if (!state->advance) return FATE_EINVAL;
+    *bytes = fate::commit_ws_layout(state->N, state->B).total;
+    return FATE_OK;
+}
+
+fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
+                                  int32_t sel_stride, void *d_ws, size_t ws_bytes, void *stream) {
+    fate_status_t st = check_pair(dags, state);
+    if (st != FATE_OK) return st;
+    if (!state->advance || !state->status || !state->counts || sel_stride < 1) return FATE_EINVAL;
+    if (state->n_frontier > 0 && !d_sel) return FATE_EINVAL;
+    const fate::CommitWs W = fate::commit_ws_layout(state->N, state->B);
+    if (ws_bytes < W.total) return FATE_ESIZE;
+    if (W.total > 0 && !d_ws) return FATE_EINVAL;
+    uint8_t *ws = static_cast<uint8_t *>(d_ws);
+    fate::CommitLaunch a;
+    a.rec = static_cast<const StageRec *>(dags->records);
+    a.par_idx = dags->par_idx;
+    a.stage_off = dags->stage_off;
+    a.exec = dags->exec;
+    a.ksw = dags->switch_s;
+    a.weight = dags->weight;
+    a.cap = dags->cap;
+    a.fits = dags->fits;
+    // the planning state's buffer is the caller's, handed over for update
+    a.resident = const_cast<uint64_t *>(state->resident);
+    a.pcache = const_cast<uint64_t *>(state->prefix_cache);
+    a.holders = const_cast<uint64_t *>(state->holders);
+    a.tau = const_cast<float *>(state->tau_free);
+    a.tnow = state->t_now;
+    a.status = const_cast<uint8_t *>(state->status);
+    a.frontier = const_cast<uint32_t *>(state->frontier);
+    a.cand_off = const_cast<uint32_t *>(state->cand_off);
+    a.slices = const_cast<uint32_t *>(state->slices);
+    a.done_off = const_cast<uint32_t *>(state->done_off);
+    a.done = static_cast<fate::DoneParent *>(const_cast<void *>(state->done));
+    a.counts = const_cast<uint32_t *>(state->counts);
+    a.sel = d_sel;
+    a.sel_stride = sel_stride;
+    a.cp = reinterpret_cast<uint32_t *>(ws + W.cp);
+    a.nc = reinterpret_cast<uint32_t *>(ws + W.nc);
+    a.fidx = reinterpret_cast<uint32_t *>(ws + W.fidx);
+    a.bsum = reinterpret_cast<uint32_t *>(ws + W.bsum);
+    a.rej = reinterpret_cast<uint32_t *>(ws + W.rej);
+    a.N = state->N;
+    a.B = state->B;
+    a.D = dags->D;
+    a.M = dags->M;
+    a.K = state->K;
+    a.max_shard = state->max_shard;
+    a.slice = fate::slice_len(dags->D);
+    a.nblk = (int32_t)((state->N + fate::kPlanStages - 1) / fate::kPlanStages);
+    return fate::launch_commit(a, stream) == 0 ? FATE_OK : FATE_EHIP;
 }
 
 fate_status_t fate_score_ws_size(const fate_dags_t *dags, const fate_state_h *state, size_t *bytes) {
@@ -661,6 +800,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.done_off = state->done_off;
     a.done = static_cast<const fate::DoneParent *>(state->done);
     a.scores = d_scores;
+    a.dcounts = state->advance ? state->counts : nullptr;
     a.topk = k;
     a.tk_idx = d_idx;
     a.tk_val = d_val;
@@ -714,6 +854,7 @@ fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_
     a.scores = d_scores;
     a.idx = d_idx;
     a.val = d_val;
+    a.dcounts = state->advance ? state->counts : nullptr;
     a.nF = state->n_frontier;
     a.D = state->D;
     a.k = k;

@@ -55,6 +55,7 @@ struct ScoreLaunch {
     const uint32_t *done_off;
     const DoneParent *done;
     float *scores;
+    const uint32_t *dcounts;  // planning state: counts[2] = current slices, else null
     int32_t *tk_idx;  // fused top-k outputs (topk > 0), [nF][topk]
     float *tk_val;
     int32_t topk;
@@ -69,9 +70,54 @@ struct TopkLaunch {
     const float *scores;
     int32_t *idx;
     float *val;
-    int64_t nF;
+    const uint32_t *dcounts;  // planning state: counts[0] = current frontier size, else null
+    int64_t nF;               // frontier size, or its capacity with dcounts
     int32_t D, k;
 };
+
+// Commit-and-advance of a planning state (fate_commit.hip).
+struct CommitLaunch {
+    // packed DAGs
+    const StageRec *rec;
+    const uint32_t *par_idx;
+    const int64_t *stage_off;
+    const float *exec, *ksw;
+    const uint64_t *weight, *cap, *fits;
+    // planning state, updated in place
+    uint64_t *resident, *pcache, *holders;
+    float *tau;
+    const float *tnow;
+    uint8_t *status;
+    uint32_t *frontier, *cand_off, *slices, *done_off;
+    DoneParent *done;
+    uint32_t *counts;
+    // selections: sel[f * sel_stride] for frontier slot f
+    const int32_t *sel;
+    int32_t sel_stride;
+    // workspace (commit_ws_layout)
+    uint32_t *cp, *nc, *fidx, *bsum, *rej;
+    int64_t N;
+    int32_t B, D, M, K, max_shard, slice, nblk;
+};
+
+// Stages per workgroup of the planning scans, and the workspace layout.
+constexpr int kPlanBlock = 256, kPlanItems = 4, kPlanStages = kPlanBlock * kPlanItems;
+struct CommitWs {
+    size_t cp, nc, fidx, bsum, rej, total;
+};
+inline CommitWs commit_ws_layout(int64_t N, int B) {
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    const int64_t nblk = (N + kPlanStages - 1) / kPlanStages;
+    CommitWs w;
+    size_t o = 0;
+    w.cp = o; o = up(o + 4 * (size_t)N);
+    w.nc = o; o = up(o + 4 * (size_t)N);
+    w.fidx = o; o = up(o + 4 * ((size_t)N + 1));
+    w.bsum = o; o = up(o + 12 * (size_t)nblk);
+    w.rej = o; o = up(o + 4 * ((size_t)B + 1));
+    w.total = o;
+    return w;
+}
 
 // Lane-group width for D devices (power of two, 4..64) and the number of
 // frontier stages per scoring workgroup slice (eight rounds of its groups).
@@ -89,5 +135,6 @@ inline int slice_len(int D) {
 // Kernel launchers (fate_kernels.hip).  Return a hipError_t as int.
 int launch_score(const ScoreLaunch &a, void *stream);
 int launch_topk(const TopkLaunch &a, void *stream);
+int launch_commit(const CommitLaunch &a, void *stream);  // fate_commit.hip
 
 }  // namespace fate

@@ -35,30 +35,13 @@
 
 #include <type_traits>
 
+#include "fate_device.h"
 #include "fate_internal.h"
 
 namespace fate {
 namespace {
 
 constexpr int kBlock = kScoreBlock;
-
-__device__ __forceinline__ bool bit(uint64_t m, int i) { return (m >> i) & 1ull; }
-
-__device__ __forceinline__ float inf_f() { return __builtin_huge_valf(); }
-
-// Model load under capacity (post-state of a device receiving v).
-__device__ __forceinline__ uint64_t load_model(uint64_t res, int m, uint64_t cap, const uint64_t *weight) {
-    if (bit(res, m)) return res;
-    res |= 1ull << m;
-    uint64_t total = 0;
-    for (uint64_t t = res; t; t &= t - 1) total += weight[__builtin_ctzll(t)];
-    for (uint64_t t = res & ~(1ull << m); t && total > cap; t &= t - 1) {
-        const int i = __builtin_ctzll(t);
-        res &= ~(1ull << i);
-        total -= weight[i];
-    }
-    return res;
-}
 
 // Cheapest transfer coefficient into device d from any device holding an output.
 __device__ __forceinline__ float min_beta_into(const float *beta, uint64_t holders, int d, int D) {
@@ -513,6 +496,9 @@ __device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, fl
 template <int G, bool UNI, bool SLOTS>
 __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     static_assert(!SLOTS || (UNI && G == 16), "the slot layout needs 16-lane groups and uniform beta");
+    // a planning state is launched over its slice capacity; the current
+    // number of slices is on the device
+    if (a.dcounts && blockIdx.x >= a.dcounts[2]) return;
     extern __shared__ uint64_t smem[];
     uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
     const int tid = threadIdx.x;
@@ -1075,6 +1061,7 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
     constexpr int kGroups = kBlock / G;
     const int tid = threadIdx.x;
     const int lane = tid & (G - 1);
+    const int64_t nF = a.dcounts ? (int64_t)a.dcounts[0] : a.nF;  // planning state: current frontier
     uint32_t c0[kTopkRounds];
     int C[kTopkRounds];
     int64_t f[kTopkRounds];
@@ -1082,7 +1069,7 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
     for (int r = 0; r < kTopkRounds; ++r) {  // round r: the block's groups take consecutive stages
         const int64_t fr = ((int64_t)blockIdx.x * kTopkRounds + r) * kGroups + tid / G;
         c0[r] = 0; C[r] = 0; f[r] = -1;
-        if (fr < a.nF) {
+        if (fr < nF) {
             c0[r] = a.cand_off[fr];
             C[r] = (int)(a.cand_off[fr + 1] - c0[r]);
             f[r] = fr;

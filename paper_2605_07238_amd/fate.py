@@ -22,13 +22,15 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libfate.so")
 
 FATE_OK = 0
+FATE_EINVAL, FATE_ERANGE, FATE_ECYCLE, FATE_ENOFEAS, FATE_ESIZE, FATE_ESTATE, FATE_EHIP = -1, -2, -3, -4, -5, -6, -7
 STATUS_NAMES = {0: "FATE_OK", -1: "FATE_EINVAL", -2: "FATE_ERANGE", -3: "FATE_ECYCLE", -4: "FATE_ENOFEAS",
                 -5: "FATE_ESIZE", -6: "FATE_ESTATE", -7: "FATE_EHIP"}
 
 # Every symbol declared in include/fate.h.
 EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_dags", "fate_layout_dags",
            "fate_pack_state_size", "fate_pack_state", "fate_layout_state", "fate_score_ws_size",
-           "fate_score_frontier", "fate_score_topk", "fate_topk"]
+           "fate_score_frontier", "fate_score_topk", "fate_topk", "fate_pack_state_advance_size",
+           "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance"]
 
 
 class FateError(RuntimeError):
@@ -78,7 +80,8 @@ class StateH(C.Structure):
                 ("tau_free", C.c_void_p), ("t_now", C.c_void_p),
                 ("frontier", C.c_void_p), ("cand_off", C.c_void_p),
                 ("n_slices", C.c_int64), ("slices", C.c_void_p),
-                ("n_done_edges", C.c_int64), ("done_off", C.c_void_p), ("done", C.c_void_p)]
+                ("n_done_edges", C.c_int64), ("done_off", C.c_void_p), ("done", C.c_void_p),
+                ("advance", C.c_int32), ("status", C.c_void_p), ("counts", C.c_void_p)]
 
 
 _lib = None
@@ -112,6 +115,12 @@ def load(path: Optional[str] = None):
     lib.fate_score_topk.argtypes = [P(Dags), P(StateH), P(Params), C.c_void_p, C.c_int64, C.c_int32, C.c_void_p,
                                     C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
     lib.fate_topk.argtypes = [P(StateH), C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
+    lib.fate_pack_state_advance_size.argtypes = [P(Dags), P(DagBatch), P(State), C.c_int32, P(C.c_size_t)]
+    lib.fate_pack_state_advance.argtypes = [P(Dags), P(DagBatch), P(State), C.c_int32, C.c_void_p, C.c_size_t,
+                                            C.c_void_p, P(StateH)]
+    lib.fate_commit_ws_size.argtypes = [P(Dags), P(StateH), P(C.c_size_t)]
+    lib.fate_commit_advance.argtypes = [P(Dags), P(StateH), C.c_void_p, C.c_int32, C.c_void_p, C.c_size_t,
+                                        C.c_void_p]
     for name in EXPORTS[2:]:
         getattr(lib, name).restype = st
     if path is None:
@@ -192,6 +201,21 @@ class PackedState:
     def n_cand(self) -> int:
         return int(self.handle.n_cand)
 
+    @property
+    def advance(self) -> bool:
+        return bool(self.handle.advance)
+
+    def counts(self):
+        """Current (frontier stages, candidates, slices, rejected selections):
+        read from the device for a planning state (synchronises)."""
+        import torch
+        h = self.handle
+        if not h.advance:
+            return int(h.n_frontier), int(h.n_cand), int(h.n_slices), 0
+        off = h.counts - self.buf.data_ptr()
+        c = self.buf[off:off + 16].view(torch.int32).cpu().numpy().astype(np.int64)
+        return int(c[0]), int(c[1]), int(c[2]), int(c[3])
+
 
 def fate_pack_dags_size(w, H: int) -> int:
     hi = HostInputs(w)
@@ -231,13 +255,23 @@ def fate_layout_dags(w, H: Optional[int] = None):
 
 
 def fate_pack_state(packed: PackedDags, w, max_shard: Optional[int] = None, device="cuda",
-                    stream=None) -> PackedState:
-    """Validate the state of ``w`` against ``packed`` and pack state + frontier."""
+                    stream=None, advance: bool = False) -> PackedState:
+    """Validate the state of ``w`` against ``packed`` and pack state + frontier.
+    ``advance`` packs a planning state for fate_commit_advance."""
     import torch
     ms = int(w.max_shard if max_shard is None else max_shard)
     lib = load()
     hi = HostInputs(w)
     nbytes = C.c_size_t(0)
+    if advance:
+        _check(lib.fate_pack_state_advance_size(C.byref(packed.handle), C.byref(hi.batch), C.byref(hi.state), ms,
+                                                C.byref(nbytes)), "fate_pack_state_advance_size")
+        buf = torch.empty(max(1, nbytes.value), dtype=torch.uint8, device=device)
+        h = StateH()
+        _check(lib.fate_pack_state_advance(C.byref(packed.handle), C.byref(hi.batch), C.byref(hi.state), ms,
+                                           C.c_void_p(buf.data_ptr()), nbytes.value,
+                                           C.c_void_p(_stream_ptr(stream)), C.byref(h)), "fate_pack_state_advance")
+        return PackedState(buf, h, hi)
     nf, nc = C.c_int64(0), C.c_int64(0)
     _check(lib.fate_pack_state_size(C.byref(packed.handle), C.byref(hi.batch), C.byref(hi.state), ms,
                                     C.byref(nbytes), C.byref(nf), C.byref(nc)), "fate_pack_state_size")
@@ -332,11 +366,59 @@ def fate_topk(state: PackedState, scores, k: int, idx=None, val=None, stream=Non
     return idx[:F], val[:F]
 
 
+def fate_commit_ws_size(packed: PackedDags, state: PackedState) -> int:
+    ws = C.c_size_t(0)
+    _check(load().fate_commit_ws_size(C.byref(packed.handle), C.byref(state.handle), C.byref(ws)),
+           "fate_commit_ws_size")
+    return int(ws.value)
+
+
+def fate_commit_advance(packed: PackedDags, state: PackedState, sel, ws=None, stream=None):
+    """Commit the candidate chosen per frontier slot and advance the planning
+    state on the device.  ``sel``: int32 device tensor [F] or [F, k] (a top-k
+    array: its first column is used), -1 = leave pending.  Returns ``ws``."""
+    import torch
+    lib = load()
+    if sel.dtype != torch.int32 or not sel.is_contiguous():
+        raise ValueError("sel must be a contiguous int32 tensor")
+    stride = int(sel.shape[1]) if sel.dim() == 2 else 1
+    nbytes = fate_commit_ws_size(packed, state)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=packed.buf.device)
+    _check(lib.fate_commit_advance(C.byref(packed.handle), C.byref(state.handle), C.c_void_p(sel.data_ptr()),
+                                   stride, C.c_void_p(ws.data_ptr()), nbytes, C.c_void_p(_stream_ptr(stream))),
+           "fate_commit_advance")
+    return ws
+
+
+def state_arrays(state: PackedState):
+    """Host copies of the packed state arrays: resident [B, D], prefix slots
+    [B, D, K], holders [N], free times [B, D], and (planning state) status [N]."""
+    import torch
+    h = state.handle
+    base = state.buf.data_ptr()
+    B, D, K, N = int(h.B), int(h.D), int(h.K), int(h.N)
+
+    def take(ptr, n, dt):
+        off = ptr - base
+        nb = n * np.dtype(dt).itemsize
+        if n == 0:
+            return np.zeros(0, dt)
+        return state.buf[off:off + nb].cpu().numpy().view(dt).copy()
+
+    out = dict(resident=take(h.resident, B * D, np.uint64).reshape(B, D),
+               prefix_cache=take(h.prefix_cache, B * D * K, np.uint64).reshape(B, D, K),
+               holders=take(h.holders, N, np.uint64), tau_free=take(h.tau_free, B * D, np.float32).reshape(B, D))
+    if h.advance:
+        out["status"] = take(h.status, N, np.uint8)
+    return out
+
+
 def frontier_table(state: PackedState):
     """Host copies of the packed frontier: (flat stage ids, instances, cand_off)."""
     import torch
     h = state.handle
-    F = int(h.n_frontier)
+    F = state.counts()[0]
     base = state.buf.data_ptr()
     off_f = h.frontier - base
     off_c = h.cand_off - base

@@ -1,0 +1,238 @@
+"""Commit-and-advance on the GPU against the oracle (step 11), step by step.
+
+Each step selects, for every frontier stage, the oracle's best candidate (so
+no input of the oracle comes from the HIP path), commits it on the GPU with
+fate_commit_advance and in the oracle with oracle.commit, and compares:
+the state arrays (bit-exact, free times included: both sides sum them in
+fp64 and round once to fp32), the rebuilt frontier, candidate offsets, slices and
+completed-parent lists (against the host packer run on the oracle's new
+state), and the next step's scores (within the scoring tolerance).
+"""
+
+import numpy as np
+import pytest
+
+from gpu_util import RTOL
+from oracle import oracle
+from paper_2605_07238_amd import fate, parity, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _sections(st):
+    """Device planning-state sections as host arrays, cut to the current counts."""
+    import torch
+    h = st.handle
+    nF, nC, nS, rej = st.counts()
+    base = st.buf.data_ptr()
+
+    def take(ptr, n, dt=np.uint32):
+        off = ptr - base
+        nb = n * np.dtype(dt).itemsize
+        return st.buf[off:off + nb].cpu().numpy().view(dt).copy() if n else np.zeros(0, dt)
+
+    N = int(h.N)
+    done_off = take(h.done_off, N + 1)
+    done = take(h.done, 4 * int(done_off[-1])).reshape(-1, 4)
+    return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
+                slices=take(h.slices, 3 * nS).reshape(nS, 3), done_off=done_off, done=done,
+                counts=(nF, nC, nS, rej))
+
+
+def _host_sections(pk, w):
+    """The same sections from the host packer (fate_layout_state) for state w."""
+    buf, h, hi = fate.fate_layout_state(pk.handle, w)
+    base = buf.ctypes.data
+    nF, nS, N = int(h.n_frontier), int(h.n_slices), int(h.N)
+
+    def take(ptr, n, dt=np.uint32):
+        return np.frombuffer(buf, dt, n, ptr - base).copy() if n else np.zeros(0, dt)
+
+    done_off = take(h.done_off, N + 1)
+    return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
+                slices=take(h.slices, 3 * nS).reshape(nS, 3), done_off=done_off,
+                done=take(h.done, 4 * int(done_off[-1])).reshape(-1, 4), n_cand=int(h.n_cand))
+
+
+def _compare_state(st, w_ref, tau_ref):
+    got = fate.state_arrays(st)
+    assert np.array_equal(got["resident"], w_ref.resident.reshape(got["resident"].shape)), "resident models"
+    assert np.array_equal(got["prefix_cache"], w_ref.prefix_cache.reshape(got["prefix_cache"].shape)), "prefix slots"
+    assert np.array_equal(got["holders"], w_ref.holders), "holders"
+    assert np.array_equal(got["status"], w_ref.status), "status"
+    # both sides sum a step's free times in fp64 and round once to the
+    # state's fp32, so they agree bit for bit
+    ref = np.asarray(tau_ref, np.float64).astype(np.float32).reshape(got["tau_free"].shape)
+    assert np.array_equal(got["tau_free"].view(np.uint32), ref.view(np.uint32)), \
+        "free times: max err %.3g" % np.abs(got["tau_free"].astype(np.float64) - ref).max()
+
+
+def _compare_sections(pk, st, w_ref):
+    dev = _sections(st)
+    host = _host_sections(pk, w_ref)
+    nF, nC, nS, _ = dev["counts"]
+    assert np.array_equal(dev["frontier"], host["frontier"]), "frontier"
+    assert np.array_equal(dev["cand_off"], host["cand_off"]), "candidate offsets"
+    assert nC == host["n_cand"]
+    assert np.array_equal(dev["slices"], host["slices"]), "slices"
+    assert np.array_equal(dev["done_off"], host["done_off"]), "completed-parent offsets"
+    assert np.array_equal(dev["done"][:, :3], host["done"][:, :3]), "completed-parent entries"
+
+
+def _score_and_check(pk, st, w, params=None):
+    """GPU scores of the planning state against the oracle on state w."""
+    import torch
+    p = fate.make_params(w, **(params or {}))
+    scores = fate.fate_score_frontier(pk, st, p)
+    torch.cuda.synchronize()
+    nF, nC = st.counts()[:2]
+    ref = oracle.score(w, params=params)
+    fv, fb, co = fate.frontier_table(st)
+    flat = w.stage_off[ref["front_b"]] + ref["front_v"]
+    assert np.array_equal(fv, flat), "frontier differs from the oracle's"
+    assert np.array_equal(co, ref["cand_off"]), "candidate offsets differ from the oracle's"
+    err, nbad, ninf = parity.compare(scores[:nC].cpu().numpy(), ref["psi"], ref["mag"], RTOL)
+    assert ninf == 0 and nbad == 0, "scores after commit: %d bad (max rel err %.3g), %d -inf mismatches" % (
+        nbad, err, ninf)
+    return ref
+
+
+def _run_steps(w, steps, params=None, sel_fn=None):
+    import torch
+    pk = fate.fate_pack_dags(w)
+    st = fate.fate_pack_state(pk, w, advance=True)
+    cur = w
+    ws = None
+    for step in range(steps):
+        print("[gpu] commit step", step, "frontier", st.counts()[0], flush=True)
+        ref = _score_and_check(pk, st, cur, params)
+        if len(ref["front_v"]) == 0:
+            break
+        idx, _ = oracle.topk(ref, 1)
+        sel = idx[:, 0] if sel_fn is None else sel_fn(ref, idx[:, 0])
+        nxt, tau, rej = oracle.commit(cur, sel)
+        d_sel = torch.from_numpy(np.ascontiguousarray(sel, np.int32)).cuda()
+        ws = fate.fate_commit_advance(pk, st, d_sel, ws=ws)
+        torch.cuda.synchronize()
+        assert st.counts()[3] == rej, (st.counts(), rej)
+        _compare_state(st, nxt, tau)
+        _compare_sections(pk, st, nxt)
+        cur = nxt
+    return pk, st, cur
+
+
+CASES = [
+    ("d4-windows", dict(seed=3, D=4, n=24, M=3, max_shard=3, shard_frac=0.6), 5),
+    ("d6-nonuniform", dict(seed=5, D=6, n=24, M=5, K=3, max_shard=3, shard_frac=0.5), 6),
+    ("d16-uniform", dict(seed=7, D=16, n=30, M=8, K=4, max_shard=4, shard_frac=0.5, uniform_beta=True), 6),
+    ("d13-dense", dict(seed=11, D=13, n=30, M=6, p_edge=0.5, uniform_beta=True), 6),
+    ("d40", dict(seed=13, D=40, n=20, M=6, K=2), 4),
+    ("d2-chains", dict(seed=17, D=2, n=30, p_edge=0.2), 8),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_commit_steps_match_oracle(case):
+    _, spec, steps = case
+    spec = dict(spec)
+    w = synth.make_random_small(spec.pop("seed"), B=3, H=2, **spec)
+    _run_steps(w, steps)
+
+
+def test_commit_until_done():
+    """Commit best candidates until the frontier is empty: every pending stage
+    completes and the planning state agrees with the oracle at every step."""
+    w = synth.make_random_small(23, B=2, n=16, D=5, M=4, max_shard=2, shard_frac=0.4)
+    pk, st, cur = _run_steps(w, 40)
+    assert st.counts()[0] == 0
+    # what stays pending waits on a running or committed stage, which the
+    # planning state never completes
+    npar = np.diff(w.par_off)
+    inst = np.repeat(np.arange(w.B), np.diff(w.stage_off))
+    for g in np.nonzero(cur.status == 0)[0]:
+        pars = w.par_idx[w.par_off[g]:w.par_off[g + 1]].astype(np.int64) + w.stage_off[inst[g]]
+        assert npar[g] > 0 and np.any(cur.status[pars] != 1), g
+    assert np.count_nonzero(cur.status == 1) > np.count_nonzero(w.status == 1)
+
+
+@pytest.mark.parametrize("name", ["shards-1024x500-d16", "forkjoin-4096x1000-d16", "layered-1024x200-d8"])
+def test_commit_recipes(name):
+    w = synth.make_workload(name, B=12)
+    _run_steps(w, 3)
+
+
+def test_commit_partial_and_rejected_selections():
+    """Stages left at -1 stay pending; out-of-range and infeasible selections
+    are rejected, counted and change nothing."""
+    w = synth.make_random_small(29, B=3, n=24, D=6, M=4, max_shard=3, shard_frac=0.6)
+
+    def mixed(ref, best):
+        sel = best.copy()
+        co = ref["cand_off"]
+        for f in range(len(sel)):
+            if f % 3 == 1:
+                sel[f] = -1
+            elif f % 3 == 2:
+                sel[f] = int(co[f + 1] - co[f]) + 5  # past the last candidate
+        return sel
+
+    _run_steps(w, 3, sel_fn=mixed)
+
+
+def test_commit_top_k_array_as_selection():
+    """A [F, k] selection array is read through its first column."""
+    import torch
+    w = synth.make_random_small(31, B=2, n=20, D=8, M=4, max_shard=2, shard_frac=0.5)
+    pk = fate.fate_pack_dags(w)
+    st = fate.fate_pack_state(pk, w, advance=True)
+    ref = oracle.score(w)
+    idx, _ = oracle.topk(ref, 1)
+    sel2 = np.full((len(idx), 3), 12345, np.int32)  # columns 1, 2 would be rejected if read
+    sel2[:, 0] = idx[:, 0]
+    nxt, tau, rej = oracle.commit(w, idx[:, 0])
+    fate.fate_commit_advance(pk, st, torch.from_numpy(sel2).cuda())
+    torch.cuda.synchronize()
+    assert st.counts()[3] == 0
+    _compare_state(st, nxt, tau)
+
+
+def test_commit_nothing_keeps_everything():
+    import torch
+    w = synth.make_random_small(37, B=2, n=20, D=6, M=4, max_shard=3, shard_frac=0.5)
+    pk = fate.fate_pack_dags(w)
+    st = fate.fate_pack_state(pk, w, advance=True)
+    before = _sections(st)
+    arrays = fate.state_arrays(st)
+    sel = torch.full((max(1, st.counts()[0]),), -1, dtype=torch.int32, device="cuda")
+    fate.fate_commit_advance(pk, st, sel)
+    torch.cuda.synchronize()
+    after = _sections(st)
+    for k in ("frontier", "cand_off", "slices", "done_off", "done"):
+        assert np.array_equal(before[k], after[k]), k
+    now = fate.state_arrays(st)
+    for k, v in arrays.items():
+        assert np.array_equal(v, now[k]), k
+
+
+def test_planning_state_scores_and_topk_match_plain_state():
+    """Scoring, top-k and the fused call on a planning state write the same
+    bits as on the plainly packed state."""
+    import torch
+    w = synth.make_random_small(41, B=3, n=24, D=8, M=4, max_shard=3, shard_frac=0.5)
+    pk = fate.fate_pack_dags(w)
+    st0 = fate.fate_pack_state(pk, w)
+    st1 = fate.fate_pack_state(pk, w, advance=True)
+    p = fate.make_params(w)
+    nF, nC = st0.n_frontier, st0.n_cand
+    assert st1.counts()[:2] == (nF, nC)
+    s0 = fate.fate_score_frontier(pk, st0, p)
+    s1 = fate.fate_score_frontier(pk, st1, p)
+    i0, v0 = fate.fate_topk(st0, s0, 3)
+    i1, v1 = fate.fate_topk(st1, s1, 3)
+    f1, fi1, fv1 = fate.fate_score_topk(pk, st1, p, 3)
+    torch.cuda.synchronize()
+    assert np.array_equal(s0[:nC].cpu().numpy().view(np.uint32), s1[:nC].cpu().numpy().view(np.uint32))
+    assert np.array_equal(i0.cpu().numpy(), i1[:nF].cpu().numpy())
+    assert np.array_equal(v0.cpu().numpy().view(np.uint32), v1[:nF].cpu().numpy().view(np.uint32))
+    assert np.array_equal(i0.cpu().numpy(), fi1[:nF].cpu().numpy())
+    assert np.array_equal(s0[:nC].cpu().numpy().view(np.uint32), f1[:nC].cpu().numpy().view(np.uint32))

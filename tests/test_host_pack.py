@@ -235,3 +235,27 @@ def test_workload_save_load_roundtrip(tmp_path):
         a, b = getattr(w, f), getattr(v, f)
         assert a.dtype == b.dtype and np.array_equal(a, b), f
     assert (w.name, w.D, w.M, w.K, w.H, w.max_shard, w.params) == (v.name, v.D, v.M, v.K, v.H, v.max_shard, v.params)
+
+
+def test_planning_state_size_and_commit_errors():
+    """Host side of the planning state: its capacity sizing, and the commit
+    entry points refusing a plainly packed state (no HIP call is made)."""
+    import ctypes as C
+    w = synth.make_random_small(3, B=3, n=20, D=6)
+    lib = fate.load()
+    buf, h, hi = fate.fate_layout_dags(w)
+    sbuf, sh, shi = fate.fate_layout_state(h, w)
+    plain = C.c_size_t(0)
+    nf, nc = C.c_int64(0), C.c_int64(0)
+    assert lib.fate_pack_state_size(C.byref(h), C.byref(shi.batch), C.byref(shi.state), w.max_shard,
+                                    C.byref(plain), C.byref(nf), C.byref(nc)) == 0
+    adv = C.c_size_t(0)
+    assert lib.fate_pack_state_advance_size(C.byref(h), C.byref(shi.batch), C.byref(shi.state), w.max_shard,
+                                            C.byref(adv)) == 0
+    assert adv.value > plain.value
+    assert lib.fate_pack_state_advance_size(C.byref(h), C.byref(shi.batch), C.byref(shi.state), w.max_shard,
+                                            None) == fate.FATE_EINVAL
+    ws = C.c_size_t(0)
+    assert sh.advance == 0
+    assert lib.fate_commit_ws_size(C.byref(h), C.byref(sh), C.byref(ws)) == fate.FATE_EINVAL
+    assert lib.fate_commit_advance(C.byref(h), C.byref(sh), None, 1, None, 0, None) == fate.FATE_EINVAL
