@@ -154,6 +154,69 @@ def cpu_baseline(w, H, min_seconds=10.0, max_passes=50):
     return total / passes, passes, threads
 
 
+def commit_bytes(pk, st):
+    """Algorithmic bytes of one commit-and-advance on the device, counted from
+    the planning state it produced: every stage's record and status and its
+    parents' statuses are read; the completed-parent lists, frontier,
+    candidate offsets and slices are written; each (instance, device) state
+    word, free time and prefix slots are read and written; each frontier
+    slot and its selection are read once."""
+    import torch
+    h, d = st.handle, pk.handle
+    N, E, B, D, K = int(h.N), int(d.E), int(h.B), int(h.D), int(h.K)
+    nF, nC, nS, _ = st.counts()
+    base = st.buf.data_ptr()
+    off = h.done_off - base
+    n_done = int(st.buf[off + 4 * N:off + 4 * N + 4].view(torch.int32).cpu().item())
+    return (32 * N + N + E * (4 + 1)          # records, statuses, parent ids and statuses
+            + 4 * (N + 1) + 16 * n_done       # completed-parent offsets and entries
+            + 12 * (nF + 1) + 12 * nS         # frontier, candidate offsets, slices
+            + 2 * B * D * (8 + 4 + 8 * K)     # resident models, free times, prefix slots
+            + 4 * B + 16)
+
+
+def planning_loop(w, pk, params, k, steps, log):
+    """Repeated planning steps on the device: score, top-k, then commit each
+    frontier stage's best candidate; per-step kernel times from HIP events."""
+    import torch
+    from paper_2605_07238_amd import fate
+    st = fate.fate_pack_state(pk, w, advance=True)
+    scores = torch.empty(max(1, st.n_cand), dtype=torch.float32, device="cuda")
+    idx = torch.empty((max(1, st.n_frontier), k), dtype=torch.int32, device="cuda")
+    val = torch.empty((max(1, st.n_frontier), k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(1, fate.fate_commit_ws_size(pk, st)), dtype=torch.uint8, device="cuda")
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    rows = []
+    for i in range(steps):
+        nF0 = st.counts()[0]
+        e = [mk() for _ in range(4)]
+        e[0].record()
+        fate.fate_score_frontier(pk, st, params, out=scores)
+        e[1].record()
+        fate.fate_topk(st, scores, k, idx=idx, val=val)
+        e[2].record()
+        fate.fate_commit_advance(pk, st, idx, ws=ws)
+        e[3].record()
+        torch.cuda.synchronize()
+        nF1 = st.counts()[0]
+        cb = commit_bytes(pk, st)
+        row = dict(frontier=nF0, next_frontier=nF1, score_ms=e[0].elapsed_time(e[1]),
+                   topk_ms=e[1].elapsed_time(e[2]), commit_ms=e[2].elapsed_time(e[3]), commit_bytes=cb)
+        rows.append(row)
+        log("planning step %d: frontier %d -> %d, score %.4f ms, top-k %.4f ms, commit %.4f ms"
+            % (i, nF0, nF1, row["score_ms"], row["topk_ms"], row["commit_ms"]))
+        if nF1 == 0:
+            break
+    cms = [r["commit_ms"] for r in rows[1:]] or [rows[0]["commit_ms"]]  # the first launch warms up
+    cbs = [r["commit_bytes"] for r in rows[1:]] or [rows[0]["commit_bytes"]]
+    achieved = float(np.mean(cbs)) / (float(np.mean(cms)) * 1e-3) / 1e9
+    return dict(steps=rows, commit_ms_mean=float(np.mean(cms)),
+                stages_committed_per_s=float(sum(r["frontier"] for r in rows[1:]) / (sum(cms) * 1e-3))
+                if len(rows) > 1 else None,
+                commit_roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                 "frac": achieved / HBM_PEAK_GBS, "kernels": "fate_commit_advance (5 launches)"})
+
+
 def describe(k):
     """Per-recipe sizes of one planning step (one JSON line each)."""
     import torch
@@ -192,6 +255,9 @@ def main():
     ap.add_argument("--fused", action="store_true",
                     help="time fate_score_topk (one launch) instead of fate_score_frontier + fate_topk")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--planning-steps", type=int, default=6,
+                    help="after the timed steps, run this many score / top-k / commit-and-advance planning steps "
+                         "on a planning state and report them (0 = skip)")
     ap.add_argument("--no-medians", action="store_true",
                     help="skip the extra median timings of the three launch variants (profiling runs)")
     ap.add_argument("--describe", action="store_true",
@@ -351,6 +417,8 @@ def main():
             "kernel": "k_score (with top-k epilogue)" if args.fused else "k_score",
         },
     }
+    if args.planning_steps > 0:
+        out["planning_loop"] = planning_loop(w, pk, params, args.topk, args.planning_steps, log)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host ...")
         dt, passes, threads = cpu_baseline(w, H)

@@ -3,14 +3,16 @@
 // planning state; Alg. 2: commit into the action pool and update the state
 // as the stages complete).  Five launches on the caller's stream:
 //
-//   k_commit_apply  one thread per (instance, device).  It walks the
-//                   instance's frontier slots in ascending stage id and
-//                   applies every valid selection whose candidate contains
-//                   its device: start at max(tau, t), switch time if the
-//                   model was absent, Load, prefix slots, free time (summed
-//                   in fp64 over the step, stored as fp32).  The
-//                   thread of the candidate's first device marks the stage
-//                   completed with its output on the candidate's devices.
+//   k_commit_apply  one wave per instance.  The wave keeps the instance's
+//                   prefix slots, the exec and switch tables and the model
+//                   weights in LDS.  It takes the frontier slots 64 at a
+//                   time: lane q checks slot q's selection and marks the
+//                   stage completed with its output on the candidate's
+//                   devices; then lane d (device d) applies, in ascending
+//                   stage id, every placement whose candidate contains d:
+//                   start at max(tau, t), switch time if the model was
+//                   absent, Load, prefix slots, free time (summed in fp64
+//                   over the step, stored as fp32).
 //   k_plan_count    per stage (kPlanItems consecutive stages per thread):
 //                   completed parents, and the candidate count when the stage
 //                   is now in the frontier (pending, every parent completed);
@@ -73,77 +75,212 @@ __device__ int instance_of(const int64_t *stage_off, int B, int64_t s) {
     return lo;
 }
 
-// First frontier slot whose instance is >= b (the frontier is ordered by instance).
-__device__ int64_t first_slot_of(const uint32_t *frontier, int64_t nF, uint32_t b) {
-    int64_t lo = 0, hi = nF;
-    while (lo < hi) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (frontier[2 * mid + 1] < b) lo = mid + 1;
-        else hi = mid;
+// First frontier slot whose instance is >= b (the frontier is ordered by
+// instance), found by the whole wave (all 64 lanes active): each lane probes
+// one position, so every round of parallel loads shrinks the range 64-fold.
+__device__ int64_t first_slot_of_wave(const uint32_t *frontier, int64_t nF, uint32_t b) {
+    const int lane = threadIdx.x & 63;
+    int64_t lo = 0, hi = nF;  // the answer lies in [lo, hi]
+    for (;;) {  // uniform
+        const int64_t n = hi - lo;
+        if (n <= 64) {  // probe every position
+            const bool below = lane < n && frontier[2 * (lo + lane) + 1] < b;
+            return lo + __popcll(__ballot(below));
+        }
+        // probes p_l = lo + floor((l + 1) n / 64) - 1 rise strictly and end at hi - 1;
+        // those below b form a prefix of cnt probes
+        const int64_t p = lo + ((int64_t)(lane + 1) * n) / 64 - 1;
+        const int cnt = __popcll(__ballot(frontier[2 * p + 1] < b));
+        const int64_t nlo = cnt > 0 ? lo + ((int64_t)cnt * n) / 64 : lo;              // p_{cnt-1} + 1
+        const int64_t nhi = cnt < 64 ? lo + ((int64_t)(cnt + 1) * n) / 64 - 1 : hi;   // p_cnt
+        lo = nlo;
+        hi = nhi;
     }
-    return lo;
 }
 
-__global__ __launch_bounds__(256) void k_commit_apply(CommitLaunch a) {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (int64_t)a.B * a.D) return;
-    const int b = (int)(t / a.D), d = (int)(t % a.D), D = a.D, K = a.K;
+// One frontier slot of the instance, staged for the lanes of its wave:
+// the devices of its selected candidate (0 when none or rejected), the
+// stage's prefix group and model, and the candidate's size k.
+struct SlotL {
+    uint64_t win, hash, wm;  // wm: the model's weight
+    double k;
+    int32_t model, pad;
+};
+
+// Prefix-slot rows in LDS are padded to a multiple of 8 entries so that a
+// row is searched 8 entries per batch of loads.
+__host__ __device__ inline int padded_slots(int K) { return (K + 7) & ~7; }
+
+// LDS of k_commit_apply: the staged slots, the exec and switch tables, the
+// model weights and fit masks, the instance's prefix-slot rows and each
+// row's ring head.
+__host__ __device__ inline size_t apply_lds_bytes(int D, int M, int K) {
+    return 64 * sizeof(SlotL) + 8 * (size_t)M * D + 16 * (size_t)M + 8 * (size_t)D * padded_slots(K) +
+           4 * (size_t)D;
+}
+
+// Is the nonzero group h in the padded row?  Empty and padding entries
+// hold 0, which never equals h, so the whole padded row is compared.
+__device__ __forceinline__ bool row_has(const uint64_t *row, int Kp, uint64_t h) {
+    bool present = false;
+    for (int g = 0; g < Kp; g += 8) {  // uniform
+        uint64_t v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = row[g + e];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) present |= v[e] == h;
+    }
+    return present;
+}
+
+// The first empty entry among the row's K slots (the caller knows one exists).
+__device__ __forceinline__ int row_first_empty(const uint64_t *row, int K) {
+    int e = 0;
+    while (e + 1 < K && row[e] != 0ull) ++e;
+    return e;
+}
+
+__global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
+    extern __shared__ uint64_t smem[];
+    const int b = blockIdx.x, lane = threadIdx.x, D = a.D, K = a.K, M = a.M, Kp = padded_slots(K);
+    SlotL *sl = reinterpret_cast<SlotL *>(smem);
+    uint64_t *wt = smem + (64 * sizeof(SlotL)) / 8;
+    uint64_t *fit = wt + M;
+    uint64_t *pslots = fit + M;
+    float *ex = reinterpret_cast<float *>(pslots + (size_t)D * Kp);
+    float *ks = ex + (size_t)M * D;
+    int *heads = reinterpret_cast<int *>(ks + (size_t)M * D);
+    for (int i = lane; i < M * D; i += 64) {
+        ex[i] = a.exec[i];
+        ks[i] = a.ksw[i];
+    }
+    for (int i = lane; i < M; i += 64) {
+        wt[i] = a.weight[i];
+        fit[i] = a.fits[i];
+    }
+    for (int i = lane; i < D * Kp; i += 64) {
+        const int dd = i / Kp, e = i - dd * Kp;
+        pslots[i] = e < K ? a.pcache[((int64_t)b * D + dd) * K + e] : 0ull;
+    }
     const int64_t nF = a.counts[0];
-    const int64_t lo = first_slot_of(a.frontier, nF, (uint32_t)b);
-    const int64_t hi = first_slot_of(a.frontier, nF, (uint32_t)b + 1u);
-    uint64_t res = a.resident[t];
+    const int64_t lo = first_slot_of_wave(a.frontier, nF, (uint32_t)b);
+    const int64_t hi = first_slot_of_wave(a.frontier, nF, (uint32_t)b + 1u);
+    const bool live = lane < D;
+    const int d = live ? lane : 0;
+    const int64_t t = (int64_t)b * D + d;
+    uint64_t res = live ? a.resident[t] : 0ull;
+    const uint64_t cap = a.cap[d];
     // free time: summed in fp64 over the step, rounded once when stored
-    double tau = (double)a.tau[t];
+    double tau = live ? (double)a.tau[t] : 0.0;
     const double tn = (double)a.tnow[b];
-    uint64_t *slots = a.pcache + t * K;
+    uint64_t *row = pslots + d * Kp;
+    uint64_t last_h = 0;  // the group this device handled last: it is in its slots
+    int last_m = -1;      // the model this device loaded last: it is resident
     uint32_t rejected = 0;
-    for (int64_t f = lo; f < hi; ++f) {
-        const int j = a.sel[f * a.sel_stride];
-        if (j < 0) continue;
-        const uint32_t s = a.frontier[2 * f];
-        const StageRec r = a.rec[s];
-        const int m = r.model;
-        if (j >= candidates_of(shard_cap_of(r.shard, a.max_shard, D), D)) {
-            ++rejected;
-            continue;
-        }
-        int i0, k;
-        candidate_window(j, D, i0, k);
-        const uint64_t win = ((1ull << k) - 1ull) << i0;
-        if (((r.elig & a.fits[m]) & win) != win) {  // a device not eligible or too small
-            ++rejected;
-            continue;
-        }
-        if (d == i0) {
-            a.holders[s] = win;
-            a.status[s] = kCompleted;
-        }
-        if (d < i0 || d >= i0 + k) continue;
-        const double start = tau > tn ? tau : tn;
-        const double sw = bit(res, m) ? 0.0 : (double)a.ksw[m * D + d];
-        res = load_model(res, m, a.cap[d], a.weight);
-        const uint64_t h = r.hash;
-        if (h != 0 && K > 0) {
-            bool present = false;
-            int empty = -1;
-            for (int q = 0; q < K; ++q) {
-                present = present || slots[q] == h;
-                if (slots[q] == 0 && empty < 0) empty = q;
-            }
-            if (!present) {
-                if (empty >= 0) {
-                    slots[empty] = h;
-                } else {  // oldest first: drop slot 0, append
-                    for (int q = 0; q + 1 < K; ++q) slots[q] = slots[q + 1];
-                    slots[K - 1] = h;
+    __syncthreads();
+    // resident weight, kept up to date by the loads below
+    uint64_t total = 0;
+    for (uint64_t r = res; r; r &= r - 1) total += wt[__builtin_ctzll(r)];
+    // The row is kept as a ring: logical slot e is row[(head + e) mod K].
+    // Dropping slot 0 and appending is then one store and head + 1.  Empty
+    // slots exist only before the row first fills, and only then is an
+    // empty slot filled, so head stays 0 while any slot is empty.
+    int head = 0, nempty = 0;
+    for (int e = 0; e < K; ++e) nempty += row[e] == 0ull ? 1 : 0;
+    for (int64_t c0 = lo; c0 < hi; c0 += 64) {  // uniform: chunks of 64 slots
+        // lane q checks slot c0 + q and records its stage as completed
+        const int64_t f = c0 + lane;
+        uint64_t win = 0;
+        bool rej = false;
+        if (f < hi) {
+            const uint32_t s = a.frontier[2 * f];
+            const int j = a.sel[f * a.sel_stride];
+            const StageRec r = a.rec[s];
+            SlotL x;
+            x.hash = r.hash;
+            x.model = r.model;
+            x.wm = wt[r.model];
+            x.pad = 0;
+            x.k = 1.0;
+            if (j >= 0) {
+                if (j >= candidates_of(shard_cap_of(r.shard, a.max_shard, D), D)) {
+                    rej = true;
+                } else {
+                    int i0, k;
+                    candidate_window(j, D, i0, k);
+                    const uint64_t w = ((1ull << k) - 1ull) << i0;
+                    if (((r.elig & fit[r.model]) & w) != w) {  // a device not eligible or too small
+                        rej = true;
+                    } else {
+                        win = w;
+                        x.k = (double)k;
+                        a.holders[s] = w;
+                        a.status[s] = kCompleted;
+                    }
                 }
             }
+            x.win = win;
+            sl[lane] = x;
         }
-        tau = start + (double)a.exec[m * D + d] / (double)k + sw;
+        rejected += (uint32_t)__popcll(__ballot(rej));
+        // lane d collects the slots whose candidate contains device d
+        uint64_t mine = 0;
+        for (int dd = 0; dd < D; ++dd) {  // uniform
+            const uint64_t m = __ballot((win >> dd) & 1ull);
+            if (lane == dd) mine = m;
+        }
+        __syncthreads();
+        // each device applies its own placements in ascending stage id
+        while (live && mine) {
+            const int q = __builtin_ctzll(mine);
+            mine &= mine - 1;
+            const SlotL x = sl[q];
+            const int m = x.model;
+            const double start = tau > tn ? tau : tn;
+            const double c = (double)ex[m * D + d];
+            double sw = 0.0;
+            if (m != last_m) {
+                last_m = m;
+                if (!bit(res, m)) {  // Load, with the resident weight kept running
+                    sw = (double)ks[m * D + d];
+                    res |= 1ull << m;
+                    total += x.wm;
+                    for (uint64_t r = res & ~(1ull << m); r && total > cap; r &= r - 1) {
+                        const int i = __builtin_ctzll(r);
+                        res &= ~(1ull << i);
+                        total -= wt[i];
+                    }
+                }
+            }
+            if (x.hash != 0 && K > 0 && x.hash != last_h) {  // placements often repeat a group
+                last_h = x.hash;
+                if (!row_has(row, Kp, x.hash)) {
+                    if (nempty > 0) {  // head is 0: the first empty slot in order
+                        row[row_first_empty(row, K)] = x.hash;
+                        --nempty;
+                    } else {  // oldest first: drop slot 0, append
+                        row[head] = x.hash;
+                        head = head + 1 == K ? 0 : head + 1;
+                    }
+                }
+            }
+            tau = start + (x.k == 1.0 ? c : c / x.k) + sw;  // c / 1 is c
+        }
+        __syncthreads();  // the next chunk overwrites the staged slots
     }
-    a.resident[t] = res;
-    a.tau[t] = (float)tau;
-    if (d == 0) a.rej[b] = rejected;
+    if (live) {
+        a.resident[t] = res;
+        a.tau[t] = (float)tau;
+        heads[d] = head;
+    }
+    __syncthreads();
+    for (int i = lane; i < D * K; i += 64) {  // rows back in slot order
+        const int dd = i / K, e = i - dd * K;
+        int p = heads[dd] + e;
+        p = p >= K ? p - K : p;
+        a.pcache[(int64_t)b * D * K + i] = pslots[dd * Kp + p];
+    }
+    if (lane == 0) a.rej[b] = rejected;
 }
 
 __global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
@@ -289,8 +426,8 @@ __global__ __launch_bounds__(1024) void k_plan_slices(CommitLaunch a) {
 
 int launch_commit(const CommitLaunch &a, void *stream) {
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const int64_t nthr = (int64_t)a.B * a.D;
-    if (nthr > 0) hipLaunchKernelGGL(k_commit_apply, dim3((unsigned)((nthr + 255) / 256)), dim3(256), 0, s, a);
+    if (a.B > 0)
+        hipLaunchKernelGGL(k_commit_apply, dim3((unsigned)a.B), dim3(64), apply_lds_bytes(a.D, a.M, a.K), s, a);
     if (a.nblk > 0) hipLaunchKernelGGL(k_plan_count, dim3((unsigned)a.nblk), dim3(kPlanBlock), 0, s, a);
     hipLaunchKernelGGL(k_plan_offsets, dim3(1), dim3(1024), 0, s, a);
     if (a.nblk > 0) hipLaunchKernelGGL(k_plan_fill, dim3((unsigned)a.nblk), dim3(kPlanBlock), 0, s, a);

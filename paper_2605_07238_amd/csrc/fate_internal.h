@@ -101,7 +101,7 @@ struct CommitLaunch {
 };
 
 // Stages per workgroup of the planning scans, and the workspace layout.
-constexpr int kPlanBlock = 256, kPlanItems = 4, kPlanStages = kPlanBlock * kPlanItems;
+constexpr int kPlanBlock = 256, kPlanItems = 1, kPlanStages = kPlanBlock * kPlanItems;
 struct CommitWs {
     size_t cp, nc, fidx, bsum, rej, total;
 };

@@ -236,3 +236,30 @@ def test_planning_state_scores_and_topk_match_plain_state():
     assert np.array_equal(v0.cpu().numpy().view(np.uint32), v1[:nF].cpu().numpy().view(np.uint32))
     assert np.array_equal(i0.cpu().numpy(), fi1[:nF].cpu().numpy())
     assert np.array_equal(s0[:nC].cpu().numpy().view(np.uint32), f1[:nC].cpu().numpy().view(np.uint32))
+
+
+def _lowest_feasible(ref, best):
+    """Each stage's lowest-numbered candidate with a finite score."""
+    co, psi = ref["cand_off"], ref["psi"]
+    sel = best.copy()
+    for f in range(len(sel)):
+        fin = np.nonzero(np.isfinite(psi[co[f]:co[f + 1]]))[0]
+        sel[f] = fin[0] if len(fin) else -1
+    return sel
+
+
+def test_commit_long_device_chains_wrap_prefix_rows():
+    """Every stage takes its lowest feasible candidate, so the low devices get
+    long chains of placements in one step; with more prefix groups than
+    slots the rows wrap many times, and they start with holes."""
+    import dataclasses
+    w = synth.make_random_small(43, B=2, n=120, D=4, M=5, K=3, max_shard=2, p_edge=0.03, shard_frac=0.3)
+    rng = np.random.default_rng(43)
+    pool = rng.integers(1, 1 << 62, size=7).astype(np.uint64)
+    ph = pool[rng.integers(0, 7, size=w.N)]
+    ph[rng.random(w.N) < 0.1] = 0
+    pc = w.prefix_cache.copy().reshape(-1)
+    pc[::4] = 0  # holes before filled slots
+    w = dataclasses.replace(w, prefix_hash=ph, prefix_cache=pc.reshape(w.prefix_cache.shape))
+    assert np.count_nonzero(np.isfinite(oracle.score(w)["psi"])) > 40
+    _run_steps(w, 4, sel_fn=_lowest_feasible)
