@@ -71,6 +71,24 @@
  *     then v is completed with its output held by exactly S.  The next
  *     frontier follows from step 1 on the updated state.
  *
+ * Scoring variants (all off by default):
+ *   V1. Same-model preference (Sec. 4 implementation summary: model-
+ *       specialised placement preferences; App. C.3, "w/o same-model bonus"
+ *       removes the reward for continuing with a model already resident
+ *       while keeping the switch cost) [reading]: every place a switch cost
+ *       Sw(x,d) enters (steps 4 and 5), the term - l_m SM(x,d) enters beside
+ *       it, SM(x,d) = 1 if m(x) is resident on d in the state at hand, else 0.
+ *   V2. Topological levels (Sec. 3.3 "downstream DAG levels", the other
+ *       reading of step 7) [reading]: level(x) = 0 for a stage without
+ *       parents, else 1 + the largest level of its parents; the horizon set of
+ *       v is every stage reachable from v with 1 <= level(w) - level(v) <= H,
+ *       at depth level(w) - level(v).
+ *   V3. Mean per level (the alternative to the sum in step 9) [reading]: the
+ *       values of the stages at depth h are averaged, each weighted
+ *       gamma^h / n_h, n_h the number of horizon stages at depth h.
+ *   V4. No windows (App. C.3, "w/o shard parallelism"): candidates with
+ *       k > 1 keep their slots but score -infinity.
+ *
  * Alongside Psi the oracle reports A, the sum of the absolute values of every
  * weighted term it added (for the maximising device of step 5 and the
  * minimising device of step 8).  Parity tolerances are relative to A.
@@ -95,6 +113,9 @@ typedef struct {
     const uint8_t *status;                    /* [N] */
     const float *tau, *t_now;                 /* [B*D], [B] */
     double lam_q, lam_s, lam_tr, lam_c, lam_p, kappa_prefix, gamma;
+    /* variants V1-V4 */
+    double lam_m;
+    int topo_levels, mean_levels, no_windows;
 } oracle_in_t;
 
 enum { ST_PENDING = 0, ST_COMPLETED = 1 };
@@ -183,6 +204,11 @@ static double prefix_benefit(const view_t *s, int x, int d) {
     return hit ? in->kappa_prefix * (double)in->tokens[g] : 0.0;
 }
 
+/* V1: 1 if the model of stage x is already resident on d. */
+static double same_model(const view_t *s, int x, int d) {
+    return has_bit(s->res[d], s->in->model[s->base + x]) ? 1.0 : 0.0;
+}
+
 /* App. A.1 / A.4 state-corrected cost of stage x on device d, plus the sum
  * of the absolute values of its weighted terms. */
 static double c_hat(const view_t *s, int x, int d, double *mag) {
@@ -193,8 +219,9 @@ static double c_hat(const view_t *s, int x, int d, double *mag) {
     double t_tr = in->lam_tr * transfer_cost(s, x, d);
     double t_co = in->lam_c * colo_benefit(s, x, d);
     double t_pf = in->lam_p * prefix_benefit(s, x, d);
-    if (mag) *mag = fabs(c) + fabs(t_sw) + fabs(t_tr) + fabs(t_co) + fabs(t_pf);
-    return c + t_sw + t_tr - t_co - t_pf;
+    double t_sm = in->lam_m * same_model(s, x, d);
+    if (mag) *mag = fabs(c) + fabs(t_sw) + fabs(t_tr) + fabs(t_co) + fabs(t_pf) + fabs(t_sm);
+    return c + t_sw + t_tr - t_co - t_pf - t_sm;
 }
 
 /* Model load under capacity: add m, then evict the smallest-id other
@@ -282,7 +309,29 @@ int oracle_frontier(const oracle_in_t *in, int B, const int64_t *f_off, int32_t 
     return 0;
 }
 
-typedef struct { int *depth; int *queue; int *list; int *cptr; int *cidx; } scratch_t;
+typedef struct { int *depth; int *queue; int *list; int *cptr; int *cidx; int *level; int *nlev; } scratch_t;
+
+/* V2 horizon set of v: every stage reachable from v whose topological level
+ * exceeds v's by 1..H, at depth = that difference.  Levels rise along every
+ * edge, so a stage beyond the window has no descendant inside it. */
+static int horizon_levels(const scratch_t *sc, int n, int v, int H) {
+    for (int i = 0; i < n; ++i) sc->depth[i] = -1;
+    sc->depth[v] = 0;
+    int head = 0, tail = 0, count = 0;
+    sc->queue[tail++] = v;
+    while (head < tail) {
+        int x = sc->queue[head++];
+        for (int q = sc->cptr[x]; q < sc->cptr[x + 1]; ++q) {
+            int c = sc->cidx[q];
+            int dl = sc->level[c] - sc->level[v];
+            if (sc->depth[c] >= 0 || dl > H) continue;
+            sc->depth[c] = dl;
+            sc->queue[tail++] = c;
+            sc->list[count++] = c;
+        }
+    }
+    return count;
+}
 
 /* Breadth-first horizon set of v: fills list[0..count) with stages at hop
  * distance 1..H (each once, at its minimum distance) and depth[] for them. */
@@ -329,6 +378,14 @@ static void score_instance(const oracle_in_t *in, int b, int64_t f0, int64_t c0,
             sc.cidx[sc.cptr[u] + fill[u]++] = x;
         }
     free(fill);
+    /* V2: topological levels (parents have smaller ids) */
+    sc.level = (int *)calloc((size_t)n + 1, sizeof(int));
+    for (int x = 0; x < n; ++x)
+        for (int64_t q = in->par_off[base + x]; q < in->par_off[base + x + 1]; ++q) {
+            int l = sc.level[in->par_idx[q]] + 1;
+            if (l > sc.level[x]) sc.level[x] = l;
+        }
+    sc.nlev = (int *)calloc(17, sizeof(int));
 
     view_t cur;
     init_view(&cur, in, b);
@@ -340,14 +397,16 @@ static void score_instance(const oracle_in_t *in, int b, int64_t f0, int64_t c0,
         int64_t nc = n_candidates(in, g);
         front_v[f] = v;
         cand_off[f] = c;
-        int count = horizon(&sc, n, v, in->H);
+        int count = in->topo_levels ? horizon_levels(&sc, n, v, in->H) : horizon(&sc, n, v, in->H);
+        for (int h = 0; h <= 16; ++h) sc.nlev[h] = 0;
+        for (int q = 0; q < count; ++q) sc.nlev[sc.depth[sc.list[q]]] += 1;
         for (int64_t j = 0; j < nc; ++j, ++c) {
             int i0, k;
             candidate(in, j, &i0, &k);
             int ok = 1;
             for (int d = i0; d < i0 + k; ++d)
                 if (!feasible(in, g, d)) ok = 0;
-            if (!ok) { psi[c] = -INFINITY; mag[c] = 0.0; continue; }
+            if (!ok || (k > 1 && in->no_windows)) { psi[c] = -INFINITY; mag[c] = 0.0; continue; }
             /* step 5: immediate cost */
             double best_t = -INFINITY, best_mag = 0.0;
             for (int d = i0; d < i0 + k; ++d) {
@@ -357,10 +416,12 @@ static void score_instance(const oracle_in_t *in, int b, int64_t f0, int64_t c0,
                 double a_tr = in->lam_tr * transfer_cost(&cur, v, d) / k;
                 double a_pf = in->lam_p * prefix_benefit(&cur, v, d) / k;
                 double a_co = in->lam_c * colo_benefit(&cur, v, d);
-                double t = a_q + a_c + a_s + a_tr - a_pf - a_co;
+                double a_sm = in->lam_m * same_model(&cur, v, d);
+                double t = a_q + a_c + a_s + a_tr - a_pf - a_co - a_sm;
                 if (t > best_t) {
                     best_t = t;
-                    best_mag = fabs(a_q) + fabs(a_c) + fabs(a_s) + fabs(a_tr) + fabs(a_pf) + fabs(a_co);
+                    best_mag = fabs(a_q) + fabs(a_c) + fabs(a_s) + fabs(a_tr) + fabs(a_pf) + fabs(a_co) +
+                               fabs(a_sm);
                 }
             }
             double gsum = 0.0;
@@ -390,6 +451,7 @@ static void score_instance(const oracle_in_t *in, int b, int64_t f0, int64_t c0,
                 int w = sc.list[q];
                 int64_t gw = base + w;
                 double gw_pow = pow(in->gamma, (double)sc.depth[w]);
+                if (in->mean_levels) gw_pow /= (double)sc.nlev[sc.depth[w]];
                 double vbest = INFINITY, vmag = 0.0;
                 for (int d = 0; d < D; ++d) {
                     if (!feasible(in, gw, d)) continue;
@@ -405,7 +467,7 @@ static void score_instance(const oracle_in_t *in, int b, int64_t f0, int64_t c0,
         }
         ++f;
     }
-    free(sc.depth); free(sc.queue); free(sc.list); free(sc.cptr); free(sc.cidx);
+    free(sc.depth); free(sc.queue); free(sc.list); free(sc.cptr); free(sc.cidx); free(sc.level); free(sc.nlev);
 }
 
 /* Score every candidate of every frontier stage.  f_off/c_off[b] are the
@@ -415,6 +477,7 @@ static void score_instance(const oracle_in_t *in, int b, int64_t f0, int64_t c0,
 int oracle_score(const oracle_in_t *in, int B, const int64_t *f_off, const int64_t *c_off,
                  int32_t *front_v, int64_t *cand_off, double *psi, double *mag, int threads) {
     if (in->D < 1 || in->D > 64 || in->M < 1 || in->M > 64) return -1;
+    if (in->H < 0 || in->H > 16) return -1;
     if (threads < 1) threads = 1;
 #pragma omp parallel for schedule(dynamic, 1) num_threads(threads)
     for (int b = 0; b < B; ++b) score_instance(in, b, f_off[b], c_off[b], front_v, cand_off, psi, mag);

@@ -50,6 +50,7 @@ class _In(C.Structure):
         ("lam_q", C.c_double), ("lam_s", C.c_double), ("lam_tr", C.c_double),
         ("lam_c", C.c_double), ("lam_p", C.c_double), ("kappa_prefix", C.c_double),
         ("gamma", C.c_double),
+        ("lam_m", C.c_double), ("topo_levels", C.c_int), ("mean_levels", C.c_int), ("no_windows", C.c_int),
     ]
 
 
@@ -117,6 +118,12 @@ def _record(w, params=None, H=None, max_shard=None):
         setattr(rec, k, a.ctypes.data)
     for k in ("lam_q", "lam_s", "lam_tr", "lam_c", "lam_p", "kappa_prefix", "gamma"):
         setattr(rec, k, f32(p[k]))
+    # scoring variants, off unless asked for: same-model weight, topological
+    # levels, mean per level, no windows
+    rec.lam_m = f32(p.get("lam_m", 0.0))
+    rec.topo_levels = int(bool(p.get("topo_levels", 0)))
+    rec.mean_levels = int(bool(p.get("mean_levels", 0)))
+    rec.no_windows = int(bool(p.get("no_windows", 0)))
     return rec, keep
 
 

@@ -389,6 +389,178 @@ def check_commit_invariants(seed: int, lib=None):
     assert np.array_equal(got, ready), (got, ready)
 
 
+# ---------------------------------------------------------------------------
+# scoring variants (oracle V1-V4)
+# ---------------------------------------------------------------------------
+
+def check_variant_scenario(name: str, lib=None):
+    sc = scenarios.VARIANTS[name]
+    w = builders.from_spec(sc["spec"], H=sc["H"], params=sc["params"])
+    r = oracle.score(w, lib=lib)
+    assert list(r["front_v"]) == sc["front_v"], (list(r["front_v"]), sc["front_v"])
+    _close(r["psi"], sc["psi"], rtol=1e-12)
+    if "topk3" in sc:
+        idx, _ = oracle.topk(r, 3, lib=lib)
+        assert idx[0].tolist() == sc["topk3"], idx
+
+
+def _levels_scipy(adj):
+    """Topological level of every stage: the length of the longest path that
+    ends there, from Bellman-Ford shortest paths with every edge weighted -1."""
+    n = adj.shape[0]
+    neg = sp.csr_matrix((-np.ones(adj.nnz), adj.indices, adj.indptr), shape=(n, n))
+    dist = shortest_path(neg, method="BF", directed=True)
+    lv = np.where(np.isfinite(dist), -dist, 0.0).max(axis=0)
+    return np.maximum(lv, 0.0).astype(np.int64)
+
+
+def check_variant_reduction(seed: int, lib=None, H: int = 3, topo: bool = False, mean: bool = False):
+    """Base runtimes only, under the horizon variants: the tail is
+    sum_h gamma^h agg_{w at depth h} min_feasible c(w,.), agg = sum or mean,
+    depth = hop distance (scipy, unweighted) or the difference of longest-path
+    levels (scipy Bellman-Ford on -1 weights) among stages reachable from v."""
+    w = synth.make_random_small(seed, B=2, n=16, D=4, M=3, K=2, H=H, max_shard=3, p_edge=0.35)
+    zero = dict(lam_q=0.0, lam_s=0.0, lam_tr=0.0, lam_c=0.0, lam_p=0.0, gamma=0.5,
+                topo_levels=int(topo), mean_levels=int(mean))
+    r = oracle.score(w, params=zero, lib=lib)
+    gam = oracle.f32(0.5)
+    exp, fronts = [], []
+    for b in range(w.B):
+        lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+        n = hi - lo
+        rows, cols = [], []
+        for x in range(n):
+            g = lo + x
+            for p in w.par_idx[w.par_off[g]:w.par_off[g + 1]]:
+                rows.append(int(p))
+                cols.append(x)
+        adj = sp.csr_matrix((np.ones(len(rows)), (rows, cols)), shape=(n, n))
+        dist = shortest_path(adj, directed=True, unweighted=True)
+        lv = _levels_scipy(adj)
+        for v in _frontier(w, b):
+            fronts.append(v)
+            g = lo + v
+            by_depth = {}
+            for x in range(n):
+                if not np.isfinite(dist[v, x]) or x == v:
+                    continue
+                h = int(lv[x] - lv[v]) if topo else int(dist[v, x])
+                if 1 <= h <= H:
+                    gx = lo + x
+                    best = min(float(w.exec[w.model[gx], d]) for d in range(w.D) if _feasible(w, gx, d))
+                    by_depth.setdefault(h, []).append(best)
+            tail = sum(gam ** h * (np.mean(vals) if mean else np.sum(vals)) for h, vals in by_depth.items())
+            r_v = min(int(w.shard_max[g]), w.max_shard, w.D)
+            for (i, k) in _windows(w.D, r_v):
+                S = range(i, i + k)
+                if not all(_feasible(w, g, d) for d in S):
+                    exp.append(-np.inf)
+                    continue
+                j0 = max(float(w.exec[w.model[g], d]) / k for d in S)
+                exp.append(-(j0 + tail))
+    assert list(r["front_v"]) == fronts
+    _close(r["psi"], exp, rtol=1e-12)
+
+
+def check_topo_equals_hop_on_layers(seed: int, lib=None):
+    """Where every edge joins consecutive layers (the layered and fork-join
+    recipes) the topological-level horizon is the breadth-first one."""
+    name = ("tiny-layered-1x24-d4", "layered-1024x200-d8", "forkjoin-4096x1000-d16")[seed]
+    w = synth.make_workload(name, B=2 if seed else 1)
+    a = oracle.score(w, lib=lib)
+    b = oracle.score(w, params=dict(topo_levels=1), lib=lib)
+    assert np.array_equal(a["psi"], b["psi"])
+
+
+def check_mean_equals_sum_on_chains(seed: int, lib=None):
+    """On chains every horizon level holds one stage, so mean = sum."""
+    w = synth.make_random_small(seed, B=2, n=12, D=4, M=3, K=2, H=4, max_shard=3, p_edge=0.0)
+    # relink every stage to its predecessor only: a chain per instance
+    par_off = [0]
+    par_idx = []
+    for b in range(w.B):
+        lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+        for x in range(hi - lo):
+            if x > 0:
+                par_idx.append(x - 1)
+            par_off.append(len(par_idx))
+    import dataclasses
+    st = w.status.copy()
+    hold = w.holders.copy()
+    for b in range(w.B):  # completed stages must stay down-closed on the chain
+        lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+        done = True
+        for g in range(lo, hi):
+            done = done and st[g] == 1
+            if not done and st[g] in (1, 2):
+                st[g], hold[g] = 0, 0
+    w = dataclasses.replace(w, par_off=np.array(par_off, np.int64), par_idx=np.array(par_idx, np.int32),
+                            status=st, holders=hold)
+    a = oracle.score(w, lib=lib)
+    b = oracle.score(w, params=dict(mean_levels=1), lib=lib)
+    assert len(a["psi"]) > 0
+    _close(b["psi"], a["psi"], rtol=1e-15)
+
+
+def check_no_windows_keeps_singletons(seed: int, lib=None):
+    """Without windows the singletons score as under max_shard = 1, and every
+    window slot is -inf."""
+    w = synth.make_random_small(seed, B=3, n=16, D=5, M=3, K=2, max_shard=3, shard_frac=0.6)
+    a = oracle.score(w, params=dict(no_windows=1), lib=lib)
+    b = oracle.score(w, max_shard=1, lib=lib)
+    nf = len(a["front_v"])
+    assert nf == len(b["front_v"]) and nf > 0
+    for f in range(nf):
+        seg = a["psi"][a["cand_off"][f]:a["cand_off"][f + 1]]
+        assert np.array_equal(seg[:w.D], b["psi"][b["cand_off"][f]:b["cand_off"][f + 1]])
+        assert np.all(np.isneginf(seg[w.D:]))
+    assert any(a["cand_off"][f + 1] - a["cand_off"][f] > w.D for f in range(nf))
+
+
+def check_same_model_weight_linear(seed: int, lib=None):
+    """Psi is affine in lam_m with slope -(number of same-model events the
+    maximising shard and the minimising descendant devices see): checked by
+    Psi(2x) - Psi(x) = Psi(x) - Psi(0) on candidates whose choices do not flip,
+    which holds for every candidate when all devices share one speed class
+    and every model is resident everywhere (the bonus is then uniform)."""
+    w = synth.make_random_small(seed, B=2, n=16, D=4, M=3, K=2, max_shard=3, tight_caps=False)
+    import dataclasses
+    full = np.uint64((1 << w.M) - 1)
+    w = dataclasses.replace(w, resident=np.full_like(w.resident, full))
+    if any(int(w.weight_bytes.sum()) > int(c) for c in w.cap_bytes):
+        return  # all models cannot be resident together: not this check's case
+    r0 = oracle.score(w, params=dict(lam_m=0.0), lib=lib)
+    r1 = oracle.score(w, params=dict(lam_m=0.125), lib=lib)
+    H = int(w.H)
+    fin = np.isfinite(r0["psi"])
+    # every shard device and every descendant device holds its model: the
+    # immediate cost drops by lam_m and each horizon stage's value by lam_m
+    for f in range(len(r0["front_v"])):
+        lo, hi = r0["cand_off"][f], r0["cand_off"][f + 1]
+        b, v = int(r0["front_b"][f]), int(r0["front_v"][f])
+        n_at = _horizon_counts(w, b, v, H)
+        drop = 0.125 * (1.0 + sum(oracle.f32(w.params["gamma"]) ** h * c for h, c in n_at.items()))
+        _close(r1["psi"][lo:hi][fin[lo:hi]], r0["psi"][lo:hi][fin[lo:hi]] + drop, rtol=1e-12)
+
+
+def _horizon_counts(w, b, v, H):
+    lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+    n = hi - lo
+    rows, cols = [], []
+    for x in range(n):
+        for p in w.par_idx[w.par_off[lo + x]:w.par_off[lo + x + 1]]:
+            rows.append(int(p))
+            cols.append(x)
+    adj = sp.csr_matrix((np.ones(len(rows)), (rows, cols)), shape=(n, n))
+    dist = shortest_path(adj, directed=True, unweighted=True, indices=[v])[0]
+    out = {}
+    for x in range(n):
+        h = dist[x]
+        if np.isfinite(h) and 1 <= h <= H:
+            out[int(h)] = out.get(int(h), 0) + 1
+    return out
+
+
 ALL_CHECKS = (
     [("scenario:" + k, (lambda k: lambda lib: check_scenario(k, lib))(k)) for k in scenarios.ALL]
     + [("worked_example", check_worked_example)]
@@ -401,4 +573,16 @@ ALL_CHECKS = (
     + [("isolated:%d" % s, (lambda s: lambda lib: check_isolated_stage(s, lib))(s)) for s in range(2)]
     + [("commit:" + k, (lambda k: lambda lib: check_commit_scenario(k, lib))(k)) for k in scenarios.COMMITS]
     + [("commit_invariants:%d" % s, (lambda s: lambda lib: check_commit_invariants(s, lib))(s)) for s in range(3)]
+    + [("variant:" + k, (lambda k: lambda lib: check_variant_scenario(k, lib))(k)) for k in scenarios.VARIANTS]
+    + [("variant_reduction:%s:%d" % (m, s),
+        (lambda s, t, mn: lambda lib: check_variant_reduction(s, lib, topo=t, mean=mn))(s, t, mn))
+       for m, t, mn in (("topo", True, False), ("mean", False, True), ("topo_mean", True, True))
+       for s in range(3)]
+    + [("topo_equals_hop:%d" % s, (lambda s: lambda lib: check_topo_equals_hop_on_layers(s, lib))(s))
+       for s in range(2)]
+    + [("mean_equals_sum_chain:%d" % s, (lambda s: lambda lib: check_mean_equals_sum_on_chains(s, lib))(s))
+       for s in range(2)]
+    + [("no_windows:%d" % s, (lambda s: lambda lib: check_no_windows_keeps_singletons(s, lib))(s)) for s in range(2)]
+    + [("same_model_uniform:%d" % s, (lambda s: lambda lib: check_same_model_weight_linear(s, lib))(s))
+       for s in range(3)]
 )

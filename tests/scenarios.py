@@ -201,3 +201,54 @@ COMMIT_REJECT = dict(
     holders=[0, 0], status=[0, 0], next_front_v=[0, 1], rejected=2)
 
 COMMITS = dict(COMMIT_SINGLE=COMMIT_SINGLE, COMMIT_WINDOW=COMMIT_WINDOW, COMMIT_REJECT=COMMIT_REJECT)
+
+
+# ---------------------------------------------------------------------------
+# Scoring variants (oracle V1-V4), each on an input of a scenario above.
+# ---------------------------------------------------------------------------
+
+# V1 same-model weight lam_m = 1/4, beside the switch cost.
+#   WAIT_SWITCH: d0 holds m0 -> 1.0 - 0.25; d1 does not -> 2.25 unchanged.
+_SM = dict(P, lam_m=0.25)
+SM_IMMEDIATE = dict(WAIT_SWITCH, params=_SM, psi=[-0.75, -2.25])
+#   WINDOWS (d0 holds m0, so only T(d0) drops by 1/4, inside the max):
+#   k=1: 2.625, 3.0, 5.0; {0,1}: max(2.125, 1.75) + 0.375 = 2.5;
+#   {1,2}: 2.9375; {0,1,2}: max(2 + 1/3 - 1/8 - 1/4, 4/3, 4/3 + 1/2 + 1/6) + 0.625
+#   = 2.0 + 0.625 (d2 is now the slowest shard).
+SM_WINDOWS = dict(WINDOWS, params=_SM, psi=[-2.625, -3.0, -5.0, -2.5, -2.9375, -(4.0 / 3.0 + 2.0 / 3.0 + 0.625)])
+SM_WINDOWS.pop("topk3")
+#   POST_STATE: m1 (v's model) is resident nowhere, so the immediate costs
+#   stay 2.0 / 1.375; the descendants see s':
+#   v on d0 -> d0 {m1, m2}, d1 {m2}: w1 (m0) 0.6875 / 2.25 (no bonus: m0 was
+#     evicted from d0); w2 (m2) 0.875 - 0.25 / 2.0 - 0.25 -> 0.625.
+#     J = 2.0 + 0.5 (0.6875 + 0.625) = 2.65625
+#   v on d1 -> d0 {m0, m2}, d1 {m1, m2}: w1 2.0 - 0.25 / 0.6875; w2 2.0 - 0.25 /
+#     0.875 - 0.25 -> 0.625.  J = 1.375 + 0.5 (0.6875 + 0.625) = 2.03125
+SM_POST_STATE = dict(POST_STATE, params=_SM, psi=[-2.65625, -2.03125])
+
+# V2 / V3 on the horizon scenario with f (stage 6) eligible on d1 only.
+#   Hop distances from v: {2, 3, 6} at 1, {4} at 2, {5} at 3.
+#   Topological levels: 0,1,2,2,3,4,4 -> from v: {2, 3} at 1, {4} at 2,
+#   {5, 6} at 3 (6 has parents 1 and 4, so its level is 1 + 3).
+#   Best runtimes: 2, 3, 5 -> 1 (d0); 4, 6 -> 2 (d1 only).
+_HV_SPEC = dict(HORIZON_SET["spec"])
+_HV_SPEC["instances"] = [dict(HORIZON_SET["spec"]["instances"][0], elig=[3, 3, 3, 3, 2, 3, 2])]
+#   hop, sum:  tail = 0.5 (1 + 1 + 2) + 0.25 * 2 + 0.125 * 1 = 2.625
+HV_HOP_SUM = dict(HORIZON_SET, spec=_HV_SPEC, H=3, psi=[-3.625, -4.625])
+#   hop, mean: tail = 0.5 * 4/3 + 0.25 * 2 + 0.125 * 1 = 2/3 + 0.625
+HV_HOP_MEAN = dict(HV_HOP_SUM, params=dict(_E_P, mean_levels=1),
+                   psi=[-(1.0 + 2.0 / 3.0 + 0.625), -(2.0 + 2.0 / 3.0 + 0.625)])
+#   topological, sum: tail = 0.5 (1 + 1) + 0.25 * 2 + 0.125 (1 + 2) = 1.875
+HV_TOPO_SUM = dict(HV_HOP_SUM, params=dict(_E_P, topo_levels=1), psi=[-2.875, -3.875])
+#   topological, H = 2: {5, 6} drop out -> tail = 1.5
+HV_TOPO_SUM_H2 = dict(HV_TOPO_SUM, H=2, psi=[-2.5, -3.5])
+#   topological, mean: tail = 0.5 * 1 + 0.25 * 2 + 0.125 * 1.5 = 1.1875
+HV_TOPO_MEAN = dict(HV_HOP_SUM, params=dict(_E_P, topo_levels=1, mean_levels=1), psi=[-2.1875, -3.1875])
+
+# V4 no windows: WINDOWS keeps its six slots, the three windows at -inf.
+NO_WINDOWS = dict(WINDOWS, params=dict(P, no_windows=1), psi=[-2.875, -3.0, -5.0, -INF, -INF, -INF],
+                  topk3=[0, 1, 2])
+
+VARIANTS = dict(SM_IMMEDIATE=SM_IMMEDIATE, SM_WINDOWS=SM_WINDOWS, SM_POST_STATE=SM_POST_STATE,
+                HV_HOP_SUM=HV_HOP_SUM, HV_HOP_MEAN=HV_HOP_MEAN, HV_TOPO_SUM=HV_TOPO_SUM,
+                HV_TOPO_SUM_H2=HV_TOPO_SUM_H2, HV_TOPO_MEAN=HV_TOPO_MEAN, NO_WINDOWS=NO_WINDOWS)

@@ -23,7 +23,7 @@ MUTANTS = {
     "transfer_first_holder": [("if (has_bit(hu, i) && (double)in->beta[i * in->D + d] < bmin)",
                                "if (has_bit(hu, i) && bmin == INFINITY)")],
     "transfer_child_size": [("tr += (double)in->sigma[s->base + u] * bmin;", "tr += (double)in->sigma[g] * bmin;")],
-    "colo_sign": [("return c + t_sw + t_tr - t_co - t_pf;", "return c + t_sw + t_tr + t_co - t_pf;")],
+    "colo_sign": [("return c + t_sw + t_tr - t_co - t_pf - t_sm;", "return c + t_sw + t_tr + t_co - t_pf - t_sm;")],
     "colo_not_normalised": [("return (double)cnt / (double)np;", "return (double)cnt;")],
     "prefix_group_zero_counts": [("if (h == 0) return 0.0;", "if (0) return 0.0;")],
     "post_state_no_prefix": [("post.extra_hash[d] = in->hash[g];", "post.extra_hash[d] = 0;")],
@@ -50,7 +50,7 @@ MUTANTS = {
                                    "if (in->status[g] == ST_COMPLETED) return 0;")],
     "descendant_max_device": [("if (val < vbest) { vbest = val; vmag = m_; }",
                                "if (vbest == INFINITY || val > vbest) { vbest = val; vmag = m_; }")],
-    "prefix_sign": [("return c + t_sw + t_tr - t_co - t_pf;", "return c + t_sw + t_tr - t_co + t_pf;")],
+    "prefix_sign": [("return c + t_sw + t_tr - t_co - t_pf - t_sm;", "return c + t_sw + t_tr - t_co + t_pf - t_sm;")],
     # commit-and-advance
     "commit_start_ignores_now": [("double start = tau_out[bd] > (double)in->t_now[b] ? tau_out[bd] : (double)in->t_now[b];",
                                   "double start = tau_out[bd];")],
@@ -63,6 +63,20 @@ MUTANTS = {
     "commit_no_load": [("res_out[bd] = load_model(in, res_out[bd], m, d);", "res_out[bd] = res_out[bd];")],
     "commit_ignores_feasibility": [("if (!ok) { ++rejected; continue; }", "if (0) { ++rejected; continue; }")],
     "commit_not_completed": [("status_out[g] = ST_COMPLETED;", "status_out[g] = status_out[g];")],
+    # scoring variants
+    "same_model_when_absent": [("return has_bit(s->res[d], s->in->model[s->base + x]) ? 1.0 : 0.0;",
+                                "return has_bit(s->res[d], s->in->model[s->base + x]) ? 0.0 : 1.0;")],
+    "same_model_not_in_horizon": [("double t_sm = in->lam_m * same_model(s, x, d);", "double t_sm = 0.0;")],
+    "same_model_not_immediate": [("double a_sm = in->lam_m * same_model(&cur, v, d);", "double a_sm = 0.0;")],
+    "same_model_in_current_state": [("double t_sm = in->lam_m * same_model(s, x, d);",
+                                     "double t_sm = in->lam_m * (has_bit(s->in->resident[(int64_t)s->b * s->in->D + d], "
+                                     "s->in->model[s->base + x]) ? 1.0 : 0.0);")],
+    "topo_level_min_parent": [("if (l > sc.level[x]) sc.level[x] = l;",
+                               "if (sc.level[x] == 0 || l < sc.level[x]) sc.level[x] = l;")],
+    "topo_depth_is_hops": [("sc->depth[c] = dl;", "sc->depth[c] = sc->depth[x] + 1;")],
+    "mean_over_all_levels": [("if (in->mean_levels) gw_pow /= (double)sc.nlev[sc.depth[w]];",
+                              "if (in->mean_levels) gw_pow /= (double)count;")],
+    "no_windows_ignored": [("if (!ok || (k > 1 && in->no_windows))", "if (!ok)")],
 }
 
 
