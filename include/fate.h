@@ -48,6 +48,7 @@ extern "C" {
 #define FATE_MAX_TOPK 64
 #define FATE_MAX_SHARD 4
 #define FATE_MAX_PARENTS 65535
+#define FATE_MAX_SWEEP 16 /* parameter sets per fate_score_sweep / fate_topk_sweep launch */
 /* Total stages over the batch must fit 28 bits (stage ids share a 32-bit word
  * with their horizon depth in the packed descendant lists). */
 #define FATE_MAX_TOTAL_STAGES ((1 << 28) - 1)
@@ -127,13 +128,50 @@ typedef struct {
     const float *t_now;
 } fate_state_t;
 
+/* Scoring variants (fate_params_t.flags).
+ *   FATE_MEAN_PER_LEVEL  the horizon tail averages the values of the stages at
+ *                        each depth (weight gamma^h / n_h, n_h = v's horizon
+ *                        stages at depth h) instead of summing them; needs
+ *                        DAGs packed with level_weights
+ *   FATE_NO_WINDOWS      shard windows (k > 1) keep their score slots but score
+ *                        -infinity (App. C.3 "w/o shard parallelism")        */
+enum { FATE_MEAN_PER_LEVEL = 1, FATE_NO_WINDOWS = 2 };
+
 /* Score weights (Sec. 3.4 lambda_q, lambda_s, lambda_tr, lambda_c, lambda_p;
- * App. A.3 kappa_prefix), the horizon discount gamma (Sec. 3.2) and the
- * horizon H (Sec. 3.3; 0 <= H <= the H the DAGs were packed with). */
+ * App. A.3 kappa_prefix), the horizon discount gamma (Sec. 3.2), the
+ * horizon H (Sec. 3.3; 0 <= H <= the H the DAGs were packed with), the
+ * same-model weight lam_m and the variant flags above.
+ *   lam_m: the model-specialised placement preference (Sec. 4 implementation
+ *   summary; App. C.3 "w/o same-model bonus"): wherever a switch cost
+ *   Sw(x, d) enters a cost, -lam_m enters beside it when m(x) is resident on
+ *   d in the state at hand (s_t for the frontier stage, on every shard
+ *   device; s' for the horizon stages).  0 turns it off.
+ * Every weight must be finite and >= 0; unknown flag bits are EINVAL. */
 typedef struct {
     float lam_q, lam_s, lam_tr, lam_c, lam_p, kappa_prefix, gamma;
     int32_t H;
+    float lam_m;
+    int32_t flags;
 } fate_params_t;
+
+/* Horizon levels for packing (fate_pack_opts_t.levels; Sec. 3.3 "downstream
+ * DAG levels").
+ *   FATE_LEVELS_HOP   breadth-first hop distance from v, each stage once at
+ *                     its minimum distance
+ *   FATE_LEVELS_TOPO  topological level difference: level = 0 for a stage
+ *                     without parents, else 1 + its parents' largest level;
+ *                     the horizon of v is every stage reachable from v with
+ *                     1 <= level(w) - level(v) <= H, at that depth           */
+enum { FATE_LEVELS_HOP = 0, FATE_LEVELS_TOPO = 1 };
+
+/* Packing options: the horizon H (0..15), the level definition, and
+ * level_weights = 1 to also pack, per horizon entry, 1 / (number of v's
+ * horizon stages at that depth) for FATE_MEAN_PER_LEVEL (4 bytes per entry). */
+typedef struct {
+    int32_t H;
+    int32_t levels;
+    int32_t level_weights;
+} fate_pack_opts_t;
 
 /* Packed DAG batch: plain data pointing into the caller's device buffer.
  * Valid while that buffer lives; filled by fate_pack_dags. */
@@ -151,6 +189,8 @@ typedef struct {
     const uint32_t *desc_off;             /* [N+1] */
     const uint32_t *desc;                 /* [n_desc]: flat id | depth << 28 */
     const int64_t *stage_off;             /* [B+1] */
+    int32_t levels;                       /* FATE_LEVELS_HOP or FATE_LEVELS_TOPO */
+    const float *desc_w;                  /* [n_desc] level weights, or null */
 } fate_dags_t;
 
 /* Packed state of one planning step: plain data pointing into the caller's
@@ -204,6 +244,19 @@ fate_status_t fate_pack_dags(const fate_cluster_t *cluster, const fate_dag_batch
  * into host memory h_buf (no HIP call; `out` points into h_buf). */
 fate_status_t fate_layout_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
                                void *h_buf, size_t bytes, fate_dags_t *out);
+
+/* fate_pack_dags_opt_size / fate_pack_dags_opt / fate_layout_dags_opt: as the
+ * three calls above with the options of fate_pack_opts_t (horizon levels,
+ * level weights); {H, FATE_LEVELS_HOP, 0} gives the same image.  Descendant
+ * lists are ordered by (depth, id) either way.
+ * Errors: as above, plus EINVAL for a null or unknown option. */
+fate_status_t fate_pack_dags_opt_size(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                      const fate_pack_opts_t *opts, size_t *bytes);
+fate_status_t fate_pack_dags_opt(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                 const fate_pack_opts_t *opts, void *d_buf, size_t bytes, void *stream,
+                                 fate_dags_t *out);
+fate_status_t fate_layout_dags_opt(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                   const fate_pack_opts_t *opts, void *h_buf, size_t bytes, fate_dags_t *out);
 
 /* fate_pack_state_size: validate a state against a packed batch and the same
  * host DAG arrays it was packed from; return the device bytes needed, the
@@ -317,6 +370,27 @@ fate_status_t fate_score_topk(const fate_dags_t *dags, const fate_state_h *state
  * Errors: EINVAL, ERANGE (k), ESIZE (n_scores < n_cand), EHIP. */
 fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_t n_scores, int32_t k,
                         int32_t *d_idx, float *d_val, void *stream);
+
+/* fate_score_sweep: fate_score_frontier for n_sets (1..FATE_MAX_SWEEP)
+ * parameter sets in one launch - the weight, horizon and variant grids of the
+ * paper's ablations (App. C.3) and sensitivity study (App. D.4, Tab. 6) over
+ * one packed state.  params[p] (host memory) scores into
+ * d_scores + p * score_stride; score_stride >= n_cand, and d_scores holds
+ * n_scores >= score_stride * (n_sets - 1) + n_cand floats.  Set p writes
+ * exactly what fate_score_frontier with params[p] writes.
+ * Errors: those of fate_score_frontier, plus ERANGE (n_sets), ESIZE (stride). */
+fate_status_t fate_score_sweep(const fate_dags_t *dags, const fate_state_h *state, const fate_params_t *params,
+                               int32_t n_sets, float *d_scores, int64_t n_scores, int64_t score_stride,
+                               void *d_ws, size_t ws_bytes, void *stream);
+
+/* fate_topk_sweep: fate_topk for n_sets score arrays at d_scores +
+ * p * score_stride (the layout fate_score_sweep writes); set p's top-k goes to
+ * d_idx / d_val + p * n_frontier * k (n_frontier of the handle: for a
+ * planning state, its capacity).  One launch.
+ * Errors: those of fate_topk, plus ERANGE (n_sets), ESIZE (stride). */
+fate_status_t fate_topk_sweep(const fate_state_h *state, const float *d_scores, int64_t n_scores,
+                              int64_t score_stride, int32_t n_sets, int32_t k, int32_t *d_idx, float *d_val,
+                              void *stream);
 
 #ifdef __cplusplus
 }

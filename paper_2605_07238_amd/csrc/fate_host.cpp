@@ -135,10 +135,14 @@ fate_status_t validate_batch(const fate_cluster_t *c, const fate_dag_batch_t *g,
 // horizon descendants
 // ---------------------------------------------------------------------------
 
-// Breadth-first levels 1..H below every stage of instance b.  With `out`,
-// stores each stage's entries (flat id | depth << 28) ordered by (depth, id);
-// always stores the per-stage counts into count[] (indexed by flat id).
-void instance_horizons(const fate_dag_batch_t *g, int b, int H, uint32_t *count,
+// Horizon descendants of every stage of instance b (Sec. 3.3): with
+// FATE_LEVELS_HOP the stages at breadth-first distance 1..H, each at its
+// minimum distance; with FATE_LEVELS_TOPO the stages reachable from v whose
+// topological level (longest path from a stage without parents) exceeds v's
+// by 1..H, at that difference.  With `out`, stores each stage's entries (flat
+// id | depth << 28) ordered by (depth, id); always stores the per-stage
+// counts into count[] (indexed by flat id).
+void instance_horizons(const fate_dag_batch_t *g, int b, int H, int levels, uint32_t *count,
                        std::vector<uint32_t> *out) {
     const int64_t base = g->stage_off[b];
     const int64_t n = g->stage_off[b + 1] - base;
@@ -155,6 +159,40 @@ void instance_horizons(const fate_dag_batch_t *g, int b, int H, uint32_t *count,
     std::vector<int64_t> stamp(n, -1);
     std::vector<int32_t> cur, nxt;
     if (out) out->clear();
+    if (levels == FATE_LEVELS_TOPO) {
+        std::vector<int32_t> lv(n, 0);  // parents have smaller ids
+        for (int64_t v = 0; v < n; ++v)
+            for (int64_t q = g->par_off[base + v]; q < g->par_off[base + v + 1]; ++q)
+                lv[v] = std::max(lv[v], lv[g->par_idx[q]] + 1);
+        std::vector<int32_t> reach;
+        for (int64_t v = 0; v < n; ++v) {
+            // levels rise along every edge, so nothing below a stage past the
+            // window is inside it
+            reach.clear();
+            stamp[v] = v;
+            cur.assign(1, (int32_t)v);
+            while (!cur.empty()) {
+                nxt.clear();
+                for (int32_t x : cur)
+                    for (int64_t q = cptr[x]; q < cptr[x + 1]; ++q) {
+                        const int32_t c = cidx[q];
+                        if (stamp[c] == v || lv[c] - lv[v] > H) continue;
+                        stamp[c] = v;
+                        nxt.push_back(c);
+                        reach.push_back(c);
+                    }
+                cur.swap(nxt);
+            }
+            std::sort(reach.begin(), reach.end(), [&](int32_t x, int32_t y) {
+                return lv[x] != lv[y] ? lv[x] < lv[y] : x < y;
+            });
+            count[base + v] = (uint32_t)reach.size();
+            if (out)
+                for (int32_t c : reach)
+                    out->push_back((uint32_t)(base + c) | ((uint32_t)(lv[c] - lv[v]) << fate::kDescDepthShift));
+        }
+        return;
+    }
     for (int64_t v = 0; v < n; ++v) {
         uint32_t cnt = 0;
         stamp[v] = v;
@@ -180,10 +218,11 @@ void instance_horizons(const fate_dag_batch_t *g, int b, int H, uint32_t *count,
 }
 
 struct DagLayout {
-    size_t exec, ksw, beta, weight, cap, fits, stage_off, rec, par, desc_off, desc, total;
+    size_t exec, ksw, beta, weight, cap, fits, stage_off, rec, par, desc_off, desc, desc_w, total;
 };
 
-DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc) {
+// desc_w (one float per horizon entry) only with level weights
+DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc, bool level_weights) {
     DagLayout L;
     size_t o = 0;
     L.exec = o; o = align_up(o + sizeof(float) * M * D);
@@ -197,6 +236,7 @@ DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc) {
     L.par = o; o = align_up(o + sizeof(uint32_t) * E);
     L.desc_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
     L.desc = o; o = align_up(o + sizeof(uint32_t) * ndesc);
+    L.desc_w = o; o = align_up(o + (level_weights ? sizeof(float) * ndesc : 0));
     L.total = o;
     return L;
 }
@@ -207,16 +247,23 @@ struct DagsPlan {
     std::vector<std::vector<uint32_t>> lists;  // per instance, when building
 };
 
-fate_status_t plan_dags(const fate_cluster_t *c, const fate_dag_batch_t *g, int H, bool keep, DagsPlan *p) {
+bool opts_ok(const fate_pack_opts_t *o) {
+    return o && (o->levels == FATE_LEVELS_HOP || o->levels == FATE_LEVELS_TOPO) &&
+           (o->level_weights == 0 || o->level_weights == 1);
+}
+
+fate_status_t plan_dags(const fate_cluster_t *c, const fate_dag_batch_t *g, const fate_pack_opts_t &o, bool keep,
+                        DagsPlan *p) {
     fate_status_t st = validate_cluster(c);
     if (st != FATE_OK) return st;
+    const int H = o.H;
     if (H < 0 || H > FATE_MAX_HORIZON) return FATE_ERANGE;
     st = validate_batch(c, g, &p->N, &p->E);
     if (st != FATE_OK) return st;
     p->count.assign(p->N, 0);
     if (keep) p->lists.assign(g->B, {});
     parallel_for(g->B, [&](int64_t b) {
-        instance_horizons(g, (int)b, H, p->count.data(), keep ? &p->lists[b] : nullptr);
+        instance_horizons(g, (int)b, H, o.levels, p->count.data(), keep ? &p->lists[b] : nullptr);
     });
     int64_t tot = 0;
     for (uint32_t x : p->count) tot += x;
@@ -225,13 +272,15 @@ fate_status_t plan_dags(const fate_cluster_t *c, const fate_dag_batch_t *g, int 
     return FATE_OK;
 }
 
-void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, int H, const DagsPlan &p,
-                      const DagLayout &L, uint8_t *base, size_t bytes, fate_dags_t *out) {
+void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, const fate_pack_opts_t &o,
+                      const DagsPlan &p, const DagLayout &L, uint8_t *base, size_t bytes, fate_dags_t *out) {
     std::memset(out, 0, sizeof(*out));
     out->B = g->B;
     out->D = c->D;
     out->M = c->M;
-    out->H = H;
+    out->H = o.H;
+    out->levels = o.levels;
+    out->desc_w = o.level_weights ? reinterpret_cast<const float *>(base + L.desc_w) : nullptr;
     out->N = p.N;
     out->E = p.E;
     out->n_desc = p.ndesc;
@@ -263,7 +312,8 @@ void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, int H,
 }
 
 void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const DagsPlan &p,
-                      const DagLayout &L, uint8_t *img) {
+                      const DagLayout &L, bool level_weights, uint8_t *img) {
+    float *wts = level_weights ? reinterpret_cast<float *>(img + L.desc_w) : nullptr;
     const int D = c->D, M = c->M;
     std::memcpy(img + L.exec, c->exec, sizeof(float) * M * D);
     std::memcpy(img + L.ksw, c->switch_s, sizeof(float) * M * D);
@@ -301,6 +351,19 @@ void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
         }
         if (n > 0 && !p.lists[b].empty())
             std::memcpy(desc + doff[base], p.lists[b].data(), sizeof(uint32_t) * p.lists[b].size());
+    });
+    if (!wts) return;
+    // level weights: 1 / (number of v's horizon stages at that depth), for
+    // the mean-per-level tail; the entries of a stage are ordered by depth
+    parallel_for(p.N, [&](int64_t s) {
+        uint32_t e = doff[s];
+        while (e < doff[s + 1]) {
+            uint32_t f = e;
+            while (f < doff[s + 1] && (desc[f] >> fate::kDescDepthShift) == (desc[e] >> fate::kDescDepthShift)) ++f;
+            const float w = 1.0f / (float)(f - e);
+            for (uint32_t q = e; q < f; ++q) wts[q] = w;
+            e = f;
+        }
     });
 }
 
@@ -531,10 +594,10 @@ fate_status_t copy_to_device(void *d_buf, const void *h, size_t bytes, void *str
 }
 
 bool params_ok(const fate_params_t *p) {
-    const float v[] = {p->lam_q, p->lam_s, p->lam_tr, p->lam_c, p->lam_p, p->kappa_prefix, p->gamma};
+    const float v[] = {p->lam_q, p->lam_s, p->lam_tr, p->lam_c, p->lam_p, p->kappa_prefix, p->gamma, p->lam_m};
     for (float x : v)
         if (!finite_nonneg(x)) return false;
-    return true;
+    return (p->flags & ~(FATE_MEAN_PER_LEVEL | FATE_NO_WINDOWS)) == 0;
 }
 
 }  // namespace
@@ -557,52 +620,80 @@ const char *fate_strerror(fate_status_t s) {
     return "unknown status";
 }
 
-fate_status_t fate_pack_dags_size(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
-                                  size_t *bytes) {
-    if (!bytes) return FATE_EINVAL;
+fate_status_t fate_pack_dags_opt_size(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                      const fate_pack_opts_t *opts, size_t *bytes) {
+    if (!bytes || !opts_ok(opts)) return FATE_EINVAL;
     DagsPlan p;
-    fate_status_t st = plan_dags(cluster, dags, H, false, &p);
+    fate_status_t st = plan_dags(cluster, dags, *opts, false, &p);
     if (st != FATE_OK) return st;
-    *bytes = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc).total;
+    *bytes = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc, opts->level_weights != 0).total;
     return FATE_OK;
 }
 
-static fate_status_t build_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
-                                size_t bytes, std::vector<uint8_t> &img, DagsPlan &p, DagLayout &L) {
-    fate_status_t st = plan_dags(cluster, dags, H, true, &p);
+static fate_status_t build_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                const fate_pack_opts_t &o, size_t bytes, std::vector<uint8_t> &img, DagsPlan &p,
+                                DagLayout &L) {
+    fate_status_t st = plan_dags(cluster, dags, o, true, &p);
     if (st != FATE_OK) return st;
-    L = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc);
+    L = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc, o.level_weights != 0);
     if (bytes < L.total) return FATE_ESIZE;
     img.assign(L.total, 0);
-    write_dags_image(cluster, dags, p, L, img.data());
+    write_dags_image(cluster, dags, p, L, o.level_weights != 0, img.data());
     return FATE_OK;
+}
+
+fate_status_t fate_layout_dags_opt(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                   const fate_pack_opts_t *opts, void *h_buf, size_t bytes, fate_dags_t *out) {
+    if (!h_buf || !out || !opts_ok(opts)) return FATE_EINVAL;
+    std::vector<uint8_t> img;
+    DagsPlan p;
+    DagLayout L;
+    fate_status_t st = build_dags(cluster, dags, *opts, bytes, img, p, L);
+    if (st != FATE_OK) return st;
+    std::memcpy(h_buf, img.data(), L.total);
+    fill_dags_handle(cluster, dags, *opts, p, L, static_cast<uint8_t *>(h_buf), bytes, out);
+    return FATE_OK;
+}
+
+fate_status_t fate_pack_dags_opt(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                 const fate_pack_opts_t *opts, void *d_buf, size_t bytes, void *stream,
+                                 fate_dags_t *out) {
+    if (!d_buf || !out || !opts_ok(opts)) return FATE_EINVAL;
+    std::vector<uint8_t> img;
+    DagsPlan p;
+    DagLayout L;
+    fate_status_t st = build_dags(cluster, dags, *opts, bytes, img, p, L);
+    if (st != FATE_OK) return st;
+    st = copy_to_device(d_buf, img.data(), L.total, stream);
+    if (st != FATE_OK) return st;
+    fill_dags_handle(cluster, dags, *opts, p, L, static_cast<uint8_t *>(d_buf), bytes, out);
+    return FATE_OK;
+}
+
+static fate_pack_opts_t hop_opts(int32_t H) {
+    fate_pack_opts_t o;
+    o.H = H;
+    o.levels = FATE_LEVELS_HOP;
+    o.level_weights = 0;
+    return o;
+}
+
+fate_status_t fate_pack_dags_size(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
+                                  size_t *bytes) {
+    const fate_pack_opts_t o = hop_opts(H);
+    return fate_pack_dags_opt_size(cluster, dags, &o, bytes);
 }
 
 fate_status_t fate_layout_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
                                void *h_buf, size_t bytes, fate_dags_t *out) {
-    if (!h_buf || !out) return FATE_EINVAL;
-    std::vector<uint8_t> img;
-    DagsPlan p;
-    DagLayout L;
-    fate_status_t st = build_dags(cluster, dags, H, bytes, img, p, L);
-    if (st != FATE_OK) return st;
-    std::memcpy(h_buf, img.data(), L.total);
-    fill_dags_handle(cluster, dags, H, p, L, static_cast<uint8_t *>(h_buf), bytes, out);
-    return FATE_OK;
+    const fate_pack_opts_t o = hop_opts(H);
+    return fate_layout_dags_opt(cluster, dags, &o, h_buf, bytes, out);
 }
 
 fate_status_t fate_pack_dags(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, int32_t H,
                              void *d_buf, size_t bytes, void *stream, fate_dags_t *out) {
-    if (!d_buf || !out) return FATE_EINVAL;
-    std::vector<uint8_t> img;
-    DagsPlan p;
-    DagLayout L;
-    fate_status_t st = build_dags(cluster, dags, H, bytes, img, p, L);
-    if (st != FATE_OK) return st;
-    st = copy_to_device(d_buf, img.data(), L.total, stream);
-    if (st != FATE_OK) return st;
-    fill_dags_handle(cluster, dags, H, p, L, static_cast<uint8_t *>(d_buf), bytes, out);
-    return FATE_OK;
+    const fate_pack_opts_t o = hop_opts(H);
+    return fate_pack_dags_opt(cluster, dags, &o, d_buf, bytes, stream, out);
 }
 
 fate_status_t fate_pack_state_size(const fate_dags_t *packed, const fate_dag_batch_t *dags,
@@ -768,14 +859,21 @@ fate_status_t fate_score_ws_size(const fate_dags_t *dags, const fate_state_h *st
     return FATE_OK;
 }
 
+// Scoring launch over P parameter sets: set p writes d_scores + p * stride.
 static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *state, const fate_params_t *params,
-                                float *d_scores, int64_t n_scores, int32_t k, int32_t *d_idx, float *d_val,
-                                void *stream) {
+                                int32_t P, float *d_scores, int64_t n_scores, int64_t stride, int32_t k,
+                                int32_t *d_idx, float *d_val, void *stream) {
     fate_status_t st = check_pair(dags, state);
     if (st != FATE_OK) return st;
-    if (!params || !params_ok(params)) return FATE_EINVAL;
-    if (params->H < 0 || params->H > dags->H) return FATE_EINVAL;
-    if (n_scores < state->n_cand) return FATE_ESIZE;
+    if (!params) return FATE_EINVAL;
+    if (P < 1 || P > FATE_MAX_SWEEP) return FATE_ERANGE;
+    for (int p = 0; p < P; ++p) {
+        if (!params_ok(&params[p])) return FATE_EINVAL;
+        if (params[p].H < 0 || params[p].H > dags->H) return FATE_EINVAL;
+        if ((params[p].flags & FATE_MEAN_PER_LEVEL) && !dags->desc_w) return FATE_EINVAL;
+    }
+    if (stride < state->n_cand) return FATE_ESIZE;
+    if (n_scores < stride * (P - 1) + state->n_cand) return FATE_ESIZE;
     if (state->n_frontier == 0) return FATE_OK;
     if (!d_scores) return FATE_EINVAL;
     fate::ScoreLaunch a;
@@ -783,6 +881,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.par_idx = dags->par_idx;
     a.desc_off = dags->desc_off;
     a.desc = dags->desc;
+    a.desc_w = dags->desc_w;
     a.exec = dags->exec;
     a.ksw = dags->switch_s;
     a.beta = dags->beta;
@@ -800,6 +899,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.done_off = state->done_off;
     a.done = static_cast<const fate::DoneParent *>(state->done);
     a.scores = d_scores;
+    a.score_stride = stride;
     a.dcounts = state->advance ? state->counts : nullptr;
     a.topk = k;
     a.tk_idx = d_idx;
@@ -809,18 +909,26 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.D = dags->D;
     a.M = dags->M;
     a.K = state->K;
-    a.H = params->H;
     a.max_shard = state->max_shard;
     a.beta_uniform = dags->beta_uniform;
     a.slice = fate::slice_len(dags->D);
     a.beta0 = dags->beta0;
-    a.lam_q = params->lam_q;
-    a.lam_s = params->lam_s;
-    a.lam_tr = params->lam_tr;
-    a.lam_c = params->lam_c;
-    a.lam_p = params->lam_p;
-    a.kpf = params->kappa_prefix;
-    a.gamma = params->gamma;
+    a.topo = dags->levels == FATE_LEVELS_TOPO ? 1 : 0;
+    a.nsets = P;
+    for (int p = 0; p < fate::kMaxSets; ++p) {
+        const fate_params_t &q = params[p < P ? p : 0];
+        fate::ParamSet &ps = a.ps[p];
+        ps.lam_q = q.lam_q;
+        ps.lam_s = q.lam_s;
+        ps.lam_tr = q.lam_tr;
+        ps.lam_c = q.lam_c;
+        ps.lam_p = q.lam_p;
+        ps.kpf = q.kappa_prefix;
+        ps.gamma = q.gamma;
+        ps.lam_m = q.lam_m;
+        ps.H = q.H;
+        ps.flags = q.flags;
+    }
     return fate::launch_score(a, stream) == 0 ? FATE_OK : FATE_EHIP;
 }
 
@@ -829,7 +937,16 @@ fate_status_t fate_score_frontier(const fate_dags_t *dags, const fate_state_h *s
                                   void *d_ws, size_t ws_bytes, void *stream) {
     (void)d_ws;
     (void)ws_bytes;
-    return score_impl(dags, state, params, d_scores, n_scores, 0, nullptr, nullptr, stream);
+    return score_impl(dags, state, params, 1, d_scores, n_scores, state ? state->n_cand : 0, 0, nullptr, nullptr,
+                      stream);
+}
+
+fate_status_t fate_score_sweep(const fate_dags_t *dags, const fate_state_h *state, const fate_params_t *params,
+                               int32_t n_sets, float *d_scores, int64_t n_scores, int64_t score_stride,
+                               void *d_ws, size_t ws_bytes, void *stream) {
+    (void)d_ws;
+    (void)ws_bytes;
+    return score_impl(dags, state, params, n_sets, d_scores, n_scores, score_stride, 0, nullptr, nullptr, stream);
 }
 
 fate_status_t fate_score_topk(const fate_dags_t *dags, const fate_state_h *state, const fate_params_t *params,
@@ -839,14 +956,18 @@ fate_status_t fate_score_topk(const fate_dags_t *dags, const fate_state_h *state
     (void)ws_bytes;
     if (k < 1 || k > FATE_MAX_TOPK) return FATE_ERANGE;
     if (state && state->n_frontier > 0 && (!d_idx || !d_val)) return FATE_EINVAL;
-    return score_impl(dags, state, params, d_scores, n_scores, k, d_idx, d_val, stream);
+    return score_impl(dags, state, params, 1, d_scores, n_scores, state ? state->n_cand : 0, k, d_idx, d_val,
+                      stream);
 }
 
-fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_t n_scores, int32_t k,
-                        int32_t *d_idx, float *d_val, void *stream) {
+static fate_status_t topk_impl(const fate_state_h *state, const float *d_scores, int64_t n_scores,
+                               int64_t score_stride, int32_t n_sets, int32_t k, int32_t *d_idx, float *d_val,
+                               void *stream) {
     if (!state) return FATE_EINVAL;
     if (k < 1 || k > FATE_MAX_TOPK) return FATE_ERANGE;
-    if (n_scores < state->n_cand) return FATE_ESIZE;
+    if (n_sets < 1 || n_sets > FATE_MAX_SWEEP) return FATE_ERANGE;
+    if (score_stride < state->n_cand) return FATE_ESIZE;
+    if (n_scores < score_stride * (n_sets - 1) + state->n_cand) return FATE_ESIZE;
     if (state->n_frontier == 0) return FATE_OK;
     if (!d_scores || !d_idx || !d_val || !state->cand_off) return FATE_EINVAL;
     fate::TopkLaunch a;
@@ -856,9 +977,23 @@ fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_
     a.val = d_val;
     a.dcounts = state->advance ? state->counts : nullptr;
     a.nF = state->n_frontier;
+    a.score_stride = score_stride;
+    a.out_stride = state->n_frontier * (int64_t)k;
+    a.nsets = n_sets;
     a.D = state->D;
     a.k = k;
     return fate::launch_topk(a, stream) == 0 ? FATE_OK : FATE_EHIP;
+}
+
+fate_status_t fate_topk(const fate_state_h *state, const float *d_scores, int64_t n_scores, int32_t k,
+                        int32_t *d_idx, float *d_val, void *stream) {
+    return topk_impl(state, d_scores, n_scores, state ? state->n_cand : 0, 1, k, d_idx, d_val, stream);
+}
+
+fate_status_t fate_topk_sweep(const fate_state_h *state, const float *d_scores, int64_t n_scores,
+                              int64_t score_stride, int32_t n_sets, int32_t k, int32_t *d_idx, float *d_val,
+                              void *stream) {
+    return topk_impl(state, d_scores, n_scores, score_stride, n_sets, k, d_idx, d_val, stream);
 }
 
 }  // extern "C"

@@ -33,11 +33,21 @@ static_assert(sizeof(DoneParent) == 16, "completed-parent entry must be 16 bytes
 constexpr uint32_t kDescIdMask = (1u << 28) - 1u;
 constexpr int kDescDepthShift = 28;
 
+// One parameter set of a scoring launch (fate_params_t, as the kernels use
+// it): Sec. 3.4 weights, App. A.3 kappa_prefix, Sec. 3.2 gamma, Sec. 3.3 H,
+// the same-model weight and the variant flags.
+struct ParamSet {
+    float lam_q, lam_s, lam_tr, lam_c, lam_p, kpf, gamma, lam_m;
+    int32_t H, flags;
+};
+constexpr int kMaxSets = FATE_MAX_SWEEP;
+
 struct ScoreLaunch {
     const StageRec *rec;
     const uint32_t *par_idx;
     const uint32_t *desc_off;
     const uint32_t *desc;
+    const float *desc_w;  // level weights (FATE_MEAN_PER_LEVEL), or null
     const float *exec;
     const float *ksw;
     const float *beta;
@@ -54,15 +64,18 @@ struct ScoreLaunch {
     const uint32_t *slices;
     const uint32_t *done_off;
     const DoneParent *done;
-    float *scores;
+    float *scores;            // parameter set p (blockIdx.y) writes scores + p * score_stride
+    int64_t score_stride;
     const uint32_t *dcounts;  // planning state: counts[2] = current slices, else null
     int32_t *tk_idx;  // fused top-k outputs (topk > 0), [nF][topk]
     float *tk_val;
     int32_t topk;
     int64_t nF, n_slices;
-    int32_t D, M, K, H, max_shard, beta_uniform, slice;
+    int32_t D, M, K, max_shard, beta_uniform, slice;
     float beta0;
-    float lam_q, lam_s, lam_tr, lam_c, lam_p, kpf, gamma;
+    int32_t topo;  // descendant lists by topological level (FATE_LEVELS_TOPO)
+    int32_t nsets;
+    ParamSet ps[kMaxSets];
 };
 
 struct TopkLaunch {
@@ -72,6 +85,9 @@ struct TopkLaunch {
     float *val;
     const uint32_t *dcounts;  // planning state: counts[0] = current frontier size, else null
     int64_t nF;               // frontier size, or its capacity with dcounts
+    int64_t score_stride;     // score set p (blockIdx.y) at scores + p * score_stride,
+    int64_t out_stride;       // its top-k at idx / val + p * out_stride
+    int32_t nsets;
     int32_t D, k;
 };
 

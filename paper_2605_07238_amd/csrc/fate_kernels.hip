@@ -493,12 +493,27 @@ __device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, fl
     tr += local ? 0.0f : su * bm;
 }
 
+// Is horizon stage w (record rw, at `depth`) a child of the frontier stage v?
+// With hop levels exactly the depth-1 stages are.  With topological levels a
+// child can sit deeper (another of its parents may have a higher level), so
+// its parent list is searched.
+__device__ __forceinline__ bool child_of(const ScoreLaunch &a, const StageRec &rw, int depth, uint32_t v) {
+    if (depth == 1) return true;
+    if (!a.topo) return false;
+    for (uint32_t q = 0; q < rw.npar; ++q)
+        if (a.par_idx[rw.par_begin + q] == v) return true;
+    return false;
+}
+
 template <int G, bool UNI, bool SLOTS>
 __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     static_assert(!SLOTS || (UNI && G == 16), "the slot layout needs 16-lane groups and uniform beta");
     // a planning state is launched over its slice capacity; the current
     // number of slices is on the device
     if (a.dcounts && blockIdx.x >= a.dcounts[2]) return;
+    // parameter set of this block (a sweep launches one grid row per set)
+    const ParamSet ps = a.ps[blockIdx.y];
+    float *const scores = a.scores + (int64_t)blockIdx.y * a.score_stride;
     extern __shared__ uint64_t smem[];
     uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
     const int tid = threadIdx.x;
@@ -543,10 +558,10 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     if (tid < M) { L.fits[tid] = a.fits[tid]; L.wt[tid] = a.weight[tid]; }
     if (tid == 0) {
         float g = 1.0f;
-        for (int h = 0; h < 16; ++h) { L.gpow[h] = g; g *= a.gamma; }
+        for (int h = 0; h < 16; ++h) { L.gpow[h] = g; g *= ps.gamma; }
         *L.next = 0u;
     }
-    for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = a.lam_s * a.ksw[i]; }
+    for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = ps.lam_s * a.ksw[i]; }
     for (int i = tid; i < P; i += kBlock) {
         uint64_t key = ~0ull;
         if (i < nF) {
@@ -616,7 +631,12 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     const float *exec_col = L.exec + dl;
     const float *ksw_col = L.ksw + dl;
     Entry *area = reinterpret_cast<Entry *>(L.entries) + (tid & ~(G - 1));  // this group's G staging slots
-    const float lam_tr = a.lam_tr, lam_c = a.lam_c, lam_p = a.lam_p;
+    const float lam_tr = ps.lam_tr, lam_c = ps.lam_c, lam_p = ps.lam_p;
+    // same-model weight: a resident model costs -lam_m where an absent one
+    // costs its (weighted) switch time
+    const float res_cost = -ps.lam_m;
+    const bool mean_levels = (ps.flags & FATE_MEAN_PER_LEVEL) != 0;
+    const bool windows_on = (ps.flags & FATE_NO_WINDOWS) == 0;
 
     // Waves claim chunks of consecutive work positions (one per group of the
     // wave) from a shared counter: the largest stages go first and a wave
@@ -644,10 +664,10 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         }
         const bool feas_v = live && bit(sv.elig, lane) && bit(L.fits[mv], lane);
         const float c_v = L.exec[mv * D + dl];
-        const float sw_v = bit(rho, mv) ? 0.0f : L.ksw[mv * D + dl];
+        const float sw_v = bit(rho, mv) ? res_cost : L.ksw[mv * D + dl];
         const float colo_v = sv.npar ? cnt / (float)sv.npar : 0.0f;
-        const float pf_v = hv_cached ? a.kpf * sv.tokens : 0.0f;
-        const float a_imm = a.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
+        const float pf_v = hv_cached ? ps.kpf * sv.tokens : 0.0f;
+        const float a_imm = ps.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
         const float b_imm = c_v + lam_tr * tr - lam_p * pf_v;
         const uint64_t rho_new = load_model(rho, mv, L.cap[dl], L.wt);
         const bool prefix_added = sv.hash != 0 && !hv_cached;
@@ -663,7 +683,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             uint32_t ent = 0;
             if (valid) {
                 ent = a.desc[e];
-                valid = (int)(ent >> kDescDepthShift) <= a.H;
+                valid = (int)(ent >> kDescDepthShift) <= ps.H;
             }
             if (valid) {
                 const uint32_t w = ent & kDescIdMask;
@@ -674,13 +694,13 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 Entry &E = area[lane];
                 E.feas = (Mask)(rw.elig & L.fits[rw.model]);
                 E.pfdevs = table_find<Mask>(L, rw.hash);
-                E.gh = L.gpow[depth];
+                E.gh = mean_levels ? L.gpow[depth] * a.desc_w[e] : L.gpow[depth];
                 const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
                 E.cw = cw;
-                E.pfp = lam_p * a.kpf * rw.tokens;
+                E.pfp = lam_p * ps.kpf * rw.tokens;
                 E.moff = (uint32_t)rw.model * (uint32_t)D;
                 E.model = rw.model;
-                E.flags = (uint8_t)((depth == 1 ? 1 : 0) | (rw.hash != 0 && rw.hash == sv.hash ? 2 : 0));
+                E.flags = (uint8_t)((child_of(a, rw, depth, sv.v) ? 1 : 0) | (rw.hash != 0 && rw.hash == sv.hash ? 2 : 0));
                 E.dn = (uint16_t)dn;
                 E.dbeg = db;
                 float base_tr = 0.0f;
@@ -729,8 +749,8 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             const bool in_new = ((rho_new >> mw) & 1ull) != 0;
             const bool pf_old = (pfd & mybit) != 0;
             const bool pf_new = pf_old || ((flags & 2) && prefix_added);
-            const float Braw = X + (in_old ? 0.0f : sw) - (pf_old ? pfp : 0.0f);
-            const float Bnew = X + (in_new ? 0.0f : sw) - (pf_new ? pfp : 0.0f) - (child ? cw : 0.0f);
+            const float Braw = X + (in_old ? res_cost : sw) - (pf_old ? pfp : 0.0f);
+            const float Bnew = X + (in_new ? res_cost : sw) - (pf_new ? pfp : 0.0f) - (child ? cw : 0.0f);
             const bool fw = (feas & mybit) != 0;
             const float Bd = fw ? Braw : inf_f();
             const float inval = fw ? Bnew : inf_f();
@@ -761,7 +781,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 if (k >= 3) m = fmaxf(m, dpp_b0<0x102>(y));
                 if (k >= 4) m = fmaxf(m, dpp_b0<0x103>(y));
                 const uint32_t wm = (1u << k) - 1u;
-                w_ok[s] = s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
+                w_ok[s] = windows_on && s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
                 // gather with uniform beta: each of the k-1 other devices sends sigma/k
                 w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma / (float)k);
             }
@@ -776,7 +796,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 uint32_t ent = 0;
                 if (valid) {
                     ent = a.desc[e];
-                    valid = (int)(ent >> kDescDepthShift) <= a.H;
+                    valid = (int)(ent >> kDescDepthShift) <= ps.H;
                 }
                 if (valid) {
                     const uint32_t w = ent & kDescIdMask;
@@ -806,10 +826,10 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     // once v runs on a device, that device also caches grp(v)
                     S.m2 = (same ? 0xffffu : pfo) | (ph[2] << 16);
                     S.mdn = (uint32_t)rw.model | (dn << 8);
-                    S.gh = L.gpow[depth];
+                    S.gh = mean_levels ? L.gpow[depth] * a.desc_w[e] : L.gpow[depth];
                     S.xbase = base_tr;
-                    S.pfp = lam_p * a.kpf * rw.tokens;
-                    S.ccw = depth == 1 ? -cw : 0.0f;
+                    S.pfp = lam_p * ps.kpf * rw.tokens;
+                    S.ccw = child_of(a, rw, depth, sv.v) ? -cw : 0.0f;
                     S.dbeg = db;
                     S.ph01 = ph[0] | (ph[1] << 16);
                     S.pw0 = pw[0];
@@ -857,8 +877,8 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     const bool fw = (q0.y & bit_lo) != 0;
                     const bool pf_old = (q0.y & bit_hi) != 0;
                     const bool pf_new = (q0.z & bit_lo) != 0;
-                    const float Braw = X + (in_old ? 0.0f : sw) - (pf_old ? q1.z : 0.0f);
-                    const float Bnew = X + (in_new ? 0.0f : sw) - (pf_new ? q1.z : 0.0f) + q1.w;
+                    const float Braw = X + (in_old ? res_cost : sw) - (pf_old ? q1.z : 0.0f);
+                    const float Bnew = X + (in_new ? res_cost : sw) - (pf_new ? q1.z : 0.0f) + q1.w;
                     const bool child = __float_as_int(q1.w) < 0;
                     const float inval = fw ? Bnew : inf_f();
                     // outside S: a child also receives v's output there
@@ -890,13 +910,13 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
 
             // ---- emit scores
             const float psi0 = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
-            if (live) a.scores[c0 + lane] = psi0;
+            if (live) scores[c0 + lane] = psi0;
             uint32_t off = c0 + (uint32_t)D;
 #pragma unroll
             for (int s = 0; s < 3; ++s) {
                 if (s >= nk) break;  // uniform
                 const int k = s + 2;
-                if (lane <= D - k) a.scores[off + lane] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
+                if (lane <= D - k) scores[off + lane] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
                 off += (uint32_t)(D - k + 1);
             }
             continue;
@@ -928,7 +948,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 if (q < k) tmax = fmaxf(tmax, aq + bq / (float)k);
             }
             const uint64_t wm = ((1ull << k) - 1ull) << i;
-            const bool feasible = (t < nwin) && ((feas_mask & wm) == wm);
+            const bool feasible = windows_on && (t < nwin) && ((feas_mask & wm) == wm);
             float gat = inf_f();
             if (feasible) {
                 for (int p = i; p < i + k; ++p) {
@@ -1021,12 +1041,12 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
 
         // ---- emit scores
         const float psi0 = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
-        if (live) a.scores[c0 + lane] = psi0;
+        if (live) scores[c0 + lane] = psi0;
 #pragma unroll
         for (int s = 0; s < 3; ++s) {
             if (s >= wslots) continue;  // uniform
             const int t = lane + s * G;
-            if (t < nwin) a.scores[c0 + D + t] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
+            if (t < nwin) scores[c0 + D + t] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
         }
     }
 
@@ -1050,7 +1070,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 f[r] = (int64_t)f0 + si;
             }
         }
-        rank_stages<G, kRounds>(a.scores, c0, C, f, lane, a.topk, a.tk_idx, a.tk_val);
+        rank_stages<G, kRounds>(scores, c0, C, f, lane, a.topk, a.tk_idx, a.tk_val);
     }
 }
 
@@ -1075,7 +1095,8 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
             f[r] = fr;
         }
     }
-    rank_stages<G, kTopkRounds>(a.scores, c0, C, f, lane, a.k, a.idx, a.val);
+    const int64_t so = (int64_t)blockIdx.y * a.score_stride, oo = (int64_t)blockIdx.y * a.out_stride;
+    rank_stages<G, kTopkRounds>(a.scores + so, c0, C, f, lane, a.k, a.idx + oo, a.val + oo);
 }
 
 }  // namespace
@@ -1085,7 +1106,7 @@ static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int G = group_width(a.D);
     const int sb = G == 16 ? staging_bytes<16>() : G <= 32 ? staging_bytes<8>() : staging_bytes<64>();
     const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb).total;
-    const dim3 grid((unsigned)a.n_slices), block(kBlock);
+    const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block(kBlock);
     switch (G) {
         case 4: hipLaunchKernelGGL((k_score<4, UNI, false>), grid, block, lds, s, a); break;
         case 8: hipLaunchKernelGGL((k_score<8, UNI, false>), grid, block, lds, s, a); break;
@@ -1110,12 +1131,13 @@ int launch_topk(const TopkLaunch &a, void *stream) {
     const int64_t per_block = (int64_t)(kBlock / G) * kTopkRounds;
     const int64_t blocks = (a.nF + per_block - 1) / per_block;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const dim3 grid((unsigned)blocks, (unsigned)a.nsets);
     switch (G) {
-        case 4: hipLaunchKernelGGL(k_topk<4>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        case 8: hipLaunchKernelGGL(k_topk<8>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        case 16: hipLaunchKernelGGL(k_topk<16>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        case 32: hipLaunchKernelGGL(k_topk<32>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
-        default: hipLaunchKernelGGL(k_topk<64>, dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
+        case 4: hipLaunchKernelGGL(k_topk<4>, grid, dim3(kBlock), 0, s, a); break;
+        case 8: hipLaunchKernelGGL(k_topk<8>, grid, dim3(kBlock), 0, s, a); break;
+        case 16: hipLaunchKernelGGL(k_topk<16>, grid, dim3(kBlock), 0, s, a); break;
+        case 32: hipLaunchKernelGGL(k_topk<32>, grid, dim3(kBlock), 0, s, a); break;
+        default: hipLaunchKernelGGL(k_topk<64>, grid, dim3(kBlock), 0, s, a); break;
     }
     return (int)hipGetLastError();
 }

@@ -30,7 +30,13 @@ STATUS_NAMES = {0: "FATE_OK", -1: "FATE_EINVAL", -2: "FATE_ERANGE", -3: "FATE_EC
 EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_dags", "fate_layout_dags",
            "fate_pack_state_size", "fate_pack_state", "fate_layout_state", "fate_score_ws_size",
            "fate_score_frontier", "fate_score_topk", "fate_topk", "fate_pack_state_advance_size",
-           "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance"]
+           "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance", "fate_pack_dags_opt_size",
+           "fate_pack_dags_opt", "fate_layout_dags_opt", "fate_score_sweep", "fate_topk_sweep"]
+
+# Scoring variants and packing options (fate_params_t.flags, fate_pack_opts_t.levels).
+FATE_MEAN_PER_LEVEL, FATE_NO_WINDOWS = 1, 2
+FATE_LEVELS_HOP, FATE_LEVELS_TOPO = 0, 1
+FATE_MAX_SWEEP = 16
 
 
 class FateError(RuntimeError):
@@ -58,7 +64,12 @@ class State(C.Structure):
 
 class Params(C.Structure):
     _fields_ = [("lam_q", C.c_float), ("lam_s", C.c_float), ("lam_tr", C.c_float), ("lam_c", C.c_float),
-                ("lam_p", C.c_float), ("kappa_prefix", C.c_float), ("gamma", C.c_float), ("H", C.c_int32)]
+                ("lam_p", C.c_float), ("kappa_prefix", C.c_float), ("gamma", C.c_float), ("H", C.c_int32),
+                ("lam_m", C.c_float), ("flags", C.c_int32)]
+
+
+class PackOpts(C.Structure):
+    _fields_ = [("H", C.c_int32), ("levels", C.c_int32), ("level_weights", C.c_int32)]
 
 
 class Dags(C.Structure):
@@ -69,7 +80,7 @@ class Dags(C.Structure):
                 ("exec", C.c_void_p), ("switch_s", C.c_void_p), ("beta", C.c_void_p),
                 ("weight", C.c_void_p), ("cap", C.c_void_p), ("fits", C.c_void_p),
                 ("records", C.c_void_p), ("par_idx", C.c_void_p), ("desc_off", C.c_void_p),
-                ("desc", C.c_void_p), ("stage_off", C.c_void_p)]
+                ("desc", C.c_void_p), ("stage_off", C.c_void_p), ("levels", C.c_int32), ("desc_w", C.c_void_p)]
 
 
 class StateH(C.Structure):
@@ -121,6 +132,14 @@ def load(path: Optional[str] = None):
     lib.fate_commit_ws_size.argtypes = [P(Dags), P(StateH), P(C.c_size_t)]
     lib.fate_commit_advance.argtypes = [P(Dags), P(StateH), C.c_void_p, C.c_int32, C.c_void_p, C.c_size_t,
                                         C.c_void_p]
+    lib.fate_pack_dags_opt_size.argtypes = [P(Cluster), P(DagBatch), P(PackOpts), P(C.c_size_t)]
+    lib.fate_pack_dags_opt.argtypes = [P(Cluster), P(DagBatch), P(PackOpts), C.c_void_p, C.c_size_t, C.c_void_p,
+                                       P(Dags)]
+    lib.fate_layout_dags_opt.argtypes = [P(Cluster), P(DagBatch), P(PackOpts), C.c_void_p, C.c_size_t, P(Dags)]
+    lib.fate_score_sweep.argtypes = [P(Dags), P(StateH), P(Params), C.c_int32, C.c_void_p, C.c_int64, C.c_int64,
+                                     C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.fate_topk_sweep.argtypes = [P(StateH), C.c_void_p, C.c_int64, C.c_int64, C.c_int32, C.c_int32, C.c_void_p,
+                                    C.c_void_p, C.c_void_p]
     for name in EXPORTS[2:]:
         getattr(lib, name).restype = st
     if path is None:
@@ -225,32 +244,45 @@ def fate_pack_dags_size(w, H: int) -> int:
     return int(nbytes.value)
 
 
-def fate_pack_dags(w, H: Optional[int] = None, device="cuda", stream=None) -> PackedDags:
-    """Validate and pack workload ``w``'s DAG batch into a device buffer."""
+def _pack_opts(w, H, levels, level_weights) -> PackOpts:
+    p = dict(w.params) if w is not None else {}
+    lv = int(levels if levels is not None else (FATE_LEVELS_TOPO if p.get("topo_levels") else FATE_LEVELS_HOP))
+    lw = int(bool(level_weights if level_weights is not None else p.get("mean_levels", 0)))
+    return PackOpts(int(w.H if H is None else H), lv, lw)
+
+
+def fate_pack_dags(w, H: Optional[int] = None, device="cuda", stream=None, levels: Optional[int] = None,
+                   level_weights: Optional[bool] = None) -> PackedDags:
+    """Validate and pack workload ``w``'s DAG batch into a device buffer.
+    ``levels`` (FATE_LEVELS_HOP / _TOPO) and ``level_weights`` default to the
+    workload's ``topo_levels`` / ``mean_levels`` parameters."""
     import torch
-    H = int(w.H if H is None else H)
+    o = _pack_opts(w, H, levels, level_weights)
     lib = load()
     hi = HostInputs(w)
     nbytes = C.c_size_t(0)
-    _check(lib.fate_pack_dags_size(C.byref(hi.cluster), C.byref(hi.batch), H, C.byref(nbytes)), "fate_pack_dags_size")
+    _check(lib.fate_pack_dags_opt_size(C.byref(hi.cluster), C.byref(hi.batch), C.byref(o), C.byref(nbytes)),
+           "fate_pack_dags_opt_size")
     buf = torch.empty(max(1, nbytes.value), dtype=torch.uint8, device=device)
     h = Dags()
-    _check(lib.fate_pack_dags(C.byref(hi.cluster), C.byref(hi.batch), H, C.c_void_p(buf.data_ptr()),
-                              nbytes.value, C.c_void_p(_stream_ptr(stream)), C.byref(h)), "fate_pack_dags")
+    _check(lib.fate_pack_dags_opt(C.byref(hi.cluster), C.byref(hi.batch), C.byref(o), C.c_void_p(buf.data_ptr()),
+                                  nbytes.value, C.c_void_p(_stream_ptr(stream)), C.byref(h)), "fate_pack_dags_opt")
     return PackedDags(buf, h, hi)
 
 
-def fate_layout_dags(w, H: Optional[int] = None):
+def fate_layout_dags(w, H: Optional[int] = None, levels: Optional[int] = None,
+                     level_weights: Optional[bool] = None):
     """Host-only packed image of the DAG batch: (numpy uint8 buffer, Dags handle)."""
-    H = int(w.H if H is None else H)
+    o = _pack_opts(w, H, levels, level_weights)
     lib = load()
     hi = HostInputs(w)
     nbytes = C.c_size_t(0)
-    _check(lib.fate_pack_dags_size(C.byref(hi.cluster), C.byref(hi.batch), H, C.byref(nbytes)), "fate_pack_dags_size")
+    _check(lib.fate_pack_dags_opt_size(C.byref(hi.cluster), C.byref(hi.batch), C.byref(o), C.byref(nbytes)),
+           "fate_pack_dags_opt_size")
     buf = np.zeros(max(1, nbytes.value), np.uint8)
     h = Dags()
-    _check(lib.fate_layout_dags(C.byref(hi.cluster), C.byref(hi.batch), H, buf.ctypes.data, nbytes.value,
-                                C.byref(h)), "fate_layout_dags")
+    _check(lib.fate_layout_dags_opt(C.byref(hi.cluster), C.byref(hi.batch), C.byref(o), buf.ctypes.data,
+                                    nbytes.value, C.byref(h)), "fate_layout_dags_opt")
     return buf, h, hi
 
 
@@ -306,7 +338,9 @@ def make_params(w=None, H: Optional[int] = None, **over) -> Params:
         p.update(w.params)
     p.update({k: v for k, v in over.items() if k != "H"})
     Hv = int(H if H is not None else (w.H if w is not None else 0))
-    return Params(p["lam_q"], p["lam_s"], p["lam_tr"], p["lam_c"], p["lam_p"], p["kappa_prefix"], p["gamma"], Hv)
+    flags = (FATE_MEAN_PER_LEVEL if p.get("mean_levels") else 0) | (FATE_NO_WINDOWS if p.get("no_windows") else 0)
+    return Params(p["lam_q"], p["lam_s"], p["lam_tr"], p["lam_c"], p["lam_p"], p["kappa_prefix"], p["gamma"], Hv,
+                  float(p.get("lam_m", 0.0)), flags)
 
 
 def fate_score_frontier(packed: PackedDags, state: PackedState, params: Params, out=None, stream=None):
@@ -364,6 +398,43 @@ def fate_topk(state: PackedState, scores, k: int, idx=None, val=None, stream=Non
                          C.c_void_p(idx.data_ptr()), C.c_void_p(val.data_ptr()),
                          C.c_void_p(_stream_ptr(stream))), "fate_topk")
     return idx[:F], val[:F]
+
+
+def fate_score_sweep(packed: PackedDags, state: PackedState, params, out=None, stride: Optional[int] = None,
+                     stream=None):
+    """Score every candidate under each of ``params`` (a list of Params, at
+    most FATE_MAX_SWEEP) in one launch; returns a float32 device tensor
+    [len(params), stride] (set p in row p)."""
+    import torch
+    lib = load()
+    P = len(params)
+    stride = int(stride if stride is not None else max(1, state.n_cand))
+    if out is None:
+        out = torch.empty((max(1, P), stride), dtype=torch.float32, device=packed.buf.device)
+    arr = (Params * max(1, P))(*params)
+    _check(lib.fate_score_sweep(C.byref(packed.handle), C.byref(state.handle), arr, int(P),
+                                C.c_void_p(out.data_ptr()), int(out.numel()), stride, None, 0,
+                                C.c_void_p(_stream_ptr(stream))), "fate_score_sweep")
+    return out
+
+
+def fate_topk_sweep(state: PackedState, scores, k: int, idx=None, val=None, stream=None):
+    """Top-k of every row of a [P, stride] score tensor (the fate_score_sweep
+    layout); returns (int32 [P, F, k], float32 [P, F, k]) device tensors, F the
+    handle's frontier size (its capacity for a planning state)."""
+    import torch
+    lib = load()
+    P, stride = int(scores.shape[0]), int(scores.shape[1])
+    F = state.n_frontier
+    dev = scores.device
+    if idx is None:
+        idx = torch.empty((P, max(1, F), k), dtype=torch.int32, device=dev)
+    if val is None:
+        val = torch.empty((P, max(1, F), k), dtype=torch.float32, device=dev)
+    _check(lib.fate_topk_sweep(C.byref(state.handle), C.c_void_p(scores.data_ptr()), int(scores.numel()), stride,
+                               P, int(k), C.c_void_p(idx.data_ptr()), C.c_void_p(val.data_ptr()),
+                               C.c_void_p(_stream_ptr(stream))), "fate_topk_sweep")
+    return idx[:, :F], val[:, :F]
 
 
 def fate_commit_ws_size(packed: PackedDags, state: PackedState) -> int:

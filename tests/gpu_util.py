@@ -13,7 +13,10 @@ RTOL = 1e-5  # relative to the sum of absolute weighted terms
 
 def run_gpu(w, H=None, params=None, max_shard=None, k=4, pack_H=None):
     import torch
-    pk = fate.fate_pack_dags(w, H=pack_H if pack_H is not None else (w.H if H is None else H))
+    pp = dict(w.params, **(params or {}))
+    pk = fate.fate_pack_dags(w, H=pack_H if pack_H is not None else (w.H if H is None else H),
+                             levels=fate.FATE_LEVELS_TOPO if pp.get("topo_levels") else fate.FATE_LEVELS_HOP,
+                             level_weights=bool(pp.get("mean_levels")))
     st = fate.fate_pack_state(pk, w, max_shard=max_shard)
     p = fate.make_params(w, H=(w.H if H is None else H), **(params or {}))
     scores = fate.fate_score_frontier(pk, st, p)

@@ -259,3 +259,93 @@ def test_planning_state_size_and_commit_errors():
     assert sh.advance == 0
     assert lib.fate_commit_ws_size(C.byref(h), C.byref(sh), C.byref(ws)) == fate.FATE_EINVAL
     assert lib.fate_commit_advance(C.byref(h), C.byref(sh), None, 1, None, 0, None) == fate.FATE_EINVAL
+
+
+def _levels_bf(adj):
+    """Longest-path levels from Bellman-Ford shortest paths on -1 weights."""
+    n = adj.shape[0]
+    neg = sp.csr_matrix((-np.ones(adj.nnz), adj.indices, adj.indptr), shape=(n, n))
+    d = shortest_path(neg, method="BF", directed=True)
+    return np.maximum(np.where(np.isfinite(d), -d, 0.0).max(axis=0), 0.0).astype(np.int64)
+
+
+@pytest.mark.parametrize("maker", [
+    lambda: synth.make_workload("layered-1024x200-d8", B=2),
+    lambda: synth.make_random_small(4, B=3, n=20, p_edge=0.35, H=3),
+    lambda: synth.make_random_small(5, B=2, n=25, p_edge=0.5, H=5),
+])
+def test_topological_level_lists_and_weights(maker):
+    """With topological levels the lists hold every stage reachable from v whose
+    longest-path level exceeds v's by 1..H, at that difference, ordered by
+    (depth, id); level weights are 1 / (entries at that depth)."""
+    w = maker()
+    H = min(int(w.H), 4)
+    buf, h, _ = fate.fate_layout_dags(w, H=H, levels=fate.FATE_LEVELS_TOPO, level_weights=True)
+    assert int(h.levels) == fate.FATE_LEVELS_TOPO and h.desc_w
+    u = unpack_dags(buf, h)
+    wts = _view(buf, buf.ctypes.data, h.desc_w, np.float32, int(h.n_desc))
+    for b in range(w.B):
+        lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
+        n = hi - lo
+        rows, cols = [], []
+        for x in range(n):
+            for p in w.par_idx[w.par_off[lo + x]:w.par_off[lo + x + 1]]:
+                rows.append(int(p))
+                cols.append(x)
+        adj = sp.csr_matrix((np.ones(len(rows)), (rows, cols)), shape=(n, n))
+        reach = np.isfinite(shortest_path(adj, directed=True, unweighted=True))
+        lv = _levels_bf(adj)
+        for v in range(n):
+            e0, e1 = u["desc_off"][lo + v], u["desc_off"][lo + v + 1]
+            ents = u["desc"][e0:e1]
+            got = [(int(e >> 28), int(e & ((1 << 28) - 1)) - lo) for e in ents]
+            exp = sorted((int(lv[x] - lv[v]), x) for x in range(n)
+                         if x != v and reach[v, x] and 1 <= lv[x] - lv[v] <= H)
+            assert got == exp, (b, v)
+            depths = np.array([d for d, _ in got], np.int64)
+            if len(depths):
+                cnt = np.bincount(depths)[depths]
+                assert np.array_equal(wts[e0:e1], (1.0 / cnt).astype(np.float32)), (b, v)
+
+
+def test_hop_options_give_the_plain_image():
+    w = synth.make_random_small(6, B=3, n=20, p_edge=0.35, H=3)
+    a, ha, _ = fate.fate_layout_dags(w)
+    b, hb, _ = fate.fate_layout_dags(w, levels=fate.FATE_LEVELS_HOP, level_weights=False)
+    assert int(ha.n_desc) == int(hb.n_desc) and not hb.desc_w
+    assert np.array_equal(a[:int(ha.bytes) if ha.bytes else len(a)], b[:len(a)])
+    c, hc, _ = fate.fate_layout_dags(w, level_weights=True)  # weights appended after the lists
+    uc, ua = unpack_dags(c, hc), unpack_dags(a, ha)
+    assert np.array_equal(uc["desc"], ua["desc"]) and np.array_equal(uc["desc_off"], ua["desc_off"])
+
+
+def test_pack_option_and_flag_errors():
+    import ctypes as C
+    w = synth.make_random_small(7, B=1, n=10, D=4)
+    lib = fate.load()
+    hi = fate.HostInputs(w)
+    for lv, lw in ((2, 0), (-1, 0), (0, 2)):
+        o = fate.PackOpts(int(w.H), lv, lw)
+        n = C.c_size_t(0)
+        assert lib.fate_pack_dags_opt_size(C.byref(hi.cluster), C.byref(hi.batch), C.byref(o), C.byref(n)) \
+            == fate.FATE_EINVAL, (lv, lw)
+    assert lib.fate_pack_dags_opt_size(C.byref(hi.cluster), C.byref(hi.batch), None, C.byref(n)) == fate.FATE_EINVAL
+    # scoring validates parameters before touching any device memory
+    _, dh, _ = fate.fate_layout_dags(w)
+    _, sh, _ = fate.fate_layout_state(dh, w)
+    for over in (dict(flags=4), dict(lam_m=-1.0), dict(lam_m=float("nan")), dict(flags=fate.FATE_MEAN_PER_LEVEL)):
+        p = fate.make_params(w)
+        for k, v in over.items():
+            setattr(p, k, v)
+        st = lib.fate_score_frontier(C.byref(dh), C.byref(sh), C.byref(p), None, 1 << 20, None, 0, None)
+        assert st == fate.FATE_EINVAL, over
+    p = fate.make_params(w)
+    arr = (fate.Params * 17)(*([p] * 17))
+    st = lib.fate_score_sweep(C.byref(dh), C.byref(sh), arr, 17, None, 1 << 20, int(sh.n_cand), None, 0, None)
+    assert st == fate.FATE_ERANGE
+    st = lib.fate_score_sweep(C.byref(dh), C.byref(sh), arr, 0, None, 1 << 20, int(sh.n_cand), None, 0, None)
+    assert st == fate.FATE_ERANGE
+    st = lib.fate_score_sweep(C.byref(dh), C.byref(sh), arr, 2, None, 1 << 20, int(sh.n_cand) - 1, None, 0, None)
+    assert st == fate.FATE_ESIZE
+    st = lib.fate_topk_sweep(C.byref(sh), None, 1 << 20, int(sh.n_cand), 17, 4, None, None, None)
+    assert st == fate.FATE_ERANGE
