@@ -175,6 +175,95 @@ def commit_bytes(pk, st):
             + 4 * B + 16)
 
 
+def sweep_grid(w, H_max=4):
+    """The sensitivity grid of App. D.4 (Tab. 6: H = 0..4, then the state,
+    locality and prefix weight groups at x0.5 and x1.5 with H = 4) and the
+    scoring-side ablations of App. C.3 (locality off, prefix off, no windows)."""
+    from paper_2605_07238_amd import fate
+    b = dict(w.params)
+    lm = float(b.get("lam_m", 0.0))
+    sets, names = [], []
+    for H in range(H_max + 1):
+        sets.append(fate.make_params(w, H=H))
+        names.append("H=%d" % H)
+    for f in (0.5, 1.5):
+        sets.append(fate.make_params(w, H=H_max, lam_s=b["lam_s"] * f, lam_m=lm * f))
+        names.append("state x%g" % f)
+        sets.append(fate.make_params(w, H=H_max, lam_tr=b["lam_tr"] * f, lam_c=b["lam_c"] * f))
+        names.append("locality x%g" % f)
+        sets.append(fate.make_params(w, H=H_max, lam_p=b["lam_p"] * f))
+        names.append("prefix x%g" % f)
+    sets.append(fate.make_params(w, H=H_max, lam_tr=0.0, lam_c=0.0))
+    names.append("w/o locality")
+    sets.append(fate.make_params(w, H=H_max, lam_p=0.0))
+    names.append("w/o prefix")
+    sets.append(fate.make_params(w, H=H_max, no_windows=1))
+    names.append("w/o shard")
+    return sets, names
+
+
+def sweep_bench(w, k, reps, log):
+    """One fate_score_sweep + fate_topk_sweep launch over the grid of
+    sweep_grid, against the same sets scored and ranked one call at a time;
+    every set's scores must match the single call bit for bit."""
+    import torch
+    from paper_2605_07238_amd import fate
+    H_max = 4
+    pk = fate.fate_pack_dags(w, H=H_max)
+    st = fate.fate_pack_state(pk, w)
+    sets, names = sweep_grid(w, H_max)
+    P, nc = len(sets), st.n_cand
+    out = torch.empty((P, max(1, nc)), dtype=torch.float32, device="cuda")
+    idx = torch.empty((P, max(1, st.n_frontier), k), dtype=torch.int32, device="cuda")
+    val = torch.empty_like(idx, dtype=torch.float32)
+    one = torch.empty(max(1, nc), dtype=torch.float32, device="cuda")
+    i1 = torch.empty((max(1, st.n_frontier), k), dtype=torch.int32, device="cuda")
+    v1 = torch.empty_like(i1, dtype=torch.float32)
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+
+    def sweep():
+        fate.fate_score_sweep(pk, st, sets, out=out)
+        fate.fate_topk_sweep(st, out, k, idx=idx, val=val)
+
+    def singles():
+        for prm in sets:
+            fate.fate_score_frontier(pk, st, prm, out=one)
+            fate.fate_topk(st, one, k, idx=i1, val=v1)
+
+    t = {}
+    for name, fn in (("sweep", sweep), ("single_calls", singles)):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = mk(), mk()
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        t[name] = float(np.median(ts))
+    sweep()
+    torch.cuda.synchronize()
+    same = True
+    host = out.cpu().numpy()
+    for p_, prm in enumerate(sets):
+        fate.fate_score_frontier(pk, st, prm, out=one)
+        torch.cuda.synchronize()
+        same = same and np.array_equal(host[p_, :nc].view(np.uint32), one[:nc].cpu().numpy().view(np.uint32))
+    evals, seen = 0, {}
+    for p_, prm in enumerate(sets):  # the count depends on H and on which candidates are feasible
+        key = (int(prm.H), int(prm.flags) & fate.FATE_NO_WINDOWS)
+        if key not in seen:
+            seen[key] = counted_work(w, pk, st, host[p_, :nc], int(prm.H))[0]
+        evals += seen[key]
+    log("sweep: %d sets in %.3f ms (one launch each for scores and top-k), %.3f ms as single calls"
+        % (P, t["sweep"], t["single_calls"]))
+    return dict(sets=names, H_packed=H_max, ms=t["sweep"], single_calls_ms=t["single_calls"],
+                evals=evals, evals_per_s=evals / (t["sweep"] * 1e-3), bitwise_equal_to_single_calls=bool(same),
+                kernels="k_score (grid rows = parameter sets) + k_topk")
+
+
 def planning_loop(w, pk, params, k, steps, log):
     """Repeated planning steps on the device: score, top-k, then commit each
     frontier stage's best candidate; per-step kernel times from HIP events."""
@@ -258,6 +347,8 @@ def main():
     ap.add_argument("--planning-steps", type=int, default=6,
                     help="after the timed steps, run this many score / top-k / commit-and-advance planning steps "
                          "on a planning state and report them (0 = skip)")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the parameter-sweep measurement (fate_score_sweep over the sensitivity grid)")
     ap.add_argument("--no-medians", action="store_true",
                     help="skip the extra median timings of the three launch variants (profiling runs)")
     ap.add_argument("--describe", action="store_true",
@@ -419,6 +510,8 @@ def main():
     }
     if args.planning_steps > 0:
         out["planning_loop"] = planning_loop(w, pk, params, args.topk, args.planning_steps, log)
+    if not args.no_sweep:
+        out["sweep"] = sweep_bench(w, args.topk, 5, log)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host ...")
         dt, passes, threads = cpu_baseline(w, H)

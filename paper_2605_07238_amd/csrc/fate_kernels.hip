@@ -505,12 +505,16 @@ __device__ __forceinline__ bool child_of(const ScoreLaunch &a, const StageRec &r
     return false;
 }
 
-template <int G, bool UNI, bool SLOTS>
+// VAR = false compiles the scoring variants out (no same-model weight, sum
+// over levels, windows on, hop levels); the launcher picks it when no
+// parameter set of the launch uses a variant.
+template <int G, bool UNI, bool SLOTS, bool VAR>
 __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     static_assert(!SLOTS || (UNI && G == 16), "the slot layout needs 16-lane groups and uniform beta");
     // a planning state is launched over its slice capacity; the current
     // number of slices is on the device
-    if (a.dcounts && blockIdx.x >= a.dcounts[2]) return;
+    const uint32_t slice = blockIdx.x;
+    if (a.dcounts && slice >= a.dcounts[2]) return;
     // parameter set of this block (a sweep launches one grid row per set)
     const ParamSet ps = a.ps[blockIdx.y];
     float *const scores = a.scores + (int64_t)blockIdx.y * a.score_stride;
@@ -518,9 +522,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
     const int tid = threadIdx.x;
     const int D = a.D, K = a.K, M = a.M;
-    const uint32_t b = a.slices[3 * blockIdx.x];
-    const uint32_t f0 = a.slices[3 * blockIdx.x + 1];
-    const int nF = (int)(a.slices[3 * blockIdx.x + 2] - f0);
+    const uint32_t b = a.slices[3 * slice];
+    const uint32_t f0 = a.slices[3 * slice + 1];
+    const int nF = (int)(a.slices[3 * slice + 2] - f0);
     const int P = pow2_at_least(nF);
     using Mask = MaskFor<G>;  // device bitmask
     // slot layout: 16-lane groups, uniform beta, at most 32 models (chosen by the launcher)
@@ -634,9 +638,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     const float lam_tr = ps.lam_tr, lam_c = ps.lam_c, lam_p = ps.lam_p;
     // same-model weight: a resident model costs -lam_m where an absent one
     // costs its (weighted) switch time
-    const float res_cost = -ps.lam_m;
-    const bool mean_levels = (ps.flags & FATE_MEAN_PER_LEVEL) != 0;
-    const bool windows_on = (ps.flags & FATE_NO_WINDOWS) == 0;
+    const float res_cost = VAR ? -ps.lam_m : 0.0f;
+    const bool mean_levels = VAR && (ps.flags & FATE_MEAN_PER_LEVEL) != 0;
+    const bool windows_on = !VAR || (ps.flags & FATE_NO_WINDOWS) == 0;
 
     // Waves claim chunks of consecutive work positions (one per group of the
     // wave) from a shared counter: the largest stages go first and a wave
@@ -700,7 +704,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 E.pfp = lam_p * ps.kpf * rw.tokens;
                 E.moff = (uint32_t)rw.model * (uint32_t)D;
                 E.model = rw.model;
-                E.flags = (uint8_t)((child_of(a, rw, depth, sv.v) ? 1 : 0) | (rw.hash != 0 && rw.hash == sv.hash ? 2 : 0));
+                E.flags = (uint8_t)(((VAR ? child_of(a, rw, depth, sv.v) : depth == 1) ? 1 : 0) | (rw.hash != 0 && rw.hash == sv.hash ? 2 : 0));
                 E.dn = (uint16_t)dn;
                 E.dbeg = db;
                 float base_tr = 0.0f;
@@ -829,7 +833,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     S.gh = mean_levels ? L.gpow[depth] * a.desc_w[e] : L.gpow[depth];
                     S.xbase = base_tr;
                     S.pfp = lam_p * ps.kpf * rw.tokens;
-                    S.ccw = child_of(a, rw, depth, sv.v) ? -cw : 0.0f;
+                    S.ccw = (VAR ? child_of(a, rw, depth, sv.v) : depth == 1) ? -cw : 0.0f;
                     S.dbeg = db;
                     S.ph01 = ph[0] | (ph[1] << 16);
                     S.pw0 = pw[0];
@@ -1107,15 +1111,21 @@ static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int sb = G == 16 ? staging_bytes<16>() : G <= 32 ? staging_bytes<8>() : staging_bytes<64>();
     const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb).total;
     const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block(kBlock);
+    bool var = a.topo != 0;
+    for (int p = 0; p < a.nsets; ++p) var = var || a.ps[p].lam_m != 0.0f || a.ps[p].flags != 0;
     switch (G) {
-        case 4: hipLaunchKernelGGL((k_score<4, UNI, false>), grid, block, lds, s, a); break;
-        case 8: hipLaunchKernelGGL((k_score<8, UNI, false>), grid, block, lds, s, a); break;
+        case 4: hipLaunchKernelGGL((k_score<4, UNI, false, true>), grid, block, lds, s, a); break;
+        case 8: hipLaunchKernelGGL((k_score<8, UNI, false, true>), grid, block, lds, s, a); break;
         case 16:
-            if (UNI && a.M <= 32) hipLaunchKernelGGL((k_score<16, UNI, UNI>), grid, block, lds, s, a);
-            else hipLaunchKernelGGL((k_score<16, UNI, false>), grid, block, lds, s, a);
+            if (UNI && a.M <= 32) {
+                if (var) hipLaunchKernelGGL((k_score<16, UNI, UNI, true>), grid, block, lds, s, a);
+                else hipLaunchKernelGGL((k_score<16, UNI, UNI, false>), grid, block, lds, s, a);
+            } else {
+                hipLaunchKernelGGL((k_score<16, UNI, false, true>), grid, block, lds, s, a);
+            }
             break;
-        case 32: hipLaunchKernelGGL((k_score<32, UNI, false>), grid, block, lds, s, a); break;
-        default: hipLaunchKernelGGL((k_score<64, UNI, false>), grid, block, lds, s, a); break;
+        case 32: hipLaunchKernelGGL((k_score<32, UNI, false, true>), grid, block, lds, s, a); break;
+        default: hipLaunchKernelGGL((k_score<64, UNI, false, true>), grid, block, lds, s, a); break;
     }
 }
 
