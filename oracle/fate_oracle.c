@@ -71,6 +71,19 @@
  *     then v is completed with its output held by exactly S.  The next
  *     frontier follows from step 1 on the updated state.
  *
+ * 12. Frontier planning wave (App. A.2 frontier placement problem: each
+ *     device takes at most one shard-slot assignment per wave, each shard
+ *     slot at most one device, slots enabled in order; Alg. 1 solves it with
+ *     CP-SAT) [reading: the top-k candidates of each frontier stage are the
+ *     choices; a candidate uses the devices of its window, which is the
+ *     stage's slots 0..k-1 on k devices, so slot order holds by itself; the
+ *     wave is built greedily]: among the choices whose stage has no
+ *     assignment yet and whose devices are all still free in this wave, take
+ *     the one with the highest score (ties: lower frontier slot, then lower
+ *     rank), mark its stage assigned and its devices used, and repeat until
+ *     no choice is left.  Choices scored -infinity or padded (-1) are never
+ *     taken.  Instances plan independently.
+ *
  * Scoring variants (all off by default):
  *   V1. Same-model preference (Sec. 4 implementation summary: model-
  *       specialised placement preferences; App. C.3, "w/o same-model bonus"
@@ -265,6 +278,17 @@ static int64_t n_candidates(const oracle_in_t *in, int64_t g) {
     int64_t c = in->D;
     for (int k = 2; k <= r; ++k) c += in->D - k + 1;
     return c;
+}
+
+/* Candidate j of a stage with D devices -> window start i and size k. */
+static void window_of(int D, int64_t j, int *i_out, int *k_out) {
+    if (j < D) { *i_out = (int)j; *k_out = 1; return; }
+    j -= D;
+    for (int k = 2;; ++k) {
+        int64_t nw = D - k + 1;
+        if (j < nw) { *i_out = (int)j; *k_out = k; return; }
+        j -= nw;
+    }
 }
 
 /* Candidate j of a stage -> window start i and size k. */
@@ -560,4 +584,45 @@ int oracle_commit(const oracle_in_t *in, int B, const int64_t *f_off, const int3
         }
     }
     return rejected;
+}
+
+/* Step 12: one frontier planning wave per instance.  For frontier slot f
+ * (f_off[b] the first slot of instance b) the choices are idx[f*k + r],
+ * r < k (local candidate indices, -1 = none) with scores val[f*k + r].
+ * sel_out[f] receives the chosen candidate or -1.  Returns the number of
+ * stages assigned. */
+int oracle_plan_wave(int B, int D, const int64_t *f_off, const int32_t *idx, const float *val, int k,
+                     int32_t *sel_out) {
+    int total = 0;
+    for (int b = 0; b < B; ++b) {
+        int64_t f0 = f_off[b], f1 = f_off[b + 1];
+        for (int64_t f = f0; f < f1; ++f) sel_out[f] = -1;
+        uint64_t used = 0;
+        for (;;) {
+            int64_t best_f = -1;
+            int best_r = -1;
+            double best_v = -INFINITY;
+            uint64_t best_m = 0;
+            for (int64_t f = f0; f < f1; ++f) {
+                if (sel_out[f] >= 0) continue;
+                for (int r = 0; r < k; ++r) {
+                    int32_t j = idx[f * k + r];
+                    double v = (double)val[f * k + r];
+                    if (j < 0 || v == -INFINITY) continue;
+                    int i0, w;
+                    window_of(D, j, &i0, &w);
+                    uint64_t m = 0;
+                    for (int d = i0; d < i0 + w; ++d) m |= (uint64_t)1 << d;
+                    if (m & used) continue;
+                    /* strictly better only: earlier slots and ranks win ties */
+                    if (best_f < 0 || v > best_v) { best_f = f; best_r = r; best_v = v; best_m = m; }
+                }
+            }
+            if (best_f < 0) break;
+            sel_out[best_f] = idx[best_f * k + best_r];
+            used |= best_m;
+            ++total;
+        }
+    }
+    return total;
 }

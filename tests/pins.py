@@ -561,6 +561,98 @@ def _horizon_counts(w, b, v, H):
     return out
 
 
+# ---------------------------------------------------------------------------
+# frontier planning wave (oracle step 12)
+# ---------------------------------------------------------------------------
+
+def check_plan_scenario(name: str, lib=None):
+    sc = scenarios.PLANS[name]
+    sel, n = oracle.plan_wave(sc["D"], sc["f_off"], np.array(sc["idx"], np.int32), np.array(sc["val"], np.float32),
+                              lib=lib)
+    assert sel.tolist() == sc["sel"], (sel.tolist(), sc["sel"])
+    assert n == sum(1 for x in sc["sel"] if x >= 0)
+
+
+def _window_mask(D, j):
+    k, i = 1, int(j)
+    if j >= D:
+        t, k = int(j) - D, 2
+        while t >= D - k + 1:
+            t -= D - k + 1
+            k += 1
+        i = t
+    return ((1 << k) - 1) << i
+
+
+def random_plan_input(seed: int, B=5, D=6, k=4, max_shard=3, p_inf=0.15, ties=False):
+    """Seeded top-k-like choices: per slot k distinct candidates of a stage
+    with windows up to max_shard, scores descending per slot (as a top-k
+    reports them), some -inf / padded."""
+    rng = np.random.default_rng(seed)
+    nC = D + sum(D - w + 1 for w in range(2, max_shard + 1))
+    nf = rng.integers(0, 9, size=B)
+    f_off = np.concatenate([[0], np.cumsum(nf)]).astype(np.int64)
+    F = int(f_off[-1])
+    idx = np.full((F, k), -1, np.int32)
+    val = np.full((F, k), -np.inf, np.float32)
+    for f in range(F):
+        m = int(rng.integers(0, k + 1))
+        js = rng.choice(nC, size=min(m, nC), replace=False)
+        vs = (np.round(rng.normal(-3.0, 1.0, size=len(js)) * 4) / 4) if ties else rng.normal(-3.0, 1.0, size=len(js))
+        order = np.argsort(-vs, kind="stable")
+        for r, o in enumerate(order):
+            if rng.random() < p_inf:
+                break  # the rest of this slot is padding
+            idx[f, r] = js[o]
+            val[f, r] = vs[o]
+    return D, f_off, idx, val
+
+
+def check_plan_certificate(seed: int, lib=None, ties=False):
+    """The greedy wave is feasible (one choice per stage, devices disjoint per
+    instance), maximal (no untaken valid choice has a free stage and free
+    devices), and every untaken valid choice is blocked by a taken choice
+    that scores at least as high (the greedy exchange certificate)."""
+    D, f_off, idx, val = random_plan_input(seed, ties=ties)
+    sel, n = oracle.plan_wave(D, f_off, idx, val, lib=lib)
+    assert n == int(np.count_nonzero(sel >= 0))
+    for b in range(len(f_off) - 1):
+        lo, hi = int(f_off[b]), int(f_off[b + 1])
+        taken = {}
+        used = 0
+        for f in range(lo, hi):
+            if sel[f] < 0:
+                continue
+            rs = [r for r in range(idx.shape[1]) if idx[f, r] == sel[f] and np.isfinite(val[f, r])]
+            assert rs, (f, sel[f])
+            m = _window_mask(D, sel[f])
+            assert used & m == 0, "devices used twice"
+            used |= m
+            taken[f] = (float(val[f, rs[0]]), m)
+        for f in range(lo, hi):
+            for r in range(idx.shape[1]):
+                if idx[f, r] < 0 or not np.isfinite(val[f, r]) or sel[f] == idx[f, r]:
+                    continue
+                m, v = _window_mask(D, idx[f, r]), float(val[f, r])
+                if f not in taken:
+                    assert used & m, "maximality: slot %d choice %d fits" % (f, r)
+                # blocked by its own stage or by a device: some blocker scores >= v
+                blockers = [tv for g, (tv, tm) in taken.items() if g == f or tm & m]
+                assert blockers and max(blockers) >= v, (f, r, v, blockers)
+
+
+def check_plan_no_conflicts(seed: int, lib=None):
+    """With one instance per slot (nothing shared), the wave takes every
+    stage's best valid choice."""
+    D, f_off, idx, val = random_plan_input(seed)
+    F = int(f_off[-1])
+    sel, _ = oracle.plan_wave(D, np.arange(F + 1), idx, val, lib=lib)
+    for f in range(F):
+        ok = [r for r in range(idx.shape[1]) if idx[f, r] >= 0 and np.isfinite(val[f, r])]
+        want = idx[f, max(ok, key=lambda r: (val[f, r], -r))] if ok else -1
+        assert sel[f] == want, (f, sel[f], want)
+
+
 ALL_CHECKS = (
     [("scenario:" + k, (lambda k: lambda lib: check_scenario(k, lib))(k)) for k in scenarios.ALL]
     + [("worked_example", check_worked_example)]
@@ -585,4 +677,8 @@ ALL_CHECKS = (
     + [("no_windows:%d" % s, (lambda s: lambda lib: check_no_windows_keeps_singletons(s, lib))(s)) for s in range(2)]
     + [("same_model_uniform:%d" % s, (lambda s: lambda lib: check_same_model_weight_linear(s, lib))(s))
        for s in range(3)]
+    + [("plan:" + k, (lambda k: lambda lib: check_plan_scenario(k, lib))(k)) for k in scenarios.PLANS]
+    + [("plan_certificate:%d" % s, (lambda s: lambda lib: check_plan_certificate(s, lib, ties=s % 2 == 1))(s))
+       for s in range(6)]
+    + [("plan_no_conflicts:%d" % s, (lambda s: lambda lib: check_plan_no_conflicts(s, lib))(s)) for s in range(2)]
 )

@@ -77,6 +77,12 @@ MUTANTS = {
     "mean_over_all_levels": [("if (in->mean_levels) gw_pow /= (double)sc.nlev[sc.depth[w]];",
                               "if (in->mean_levels) gw_pow /= (double)count;")],
     "no_windows_ignored": [("if (!ok || (k > 1 && in->no_windows))", "if (!ok)")],
+    # frontier planning wave
+    "plan_ties_to_later": [("if (best_f < 0 || v > best_v)", "if (best_f < 0 || v >= best_v)")],
+    "plan_ignores_devices": [("if (m & used) continue;", "if (0) continue;")],
+    "plan_window_one_device": [("for (int d = i0; d < i0 + w; ++d) m |= (uint64_t)1 << d;", "m = (uint64_t)1 << i0;")],
+    "plan_takes_inf": [("if (j < 0 || v == -INFINITY) continue;", "if (j < 0) continue;")],
+    "plan_stage_twice": [("if (sel_out[f] >= 0) continue;", "if (0) continue;")],
 }
 
 
