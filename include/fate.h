@@ -392,6 +392,25 @@ fate_status_t fate_topk_sweep(const fate_state_h *state, const float *d_scores, 
                               int64_t score_stride, int32_t n_sets, int32_t k, int32_t *d_idx, float *d_val,
                               void *stream);
 
+/* fate_plan_wave: one frontier planning wave per instance on the device (the
+ * planner step of Alg. 1 under the wave constraints of App. A.2: each device
+ * takes at most one shard-slot assignment per wave, each stage at most one
+ * placement; a window candidate is the stage's slots 0..k-1 on k devices,
+ * so slots are enabled in order).  The choices of frontier slot f are
+ * d_idx[f * k + r], r < k, with scores d_val[f * k + r] - the layout fate_topk
+ * writes (device memory).  Greedy: the best remaining choice whose stage is
+ * unassigned and whose devices are all free in this wave is taken (ties: the
+ * lower frontier slot, then the lower rank), until none is left; choices of
+ * -1, -infinity or an index past the stage's candidates are never taken.
+ * d_sel[n_frontier] (device) receives each slot's chosen candidate or -1 (not
+ * placed in this wave) - the selection fate_commit_advance takes with
+ * sel_stride 1.  For a planning state the current frontier size is read on
+ * the device.  Enqueued on `stream`.
+ * Errors: EINVAL (null pointers), ERANGE (k outside 1..64, n_frontier * k
+ * >= 2^32), EHIP. */
+fate_status_t fate_plan_wave(const fate_state_h *state, const int32_t *d_idx, const float *d_val, int32_t k,
+                             int32_t *d_sel, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

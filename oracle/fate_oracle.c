@@ -81,8 +81,8 @@
  *     assignment yet and whose devices are all still free in this wave, take
  *     the one with the highest score (ties: lower frontier slot, then lower
  *     rank), mark its stage assigned and its devices used, and repeat until
- *     no choice is left.  Choices scored -infinity or padded (-1) are never
- *     taken.  Instances plan independently.
+ *     no choice is left.  Choices scored -infinity, padded (-1) or past the
+ *     stage's candidates are never taken.  Instances plan independently.
  *
  * Scoring variants (all off by default):
  *   V1. Same-model preference (Sec. 4 implementation summary: model-
@@ -587,12 +587,12 @@ int oracle_commit(const oracle_in_t *in, int B, const int64_t *f_off, const int3
 }
 
 /* Step 12: one frontier planning wave per instance.  For frontier slot f
- * (f_off[b] the first slot of instance b) the choices are idx[f*k + r],
- * r < k (local candidate indices, -1 = none) with scores val[f*k + r].
- * sel_out[f] receives the chosen candidate or -1.  Returns the number of
- * stages assigned. */
-int oracle_plan_wave(int B, int D, const int64_t *f_off, const int32_t *idx, const float *val, int k,
-                     int32_t *sel_out) {
+ * (f_off[b] the first slot of instance b, n_cand[f] its stage's number of
+ * candidates) the choices are idx[f*k + r], r < k (local candidate indices,
+ * -1 = none) with scores val[f*k + r].  sel_out[f] receives the chosen
+ * candidate or -1.  Returns the number of stages assigned. */
+int oracle_plan_wave(int B, int D, const int64_t *f_off, const int64_t *n_cand, const int32_t *idx,
+                     const float *val, int k, int32_t *sel_out) {
     int total = 0;
     for (int b = 0; b < B; ++b) {
         int64_t f0 = f_off[b], f1 = f_off[b + 1];
@@ -608,7 +608,7 @@ int oracle_plan_wave(int B, int D, const int64_t *f_off, const int32_t *idx, con
                 for (int r = 0; r < k; ++r) {
                     int32_t j = idx[f * k + r];
                     double v = (double)val[f * k + r];
-                    if (j < 0 || v == -INFINITY) continue;
+                    if (j < 0 || j >= n_cand[f] || v == -INFINITY) continue;
                     int i0, w;
                     window_of(D, j, &i0, &w);
                     uint64_t m = 0;

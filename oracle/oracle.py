@@ -83,7 +83,8 @@ def _bind(lib):
     lib.oracle_commit.argtypes = [C.POINTER(_In), C.c_int, C.c_void_p, C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.oracle_commit.restype = C.c_int
-    lib.oracle_plan_wave.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_void_p]
+    lib.oracle_plan_wave.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int,
+                                     C.c_void_p]
     lib.oracle_plan_wave.restype = C.c_int
 
 
@@ -223,19 +224,21 @@ def commit(w, sel, max_shard: Optional[int] = None, lib=None):
     return new, tau, int(rejected)
 
 
-def plan_wave(D: int, f_off, idx, val, lib=None):
+def plan_wave(D: int, f_off, n_cand, idx, val, lib=None):
     """One frontier planning wave (oracle step 12).  ``f_off`` [B+1] gives
-    each instance's frontier slots; ``idx`` / ``val`` [F, k] are each slot's
-    choices (local candidate indices, -1 = none) and their float32 scores.
-    Returns (sel [F] int32, -1 = not assigned in this wave; stages assigned)."""
+    each instance's frontier slots, ``n_cand`` [F] each slot's number of
+    candidates; ``idx`` / ``val`` [F, k] are each slot's choices (local
+    candidate indices, -1 = none) and their float32 scores.  Returns
+    (sel [F] int32, -1 = not assigned in this wave; stages assigned)."""
     lib = lib or load()
     f_off = np.ascontiguousarray(f_off, np.int64)
+    n_cand = np.ascontiguousarray(n_cand, np.int64)
     idx = np.ascontiguousarray(idx, np.int32)
     val = np.ascontiguousarray(val, np.float32)
     F = int(f_off[-1])
-    if idx.ndim != 2 or idx.shape[0] != F or val.shape != idx.shape:
-        raise ValueError("idx / val must be [F, k] with F = f_off[-1]")
+    if idx.ndim != 2 or idx.shape[0] != F or val.shape != idx.shape or n_cand.shape != (F,):
+        raise ValueError("idx / val must be [F, k] and n_cand [F] with F = f_off[-1]")
     sel = np.full(F, -1, np.int32)
-    n = lib.oracle_plan_wave(len(f_off) - 1, int(D), f_off.ctypes.data, idx.ctypes.data, val.ctypes.data,
-                             int(idx.shape[1]), sel.ctypes.data)
+    n = lib.oracle_plan_wave(len(f_off) - 1, int(D), f_off.ctypes.data, n_cand.ctypes.data, idx.ctypes.data,
+                             val.ctypes.data, int(idx.shape[1]), sel.ctypes.data)
     return sel, int(n)

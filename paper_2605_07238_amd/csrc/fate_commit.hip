@@ -75,29 +75,6 @@ __device__ int instance_of(const int64_t *stage_off, int B, int64_t s) {
     return lo;
 }
 
-// First frontier slot whose instance is >= b (the frontier is ordered by
-// instance), found by the whole wave (all 64 lanes active): each lane probes
-// one position, so every round of parallel loads shrinks the range 64-fold.
-__device__ int64_t first_slot_of_wave(const uint32_t *frontier, int64_t nF, uint32_t b) {
-    const int lane = threadIdx.x & 63;
-    int64_t lo = 0, hi = nF;  // the answer lies in [lo, hi]
-    for (;;) {  // uniform
-        const int64_t n = hi - lo;
-        if (n <= 64) {  // probe every position
-            const bool below = lane < n && frontier[2 * (lo + lane) + 1] < b;
-            return lo + __popcll(__ballot(below));
-        }
-        // probes p_l = lo + floor((l + 1) n / 64) - 1 rise strictly and end at hi - 1;
-        // those below b form a prefix of cnt probes
-        const int64_t p = lo + ((int64_t)(lane + 1) * n) / 64 - 1;
-        const int cnt = __popcll(__ballot(frontier[2 * p + 1] < b));
-        const int64_t nlo = cnt > 0 ? lo + ((int64_t)cnt * n) / 64 : lo;              // p_{cnt-1} + 1
-        const int64_t nhi = cnt < 64 ? lo + ((int64_t)(cnt + 1) * n) / 64 - 1 : hi;   // p_cnt
-        lo = nlo;
-        hi = nhi;
-    }
-}
-
 // One frontier slot of the instance, staged for the lanes of its wave:
 // the devices of its selected candidate (0 when none or rejected), the
 // stage's prefix group and model, and the candidate's size k.

@@ -996,4 +996,25 @@ fate_status_t fate_topk_sweep(const fate_state_h *state, const float *d_scores, 
     return topk_impl(state, d_scores, n_scores, score_stride, n_sets, k, d_idx, d_val, stream);
 }
 
+fate_status_t fate_plan_wave(const fate_state_h *state, const int32_t *d_idx, const float *d_val, int32_t k,
+                             int32_t *d_sel, void *stream) {
+    if (!state) return FATE_EINVAL;
+    if (k < 1 || k > FATE_MAX_TOPK) return FATE_ERANGE;
+    if (state->n_frontier == 0) return FATE_OK;
+    if (!d_idx || !d_val || !d_sel || !state->frontier || !state->cand_off) return FATE_EINVAL;
+    if (state->n_frontier * (int64_t)k >= (int64_t(1) << 32)) return FATE_ERANGE;
+    fate::PlanLaunch a;
+    a.frontier = state->frontier;
+    a.cand_off = state->cand_off;
+    a.dcounts = state->advance ? state->counts : nullptr;
+    a.idx = d_idx;
+    a.val = d_val;
+    a.sel = d_sel;
+    a.nF = state->n_frontier;
+    a.B = state->B;
+    a.D = state->D;
+    a.k = k;
+    return fate::launch_plan(a, stream) == 0 ? FATE_OK : FATE_EHIP;
+}
+
 }  // extern "C"

@@ -153,4 +153,17 @@ int launch_score(const ScoreLaunch &a, void *stream);
 int launch_topk(const TopkLaunch &a, void *stream);
 int launch_commit(const CommitLaunch &a, void *stream);  // fate_commit.hip
 
+// Frontier planning wave (fate_plan.hip).
+struct PlanLaunch {
+    const uint32_t *frontier;  // [nF][2]: flat stage id, instance
+    const uint32_t *cand_off;  // [nF + 1]: a stage's candidates are its choices' valid range
+    const uint32_t *dcounts;   // planning state: counts[0] = current frontier size, else null
+    const int32_t *idx;        // [nF][k] choices (local candidate indices, -1 = none)
+    const float *val;          // [nF][k] their scores
+    int32_t *sel;              // [nF] chosen candidate or -1
+    int64_t nF;                // frontier size, or its capacity with dcounts
+    int32_t B, D, k;
+};
+int launch_plan(const PlanLaunch &a, void *stream);
+
 }  // namespace fate

@@ -31,7 +31,7 @@ EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_da
            "fate_pack_state_size", "fate_pack_state", "fate_layout_state", "fate_score_ws_size",
            "fate_score_frontier", "fate_score_topk", "fate_topk", "fate_pack_state_advance_size",
            "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance", "fate_pack_dags_opt_size",
-           "fate_pack_dags_opt", "fate_layout_dags_opt", "fate_score_sweep", "fate_topk_sweep"]
+           "fate_pack_dags_opt", "fate_layout_dags_opt", "fate_score_sweep", "fate_topk_sweep", "fate_plan_wave"]
 
 # Scoring variants and packing options (fate_params_t.flags, fate_pack_opts_t.levels).
 FATE_MEAN_PER_LEVEL, FATE_NO_WINDOWS = 1, 2
@@ -140,6 +140,7 @@ def load(path: Optional[str] = None):
                                      C.c_void_p, C.c_size_t, C.c_void_p]
     lib.fate_topk_sweep.argtypes = [P(StateH), C.c_void_p, C.c_int64, C.c_int64, C.c_int32, C.c_int32, C.c_void_p,
                                     C.c_void_p, C.c_void_p]
+    lib.fate_plan_wave.argtypes = [P(StateH), C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
     for name in EXPORTS[2:]:
         getattr(lib, name).restype = st
     if path is None:
@@ -435,6 +436,21 @@ def fate_topk_sweep(state: PackedState, scores, k: int, idx=None, val=None, stre
                                P, int(k), C.c_void_p(idx.data_ptr()), C.c_void_p(val.data_ptr()),
                                C.c_void_p(_stream_ptr(stream))), "fate_topk_sweep")
     return idx[:, :F], val[:, :F]
+
+
+def fate_plan_wave(state: PackedState, idx, val, sel=None, stream=None):
+    """One frontier planning wave from per-stage choices ``idx`` / ``val``
+    ([F, k] device tensors, the fate_topk layout); returns the int32 device
+    tensor sel [F] (-1 = not placed in this wave)."""
+    import torch
+    lib = load()
+    F = state.n_frontier
+    k = int(idx.shape[1]) if idx.dim() == 2 else 1
+    if sel is None:
+        sel = torch.empty(max(1, F), dtype=torch.int32, device=idx.device)
+    _check(lib.fate_plan_wave(C.byref(state.handle), C.c_void_p(idx.data_ptr()), C.c_void_p(val.data_ptr()), k,
+                              C.c_void_p(sel.data_ptr()), C.c_void_p(_stream_ptr(stream))), "fate_plan_wave")
+    return sel[:F]
 
 
 def fate_commit_ws_size(packed: PackedDags, state: PackedState) -> int:

@@ -567,8 +567,8 @@ def _horizon_counts(w, b, v, H):
 
 def check_plan_scenario(name: str, lib=None):
     sc = scenarios.PLANS[name]
-    sel, n = oracle.plan_wave(sc["D"], sc["f_off"], np.array(sc["idx"], np.int32), np.array(sc["val"], np.float32),
-                              lib=lib)
+    sel, n = oracle.plan_wave(sc["D"], sc["f_off"], sc["n_cand"], np.array(sc["idx"], np.int32),
+                              np.array(sc["val"], np.float32), lib=lib)
     assert sel.tolist() == sc["sel"], (sel.tolist(), sc["sel"])
     assert n == sum(1 for x in sc["sel"] if x >= 0)
 
@@ -585,19 +585,21 @@ def _window_mask(D, j):
 
 
 def random_plan_input(seed: int, B=5, D=6, k=4, max_shard=3, p_inf=0.15, ties=False):
-    """Seeded top-k-like choices: per slot k distinct candidates of a stage
-    with windows up to max_shard, scores descending per slot (as a top-k
-    reports them), some -inf / padded."""
+    """Seeded top-k-like choices: per slot k distinct candidate indices of a
+    stage with windows up to max_shard (or singletons only), a few past the
+    stage's candidates, scores descending per slot (as a top-k reports them),
+    some -inf / padded."""
     rng = np.random.default_rng(seed)
     nC = D + sum(D - w + 1 for w in range(2, max_shard + 1))
     nf = rng.integers(0, 9, size=B)
     f_off = np.concatenate([[0], np.cumsum(nf)]).astype(np.int64)
     F = int(f_off[-1])
+    n_cand = np.where(rng.random(F) < 0.3, D, nC).astype(np.int64)
     idx = np.full((F, k), -1, np.int32)
     val = np.full((F, k), -np.inf, np.float32)
     for f in range(F):
         m = int(rng.integers(0, k + 1))
-        js = rng.choice(nC, size=min(m, nC), replace=False)
+        js = rng.choice(nC + 3, size=min(m, nC), replace=False)  # indices up to nC + 2 < D (D + 1) / 2
         vs = (np.round(rng.normal(-3.0, 1.0, size=len(js)) * 4) / 4) if ties else rng.normal(-3.0, 1.0, size=len(js))
         order = np.argsort(-vs, kind="stable")
         for r, o in enumerate(order):
@@ -605,7 +607,7 @@ def random_plan_input(seed: int, B=5, D=6, k=4, max_shard=3, p_inf=0.15, ties=Fa
                 break  # the rest of this slot is padding
             idx[f, r] = js[o]
             val[f, r] = vs[o]
-    return D, f_off, idx, val
+    return D, f_off, n_cand, idx, val
 
 
 def check_plan_certificate(seed: int, lib=None, ties=False):
@@ -613,8 +615,8 @@ def check_plan_certificate(seed: int, lib=None, ties=False):
     instance), maximal (no untaken valid choice has a free stage and free
     devices), and every untaken valid choice is blocked by a taken choice
     that scores at least as high (the greedy exchange certificate)."""
-    D, f_off, idx, val = random_plan_input(seed, ties=ties)
-    sel, n = oracle.plan_wave(D, f_off, idx, val, lib=lib)
+    D, f_off, n_cand, idx, val = random_plan_input(seed, ties=ties)
+    sel, n = oracle.plan_wave(D, f_off, n_cand, idx, val, lib=lib)
     assert n == int(np.count_nonzero(sel >= 0))
     for b in range(len(f_off) - 1):
         lo, hi = int(f_off[b]), int(f_off[b + 1])
@@ -624,6 +626,7 @@ def check_plan_certificate(seed: int, lib=None, ties=False):
             if sel[f] < 0:
                 continue
             rs = [r for r in range(idx.shape[1]) if idx[f, r] == sel[f] and np.isfinite(val[f, r])]
+            assert sel[f] < n_cand[f], (f, sel[f])
             assert rs, (f, sel[f])
             m = _window_mask(D, sel[f])
             assert used & m == 0, "devices used twice"
@@ -631,7 +634,7 @@ def check_plan_certificate(seed: int, lib=None, ties=False):
             taken[f] = (float(val[f, rs[0]]), m)
         for f in range(lo, hi):
             for r in range(idx.shape[1]):
-                if idx[f, r] < 0 or not np.isfinite(val[f, r]) or sel[f] == idx[f, r]:
+                if idx[f, r] < 0 or idx[f, r] >= n_cand[f] or not np.isfinite(val[f, r]) or sel[f] == idx[f, r]:
                     continue
                 m, v = _window_mask(D, idx[f, r]), float(val[f, r])
                 if f not in taken:
@@ -644,11 +647,11 @@ def check_plan_certificate(seed: int, lib=None, ties=False):
 def check_plan_no_conflicts(seed: int, lib=None):
     """With one instance per slot (nothing shared), the wave takes every
     stage's best valid choice."""
-    D, f_off, idx, val = random_plan_input(seed)
+    D, f_off, n_cand, idx, val = random_plan_input(seed)
     F = int(f_off[-1])
-    sel, _ = oracle.plan_wave(D, np.arange(F + 1), idx, val, lib=lib)
+    sel, _ = oracle.plan_wave(D, np.arange(F + 1), n_cand, idx, val, lib=lib)
     for f in range(F):
-        ok = [r for r in range(idx.shape[1]) if idx[f, r] >= 0 and np.isfinite(val[f, r])]
+        ok = [r for r in range(idx.shape[1]) if 0 <= idx[f, r] < n_cand[f] and np.isfinite(val[f, r])]
         want = idx[f, max(ok, key=lambda r: (val[f, r], -r))] if ok else -1
         assert sel[f] == want, (f, sel[f], want)
 

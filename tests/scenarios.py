@@ -263,15 +263,20 @@ VARIANTS = dict(SM_IMMEDIATE=SM_IMMEDIATE, SM_WINDOWS=SM_WINDOWS, SM_POST_STATE=
 #     window (-1.0, the best score).  Round 2: slot 1 has {1} (used) or {2}
 #     at -2.0; slot 2 has {2} at -1.2 or {0} (used).  It takes slot 2's {2}.
 #     Every device is then used, so slot 1 waits for the next wave.
-PLAN_WINDOW = dict(D=3, f_off=[0, 3], idx=[[3, 0], [1, 2], [2, 0]],
+PLAN_WINDOW = dict(D=3, f_off=[0, 3], n_cand=[5, 5, 5], idx=[[3, 0], [1, 2], [2, 0]],
                    val=[[-1.0, -1.5], [-1.2, -2.0], [-1.2, -3.0]], sel=[3, -1, 2])
-# W2: ties go to the lower frontier slot; -inf and padded choices are never
-#     taken; instances plan independently (both use device 0).
+# W2: ties go to the lower frontier slot; -inf, padded and past-the-end
+#     choices are never taken (slot 3's best, index 4, is past its 2
+#     candidates); instances plan independently (both use device 0).
 INF_ = float("inf")
-PLAN_TIES = dict(D=2, f_off=[0, 2, 4], idx=[[0, 1], [0, 1], [1, -1], [0, 1]],
-                 val=[[-1.0, -2.0], [-1.0, -2.0], [-INF_, -INF_], [-5.0, -6.0]], sel=[0, 1, -1, 0])
+PLAN_TIES = dict(D=2, f_off=[0, 2, 4], n_cand=[3, 3, 2, 2], idx=[[0, 1], [0, 1], [1, -1], [4, 0]],
+                 val=[[-1.0, -2.0], [-1.0, -2.0], [-INF_, -INF_], [-0.5, -5.0]], sel=[0, 1, -1, 0])
 # W3: a higher score on a later rank beats an earlier rank; a stage takes at
 #     most one choice even when its devices are free.
-PLAN_RANKS = dict(D=4, f_off=[0, 2], idx=[[0, 1], [2, 3]], val=[[-3.0, -3.0], [-1.0, -0.5]], sel=[0, 3])
+PLAN_RANKS = dict(D=4, f_off=[0, 2], n_cand=[4, 4], idx=[[0, 1], [2, 3]], val=[[-3.0, -3.0], [-1.0, -0.5]],
+                  sel=[0, 3])
 
-PLANS = dict(PLAN_WINDOW=PLAN_WINDOW, PLAN_TIES=PLAN_TIES, PLAN_RANKS=PLAN_RANKS)
+# W4: -0 and +0 are the same score, so the lower slot wins the tie.
+PLAN_SIGNED_ZERO = dict(D=1, f_off=[0, 2], n_cand=[1, 1], idx=[[0], [0]], val=[[-0.0], [0.0]], sel=[0, -1])
+
+PLANS = dict(PLAN_WINDOW=PLAN_WINDOW, PLAN_TIES=PLAN_TIES, PLAN_RANKS=PLAN_RANKS, PLAN_SIGNED_ZERO=PLAN_SIGNED_ZERO)

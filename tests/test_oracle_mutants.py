@@ -81,7 +81,10 @@ MUTANTS = {
     "plan_ties_to_later": [("if (best_f < 0 || v > best_v)", "if (best_f < 0 || v >= best_v)")],
     "plan_ignores_devices": [("if (m & used) continue;", "if (0) continue;")],
     "plan_window_one_device": [("for (int d = i0; d < i0 + w; ++d) m |= (uint64_t)1 << d;", "m = (uint64_t)1 << i0;")],
-    "plan_takes_inf": [("if (j < 0 || v == -INFINITY) continue;", "if (j < 0) continue;")],
+    "plan_takes_inf": [("if (j < 0 || j >= n_cand[f] || v == -INFINITY) continue;",
+                        "if (j < 0 || j >= n_cand[f]) continue;")],
+    "plan_past_candidates": [("if (j < 0 || j >= n_cand[f] || v == -INFINITY) continue;",
+                              "if (j < 0 || v == -INFINITY) continue;")],
     "plan_stage_twice": [("if (sel_out[f] >= 0) continue;", "if (0) continue;")],
 }
 
