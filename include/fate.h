@@ -411,6 +411,57 @@ fate_status_t fate_topk_sweep(const fate_state_h *state, const float *d_scores, 
 fate_status_t fate_plan_wave(const fate_state_h *state, const int32_t *d_idx, const float *d_val, int32_t k,
                              int32_t *d_sel, void *stream);
 
+/* Plan execution (host memory, no device work).  Per instance:
+ *   tasks       stages executed (the placed pending stages)
+ *   makespan    latest finish - t_now, seconds
+ *   p95         nearest-rank 95th percentile of finish - t_now over the
+ *               executed stages without children
+ *   xdev_edges  parent edges u -> v with v on no device holding u's output
+ *   cache_hits  executed stages whose first device had grp(v) cached
+ *   model_cont  executed stages whose first device ran the same model just
+ *               before them
+ * (App. C.2 makespan, p95 latency and mechanism proxies; normalising by the
+ * task count or by a baseline is left to the caller.) */
+typedef struct {
+    int64_t tasks;
+    double makespan, p95;
+    int64_t xdev_edges, cache_hits, model_cont;
+} fate_sim_metrics_t;
+
+/* fate_simulate: execute a placement on every instance.  devices[N]: S(v)
+ * as a device bitmask for each pending stage to run (0 = not run);
+ * order[N]: each device runs its stages by (order, stage id).  A shard of v
+ * on d, k = |S(v)|, starts when d is free and every parent's output has
+ * arrived (finish(u) + sigma(u) * min over u's holders i of beta[i][d] / k,
+ * or finish(u) when d holds it); it pays kappa_switch(m(v), d) if m(v) is not
+ * resident (then m(v) is loaded with the eviction rule of scoring), and runs
+ * c(v, d) / k, less kappa_prefix * L(v) / k (not below 0) when grp(v) is in
+ * d's prefix slots; grp(v) then joins the slots (oldest dropped when full).
+ * v finishes with its last shard; its output is then held by S(v).  The
+ * state's statuses must be pending or completed (completed stages are
+ * available at t_now on their holders).  Host memory; out[B].
+ * Errors: EINVAL, ERANGE, ECYCLE, ENOFEAS (as packing), ESTATE (a status
+ * other than pending / completed, holders inconsistent, or an order that runs
+ * a stage before a parent that is not completed or run earlier). */
+fate_status_t fate_simulate(const fate_cluster_t *cluster, const fate_dag_batch_t *dags, const fate_state_t *state,
+                            const uint64_t *devices, const int64_t *order, float kappa_prefix,
+                            fate_sim_metrics_t *out);
+
+/* Baseline placements for fate_simulate (App. B comparison schedulers). */
+enum { FATE_PLACE_ROUND_ROBIN = 0, FATE_PLACE_HEFT = 1 };
+
+/* fate_place_baseline: FATE_PLACE_ROUND_ROBIN puts each pending stage, in id
+ * order, on the next feasible device after the previous placement;
+ * FATE_PLACE_HEFT orders pending stages by upward rank (mean runtime over
+ * feasible devices plus the largest sigma * mean off-diagonal beta + rank over
+ * its children; ties to the lower id) and gives each the feasible device with
+ * the earliest finish under fate_simulate's rule (ties to the lower device).
+ * Writes devices[N] and order[N] (host memory; 0 for completed stages).
+ * Errors: EINVAL (policy, pointers), and those of fate_simulate's inputs. */
+fate_status_t fate_place_baseline(const fate_cluster_t *cluster, const fate_dag_batch_t *dags,
+                                  const fate_state_t *state, int32_t policy, float kappa_prefix, uint64_t *devices,
+                                  int64_t *order);
+
 #ifdef __cplusplus
 }
 #endif

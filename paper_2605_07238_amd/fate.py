@@ -31,12 +31,14 @@ EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_da
            "fate_pack_state_size", "fate_pack_state", "fate_layout_state", "fate_score_ws_size",
            "fate_score_frontier", "fate_score_topk", "fate_topk", "fate_pack_state_advance_size",
            "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance", "fate_pack_dags_opt_size",
-           "fate_pack_dags_opt", "fate_layout_dags_opt", "fate_score_sweep", "fate_topk_sweep", "fate_plan_wave"]
+           "fate_pack_dags_opt", "fate_layout_dags_opt", "fate_score_sweep", "fate_topk_sweep", "fate_plan_wave",
+           "fate_simulate", "fate_place_baseline"]
 
 # Scoring variants and packing options (fate_params_t.flags, fate_pack_opts_t.levels).
 FATE_MEAN_PER_LEVEL, FATE_NO_WINDOWS = 1, 2
 FATE_LEVELS_HOP, FATE_LEVELS_TOPO = 0, 1
 FATE_MAX_SWEEP = 16
+FATE_PLACE_ROUND_ROBIN, FATE_PLACE_HEFT = 0, 1
 
 
 class FateError(RuntimeError):
@@ -66,6 +68,11 @@ class Params(C.Structure):
     _fields_ = [("lam_q", C.c_float), ("lam_s", C.c_float), ("lam_tr", C.c_float), ("lam_c", C.c_float),
                 ("lam_p", C.c_float), ("kappa_prefix", C.c_float), ("gamma", C.c_float), ("H", C.c_int32),
                 ("lam_m", C.c_float), ("flags", C.c_int32)]
+
+
+class SimMetrics(C.Structure):
+    _fields_ = [("tasks", C.c_int64), ("makespan", C.c_double), ("p95", C.c_double), ("xdev_edges", C.c_int64),
+                ("cache_hits", C.c_int64), ("model_cont", C.c_int64)]
 
 
 class PackOpts(C.Structure):
@@ -141,6 +148,10 @@ def load(path: Optional[str] = None):
     lib.fate_topk_sweep.argtypes = [P(StateH), C.c_void_p, C.c_int64, C.c_int64, C.c_int32, C.c_int32, C.c_void_p,
                                     C.c_void_p, C.c_void_p]
     lib.fate_plan_wave.argtypes = [P(StateH), C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
+    lib.fate_simulate.argtypes = [P(Cluster), P(DagBatch), P(State), C.c_void_p, C.c_void_p, C.c_float,
+                                  P(SimMetrics)]
+    lib.fate_place_baseline.argtypes = [P(Cluster), P(DagBatch), P(State), C.c_int32, C.c_float, C.c_void_p,
+                                        C.c_void_p]
     for name in EXPORTS[2:]:
         getattr(lib, name).restype = st
     if path is None:
@@ -451,6 +462,38 @@ def fate_plan_wave(state: PackedState, idx, val, sel=None, stream=None):
     _check(lib.fate_plan_wave(C.byref(state.handle), C.c_void_p(idx.data_ptr()), C.c_void_p(val.data_ptr()), k,
                               C.c_void_p(sel.data_ptr()), C.c_void_p(_stream_ptr(stream))), "fate_plan_wave")
     return sel[:F]
+
+
+def fate_simulate(w, devices, order, kappa_prefix: Optional[float] = None) -> dict:
+    """Execute a placement (host arrays: devices [N] uint64 masks, order [N]
+    int64 keys) on every instance of ``w``; returns per-instance numpy arrays
+    tasks, makespan, p95, xdev_edges, cache_hits, model_cont."""
+    lib = load()
+    hi = HostInputs(w)
+    kpf = float(w.params["kappa_prefix"] if kappa_prefix is None else kappa_prefix)
+    dev = np.ascontiguousarray(devices, np.uint64)
+    odr = np.ascontiguousarray(order, np.int64)
+    out = (SimMetrics * max(1, w.B))()
+    _check(lib.fate_simulate(C.byref(hi.cluster), C.byref(hi.batch), C.byref(hi.state), dev.ctypes.data,
+                             odr.ctypes.data, kpf, out), "fate_simulate")
+    res = {}
+    for name, _ in SimMetrics._fields_:
+        res[name] = np.array([getattr(out[b], name) for b in range(w.B)],
+                             np.float64 if name in ("makespan", "p95") else np.int64)
+    return res
+
+
+def fate_place_baseline(w, policy: int, kappa_prefix: Optional[float] = None):
+    """Round-robin or HEFT-style placement of ``w``'s pending stages:
+    (devices [N] uint64, order [N] int64) host arrays."""
+    lib = load()
+    hi = HostInputs(w)
+    kpf = float(w.params["kappa_prefix"] if kappa_prefix is None else kappa_prefix)
+    dev = np.zeros(w.N, np.uint64)
+    odr = np.zeros(w.N, np.int64)
+    _check(lib.fate_place_baseline(C.byref(hi.cluster), C.byref(hi.batch), C.byref(hi.state), int(policy), kpf,
+                                   dev.ctypes.data, odr.ctypes.data), "fate_place_baseline")
+    return dev, odr
 
 
 def fate_commit_ws_size(packed: PackedDags, state: PackedState) -> int:
