@@ -348,6 +348,85 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
     return out
 
 
+def record_fate_plan(w, params, k, log, max_waves=2000):
+    """Run the device planning loop to the end and record the plan: each
+    placed stage's devices (its holders in the planning state) and the wave it
+    was placed in (the execution order key; commit order within a wave is by
+    stage id).  Reads the frontier and the wave's selection each wave."""
+    import torch
+    from paper_2605_07238_amd import fate
+    pk = fate.fate_pack_dags(w)
+    st = fate.fate_pack_state(pk, w, advance=True)
+    cap = max(1, st.n_frontier)
+    scores = torch.empty(max(1, st.n_cand), dtype=torch.float32, device="cuda")
+    idx = torch.empty((cap, k), dtype=torch.int32, device="cuda")
+    val = torch.empty((cap, k), dtype=torch.float32, device="cuda")
+    sel = torch.empty(cap, dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(1, fate.fate_commit_ws_size(pk, st)), dtype=torch.uint8, device="cuda")
+    wave_of = np.full(w.N, -1, np.int64)
+    t0 = time.perf_counter()
+    waves = 0
+    while waves < max_waves:
+        nF = st.counts()[0]
+        if nF == 0:
+            break
+        fate.fate_score_frontier(pk, st, params, out=scores)
+        fate.fate_topk(st, scores, k, idx=idx, val=val)
+        fate.fate_plan_wave(st, idx, val, sel=sel)
+        fv, _, _ = fate.frontier_table(st)
+        s_host = sel[:nF].cpu().numpy()
+        wave_of[fv[s_host >= 0]] = waves
+        fate.fate_commit_advance(pk, st, sel, ws=ws)
+        waves += 1
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    holders = fate.state_arrays(st)["holders"]
+    devices = np.where(wave_of >= 0, holders, 0).astype(np.uint64)
+    log("recorded FATE plan: %d waves in %.2f s (with a host read of each wave's selection)" % (waves, dt))
+    return devices, np.maximum(wave_of, 0), waves, dt
+
+
+def sim_compare(w, params, k, log):
+    """Execute the FATE plan and the round-robin and HEFT-style placements of
+    the same batch (running / committed stages made pending) and report the
+    App. C.2 metrics, normalised by round robin as the paper does."""
+    import dataclasses
+    from paper_2605_07238_amd import fate
+    ws = dataclasses.replace(w, status=np.where(w.status == 1, 1, 0).astype(np.uint8))
+    plans = {}
+    plans["FATE"] = record_fate_plan(ws, params, k, log)[:2]
+    t = {}
+    for name, pol in (("RoundRobin", fate.FATE_PLACE_ROUND_ROBIN), ("HEFT", fate.FATE_PLACE_HEFT)):
+        t0 = time.perf_counter()
+        plans[name] = fate.fate_place_baseline(ws, pol)
+        t[name] = time.perf_counter() - t0
+    res, sim_s = {}, {}
+    for name, (dev, order) in plans.items():
+        t0 = time.perf_counter()
+        res[name] = fate.fate_simulate(ws, dev, order)
+        sim_s[name] = time.perf_counter() - t0
+    rr = res["RoundRobin"]
+    ok = rr["makespan"] > 0
+    out = {}
+    for name, r in res.items():
+        tasks = max(1, int(r["tasks"].sum()))
+        out[name] = dict(
+            NormMS=float(np.exp(np.mean(np.log(r["makespan"][ok] / rr["makespan"][ok])))),
+            NormP95=float(np.exp(np.mean(np.log(r["p95"][ok] / rr["p95"][ok])))),
+            XDevEdge=float(r["xdev_edges"].sum() / tasks), CacheScore=float(r["cache_hits"].sum() / tasks),
+            ModelCont=float(r["model_cont"].sum() / tasks), tasks=int(r["tasks"].sum()),
+            mean_makespan_s=float(r["makespan"].mean()), simulate_s=sim_s[name],
+            simulated_tasks_per_s=float(r["tasks"].sum() / sim_s[name]))
+        if name in t:
+            out[name]["place_s"] = t[name]
+        log("%-10s NormMS %.3f NormP95 %.3f XDevEdge %.3f CacheScore %.3f ModelCont %.3f (%d tasks)"
+            % (name, out[name]["NormMS"], out[name]["NormP95"], out[name]["XDevEdge"], out[name]["CacheScore"],
+               out[name]["ModelCont"], out[name]["tasks"]))
+    out["note"] = ("synthetic execution model (fate_simulate); running / committed stages made pending; "
+                   "FATE = device planning loop with top-%d choices per stage" % k)
+    return out
+
+
 def describe(k):
     """Per-recipe sizes of one planning step (one JSON line each)."""
     import torch
@@ -389,6 +468,8 @@ def main():
     ap.add_argument("--planning-steps", type=int, default=6,
                     help="after the timed steps, run this many score / top-k / commit-and-advance planning steps "
                          "on a planning state and report them (0 = skip)")
+    ap.add_argument("--no-sim", action="store_true",
+                    help="skip the plan execution comparison (FATE plan vs round robin vs HEFT-style)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the parameter-sweep measurement (fate_score_sweep over the sensitivity grid)")
     ap.add_argument("--no-medians", action="store_true",
@@ -554,6 +635,8 @@ def main():
         out["planning_loop"] = planning_loop(w, pk, params, args.topk, args.planning_steps, log)
     if not args.no_sweep:
         out["sweep"] = sweep_bench(w, args.topk, 5, log)
+    if not args.no_sim:
+        out["execution"] = sim_compare(w, params, args.topk, log)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host ...")
         dt, passes, threads = cpu_baseline(w, H)

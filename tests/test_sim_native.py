@@ -92,3 +92,44 @@ def test_simulate_errors():
     with pytest.raises(fate.FateError) as e:
         fate.fate_place_baseline(w, 7)
     assert e.value.status == fate.FATE_EINVAL
+
+
+def _oracle_fate_plan(w, k=4, max_waves=200):
+    """A FATE plan built by the oracle alone: score, top-k, one planning wave,
+    commit, until the frontier is empty.  Returns (devices, order) with the
+    wave number as the order key (commit order within a wave is by stage id)."""
+    from oracle import oracle
+    devices = np.zeros(w.N, np.uint64)
+    order = np.zeros(w.N, np.int64)
+    cur = w
+    for wave in range(max_waves):
+        ref = oracle.score(cur)
+        if len(ref["front_v"]) == 0:
+            return devices, order, wave
+        idx, val = oracle.topk(ref, k)
+        _, _, f_off = oracle.frontier(cur)
+        sel, n = oracle.plan_wave(cur.D, f_off, np.diff(ref["cand_off"]), idx, val.astype(np.float32))
+        assert n > 0
+        nxt, _, rej = oracle.commit(cur, sel)
+        assert rej == 0
+        for f in np.nonzero(sel >= 0)[0]:
+            g = int(cur.stage_off[ref["front_b"][f]]) + int(ref["front_v"][f])
+            devices[g] = nxt.holders[g]
+            order[g] = wave
+        cur = nxt
+    raise AssertionError("the plan did not finish")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_fate_plan_executes_alike(seed):
+    """A FATE plan from the oracle's own planning loop runs through both
+    executions alike, and every pending stage is placed."""
+    w = _pending_completed(synth.make_random_small(40 + seed, B=3, n=24, D=5, M=4, K=2, max_shard=3,
+                                                   shard_frac=0.4, p_edge=0.3))
+    dev, order, waves = _oracle_fate_plan(w)
+    assert waves > 1
+    assert np.all((dev != 0) == (w.status == 0))
+    got = fate.fate_simulate(w, dev, order)
+    _compare(got, S.simulate(w, dev, order))
+    assert np.array_equal(got["tasks"], np.array([np.count_nonzero(w.status[int(w.stage_off[b]):int(w.stage_off[b + 1])] == 0)
+                                                  for b in range(w.B)]))
