@@ -154,24 +154,28 @@ def cpu_baseline(w, H, min_seconds=10.0, max_passes=50):
     return total / passes, passes, threads
 
 
-def commit_bytes(pk, st):
+def commit_bytes(pk, st, w):
     """Algorithmic bytes of one commit-and-advance on the device, counted from
-    the planning state it produced: every stage's record and status and its
-    parents' statuses are read; the completed-parent lists, frontier,
-    candidate offsets and slices are written; each (instance, device) state
-    word, free time and prefix slots are read and written; each frontier
-    slot and its selection are read once."""
+    the planning state it produced: every stage's status is read, and a
+    pending stage's record and its parents' statuses; the completed-parent
+    lists, frontier, candidate offsets and slices are written; each
+    (instance, device) state word, free time and prefix slots are read and
+    written; each frontier slot and its selection are read once."""
     import torch
-    h, d = st.handle, pk.handle
-    N, E, B, D, K = int(h.N), int(d.E), int(h.B), int(h.D), int(h.K)
+    from paper_2605_07238_amd import fate
+    h = st.handle
+    N, B, D, K = int(h.N), int(h.B), int(h.D), int(h.K)
     nF, nC, nS, _ = st.counts()
     base = st.buf.data_ptr()
     off = h.done_off - base
     n_done = int(st.buf[off + 4 * N:off + 4 * N + 4].view(torch.int32).cpu().item())
-    return (32 * N + N + E * (4 + 1)          # records, statuses, parent ids and statuses
-            + 4 * (N + 1) + 16 * n_done       # completed-parent offsets and entries
-            + 12 * (nF + 1) + 12 * nS         # frontier, candidate offsets, slices
-            + 2 * B * D * (8 + 4 + 8 * K)     # resident models, free times, prefix slots
+    status = fate.state_arrays(st)["status"]
+    pend = status == 0
+    e_pend = int(np.diff(w.par_off)[pend].sum())
+    return (N + int(pend.sum()) * 32 + e_pend * (4 + 1)  # statuses; pending records, parent ids and statuses
+            + 4 * (N + 1) + 16 * n_done                  # completed-parent offsets and entries
+            + 12 * (nF + 1) + 12 * nS                    # frontier, candidate offsets, slices
+            + 2 * B * D * (8 + 4 + 8 * K)                # resident models, free times, prefix slots
             + 4 * B + 16)
 
 
@@ -306,7 +310,7 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         e[4].record()
         torch.cuda.synchronize()
         nF1 = st.counts()[0]
-        cb = commit_bytes(pk, st)
+        cb = commit_bytes(pk, st, w)
         placed = int(torch.count_nonzero(sel[:nF0] >= 0).item())
         row = dict(frontier=nF0, placed=placed, next_frontier=nF1, score_ms=e[0].elapsed_time(e[1]),
                    topk_ms=e[1].elapsed_time(e[2]), plan_ms=e[2].elapsed_time(e[3]),

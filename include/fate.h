@@ -208,8 +208,9 @@ typedef struct {
     const uint32_t *slices;   /* [n_slices][3]: instance, first and end frontier slot; the
                                  scoring kernel runs one workgroup per slice */
     int64_t n_done_edges;
-    const uint32_t *done_off; /* [N+1]: completed parents of flat stage g are
-                                 done[done_off[g] .. done_off[g+1]) */
+    const uint32_t *done_off; /* [N+1]: completed parents of pending flat stage g
+                                 are done[done_off[g] .. done_off[g+1]); other
+                                 stages have empty lists */
     const void *done;         /* 16-byte entries {uint64 holders; float out_bytes; pad} */
     /* Planning state (fate_pack_state_advance; all zero otherwise).  Its
      * sections are sized for any later planning step, so n_frontier,

@@ -13,10 +13,10 @@
 //                   start at max(tau, t), switch time if the model was
 //                   absent, Load, prefix slots, free time (summed in fp64
 //                   over the step, stored as fp32).
-//   k_plan_count    per stage (kPlanItems consecutive stages per thread):
-//                   completed parents, and the candidate count when the stage
-//                   is now in the frontier (pending, every parent completed);
-//                   workgroup totals.
+//   k_plan_count    per stage (kPlanItems consecutive stages per thread): for
+//                   a pending stage its completed parents, and its candidate
+//                   count when it is now in the frontier (every parent
+//                   completed); workgroup totals.
 //   k_plan_offsets  one workgroup: exclusive scan of the workgroup totals;
 //                   frontier and candidate totals.
 //   k_plan_fill     per stage: offset and entries of its completed-parent
@@ -267,14 +267,18 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
     for (int i = 0; i < kPlanItems; ++i) {
         const int64_t s = s0 + i;
         if (s >= a.N) break;
-        const StageRec r = a.rec[s];
+        // only pending stages can be scored (in the frontier or a horizon),
+        // so only they carry completed-parent lists
         bool ready = a.status[s] == kPending;
-        uint32_t cp = 0;
-        for (uint32_t q = 0; q < r.npar; ++q) {
-            if (a.status[a.par_idx[r.par_begin + q]] == kCompleted) ++cp;
-            else ready = false;
+        uint32_t cp = 0, nc = 0;
+        if (ready) {
+            const StageRec r = a.rec[s];
+            for (uint32_t q = 0; q < r.npar; ++q) {
+                if (a.status[a.par_idx[r.par_begin + q]] == kCompleted) ++cp;
+                else ready = false;
+            }
+            nc = ready ? (uint32_t)candidates_of(shard_cap_of(r.shard, a.max_shard, a.D), a.D) : 0u;
         }
-        const uint32_t nc = ready ? (uint32_t)candidates_of(shard_cap_of(r.shard, a.max_shard, a.D), a.D) : 0u;
         a.cp[s] = cp;
         a.nc[s] = nc;
         tcp += cp;

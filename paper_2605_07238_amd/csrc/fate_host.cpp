@@ -347,7 +347,8 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
         }
     }
     p->nS = (int64_t)p->slices.size() / 3;
-    // completed parents of every stage, with the state's holders and sizes
+    // completed parents of every pending stage (only pending stages are
+    // scored, in the frontier or in a horizon), with their holders and sizes
     p->done_off.assign(N + 1, 0);
     p->done.clear();
     {
@@ -358,6 +359,7 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
             for (int64_t v = 0; v < n; ++v) {
                 const int64_t s = base + v;
                 p->done_off[s] = (uint32_t)acc;
+                if (st->status[s] != FATE_PENDING) continue;
                 for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) {
                     const int64_t u = base + g->par_idx[q];
                     if (st->holders[u] == 0) continue;
