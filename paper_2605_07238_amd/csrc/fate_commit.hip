@@ -35,33 +35,43 @@ namespace {
 
 constexpr uint8_t kPending = FATE_PENDING, kCompleted = FATE_COMPLETED;
 
-// Exclusive scan over the workgroup (NT threads, a multiple of 64); `total`
-// receives the sum.  sh holds NT/64 + 1 words.
-template <int NT>
-__device__ uint32_t block_exscan(uint32_t x, uint32_t *sh, uint32_t &total) {
+// Exclusive scan over the workgroup (NT threads, a multiple of 64) of F
+// fields at once; total[] receives the sums.  sh holds F * NT / 64 words.
+// Wave-level shuffle scans, one barrier to publish the wave totals (every
+// thread adds the totals of the waves before its own), one barrier before sh
+// may be reused.
+template <int NT, int F>
+__device__ void block_exscan(const uint32_t (&x)[F], uint32_t *sh, uint32_t (&ex)[F], uint32_t (&total)[F]) {
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    uint32_t v = x;
+    constexpr int NW = NT / 64;
+    uint32_t v[F];
+#pragma unroll
+    for (int c = 0; c < F; ++c) v[c] = x[c];
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(v, off, 64);
-        if (lane >= off) v += y;
-    }
-    if (lane == 63) sh[wid] = v;
-    __syncthreads();
-    if (tid == 0) {
-        uint32_t run = 0;
-        for (int w = 0; w < NT / 64; ++w) {
-            const uint32_t t = sh[w];
-            sh[w] = run;
-            run += t;
+#pragma unroll
+        for (int c = 0; c < F; ++c) {
+            const uint32_t y = __shfl_up(v[c], off, 64);
+            if (lane >= off) v[c] += y;
         }
-        sh[NT / 64] = run;
+    }
+    if (lane == 63) {
+#pragma unroll
+        for (int c = 0; c < F; ++c) sh[c * NW + wid] = v[c];
     }
     __syncthreads();
-    const uint32_t r = sh[wid] + v - x;
-    total = sh[NT / 64];
+#pragma unroll
+    for (int c = 0; c < F; ++c) {
+        uint32_t before = 0, all = 0;
+        for (int w = 0; w < NW; ++w) {
+            const uint32_t t = sh[c * NW + w];
+            before += w < wid ? t : 0u;
+            all += t;
+        }
+        ex[c] = before + v[c] - x[c];
+        total[c] = all;
+    }
     __syncthreads();  // sh may be reused
-    return r;
 }
 
 // Instance of flat stage s: the last b with stage_off[b] <= s.
@@ -261,7 +271,7 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
 }
 
 __global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
-    __shared__ uint32_t sh[kPlanBlock / 64 + 1];
+    __shared__ uint32_t sh[3 * (kPlanBlock / 64)];
     const int64_t s0 = (int64_t)blockIdx.x * kPlanStages + (int64_t)threadIdx.x * kPlanItems;
     uint32_t tcp = 0, tfr = 0, tnc = 0;
     for (int i = 0; i < kPlanItems; ++i) {
@@ -285,48 +295,56 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
         tfr += ready ? 1u : 0u;
         tnc += nc;
     }
-    uint32_t tot_cp, tot_fr, tot_nc;
-    block_exscan<kPlanBlock>(tcp, sh, tot_cp);
-    block_exscan<kPlanBlock>(tfr, sh, tot_fr);
-    block_exscan<kPlanBlock>(tnc, sh, tot_nc);
+    const uint32_t x[3] = {tcp, tfr, tnc};
+    uint32_t ex[3], tot[3];
+    block_exscan<kPlanBlock, 3>(x, sh, ex, tot);
     if (threadIdx.x == 0) {
-        a.bsum[3 * blockIdx.x] = tot_cp;
-        a.bsum[3 * blockIdx.x + 1] = tot_fr;
-        a.bsum[3 * blockIdx.x + 2] = tot_nc;
+        a.bsum[3 * blockIdx.x] = tot[0];
+        a.bsum[3 * blockIdx.x + 1] = tot[1];
+        a.bsum[3 * blockIdx.x + 2] = tot[2];
     }
 }
 
+constexpr int kChunks = 8;  // 1024-item chunks whose loads one thread issues together
+
 __global__ __launch_bounds__(1024) void k_plan_offsets(CommitLaunch a) {
-    __shared__ uint32_t sh[1024 / 64 + 1];
-    uint32_t run_cp = 0, run_fr = 0, run_nc = 0;
-    for (int base = 0; base < a.nblk; base += 1024) {  // uniform
-        const int i = base + (int)threadIdx.x;
-        const bool in = i < a.nblk;
-        const uint32_t cp = in ? a.bsum[3 * i] : 0u, fr = in ? a.bsum[3 * i + 1] : 0u, nc = in ? a.bsum[3 * i + 2] : 0u;
-        uint32_t t_cp, t_fr, t_nc;
-        const uint32_t e_cp = block_exscan<1024>(cp, sh, t_cp);
-        const uint32_t e_fr = block_exscan<1024>(fr, sh, t_fr);
-        const uint32_t e_nc = block_exscan<1024>(nc, sh, t_nc);
-        if (in) {
-            a.bsum[3 * i] = run_cp + e_cp;
-            a.bsum[3 * i + 1] = run_fr + e_fr;
-            a.bsum[3 * i + 2] = run_nc + e_nc;
+    // chunks of 1024 workgroup triples, one triple per thread, scanned
+    // together; the loads of kChunks chunks are in flight at once
+    __shared__ uint32_t sh[3 * (1024 / 64)];
+    uint32_t run[3] = {0u, 0u, 0u};
+    for (int batch = 0; batch < a.nblk; batch += kChunks * 1024) {  // uniform
+        uint32_t x[kChunks][3];
+#pragma unroll
+        for (int q = 0; q < kChunks; ++q) {
+            const int i = batch + q * 1024 + (int)threadIdx.x;
+#pragma unroll
+            for (int c = 0; c < 3; ++c) x[q][c] = i < a.nblk ? a.bsum[3 * i + c] : 0u;
         }
-        run_cp += t_cp;
-        run_fr += t_fr;
-        run_nc += t_nc;
+#pragma unroll
+        for (int q = 0; q < kChunks; ++q) {
+            if (batch + q * 1024 >= a.nblk) break;  // uniform
+            const int i = batch + q * 1024 + (int)threadIdx.x;
+            uint32_t ex[3], tot[3];
+            block_exscan<1024, 3>(x[q], sh, ex, tot);
+            if (i < a.nblk) {
+#pragma unroll
+                for (int c = 0; c < 3; ++c) a.bsum[3 * i + c] = run[c] + ex[c];
+            }
+#pragma unroll
+            for (int c = 0; c < 3; ++c) run[c] += tot[c];
+        }
     }
     if (threadIdx.x == 0) {
-        a.done_off[a.N] = run_cp;
-        a.fidx[a.N] = run_fr;
-        a.cand_off[run_fr] = run_nc;
-        a.counts[0] = run_fr;
-        a.counts[1] = run_nc;
+        a.done_off[a.N] = run[0];
+        a.fidx[a.N] = run[1];
+        a.cand_off[run[1]] = run[2];
+        a.counts[0] = run[1];
+        a.counts[1] = run[2];
     }
 }
 
 __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
-    __shared__ uint32_t sh[kPlanBlock / 64 + 1];
+    __shared__ uint32_t sh[3 * (kPlanBlock / 64)];
     const int64_t s0 = (int64_t)blockIdx.x * kPlanStages + (int64_t)threadIdx.x * kPlanItems;
     uint32_t cp[kPlanItems], nc[kPlanItems];
     uint32_t tcp = 0, tfr = 0, tnc = 0;
@@ -339,10 +357,12 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
         tfr += nc[i] ? 1u : 0u;
         tnc += nc[i];
     }
-    uint32_t unused;
-    uint32_t dpos = a.bsum[3 * blockIdx.x] + block_exscan<kPlanBlock>(tcp, sh, unused);
-    uint32_t fpos = a.bsum[3 * blockIdx.x + 1] + block_exscan<kPlanBlock>(tfr, sh, unused);
-    uint32_t cpos = a.bsum[3 * blockIdx.x + 2] + block_exscan<kPlanBlock>(tnc, sh, unused);
+    const uint32_t x[3] = {tcp, tfr, tnc};
+    uint32_t ex[3], tot[3];
+    block_exscan<kPlanBlock, 3>(x, sh, ex, tot);
+    uint32_t dpos = a.bsum[3 * blockIdx.x] + ex[0];
+    uint32_t fpos = a.bsum[3 * blockIdx.x + 1] + ex[1];
+    uint32_t cpos = a.bsum[3 * blockIdx.x + 2] + ex[2];
     for (int i = 0; i < kPlanItems; ++i) {
         const int64_t s = s0 + i;
         if (s >= a.N) break;
@@ -373,33 +393,48 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
 }
 
 __global__ __launch_bounds__(1024) void k_plan_slices(CommitLaunch a) {
-    __shared__ uint32_t sh[1024 / 64 + 1];
-    uint32_t run = 0, rej = 0;
+    // chunks of 1024 instances, one per thread; the frontier bounds of
+    // kChunks chunks are loaded together
+    __shared__ uint32_t sh[2 * (1024 / 64)];
     const uint32_t slice = (uint32_t)a.slice;
-    for (int base = 0; base < a.B; base += 1024) {  // uniform
-        const int b = base + (int)threadIdx.x;
-        uint32_t f0 = 0, f1 = 0, nsl = 0, r = 0;
-        if (b < a.B) {
-            f0 = a.fidx[a.stage_off[b]];
-            f1 = a.fidx[a.stage_off[b + 1]];
-            nsl = (f1 - f0 + slice - 1) / slice;
-            r = a.rej[b];
+    uint32_t run[2] = {0u, 0u};
+    for (int batch = 0; batch < a.B; batch += kChunks * 1024) {  // uniform
+        int64_t s0[kChunks], s1[kChunks];
+#pragma unroll
+        for (int q = 0; q < kChunks; ++q) {
+            const int b = batch + q * 1024 + (int)threadIdx.x;
+            s0[q] = b < a.B ? a.stage_off[b] : 0;
+            s1[q] = b < a.B ? a.stage_off[b + 1] : 0;
         }
-        uint32_t t_sl, t_rej;
-        const uint32_t off = run + block_exscan<1024>(nsl, sh, t_sl);
-        block_exscan<1024>(r, sh, t_rej);
-        for (uint32_t c = 0; c < nsl; ++c) {
-            const int64_t o = 3 * (int64_t)(off + c);
-            a.slices[o] = (uint32_t)b;
-            a.slices[o + 1] = f0 + c * slice;
-            a.slices[o + 2] = min(f0 + (c + 1) * slice, f1);
+        uint32_t f0[kChunks], f1[kChunks], r[kChunks];
+#pragma unroll
+        for (int q = 0; q < kChunks; ++q) {
+            const int b = batch + q * 1024 + (int)threadIdx.x;
+            f0[q] = b < a.B ? a.fidx[s0[q]] : 0u;
+            f1[q] = b < a.B ? a.fidx[s1[q]] : 0u;
+            r[q] = b < a.B ? a.rej[b] : 0u;
         }
-        run += t_sl;
-        rej += t_rej;
+#pragma unroll
+        for (int q = 0; q < kChunks; ++q) {
+            if (batch + q * 1024 >= a.B) break;  // uniform
+            const int b = batch + q * 1024 + (int)threadIdx.x;
+            const uint32_t x[2] = {(f1[q] - f0[q] + slice - 1) / slice, r[q]};
+            uint32_t ex[2], tot[2];
+            block_exscan<1024, 2>(x, sh, ex, tot);
+            uint32_t off = run[0] + ex[0];
+            for (uint32_t f = f0[q]; f < f1[q]; f += slice, ++off) {
+                const int64_t o = 3 * (int64_t)off;
+                a.slices[o] = (uint32_t)b;
+                a.slices[o + 1] = f;
+                a.slices[o + 2] = min(f + slice, f1[q]);
+            }
+            run[0] += tot[0];
+            run[1] += tot[1];
+        }
     }
     if (threadIdx.x == 0) {
-        a.counts[2] = run;
-        a.counts[3] = rej;
+        a.counts[2] = run[0];
+        a.counts[3] = run[1];
     }
 }
 
