@@ -60,7 +60,12 @@
  *     planning step].  Per instance, the selected frontier stages are applied
  *     in ascending stage id; for each device d of the chosen candidate S
  *     (k = |S|), in ascending device id:
- *       start  = max(tau_d, t)
+ *       ready  = max over parents u of fin(u) + (0 if d holds u's output, else
+ *                sigma(u) * min over u's holders i of beta[i][d] / k)
+ *                [reading: a shard cannot start before its inputs arrive;
+ *                fin(u) is u's planned finish, t for a stage completed when
+ *                planning began]
+ *       start  = max(tau_d, t, ready)
  *       switch = kappa_switch(m(v), d) if m(v) is not resident on d, else 0
  *       rho_d  = Load(rho_d, m(v))                      (as in step 6)
  *       grp(v) joins the prefix slots of d if it is nonzero and absent: the
@@ -68,7 +73,8 @@
  *         move down by one (slot 0, the oldest, is dropped) and slot K-1
  *         takes it  [reading: the slots are kept oldest first]
  *       tau_d  = start + c(v,d)/k + switch
- *     then v is completed with its output held by exactly S.  The next
+ *     then v is completed with its output held by exactly S, and fin(v) is
+ *     the largest of those tau_d.  The next
  *     frontier follows from step 1 on the updated state.
  *
  * 12. Frontier planning wave (App. A.2 frontier placement problem: each
@@ -537,7 +543,7 @@ int oracle_topk(const double *psi, int64_t nc, int k, int32_t *idx, double *val)
  * pending. */
 int oracle_commit(const oracle_in_t *in, int B, const int64_t *f_off, const int32_t *front_v,
                   const int32_t *sel, uint64_t *res_out, uint64_t *cache_out, uint64_t *holders_out,
-                  uint8_t *status_out, double *tau_out) {
+                  uint8_t *status_out, double *tau_out, double *fin_io) {
     const int D = in->D, K = in->K;
     int rejected = 0;
     for (int b = 0; b < B; ++b) {
@@ -555,9 +561,22 @@ int oracle_commit(const oracle_in_t *in, int B, const int64_t *f_off, const int3
             int m = in->model[g];
             uint64_t h = in->hash[g];
             uint64_t held = 0;
+            double fin = -INFINITY;
             for (int d = i0; d < i0 + k; ++d) {
                 int64_t bd = (int64_t)b * D + d;
                 double start = tau_out[bd] > (double)in->t_now[b] ? tau_out[bd] : (double)in->t_now[b];
+                for (int64_t q = in->par_off[g]; q < in->par_off[g + 1]; ++q) {
+                    int64_t u = base + in->par_idx[q];
+                    double arr = fin_io[u];
+                    if (!has_bit(holders_out[u], d)) {
+                        double bmin = INFINITY;
+                        for (int i = 0; i < D; ++i)
+                            if (has_bit(holders_out[u], i) && (double)in->beta[i * D + d] < bmin)
+                                bmin = (double)in->beta[i * D + d];
+                        arr = fin_io[u] + (double)in->sigma[u] * bmin / (double)k;
+                    }
+                    if (arr > start) start = arr;
+                }
                 double sw = has_bit(res_out[bd], m) ? 0.0 : (double)in->switch_s[m * D + d];
                 res_out[bd] = load_model(in, res_out[bd], m, d);
                 if (h != 0 && K > 0) {
@@ -577,10 +596,12 @@ int oracle_commit(const oracle_in_t *in, int B, const int64_t *f_off, const int3
                     }
                 }
                 tau_out[bd] = start + exec_c(in, m, d) / (double)k + sw;
+                if (tau_out[bd] > fin) fin = tau_out[bd];
                 held |= (uint64_t)1 << d;
             }
             holders_out[g] = held;
             status_out[g] = ST_COMPLETED;
+            fin_io[g] = fin;
         }
     }
     return rejected;

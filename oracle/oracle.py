@@ -81,7 +81,7 @@ def _bind(lib):
     lib.oracle_frontier.argtypes = [C.POINTER(_In), C.c_int, C.c_void_p, C.c_void_p]
     lib.oracle_frontier.restype = C.c_int
     lib.oracle_commit.argtypes = [C.POINTER(_In), C.c_int, C.c_void_p, C.c_void_p, C.c_void_p,
-                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.oracle_commit.restype = C.c_int
     lib.oracle_plan_wave.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int,
                                      C.c_void_p]
@@ -196,14 +196,26 @@ def frontier(w, max_shard: Optional[int] = None, lib=None):
     return front_b, front_v, f_off
 
 
-def commit(w, sel, max_shard: Optional[int] = None, lib=None):
+def initial_finish(w):
+    """Planned finish times at the start of planning: t for completed stages
+    (their outputs are available when planning begins), 0 for the others
+    (never read before they are committed).  float32, the planning state's
+    format."""
+    inst = np.repeat(np.arange(w.B), np.diff(w.stage_off))
+    return np.where(w.status == 1, np.asarray(w.t_now, np.float32)[inst], 0.0).astype(np.float32)
+
+
+def commit(w, sel, max_shard: Optional[int] = None, lib=None, fin=None):
     """Commit-and-advance (oracle step 11): apply the candidate ``sel[f]``
-    chosen for each frontier slot f of ``w`` (-1 = leave pending).
+    chosen for each frontier slot f of ``w`` (-1 = leave pending).  ``fin``
+    [N] holds the planned finish times of completed stages (default:
+    initial_finish(w), the start of planning).
 
     Returns (new workload, tau in fp64 [B, D], number of rejected
-    selections).  The new workload is a copy of ``w`` whose resident models,
-    prefix slots, holders, statuses and free times (rounded to float32, the
-    state's format) are the committed state."""
+    selections, fin [N] float32).  The new workload is a copy of ``w`` whose
+    resident models, prefix slots, holders, statuses and free times (rounded
+    to float32, the state's format) are the committed state; fin gains the
+    committed stages' planned finish, rounded to float32 the same way."""
     import dataclasses
     lib = lib or load()
     front_b, front_v, f_off = frontier(w, max_shard, lib)
@@ -216,12 +228,13 @@ def commit(w, sel, max_shard: Optional[int] = None, lib=None):
     holders = np.array(w.holders, dtype=np.uint64, copy=True)
     status = np.array(w.status, dtype=np.uint8, copy=True)
     tau = np.array(w.tau_free, dtype=np.float64, copy=True)
+    fin64 = np.array(initial_finish(w) if fin is None else fin, dtype=np.float32).astype(np.float64)
     rejected = lib.oracle_commit(C.byref(rec), w.B, f_off.ctypes.data, front_v.ctypes.data, sel.ctypes.data,
                                  res.ctypes.data, cache.ctypes.data, holders.ctypes.data, status.ctypes.data,
-                                 tau.ctypes.data)
+                                 tau.ctypes.data, fin64.ctypes.data)
     new = dataclasses.replace(w, resident=res, prefix_cache=cache, holders=holders, status=status,
                               tau_free=tau.astype(np.float32))
-    return new, tau, int(rejected)
+    return new, tau, int(rejected), fin64.astype(np.float32)
 
 
 def plan_wave(D: int, f_off, n_cand, idx, val, lib=None):

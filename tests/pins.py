@@ -303,7 +303,7 @@ def check_commit_scenario(name: str, lib=None):
     w = builders.from_spec(sc["spec"], H=1)
     _, fv, _ = oracle.frontier(w, lib=lib)
     assert fv.tolist() == sc["front_v"], fv
-    new, tau, rejected = oracle.commit(w, sc["sel"], lib=lib)
+    new, tau, rejected, fin = oracle.commit(w, sc["sel"], lib=lib)
     assert rejected == sc["rejected"], rejected
     assert new.resident.reshape(-1).tolist() == sc["resident"], new.resident
     assert new.prefix_cache.reshape(w.D, w.K).tolist() == sc["prefix_cache"], new.prefix_cache
@@ -312,6 +312,20 @@ def check_commit_scenario(name: str, lib=None):
     _close(tau.reshape(-1), sc["tau"], rtol=0, atol=0)
     _, fv2, _ = oracle.frontier(new, lib=lib)
     assert fv2.tolist() == sc["next_front_v"], fv2
+
+
+def check_commit_ready(lib=None):
+    """Two commits in a row where shards wait for their parents' outputs."""
+    sc = scenarios.COMMIT_READY
+    w = builders.from_spec(sc["spec"], H=1)
+    fin = None
+    for step in sc["steps"]:
+        _, fv, _ = oracle.frontier(w, lib=lib)
+        assert fv.tolist() == step["front_v"], fv
+        w, tau, rejected, fin = oracle.commit(w, step["sel"], lib=lib, fin=fin)
+        assert rejected == 0
+        _close(tau.reshape(-1), step["tau"], rtol=0, atol=0)
+        assert fin.tolist() == step["fin"], fin
 
 
 def check_commit_invariants(seed: int, lib=None):
@@ -325,11 +339,12 @@ def check_commit_invariants(seed: int, lib=None):
     w = synth.make_random_small(seed, B=3, n=24, D=6, M=5, K=3, max_shard=3, shard_frac=0.6, tight_caps=True)
     r = oracle.score(w, lib=lib)
     idx, _ = oracle.topk(r, 1, lib=lib)
-    none, _, rej0 = oracle.commit(w, np.full(len(r["front_v"]), -1, np.int32), lib=lib)
+    none, _, rej0, fin0 = oracle.commit(w, np.full(len(r["front_v"]), -1, np.int32), lib=lib)
     assert rej0 == 0
     for f in ("resident", "prefix_cache", "holders", "status", "tau_free"):
         assert np.array_equal(getattr(none, f), getattr(w, f)), f
-    new, tau, rej = oracle.commit(w, idx[:, 0], lib=lib)
+    assert np.array_equal(fin0, oracle.initial_finish(w))
+    new, tau, rej, fin = oracle.commit(w, idx[:, 0], lib=lib)
     assert rej == 0
     D, K = w.D, w.K
 
@@ -360,10 +375,28 @@ def check_commit_invariants(seed: int, lib=None):
         S = devices(j)
         assert new.status[g] == 1 and int(new.holders[g]) == sum(1 << d for d in S)
         m = int(w.model[g])
+        k = len(S)
+        # the stage finishes with its latest shard
+        assert any(uses[b, d] != 1 for d in S) or fin[g] == np.float32(max(tau[b, d] for d in S))
         for d in S:
             assert tau[b, d] >= float(w.tau_free[b, d])
             if uses[b, d] != 1:
                 continue
+            # a shard starts no earlier than the device is free, than t, and
+            # than each parent's output is there, and at one of those times
+            run = float(w.exec[m, d]) / k + (0.0 if (int(w.resident[b, d]) >> m) & 1 else float(w.switch_s[m, d]))
+            start = tau[b, d] - run
+            lo = int(w.stage_off[b])
+            arrivals = [max(float(w.tau_free[b, d]), float(np.float32(w.t_now[b])))]
+            for p in w.par_idx[w.par_off[g]:w.par_off[g + 1]]:
+                u = lo + int(p)
+                hu = int(w.holders[u])
+                t_u = float(np.float32(w.t_now[b]))  # completed before planning
+                if not (hu >> d) & 1:
+                    t_u += float(w.out_bytes[u]) * min(float(w.beta[i, d]) for i in range(D) if (hu >> i) & 1) / k
+                arrivals.append(t_u)
+            assert start >= max(arrivals) - 1e-9 * max(1.0, start), (g, d, start, arrivals)
+            assert min(abs(start - a) for a in arrivals) <= 1e-9 * max(1.0, start), (g, d, start, arrivals)
             old = int(w.resident[b, d])
             res = int(new.resident[b, d])
             assert (res >> m) & 1
@@ -668,6 +701,7 @@ ALL_CHECKS = (
     + [("isolated:%d" % s, (lambda s: lambda lib: check_isolated_stage(s, lib))(s)) for s in range(2)]
     + [("commit:" + k, (lambda k: lambda lib: check_commit_scenario(k, lib))(k)) for k in scenarios.COMMITS]
     + [("commit_invariants:%d" % s, (lambda s: lambda lib: check_commit_invariants(s, lib))(s)) for s in range(3)]
+    + [("commit_ready", check_commit_ready)]
     + [("variant:" + k, (lambda k: lambda lib: check_variant_scenario(k, lib))(k)) for k in scenarios.VARIANTS]
     + [("variant_reduction:%s:%d" % (m, s),
         (lambda s, t, mn: lambda lib: check_variant_reduction(s, lib, topo=t, mean=mn))(s, t, mn))

@@ -200,6 +200,25 @@ COMMIT_REJECT = dict(
     resident=[0, 0], prefix_cache=[[0], [0]], tau=[0.0, 0.0],
     holders=[0, 0], status=[0, 0], next_front_v=[0, 1], rejected=2)
 
+# C4: a shard waits for its inputs.  Stage 0 is completed on d0 (2^31 bytes,
+#     available at t = 1); beta = 2^-32 between the two devices; every
+#     runtime is 1, the model is resident everywhere, tau = [0.5, 0.5].
+#   Step 1: stage 1 on the window {d0, d1} (k = 2): d0 holds stage 0's output:
+#     start max(0.5, 1, 1) = 1, tau0 = 1 + 1/2 = 1.5; d1 waits for half of it:
+#     1 + 2^31 * 2^-32 / 2 = 1.25, tau1 = 1.25 + 0.5 = 1.75; fin(1) = 1.75.
+#     Stage 2 on d1: all of stage 0's output, 1 + 0.5 = 1.5, but d1 is busy
+#     until 1.75: tau1 = 2.75 = fin(2).
+#   Step 2: stage 3 (parents 1 and 2) on d0: stage 1 is local (1.75); stage
+#     2's 2^32 bytes arrive at 2.75 + 1 = 3.75: tau0 = 4.75 = fin(3).
+COMMIT_READY = dict(
+    spec=dict(D=2, M=1, K=1, exec=[[1.0, 1.0]], switch_s=[[0.0, 0.0]], weight_gb=[10], cap_gb=[25, 25],
+              beta=[[1.0, 2.0 ** -32], [2.0 ** -32, 1.0]], max_shard=2,  # the diagonal is never used
+              instances=[dict(parents=[[], [0], [0], [1, 2]], model=[0] * 4, elig=[3] * 4, shard_max=[1, 2, 1, 1],
+                              out_bytes=[2.0 ** 31, 1.0, 2.0 ** 32, 1.0], status=[1, 0, 0, 0],
+                              holders=[1, 0, 0, 0], resident=[1, 1], tau_free=[0.5, 0.5], t_now=1.0)]),
+    steps=[dict(front_v=[1, 2], sel=[2, 1], tau=[1.5, 2.75], fin=[1.0, 1.75, 2.75, 0.0]),
+           dict(front_v=[3], sel=[0], tau=[4.75, 2.75], fin=[1.0, 1.75, 2.75, 4.75])])
+
 COMMITS = dict(COMMIT_SINGLE=COMMIT_SINGLE, COMMIT_WINDOW=COMMIT_WINDOW, COMMIT_REJECT=COMMIT_REJECT)
 
 

@@ -109,6 +109,7 @@ def test_plan_then_commit_loop():
     pk = fate.fate_pack_dags(w)
     st = fate.fate_pack_state(pk, w, advance=True)
     cur = w
+    fin = None
     k = 4
     ws = None
     for step in range(12):
@@ -132,7 +133,7 @@ def test_plan_then_commit_loop():
         assert np.array_equal(got, want), step
         ws = fate.fate_commit_advance(pk, st, sel, ws=ws)
         torch.cuda.synchronize()
-        nxt, tau, rej = oracle.commit(cur, want)
+        nxt, tau, rej, fin = oracle.commit(cur, want, fin=fin)
         assert rej == 0 and st.counts()[3] == 0
         _compare_state(st, nxt, tau)
         _compare_sections(pk, st, nxt)

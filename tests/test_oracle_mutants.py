@@ -63,6 +63,12 @@ MUTANTS = {
     "commit_no_load": [("res_out[bd] = load_model(in, res_out[bd], m, d);", "res_out[bd] = res_out[bd];")],
     "commit_ignores_feasibility": [("if (!ok) { ++rejected; continue; }", "if (0) { ++rejected; continue; }")],
     "commit_not_completed": [("status_out[g] = ST_COMPLETED;", "status_out[g] = status_out[g];")],
+    "commit_ignores_inputs": [("                    if (arr > start) start = arr;\n", "")],
+    "commit_input_not_split": [("arr = fin_io[u] + (double)in->sigma[u] * bmin / (double)k;",
+                                "arr = fin_io[u] + (double)in->sigma[u] * bmin;")],
+    "commit_local_input_transferred": [("                    if (!has_bit(holders_out[u], d)) {\n                        double bmin",
+                                        "                    if (1) {\n                        double bmin")],
+    "commit_finish_first_shard": [("if (tau_out[bd] > fin) fin = tau_out[bd];", "if (fin == -INFINITY) fin = tau_out[bd];")],
     # scoring variants
     "same_model_when_absent": [("return has_bit(s->res[d], s->in->model[s->base + x]) ? 1.0 : 0.0;",
                                 "return has_bit(s->res[d], s->in->model[s->base + x]) ? 0.0 : 1.0;")],

@@ -102,6 +102,7 @@ def _oracle_fate_plan(w, k=4, max_waves=200):
     devices = np.zeros(w.N, np.uint64)
     order = np.zeros(w.N, np.int64)
     cur = w
+    fin = None
     for wave in range(max_waves):
         ref = oracle.score(cur)
         if len(ref["front_v"]) == 0:
@@ -110,7 +111,7 @@ def _oracle_fate_plan(w, k=4, max_waves=200):
         _, _, f_off = oracle.frontier(cur)
         sel, n = oracle.plan_wave(cur.D, f_off, np.diff(ref["cand_off"]), idx, val.astype(np.float32))
         assert n > 0
-        nxt, _, rej = oracle.commit(cur, sel)
+        nxt, _, rej, fin = oracle.commit(cur, sel, fin=fin)
         assert rej == 0
         for f in np.nonzero(sel >= 0)[0]:
             g = int(cur.stage_off[ref["front_b"][f]]) + int(ref["front_v"][f])
