@@ -221,6 +221,8 @@ typedef struct {
     int32_t advance;
     const uint8_t *status;    /* [N] stage status: FATE_PENDING .. FATE_COMMITTED */
     const uint32_t *counts;   /* [4] device counters, see above */
+    const float *finish;      /* [N] planned finish of completed stages (t_now for
+                                 those completed when planning began) */
 } fate_state_h;
 
 const char *fate_version(void);
@@ -314,13 +316,17 @@ fate_status_t fate_commit_ws_size(const fate_dags_t *dags, const fate_state_h *s
  *     the stage pending.  Device memory, read only.
  * Per instance the selected stages are applied in ascending stage id, and on
  * each device d of the chosen candidate S (k = |S|):
- *   start = max(tau_d, t); the switch time kappa_switch(m(v), d) counts if
- *   m(v) was not resident; m(v) is loaded (the smallest-id other models are
+ *   start = max(tau_d, t, every parent u's finish(u) + (0 if d holds u's
+ *   output, else sigma(u) * min over u's holders i of beta[i][d] / k)), as a
+ *   shard starts when its inputs are there; the switch time
+ *   kappa_switch(m(v), d) counts if m(v) was not resident; m(v) is loaded
+ *   (the smallest-id other models are
  *   evicted while the weights exceed the capacity, as in the post-state of
  *   fate_score_frontier); grp(v), if nonzero and absent, takes the first
  *   empty prefix slot of d or, with all slots full, is appended after
  *   dropping slot 0 (slots are kept oldest first); tau_d = start + c(v,d)/k
- *   + switch.  Then v is completed and its output is held by exactly S.
+ *   + switch.  Then v is completed, its output is held by exactly S, and its
+ *   finish is the largest of those tau_d.
  * A selection past the stage's candidates, or whose candidate has a device
  * that is not eligible or cannot hold the model, is skipped and counted in
  * counts[3].  Afterwards the frontier (pending stages whose parents are all

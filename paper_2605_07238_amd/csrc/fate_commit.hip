@@ -91,19 +91,42 @@ __device__ int instance_of(const int64_t *stage_off, int B, int64_t s) {
 struct SlotL {
     uint64_t win, hash, wm;  // wm: the model's weight
     double k;
-    int32_t model, pad;
+    int32_t model, i0;       // i0: the window's first device
+    double ready[FATE_MAX_SHARD];  // when the inputs are on window device i0 + p
 };
 
 // Prefix-slot rows in LDS are padded to a multiple of 8 entries so that a
 // row is searched 8 entries per batch of loads.
 __host__ __device__ inline int padded_slots(int K) { return (K + 7) & ~7; }
 
-// LDS of k_commit_apply: the staged slots, the exec and switch tables, the
-// model weights and fit masks, the instance's prefix-slot rows and each
-// row's ring head.
+// LDS of k_commit_apply: the staged slots and their shards' finish times,
+// the exec and switch tables, the model weights and fit masks, the instance's
+// prefix-slot rows and each row's ring head.
 __host__ __device__ inline size_t apply_lds_bytes(int D, int M, int K) {
-    return 64 * sizeof(SlotL) + 8 * (size_t)M * D + 16 * (size_t)M + 8 * (size_t)D * padded_slots(K) +
-           4 * (size_t)D;
+    return 64 * sizeof(SlotL) + 64 * 8 * FATE_MAX_SHARD + 8 * (size_t)M * D + 16 * (size_t)M +
+           8 * (size_t)D * padded_slots(K) + 4 * (size_t)D;
+}
+
+// When the outputs of stage s's parents are on device d for a k-shard
+// placement: the latest parent finish plus, for a parent whose output d does
+// not hold, its size times the cheapest transfer coefficient into d over k.
+__device__ double inputs_ready(const CommitLaunch &a, const StageRec &r, int d, int k) {
+    double ready = -__builtin_inf();
+    for (uint32_t q = 0; q < r.npar; ++q) {
+        const uint32_t u = a.par_idx[r.par_begin + q];
+        const uint64_t hu = a.holders[u];
+        double arr = (double)a.fin[u];
+        if (!bit(hu, d)) {
+            double bmin = __builtin_inf();
+            for (uint64_t t = hu; t; t &= t - 1) {
+                const double bt = (double)a.beta[__builtin_ctzll(t) * a.D + d];
+                bmin = bt < bmin ? bt : bmin;
+            }
+            arr = (double)a.fin[u] + (double)a.rec[u].sigma * bmin / (double)k;
+        }
+        ready = arr > ready ? arr : ready;
+    }
+    return ready;
 }
 
 // Is the nonzero group h in the padded row?  Empty and padding entries
@@ -131,7 +154,8 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
     extern __shared__ uint64_t smem[];
     const int b = blockIdx.x, lane = threadIdx.x, D = a.D, K = a.K, M = a.M, Kp = padded_slots(K);
     SlotL *sl = reinterpret_cast<SlotL *>(smem);
-    uint64_t *wt = smem + (64 * sizeof(SlotL)) / 8;
+    double *sfin = reinterpret_cast<double *>(smem + (64 * sizeof(SlotL)) / 8);  // [64][FATE_MAX_SHARD]
+    uint64_t *wt = reinterpret_cast<uint64_t *>(sfin + 64 * FATE_MAX_SHARD);
     uint64_t *fit = wt + M;
     uint64_t *pslots = fit + M;
     float *ex = reinterpret_cast<float *>(pslots + (size_t)D * Kp);
@@ -179,15 +203,17 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
         const int64_t f = c0 + lane;
         uint64_t win = 0;
         bool rej = false;
+        uint32_t s = 0;
+        int kq = 0;
         if (f < hi) {
-            const uint32_t s = a.frontier[2 * f];
+            s = a.frontier[2 * f];
             const int j = a.sel[f * a.sel_stride];
             const StageRec r = a.rec[s];
             SlotL x;
             x.hash = r.hash;
             x.model = r.model;
             x.wm = wt[r.model];
-            x.pad = 0;
+            x.i0 = 0;
             x.k = 1.0;
             if (j >= 0) {
                 if (j >= candidates_of(shard_cap_of(r.shard, a.max_shard, D), D)) {
@@ -200,7 +226,12 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
                         rej = true;
                     } else {
                         win = w;
+                        kq = k;
                         x.k = (double)k;
+                        x.i0 = i0;
+                        // parents completed in earlier steps: their finish
+                        // times and holders are settled
+                        for (int p = 0; p < k; ++p) x.ready[p] = inputs_ready(a, r, i0 + p, k);
                         a.holders[s] = w;
                         a.status[s] = kCompleted;
                     }
@@ -223,7 +254,9 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
             mine &= mine - 1;
             const SlotL x = sl[q];
             const int m = x.model;
-            const double start = tau > tn ? tau : tn;
+            const double ready = x.ready[d - x.i0];
+            double start = tau > tn ? tau : tn;
+            start = ready > start ? ready : start;
             const double c = (double)ex[m * D + d];
             double sw = 0.0;
             if (m != last_m) {
@@ -252,8 +285,17 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
                 }
             }
             tau = start + (x.k == 1.0 ? c : c / x.k) + sw;  // c / 1 is c
+            sfin[q * FATE_MAX_SHARD + (d - x.i0)] = tau;
         }
         __syncthreads();  // the next chunk overwrites the staged slots
+        if (kq > 0) {  // the stage finishes with its latest shard
+            double fs = sfin[lane * FATE_MAX_SHARD];
+            for (int p = 1; p < kq; ++p) {
+                const double t2 = sfin[lane * FATE_MAX_SHARD + p];
+                fs = t2 > fs ? t2 : fs;
+            }
+            a.fin[s] = (float)fs;
+        }
     }
     if (live) {
         a.resident[t] = res;

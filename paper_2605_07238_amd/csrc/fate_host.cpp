@@ -381,7 +381,8 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
 }
 
 struct StateLayout {
-    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_off, done, status, counts, total;
+    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_off, done, status, finish, counts,
+        total;
 };
 
 // Section sizes: nF frontier slots, nS slices, nDone completed-parent entries
@@ -403,6 +404,8 @@ StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS,
     L.done = o; o = align_up(o + sizeof(fate::DoneParent) * nDone);
     L.status = o;
     if (advance) o = align_up(o + (size_t)N);
+    L.finish = o;
+    if (advance) o = align_up(o + sizeof(float) * (size_t)N);
     L.counts = o;
     if (advance) o = align_up(o + 4 * sizeof(uint32_t));
     L.total = o;
@@ -432,8 +435,8 @@ fate_status_t advance_caps(const fate_dags_t *pk, const fate_dag_batch_t *g, con
     return FATE_OK;
 }
 
-void write_state_image(const fate_dags_t *pk, const fate_state_t *st, const StatePlan &p, const StateLayout &L,
-                       uint8_t *img) {
+void write_state_image(const fate_dags_t *pk, const fate_dag_batch_t *g, const fate_state_t *st, const StatePlan &p,
+                       const StateLayout &L, uint8_t *img) {
     const int B = pk->B, D = pk->D, K = st->K;
     std::memcpy(img + L.resident, st->resident, sizeof(uint64_t) * B * D);
     if (K > 0) std::memcpy(img + L.pcache, st->prefix_cache, sizeof(uint64_t) * (size_t)B * D * K);
@@ -447,6 +450,11 @@ void write_state_image(const fate_dags_t *pk, const fate_state_t *st, const Stat
     if (!p.done.empty()) std::memcpy(img + L.done, p.done.data(), sizeof(fate::DoneParent) * p.done.size());
     if (L.counts > L.status) {  // planning state
         std::memcpy(img + L.status, st->status, (size_t)pk->N);
+        // planned finish: t for the stages completed when planning begins
+        float *fin = reinterpret_cast<float *>(img + L.finish);
+        for (int b = 0; b < B; ++b)
+            for (int64_t s = g->stage_off[b]; s < g->stage_off[b + 1]; ++s)
+                fin[s] = st->status[s] == FATE_COMPLETED ? st->t_now[b] : 0.0f;
         const uint32_t counts[4] = {(uint32_t)p.nF, (uint32_t)p.nC, (uint32_t)p.nS, 0u};
         std::memcpy(img + L.counts, counts, sizeof(counts));
     }
@@ -485,6 +493,7 @@ void fill_advance_handle(const AdvanceCaps &c, const StateLayout &L, uint8_t *ba
     out->n_done_edges = c.nDone;
     out->advance = 1;
     out->status = base + L.status;
+    out->finish = reinterpret_cast<const float *>(base + L.finish);
     out->counts = reinterpret_cast<const uint32_t *>(base + L.counts);
 }
 
@@ -619,7 +628,7 @@ static fate_status_t build_state(const fate_dags_t *packed, const fate_dag_batch
     L = state_layout(packed->B, packed->D, state->K, packed->N, p.nF, p.nS, (int64_t)p.done.size());
     if (bytes < L.total) return FATE_ESIZE;
     img.assign(L.total, 0);
-    write_state_image(packed, state, p, L, img.data());
+    write_state_image(packed, dags, state, p, L, img.data());
     return FATE_OK;
 }
 
@@ -678,7 +687,7 @@ fate_status_t fate_pack_state_advance(const fate_dags_t *packed, const fate_dag_
     const StateLayout L = state_layout(packed->B, packed->D, state->K, packed->N, c.nF, c.nS, c.nDone, true);
     if (bytes < L.total) return FATE_ESIZE;
     std::vector<uint8_t> img(L.total, 0);
-    write_state_image(packed, state, p, L, img.data());
+    write_state_image(packed, dags, state, p, L, img.data());
     st = copy_to_device(d_buf, img.data(), L.total, stream);
     if (st != FATE_OK) return st;
     fill_state_handle(packed, state, max_shard, p, L, static_cast<uint8_t *>(d_buf), bytes, out);
@@ -727,6 +736,8 @@ fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *s
     a.pcache = const_cast<uint64_t *>(state->prefix_cache);
     a.holders = const_cast<uint64_t *>(state->holders);
     a.tau = const_cast<float *>(state->tau_free);
+    a.fin = const_cast<float *>(state->finish);
+    a.beta = dags->beta;
     a.tnow = state->t_now;
     a.status = const_cast<uint8_t *>(state->status);
     a.frontier = const_cast<uint32_t *>(state->frontier);

@@ -97,11 +97,11 @@ struct CommitLaunch {
     const StageRec *rec;
     const uint32_t *par_idx;
     const int64_t *stage_off;
-    const float *exec, *ksw;
+    const float *exec, *ksw, *beta;
     const uint64_t *weight, *cap, *fits;
     // planning state, updated in place
     uint64_t *resident, *pcache, *holders;
-    float *tau;
+    float *tau, *fin;
     const float *tnow;
     uint8_t *status;
     uint32_t *frontier, *cand_off, *slices, *done_off;

@@ -99,7 +99,7 @@ class StateH(C.Structure):
                 ("frontier", C.c_void_p), ("cand_off", C.c_void_p),
                 ("n_slices", C.c_int64), ("slices", C.c_void_p),
                 ("n_done_edges", C.c_int64), ("done_off", C.c_void_p), ("done", C.c_void_p),
-                ("advance", C.c_int32), ("status", C.c_void_p), ("counts", C.c_void_p)]
+                ("advance", C.c_int32), ("status", C.c_void_p), ("counts", C.c_void_p), ("finish", C.c_void_p)]
 
 
 _lib = None
@@ -523,7 +523,8 @@ def fate_commit_advance(packed: PackedDags, state: PackedState, sel, ws=None, st
 
 def state_arrays(state: PackedState):
     """Host copies of the packed state arrays: resident [B, D], prefix slots
-    [B, D, K], holders [N], free times [B, D], and (planning state) status [N]."""
+    [B, D, K], holders [N], free times [B, D], and (planning state) status [N]
+    and planned finish [N]."""
     import torch
     h = state.handle
     base = state.buf.data_ptr()
@@ -541,6 +542,7 @@ def state_arrays(state: PackedState):
                holders=take(h.holders, N, np.uint64), tau_free=take(h.tau_free, B * D, np.float32).reshape(B, D))
     if h.advance:
         out["status"] = take(h.status, N, np.uint8)
+        out["finish"] = take(h.finish, N, np.float32)
     return out
 
 

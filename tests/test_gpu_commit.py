@@ -54,8 +54,12 @@ def _host_sections(pk, w):
                 done=take(h.done, 4 * int(done_off[-1])).reshape(-1, 4), n_cand=int(h.n_cand))
 
 
-def _compare_state(st, w_ref, tau_ref):
+def _compare_state(st, w_ref, tau_ref, fin_ref=None):
     got = fate.state_arrays(st)
+    if fin_ref is not None:  # planned finish of the completed stages, rounded once to fp32 on both sides
+        done = w_ref.status == 1
+        assert np.array_equal(got["finish"][done].view(np.uint32), np.asarray(fin_ref, np.float32)[done].view(np.uint32)), \
+            "planned finish times"
     assert np.array_equal(got["resident"], w_ref.resident.reshape(got["resident"].shape)), "resident models"
     assert np.array_equal(got["prefix_cache"], w_ref.prefix_cache.reshape(got["prefix_cache"].shape)), "prefix slots"
     assert np.array_equal(got["holders"], w_ref.holders), "holders"
@@ -102,6 +106,7 @@ def _run_steps(w, steps, params=None, sel_fn=None):
     pk = fate.fate_pack_dags(w)
     st = fate.fate_pack_state(pk, w, advance=True)
     cur = w
+    fin = None
     ws = None
     for step in range(steps):
         print("[gpu] commit step", step, "frontier", st.counts()[0], flush=True)
@@ -110,12 +115,12 @@ def _run_steps(w, steps, params=None, sel_fn=None):
             break
         idx, _ = oracle.topk(ref, 1)
         sel = idx[:, 0] if sel_fn is None else sel_fn(ref, idx[:, 0])
-        nxt, tau, rej = oracle.commit(cur, sel)
+        nxt, tau, rej, fin = oracle.commit(cur, sel, fin=fin)
         d_sel = torch.from_numpy(np.ascontiguousarray(sel, np.int32)).cuda()
         ws = fate.fate_commit_advance(pk, st, d_sel, ws=ws)
         torch.cuda.synchronize()
         assert st.counts()[3] == rej, (st.counts(), rej)
-        _compare_state(st, nxt, tau)
+        _compare_state(st, nxt, tau, fin)
         _compare_sections(pk, st, nxt)
         cur = nxt
     return pk, st, cur
@@ -189,11 +194,11 @@ def test_commit_top_k_array_as_selection():
     idx, _ = oracle.topk(ref, 1)
     sel2 = np.full((len(idx), 3), 12345, np.int32)  # columns 1, 2 would be rejected if read
     sel2[:, 0] = idx[:, 0]
-    nxt, tau, rej = oracle.commit(w, idx[:, 0])
+    nxt, tau, rej, fin = oracle.commit(w, idx[:, 0])
     fate.fate_commit_advance(pk, st, torch.from_numpy(sel2).cuda())
     torch.cuda.synchronize()
     assert st.counts()[3] == 0
-    _compare_state(st, nxt, tau)
+    _compare_state(st, nxt, tau, fin)
 
 
 def test_commit_nothing_keeps_everything():
@@ -263,3 +268,24 @@ def test_commit_long_device_chains_wrap_prefix_rows():
     w = dataclasses.replace(w, prefix_hash=ph, prefix_cache=pc.reshape(w.prefix_cache.shape))
     assert np.count_nonzero(np.isfinite(oracle.score(w)["psi"])) > 40
     _run_steps(w, 4, sel_fn=_lowest_feasible)
+
+
+def test_commit_inputs_ready_scenario():
+    """The two-step hand scenario where shards wait for their parents' outputs
+    (window shards waiting for half a transfer, a busy device, a remote parent
+    in the next step), on the GPU."""
+    import builders
+    import scenarios
+    sc = scenarios.COMMIT_READY
+    w = builders.from_spec(sc["spec"], H=1)
+    pk = fate.fate_pack_dags(w)
+    st = fate.fate_pack_state(pk, w, advance=True)
+    import torch
+    for step in sc["steps"]:
+        assert st.counts()[0] == len(step["sel"])
+        fate.fate_commit_advance(pk, st, torch.tensor(step["sel"], dtype=torch.int32, device="cuda"))
+        torch.cuda.synchronize()
+        got = fate.state_arrays(st)
+        assert got["tau_free"].reshape(-1).tolist() == step["tau"], got["tau_free"]
+        done = got["status"] == 1
+        assert got["finish"][done].tolist() == [x for x, dn in zip(step["fin"], done) if dn], got["finish"]

@@ -135,7 +135,7 @@ def test_plan_then_commit_loop():
         torch.cuda.synchronize()
         nxt, tau, rej, fin = oracle.commit(cur, want, fin=fin)
         assert rej == 0 and st.counts()[3] == 0
-        _compare_state(st, nxt, tau)
+        _compare_state(st, nxt, tau, fin)
         _compare_sections(pk, st, nxt)
         cur = nxt
     assert step >= 3
