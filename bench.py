@@ -35,7 +35,8 @@ if ROOT not in sys.path:
 DEFAULT_WORKLOAD = "forkjoin-4096x1000-d16"
 HBM_PEAK_GBS = 8000.0
 METRIC = "candidate-horizon evaluations/sec and achieved HBM GB/s (fraction of peak)"
-KERNEL_SRC = os.path.join(ROOT, "paper_2605_07238_amd", "csrc", "fate_kernels.hip")
+# the score kernel and the header that fixes its launch geometry (slice length)
+KERNEL_SRC = [os.path.join(ROOT, "paper_2605_07238_amd", "csrc", f) for f in ("fate_kernels.hip", "fate_internal.h")]
 
 
 def log(*a):
@@ -43,7 +44,10 @@ def log(*a):
 
 
 def kernel_sha() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SRC:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
 
 
 def counted_work(w, pk, st, scores_host, H):

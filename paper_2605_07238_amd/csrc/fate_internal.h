@@ -143,9 +143,14 @@ inline int group_width(int D) {
     while (g < D) g <<= 1;
     return g;
 }
+// Frontier stages per scoring workgroup: eight per lane group, but four for
+// 16-lane groups, whose slot-layout staging leaves the least LDS for stage
+// records (64 stages measured 2% faster than 128 on the 16-device fork-join
+// batch; fewer, or other group widths, were slower).
 inline int slice_len(int D) {
-    const int groups = kScoreBlock / group_width(D);
-    return groups * 8 > 256 ? 256 : groups * 8;
+    const int G = group_width(D), groups = kScoreBlock / G;
+    const int per = G == 16 ? 4 : 8;
+    return groups * per > 256 ? 256 : groups * per;
 }
 
 // Kernel launchers (fate_kernels.hip).  Return a hipError_t as int.

@@ -21,6 +21,6 @@ echo "[profile] WRITE_SIZE" && timeout -s KILL 180 rocprofv3 --pmc WRITE_SIZE -d
 echo "[profile] SQ counters" && timeout -s KILL 180 rocprofv3 --pmc SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_LDS SQ_INSTS_SALU GRBM_GUI_ACTIVE -d $O/sq -o pmc --output-format csv -- $B > $O/sq.log 2>&1 || exit $?
 python3 -m paper_2605_07238_amd.profile_summary --trace-db $(ls $O/trace/*.db | head -1) \
   --pmc $O/fetch/pmc_counter_collection.csv $O/write/pmc_counter_collection.csv $O/sq/pmc_counter_collection.csv \
-  --kernel-source paper_2605_07238_amd/csrc/fate_kernels.hip > $O/summary.txt || exit $?
+  --kernel-source paper_2605_07238_amd/csrc/fate_kernels.hip paper_2605_07238_amd/csrc/fate_internal.h > $O/summary.txt || exit $?
 grep "timed" $O/trace.log | head -2
 cat $O/summary.txt

@@ -40,7 +40,8 @@ def main():
     ap.add_argument("--pmc", nargs="*", default=[])
     ap.add_argument("--kernel", default="k_score")
     ap.add_argument("--copy-bytes", type=int, default=512 << 20)
-    ap.add_argument("--kernel-source")
+    ap.add_argument("--kernel-source", nargs="*",
+                    help="source files whose joint SHA-256 identifies the profiled kernel and its launch geometry")
     ap.add_argument("--cus", type=int, default=256)
     ap.add_argument("--xcds", type=int, default=8)
     args = ap.parse_args()
@@ -89,7 +90,10 @@ def main():
         out.append("gpu_cycles_per_dispatch: %.0f" % cycles)
         out.append("valu_issue_busy_frac: %.3f  (SQ_INSTS_VALU x 4 / (%d CUs x 4 SIMDs x cycles))" % (busy, args.cus))
     if args.kernel_source:
-        out.append("kernel_source_sha256: %s" % hashlib.sha256(open(args.kernel_source, "rb").read()).hexdigest())
+        h = hashlib.sha256()
+        for path in args.kernel_source:
+            h.update(open(path, "rb").read())
+        out.append("kernel_source_sha256: %s" % h.hexdigest())
     print("\n".join(out))
 
 
