@@ -388,8 +388,8 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// One completed parent's contribution on device d: its output is local
-// (colocation count) or has to be transferred from the cheapest holder.
+// Order-preserving 32-bit image of a score (a larger score, a larger value;
+// -0 and +0 alike), and its inverse.
 __device__ __forceinline__ uint32_t order_bits(float x) {
     const uint32_t u = __float_as_uint(x + 0.0f);  // -0 -> +0
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
@@ -485,6 +485,8 @@ __device__ __forceinline__ void rank_stages(const float *scores, const uint32_t 
     }
 }
 
+// One completed parent's contribution on device d: its output is local
+// (colocation count) or has to be transferred from the cheapest holder.
 template <bool UNI>
 __device__ __forceinline__ void add_parent(const ScoreLaunch &a, uint64_t hu, float su, int d, float &tr, float &cnt) {
     const bool local = bit(hu, d);
@@ -856,7 +858,8 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
                 const int nb = stage_rows(base);
                 float f0 = 0.0f, f1 = 0.0f, f2 = 0.0f, f3 = 0.0f;
-                for (int jj = 0; jj < nb; ++jj) {  // uniform
+                // staged row jj: the key outside S, the value inside S, and gamma^depth
+                auto row = [&](int jj, int &key, float &inval, float &gh) {
                     const EntryS *E = areaS + jj;
                     const uint4 q0 = *reinterpret_cast<const uint4 *>(E);
                     const float4 q1 = *reinterpret_cast<const float4 *>(&E->gh);
@@ -884,12 +887,14 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     const float Braw = X + (in_old ? res_cost : sw) - (pf_old ? q1.z : 0.0f);
                     const float Bnew = X + (in_new ? res_cost : sw) - (pf_new ? q1.z : 0.0f) + q1.w;
                     const bool child = __float_as_int(q1.w) < 0;
-                    const float inval = fw ? Bnew : inf_f();
+                    inval = fw ? Bnew : inf_f();
                     // outside S: a child also receives v's output there
-                    const int key = fw ? fkey(Braw + (child ? t0 : 0.0f)) : kKeyInf;
-                    const int P = kscan_up16(key), Q = kscan_down16(key);
-                    const int Pl = kshift_in<0x111>(P);  // prefix up to lane-1; +inf at lane 0
-                    const float gh = q1.x;
+                    key = fw ? fkey(Braw + (child ? t0 : 0.0f)) : kKeyInf;
+                    gh = q1.x;
+                };
+                // one row's terms: outside S from the prefix / suffix scans, inside S
+                // from the window minimum, each weighted by gamma^depth
+                auto accumulate = [&](int Pl, int Q, float inval, float gh) {
                     f0 += gh * fminf(unkey(kmin_from<0x101>(Pl, Q)), inval);
                     if (nk >= 1) {  // uniform
                         float inside = fminf(inval, dpp_b0<0x101>(inval));
@@ -903,6 +908,42 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                             }
                         }
                     }
+                };
+                int jj = 0;
+                // the wave's lane groups score different stages: the loop without
+                // window terms only when none of them has windows, so that the
+                // wave never runs both loops
+                if (__ballot(nk != 0) == 0ull) {
+                    for (; jj + 1 < nb; jj += 2) {  // two rows at a time, so their scans interleave
+                        int k0, k1;
+                        float v0, v1, g0, g1;
+                        row(jj, k0, v0, g0);
+                        row(jj + 1, k1, v1, g1);
+                        const int P0 = kscan_up16(k0), P1 = kscan_up16(k1);
+                        const int Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
+                        const int L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);  // prefix up to lane-1
+                        f0 += g0 * fminf(unkey(kmin_from<0x101>(L0, Q0)), v0);
+                        f0 += g1 * fminf(unkey(kmin_from<0x101>(L1, Q1)), v1);
+                    }
+                } else {
+                    for (; jj + 1 < nb; jj += 2) {
+                        int k0, k1;
+                        float v0, v1, g0, g1;
+                        row(jj, k0, v0, g0);
+                        row(jj + 1, k1, v1, g1);
+                        const int P0 = kscan_up16(k0), P1 = kscan_up16(k1);
+                        const int Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
+                        const int L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);
+                        accumulate(L0, Q0, v0, g0);
+                        accumulate(L1, Q1, v1, g1);
+                    }
+                }
+                if (jj < nb) {  // uniform: the odd row
+                    int key;
+                    float inval, gh;
+                    row(jj, key, inval, gh);
+                    const int P = kscan_up16(key), Q = kscan_down16(key);
+                    accumulate(kshift_in<0x111>(P), Q, inval, gh);
                 }
                 acc0 += (double)f0;
                 w_acc[0] += (double)f1;
