@@ -914,6 +914,23 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 // window terms only when none of them has windows, so that the
                 // wave never runs both loops
                 if (__ballot(nk != 0) == 0ull) {
+                    for (; jj + 3 < nb; jj += 4) {  // four rows at a time, so their scans interleave
+                        int k0, k1, k2, k3;
+                        float v0, v1, v2, v3, g0, g1, g2, g3;
+                        row(jj, k0, v0, g0);
+                        row(jj + 1, k1, v1, g1);
+                        row(jj + 2, k2, v2, g2);
+                        row(jj + 3, k3, v3, g3);
+                        const int P0 = kscan_up16(k0), P1 = kscan_up16(k1), P2 = kscan_up16(k2), P3 = kscan_up16(k3);
+                        const int Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
+                        const int Q2 = kscan_down16(k2), Q3 = kscan_down16(k3);
+                        const int L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);
+                        const int L2 = kshift_in<0x111>(P2), L3 = kshift_in<0x111>(P3);
+                        f0 += g0 * fminf(unkey(kmin_from<0x101>(L0, Q0)), v0);
+                        f0 += g1 * fminf(unkey(kmin_from<0x101>(L1, Q1)), v1);
+                        f0 += g2 * fminf(unkey(kmin_from<0x101>(L2, Q2)), v2);
+                        f0 += g3 * fminf(unkey(kmin_from<0x101>(L3, Q3)), v3);
+                    }
                     for (; jj + 1 < nb; jj += 2) {  // two rows at a time, so their scans interleave
                         int k0, k1;
                         float v0, v1, g0, g1;
