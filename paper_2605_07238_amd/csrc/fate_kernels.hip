@@ -113,14 +113,15 @@ static_assert(sizeof(EntryL<uint64_t>) == 80, "EntryL<u64>");
 // masks fit in 16 bits; at most 32 models): four 16-byte words, read with
 // wide LDS loads.  The parent words are read only when w has completed parents.
 struct alignas(16) EntryS {
-    uint32_t moff;  // m(w) * D: column of w's model in the exec / switch tables
+    uint32_t moff;  // m(w) * D: row of w's model in the block's cost table
     uint32_t m1;    // devices feasible for w | devices caching grp(w) << 16
-    uint32_t m2;    // devices caching grp(w) once v runs there | holders of parent 2 << 16
+    uint32_t m2;    // devices that gain grp(w) once v runs there | holders of parent 2 << 16
     uint32_t mdn;   // m(w) | completed parents << 8
     float gh;       // gamma^depth
-    float xbase;    // lam_tr * beta0 * sum of completed parents' sizes (every parent remote)
+    float xk;       // xbase + (child of v ? v's output to one more device : 0), where xbase =
+                    // lam_tr * beta0 * sum of completed parents' sizes (every parent remote)
+    float xn;       // xbase - (child of v ? lam_c / |Pa(w)| : 0)
     float pfp;      // lam_p * kappa_prefix * L(w)
-    float ccw;      // -lam_c / |Pa(w)| for a child of v (sign bit = child), else +0
     uint32_t dbeg;  // first completed parent
     uint32_t ph01;  // holders of parent 0 | holders of parent 1 << 16
     float pw0;      // what a device holding parent q saves: its transfer plus lam_c / |Pa(w)|
@@ -195,7 +196,8 @@ __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int 
     q.wait = o; o += 4 * (uint32_t)D;
     q.gpow = o; o += 4 * 16;
     q.next = o; o += 16;
-    q.exec = o; o += 4 * (uint32_t)(M * D);
+    o = (o + 15u) & ~15u;
+    q.exec = o; o += 4 * (uint32_t)(M * D);  // with ksw: the slot layout's [M][D] float2 cost table
     q.ksw = o; o += 4 * (uint32_t)(M * D);
     q.total = (o + 15u) & ~15u;
     return q;
@@ -243,45 +245,52 @@ __device__ __forceinline__ float dpp_move(float old, float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-// Order-preserving float <-> int32 map (an involution): the signed order of
-// the keys is the order of the floats (no NaNs); +inf maps to 0x7f800000.
-__device__ __forceinline__ int fkey(float x) {
-    const int b = __float_as_int(x);
-    return b ^ (int)((uint32_t)(b >> 31) >> 1);
+// Order-reversing float <-> uint32 map (an involution; no NaNs): the larger
+// the float, the smaller its key, so a minimum of floats is a maximum of
+// keys.  +inf maps to 0x007fffff; key 0 lies below every float's key, so it
+// is the identity of the maximum and stands for "no lane": a DPP move with
+// bound_ctrl reads 0 where its source lane is outside the row, and the move
+// folds into one v_max_u32 with no copy of the destination.
+// The map is b ^ (~(b >> 31) & 0x7fffffff): one shift, then one three-input
+// bitwise instruction (truth table A ^ (~B & C) = 0xD2 with A, B, C the
+// tables 0xF0, 0xCC, 0xAA), written out because the compiler would turn the
+// shifted sign into a compare and select.
+__device__ __forceinline__ uint32_t key_map(int b) {
+    return __builtin_amdgcn_bitop3_b32((uint32_t)b, (uint32_t)(b >> 31), 0x7fffffffu, 0xD2);
 }
-__device__ __forceinline__ float unkey(int k) { return __int_as_float(k ^ (int)((uint32_t)(k >> 31) >> 1)); }
+__device__ __forceinline__ uint32_t fkey(float x) { return key_map(__float_as_int(x)); }
+__device__ __forceinline__ float unkey(uint32_t k) { return __uint_as_float(key_map((int)k)); }
 
-constexpr int kKeyInf = 0x7f800000;  // key of +inf
-constexpr int kKeyId = 0x7fffffff;   // identity of the key minimum
+constexpr uint32_t kKeyInf = 0x007fffffu;  // key of +inf
 
-// min(x, x of the lane CTRL names); a lane without a source keeps x.  With
-// the identity as the DPP "old" value the move folds into one v_min_i32.
+// max(x, x of the lane CTRL names); a lane without a source keeps x.
 template <int CTRL>
-__device__ __forceinline__ int kmin_dpp(int x) {
-    return min(x, __builtin_amdgcn_update_dpp(kKeyId, x, CTRL, 0xF, 0xF, false));
+__device__ __forceinline__ uint32_t kmax_dpp(uint32_t x) {
+    return max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true));
 }
-// min(a, x of the lane CTRL names); a lane without a source gets a.
+// max(a, x of the lane CTRL names); a lane without a source gets a.
 template <int CTRL>
-__device__ __forceinline__ int kmin_from(int a, int x) {
-    return min(a, __builtin_amdgcn_update_dpp(kKeyId, x, CTRL, 0xF, 0xF, false));
+__device__ __forceinline__ uint32_t kmax_from(uint32_t a, uint32_t x) {
+    return max(a, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true));
 }
-// x of the lane CTRL names; the key of +inf where there is none.
+// x of the lane CTRL names; 0 ("no lane") where there is none.
 template <int CTRL>
-__device__ __forceinline__ int kshift_in(int x) {
-    return __builtin_amdgcn_update_dpp(kKeyInf, x, CTRL, 0xF, 0xF, false);
+__device__ __forceinline__ uint32_t kshift_in(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true);
 }
-// Inclusive prefix / suffix minimum of keys over a 16-lane DPP row.
-__device__ __forceinline__ int kscan_up16(int x) {
-    x = kmin_dpp<0x111>(x);
-    x = kmin_dpp<0x112>(x);
-    x = kmin_dpp<0x114>(x);
-    return kmin_dpp<0x118>(x);
+// Inclusive prefix / suffix maximum of keys (minimum of the floats) over a
+// 16-lane DPP row.
+__device__ __forceinline__ uint32_t kscan_up16(uint32_t x) {
+    x = kmax_dpp<0x111>(x);
+    x = kmax_dpp<0x112>(x);
+    x = kmax_dpp<0x114>(x);
+    return kmax_dpp<0x118>(x);
 }
-__device__ __forceinline__ int kscan_down16(int x) {
-    x = kmin_dpp<0x101>(x);
-    x = kmin_dpp<0x102>(x);
-    x = kmin_dpp<0x104>(x);
-    return kmin_dpp<0x108>(x);
+__device__ __forceinline__ uint32_t kscan_down16(uint32_t x) {
+    x = kmax_dpp<0x101>(x);
+    x = kmax_dpp<0x102>(x);
+    x = kmax_dpp<0x104>(x);
+    return kmax_dpp<0x108>(x);
 }
 // x of the lane CTRL names, 0 where there is none: only for lanes whose
 // result is discarded (lets a following min/max fold the move).
@@ -567,7 +576,21 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         for (int h = 0; h < 16; ++h) { L.gpow[h] = g; g *= ps.gamma; }
         *L.next = 0u;
     }
-    for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = ps.lam_s * a.ksw[i]; }
+    if constexpr (SLOTS) {
+        // per (model m, device d) under the instance's residency: the cost of
+        // running m there, switch included, and the switch cost's magnitude
+        // (what the switch term changes by when m's residency on d flips)
+        const float res = VAR ? -ps.lam_m : 0.0f;
+        float2 *tab = reinterpret_cast<float2 *>(L.exec);
+        for (int i = tid; i < M * D; i += kBlock) {
+            const int m = i / D, d = i - m * D;
+            const float ks = ps.lam_s * a.ksw[i];
+            const bool in_old = bit(a.resident[(int64_t)b * D + d], m);
+            tab[i] = make_float2(a.exec[i] + (in_old ? res : ks), ks - res);
+        }
+    } else {
+        for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = ps.lam_s * a.ksw[i]; }
+    }
     for (int i = tid; i < P; i += kBlock) {
         uint64_t key = ~0ull;
         if (i < nF) {
@@ -669,8 +692,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             add_parent<UNI>(a, pu.holders, pu.sigma, dl, tr, cnt);
         }
         const bool feas_v = live && bit(sv.elig, lane) && bit(L.fits[mv], lane);
-        const float c_v = L.exec[mv * D + dl];
-        const float sw_v = bit(rho, mv) ? res_cost : L.ksw[mv * D + dl];
+        // (the slot layout keeps a combined table in LDS and reads these two from HBM)
+        const float c_v = kSlots ? a.exec[mv * D + dl] : L.exec[mv * D + dl];
+        const float sw_v = bit(rho, mv) ? res_cost : (kSlots ? ps.lam_s * a.ksw[mv * D + dl] : L.ksw[mv * D + dl]);
         const float colo_v = sv.npar ? cnt / (float)sv.npar : 0.0f;
         const float pf_v = hv_cached ? ps.kpf * sv.tokens : 0.0f;
         const float a_imm = ps.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
@@ -795,7 +819,13 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             // ---- horizon rows, G at a time: lane j stages row j (EntryS)
             EntryS *areaS = reinterpret_cast<EntryS *>(static_cast<uint8_t *>(L.entries) + (tid / G) * kSlotGroupBytes);
             const uint32_t rho32 = (uint32_t)rho, rhon32 = (uint32_t)rho_new;
-            const uint32_t bit_lo = (uint32_t)mybit, bit_hi = bit_lo << 16;
+            const uint32_t chg32 = rho32 ^ rhon32, ld32 = rhon32 & ~rho32;  // models whose residency v's placement flips / loads
+            const uint32_t bit_lo = (uint32_t)mybit, dlane = (uint32_t)lane;
+            const float2 *tab_col = reinterpret_cast<const float2 *>(L.exec) + dl;
+            // x where bit `pos` of m is set, else +0
+            auto bit_sel = [](uint32_t m, uint32_t pos, float x) {
+                return __uint_as_float(__float_as_uint(x) & (uint32_t)__builtin_amdgcn_sbfe((int)m, pos, 1u));
+            };
             auto stage_rows = [&](uint32_t base) -> int {
                 const uint32_t e = base + lane;
                 bool valid = e < sv.e1;
@@ -827,15 +857,16 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                         }
                     }
                     EntryS S;
+                    const bool child = VAR ? child_of(a, rw, depth, sv.v) : depth == 1;
                     S.moff = (uint32_t)rw.model * (uint32_t)D;
                     S.m1 = feas | (pfo << 16);
                     // once v runs on a device, that device also caches grp(v)
-                    S.m2 = (same ? 0xffffu : pfo) | (ph[2] << 16);
+                    S.m2 = (same ? (~pfo & 0xffffu) : 0u) | (ph[2] << 16);
                     S.mdn = (uint32_t)rw.model | (dn << 8);
                     S.gh = mean_levels ? L.gpow[depth] * a.desc_w[e] : L.gpow[depth];
-                    S.xbase = base_tr;
+                    S.xk = base_tr + (child ? t0 : 0.0f);
+                    S.xn = base_tr + (child ? -cw : 0.0f);
                     S.pfp = lam_p * ps.kpf * rw.tokens;
-                    S.ccw = (VAR ? child_of(a, rw, depth, sv.v) : depth == 1) ? -cw : 0.0f;
                     S.dbeg = db;
                     S.ph01 = ph[0] | (ph[1] << 16);
                     S.pw0 = pw[0];
@@ -849,7 +880,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 return nb;
             };
 
-            // ---- horizon rows.  Outside S the row is scanned as order-preserving
+            // ---- horizon rows.  Outside S the row is scanned as order-reversing
             // integer keys (prefix and suffix minima, one DPP op per step); the
             // minimum outside a window {i..i+k-1} is min(prefix(i-1), suffix(i+k)).
             // Inside S the window minimum of the post-state values slides by one
@@ -858,53 +889,53 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
                 const int nb = stage_rows(base);
                 float f0 = 0.0f, f1 = 0.0f, f2 = 0.0f, f3 = 0.0f;
-                // staged row jj: the key outside S, the value inside S, and gamma^depth
-                auto row = [&](int jj, int &key, float &inval, float &gh) {
+                // staged row jj: the key outside S, the value inside S, and gamma^depth.
+                // Branch-free: a bit of a device mask selects a value by masking its bits.
+                auto row = [&](int jj, uint32_t &key, float &inval, float &gh) {
                     const EntryS *E = areaS + jj;
                     const uint4 q0 = *reinterpret_cast<const uint4 *>(E);
                     const float4 q1 = *reinterpret_cast<const float4 *>(&E->gh);
-                    // q0: moff, m1, m2, mdn; q1: gh, xbase, pfp, ccw
-                    const float ex = exec_col[q0.x];
-                    const float sw = ksw_col[q0.x];
-                    float X = ex + q1.y;  // every completed parent remote
+                    // q0: moff, m1, m2, mdn; q1: gh, xk, xn, pfp
+                    const float2 t = tab_col[q0.x];  // cost with the old switch term, switch magnitude
+                    float X = t.x;  // every completed parent remote (its transfer is in xk / xn)
                     if (q0.w > 255u) {  // completed parents: holding one's output saves its transfer and adds colocation
                         const uint4 q2 = *reinterpret_cast<const uint4 *>(&E->dbeg);
-                        const float4 q3 = *reinterpret_cast<const float4 *>(&E->pw1);
-                        X -= (q2.y & bit_lo) ? __uint_as_float(q2.z) : 0.0f;
-                        X -= (q2.y & bit_hi) ? q3.x : 0.0f;
-                        X -= (q0.z & bit_hi) ? q3.y : 0.0f;
+                        const float4 q3 = *reinterpret_cast<const float4 *>(&E->pw2);
+                        X -= bit_sel(q2.y, dlane, __uint_as_float(q2.z));
+                        X -= bit_sel(q2.y, dlane + 16u, __uint_as_float(q2.w));
+                        X -= bit_sel(q0.z, dlane + 16u, q3.x);
                         const uint32_t dn = q0.w >> 8;
                         for (uint32_t q = kCap; q < dn; ++q) {  // rare: more completed parents than staged
                             const DoneParent pu = a.done[q2.x + q];
-                            X -= ((uint32_t)pu.holders & bit_lo) ? lam_tr * a.beta0 * pu.sigma + q3.z : 0.0f;
+                            X -= ((uint32_t)pu.holders & bit_lo) ? lam_tr * a.beta0 * pu.sigma + q3.y : 0.0f;
                         }
                     }
-                    const bool in_old = ((rho32 >> (q0.w & 31u)) & 1u) != 0;
-                    const bool in_new = ((rhon32 >> (q0.w & 31u)) & 1u) != 0;
-                    const bool fw = (q0.y & bit_lo) != 0;
-                    const bool pf_old = (q0.y & bit_hi) != 0;
-                    const bool pf_new = (q0.z & bit_lo) != 0;
-                    const float Braw = X + (in_old ? res_cost : sw) - (pf_old ? q1.z : 0.0f);
-                    const float Bnew = X + (in_new ? res_cost : sw) - (pf_new ? q1.z : 0.0f) + q1.w;
-                    const bool child = __float_as_int(q1.w) < 0;
-                    inval = fw ? Bnew : inf_f();
-                    // outside S: a child also receives v's output there
-                    key = fw ? fkey(Braw + (child ? t0 : 0.0f)) : kKeyInf;
+                    X -= bit_sel(q0.y, dlane + 16u, q1.w);  // grp(w) already cached on this device
+                    // v's placement flips m(w)'s residency here: loaded (switch term drops by the
+                    // magnitude) or evicted (rises by it); the sign bit comes from the load bit
+                    const uint32_t mw = q0.w;  // the bit-field offset uses bits 4:0, m(w)
+                    const float dsw = __uint_as_float((__builtin_amdgcn_ubfe(ld32, mw, 1u) << 31) +
+                                                      (__float_as_uint(t.y) & (uint32_t)__builtin_amdgcn_sbfe((int)chg32, mw, 1u)));
+                    const float Bnew = X + q1.z + dsw - bit_sel(q0.z, dlane, q1.w);
+                    const uint32_t fm = (uint32_t)__builtin_amdgcn_sbfe((int)q0.y, dlane, 1u);  // w feasible here
+                    // outside S: a child also receives v's output here (in xk)
+                    key = (fm & fkey(X + q1.y)) | (~fm & kKeyInf);
+                    inval = __uint_as_float((fm & __float_as_uint(Bnew)) | (~fm & __float_as_uint(inf_f())));
                     gh = q1.x;
                 };
                 // one row's terms: outside S from the prefix / suffix scans, inside S
                 // from the window minimum, each weighted by gamma^depth
-                auto accumulate = [&](int Pl, int Q, float inval, float gh) {
-                    f0 += gh * fminf(unkey(kmin_from<0x101>(Pl, Q)), inval);
+                auto accumulate = [&](uint32_t Pl, uint32_t Q, float inval, float gh) {
+                    f0 += gh * fminf(unkey(kmax_from<0x101>(Pl, Q)), inval);
                     if (nk >= 1) {  // uniform
                         float inside = fminf(inval, dpp_b0<0x101>(inval));
-                        f1 += gh * fminf(unkey(kmin_from<0x102>(Pl, Q)), inside);
+                        f1 += gh * fminf(unkey(kmax_from<0x102>(Pl, Q)), inside);
                         if (nk >= 2) {
                             inside = fminf(inside, dpp_b0<0x101>(inside));
-                            f2 += gh * fminf(unkey(kmin_from<0x103>(Pl, Q)), inside);
+                            f2 += gh * fminf(unkey(kmax_from<0x103>(Pl, Q)), inside);
                             if (nk >= 3) {
                                 inside = fminf(inside, dpp_b0<0x101>(inside));
-                                f3 += gh * fminf(unkey(kmin_from<0x104>(Pl, Q)), inside);
+                                f3 += gh * fminf(unkey(kmax_from<0x104>(Pl, Q)), inside);
                             }
                         }
                     }
@@ -914,52 +945,35 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 // window terms only when none of them has windows, so that the
                 // wave never runs both loops
                 if (__ballot(nk != 0) == 0ull) {
-                    for (; jj + 3 < nb; jj += 4) {  // four rows at a time, so their scans interleave
-                        int k0, k1, k2, k3;
-                        float v0, v1, v2, v3, g0, g1, g2, g3;
-                        row(jj, k0, v0, g0);
-                        row(jj + 1, k1, v1, g1);
-                        row(jj + 2, k2, v2, g2);
-                        row(jj + 3, k3, v3, g3);
-                        const int P0 = kscan_up16(k0), P1 = kscan_up16(k1), P2 = kscan_up16(k2), P3 = kscan_up16(k3);
-                        const int Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
-                        const int Q2 = kscan_down16(k2), Q3 = kscan_down16(k3);
-                        const int L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);
-                        const int L2 = kshift_in<0x111>(P2), L3 = kshift_in<0x111>(P3);
-                        f0 += g0 * fminf(unkey(kmin_from<0x101>(L0, Q0)), v0);
-                        f0 += g1 * fminf(unkey(kmin_from<0x101>(L1, Q1)), v1);
-                        f0 += g2 * fminf(unkey(kmin_from<0x101>(L2, Q2)), v2);
-                        f0 += g3 * fminf(unkey(kmin_from<0x101>(L3, Q3)), v3);
-                    }
                     for (; jj + 1 < nb; jj += 2) {  // two rows at a time, so their scans interleave
-                        int k0, k1;
+                        uint32_t k0, k1;
                         float v0, v1, g0, g1;
                         row(jj, k0, v0, g0);
                         row(jj + 1, k1, v1, g1);
-                        const int P0 = kscan_up16(k0), P1 = kscan_up16(k1);
-                        const int Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
-                        const int L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);  // prefix up to lane-1
-                        f0 += g0 * fminf(unkey(kmin_from<0x101>(L0, Q0)), v0);
-                        f0 += g1 * fminf(unkey(kmin_from<0x101>(L1, Q1)), v1);
+                        const uint32_t P0 = kscan_up16(k0), P1 = kscan_up16(k1);
+                        const uint32_t Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
+                        const uint32_t L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);  // prefix up to lane-1
+                        f0 += g0 * fminf(unkey(kmax_from<0x101>(L0, Q0)), v0);
+                        f0 += g1 * fminf(unkey(kmax_from<0x101>(L1, Q1)), v1);
                     }
                 } else {
                     for (; jj + 1 < nb; jj += 2) {
-                        int k0, k1;
+                        uint32_t k0, k1;
                         float v0, v1, g0, g1;
                         row(jj, k0, v0, g0);
                         row(jj + 1, k1, v1, g1);
-                        const int P0 = kscan_up16(k0), P1 = kscan_up16(k1);
-                        const int Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
-                        const int L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);
+                        const uint32_t P0 = kscan_up16(k0), P1 = kscan_up16(k1);
+                        const uint32_t Q0 = kscan_down16(k0), Q1 = kscan_down16(k1);
+                        const uint32_t L0 = kshift_in<0x111>(P0), L1 = kshift_in<0x111>(P1);
                         accumulate(L0, Q0, v0, g0);
                         accumulate(L1, Q1, v1, g1);
                     }
                 }
                 if (jj < nb) {  // uniform: the odd row
-                    int key;
+                    uint32_t key;
                     float inval, gh;
                     row(jj, key, inval, gh);
-                    const int P = kscan_up16(key), Q = kscan_down16(key);
+                    const uint32_t P = kscan_up16(key), Q = kscan_down16(key);
                     accumulate(kshift_in<0x111>(P), Q, inval, gh);
                 }
                 acc0 += (double)f0;
