@@ -170,12 +170,20 @@ __host__ __device__ inline int pow2_at_least(int x) {
     return p;
 }
 
+// Slot layout: per (model m, device d) under the instance's residency, the
+// cost of running m on d with the switch term included, the switch term's
+// magnitude (what it changes by when m's residency on d flips), and the
+// execution and switch terms themselves.
+struct alignas(16) CostS {
+    float sw0, ksr, exec, swo;
+};
+
 // Byte offsets of every LDS array (shared by the launcher and the kernel).
 struct LdsPlan {
     uint32_t pkey, pmask, rm, rho, fits, wt, cap, order, wait, gpow, next, exec, ksw, stages, entries, total;
 };
 
-__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int staging) {
+__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int staging, bool slots) {
     LdsPlan q;
     const uint32_t T = 1u << table_log2(D, K);
     const uint32_t mask_bytes = D <= 32 ? 4u : 8u;
@@ -197,8 +205,13 @@ __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int 
     q.gpow = o; o += 4 * 16;
     q.next = o; o += 16;
     o = (o + 15u) & ~15u;
-    q.exec = o; o += 4 * (uint32_t)(M * D);  // with ksw: the slot layout's [M][D] float2 cost table
-    q.ksw = o; o += 4 * (uint32_t)(M * D);
+    if (slots) {  // [M][D] CostS table, then [M][D] residency after each load
+        q.exec = o; o += (uint32_t)sizeof(CostS) * (uint32_t)(M * D);
+        q.ksw = o; o += 4 * (uint32_t)(M * D);
+    } else {  // [M][D] execution times and weighted switch times
+        q.exec = o; o += 4 * (uint32_t)(M * D);
+        q.ksw = o; o += 4 * (uint32_t)(M * D);
+    }
     q.total = (o + 15u) & ~15u;
     return q;
 }
@@ -541,7 +554,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     // slot layout: 16-lane groups, uniform beta, at most 32 models (chosen by the launcher)
     constexpr bool kSlots = SLOTS;
     using Entry = EntryL<Mask>;
-    const LdsPlan plan = lds_plan(D, K, M, a.slice, staging_bytes<G>());
+    const LdsPlan plan = lds_plan(D, K, M, a.slice, staging_bytes<G>(), SLOTS);
 
     Lds L;
     L.logT = table_log2(D, K);
@@ -577,16 +590,22 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         *L.next = 0u;
     }
     if constexpr (SLOTS) {
-        // per (model m, device d) under the instance's residency: the cost of
-        // running m there, switch included, and the switch cost's magnitude
-        // (what the switch term changes by when m's residency on d flips)
+        // cost table and the residency after loading m on d (at most 32 models)
         const float res = VAR ? -ps.lam_m : 0.0f;
-        float2 *tab = reinterpret_cast<float2 *>(L.exec);
+        CostS *tab = reinterpret_cast<CostS *>(L.exec);
+        uint32_t *rnew = reinterpret_cast<uint32_t *>(L.ksw);
         for (int i = tid; i < M * D; i += kBlock) {
             const int m = i / D, d = i - m * D;
             const float ks = ps.lam_s * a.ksw[i];
-            const bool in_old = bit(a.resident[(int64_t)b * D + d], m);
-            tab[i] = make_float2(a.exec[i] + (in_old ? res : ks), ks - res);
+            const uint64_t rd = a.resident[(int64_t)b * D + d];
+            const float swo = bit(rd, m) ? res : ks;
+            CostS c;
+            c.sw0 = a.exec[i] + swo;
+            c.ksr = ks - res;
+            c.exec = a.exec[i];
+            c.swo = swo;
+            tab[i] = c;
+            rnew[i] = (uint32_t)load_model(rd, m, a.cap[d], a.weight);
         }
     } else {
         for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = ps.lam_s * a.ksw[i]; }
@@ -692,14 +711,15 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             add_parent<UNI>(a, pu.holders, pu.sigma, dl, tr, cnt);
         }
         const bool feas_v = live && bit(sv.elig, lane) && bit(L.fits[mv], lane);
-        // (the slot layout keeps a combined table in LDS and reads these two from HBM)
-        const float c_v = kSlots ? a.exec[mv * D + dl] : L.exec[mv * D + dl];
-        const float sw_v = bit(rho, mv) ? res_cost : (kSlots ? ps.lam_s * a.ksw[mv * D + dl] : L.ksw[mv * D + dl]);
+        const float c_v = kSlots ? reinterpret_cast<const CostS *>(L.exec)[mv * D + dl].exec : L.exec[mv * D + dl];
+        const float sw_v = kSlots ? reinterpret_cast<const CostS *>(L.exec)[mv * D + dl].swo
+                                  : (bit(rho, mv) ? res_cost : L.ksw[mv * D + dl]);
         const float colo_v = sv.npar ? cnt / (float)sv.npar : 0.0f;
         const float pf_v = hv_cached ? ps.kpf * sv.tokens : 0.0f;
         const float a_imm = ps.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
         const float b_imm = c_v + lam_tr * tr - lam_p * pf_v;
-        const uint64_t rho_new = load_model(rho, mv, L.cap[dl], L.wt);
+        const uint64_t rho_new = kSlots ? (uint64_t)reinterpret_cast<const uint32_t *>(L.ksw)[mv * D + dl]
+                                        : load_model(rho, mv, L.cap[dl], L.wt);
         const bool prefix_added = sv.hash != 0 && !hv_cached;
         const uint64_t feas_mask = (__ballot(feas_v) >> gbase) & gmask;
 
@@ -821,7 +841,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             const uint32_t rho32 = (uint32_t)rho, rhon32 = (uint32_t)rho_new;
             const uint32_t chg32 = rho32 ^ rhon32, ld32 = rhon32 & ~rho32;  // models whose residency v's placement flips / loads
             const uint32_t bit_lo = (uint32_t)mybit, dlane = (uint32_t)lane;
-            const float2 *tab_col = reinterpret_cast<const float2 *>(L.exec) + dl;
+            const CostS *tab_col = reinterpret_cast<const CostS *>(L.exec) + dl;
             // x where bit `pos` of m is set, else +0
             auto bit_sel = [](uint32_t m, uint32_t pos, float x) {
                 return __uint_as_float(__float_as_uint(x) & (uint32_t)__builtin_amdgcn_sbfe((int)m, pos, 1u));
@@ -896,7 +916,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     const uint4 q0 = *reinterpret_cast<const uint4 *>(E);
                     const float4 q1 = *reinterpret_cast<const float4 *>(&E->gh);
                     // q0: moff, m1, m2, mdn; q1: gh, xk, xn, pfp
-                    const float2 t = tab_col[q0.x];  // cost with the old switch term, switch magnitude
+                    const float2 t = *reinterpret_cast<const float2 *>(&tab_col[q0.x]);  // cost with the old switch term, switch magnitude
                     float X = t.x;  // every completed parent remote (its transfer is in xk / xn)
                     if (q0.w > 255u) {  // completed parents: holding one's output saves its transfer and adds colocation
                         const uint4 q2 = *reinterpret_cast<const uint4 *>(&E->dbeg);
@@ -1181,7 +1201,8 @@ template <bool UNI>
 static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int G = group_width(a.D);
     const int sb = G == 16 ? staging_bytes<16>() : G <= 32 ? staging_bytes<8>() : staging_bytes<64>();
-    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb).total;
+    const bool slots = UNI && G == 16 && a.M <= 32;  // the kernel choice below
+    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb, slots).total;
     const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block(kBlock);
     bool var = a.topo != 0;
     for (int p = 0; p < a.nsets; ++p) var = var || a.ps[p].lam_m != 0.0f || a.ps[p].flags != 0;
