@@ -706,9 +706,32 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
 
         // ---- immediate terms of v on device `lane` and the post-state there
         float tr = 0.0f, cnt = 0.0f;
-        for (int q = 0; q < sv.dn; ++q) {  // uniform trip count
-            const DoneParent pu = a.done[sv.dbeg + q];
-            add_parent<UNI>(a, pu.holders, pu.sigma, dl, tr, cnt);
+        if constexpr (kSlots) {  // lane j loads completed parent j: one round trip per 16 parents
+            for (int q0 = 0; q0 < (int)sv.dn; q0 += 16) {  // uniform within the group
+                uint32_t h = 0u;
+                float sg = 0.0f;
+                if (q0 + lane < (int)sv.dn) {
+                    const DoneParent pu = a.done[sv.dbeg + q0 + lane];
+                    h = (uint32_t)pu.holders;  // at most 16 devices
+                    sg = pu.sigma;
+                }
+                // each parent in turn goes to the whole row, in parent order
+                const int n = min(16, (int)sv.dn - q0);
+                for (int j = 0; j < n; ++j) {  // uniform within the group
+                    const uint32_t hj = j == 0 ? (uint32_t)__builtin_amdgcn_update_dpp(0, (int)h, 0x150, 0xF, 0xF, false)  // row_newbcast:0
+                                               : (uint32_t)__shfl((int)h, j, 16);
+                    const float sj = j == 0 ? __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sg), 0x150, 0xF, 0xF, false))
+                                            : __shfl(sg, j, 16);
+                    const bool local = ((hj >> dl) & 1u) != 0;
+                    cnt += local ? 1.0f : 0.0f;
+                    tr += local ? 0.0f : sj * a.beta0;
+                }
+            }
+        } else {
+            for (int q = 0; q < sv.dn; ++q) {  // uniform trip count
+                const DoneParent pu = a.done[sv.dbeg + q];
+                add_parent<UNI>(a, pu.holders, pu.sigma, dl, tr, cnt);
+            }
         }
         const bool feas_v = live && bit(sv.elig, lane) && bit(L.fits[mv], lane);
         const float c_v = kSlots ? reinterpret_cast<const CostS *>(L.exec)[mv * D + dl].exec : L.exec[mv * D + dl];
@@ -867,14 +890,22 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     float base_tr = 0.0f;
                     uint32_t ph[kCap] = {0u, 0u, 0u};
                     float pw[kCap] = {0.0f, 0.0f, 0.0f};
-                    for (uint32_t q = 0; q < dn; ++q) {
-                        const DoneParent pu = a.done[db + q];
-                        const float t = lam_tr * a.beta0 * pu.sigma;
-                        base_tr += t;
-                        if (q < (uint32_t)kCap) {
-                            ph[q] = (uint32_t)pu.holders;
-                            pw[q] = t + cw;
+                    if (dn > 0) {  // the staged parents' loads are issued together
+                        DoneParent pu[kCap];
+#pragma unroll
+                        for (int q = 0; q < kCap; ++q)
+                            if ((uint32_t)q < dn) pu[q] = a.done[db + q];
+#pragma unroll
+                        for (int q = 0; q < kCap; ++q) {
+                            if ((uint32_t)q < dn) {
+                                const float t = lam_tr * a.beta0 * pu[q].sigma;
+                                base_tr += t;
+                                ph[q] = (uint32_t)pu[q].holders;
+                                pw[q] = t + cw;
+                            }
                         }
+                        for (uint32_t q = kCap; q < dn; ++q)  // rare: more completed parents than staged
+                            base_tr += lam_tr * a.beta0 * a.done[db + q].sigma;
                     }
                     EntryS S;
                     const bool child = VAR ? child_of(a, rw, depth, sv.v) : depth == 1;
