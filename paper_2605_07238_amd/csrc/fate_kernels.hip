@@ -401,6 +401,7 @@ __device__ __forceinline__ void decode_window(int t, int D, int &i, int &k) {
     i = t;
 }
 
+// Reciprocal to about 1 ulp (one instruction; an IEEE division takes about ten).
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
 // Make the group's LDS writes visible to the other lanes of the same wave.
@@ -737,7 +738,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         const float c_v = kSlots ? reinterpret_cast<const CostS *>(L.exec)[mv * D + dl].exec : L.exec[mv * D + dl];
         const float sw_v = kSlots ? reinterpret_cast<const CostS *>(L.exec)[mv * D + dl].swo
                                   : (bit(rho, mv) ? res_cost : L.ksw[mv * D + dl]);
-        const float colo_v = sv.npar ? cnt / (float)sv.npar : 0.0f;
+        const float colo_v = sv.npar ? cnt * fast_rcp((float)sv.npar) : 0.0f;
         const float pf_v = hv_cached ? ps.kpf * sv.tokens : 0.0f;
         const float a_imm = ps.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
         const float b_imm = c_v + lam_tr * tr - lam_p * pf_v;
@@ -768,7 +769,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 E.feas = (Mask)(rw.elig & L.fits[rw.model]);
                 E.pfdevs = table_find<Mask>(L, rw.hash);
                 E.gh = mean_levels ? L.gpow[depth] * a.desc_w[e] : L.gpow[depth];
-                const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
+                const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
                 E.cw = cw;
                 E.pfp = lam_p * ps.kpf * rw.tokens;
                 E.moff = (uint32_t)rw.model * (uint32_t)D;
@@ -848,7 +849,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
 #pragma unroll
             for (int s = 0; s < 3; ++s) {
                 const int k = s + 2;
-                const float y = a_imm + b_imm / (float)k;
+                const float y = a_imm + b_imm * (1.0f / (float)k);  // k is a constant here
                 // maximum over devices i..i+k-1 (a lane whose source is past the row holds no window)
                 float m = fmaxf(y, dpp_b0<0x101>(y));
                 if (k >= 3) m = fmaxf(m, dpp_b0<0x102>(y));
@@ -856,7 +857,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 const uint32_t wm = (1u << k) - 1u;
                 w_ok[s] = windows_on && s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
                 // gather with uniform beta: each of the k-1 other devices sends sigma/k
-                w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma / (float)k);
+                w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma * (1.0f / (float)k));
             }
 
             // ---- horizon rows, G at a time: lane j stages row j (EntryS)
@@ -886,7 +887,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     const uint32_t feas = (uint32_t)(rw.elig & L.fits[rw.model]);
                     const uint32_t pfo = table_find<uint32_t>(L, rw.hash);
                     const bool same = rw.hash != 0 && rw.hash == sv.hash;
-                    const float cw = lam_c / (float)rw.npar;  // a descendant has at least one parent
+                    const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
                     float base_tr = 0.0f;
                     uint32_t ph[kCap] = {0u, 0u, 0u};
                     float pw[kCap] = {0.0f, 0.0f, 0.0f};
@@ -1066,13 +1067,14 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             const int t = lane + s * G;
             int i = 0, k = 2;
             if (t < nwin) decode_window(t, D, i, k);
+            const float rk = fast_rcp((float)k);
             float tmax = -inf_f();
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int src = min(i + q, G - 1);
                 const float aq = __shfl(a_imm, src, G);
                 const float bq = __shfl(b_imm, src, G);
-                if (q < k) tmax = fmaxf(tmax, aq + bq / (float)k);
+                if (q < k) tmax = fmaxf(tmax, aq + bq * rk);
             }
             const uint64_t wm = ((1ull << k) - 1ull) << i;
             const bool feasible = windows_on && (t < nwin) && ((feas_mask & wm) == wm);
@@ -1081,7 +1083,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                 for (int p = i; p < i + k; ++p) {
                     float sum = 0.0f;
                     for (int d = i; d < i + k; ++d)
-                        if (d != p) sum += a.beta[d * D + p] * sv.sigma / (float)k;
+                        if (d != p) sum += a.beta[d * D + p] * sv.sigma * rk;
                     gat = fminf(gat, sum);
                 }
             }
