@@ -303,6 +303,9 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         if nF0 == 0:
             break
         e = [mk() for _ in range(5)]
+        # keep the device busy while the host enqueues the step, so that the
+        # first event does not also time the host's call overhead
+        torch.cuda._sleep(1000000)
         e[0].record()
         fate.fate_score_frontier(pk, st, params, out=scores)
         e[1].record()

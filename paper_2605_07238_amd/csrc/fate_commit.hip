@@ -17,10 +17,11 @@
 //                   a pending stage its completed parents, and its candidate
 //                   count when it is now in the frontier (every parent
 //                   completed); workgroup totals.
-//   k_plan_offsets  one workgroup: exclusive scan of the workgroup totals;
-//                   frontier and candidate totals.
+//   k_plan_offsets  one workgroup: exclusive scan of the workgroup totals
+//                   (8 per thread per workgroup scan); frontier and
+//                   candidate totals.
 //   k_plan_fill     per stage: offset and entries of its completed-parent
-//                   list, its frontier slot and first candidate.
+//                   list, its frontier slot, instance and first candidate.
 //   k_plan_slices   one workgroup: each instance's frontier range cut into
 //                   workgroup slices for the scoring kernel; the counts the
 //                   scoring and top-k launches read.
@@ -83,6 +84,34 @@ __device__ int instance_of(const int64_t *stage_off, int B, int64_t s) {
         else hi = mid;
     }
     return lo;
+}
+
+// Instance of each lane's stage sw + lane, for a wave whose 64 lanes hold
+// consecutive stages from sw < N (all lanes active).  A 64-way search finds
+// the instance of sw (each round of parallel loads narrows the range
+// 64-fold), then the instance starts inside the wave's range, which form a
+// prefix of the following instances, move each lane past the starts at or
+// before its stage.  Many empty instances can put more than 63 starts in
+// the range; those waves search per lane.
+__device__ int instance_of_wave(const int64_t *stage_off, int B, int64_t sw) {
+    const int lane = threadIdx.x & 63;
+    int lo = 0, hi = B;  // stage_off[lo] <= sw < stage_off[hi] (stage_off[B] = N)
+    while (hi - lo > 1) {  // uniform
+        const int64_t n = hi - lo;
+        auto probe = [&](int l) { return lo + 1 + (int)(((int64_t)l * (n - 1)) / 64); };  // in [lo + 1, hi - 1]
+        const int cnt = __popcll(__ballot(stage_off[probe(lane)] <= sw));  // the probes at or below sw form a prefix
+        const int nlo = cnt > 0 ? probe(cnt - 1) : lo;
+        const int nhi = cnt < 64 ? probe(cnt) : hi;
+        lo = nlo;
+        hi = nhi;
+    }
+    const int64_t s = sw + lane;
+    const int64_t st = stage_off[min(lo + 1 + lane, B)];  // starts after the instance of sw, ascending
+    const int k = __popcll(__ballot(st <= sw + 63));
+    if (k == 64) return instance_of(stage_off, B, s);
+    int inst = lo;
+    for (int j = 0; j < k; ++j) inst += s >= __shfl(st, j) ? 1 : 0;  // uniform trip count
+    return inst;
 }
 
 // One frontier slot of the instance, staged for the lanes of its wave:
@@ -347,34 +376,44 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
     }
 }
 
-constexpr int kChunks = 8;  // 1024-item chunks whose loads one thread issues together
+// Workgroup totals per thread of k_plan_offsets: 8 K totals (2 M stages) per
+// workgroup scan.
+constexpr int kOffItems = 8;
 
 __global__ __launch_bounds__(1024) void k_plan_offsets(CommitLaunch a) {
-    // chunks of 1024 workgroup triples, one triple per thread, scanned
-    // together; the loads of kChunks chunks are in flight at once
+    // each thread sums kOffItems consecutive workgroup triples, the
+    // workgroup scans the thread sums, each thread writes its triples' offsets
     __shared__ uint32_t sh[3 * (1024 / 64)];
     uint32_t run[3] = {0u, 0u, 0u};
-    for (int batch = 0; batch < a.nblk; batch += kChunks * 1024) {  // uniform
-        uint32_t x[kChunks][3];
+    for (int batch = 0; batch < a.nblk; batch += kOffItems * 1024) {  // uniform
+        const int i0 = batch + (int)threadIdx.x * kOffItems;
+        uint32_t x[kOffItems][3];
 #pragma unroll
-        for (int q = 0; q < kChunks; ++q) {
-            const int i = batch + q * 1024 + (int)threadIdx.x;
+        for (int j = 0; j < kOffItems; ++j) {
 #pragma unroll
-            for (int c = 0; c < 3; ++c) x[q][c] = i < a.nblk ? a.bsum[3 * i + c] : 0u;
+            for (int c = 0; c < 3; ++c) x[j][c] = i0 + j < a.nblk ? a.bsum[3 * (i0 + j) + c] : 0u;
         }
+        uint32_t t[3] = {0u, 0u, 0u};
 #pragma unroll
-        for (int q = 0; q < kChunks; ++q) {
-            if (batch + q * 1024 >= a.nblk) break;  // uniform
-            const int i = batch + q * 1024 + (int)threadIdx.x;
-            uint32_t ex[3], tot[3];
-            block_exscan<1024, 3>(x[q], sh, ex, tot);
-            if (i < a.nblk) {
+        for (int j = 0; j < kOffItems; ++j) {  // exclusive sums within the thread, in place
 #pragma unroll
-                for (int c = 0; c < 3; ++c) a.bsum[3 * i + c] = run[c] + ex[c];
+            for (int c = 0; c < 3; ++c) {
+                const uint32_t v = x[j][c];
+                x[j][c] = t[c];
+                t[c] += v;
             }
-#pragma unroll
-            for (int c = 0; c < 3; ++c) run[c] += tot[c];
         }
+        uint32_t ex[3], tot[3];
+        block_exscan<1024, 3>(t, sh, ex, tot);
+#pragma unroll
+        for (int j = 0; j < kOffItems; ++j) {
+            if (i0 + j < a.nblk) {
+#pragma unroll
+                for (int c = 0; c < 3; ++c) a.bsum[3 * (i0 + j) + c] = run[c] + ex[c] + x[j][c];
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 3; ++c) run[c] += tot[c];
     }
     if (threadIdx.x == 0) {
         a.done_off[a.N] = run[0];
@@ -405,6 +444,9 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
     uint32_t dpos = a.bsum[3 * blockIdx.x] + ex[0];
     uint32_t fpos = a.bsum[3 * blockIdx.x + 1] + ex[1];
     uint32_t cpos = a.bsum[3 * blockIdx.x + 2] + ex[2];
+    static_assert(kPlanItems == 1, "the wave's stages are consecutive, one per lane");
+    const int64_t sw = s0 - (threadIdx.x & 63);  // first stage of the wave
+    const int inst = sw < a.N ? instance_of_wave(a.stage_off, a.B, sw) : 0;  // uniform condition
     for (int i = 0; i < kPlanItems; ++i) {
         const int64_t s = s0 + i;
         if (s >= a.N) break;
@@ -412,7 +454,7 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
         a.fidx[s] = fpos;
         if (nc[i]) {
             a.frontier[2 * (int64_t)fpos] = (uint32_t)s;
-            a.frontier[2 * (int64_t)fpos + 1] = (uint32_t)instance_of(a.stage_off, a.B, s);
+            a.frontier[2 * (int64_t)fpos + 1] = (uint32_t)inst;
             a.cand_off[fpos] = cpos;
             ++fpos;
             cpos += nc[i];
@@ -434,45 +476,48 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
     }
 }
 
+// Instances per thread of k_plan_slices: 4 K instances take one workgroup scan.
+constexpr int kSliceItems = 4;
+
 __global__ __launch_bounds__(1024) void k_plan_slices(CommitLaunch a) {
-    // chunks of 1024 instances, one per thread; the frontier bounds of
-    // kChunks chunks are loaded together
+    // each thread takes kSliceItems consecutive instances: their frontier
+    // ranges, slice and rejection counts; one workgroup scan places them
     __shared__ uint32_t sh[2 * (1024 / 64)];
     const uint32_t slice = (uint32_t)a.slice;
     uint32_t run[2] = {0u, 0u};
-    for (int batch = 0; batch < a.B; batch += kChunks * 1024) {  // uniform
-        int64_t s0[kChunks], s1[kChunks];
+    for (int batch = 0; batch < a.B; batch += kSliceItems * 1024) {  // uniform
+        const int b0 = batch + (int)threadIdx.x * kSliceItems;
+        int64_t so[kSliceItems + 1];
 #pragma unroll
-        for (int q = 0; q < kChunks; ++q) {
-            const int b = batch + q * 1024 + (int)threadIdx.x;
-            s0[q] = b < a.B ? a.stage_off[b] : 0;
-            s1[q] = b < a.B ? a.stage_off[b + 1] : 0;
+        for (int j = 0; j <= kSliceItems; ++j) so[j] = b0 + j <= a.B ? a.stage_off[b0 + j] : 0;
+        uint32_t f[kSliceItems + 1], r[kSliceItems];
+#pragma unroll
+        for (int j = 0; j <= kSliceItems; ++j) f[j] = b0 + j <= a.B ? a.fidx[so[j]] : 0u;
+#pragma unroll
+        for (int j = 0; j < kSliceItems; ++j) r[j] = b0 + j < a.B ? a.rej[b0 + j] : 0u;
+        uint32_t ns[kSliceItems], t[2] = {0u, 0u};
+#pragma unroll
+        for (int j = 0; j < kSliceItems; ++j) {
+            ns[j] = b0 + j < a.B ? (f[j + 1] - f[j] + slice - 1) / slice : 0u;
+            t[0] += ns[j];
+            t[1] += r[j];
         }
-        uint32_t f0[kChunks], f1[kChunks], r[kChunks];
+        uint32_t ex[2], tot[2];
+        block_exscan<1024, 2>(t, sh, ex, tot);
+        uint32_t off = run[0] + ex[0];
 #pragma unroll
-        for (int q = 0; q < kChunks; ++q) {
-            const int b = batch + q * 1024 + (int)threadIdx.x;
-            f0[q] = b < a.B ? a.fidx[s0[q]] : 0u;
-            f1[q] = b < a.B ? a.fidx[s1[q]] : 0u;
-            r[q] = b < a.B ? a.rej[b] : 0u;
-        }
-#pragma unroll
-        for (int q = 0; q < kChunks; ++q) {
-            if (batch + q * 1024 >= a.B) break;  // uniform
-            const int b = batch + q * 1024 + (int)threadIdx.x;
-            const uint32_t x[2] = {(f1[q] - f0[q] + slice - 1) / slice, r[q]};
-            uint32_t ex[2], tot[2];
-            block_exscan<1024, 2>(x, sh, ex, tot);
-            uint32_t off = run[0] + ex[0];
-            for (uint32_t f = f0[q]; f < f1[q]; f += slice, ++off) {
+        for (int j = 0; j < kSliceItems; ++j) {
+            if (b0 + j >= a.B) break;
+            for (uint32_t q = 0; q < ns[j]; ++q, ++off) {
+                const uint32_t fs = f[j] + q * slice;
                 const int64_t o = 3 * (int64_t)off;
-                a.slices[o] = (uint32_t)b;
-                a.slices[o + 1] = f;
-                a.slices[o + 2] = min(f + slice, f1[q]);
+                a.slices[o] = (uint32_t)(b0 + j);
+                a.slices[o + 1] = fs;
+                a.slices[o + 2] = min(fs + slice, f[j + 1]);
             }
-            run[0] += tot[0];
-            run[1] += tot[1];
         }
+        run[0] += tot[0];
+        run[1] += tot[1];
     }
     if (threadIdx.x == 0) {
         a.counts[2] = run[0];

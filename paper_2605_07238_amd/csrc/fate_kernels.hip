@@ -33,6 +33,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "fate_device.h"
@@ -1211,22 +1212,30 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
     const int tid = threadIdx.x;
     const int lane = tid & (G - 1);
     const int64_t nF = a.dcounts ? (int64_t)a.dcounts[0] : a.nF;  // planning state: current frontier
-    uint32_t c0[kTopkRounds];
-    int C[kTopkRounds];
-    int64_t f[kTopkRounds];
-#pragma unroll
-    for (int r = 0; r < kTopkRounds; ++r) {  // round r: the block's groups take consecutive stages
-        const int64_t fr = ((int64_t)blockIdx.x * kTopkRounds + r) * kGroups + tid / G;
-        c0[r] = 0; C[r] = 0; f[r] = -1;
-        if (fr < nF) {
-            c0[r] = a.cand_off[fr];
-            C[r] = (int)(a.cand_off[fr + 1] - c0[r]);
-            f[r] = fr;
-        }
-    }
     const int64_t so = (int64_t)blockIdx.y * a.score_stride, oo = (int64_t)blockIdx.y * a.out_stride;
-    rank_stages<G, kTopkRounds>(a.scores + so, c0, C, f, lane, a.k, a.idx + oo, a.val + oo);
+    // tiles of kTopkRounds * kGroups stages, grid-strided: a planning state's
+    // grid covers its frontier capacity, mostly beyond the current frontier
+    for (int64_t tile = blockIdx.x; tile * (kTopkRounds * kGroups) < nF; tile += gridDim.x) {  // uniform
+        uint32_t c0[kTopkRounds];
+        int C[kTopkRounds];
+        int64_t f[kTopkRounds];
+#pragma unroll
+        for (int r = 0; r < kTopkRounds; ++r) {  // round r: the block's groups take consecutive stages
+            const int64_t fr = (tile * kTopkRounds + r) * kGroups + tid / G;
+            c0[r] = 0; C[r] = 0; f[r] = -1;
+            if (fr < nF) {
+                c0[r] = a.cand_off[fr];
+                C[r] = (int)(a.cand_off[fr + 1] - c0[r]);
+                f[r] = fr;
+            }
+        }
+        rank_stages<G, kTopkRounds>(a.scores + so, c0, C, f, lane, a.k, a.idx + oo, a.val + oo);
+    }
 }
+
+// Most workgroups of one top-k launch (sixteen per compute unit); larger
+// frontiers loop over their tiles.
+constexpr int64_t kTopkMaxBlocks = 4096;
 
 }  // namespace
 
@@ -1265,7 +1274,7 @@ int launch_score(const ScoreLaunch &a, void *stream) {
 int launch_topk(const TopkLaunch &a, void *stream) {
     const int G = group_width(a.D);
     const int64_t per_block = (int64_t)(kBlock / G) * kTopkRounds;
-    const int64_t blocks = (a.nF + per_block - 1) / per_block;
+    const int64_t blocks = std::min((a.nF + per_block - 1) / per_block, kTopkMaxBlocks);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const dim3 grid((unsigned)blocks, (unsigned)a.nsets);
     switch (G) {
