@@ -1,7 +1,7 @@
 // Commit-and-advance of a planning state on the device (Alg. 1: materialise
 // the selected placements, then advance the planning frontier and update the
 // planning state; Alg. 2: commit into the action pool and update the state
-// as the stages complete).  Five launches on the caller's stream:
+// as the stages complete).  Six launches on the caller's stream:
 //
 //   k_commit_apply  one wave per instance.  The wave keeps the instance's
 //                   prefix slots, the exec and switch tables and the model
@@ -17,9 +17,12 @@
 //                   a pending stage its completed parents, and its candidate
 //                   count when it is now in the frontier (every parent
 //                   completed); workgroup totals.
-//   k_plan_offsets  one workgroup: exclusive scan of the workgroup totals
-//                   (8 per thread per workgroup scan); frontier and
-//                   candidate totals.
+//   k_plan_segscan  one workgroup per segment of kPlanSeg workgroup totals:
+//                   offsets within the segment, segment totals.
+//   k_plan_offsets  one workgroup: exclusive scan of the segment totals;
+//                   frontier and candidate totals.  (One workgroup reading
+//                   all the workgroup totals took 31 us: a single compute
+//                   unit keeps too few loads in flight.)
 //   k_plan_fill     per stage: offset and entries of its completed-parent
 //                   list, its frontier slot, instance and first candidate.
 //   k_plan_slices   one workgroup: each instance's frontier range cut into
@@ -376,41 +379,43 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
     }
 }
 
-// Workgroup totals per thread of k_plan_offsets: 8 K totals (2 M stages) per
-// workgroup scan.
-constexpr int kOffItems = 8;
+// One workgroup per segment of kPlanSeg workgroup totals: the totals become
+// offsets within the segment (in place), and the segment total is recorded.
+__global__ __launch_bounds__(kPlanBlock) void k_plan_segscan(CommitLaunch a) {
+    static_assert(kPlanSeg == kPlanBlock, "one workgroup total per thread");
+    __shared__ uint32_t sh[3 * (kPlanBlock / 64)];
+    const int seg = (int)blockIdx.x, i = seg * kPlanSeg + (int)threadIdx.x;
+    uint32_t x[3] = {0u, 0u, 0u};
+    if (i < a.nblk) {
+#pragma unroll
+        for (int c = 0; c < 3; ++c) x[c] = a.bsum[3 * i + c];
+    }
+    uint32_t ex[3], tot[3];
+    block_exscan<kPlanBlock, 3>(x, sh, ex, tot);
+    if (i < a.nblk) {
+#pragma unroll
+        for (int c = 0; c < 3; ++c) a.bsum[3 * i + c] = ex[c];
+    }
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int c = 0; c < 3; ++c) a.segsum[3 * seg + c] = tot[c];
+    }
+}
 
 __global__ __launch_bounds__(1024) void k_plan_offsets(CommitLaunch a) {
-    // each thread sums kOffItems consecutive workgroup triples, the
-    // workgroup scans the thread sums, each thread writes its triples' offsets
+    // exclusive scan of the segment totals, 1024 at a time, in place
     __shared__ uint32_t sh[3 * (1024 / 64)];
     uint32_t run[3] = {0u, 0u, 0u};
-    for (int batch = 0; batch < a.nblk; batch += kOffItems * 1024) {  // uniform
-        const int i0 = batch + (int)threadIdx.x * kOffItems;
-        uint32_t x[kOffItems][3];
+    for (int batch = 0; batch < a.nseg; batch += 1024) {  // uniform
+        const int i = batch + (int)threadIdx.x;
+        uint32_t x[3];
 #pragma unroll
-        for (int j = 0; j < kOffItems; ++j) {
-#pragma unroll
-            for (int c = 0; c < 3; ++c) x[j][c] = i0 + j < a.nblk ? a.bsum[3 * (i0 + j) + c] : 0u;
-        }
-        uint32_t t[3] = {0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < kOffItems; ++j) {  // exclusive sums within the thread, in place
-#pragma unroll
-            for (int c = 0; c < 3; ++c) {
-                const uint32_t v = x[j][c];
-                x[j][c] = t[c];
-                t[c] += v;
-            }
-        }
+        for (int c = 0; c < 3; ++c) x[c] = i < a.nseg ? a.segsum[3 * i + c] : 0u;
         uint32_t ex[3], tot[3];
-        block_exscan<1024, 3>(t, sh, ex, tot);
+        block_exscan<1024, 3>(x, sh, ex, tot);
+        if (i < a.nseg) {
 #pragma unroll
-        for (int j = 0; j < kOffItems; ++j) {
-            if (i0 + j < a.nblk) {
-#pragma unroll
-                for (int c = 0; c < 3; ++c) a.bsum[3 * (i0 + j) + c] = run[c] + ex[c] + x[j][c];
-            }
+            for (int c = 0; c < 3; ++c) a.segsum[3 * i + c] = run[c] + ex[c];
         }
 #pragma unroll
         for (int c = 0; c < 3; ++c) run[c] += tot[c];
@@ -441,9 +446,10 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
     const uint32_t x[3] = {tcp, tfr, tnc};
     uint32_t ex[3], tot[3];
     block_exscan<kPlanBlock, 3>(x, sh, ex, tot);
-    uint32_t dpos = a.bsum[3 * blockIdx.x] + ex[0];
-    uint32_t fpos = a.bsum[3 * blockIdx.x + 1] + ex[1];
-    uint32_t cpos = a.bsum[3 * blockIdx.x + 2] + ex[2];
+    const int seg = (int)blockIdx.x / kPlanSeg;  // segment offset + offset within the segment + within the workgroup
+    uint32_t dpos = a.segsum[3 * seg] + a.bsum[3 * blockIdx.x] + ex[0];
+    uint32_t fpos = a.segsum[3 * seg + 1] + a.bsum[3 * blockIdx.x + 1] + ex[1];
+    uint32_t cpos = a.segsum[3 * seg + 2] + a.bsum[3 * blockIdx.x + 2] + ex[2];
     static_assert(kPlanItems == 1, "the wave's stages are consecutive, one per lane");
     const int64_t sw = s0 - (threadIdx.x & 63);  // first stage of the wave
     const int inst = sw < a.N ? instance_of_wave(a.stage_off, a.B, sw) : 0;  // uniform condition
@@ -532,6 +538,7 @@ int launch_commit(const CommitLaunch &a, void *stream) {
     if (a.B > 0)
         hipLaunchKernelGGL(k_commit_apply, dim3((unsigned)a.B), dim3(64), apply_lds_bytes(a.D, a.M, a.K), s, a);
     if (a.nblk > 0) hipLaunchKernelGGL(k_plan_count, dim3((unsigned)a.nblk), dim3(kPlanBlock), 0, s, a);
+    if (a.nseg > 0) hipLaunchKernelGGL(k_plan_segscan, dim3((unsigned)a.nseg), dim3(kPlanBlock), 0, s, a);
     hipLaunchKernelGGL(k_plan_offsets, dim3(1), dim3(1024), 0, s, a);
     if (a.nblk > 0) hipLaunchKernelGGL(k_plan_fill, dim3((unsigned)a.nblk), dim3(kPlanBlock), 0, s, a);
     hipLaunchKernelGGL(k_plan_slices, dim3(1), dim3(1024), 0, s, a);

@@ -753,6 +753,7 @@ fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *s
     a.fidx = reinterpret_cast<uint32_t *>(ws + W.fidx);
     a.bsum = reinterpret_cast<uint32_t *>(ws + W.bsum);
     a.rej = reinterpret_cast<uint32_t *>(ws + W.rej);
+    a.segsum = reinterpret_cast<uint32_t *>(ws + W.segsum);
     a.N = state->N;
     a.B = state->B;
     a.D = dags->D;
@@ -761,6 +762,7 @@ fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *s
     a.max_shard = state->max_shard;
     a.slice = fate::slice_len(dags->D);
     a.nblk = (int32_t)((state->N + fate::kPlanStages - 1) / fate::kPlanStages);
+    a.nseg = (a.nblk + fate::kPlanSeg - 1) / fate::kPlanSeg;
     return fate::launch_commit(a, stream) == 0 ? FATE_OK : FATE_EHIP;
 }
 

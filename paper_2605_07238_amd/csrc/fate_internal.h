@@ -112,14 +112,18 @@ struct CommitLaunch {
     int32_t sel_stride;
     // workspace (commit_ws_layout)
     uint32_t *cp, *nc, *fidx, *bsum, *rej;
+    uint32_t *segsum;  // per segment of kPlanSeg workgroups: totals, then offsets
+    int32_t nseg;
     int64_t N;
     int32_t B, D, M, K, max_shard, slice, nblk;
 };
 
-// Stages per workgroup of the planning scans, and the workspace layout.
+// Stages per workgroup of the planning scans, workgroups per segment of the
+// two-level offset scan, and the workspace layout.
 constexpr int kPlanBlock = 256, kPlanItems = 1, kPlanStages = kPlanBlock * kPlanItems;
+constexpr int kPlanSeg = kPlanBlock;
 struct CommitWs {
-    size_t cp, nc, fidx, bsum, rej, total;
+    size_t cp, nc, fidx, bsum, rej, segsum, total;
 };
 inline CommitWs commit_ws_layout(int64_t N, int B) {
     auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
@@ -131,6 +135,8 @@ inline CommitWs commit_ws_layout(int64_t N, int B) {
     w.fidx = o; o = up(o + 4 * ((size_t)N + 1));
     w.bsum = o; o = up(o + 12 * (size_t)nblk);
     w.rej = o; o = up(o + 4 * ((size_t)B + 1));
+    const int64_t nseg = (nblk + kPlanSeg - 1) / kPlanSeg;
+    w.segsum = o; o = up(o + 12 * (size_t)nseg);
     w.total = o;
     return w;
 }
