@@ -47,13 +47,28 @@ struct ChoiceL {
     uint32_t key, pad;
 };
 
+// Maximum over the wave (all 64 lanes active), returned to every lane: DPP
+// steps within each 16-lane row (pairs, quads, half-rows, rows), then the four
+// row maxima through scalar registers.  No LDS round trips.
+template <int CTRL>
+__device__ __forceinline__ uint32_t umax_dpp(uint32_t x) {
+    return max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+    x = umax_dpp<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+    x = umax_dpp<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+    x = umax_dpp<0x141>(x);  // row_half_mirror
+    x = umax_dpp<0x140>(x);  // row_mirror
+    const uint32_t r0 = __builtin_amdgcn_readlane(x, 0), r1 = __builtin_amdgcn_readlane(x, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(x, 32), r3 = __builtin_amdgcn_readlane(x, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+// 64-bit maximum: the high words first, then the low words of the lanes
+// holding the highest high word.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint64_t y = __shfl_xor(x, off, 64);
-        x = y > x ? y : x;
-    }
-    return x;
+    const uint32_t hi = wave_max_u32((uint32_t)(x >> 32));
+    const uint32_t lo = wave_max_u32((uint32_t)(x >> 32) == hi ? (uint32_t)x : 0u);
+    return ((uint64_t)hi << 32) | lo;
 }
 
 __global__ __launch_bounds__(64) void k_plan_wave(PlanLaunch a) {

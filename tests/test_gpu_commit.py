@@ -166,6 +166,15 @@ def test_commit_recipes(name):
     _run_steps(w, 3)
 
 
+def test_commit_several_scan_segments():
+    """More than 65,536 stages: the workgroup totals span two segments of the
+    two-level offset scan (the second one ragged), and frontier slots near
+    instance starts fall inside one wave of the fill."""
+    w = synth.make_workload("forkjoin-4096x1000-d16", B=80)
+    assert w.N > 256 * 256 and (w.N + 255) // 256 % 256 != 0
+    _run_steps(w, 2)
+
+
 def test_commit_partial_and_rejected_selections():
     """Stages left at -1 stay pending; out-of-range and infeasible selections
     are rejected, counted and change nothing."""
