@@ -395,6 +395,35 @@ __device__ __forceinline__ float from_right(float x, int lane) {
     return lane + 1 < G ? y : inf_f();
 }
 
+// Minimum of x over the other lanes of a 32- or 64-lane group, for the lanes
+// of a wave that hold whole groups (every lane of the group active): DPP
+// prefix and suffix minima within each 16-lane row, then the other rows'
+// minima of the group through scalar registers.  No LDS round trips (group
+// shuffles take six dependent ones per scan).
+template <int G>
+__device__ __forceinline__ float others_min_wide(float x, int wl) {
+    static_assert(G == 32 || G == 64, "groups of whole DPP rows");
+    float p = x, q = x;
+    p = fminf(p, dpp_move<0x111>(p, p)); q = fminf(q, dpp_move<0x101>(q, q));
+    p = fminf(p, dpp_move<0x112>(p, p)); q = fminf(q, dpp_move<0x102>(q, q));
+    p = fminf(p, dpp_move<0x114>(p, p)); q = fminf(q, dpp_move<0x104>(q, q));
+    p = fminf(p, dpp_move<0x118>(p, p)); q = fminf(q, dpp_move<0x108>(q, q));
+    const float in_row = fminf(dpp_move<0x111>(inf_f(), p), dpp_move<0x101>(inf_f(), q));  // lanes before / after in the row
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), 15));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), 31));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), 47));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), 63));
+    const int row = wl >> 4;
+    float rows;
+    if constexpr (G == 64) {
+        const float m01 = fminf(r0, r1), m23 = fminf(r2, r3);
+        rows = row == 0 ? fminf(r1, m23) : row == 1 ? fminf(r0, m23) : row == 2 ? fminf(m01, r3) : fminf(m01, r2);
+    } else {  // rows 0, 1 and rows 2, 3 are two groups
+        rows = row == 0 ? r1 : row == 1 ? r0 : row == 2 ? r3 : r2;
+    }
+    return fminf(in_row, rows);
+}
+
 // Window t (0-based among a stage's windows) -> start i and size k >= 2.
 __device__ __forceinline__ void decode_window(int t, int D, int &i, int &k) {
     k = 2;
@@ -1104,10 +1133,18 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
                     bool c0c, c1c;
                     entry_row(area[jj], B0, N0, g0, c0c);
                     entry_row(area[jj + 1], B1, N1, g1, c1c);
-                    float p0 = B0, q0 = B0, p1 = B1, q1 = B1;
-                    scan_min_pair<G>(p0, q0, p1, q1, lane);
-                    const float e0 = fminf(from_left<G>(p0, lane), from_right<G>(q0, lane)) + (c0c ? t0 : 0.0f);
-                    const float e1 = fminf(from_left<G>(p1, lane), from_right<G>(q1, lane)) + (c1c ? t0 : 0.0f);
+                    float o0, o1;  // minimum over the other devices
+                    if constexpr (G >= 32) {
+                        o0 = others_min_wide<G>(B0, tid & 63);
+                        o1 = others_min_wide<G>(B1, tid & 63);
+                    } else {
+                        float p0 = B0, q0 = B0, p1 = B1, q1 = B1;
+                        scan_min_pair<G>(p0, q0, p1, q1, lane);
+                        o0 = fminf(from_left<G>(p0, lane), from_right<G>(q0, lane));
+                        o1 = fminf(from_left<G>(p1, lane), from_right<G>(q1, lane));
+                    }
+                    const float e0 = o0 + (c0c ? t0 : 0.0f);
+                    const float e1 = o1 + (c1c ? t0 : 0.0f);
                     acc0 += (double)(g0 * fminf(e0, N0));
                     acc0 += (double)(g1 * fminf(e1, N1));
                 }

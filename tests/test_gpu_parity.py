@@ -72,6 +72,12 @@ RANDOM_CASES = [
     (12, dict(D=16, n=24, M=40, K=4, uniform_beta=True), 3, 4),
     (13, dict(D=12, n=30, M=6, p_edge=0.5, uniform_beta=True), 4, 3),
     (14, dict(D=16, n=40, M=8, p_edge=0.35, uniform_beta=True, shard_frac=0.7), 3, 4),
+    # 32- and 64-lane groups with uniform beta and singletons only: the minimum over
+    # the other devices through DPP rows and scalar row minima (two 32-lane groups of
+    # a wave score different stages and may run different numbers of rows)
+    (15, dict(D=24, n=30, M=6, p_edge=0.3, uniform_beta=True), 3, 1),
+    (16, dict(D=32, n=40, M=5, p_edge=0.25, uniform_beta=True, B=5), 4, 1),
+    (17, dict(D=40, n=30, M=6, p_edge=0.3, uniform_beta=True), 3, 1),
 ]
 
 
