@@ -579,7 +579,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
     const int D = a.D, K = a.K, M = a.M;
     const uint32_t b = a.slices[3 * slice];
     const uint32_t f0 = a.slices[3 * slice + 1];
-    const int nF = (int)(a.slices[3 * slice + 2] - f0);
+    // a slice holds at most a.slice stages (the LDS plan's size); a longer one,
+    // from a state that another build packed, is cut rather than overrun LDS
+    const int nF = min((int)(a.slices[3 * slice + 2] - f0), a.slice);
     const int P = pow2_at_least(nF);
     using Mask = MaskFor<G>;  // device bitmask
     // slot layout: 16-lane groups, uniform beta, at most 32 models (chosen by the launcher)
