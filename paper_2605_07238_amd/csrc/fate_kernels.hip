@@ -623,10 +623,9 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         *L.next = 0u;
     }
     if constexpr (SLOTS) {
-        // cost table and the residency after loading m on d (at most 32 models)
+        // cost table (the residency after each load follows after the barrier)
         const float res = VAR ? -ps.lam_m : 0.0f;
         CostS *tab = reinterpret_cast<CostS *>(L.exec);
-        uint32_t *rnew = reinterpret_cast<uint32_t *>(L.ksw);
         for (int i = tid; i < M * D; i += kBlock) {
             const int m = i / D, d = i - m * D;
             const float ks = ps.lam_s * a.ksw[i];
@@ -638,7 +637,6 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
             c.exec = a.exec[i];
             c.swo = swo;
             tab[i] = c;
-            rnew[i] = (uint32_t)load_model(rd, m, a.cap[d], a.weight);
         }
     } else {
         for (int i = tid; i < M * D; i += kBlock) { L.exec[i] = a.exec[i]; L.ksw[i] = ps.lam_s * a.ksw[i]; }
@@ -690,6 +688,13 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
         for (int d = 0; d < D; ++d)
             if (bit(L.rho[d], tid)) m |= 1ull << d;
         L.rm[tid] = m;
+    }
+    if constexpr (SLOTS) {  // residency of d after loading m, from the LDS tables (the Load rule's chain of reads)
+        uint32_t *rnew = reinterpret_cast<uint32_t *>(L.ksw);
+        for (int i = tid; i < M * D; i += kBlock) {
+            const int m = i / D, d = i - m * D;
+            rnew[i] = (uint32_t)load_model(L.rho[d], m, L.cap[d], L.wt);
+        }
     }
     // work order: stage i goes to position = number of keys smaller than its
     // own (keys are distinct), so the most descendants come first
