@@ -10,7 +10,8 @@
 //   1. Lane d evaluates the immediate terms of v on device d (App. A.3):
 //      waiting, switch, transfer from completed parents, colocation, prefix
 //      reuse, and the post-state of d after loading m(v) (Load with eviction
-//      of the smallest-id other models while over capacity).
+//      of the smallest-id other models while over capacity; the slot layout
+//      reads it, and the cost terms, from per-block tables built once).
 //   2. Slot 0 of lane d is the single-device candidate {d}; slots 1..3 hold
 //      contiguous windows.  A window's immediate cost is the maximum over its
 //      devices of the per-device time with runtime, transfer and prefix split
@@ -19,8 +20,11 @@
 //      by the host) lane d' computes B(d') = c_hat(w, d' | s) and the value it
 //      takes once v sits on d' (model loaded, prefix group cached, v's output
 //      local).  Group prefix/suffix minimum scans over B (DPP row shifts for
-//      G <= 16) give the best device outside any window in O(1); the best
-//      device inside a window is a minimum over at most four lanes.
+//      G <= 16; the slot layout scans order-reversing integer keys with one
+//      v_max_u32 per step; 32- and 64-lane groups add the other rows' minima
+//      through scalar registers) give the best device outside any window in
+//      O(1); the best device inside a window is a minimum over at most four
+//      lanes.
 //      min(outside, inside) is w's value under the candidate; it is weighted
 //      by gamma^depth and accumulated in fp64.
 //   This is an exact rearrangement of evaluating c_hat from scratch in the
