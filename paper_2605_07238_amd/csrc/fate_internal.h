@@ -144,6 +144,10 @@ inline CommitWs commit_ws_layout(int64_t N, int B) {
 // Lane-group width for D devices (power of two, 4..64) and the number of
 // frontier stages per scoring workgroup slice (eight rounds of its groups).
 constexpr int kScoreBlock = 256;
+// Threads per scoring workgroup: 1024 for 64-lane groups, whose instances
+// have few frontier stages with many rows each, so that sixteen of them are
+// in flight per workgroup; 256 otherwise.
+constexpr int score_block(int G) { return G >= 64 ? 1024 : kScoreBlock; }
 inline int group_width(int D) {
     int g = 4;
     while (g < D) g <<= 1;
@@ -154,8 +158,8 @@ inline int group_width(int D) {
 // records (64 stages measured 2% faster than 128 on the 16-device fork-join
 // batch; fewer, or other group widths, were slower).
 inline int slice_len(int D) {
-    const int G = group_width(D), groups = kScoreBlock / G;
-    const int per = G == 16 ? 4 : 8;
+    const int G = group_width(D), groups = score_block(G) / G;
+    const int per = G == 16 || G >= 64 ? 4 : 8;
     return groups * per > 256 ? 256 : groups * per;
 }
 

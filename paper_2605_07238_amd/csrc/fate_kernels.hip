@@ -145,8 +145,8 @@ constexpr int kSlotGroupBytes = 16 * (int)sizeof(EntryS) + 16;
 // Bytes of the staging area for lane-group width G (host and device agree).
 template <int G>
 constexpr int staging_bytes() {
-    return G == 16 ? (kScoreBlock / 16) * kSlotGroupBytes
-                   : kScoreBlock * (G <= 32 ? (int)sizeof(EntryL<uint32_t>) : (int)sizeof(EntryL<uint64_t>));
+    return G == 16 ? (score_block(G) / 16) * kSlotGroupBytes
+                   : score_block(G) * (G <= 32 ? (int)sizeof(EntryL<uint32_t>) : (int)sizeof(EntryL<uint64_t>));
 }
 
 template <int G>
@@ -568,7 +568,8 @@ __device__ __forceinline__ bool child_of(const ScoreLaunch &a, const StageRec &r
 // over levels, windows on, hop levels); the launcher picks it when no
 // parameter set of the launch uses a variant.
 template <int G, bool UNI, bool SLOTS, bool VAR>
-__global__ __launch_bounds__(kBlock) void k_score(ScoreLaunch a) {
+__global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
+    constexpr int kBlock = score_block(G);  // threads of this workgroup
     static_assert(!SLOTS || (UNI && G == 16), "the slot layout needs 16-lane groups and uniform beta");
     // a planning state is launched over its slice capacity; the current
     // number of slices is on the device
@@ -1293,7 +1294,7 @@ static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int sb = G == 16 ? staging_bytes<16>() : G <= 32 ? staging_bytes<8>() : staging_bytes<64>();
     const bool slots = UNI && G == 16 && a.M <= 32;  // the kernel choice below
     const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb, slots).total;
-    const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block(kBlock);
+    const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block(score_block(G));
     bool var = a.topo != 0;
     for (int p = 0; p < a.nsets; ++p) var = var || a.ps[p].lam_m != 0.0f || a.ps[p].flags != 0;
     switch (G) {
