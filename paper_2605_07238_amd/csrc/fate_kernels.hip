@@ -85,8 +85,9 @@ struct StageL {
     uint32_t c0, nc;      // first score and number of candidates
     uint16_t dn, npar;
     uint8_t model, shard, pad0, pad1;
+    uint64_t pfm;         // devices caching grp(v), looked up once the prefix table is built
 };
-static_assert(sizeof(StageL) == 56, "StageL");
+static_assert(sizeof(StageL) == 64, "StageL");
 
 // Horizon descendant staged by one lane of a group for the whole group, with
 // the per-descendant values every device lane needs precomputed.  For a
@@ -667,6 +668,7 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
             st.model = r.model;
             st.shard = r.shard;
             st.pad0 = st.pad1 = 0;
+            st.pfm = 0;
             L.stages[i] = st;
             key = ((uint64_t)(0xffffffffu - (st.e1 - st.e0)) << 32) | (uint32_t)i;
         }
@@ -709,7 +711,9 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
         for (int j = 0; j < nF; ++j) rank += L.keys[j] < ki ? 1 : 0;
         L.order[rank] = (uint8_t)i;
     }
-    __syncthreads();  // the sort keys' space becomes staging slots
+    __syncthreads();  // the sort keys' space becomes staging slots; the prefix table is built
+    for (int i = tid; i < nF; i += kBlock) L.stages[i].pfm = (uint64_t)table_find<Mask>(L, L.stages[i].hash);
+    __syncthreads();
 
     constexpr int kGroups = kBlock / G;
     const int lane = tid & (G - 1);
@@ -745,7 +749,7 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
         const int si = (int)L.order[pos];
         const StageL sv = L.stages[si];
         const int mv = sv.model;
-        const bool hv_cached = bit((uint64_t)table_find<Mask>(L, sv.hash), lane);
+        const bool hv_cached = bit(sv.pfm, lane);
 
         // ---- immediate terms of v on device `lane` and the post-state there
         float tr = 0.0f, cnt = 0.0f;
@@ -886,20 +890,22 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
             for (int rem = (int)sv.nc - D; rem > 0; rem -= D - nk) ++nk;
             const float j0_single = a_imm + b_imm;
             const uint32_t fm = (uint32_t)feas_mask;
-            float w_j0[3];
-            bool w_ok[3];
+            float w_j0[3] = {0.0f, 0.0f, 0.0f};
+            bool w_ok[3] = {false, false, false};
+            if (__ballot(nk != 0) != 0ull) {  // uniform over the wave: some stage of it has windows
 #pragma unroll
-            for (int s = 0; s < 3; ++s) {
-                const int k = s + 2;
-                const float y = a_imm + b_imm * (1.0f / (float)k);  // k is a constant here
-                // maximum over devices i..i+k-1 (a lane whose source is past the row holds no window)
-                float m = fmaxf(y, dpp_b0<0x101>(y));
-                if (k >= 3) m = fmaxf(m, dpp_b0<0x102>(y));
-                if (k >= 4) m = fmaxf(m, dpp_b0<0x103>(y));
-                const uint32_t wm = (1u << k) - 1u;
-                w_ok[s] = windows_on && s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
-                // gather with uniform beta: each of the k-1 other devices sends sigma/k
-                w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma * (1.0f / (float)k));
+                for (int s = 0; s < 3; ++s) {
+                    const int k = s + 2;
+                    const float y = a_imm + b_imm * (1.0f / (float)k);  // k is a constant here
+                    // maximum over devices i..i+k-1 (a lane whose source is past the row holds no window)
+                    float m = fmaxf(y, dpp_b0<0x101>(y));
+                    if (k >= 3) m = fmaxf(m, dpp_b0<0x102>(y));
+                    if (k >= 4) m = fmaxf(m, dpp_b0<0x103>(y));
+                    const uint32_t wm = (1u << k) - 1u;
+                    w_ok[s] = windows_on && s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
+                    // gather with uniform beta: each of the k-1 other devices sends sigma/k
+                    w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma * (1.0f / (float)k));
+                }
             }
 
             // ---- horizon rows, G at a time: lane j stages row j (EntryS)
