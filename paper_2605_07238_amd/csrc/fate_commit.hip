@@ -78,6 +78,9 @@ __device__ void block_exscan(const uint32_t (&x)[F], uint32_t *sh, uint32_t (&ex
     __syncthreads();  // sh may be reused
 }
 
+// Parents whose loads one thread issues together in the planning scans.
+constexpr int kParBatch = 8;
+
 // Instance of flat stage s: the last b with stage_off[b] <= s.
 __device__ int instance_of(const int64_t *stage_off, int B, int64_t s) {
     int lo = 0, hi = B;  // stage_off[lo] <= s < stage_off[hi]
@@ -357,9 +360,19 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
         uint32_t cp = 0, nc = 0;
         if (ready) {
             const StageRec r = a.rec[s];
-            for (uint32_t q = 0; q < r.npar; ++q) {
-                if (a.status[a.par_idx[r.par_begin + q]] == kCompleted) ++cp;
-                else ready = false;
+            for (uint32_t q0 = 0; q0 < r.npar; q0 += kParBatch) {  // the batch's loads are issued together
+                uint32_t u[kParBatch];
+#pragma unroll
+                for (int j = 0; j < kParBatch; ++j) u[j] = q0 + j < r.npar ? a.par_idx[r.par_begin + q0 + j] : 0u;
+                uint8_t st[kParBatch];
+#pragma unroll
+                for (int j = 0; j < kParBatch; ++j) st[j] = q0 + j < r.npar ? a.status[u[j]] : kCompleted;
+#pragma unroll
+                for (int j = 0; j < kParBatch; ++j) {
+                    if (q0 + j >= r.npar) break;
+                    if (st[j] == kCompleted) ++cp;
+                    else ready = false;
+                }
             }
             nc = ready ? (uint32_t)candidates_of(shard_cap_of(r.shard, a.max_shard, a.D), a.D) : 0u;
         }
@@ -468,14 +481,23 @@ __global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
         if (cp[i]) {
             const StageRec r = a.rec[s];
             uint32_t e = dpos;
-            for (uint32_t q = 0; q < r.npar; ++q) {
-                const uint32_t u = a.par_idx[r.par_begin + q];
-                if (a.status[u] != kCompleted) continue;
-                DoneParent p;
-                p.holders = a.holders[u];
-                p.sigma = a.rec[u].sigma;
-                p.pad = 0u;
-                a.done[e++] = p;
+            for (uint32_t q0 = 0; q0 < r.npar; q0 += kParBatch) {  // the batch's loads are issued together
+                uint32_t u[kParBatch];
+#pragma unroll
+                for (int j = 0; j < kParBatch; ++j) u[j] = q0 + j < r.npar ? a.par_idx[r.par_begin + q0 + j] : 0u;
+                bool done[kParBatch];
+#pragma unroll
+                for (int j = 0; j < kParBatch; ++j) done[j] = q0 + j < r.npar && a.status[u[j]] == kCompleted;
+                DoneParent p[kParBatch];
+#pragma unroll
+                for (int j = 0; j < kParBatch; ++j) {
+                    p[j].holders = done[j] ? a.holders[u[j]] : 0ull;
+                    p[j].sigma = done[j] ? a.rec[u[j]].sigma : 0.0f;
+                    p[j].pad = 0u;
+                }
+#pragma unroll
+                for (int j = 0; j < kParBatch; ++j)
+                    if (done[j]) a.done[e++] = p[j];
             }
             dpos += cp[i];
         }
