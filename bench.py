@@ -2,10 +2,10 @@
 """Benchmark of horizon-aware candidate scoring on one MI355X.
 
 One step = one pass of the scoring path over the whole batch with the packed
-DAGs and state already resident in HBM: fate_score_frontier, which scores
-every candidate of every frontier stage (immediate cost plus the depth-H
-horizon), then fate_topk (each stage's top-k); --fused times the one-launch
-fate_score_topk instead.  Packing (host validation, layout and the
+DAGs and state already resident in HBM: fate_score_topk, one launch that
+scores every candidate of every frontier stage (immediate cost plus the
+depth-H horizon) and ranks each stage's top-k; --two-calls times
+fate_score_frontier then fate_topk instead.  Packing (host validation, layout and the
 host-to-device copy) is done once before timing and reported separately.
 
 Prints one JSON line (rank 0, N=1):
@@ -473,8 +473,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--topk", type=int, default=4)
-    ap.add_argument("--fused", action="store_true",
-                    help="time fate_score_topk (one launch) instead of fate_score_frontier + fate_topk")
+    ap.add_argument("--two-calls", action="store_true",
+                    help="time fate_score_frontier then fate_topk instead of the one-launch fate_score_topk")
+    ap.add_argument("--fused", action="store_true", help="the default: time fate_score_topk (one launch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--planning-steps", type=int, default=6,
                     help="after the timed steps, run this many score / top-k / commit-and-advance planning steps "
@@ -536,6 +537,7 @@ def main():
     idx = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.int32, device="cuda")
     val = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.float32, device="cuda")
 
+    args.fused = not args.two_calls
     if args.fused:
         def step():
             fate.fate_score_topk(pk, st, params, args.topk, out=scores, idx=idx, val=val)

@@ -483,8 +483,11 @@ __device__ __forceinline__ uint32_t group_reduce_u32(uint32_t x) {
 // pick is (index, score), or (-1, -inf) once the group runs out.  For k <= G
 // lane r keeps round r's pick and lanes 0..k-1 store them together;
 // otherwise lane 0 stores each round's pick.
+// The candidate index of slot s on this lane is ci[s] (distinct over the
+// group's lanes and slots).
 template <int G, int S>
-__device__ __forceinline__ void group_topk(uint32_t (&sb)[S], int lane, int k, int32_t *out_i, float *out_v) {
+__device__ __forceinline__ void group_topk_at(uint32_t (&sb)[S], const uint32_t (&ci)[S], int lane, int k,
+                                              int32_t *out_i, float *out_v) {
     int32_t my_i = -1;
     uint32_t my_m = 0u;
     for (int r = 0; r < k; ++r) {
@@ -494,7 +497,7 @@ __device__ __forceinline__ void group_topk(uint32_t (&sb)[S], int lane, int k, i
         m = group_reduce_u32<G, true>(m);
         uint32_t jm = 0xffffffffu;
 #pragma unroll
-        for (int s = S - 1; s >= 0; --s) jm = sb[s] == m ? (uint32_t)(lane + s * G) : jm;
+        for (int s = S - 1; s >= 0; --s) jm = sb[s] == m && ci[s] < jm ? ci[s] : jm;
         jm = group_reduce_u32<G, false>(jm);
         const int32_t pick = m != 0 ? (int32_t)jm : -1;
         if (k <= G) {  // uniform
@@ -507,12 +510,20 @@ __device__ __forceinline__ void group_topk(uint32_t (&sb)[S], int lane, int k, i
             out_v[r] = m != 0 ? order_bits_inv(m) : -inf_f();
         }
 #pragma unroll
-        for (int s = 0; s < S; ++s) sb[s] = (uint32_t)(lane + s * G) == jm ? 0u : sb[s];
+        for (int s = 0; s < S; ++s) sb[s] = ci[s] == jm ? 0u : sb[s];
     }
     if (k <= G && lane < k) {
         out_i[lane] = my_i;
         out_v[lane] = my_m != 0 ? order_bits_inv(my_m) : -inf_f();
     }
+}
+// Candidate l + s*G on lane l, slot s.
+template <int G, int S>
+__device__ __forceinline__ void group_topk(uint32_t (&sb)[S], int lane, int k, int32_t *out_i, float *out_v) {
+    uint32_t ci[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) ci[s] = (uint32_t)(lane + s * G);
+    group_topk_at<G, S>(sb, ci, lane, k, out_i, out_v);
 }
 
 __device__ __forceinline__ uint32_t topk_bits(float x) { return x > -inf_f() ? order_bits(x) : 0u; }
@@ -1088,12 +1099,40 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
             const float psi0 = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
             if (live) scores[c0 + lane] = psi0;
             uint32_t off = c0 + (uint32_t)D;
+            float psiw[3] = {-inf_f(), -inf_f(), -inf_f()};
 #pragma unroll
             for (int s = 0; s < 3; ++s) {
                 if (s >= nk) break;  // uniform
                 const int k = s + 2;
-                if (lane <= D - k) scores[off + lane] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
+                psiw[s] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
+                if (lane <= D - k) scores[off + lane] = psiw[s];
                 off += (uint32_t)(D - k + 1);
+            }
+            // ---- fused top-k: the group ranks the scores it holds (the same
+            // float values it stored), candidate index = offset within the stage
+            if (a.topk > 0) {  // uniform over the launch
+                const int64_t f = (int64_t)f0 + si;
+                int32_t *ti = a.tk_idx + f * a.topk;
+                float *tv = a.tk_val + f * a.topk;
+                if (__ballot(nk != 0) == 0ull) {  // uniform over the wave: singletons only
+                    uint32_t sb[1] = {live ? topk_bits(psi0) : 0u};
+                    const uint32_t ci[1] = {(uint32_t)lane};
+                    group_topk_at<G, 1>(sb, ci, lane, a.topk, ti, tv);
+                } else {
+                    uint32_t sb[4], ci[4];
+                    sb[0] = live ? topk_bits(psi0) : 0u;
+                    ci[0] = (uint32_t)lane;
+                    uint32_t base_c = (uint32_t)D;
+#pragma unroll
+                    for (int s = 0; s < 3; ++s) {
+                        const int k = s + 2;
+                        const bool has = s < nk && lane <= D - k;
+                        sb[s + 1] = has ? topk_bits(psiw[s]) : 0u;
+                        ci[s + 1] = has ? base_c + (uint32_t)lane : 0xfffffff0u + (uint32_t)s;  // distinct, never picked
+                        base_c += s < nk ? (uint32_t)(D - k + 1) : 0u;
+                    }
+                    group_topk_at<G, 4>(sb, ci, lane, a.topk, ti, tv);
+                }
             }
             continue;
           }
@@ -1238,7 +1277,7 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
     // ---- fused top-k: after the block's scoring, each group ranks a fixed
     // share of its stages, re-reading the scores just written (outside the
     // scoring loop, so it adds no register pressure there)
-    if (a.topk > 0) {  // uniform over the block
+    if (a.topk > 0 && !kSlots) {  // uniform over the block; the slot layout ranks in its loop
         __syncthreads();  // stages were scored by whichever wave claimed them
         constexpr int kRounds = 8;  // a slice holds at most eight rounds of groups
         uint32_t c0[kRounds];
