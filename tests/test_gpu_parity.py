@@ -182,7 +182,7 @@ def test_relabel_singletons_bitwise():
     ("recipe", "shards-1024x500-d16", None, None),
     ("recipe", "forkjoin-4096x1000-d16", None, None),
 ], ids=["windows-d8", "d64", "d7-k0", "shards", "forkjoin"])
-@pytest.mark.parametrize("k", [1, 4, 9])
+@pytest.mark.parametrize("k", [1, 4, 9, 20])
 def test_fused_score_topk_matches_two_calls(case, k):
     """fate_score_topk writes bit-identical scores and top-k to
     fate_score_frontier followed by fate_topk."""
