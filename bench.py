@@ -273,8 +273,8 @@ def sweep_bench(w, k, reps, log):
 
 
 def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
-    """Repeated planning steps on the device (Alg. 1): score the frontier,
-    take each stage's top-k, build one planning wave (fate_plan_wave: each
+    """Repeated planning steps on the device (Alg. 1): score the frontier and
+    take each stage's top-k (one launch), build one planning wave (fate_plan_wave: each
     device at most once per instance), then commit it and advance the
     frontier (fate_commit_advance).  The first ``steps`` steps are timed one
     launch at a time with HIP events; with ``full_plan`` the loop then
@@ -292,8 +292,7 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
     mk = lambda: torch.cuda.Event(enable_timing=True)
 
     def step():
-        fate.fate_score_frontier(pk, st, params, out=scores)
-        fate.fate_topk(st, scores, k, idx=idx, val=val)
+        fate.fate_score_topk(pk, st, params, k, out=scores, idx=idx, val=val)
         fate.fate_plan_wave(st, idx, val, sel=sel)
         fate.fate_commit_advance(pk, st, sel, ws=ws)
 
@@ -302,29 +301,26 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         nF0 = st.counts()[0]
         if nF0 == 0:
             break
-        e = [mk() for _ in range(5)]
+        e = [mk() for _ in range(4)]
         # keep the device busy while the host enqueues the step, so that the
         # first event does not also time the host's call overhead
         torch.cuda._sleep(1000000)
         e[0].record()
-        fate.fate_score_frontier(pk, st, params, out=scores)
+        fate.fate_score_topk(pk, st, params, k, out=scores, idx=idx, val=val)
         e[1].record()
-        fate.fate_topk(st, scores, k, idx=idx, val=val)
-        e[2].record()
         fate.fate_plan_wave(st, idx, val, sel=sel)
-        e[3].record()
+        e[2].record()
         fate.fate_commit_advance(pk, st, sel, ws=ws)
-        e[4].record()
+        e[3].record()
         torch.cuda.synchronize()
         nF1 = st.counts()[0]
         cb = commit_bytes(pk, st, w)
         placed = int(torch.count_nonzero(sel[:nF0] >= 0).item())
-        row = dict(frontier=nF0, placed=placed, next_frontier=nF1, score_ms=e[0].elapsed_time(e[1]),
-                   topk_ms=e[1].elapsed_time(e[2]), plan_ms=e[2].elapsed_time(e[3]),
-                   commit_ms=e[3].elapsed_time(e[4]), commit_bytes=cb)
+        row = dict(frontier=nF0, placed=placed, next_frontier=nF1, score_topk_ms=e[0].elapsed_time(e[1]),
+                   plan_ms=e[1].elapsed_time(e[2]), commit_ms=e[2].elapsed_time(e[3]), commit_bytes=cb)
         rows.append(row)
-        log("planning step %d: frontier %d, placed %d -> %d; score %.4f, top-k %.4f, plan %.4f, commit %.4f ms"
-            % (i, nF0, placed, nF1, row["score_ms"], row["topk_ms"], row["plan_ms"], row["commit_ms"]))
+        log("planning step %d: frontier %d, placed %d -> %d; score + top-k %.4f, plan %.4f, commit %.4f ms"
+            % (i, nF0, placed, nF1, row["score_topk_ms"], row["plan_ms"], row["commit_ms"]))
     out = dict(steps=rows, planner="fate_plan_wave (greedy wave, top-%d choices)" % k)
     timed = rows[1:] or rows  # the first launch of each kernel warms up
     if timed:
@@ -332,10 +328,9 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         cbs = [r["commit_bytes"] for r in timed]
         achieved = float(np.mean(cbs)) / (float(np.mean(cms)) * 1e-3) / 1e9
         out.update(commit_ms_mean=float(np.mean(cms)), plan_ms_mean=float(np.mean([r["plan_ms"] for r in timed])),
-                   step_ms_mean=float(np.mean([r["score_ms"] + r["topk_ms"] + r["plan_ms"] + r["commit_ms"]
-                                               for r in timed])),
+                   step_ms_mean=float(np.mean([r["score_topk_ms"] + r["plan_ms"] + r["commit_ms"] for r in timed])),
                    commit_roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                    "frac": achieved / HBM_PEAK_GBS, "kernels": "fate_commit_advance (5 launches)"})
+                                    "frac": achieved / HBM_PEAK_GBS, "kernels": "fate_commit_advance (6 launches)"})
     if full_plan:
         # the rest of the plan, untimed per launch: one event pair around the whole loop
         n = len(rows)
@@ -347,7 +342,7 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         e1.record()
         torch.cuda.synchronize()
         rest_ms = e0.elapsed_time(e1)
-        total_ms = rest_ms + sum(r["score_ms"] + r["topk_ms"] + r["plan_ms"] + r["commit_ms"] for r in rows)
+        total_ms = rest_ms + sum(r["score_topk_ms"] + r["plan_ms"] + r["commit_ms"] for r in rows)
         arr = fate.state_arrays(st)
         planned = int(np.count_nonzero(arr["status"] == 1) - np.count_nonzero(w.status == 1))
         out["full_plan"] = dict(waves=n, ms=total_ms, stages_planned=planned,
