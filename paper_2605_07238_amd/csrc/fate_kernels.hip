@@ -187,9 +187,17 @@ struct alignas(16) CostS {
 // Byte offsets of every LDS array (shared by the launcher and the kernel).
 struct LdsPlan {
     uint32_t pkey, pmask, rm, rho, fits, wt, cap, order, wait, gpow, next, exec, ksw, stages, entries, total;
+    uint32_t items, parts, left, pbase, pool;  // row splits of heavy stages (64-lane groups)
 };
 
-__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int staging, bool slots) {
+// 64-lane groups: a singletons-only stage with more than kSplitRows
+// descendant rows is scored in parts of kSplitRows rows by several waves of
+// its workgroup; each part's fp64 sums go to a pool slot, and the wave that
+// finishes last adds them in part order and emits.  At most kSplitItems work
+// items and kSplitSlots pool slots per workgroup (later stages stay whole).
+constexpr int kSplitRows = 128, kSplitItems = 256, kSplitSlots = 32;
+
+__host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int staging, bool slots, bool split) {
     LdsPlan q;
     const uint32_t T = 1u << table_log2(D, K);
     const uint32_t mask_bytes = D <= 32 ? 4u : 8u;
@@ -217,6 +225,16 @@ __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int 
     } else {  // [M][D] execution times and weighted switch times
         q.exec = o; o += 4 * (uint32_t)(M * D);
         q.ksw = o; o += 4 * (uint32_t)(M * D);
+    }
+    q.items = q.parts = q.left = q.pbase = q.pool = o;
+    if (split) {  // items (position | part << 8), parts, parts left, first pool slot, then the pool
+        q.items = o; o += 2 * kSplitItems;
+        q.parts = o; o += ((uint32_t)slice + 3u) & ~3u;
+        o = (o + 3u) & ~3u;
+        q.left = o; o += 4 * (uint32_t)slice;
+        q.pbase = o; o += ((uint32_t)slice + 3u) & ~3u;
+        o = (o + 7u) & ~7u;
+        q.pool = o; o += 8 * 64 * kSplitSlots;
     }
     q.total = (o + 15u) & ~15u;
     return q;
@@ -604,7 +622,8 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
     // slot layout: 16-lane groups, uniform beta, at most 32 models (chosen by the launcher)
     constexpr bool kSlots = SLOTS;
     using Entry = EntryL<Mask>;
-    const LdsPlan plan = lds_plan(D, K, M, a.slice, staging_bytes<G>(), SLOTS);
+    constexpr bool kSplit = G == 64 && !SLOTS;
+    const LdsPlan plan = lds_plan(D, K, M, a.slice, staging_bytes<G>(), SLOTS, kSplit);
 
     Lds L;
     L.logT = table_log2(D, K);
@@ -724,6 +743,24 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
     }
     __syncthreads();  // the sort keys' space becomes staging slots; the prefix table is built
     for (int i = tid; i < nF; i += kBlock) L.stages[i].pfm = (uint64_t)table_find<Mask>(L, L.stages[i].hash);
+    if (kSplit && tid == kBlock - 1) {  // work items in rank order; heavy singletons-only stages in parts
+        uint16_t *items = reinterpret_cast<uint16_t *>(sb + plan.items);
+        uint8_t *parts = sb + plan.parts, *pbase = sb + plan.pbase;
+        uint32_t *left = reinterpret_cast<uint32_t *>(sb + plan.left);
+        int ni = 0, used = 0;
+        for (int pos = 0; pos < nF; ++pos) {
+            const StageL &st = L.stages[L.order[pos]];
+            const int ne = (int)(st.e1 - st.e0);
+            int np = st.nc == (uint32_t)D && ne > kSplitRows ? (ne + kSplitRows - 1) / kSplitRows : 1;
+            if (np > 1 && (used + np > kSplitSlots || ni + np + (nF - 1 - pos) > kSplitItems)) np = 1;
+            parts[pos] = (uint8_t)np;
+            left[pos] = (uint32_t)np;
+            pbase[pos] = (uint8_t)used;
+            if (np > 1) used += np;
+            for (int q = 0; q < np; ++q) items[ni++] = (uint16_t)(pos | (q << 8));
+        }
+        L.next[1] = (uint32_t)ni;
+    }
     __syncthreads();
 
     constexpr int kGroups = kBlock / G;
@@ -749,13 +786,18 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
     // that finishes early takes the next chunk (list scheduling).
     constexpr int kGpw = 64 / G;  // lane groups per wave
     const int gw = (tid & 63) / G;
-    const int nchunks = (nF + kGpw - 1) / kGpw;
+    const int nchunks = kSplit ? (int)L.next[1] : (nF + kGpw - 1) / kGpw;
     for (;;) {
         uint32_t chunk = 0;
         if ((tid & 63) == 0) chunk = atomicAdd(L.next, 1u);
         chunk = __builtin_amdgcn_readfirstlane(chunk);
         if ((int)chunk >= nchunks) break;  // uniform within the wave
-        const int pos = (int)chunk * kGpw + gw;
+        int pos = (int)chunk * kGpw + gw, part = 0;
+        if constexpr (kSplit) {  // one group per wave: the work item names the position and part
+            const uint32_t item = reinterpret_cast<const uint16_t *>(sb + plan.items)[chunk];
+            pos = (int)(item & 0xffu);
+            part = (int)(item >> 8);
+        }
         if (pos >= nF) continue;  // the last chunk may be partial
         const int si = (int)L.order[pos];
         const StageL sv = L.stages[si];
@@ -1180,8 +1222,11 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
             w_j0[s] = tmax + lam_tr * gat;
         }
 
-        // ---- horizon descendants, G at a time
-        for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
+        // ---- horizon descendants, G at a time (a part of a heavy stage: its kSplitRows rows)
+        const int nparts = kSplit ? (int)(sb + plan.parts)[pos] : 1;
+        const uint32_t b_lo = sv.e0 + (uint32_t)(part * kSplitRows);
+        const uint32_t b_hi = nparts > 1 ? min(sv.e1, b_lo + (uint32_t)kSplitRows) : sv.e1;
+        for (uint32_t base = b_lo; base < b_hi; base += G) {  // uniform; kSplitRows is a multiple of G
             const int nb = stage_batch(base);
             int jj = 0;
             if (UNI && wslots == 0) {  // singletons only: two descendants per iteration
@@ -1261,7 +1306,19 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
             wave_sync();  // the next batch overwrites the staging slots
             if (nb < G) break;  // past the horizon depth or the list end
         }
-
+        if (kSplit && nparts > 1) {  // uniform: the part's sum to its slot; the last part's wave emits
+            double *pool = reinterpret_cast<double *>(sb + plan.pool);
+            const int slot0 = (int)(sb + plan.pbase)[pos];
+            pool[(slot0 + part) * 64 + lane] = acc0;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            uint32_t before = 0;
+            if (lane == 0) before = atomicSub(reinterpret_cast<uint32_t *>(sb + plan.left) + pos, 1u);
+            before = __builtin_amdgcn_readfirstlane(before);
+            if (before != 1u) continue;  // another part is still being scored
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            acc0 = 0.0;
+            for (int q = 0; q < nparts; ++q) acc0 += pool[(slot0 + q) * 64 + lane];
+        }
 
         // ---- emit scores
         const float psi0 = feas_v ? (float)(-((double)j0_single + acc0)) : -inf_f();
@@ -1338,7 +1395,7 @@ static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
     const int G = group_width(a.D);
     const int sb = G == 16 ? staging_bytes<16>() : G <= 32 ? staging_bytes<8>() : staging_bytes<64>();
     const bool slots = UNI && G == 16 && a.M <= 32;  // the kernel choice below
-    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb, slots).total;
+    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb, slots, G == 64 && !slots).total;
     const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block(score_block(G));
     bool var = a.topo != 0;
     for (int p = 0; p < a.nsets; ++p) var = var || a.ps[p].lam_m != 0.0f || a.ps[p].flags != 0;

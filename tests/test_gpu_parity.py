@@ -92,6 +92,31 @@ def test_random_small_parity(case):
     check_against_oracle(w, g, H=H, max_shard=ms, k=5)
 
 
+def test_heavy_stages_scored_in_parts():
+    """64 devices: a singletons-only frontier stage with more than 128 horizon
+    rows is scored in parts by several waves of its workgroup, whose sums the
+    last one adds in part order; scores against the oracle, fused and two-call
+    bits equal (run_gpu), and the same bits on a second run."""
+    from paper_2605_07238_amd import fate
+    w = synth.make_workload("powerlaw-256x10000-d64", B=6)
+    buf, h, _ = fate.fate_layout_dags(w)
+    base, N = buf.ctypes.data, int(h.N)
+    doff = np.frombuffer(buf, np.uint32, N + 1, h.desc_off - base).astype(np.int64)
+    npar = np.diff(w.par_off)
+    inst = np.repeat(np.arange(w.B), np.diff(w.stage_off))
+    pg = w.par_idx.astype(np.int64) + w.stage_off[np.repeat(inst, npar)]
+    ndone = np.add.reduceat((w.status[pg] == 1).astype(np.int64), w.par_off[:-1])
+    ndone[npar == 0] = 0
+    fv = np.nonzero((w.status == 0) & (ndone == npar))[0]
+    rows = doff[fv + 1] - doff[fv]
+    print("[gpu] heavy stages: max rows", int(rows.max()), "stages over 128:", int((rows > 128).sum()), flush=True)
+    assert (rows > 128).sum() >= 2
+    g = run_gpu(w)
+    check_against_oracle(w, g)
+    g2 = run_gpu(w)
+    assert np.array_equal(g["psi"].view(np.uint32), g2["psi"].view(np.uint32))
+
+
 @pytest.mark.parametrize("H", [0, 1, 2])
 def test_smaller_horizon_than_packed(H):
     w = synth.make_random_small(21, B=2, n=16, D=6, H=3)
