@@ -92,13 +92,20 @@ def test_random_small_parity(case):
     check_against_oracle(w, g, H=H, max_shard=ms, k=5)
 
 
-def test_heavy_stages_scored_in_parts():
+@pytest.mark.parametrize("beta", ["uniform", "asymmetric"])
+def test_heavy_stages_scored_in_parts(beta):
     """64 devices: a singletons-only frontier stage with more than 128 horizon
     rows is scored in parts by several waves of its workgroup, whose sums the
     last one adds in part order; scores against the oracle, fused and two-call
-    bits equal (run_gpu), and the same bits on a second run."""
+    bits equal (run_gpu), and the same bits on a second run.  With an
+    asymmetric beta the non-uniform kernel instance takes the same path."""
     from paper_2605_07238_amd import fate
     w = synth.make_workload("powerlaw-256x10000-d64", B=6)
+    if beta == "asymmetric":
+        rng = np.random.default_rng(5)
+        b = (w.beta.astype(np.float64) * rng.uniform(0.5, 2.0, size=w.beta.shape)).astype(np.float32)
+        np.fill_diagonal(b, 0.0)
+        w = dataclasses.replace(w, beta=b)
     buf, h, _ = fate.fate_layout_dags(w)
     base, N = buf.ctypes.data, int(h.N)
     doff = np.frombuffer(buf, np.uint32, N + 1, h.desc_off - base).astype(np.int64)
