@@ -196,6 +196,7 @@ struct LdsPlan {
 // finishes last adds them in part order and emits.  At most kSplitItems work
 // items and kSplitSlots pool slots per workgroup (later stages stay whole).
 constexpr int kSplitRows = 128, kSplitItems = 256, kSplitSlots = 32;
+static_assert(kSplitRows % 64 == 0, "a part is whole 64-row batches");
 
 __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int staging, bool slots, bool split) {
     LdsPlan q;
