@@ -11,7 +11,12 @@ Kinds of pins used here:
 * closed-form reductions computed with numpy and scipy's breadth-first
   shortest paths (only base runtimes, or only waiting costs, switched on);
 * invariants: device relabelling, H = 0 equals gamma = 0, stages outside the
-  horizon do not matter, an added isolated stage changes nothing else.
+  horizon do not matter, an added isolated stage changes nothing else;
+* the magnitude A that every parity tolerance divides by: hand-derived values,
+  A >= |Psi|, and A = |Psi| exactly when no benefit term enters;
+* an independent brute-force evaluation (tests/brute.py): materialised
+  post-states, costs from scratch, joint enumeration of the horizon stages'
+  placements, and the GPU kernel's outside / inside rearrangement.
 """
 
 from __future__ import annotations
@@ -24,6 +29,7 @@ import numpy as np
 import scipy.sparse as sp
 from scipy.sparse.csgraph import shortest_path
 
+import brute
 import builders
 import scenarios
 from oracle import oracle
@@ -48,6 +54,8 @@ def check_scenario(name: str, lib=None):
     r = oracle.score(w, lib=lib)
     assert list(r["front_v"]) == sc["front_v"], (list(r["front_v"]), sc["front_v"])
     _close(r["psi"], sc["psi"], rtol=1e-12)
+    if "mag" in sc:
+        _close(r["mag"], sc["mag"], rtol=1e-12)
     if "topk3" in sc:
         idx, _ = oracle.topk(r, 3, lib=lib)
         assert idx[0].tolist() == sc["topk3"], idx
@@ -65,6 +73,7 @@ def check_worked_example(lib=None):
         assert list(r["front_v"]) == exp["front_v"]
         # inputs such as 1.1 s are float32-rounded, hence 1e-6
         _close(r["psi"], exp["psi"], rtol=1e-6, atol=0)
+        _close(r["mag"], exp["mag"], rtol=1e-6, atol=0)
         idx, _ = oracle.topk(r, 3, lib=lib)
         assert idx[0].tolist() == exp["topk3"], idx
 
@@ -295,6 +304,45 @@ def check_isolated_stage(seed: int, lib=None):
     F = len(r0["front_v"])
     assert list(r1["front_v"][:F]) == list(r0["front_v"]) and r1["front_v"][F] == n
     assert np.array_equal(r1["psi"][:len(r0["psi"])], r0["psi"])
+
+
+def check_mag_bounds(seed: int, lib=None):
+    """A >= |Psi| for every finite score (triangle inequality over the terms
+    that were added).  With the benefit weights (colocation, prefix) at zero
+    every term is a cost, so A = |Psi| up to rounding: a slip that adds a term
+    to A twice, weights a horizon stage without gamma^depth, or takes the
+    terms of more than one device breaks the equality."""
+    w = synth.make_random_small(seed, B=3, n=14, D=5, M=3, K=2, H=3, max_shard=3, shard_frac=0.6)
+    r = oracle.score(w, lib=lib)
+    fin = np.isfinite(r["psi"])
+    assert fin.sum() > 10
+    assert np.all(r["mag"][fin] >= np.abs(r["psi"][fin]) * (1 - 1e-14)), "A below |Psi|"
+    assert np.all(r["mag"][~fin] == 0.0)
+    costs = oracle.score(w, params=dict(lam_c=0.0, lam_p=0.0), lib=lib)
+    fin = np.isfinite(costs["psi"])
+    _close(costs["mag"][fin], np.abs(costs["psi"][fin]), rtol=1e-14, atol=0)
+    # and some candidate's A exceeds |Psi| once the benefits are back
+    assert np.any(r["mag"][fin] > np.abs(r["psi"][fin]) * (1 + 1e-9))
+
+
+def check_brute_force(group: int, lib=None, per_group: int = 10):
+    """Scores and magnitudes of the oracle equal tests/brute.py's on tiny
+    seeded DAGs (windows, multi-device holders, running and committed stages,
+    asymmetric and uniform beta) at 1e-12: the post-state materialised by an
+    independent state update and priced from scratch, the horizon enumerated
+    jointly over every placement of its stages, and the GPU kernel's
+    outside / inside rearrangement (brute.py asserts the three agree)."""
+    cases = list(brute.tiny_cases(5 * per_group))[group * per_group:(group + 1) * per_group]
+    n_fin = 0
+    for seed, w, H, ms in cases:
+        psi, mag, front = brute.score(w, H=H, max_shard=ms)
+        r = oracle.score(w, H=H, max_shard=ms, lib=lib)
+        assert [(b, v) for b, v, _ in front] == list(zip(r["front_b"].tolist(), r["front_v"].tolist())), seed
+        _close(r["psi"], psi, rtol=1e-12, atol=1e-12)
+        fin = np.isfinite(psi)
+        _close(r["mag"][fin], mag[fin], rtol=1e-12, atol=1e-12)
+        n_fin += int(fin.sum())
+    assert n_fin > 0
 
 
 def check_commit_scenario(name: str, lib=None):
@@ -697,6 +745,8 @@ ALL_CHECKS = (
     + [("relabel:%d" % s, (lambda s: lambda lib: check_relabel_singletons(s, lib))(s)) for s in range(2)]
     + [("reversal:%d" % s, (lambda s: lambda lib: check_reversal_windows(s, lib))(s)) for s in range(2)]
     + [("h0_gamma0:%d" % s, (lambda s: lambda lib: check_h0_equals_gamma0(s, lib))(s)) for s in range(2)]
+    + [("mag_bounds:%d" % s, (lambda s: lambda lib: check_mag_bounds(s, lib))(s)) for s in range(3)]
+    + [("brute_force:%d" % g, (lambda g: lambda lib: check_brute_force(g, lib))(g)) for g in range(5)]
     + [("truncation:%d" % s, (lambda s: lambda lib: check_truncation(s, lib))(s)) for s in range(3)]
     + [("isolated:%d" % s, (lambda s: lambda lib: check_isolated_stage(s, lib))(s)) for s in range(2)]
     + [("commit:" + k, (lambda k: lambda lib: check_commit_scenario(k, lib))(k)) for k in scenarios.COMMITS]

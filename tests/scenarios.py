@@ -10,6 +10,13 @@ lam_c = 1/8, kappa_prefix = 2^-10) so every expected value is exact in fp64
 Each scenario is chosen so that a plausible slip (dropped term, wrong sign,
 transposed transfer coefficient, wrong divisor, wrong eviction order, wrong
 depth weight, missing de-duplication, ...) changes at least one number.
+
+Where a scenario lists ``mag``, those are the hand-derived magnitudes A that
+the parity tolerance divides by: the absolute values of the weighted terms
+of the device that sets the immediate cost (the maximising shard device,
+plus the gather term), plus gamma^depth times the absolute terms of the
+device that gives each horizon stage its value (the minimising device).
+A equals |Psi| when no benefit term (colocation, prefix, same model) enters.
 """
 
 from __future__ import annotations
@@ -20,12 +27,13 @@ P = dict(lam_c=0.125, kappa_prefix=2.0 ** -10)
 # A: waiting cost is clamped at zero; switch only when the model is absent.
 #   d0: wait max(0, 0.25-1) = 0, exec 1.0, m0 resident            -> 1.0
 #   d1: wait 2-1 = 1, exec 0.5, switch 0.75                         -> 2.25
+#   A: every term is a cost, so A = |Psi| = 1.0, 2.25.
 WAIT_SWITCH = dict(
     spec=dict(D=2, M=1, K=1, exec=[[1.0, 0.5]], switch_s=[[0.75, 0.75]], weight_gb=[10], cap_gb=[20, 20],
               beta=[[0, 0], [0, 0]],
               instances=[dict(parents=[[]], model=[0], elig=[3], out_bytes=[1.0], status=[0], holders=[0],
                               resident=[1, 0], tau_free=[0.25, 2.0], t_now=1.0)]),
-    H=0, params=P, front_v=[0], psi=[-1.0, -2.25])
+    H=0, params=P, front_v=[0], psi=[-1.0, -2.25], mag=[1.0, 2.25])
 
 # B: transfer uses beta[from][to], the cheapest of several holders, and
 #    colocation counts the fraction of parents held on the device.
@@ -34,6 +42,8 @@ WAIT_SWITCH = dict(
 #       J0 = 1 + 0.5 - 1/16 = 1.4375
 #   d1: u0 -> 2^32 * beta[0][1] (2^-32) = 1.0; colo 1/2  -> 1.9375
 #   d2: u0 -> 2^32 * beta[0][2] (2^-31) = 2.0; colo 1/2  -> 2.9375
+#   A adds the colocation benefit 1/16 instead of taking it off:
+#   1 + 0.5 + 1/16 = 1.5625, 1 + 1 + 1/16 = 2.0625, 1 + 2 + 1/16 = 3.0625.
 _B_BETA = [[0.0, 2.0 ** -32, 2.0 ** -31],
            [2.0 ** -30, 0.0, 2.0 ** -33],
            [2.0 ** -31, 2.0 ** -34, 0.0]]
@@ -43,7 +53,7 @@ TRANSFER_COLO = dict(
               instances=[dict(parents=[[], [], [0, 1]], model=[0, 0, 0], elig=[7, 7, 7],
                               out_bytes=[2.0 ** 32, 2.0 ** 30, 1.0], status=[1, 1, 0], holders=[1, 6, 0],
                               resident=[1, 1, 1], tau_free=[0.0, 0.0, 0.0], t_now=0.0)]),
-    H=0, params=P, front_v=[2], psi=[-1.4375, -1.9375, -2.9375])
+    H=0, params=P, front_v=[2], psi=[-1.4375, -1.9375, -2.9375], mag=[1.5625, 2.0625, 3.0625])
 
 # C: shard windows.  Per device (wait, exec, switch, transfer, colo, prefix):
 #   d0: (2.0, 1.0, 0,   0,   1, 0)    d1: (0, 2.0, 0.5, 0.5, 0, 0)
@@ -55,6 +65,11 @@ TRANSFER_COLO = dict(
 #   {0,1,2}: max(2 + 1/3 - 1/8, 2/3 + 1/2 + 1/6, 4/3 + 1/2 + 1/6) + G
 #            G = min over p of the column sum into p times sigma/3
 #              = min(1.25, 0.75, 0.625) = 0.625               -> 2.833333...
+#   A, from the device that sets the maximum, plus the gather term:
+#   k=1: d0 2 + 1 + 1/8 = 3.125; d1 3.0; d2 4 + 0.5 + 1 + 0.5 = 6.0
+#   {0,1}: d0 (2.375 > 1.75): 2 + 0.5 + 1/8 = 2.625, + 0.375 = 3.0
+#   {1,2}: d2 (2.75 > 1.75): 2 + 0.5 + 0.5 + 0.25 = 3.25, + 0.1875 = 3.4375
+#   {0,1,2}: d0 (2.2083 > 2.0 > 1.3333): 2 + 1/3 + 1/8, + 0.625 = 3 + 1/12
 _C_BETA = [[0.0, 2.0 ** -33, 2.0 ** -32],
            [2.0 ** -31, 0.0, 2.0 ** -34],
            [2.0 ** -33, 2.0 ** -32, 0.0]]
@@ -68,6 +83,7 @@ WINDOWS = dict(
                               tau_free=[3.0, 1.0, 1.0], t_now=1.0)]),
     H=0, params=P, front_v=[1],
     psi=[-2.875, -3.0, -5.0, -2.75, -2.9375, -(2.0 + 1.0 / 3.0 - 0.125 + 0.625)],
+    mag=[3.125, 3.0, 6.0, 3.0, 3.4375, 2.0 + 1.0 / 3.0 + 0.125 + 0.625],
     topk3=[3, 5, 0])
 
 # D: post-state seen by the descendants.
@@ -85,6 +101,10 @@ WINDOWS = dict(
 #     w1: d0 = 1 + 1.0 = 2.0; d1 = 1 + 0.25 - 1/16 - 0.5 = 0.6875
 #     w2: d0 = 1 + 1.0 = 2.0; d1 = 1 - 1/8 = 0.875
 #     J = 1.375 + 0.78125 = 2.15625
+#   A: immediate d0 1 + 0.5 + 0.5 = 2.0 (no benefit); d1 1 + 0.5 + 1/8 = 1.625.
+#     Horizon (same minimising devices as above, each term's absolute value):
+#     w1 1 + 0.25 + 1/16 + 0.5 = 1.8125, w2 1 + 1/8 = 1.125, times 0.5: 1.46875.
+#     A = 3.46875 (v on d0), 3.09375 (v on d1); at H = 0: 2.0, 1.625.
 _UNI = [[0.0, 2.0 ** -32], [2.0 ** -32, 0.0]]
 POST_STATE = dict(
     spec=dict(D=2, M=3, K=1, exec=[[1.0, 1.0]] * 3, switch_s=[[0.25, 0.25], [0.5, 0.5], [1.0, 1.0]],
@@ -95,8 +115,8 @@ POST_STATE = dict(
                               status=[1, 0, 2, 0, 0], holders=[2, 0, 0, 0, 0],
                               resident=[5, 4], prefix_cache=[[0], [0]],
                               tau_free=[1.0, 1.0], t_now=1.0)]),
-    H=1, params=P, front_v=[1], psi=[-2.78125, -2.15625])
-POST_STATE_H0 = dict(POST_STATE, H=0, psi=[-2.0, -1.375])
+    H=1, params=P, front_v=[1], psi=[-2.78125, -2.15625], mag=[3.46875, 3.09375])
+POST_STATE_H0 = dict(POST_STATE, H=0, psi=[-2.0, -1.375], mag=[2.0, 1.625])
 
 # E: horizon set = breadth-first levels 1..H, each stage once at its minimum
 #    distance; descendants use only their feasible devices.  Only base
@@ -104,6 +124,7 @@ POST_STATE_H0 = dict(POST_STATE, H=0, psi=[-2.0, -1.375])
 #    Levels from v: {a, b, f} at 1, {c} at 2, {e} at 3 (f is also a child of c).
 #    H=2: J(d0) = 1 + 0.5*3 + 0.25*2 = 3.0; J(d1) = 4.0
 #    H=3: plus 0.125*1 for e.
+#    Only costs enter, so A = |Psi|.
 _E_P = dict(lam_c=0.0, kappa_prefix=0.0)
 HORIZON_SET = dict(
     spec=dict(D=2, M=1, K=1, exec=[[1.0, 2.0]], switch_s=[[0.0, 0.0]], weight_gb=[10], cap_gb=[20, 20],
@@ -112,8 +133,8 @@ HORIZON_SET = dict(
                               elig=[3, 3, 3, 3, 2, 3, 3], out_bytes=[1.0] * 7,
                               status=[1, 0, 0, 0, 0, 0, 0], holders=[1, 0, 0, 0, 0, 0, 0],
                               resident=[1, 1], tau_free=[0.0, 0.0], t_now=0.0)]),
-    H=2, params=_E_P, front_v=[1], psi=[-3.0, -4.0])
-HORIZON_SET_H3 = dict(HORIZON_SET, H=3, psi=[-3.125, -4.125])
+    H=2, params=_E_P, front_v=[1], psi=[-3.0, -4.0], mag=[3.0, 4.0])
+HORIZON_SET_H3 = dict(HORIZON_SET, H=3, psi=[-3.125, -4.125], mag=[3.125, 4.125])
 
 # F: feasibility needs eligibility and capacity; top-k skips -inf, breaks
 #    ties by candidate index and pads with (-1, -inf).

@@ -51,6 +51,17 @@ MUTANTS = {
     "descendant_max_device": [("if (val < vbest) { vbest = val; vmag = m_; }",
                                "if (vbest == INFINITY || val > vbest) { vbest = val; vmag = m_; }")],
     "prefix_sign": [("return c + t_sw + t_tr - t_co - t_pf - t_sm;", "return c + t_sw + t_tr - t_co + t_pf - t_sm;")],
+    # the magnitude A that parity tolerances divide by
+    "mag_gamma_dropped": [("A += gw_pow * vmag;", "A += vmag;")],
+    "mag_all_horizon_devices": [("if (val < vbest) { vbest = val; vmag = m_; }",
+                                 "vmag += m_;\n                    if (val < vbest) vbest = val;")],
+    "mag_all_shard_devices": [("best_mag = fabs(a_q) + fabs(a_c)", "best_mag += fabs(a_q) + fabs(a_c)")],
+    "mag_gather_twice": [("double A = best_mag + fabs(in->lam_tr * gsum);",
+                          "double A = best_mag + 2.0 * fabs(in->lam_tr * gsum);")],
+    "mag_horizon_max_device": [("if (val < vbest) { vbest = val; vmag = m_; }",
+                                "if (val < vbest) vbest = val;\n                    if (m_ > vmag) vmag = m_;")],
+    "mag_signed_benefit": [("if (mag) *mag = fabs(c) + fabs(t_sw) + fabs(t_tr) + fabs(t_co) + fabs(t_pf) + fabs(t_sm);",
+                            "if (mag) *mag = fabs(c) + fabs(t_sw) + fabs(t_tr) - fabs(t_co) - fabs(t_pf) + fabs(t_sm);")],
     # commit-and-advance
     "commit_start_ignores_now": [("double start = tau_out[bd] > (double)in->t_now[b] ? tau_out[bd] : (double)in->t_now[b];",
                                   "double start = tau_out[bd];")],
