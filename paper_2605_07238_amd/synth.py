@@ -17,7 +17,10 @@ state s_t; App. C.1 proxies for runtime, switch, transfer and prefix reuse):
 * The state is what a random partial execution of 30% of the stages leaves
   behind: resident-model bitmasks per device, a K-slot prefix ring per device,
   device bitmasks holding each completed stage's output, device free times and
-  the current time t = min_d tau_d.
+  the current time t = min_d tau_d.  Every stage that is ready afterwards is
+  pending, so the frontier is the whole ready set.  On request
+  (``mark_statuses``) a share of the ready stages is marked running or
+  committed instead, which exercises the frontier rule of App. A.1 at scale.
 
 Randomness: instance b of a recipe draws from
 ``Generator(PCG64(SeedSequence([seed, b])))`` so its data does not depend on
@@ -311,7 +314,7 @@ def _bits(mask: int) -> List[int]:
     return out
 
 
-def _gen_instance(rc: dict, cluster, seed: int, b: int, K: int, max_shard: int):
+def _gen_instance(rc: dict, cluster, seed: int, b: int, K: int, max_shard: int, mark_statuses: bool = False):
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, b])))
     D, M = rc["D"], rc["M"]
     exec_, switch, weight, cap, _beta = cluster
@@ -438,13 +441,15 @@ def _gen_instance(rc: dict, cluster, seed: int, b: int, K: int, max_shard: int):
             remaining[c] -= 1
             if remaining[c] == 0:
                 ready.append(c)
-    # some ready stages are already running or committed (App. A.1)
-    for v in ready:
-        u = rng.random()
-        if u < COMMON["p_running"]:
-            status[v] = RUNNING
-        elif u < COMMON["p_running"] + COMMON["p_committed"]:
-            status[v] = COMMITTED
+    # on request, some ready stages are already running or committed
+    # (App. A.1); these draws come last, so nothing else depends on them
+    if mark_statuses:
+        for v in ready:
+            u = rng.random()
+            if u < COMMON["p_running"]:
+                status[v] = RUNNING
+            elif u < COMMON["p_running"] + COMMON["p_committed"]:
+                status[v] = COMMITTED
 
     tau_a = np.array(tau, np.float32)
     t_now = np.float32(tau_a.min()) if D else np.float32(0)
@@ -488,18 +493,20 @@ def _assemble(name: str, rc: dict, cluster, insts: List[dict], K: int, max_shard
 
 
 def _gen_range(args):
-    name, rc, seed, lo, hi, K, max_shard = args
+    name, rc, seed, lo, hi, K, max_shard, mark = args
     cluster = make_cluster(rc, seed)
-    return [_gen_instance(rc, cluster, seed, b, K, max_shard) for b in range(lo, hi)]
+    return [_gen_instance(rc, cluster, seed, b, K, max_shard, mark) for b in range(lo, hi)]
 
 
 def make_workload(name: str, B: Optional[int] = None, instances: Optional[Sequence[int]] = None,
-                  seed: Optional[int] = None, workers: int = 1) -> Workload:
+                  seed: Optional[int] = None, workers: int = 1, mark_statuses: bool = False) -> Workload:
     """Build a recipe's workload.
 
     ``B`` truncates the batch to its first B instances; ``instances`` picks
     explicit instance ids (their data equals that of the full batch).
     ``workers`` > 1 spreads instance generation over forked processes.
+    ``mark_statuses`` marks 10% of the ready stages running and 5% committed
+    (off for the recipes themselves: their frontier is every ready stage).
     """
     rc = dict(RECIPES[name])
     seed = rc["seed"] if seed is None else seed
@@ -511,14 +518,14 @@ def make_workload(name: str, B: Optional[int] = None, instances: Optional[Sequen
         chunks = []
         step = max(1, (len(ids) + workers * 4 - 1) // (workers * 4))
         for lo in range(0, len(ids), step):
-            chunks.append((name, rc, seed, lo, min(len(ids), lo + step), K, max_shard))
+            chunks.append((name, rc, seed, lo, min(len(ids), lo + step), K, max_shard, mark_statuses))
         ctx = mp.get_context("fork")
         with ctx.Pool(workers) as pool:
             parts = pool.map(_gen_range, chunks)
         insts = [it for part in parts for it in part]
     else:
-        insts = [_gen_instance(rc, cluster, seed, b, K, max_shard) for b in ids]
-    return _assemble(name, rc, cluster, insts, K, max_shard)
+        insts = [_gen_instance(rc, cluster, seed, b, K, max_shard, mark_statuses) for b in ids]
+    return _assemble(name + ("+statuses" if mark_statuses else ""), rc, cluster, insts, K, max_shard)
 
 
 # ---------------------------------------------------------------------------
