@@ -8,12 +8,22 @@ depth-H horizon) and ranks each stage's top-k; --two-calls times
 fate_score_frontier then fate_topk instead.  Packing (host validation, layout and the
 host-to-device copy) is done once before timing and reported separately.
 
+The timed steps rotate through --copies independently packed copies of the
+DAGs and the state (default 3, about 3 x 170 MB touched per launch on the
+fork-join batch), so that no launch finds its inputs in the 256 MB Infinity
+Cache that the previous launch filled; the same launches repeated on one copy
+are timed as well and reported as the warm figure.
+
 Prints one JSON line (rank 0, N=1):
   value          candidate-horizon evaluations per second over the timed steps;
                  one evaluation per feasible candidate and per (feasible
                  candidate, horizon descendant) pair
   roofline       the score kernel's algorithmic bytes per launch / its average
-                 launch time (HIP events on the launch stream) vs 8 TB/s HBM
+                 launch time over rotated copies (HIP events on the launch
+                 stream) vs 8 TB/s HBM
+  roofline_valu  VALU wave-instructions per launch (rocprofv3 SQ_INSTS_VALU in
+                 the committed profile of the same kernel source) / the same
+                 launch time vs 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles
   cpu_baseline   the fp64 oracle timed on this host's cores over the same batch
 """
 
@@ -34,6 +44,9 @@ if ROOT not in sys.path:
 
 DEFAULT_WORKLOAD = "forkjoin-4096x1000-d16"
 HBM_PEAK_GBS = 8000.0
+# VALU issue: 256 CUs x 4 SIMDs x 2.4 GHz, one wave64 instruction per SIMD every
+# 4 cycles (16 lanes wide), in G wave-instructions per second
+VALU_PEAK_GIPS = 256 * 4 * 2.4 / 4.0
 METRIC = "candidate-horizon evaluations/sec and achieved HBM GB/s (fraction of peak)"
 # the score kernel and the header that fixes its launch geometry (slice length)
 KERNEL_SRC = [os.path.join(ROOT, "paper_2605_07238_amd", "csrc", f) for f in ("fate_kernels.hip", "fate_internal.h")]
@@ -102,23 +115,31 @@ def counted_work(w, pk, st, scores_host, H):
                                                             per_stage=per_stage, stage_inst=fb)
 
 
-def read_traffic(workload: str):
-    """HBM traffic of the score kernel from committed rocprofv3 counter runs,
-    if they were taken on the current kernel source."""
+def read_counters(workload: str):
+    """HBM traffic and VALU instructions per launch of the score kernel from
+    the committed rocprofv3 counter runs, if they were taken on the current
+    kernel source: (hbm bytes or None, SQ_INSTS_VALU or None)."""
     path = os.path.join(ROOT, "profiles", "k_score_%s_counters.txt" % workload)
     if not os.path.exists(path):
-        return None
+        return None, None
     vals = {}
+    valu = None
     for line in open(path):
-        if ":" in line and not line.startswith("#"):
+        if line.startswith("counter SQ_INSTS_VALU"):
+            try:
+                valu = float(line.rsplit(":", 1)[1])
+            except ValueError:
+                valu = None
+        elif ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     if vals.get("kernel_source_sha256") != kernel_sha():
-        return None
+        return None, None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        hbm = float(vals["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
-        return None
+        hbm = None
+    return hbm, valu
 
 
 def host_info():
@@ -489,6 +510,10 @@ def main():
                          "(lets profiled runs skip the forked generator)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one plain device copy of 512 MiB (counter calibration)")
+    ap.add_argument("--copies", type=int, default=3,
+                    help="independently packed copies of the DAGs and state the timed steps rotate through")
+    ap.add_argument("--no-warm", action="store_true",
+                    help="skip timing repeated launches on one copy (profiling runs: every launch rotates)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the scoring path has no cross-GPU step "
@@ -519,81 +544,107 @@ def main():
     torch.cuda.set_device(0)
     fate.load()
     H = w.H
-    t0 = time.perf_counter()
-    pk = fate.fate_pack_dags(w, H=H)
-    t_pack_dags = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    st = fate.fate_pack_state(pk, w)
-    t_pack_state = time.perf_counter() - t0
-    log("packed: dags %.2fs (%.1f MB), state %.2fs (%.1f MB); %d frontier stages, %d candidates"
-        % (t_pack_dags, pk.handle.bytes / 1e6, t_pack_state, st.handle.bytes / 1e6, st.n_frontier, st.n_cand))
+    R = max(1, args.copies)
+    copies = []
+    t_pack_dags = t_pack_state = 0.0
+    for c in range(R):  # independently packed copies: separate device buffers, same contents
+        t0 = time.perf_counter()
+        pk_c = fate.fate_pack_dags(w, H=H)
+        t_pack_dags = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        st_c = fate.fate_pack_state(pk_c, w)
+        t_pack_state = time.perf_counter() - t0
+        copies.append(dict(
+            pk=pk_c, st=st_c, scores=torch.empty(max(1, st_c.n_cand), dtype=torch.float32, device="cuda"),
+            idx=torch.empty((max(1, st_c.n_frontier), args.topk), dtype=torch.int32, device="cuda"),
+            val=torch.empty((max(1, st_c.n_frontier), args.topk), dtype=torch.float32, device="cuda")))
+    pk, st = copies[0]["pk"], copies[0]["st"]
+    scores, idx, val = copies[0]["scores"], copies[0]["idx"], copies[0]["val"]
+    log("packed %d copies: dags %.2fs (%.1f MB), state %.2fs (%.1f MB) each; %d frontier stages, %d candidates"
+        % (R, t_pack_dags, pk.handle.bytes / 1e6, t_pack_state, st.handle.bytes / 1e6, st.n_frontier, st.n_cand))
     params = fate.make_params(w, H=H)
-    scores = torch.empty(max(1, st.n_cand), dtype=torch.float32, device="cuda")
-    idx = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.int32, device="cuda")
-    val = torch.empty((max(1, st.n_frontier), args.topk), dtype=torch.float32, device="cuda")
 
     args.fused = not args.two_calls
-    if args.fused:
-        def step():
-            fate.fate_score_topk(pk, st, params, args.topk, out=scores, idx=idx, val=val)
-    else:
-        def step():
-            fate.fate_score_frontier(pk, st, params, out=scores)
-            fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
 
-    for _ in range(args.warmup):
-        step()
+    def score_call(c):
+        x = copies[c]
+        if args.fused:
+            fate.fate_score_topk(x["pk"], x["st"], params, args.topk, out=x["scores"], idx=x["idx"], val=x["val"])
+        else:
+            fate.fate_score_frontier(x["pk"], x["st"], params, out=x["scores"])
+
+    def topk_call(c):
+        x = copies[c]
+        if not args.fused:
+            fate.fate_topk(x["st"], x["scores"], args.topk, idx=x["idx"], val=x["val"])
+
+    for i in range(args.warmup):
+        score_call(i % R)
+        topk_call(i % R)
     torch.cuda.synchronize()
     log("warmup done (%d steps)" % args.warmup)
 
-    # Timed region: K steps.  Events on the launch stream bracket the score
-    # kernel (the dominant one) and the whole step.
+    # Timed region: K steps, step i on copy i mod R.  Events on the launch
+    # stream bracket the score kernel (the dominant one) and the whole step.
     K = args.steps
     mk = lambda: torch.cuda.Event(enable_timing=True)
-    ev = [(mk(), mk(), mk()) for _ in range(K)]
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for i in range(K):
-        ev[i][0].record()
-        if args.fused:
-            step()
+
+    def timed(n, rotate):
+        ev = [(mk(), mk(), mk()) for _ in range(n)]
+        torch.cuda.synchronize()
+        t_a = time.perf_counter()
+        for i in range(n):
+            c = i % R if rotate else 0
+            ev[i][0].record()
+            score_call(c)
             ev[i][1].record()
-        else:
-            fate.fate_score_frontier(pk, st, params, out=scores)
-            ev[i][1].record()
-            fate.fate_topk(st, scores, args.topk, idx=idx, val=val)
-        ev[i][2].record()
-    torch.cuda.synchronize()
-    t_end = time.perf_counter()
-    ms_step = (t_end - t_start) * 1e3 / K
-    kern_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))  # score kernel (fused: score + top-k)
-    step_kern_ms = float(np.mean([a.elapsed_time(c) for a, _, c in ev]))
-    log("timed %d steps: %.4f ms/step; %s kernel %.4f ms, all kernels %.4f ms"
-        % (K, ms_step, "fused score + top-k" if args.fused else "score", kern_ms, step_kern_ms))
+            topk_call(c)
+            ev[i][2].record()
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t_a) * 1e3 / n
+        return (wall, float(np.mean([a.elapsed_time(b) for a, b, _ in ev])),
+                float(np.mean([a.elapsed_time(c) for a, _, c in ev])))
+
+    ms_step, kern_ms, step_kern_ms = timed(K, rotate=True)
+    log("timed %d steps over %d copies: %.4f ms/step; %s kernel %.4f ms, all kernels %.4f ms"
+        % (K, R, ms_step, "fused score + top-k" if args.fused else "score", kern_ms, step_kern_ms))
+    warm_kern_ms = None
+    if not args.no_warm:
+        warm_kern_ms = timed(K, rotate=False)[1]
+        log("the same launches repeated on one copy (warm): kernel %.4f ms" % warm_kern_ms)
 
     def median_ms(fn, n=20):
-        for _ in range(3):
-            fn()
+        for i in range(3):
+            fn(i % R)
         evs = [(mk(), mk()) for _ in range(n)]
-        for e0, e1 in evs:
+        for i, (e0, e1) in enumerate(evs):
             e0.record()
-            fn()
+            fn(i % R)
             e1.record()
         torch.cuda.synchronize()
         return float(np.median([e0.elapsed_time(e1) for e0, e1 in evs]))
 
+    def fused_c(c):
+        x = copies[c]
+        fate.fate_score_topk(x["pk"], x["st"], params, args.topk, out=x["scores"], idx=x["idx"], val=x["val"])
+
+    def score_c(c):
+        x = copies[c]
+        fate.fate_score_frontier(x["pk"], x["st"], params, out=x["scores"])
+
+    def two_c(c):
+        score_c(c)
+        x = copies[c]
+        fate.fate_topk(x["st"], x["scores"], args.topk, idx=x["idx"], val=x["val"])
+
     medians = None
     if not args.no_medians:
-        medians = {
-            "fused_score_topk": median_ms(
-                lambda: fate.fate_score_topk(pk, st, params, args.topk, out=scores, idx=idx, val=val)),
-            "score_only": median_ms(lambda: fate.fate_score_frontier(pk, st, params, out=scores)),
-            "score_then_topk_two_calls": median_ms(lambda: (fate.fate_score_frontier(pk, st, params, out=scores),
-                                                            fate.fate_topk(st, scores, args.topk, idx=idx, val=val))),
-        }
-        step()  # leave this step's results in place for the counts below
+        medians = {"fused_score_topk": median_ms(fused_c), "score_only": median_ms(score_c),
+                   "score_then_topk_two_calls": median_ms(two_c), "copies_rotated": R}
+        score_call(0)  # leave this step's results in place for the counts below
+        topk_call(0)
         torch.cuda.synchronize()
-        log("medians (ms): %s" % json.dumps(medians))
+        log("medians (ms, rotated copies): %s" % json.dumps(medians))
 
     if args.copy_calibration:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -608,7 +659,7 @@ def main():
         parts["topk"] = 8 * args.topk * counts["F"]
         alg_bytes += parts["topk"]
     achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
-    traffic = read_traffic(args.workload)
+    traffic, valu_insts = read_counters(args.workload) if args.fused else (None, None)
     out = {
         "metric": METRIC,
         "value": n_eval / (ms_step * 1e-3),
@@ -627,7 +678,8 @@ def main():
             "D": w.D, "M": w.M, "K": w.K, "H": H, "max_shard": w.max_shard, "topk": args.topk,
             "frontier_stages": counts["F"], "candidates": counts["C"], "horizon_entries": counts["desc_entries"],
             "evals_per_step": n_eval, "step": "fused score + top-k" if args.fused else "score, then top-k",
-            "kernel_ms": kern_ms, "step_kernels_ms": step_kern_ms,
+            "kernel_ms": kern_ms, "step_kernels_ms": step_kern_ms, "copies_rotated": R,
+            "kernel_ms_warm_one_copy": warm_kern_ms,
             "median_ms": medians,
             "input_sha256": synth.fingerprint(w),
             "pack_dags_s": t_pack_dags, "pack_state_s": t_pack_state,
@@ -637,7 +689,18 @@ def main():
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
             "kernel": "k_score (with top-k epilogue)" if args.fused else "k_score",
+            "kernel_ms": kern_ms, "copies_rotated": R,
         },
+    }
+    # the roof the kernel meets first: VALU issue (SQ_INSTS_VALU of the profiled
+    # kernel source over the same rotated launch time)
+    valu_g = valu_insts / (kern_ms * 1e-3) / 1e9 if valu_insts else None
+    out["roofline_valu"] = {
+        "bound": "alu", "achieved": valu_g, "peak": VALU_PEAK_GIPS, "unit": "G VALU wave-instructions/s",
+        "frac": valu_g / VALU_PEAK_GIPS if valu_g else None,
+        "valu_insts_per_launch": valu_insts,
+        "note": "peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per wave64 VALU instruction; instructions from "
+                "profiles/k_score_%s_counters.txt when its kernel source hash matches, else null" % args.workload,
     }
     if args.planning_steps > 0:
         out["planning_loop"] = planning_loop(w, pk, params, args.topk, args.planning_steps, log)

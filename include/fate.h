@@ -223,6 +223,9 @@ typedef struct {
     const uint32_t *counts;   /* [4] device counters, see above */
     const float *finish;      /* [N] planned finish of completed stages (t_now for
                                  those completed when planning began) */
+    int32_t slice;            /* frontier stages per slice the state was cut into;
+                                 scoring rejects a state whose slice length differs
+                                 from this build's for the DAGs' device count (ESTATE) */
 } fate_state_h;
 
 const char *fate_version(void);

@@ -484,6 +484,7 @@ void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_sh
     out->n_done_edges = (int64_t)p.done.size();
     out->done_off = reinterpret_cast<const uint32_t *>(base + L.done_off);
     out->done = base + L.done;
+    out->slice = (int32_t)fate::slice_len(pk->D);
 }
 
 void fill_advance_handle(const AdvanceCaps &c, const StateLayout &L, uint8_t *base, fate_state_h *out) {
@@ -698,6 +699,8 @@ fate_status_t fate_pack_state_advance(const fate_dags_t *packed, const fate_dag_
 static fate_status_t check_pair(const fate_dags_t *dags, const fate_state_h *state) {
     if (!dags || !state) return FATE_EINVAL;
     if (dags->B != state->B || dags->D != state->D || dags->N != state->N) return FATE_ESTATE;
+    // the scoring kernel's LDS holds one slice of this build's length
+    if (state->slice != fate::slice_len(dags->D)) return FATE_ESTATE;
     if (!dags->records || !state->frontier || !state->cand_off || !state->slices || !state->done_off)
         return FATE_EINVAL;
     return FATE_OK;
@@ -789,6 +792,8 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     }
     if (stride < state->n_cand) return FATE_ESIZE;
     if (n_scores < stride * (P - 1) + state->n_cand) return FATE_ESIZE;
+    // the instance's prefix table, model tables and staging must fit one workgroup's LDS
+    if (!fate::score_fits(dags->D, state->K, dags->M, dags->beta_uniform)) return FATE_ERANGE;
     if (state->n_frontier == 0) return FATE_OK;
     if (!d_scores) return FATE_EINVAL;
     fate::ScoreLaunch a;

@@ -165,6 +165,9 @@ inline int slice_len(int D) {
 
 // Kernel launchers (fate_kernels.hip).  Return a hipError_t as int.
 int launch_score(const ScoreLaunch &a, void *stream);
+// Whether some instance of the scoring kernel fits its LDS for this shape
+// (devices, prefix slots, models, uniform beta).
+bool score_fits(int D, int K, int M, int beta_uniform);
 int launch_topk(const TopkLaunch &a, void *stream);
 int launch_commit(const CommitLaunch &a, void *stream);  // fate_commit.hip
 

@@ -143,11 +143,12 @@ static_assert(sizeof(EntryS) == 64, "EntryS");
 // row reads do not conflict.
 constexpr int kSlotGroupBytes = 16 * (int)sizeof(EntryS) + 16;
 
-// Bytes of the staging area for lane-group width G (host and device agree).
-template <int G>
+// Bytes of the staging area for lane-group width G in workgroups of BLK
+// threads (host and device agree).
+template <int G, int BLK>
 constexpr int staging_bytes() {
-    return G == 16 ? (score_block(G) / 16) * kSlotGroupBytes
-                   : score_block(G) * (G <= 32 ? (int)sizeof(EntryL<uint32_t>) : (int)sizeof(EntryL<uint64_t>));
+    return G == 16 ? (BLK / 16) * kSlotGroupBytes
+                   : BLK * (G <= 32 ? (int)sizeof(EntryL<uint32_t>) : (int)sizeof(EntryL<uint64_t>));
 }
 
 template <int G>
@@ -187,14 +188,16 @@ struct alignas(16) CostS {
 // Byte offsets of every LDS array (shared by the launcher and the kernel).
 struct LdsPlan {
     uint32_t pkey, pmask, rm, rho, fits, wt, cap, order, wait, gpow, next, exec, ksw, stages, entries, total;
-    uint32_t items, parts, left, pbase, pool;  // row splits of heavy stages (64-lane groups)
+    uint32_t items, parts, left, pbase, plen, pool;  // row splits of heavy stages (64-lane groups)
 };
 
 // 64-lane groups: a singletons-only stage with more than kSplitRows
 // descendant rows is scored in parts of kSplitRows rows by several waves of
 // its workgroup; each part's fp64 sums go to a pool slot, and the wave that
 // finishes last adds them in part order and emits.  At most kSplitItems work
-// items and kSplitSlots pool slots per workgroup (later stages stay whole).
+// items and kSplitSlots pool slots per workgroup: once they run short a stage
+// gets fewer, longer parts (whole 64-row batches), and a stage that cannot
+// have two stays whole.
 constexpr int kSplitRows = 128, kSplitItems = 256, kSplitSlots = 32;
 static_assert(kSplitRows % 64 == 0, "a part is whole 64-row batches");
 
@@ -227,13 +230,14 @@ __host__ __device__ inline LdsPlan lds_plan(int D, int K, int M, int slice, int 
         q.exec = o; o += 4 * (uint32_t)(M * D);
         q.ksw = o; o += 4 * (uint32_t)(M * D);
     }
-    q.items = q.parts = q.left = q.pbase = q.pool = o;
-    if (split) {  // items (position | part << 8), parts, parts left, first pool slot, then the pool
+    q.items = q.parts = q.left = q.pbase = q.plen = q.pool = o;
+    if (split) {  // items (position | part << 8), parts, parts left, first pool slot, rows per part, then the pool
         q.items = o; o += 2 * kSplitItems;
         q.parts = o; o += ((uint32_t)slice + 3u) & ~3u;
         o = (o + 3u) & ~3u;
         q.left = o; o += 4 * (uint32_t)slice;
         q.pbase = o; o += ((uint32_t)slice + 3u) & ~3u;
+        q.plen = o; o += 4 * (uint32_t)slice;
         o = (o + 7u) & ~7u;
         q.pool = o; o += 8 * 64 * kSplitSlots;
     }
@@ -597,11 +601,15 @@ __device__ __forceinline__ bool child_of(const ScoreLaunch &a, const StageRec &r
 
 // VAR = false compiles the scoring variants out (no same-model weight, sum
 // over levels, windows on, hop levels); the launcher picks it when no
-// parameter set of the launch uses a variant.
-template <int G, bool UNI, bool SLOTS, bool VAR>
-__global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
-    constexpr int kBlock = score_block(G);  // threads of this workgroup
+// parameter set of the launch uses a variant.  SPLIT (64-lane groups) scores
+// heavy stages in parts; BLK is the workgroup size.  The launcher takes the
+// first of (split, score_block(G)), (no split, score_block(G)), (no split,
+// half that) whose LDS plan fits a workgroup.
+template <int G, bool UNI, bool SLOTS, bool VAR, bool SPLIT, int BLK>
+__global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
+    constexpr int kBlock = BLK;  // threads of this workgroup
     static_assert(!SLOTS || (UNI && G == 16), "the slot layout needs 16-lane groups and uniform beta");
+    static_assert(!SPLIT || (G == 64 && !SLOTS), "heavy-stage parts are for 64-lane groups");
     // a planning state is launched over its slice capacity; the current
     // number of slices is on the device
     const uint32_t slice = blockIdx.x;
@@ -623,8 +631,8 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
     // slot layout: 16-lane groups, uniform beta, at most 32 models (chosen by the launcher)
     constexpr bool kSlots = SLOTS;
     using Entry = EntryL<Mask>;
-    constexpr bool kSplit = G == 64 && !SLOTS;
-    const LdsPlan plan = lds_plan(D, K, M, a.slice, staging_bytes<G>(), SLOTS, kSplit);
+    constexpr bool kSplit = SPLIT;
+    const LdsPlan plan = lds_plan(D, K, M, a.slice, staging_bytes<G, BLK>(), SLOTS, kSplit);
 
     Lds L;
     L.logT = table_log2(D, K);
@@ -748,15 +756,28 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
         uint16_t *items = reinterpret_cast<uint16_t *>(sb + plan.items);
         uint8_t *parts = sb + plan.parts, *pbase = sb + plan.pbase;
         uint32_t *left = reinterpret_cast<uint32_t *>(sb + plan.left);
+        uint32_t *plen = reinterpret_cast<uint32_t *>(sb + plan.plen);
         int ni = 0, used = 0;
         for (int pos = 0; pos < nF; ++pos) {
             const StageL &st = L.stages[L.order[pos]];
             const int ne = (int)(st.e1 - st.e0);
-            int np = st.nc == (uint32_t)D && ne > kSplitRows ? (ne + kSplitRows - 1) / kSplitRows : 1;
-            if (np > 1 && (used + np > kSplitSlots || ni + np + (nF - 1 - pos) > kSplitItems)) np = 1;
+            int np = 1;
+            uint32_t pl = (uint32_t)ne;
+            if (st.nc == (uint32_t)D && ne > kSplitRows) {
+                // as many parts of kSplitRows rows as the pool slots and the
+                // work items left allow (every later stage keeps one item)
+                np = min((ne + kSplitRows - 1) / kSplitRows, min(kSplitSlots - used, kSplitItems - ni - (nF - 1 - pos)));
+                if (np >= 2) {  // rows per part: whole 64-row batches; ne > 128 keeps np >= 2
+                    pl = (uint32_t)((((ne + np - 1) / np) + 63) & ~63);
+                    np = (ne + (int)pl - 1) / (int)pl;
+                } else {
+                    np = 1;
+                }
+            }
             parts[pos] = (uint8_t)np;
             left[pos] = (uint32_t)np;
             pbase[pos] = (uint8_t)used;
+            plen[pos] = pl;
             if (np > 1) used += np;
             for (int q = 0; q < np; ++q) items[ni++] = (uint16_t)(pos | (q << 8));
         }
@@ -1223,11 +1244,12 @@ __global__ __launch_bounds__(score_block(G)) void k_score(ScoreLaunch a) {
             w_j0[s] = tmax + lam_tr * gat;
         }
 
-        // ---- horizon descendants, G at a time (a part of a heavy stage: its kSplitRows rows)
+        // ---- horizon descendants, G at a time (a part of a heavy stage: its rows)
         const int nparts = kSplit ? (int)(sb + plan.parts)[pos] : 1;
-        const uint32_t b_lo = sv.e0 + (uint32_t)(part * kSplitRows);
-        const uint32_t b_hi = nparts > 1 ? min(sv.e1, b_lo + (uint32_t)kSplitRows) : sv.e1;
-        for (uint32_t base = b_lo; base < b_hi; base += G) {  // uniform; kSplitRows is a multiple of G
+        const uint32_t plen = kSplit && nparts > 1 ? reinterpret_cast<const uint32_t *>(sb + plan.plen)[pos] : 0u;
+        const uint32_t b_lo = sv.e0 + (uint32_t)part * plen;
+        const uint32_t b_hi = nparts > 1 ? min(sv.e1, b_lo + plen) : sv.e1;
+        for (uint32_t base = b_lo; base < b_hi; base += G) {  // uniform; a part is whole G-row batches
             const int nb = stage_batch(base);
             int jj = 0;
             if (UNI && wslots == 0) {  // singletons only: two descendants per iteration
@@ -1391,35 +1413,85 @@ constexpr int64_t kTopkMaxBlocks = 4096;
 
 }  // namespace
 
+// Most LDS one workgroup may use on gfx950 (160 KiB per compute unit).
+constexpr size_t kLdsLimit = 160 * 1024;
+
+// Kernel instance of a launch and its LDS bytes.
+struct ScoreShape {
+    bool slots, split;
+    int block;
+    size_t lds;
+};
+
+// 16-lane groups with uniform beta and at most 32 models take the slot
+// layout; 64-lane groups take the first of (heavy-stage parts, 1024 threads),
+// (no parts, 1024 threads), (no parts, 512 threads) whose LDS fits.  False if
+// none fits (the host rejects such shapes before anything is enqueued).
+static bool score_shape(int D, int K, int M, int slice, bool uni, ScoreShape &sh) {
+    const int G = group_width(D);
+    sh.slots = uni && G == 16 && M <= 32;
+    sh.split = false;
+    sh.block = score_block(G);
+    if (G < 64) {
+        const int sb = G == 16 ? staging_bytes<16, score_block(16)>() : staging_bytes<8, score_block(8)>();
+        sh.lds = lds_plan(D, K, M, slice, sb, sh.slots, false).total;
+        return sh.lds <= kLdsLimit;
+    }
+    const bool split[3] = {true, false, false};
+    const int block[3] = {score_block(64), score_block(64), score_block(64) / 2};
+    for (int c = 0; c < 3; ++c) {
+        const int sb = block[c] == score_block(64) ? staging_bytes<64, score_block(64)>()
+                                                   : staging_bytes<64, score_block(64) / 2>();
+        const size_t lds = lds_plan(D, K, M, slice, sb, false, split[c]).total;
+        if (lds <= kLdsLimit) {
+            sh.split = split[c];
+            sh.block = block[c];
+            sh.lds = lds;
+            return true;
+        }
+    }
+    return false;
+}
+
+bool score_fits(int D, int K, int M, int beta_uniform) {
+    ScoreShape sh;
+    return score_shape(D, K, M, slice_len(D), beta_uniform != 0, sh);
+}
+
 template <bool UNI>
-static void launch_score_g(const ScoreLaunch &a, hipStream_t s) {
+static void launch_score_g(const ScoreLaunch &a, const ScoreShape &sh, hipStream_t s) {
     const int G = group_width(a.D);
-    const int sb = G == 16 ? staging_bytes<16>() : G <= 32 ? staging_bytes<8>() : staging_bytes<64>();
-    const bool slots = UNI && G == 16 && a.M <= 32;  // the kernel choice below
-    const size_t lds = lds_plan(a.D, a.K, a.M, a.slice, sb, slots, G == 64 && !slots).total;
-    const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block(score_block(G));
+    const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block((unsigned)sh.block);
+    const size_t lds = sh.lds;
     bool var = a.topo != 0;
     for (int p = 0; p < a.nsets; ++p) var = var || a.ps[p].lam_m != 0.0f || a.ps[p].flags != 0;
+    constexpr int B0 = kScoreBlock, B64 = score_block(64);
     switch (G) {
-        case 4: hipLaunchKernelGGL((k_score<4, UNI, false, true>), grid, block, lds, s, a); break;
-        case 8: hipLaunchKernelGGL((k_score<8, UNI, false, true>), grid, block, lds, s, a); break;
+        case 4: hipLaunchKernelGGL((k_score<4, UNI, false, true, false, B0>), grid, block, lds, s, a); break;
+        case 8: hipLaunchKernelGGL((k_score<8, UNI, false, true, false, B0>), grid, block, lds, s, a); break;
         case 16:
-            if (UNI && a.M <= 32) {
-                if (var) hipLaunchKernelGGL((k_score<16, UNI, UNI, true>), grid, block, lds, s, a);
-                else hipLaunchKernelGGL((k_score<16, UNI, UNI, false>), grid, block, lds, s, a);
+            if (UNI && sh.slots) {
+                if (var) hipLaunchKernelGGL((k_score<16, UNI, UNI, true, false, B0>), grid, block, lds, s, a);
+                else hipLaunchKernelGGL((k_score<16, UNI, UNI, false, false, B0>), grid, block, lds, s, a);
             } else {
-                hipLaunchKernelGGL((k_score<16, UNI, false, true>), grid, block, lds, s, a);
+                hipLaunchKernelGGL((k_score<16, UNI, false, true, false, B0>), grid, block, lds, s, a);
             }
             break;
-        case 32: hipLaunchKernelGGL((k_score<32, UNI, false, true>), grid, block, lds, s, a); break;
-        default: hipLaunchKernelGGL((k_score<64, UNI, false, true>), grid, block, lds, s, a); break;
+        case 32: hipLaunchKernelGGL((k_score<32, UNI, false, true, false, B0>), grid, block, lds, s, a); break;
+        default:
+            if (sh.split) hipLaunchKernelGGL((k_score<64, UNI, false, true, true, B64>), grid, block, lds, s, a);
+            else if (sh.block == B64) hipLaunchKernelGGL((k_score<64, UNI, false, true, false, B64>), grid, block, lds, s, a);
+            else hipLaunchKernelGGL((k_score<64, UNI, false, true, false, B64 / 2>), grid, block, lds, s, a);
+            break;
     }
 }
 
 int launch_score(const ScoreLaunch &a, void *stream) {
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (a.beta_uniform) launch_score_g<true>(a, s);
-    else launch_score_g<false>(a, s);
+    ScoreShape sh;
+    if (!score_shape(a.D, a.K, a.M, a.slice, a.beta_uniform != 0, sh)) return (int)hipErrorInvalidValue;
+    if (a.beta_uniform) launch_score_g<true>(a, sh, s);
+    else launch_score_g<false>(a, sh, s);
     return (int)hipGetLastError();
 }
 

@@ -14,7 +14,7 @@ WF=/tmp/fate_workload_$W.npz
 # generate once, unprofiled (the generator forks worker processes); the
 # profiled runs load the saved batch
 echo "[profile] generate" && timeout -k 10 300 python3 bench.py --workload $W --workload-file $WF --steps 2 --warmup 1 --no-cpu-baseline --no-sweep --no-sim --planning-steps 0 > $O/generate.log 2>&1 || exit $?
-B="python3 bench.py --workload $W --workload-file $WF --steps $S --warmup 2 --no-cpu-baseline --no-medians --no-sweep --no-sim --planning-steps 0 --copy-calibration"
+B="python3 bench.py --workload $W --workload-file $WF --steps $S --warmup 2 --no-cpu-baseline --no-medians --no-warm --no-sweep --no-sim --planning-steps 0 --copy-calibration"
 echo "[profile] kernel trace" && timeout -k 10 300 rocprofv3 --kernel-trace --stats -d $O/trace -o kt -- $B > $O/trace.log 2>&1 || exit $?
 echo "[profile] FETCH_SIZE" && timeout -s KILL 180 rocprofv3 --pmc FETCH_SIZE -d $O/fetch -o pmc --output-format csv -- $B > $O/fetch.log 2>&1 || exit $?
 echo "[profile] WRITE_SIZE" && timeout -s KILL 180 rocprofv3 --pmc WRITE_SIZE -d $O/write -o pmc --output-format csv -- $B > $O/write.log 2>&1 || exit $?
