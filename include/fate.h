@@ -49,6 +49,11 @@ extern "C" {
 #define FATE_MAX_SHARD 4
 #define FATE_MAX_PARENTS 65535
 #define FATE_MAX_SWEEP 16 /* parameter sets per fate_score_sweep / fate_topk_sweep launch */
+/* Workspace that the library holds on each GPU for fate_commit_advance_noalloc
+ * (32 MiB: planning states of up to about 2.7 million stages), and the number
+ * of GPUs per process it keeps one for. */
+#define FATE_NOALLOC_WS_BYTES (32u << 20)
+#define FATE_MAX_DEVICES_PER_PROCESS 64
 /* Total stages over the batch must fit 28 bits (stage ids share a 32-bit word
  * with their horizon depth in the packed descendant lists). */
 #define FATE_MAX_TOTAL_STAGES ((1 << 28) - 1)
@@ -342,6 +347,23 @@ fate_status_t fate_commit_ws_size(const fate_dags_t *dags, const fate_state_h *s
  * ESIZE (workspace), ESTATE, EHIP. */
 fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
                                   int32_t sel_stride, void *d_ws, size_t ws_bytes, void *stream);
+
+/* fate_commit_advance_noalloc: fate_commit_advance for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments without the workspace,
+ * same kernels and results: the workspace is a library-held device array of
+ * FATE_NOALLOC_WS_BYTES on each GPU, kept until the process ends; its
+ * address is looked up on the first call on each device, which must be the
+ * current device (the stream's device).  The call allocates and frees
+ * nothing.  Every call on a GPU shares that GPU's array and leaves its
+ * contents behind (nothing in it needs clearing), so calls that overlap on
+ * one GPU - concurrent streams, threads or processes sharing the library's
+ * copy - race and must be serialised by the caller.
+ * Errors: as fate_commit_advance, except ESIZE; ERANGE when the planning
+ * state needs more workspace than FATE_NOALLOC_WS_BYTES (fate_commit_ws_size
+ * tells how much); EHIP if the array's device address cannot be found. */
+fate_status_t fate_commit_advance_noalloc(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
+                                          int32_t sel_stride, void *stream);
 
 /* fate_score_ws_size: device workspace bytes fate_score_frontier needs
  * (may be 0).  Errors: EINVAL, ESTATE. */

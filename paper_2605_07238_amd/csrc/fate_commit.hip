@@ -31,6 +31,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "fate_device.h"
 #include "fate_internal.h"
 
@@ -568,3 +570,46 @@ int launch_commit(const CommitLaunch &a, void *stream) {
 }
 
 }  // namespace fate
+
+// ---- commit-and-advance without a caller workspace -------------------------
+// The workspace of fate_commit_advance_noalloc lives in a file-scope device
+// array, one copy per GPU, held until the process ends.  In host code the
+// array's name is not a device address: its address on each device comes
+// from hipGetSymbolAddress, taken once per device with that device current,
+// and only that pointer is handed to the kernels.  Every word of the
+// workspace is written before it is read within a call, so a call needs no
+// clearing; calls that overlap on one GPU share the array and race.
+namespace {
+
+__device__ __align__(256) uint8_t scratch[FATE_NOALLOC_WS_BYTES];
+
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[FATE_MAX_DEVICES_PER_PROCESS] = {};
+
+// The current device's copy of the array (looked up on the first call).
+fate_status_t scratch_of_current_device(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= FATE_MAX_DEVICES_PER_PROCESS) return FATE_EHIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FATE_EHIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return FATE_OK;
+}
+
+}  // namespace
+
+extern "C" fate_status_t fate_commit_advance_noalloc(const fate_dags_t *dags, const fate_state_h *state,
+                                                     const int32_t *d_sel, int32_t sel_stride, void *stream) {
+    size_t need = 0;
+    fate_status_t st = fate::commit_check(dags, state, d_sel, sel_stride, &need);
+    if (st != FATE_OK) return st;
+    if (need > (size_t)FATE_NOALLOC_WS_BYTES) return FATE_ERANGE;
+    void *ws = nullptr;
+    st = scratch_of_current_device(&ws);
+    if (st != FATE_OK) return st;
+    return fate::commit_impl(dags, state, d_sel, sel_stride, ws, (size_t)FATE_NOALLOC_WS_BYTES, stream);
+}

@@ -717,6 +717,25 @@ fate_status_t fate_commit_ws_size(const fate_dags_t *dags, const fate_state_h *s
 
 fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
                                   int32_t sel_stride, void *d_ws, size_t ws_bytes, void *stream) {
+    return fate::commit_impl(dags, state, d_sel, sel_stride, d_ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace fate {
+
+fate_status_t commit_check(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
+                           int32_t sel_stride, size_t *ws_total) {
+    fate_status_t st = check_pair(dags, state);
+    if (st != FATE_OK) return st;
+    if (!state->advance || !state->status || !state->counts || sel_stride < 1) return FATE_EINVAL;
+    if (state->n_frontier > 0 && !d_sel) return FATE_EINVAL;
+    *ws_total = fate::commit_ws_layout(state->N, state->B).total;
+    return FATE_OK;
+}
+
+fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
+                          int32_t sel_stride, void *d_ws, size_t ws_bytes, void *stream) {
     fate_status_t st = check_pair(dags, state);
     if (st != FATE_OK) return st;
     if (!state->advance || !state->status || !state->counts || sel_stride < 1) return FATE_EINVAL;
@@ -768,6 +787,10 @@ fate_status_t fate_commit_advance(const fate_dags_t *dags, const fate_state_h *s
     a.nseg = (a.nblk + fate::kPlanSeg - 1) / fate::kPlanSeg;
     return fate::launch_commit(a, stream) == 0 ? FATE_OK : FATE_EHIP;
 }
+
+}  // namespace fate
+
+extern "C" {
 
 fate_status_t fate_score_ws_size(const fate_dags_t *dags, const fate_state_h *state, size_t *bytes) {
     if (!bytes) return FATE_EINVAL;

@@ -171,6 +171,14 @@ bool score_fits(int D, int K, int M, int beta_uniform);
 int launch_topk(const TopkLaunch &a, void *stream);
 int launch_commit(const CommitLaunch &a, void *stream);  // fate_commit.hip
 
+// Commit-and-advance behind both entry points (fate_host.cpp): validation,
+// then the six launches with the workspace d_ws of ws_bytes.  commit_check
+// runs the validation alone and returns the workspace bytes needed.
+fate_status_t commit_check(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
+                           int32_t sel_stride, size_t *ws_total);
+fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
+                          int32_t sel_stride, void *d_ws, size_t ws_bytes, void *stream);
+
 // Frontier planning wave (fate_plan.hip).
 struct PlanLaunch {
     const uint32_t *frontier;  // [nF][2]: flat stage id, instance

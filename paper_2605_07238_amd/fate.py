@@ -30,7 +30,8 @@ STATUS_NAMES = {0: "FATE_OK", -1: "FATE_EINVAL", -2: "FATE_ERANGE", -3: "FATE_EC
 EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_dags", "fate_layout_dags",
            "fate_pack_state_size", "fate_pack_state", "fate_layout_state", "fate_score_ws_size",
            "fate_score_frontier", "fate_score_topk", "fate_topk", "fate_pack_state_advance_size",
-           "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance", "fate_pack_dags_opt_size",
+           "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance", "fate_commit_advance_noalloc",
+           "fate_pack_dags_opt_size",
            "fate_pack_dags_opt", "fate_layout_dags_opt", "fate_score_sweep", "fate_topk_sweep", "fate_plan_wave",
            "fate_simulate", "fate_place_baseline"]
 
@@ -39,6 +40,7 @@ FATE_MEAN_PER_LEVEL, FATE_NO_WINDOWS = 1, 2
 FATE_LEVELS_HOP, FATE_LEVELS_TOPO = 0, 1
 FATE_MAX_SWEEP = 16
 FATE_PLACE_ROUND_ROBIN, FATE_PLACE_HEFT = 0, 1
+FATE_NOALLOC_WS_BYTES = 32 << 20  # workspace the library holds per GPU for fate_commit_advance_noalloc
 
 
 class FateError(RuntimeError):
@@ -140,6 +142,7 @@ def load(path: Optional[str] = None):
     lib.fate_commit_ws_size.argtypes = [P(Dags), P(StateH), P(C.c_size_t)]
     lib.fate_commit_advance.argtypes = [P(Dags), P(StateH), C.c_void_p, C.c_int32, C.c_void_p, C.c_size_t,
                                         C.c_void_p]
+    lib.fate_commit_advance_noalloc.argtypes = [P(Dags), P(StateH), C.c_void_p, C.c_int32, C.c_void_p]
     lib.fate_pack_dags_opt_size.argtypes = [P(Cluster), P(DagBatch), P(PackOpts), P(C.c_size_t)]
     lib.fate_pack_dags_opt.argtypes = [P(Cluster), P(DagBatch), P(PackOpts), C.c_void_p, C.c_size_t, C.c_void_p,
                                        P(Dags)]
@@ -520,6 +523,18 @@ def fate_commit_advance(packed: PackedDags, state: PackedState, sel, ws=None, st
                                    stride, C.c_void_p(ws.data_ptr()), nbytes, C.c_void_p(_stream_ptr(stream))),
            "fate_commit_advance")
     return ws
+
+
+def fate_commit_advance_noalloc(packed: PackedDags, state: PackedState, sel, stream=None):
+    """fate_commit_advance with the library-held workspace (no device
+    allocation by the library or here).  ``sel`` as for fate_commit_advance."""
+    import torch
+    if sel.dtype != torch.int32 or not sel.is_contiguous():
+        raise ValueError("sel must be a contiguous int32 tensor")
+    stride = int(sel.shape[1]) if sel.dim() == 2 else 1
+    _check(load().fate_commit_advance_noalloc(C.byref(packed.handle), C.byref(state.handle),
+                                              C.c_void_p(sel.data_ptr()), stride, C.c_void_p(_stream_ptr(stream))),
+           "fate_commit_advance_noalloc")
 
 
 def state_arrays(state: PackedState):
