@@ -19,7 +19,8 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "fate_oracle.c")
-LIB = os.path.join(HERE, "libfate_oracle.so")
+# FATE_ORACLE_LIBRARY names another build of the same source (the sanitizer build).
+LIB = os.environ.get("FATE_ORACLE_LIBRARY") or os.path.join(HERE, "libfate_oracle.so")
 _lock = threading.Lock()
 _lib = None
 
@@ -32,6 +33,22 @@ def build(force: bool = False, src: str = SRC, out: str = LIB) -> str:
                "-Wno-unused-parameter", src, "-o", tmp, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, out)
+    return out
+
+
+SAN_LIB = os.path.join(HERE, "_build_san", "libfate_oracle_san.so")
+
+
+def build_sanitized(out: str = SAN_LIB) -> str:
+    """The oracle built with clang's AddressSanitizer and
+    UndefinedBehaviorSanitizer (load it with the matching runtime preloaded;
+    OpenMP off, so the build needs no sanitized OpenMP runtime)."""
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    clang = "/opt/rocm/llvm/bin/clang"
+    cmd = [clang, "-O1", "-g", "-std=c11", "-shared", "-fPIC", "-fno-omit-frame-pointer",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-shared-libasan",
+           "-Wno-unknown-pragmas", SRC, "-o", out, "-lm"]
+    subprocess.run(cmd, check=True)
     return out
 
 

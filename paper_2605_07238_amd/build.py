@@ -69,7 +69,41 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+SAN_DIR = os.path.join(HERE, "_build_san")
+SAN_LIB = os.path.join(SAN_DIR, "libfate_san.so")
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """The library with its host code (packer, layouts, plan execution)
+    built with clang's AddressSanitizer and UndefinedBehaviorSanitizer, for
+    CPU test runs with the runtime preloaded; the device code is built as
+    usual (no sanitizer reaches the GPU code)."""
+    os.makedirs(SAN_DIR, exist_ok=True)
+    san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-Xarch_host",
+           "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
+    inc = ["-I", INCLUDE, "-I", CSRC]
+    objs = []
+    for src in SOURCES:
+        obj = os.path.join(SAN_DIR, os.path.basename(src) + ".o")
+        host_only = src.endswith(".cpp")
+        cmd = [hipcc(), *COMMON, *([] if host_only else KERNEL_FLAGS), *(san if host_only else []), *inc, "-c", src,
+               "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        objs.append(obj)
+    cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-shared-libasan", "-Xarch_host", "-fsanitize=address",
+           "-Xarch_host", "-fsanitize=undefined", *objs, "-o", SAN_LIB, "-lpthread"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    build(verbose=True)
-    print(LIB)
+    if "--sanitize" in sys.argv:
+        print(build_sanitized(verbose=True))
+    else:
+        build(verbose=True)
+        print(LIB)
     sys.exit(0)

@@ -20,6 +20,11 @@
 
 namespace {
 
+// memcpy for byte counts that may be 0 (the source of an empty copy may be null)
+void copy_bytes(void *dst, const void *src, size_t n) {
+    if (n) std::memcpy(dst, src, n);
+}
+
 using fate::StageRec;
 using fate_host::dev_mask;
 using fate_host::finite_nonneg;
@@ -215,16 +220,16 @@ void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
                       const DagLayout &L, bool level_weights, uint8_t *img) {
     float *wts = level_weights ? reinterpret_cast<float *>(img + L.desc_w) : nullptr;
     const int D = c->D, M = c->M;
-    std::memcpy(img + L.exec, c->exec, sizeof(float) * M * D);
-    std::memcpy(img + L.ksw, c->switch_s, sizeof(float) * M * D);
-    std::memcpy(img + L.beta, c->beta, sizeof(float) * D * D);
+    copy_bytes(img + L.exec, c->exec, sizeof(float) * M * D);
+    copy_bytes(img + L.ksw, c->switch_s, sizeof(float) * M * D);
+    copy_bytes(img + L.beta, c->beta, sizeof(float) * D * D);
     uint64_t *w = reinterpret_cast<uint64_t *>(img + L.weight);
     uint64_t *cp = reinterpret_cast<uint64_t *>(img + L.cap);
     uint64_t *ft = reinterpret_cast<uint64_t *>(img + L.fits);
     const std::vector<uint64_t> fits = fit_masks(c);
     for (int m = 0; m < M; ++m) { w[m] = (uint64_t)c->weight_bytes[m]; ft[m] = fits[m]; }
     for (int d = 0; d < D; ++d) cp[d] = (uint64_t)c->cap_bytes[d];
-    std::memcpy(img + L.stage_off, g->stage_off, sizeof(int64_t) * (g->B + 1));
+    copy_bytes(img + L.stage_off, g->stage_off, sizeof(int64_t) * (g->B + 1));
     StageRec *rec = reinterpret_cast<StageRec *>(img + L.rec);
     uint32_t *par = reinterpret_cast<uint32_t *>(img + L.par);
     uint32_t *doff = reinterpret_cast<uint32_t *>(img + L.desc_off);
@@ -250,7 +255,7 @@ void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
             for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) par[q] = (uint32_t)(base + g->par_idx[q]);
         }
         if (n > 0 && !p.lists[b].empty())
-            std::memcpy(desc + doff[base], p.lists[b].data(), sizeof(uint32_t) * p.lists[b].size());
+            copy_bytes(desc + doff[base], p.lists[b].data(), sizeof(uint32_t) * p.lists[b].size());
     });
     if (!wts) return;
     // level weights: 1 / (number of v's horizon stages at that depth), for
@@ -438,18 +443,18 @@ fate_status_t advance_caps(const fate_dags_t *pk, const fate_dag_batch_t *g, con
 void write_state_image(const fate_dags_t *pk, const fate_dag_batch_t *g, const fate_state_t *st, const StatePlan &p,
                        const StateLayout &L, uint8_t *img) {
     const int B = pk->B, D = pk->D, K = st->K;
-    std::memcpy(img + L.resident, st->resident, sizeof(uint64_t) * B * D);
-    if (K > 0) std::memcpy(img + L.pcache, st->prefix_cache, sizeof(uint64_t) * (size_t)B * D * K);
-    std::memcpy(img + L.holders, st->holders, sizeof(uint64_t) * pk->N);
-    std::memcpy(img + L.tau, st->tau_free, sizeof(float) * B * D);
-    std::memcpy(img + L.tnow, st->t_now, sizeof(float) * B);
-    std::memcpy(img + L.frontier, p.frontier.data(), sizeof(uint32_t) * p.frontier.size());
-    std::memcpy(img + L.cand_off, p.cand_off.data(), sizeof(uint32_t) * p.cand_off.size());
-    if (!p.slices.empty()) std::memcpy(img + L.slices, p.slices.data(), sizeof(uint32_t) * p.slices.size());
-    std::memcpy(img + L.done_off, p.done_off.data(), sizeof(uint32_t) * p.done_off.size());
-    if (!p.done.empty()) std::memcpy(img + L.done, p.done.data(), sizeof(fate::DoneParent) * p.done.size());
+    copy_bytes(img + L.resident, st->resident, sizeof(uint64_t) * B * D);
+    copy_bytes(img + L.pcache, st->prefix_cache, sizeof(uint64_t) * (size_t)B * D * K);
+    copy_bytes(img + L.holders, st->holders, sizeof(uint64_t) * pk->N);
+    copy_bytes(img + L.tau, st->tau_free, sizeof(float) * B * D);
+    copy_bytes(img + L.tnow, st->t_now, sizeof(float) * B);
+    copy_bytes(img + L.frontier, p.frontier.data(), sizeof(uint32_t) * p.frontier.size());
+    copy_bytes(img + L.cand_off, p.cand_off.data(), sizeof(uint32_t) * p.cand_off.size());
+    copy_bytes(img + L.slices, p.slices.data(), sizeof(uint32_t) * p.slices.size());
+    copy_bytes(img + L.done_off, p.done_off.data(), sizeof(uint32_t) * p.done_off.size());
+    copy_bytes(img + L.done, p.done.data(), sizeof(fate::DoneParent) * p.done.size());
     if (L.counts > L.status) {  // planning state
-        std::memcpy(img + L.status, st->status, (size_t)pk->N);
+        copy_bytes(img + L.status, st->status, (size_t)pk->N);
         // planned finish: t for the stages completed when planning begins
         float *fin = reinterpret_cast<float *>(img + L.finish);
         for (int b = 0; b < B; ++b)
@@ -519,7 +524,11 @@ extern "C" {
 const char *fate_version(void) { return "fate-mi355x 0.1.0 (gfx950)"; }
 
 const char *fate_strerror(fate_status_t s) {
-    switch (s) {
+    // a caller may pass any int; read it as one (an enum value outside the
+    // enumerators' range is not a valid fate_status_t in C++)
+    int code;
+    std::memcpy(&code, &s, sizeof code);
+    switch (code) {
         case FATE_OK: return "ok";
         case FATE_EINVAL: return "invalid argument";
         case FATE_ERANGE: return "value out of supported range";
@@ -562,7 +571,7 @@ fate_status_t fate_layout_dags_opt(const fate_cluster_t *cluster, const fate_dag
     DagLayout L;
     fate_status_t st = build_dags(cluster, dags, *opts, bytes, img, p, L);
     if (st != FATE_OK) return st;
-    std::memcpy(h_buf, img.data(), L.total);
+    copy_bytes(h_buf, img.data(), L.total);
     fill_dags_handle(cluster, dags, *opts, p, L, static_cast<uint8_t *>(h_buf), bytes, out);
     return FATE_OK;
 }
@@ -642,7 +651,7 @@ fate_status_t fate_layout_state(const fate_dags_t *packed, const fate_dag_batch_
     StateLayout L;
     fate_status_t st = build_state(packed, dags, state, max_shard, bytes, img, p, L);
     if (st != FATE_OK) return st;
-    std::memcpy(h_buf, img.data(), L.total);
+    copy_bytes(h_buf, img.data(), L.total);
     fill_state_handle(packed, state, max_shard, p, L, static_cast<uint8_t *>(h_buf), bytes, out);
     return FATE_OK;
 }

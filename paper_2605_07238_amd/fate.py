@@ -19,7 +19,8 @@ from typing import Optional
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libfate.so")
+# FATE_LIBRARY names another build of the same sources (the sanitizer build).
+LIB_PATH = os.environ.get("FATE_LIBRARY") or os.path.join(HERE, "libfate.so")
 
 FATE_OK = 0
 FATE_EINVAL, FATE_ERANGE, FATE_ECYCLE, FATE_ENOFEAS, FATE_ESIZE, FATE_ESTATE, FATE_EHIP = -1, -2, -3, -4, -5, -6, -7
