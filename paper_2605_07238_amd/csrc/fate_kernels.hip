@@ -96,6 +96,7 @@ static_assert(sizeof(StageL) == 64, "StageL");
 // device holding that parent's output saves (its transfer plus the
 // colocation benefit).
 constexpr int kCap = 3;  // completed parents staged per descendant
+constexpr int kMore = 4;  // further completed parents loaded per round trip
 template <class Mask>
 struct EntryL {
     Mask feas;         // devices feasible for w: eligible and able to hold its model
@@ -469,6 +470,12 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Lane J of each 16-lane row, to the whole row (DPP row_newbcast).
+template <int J>
+__device__ __forceinline__ int row_bcast(int x) {
+    return __builtin_amdgcn_update_dpp(0, x, 0x150 + J, 0xF, 0xF, false);
+}
+
 // Order-preserving 32-bit image of a score (a larger score, a larger value;
 // -0 and +0 alike), and its inverse.
 __device__ __forceinline__ uint32_t order_bits(float x) {
@@ -550,6 +557,45 @@ __device__ __forceinline__ void group_topk(uint32_t (&sb)[S], int lane, int k, i
 }
 
 __device__ __forceinline__ uint32_t topk_bits(float x) { return x > -inf_f() ? order_bits(x) : 0u; }
+
+// The slot layout ranks a singletons-only stage after its scoring loop, one
+// lane per stage, for k up to kLaneTopk; a stage ranked inside the loop marks
+// its slot with kRankedInLoop (the score bits of no float).
+constexpr int kLaneTopk = 4;
+constexpr uint32_t kRankedInLoop = 0xffffffffu;
+
+// Top-k (k <= kLaneTopk) of up to 16 candidates held by one lane as score
+// bits x[0..15] (0 for none or -inf): each candidate, in index order, enters
+// a list sorted by bits descending and displaces only strictly smaller
+// entries, so among equal scores the lower index ranks first.  The pick is
+// (index, score), or (-1, -inf) once the candidates run out.
+__device__ __forceinline__ void lane_topk16(const uint32_t (&x)[16], int k, int32_t *out_i, float *out_v) {
+    uint32_t t[kLaneTopk];
+    int32_t ix[kLaneTopk];
+#pragma unroll
+    for (int r = 0; r < kLaneTopk; ++r) { t[r] = 0u; ix[r] = -1; }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const uint32_t c = x[j];
+        bool gt[kLaneTopk];
+#pragma unroll
+        for (int r = 0; r < kLaneTopk; ++r) gt[r] = c > t[r];  // gt[r] implies gt[r + 1]
+#pragma unroll
+        for (int r = kLaneTopk - 1; r > 0; --r) {
+            t[r] = gt[r - 1] ? t[r - 1] : (gt[r] ? c : t[r]);
+            ix[r] = gt[r - 1] ? ix[r - 1] : (gt[r] ? j : ix[r]);
+        }
+        t[0] = gt[0] ? c : t[0];
+        ix[0] = gt[0] ? j : ix[0];
+    }
+#pragma unroll
+    for (int r = 0; r < kLaneTopk; ++r) {
+        if (r < k) {
+            out_i[r] = ix[r];
+            out_v[r] = t[r] != 0u ? order_bits_inv(t[r]) : -inf_f();
+        }
+    }
+}
 
 template <int G, int R>
 __device__ __forceinline__ void rank_stages(const float *scores, const uint32_t (&c0)[R], const int (&C)[R],
@@ -828,28 +874,31 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
 
         // ---- immediate terms of v on device `lane` and the post-state there
         float tr = 0.0f, cnt = 0.0f;
-        if constexpr (kSlots) {  // lane j loads completed parent j: one round trip per 16 parents
-            for (int q0 = 0; q0 < (int)sv.dn; q0 += 16) {  // uniform within the group
-                uint32_t h = 0u;
-                float sg = 0.0f;
-                if (q0 + lane < (int)sv.dn) {
-                    const DoneParent pu = a.done[sv.dbeg + q0 + lane];
-                    h = (uint32_t)pu.holders;  // at most 16 devices
-                    sg = pu.sigma;
-                }
-                // each parent in turn goes to the whole row, in parent order
-                const int n = min(16, (int)sv.dn - q0);
-                for (int j = 0; j < n; ++j) {  // uniform within the group
-                    const uint32_t hj = j == 0 ? (uint32_t)__builtin_amdgcn_update_dpp(0, (int)h, 0x150, 0xF, 0xF, false)  // row_newbcast:0
-                                               : (uint32_t)__shfl((int)h, j, 16);
-                    const float sj = j == 0 ? __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(sg), 0x150, 0xF, 0xF, false))
-                                            : __shfl(sg, j, 16);
-                    const bool local = ((hj >> dl) & 1u) != 0;
-                    cnt += local ? 1.0f : 0.0f;
-                    tr += local ? 0.0f : sj * a.beta0;
-                }
+        // slot layout: lane j holds completed parent j of v (the first 16 are
+        // loaded here, before the first horizon batch is staged, so that the
+        // two chains of loads overlap)
+        uint32_t par_h = 0u;
+        float par_s = 0.0f;
+        if constexpr (kSlots) {
+            if (lane < (int)sv.dn) {
+                const DoneParent pu = a.done[sv.dbeg + lane];
+                par_h = (uint32_t)pu.holders;  // at most 16 devices
+                par_s = pu.sigma;
             }
-        } else {
+        }
+        // each parent in turn goes to the whole row, in parent order (the first
+        // by a DPP row broadcast, the rest by shuffles); one round trip per 16
+        // parents
+        auto add_parents16 = [&](uint32_t h, float sg, int n) {
+            for (int j = 0; j < n; ++j) {
+                const uint32_t hj = j == 0 ? (uint32_t)row_bcast<0>((int)h) : (uint32_t)__shfl((int)h, j, 16);
+                const float sj = j == 0 ? __int_as_float(row_bcast<0>(__float_as_int(sg))) : __shfl(sg, j, 16);
+                const bool local = ((hj >> dl) & 1u) != 0;
+                cnt += local ? 1.0f : 0.0f;
+                tr += local ? 0.0f : sj * a.beta0;
+            }
+        };
+        if constexpr (!kSlots) {  // (the slot layout adds its parents once its first batch is staged)
             for (int q = 0; q < sv.dn; ++q) {  // uniform trip count
                 const DoneParent pu = a.done[sv.dbeg + q];
                 add_parent<UNI>(a, pu.holders, pu.sigma, dl, tr, cnt);
@@ -859,10 +908,15 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
         const float c_v = kSlots ? reinterpret_cast<const CostS *>(L.exec)[mv * D + dl].exec : L.exec[mv * D + dl];
         const float sw_v = kSlots ? reinterpret_cast<const CostS *>(L.exec)[mv * D + dl].swo
                                   : (bit(rho, mv) ? res_cost : L.ksw[mv * D + dl]);
-        const float colo_v = sv.npar ? cnt * fast_rcp((float)sv.npar) : 0.0f;
         const float pf_v = hv_cached ? ps.kpf * sv.tokens : 0.0f;
-        const float a_imm = ps.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
-        const float b_imm = c_v + lam_tr * tr - lam_p * pf_v;
+        // the immediate cost's two parts, once the parents' transfer and colocation are summed
+        auto imm_terms = [&](float &a_out, float &b_out) {
+            const float colo_v = sv.npar ? cnt * fast_rcp((float)sv.npar) : 0.0f;
+            a_out = ps.lam_q * L.wait[dl] + sw_v - lam_c * colo_v;  // the switch table holds lam_s * kappa
+            b_out = c_v + lam_tr * tr - lam_p * pf_v;
+        };
+        float a_imm = 0.0f, b_imm = 0.0f;
+        if constexpr (!kSlots) imm_terms(a_imm, b_imm);
         const uint64_t rho_new = kSlots ? (uint64_t)reinterpret_cast<const uint32_t *>(L.ksw)[mv * D + dl]
                                         : load_model(rho, mv, L.cap[dl], L.wt);
         const bool prefix_added = sv.hash != 0 && !hv_cached;
@@ -957,32 +1011,6 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
 
         if constexpr (kSlots) {
           {
-            // ---- candidates: the single {lane} on its own lane; the window of
-            // size k = s + 2 starting at device i on lane i of slot s (windows
-            // are ordered by size, then start: slot s writes one contiguous run)
-            const uint32_t c0 = sv.c0;
-            int nk = 0;  // window sizes present: 2 .. nk + 1
-            for (int rem = (int)sv.nc - D; rem > 0; rem -= D - nk) ++nk;
-            const float j0_single = a_imm + b_imm;
-            const uint32_t fm = (uint32_t)feas_mask;
-            float w_j0[3] = {0.0f, 0.0f, 0.0f};
-            bool w_ok[3] = {false, false, false};
-            if (__ballot(nk != 0) != 0ull) {  // uniform over the wave: some stage of it has windows
-#pragma unroll
-                for (int s = 0; s < 3; ++s) {
-                    const int k = s + 2;
-                    const float y = a_imm + b_imm * (1.0f / (float)k);  // k is a constant here
-                    // maximum over devices i..i+k-1 (a lane whose source is past the row holds no window)
-                    float m = fmaxf(y, dpp_b0<0x101>(y));
-                    if (k >= 3) m = fmaxf(m, dpp_b0<0x102>(y));
-                    if (k >= 4) m = fmaxf(m, dpp_b0<0x103>(y));
-                    const uint32_t wm = (1u << k) - 1u;
-                    w_ok[s] = windows_on && s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
-                    // gather with uniform beta: each of the k-1 other devices sends sigma/k
-                    w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma * (1.0f / (float)k));
-                }
-            }
-
             // ---- horizon rows, G at a time: lane j stages row j (EntryS)
             EntryS *areaS = reinterpret_cast<EntryS *>(static_cast<uint8_t *>(L.entries) + (tid / G) * kSlotGroupBytes);
             const uint32_t rho32 = (uint32_t)rho, rhon32 = (uint32_t)rho_new;
@@ -1028,8 +1056,14 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
                                 pw[q] = t + cw;
                             }
                         }
-                        for (uint32_t q = kCap; q < dn; ++q)  // rare: more completed parents than staged
-                            base_tr += lam_tr * a.beta0 * a.done[db + q].sigma;
+                        for (uint32_t q0 = kCap; q0 < dn; q0 += kMore) {  // rare: more completed parents than staged
+                            float sg[kMore];  // loads issued together, added in parent order
+#pragma unroll
+                            for (int i = 0; i < kMore; ++i) sg[i] = q0 + i < dn ? a.done[db + q0 + i].sigma : 0.0f;
+#pragma unroll
+                            for (int i = 0; i < kMore; ++i)
+                                if (q0 + i < dn) base_tr += lam_tr * a.beta0 * sg[i];
+                        }
                     }
                     EntryS S;
                     const bool child = VAR ? child_of(a, rw, depth, sv.v) : depth == 1;
@@ -1055,6 +1089,52 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
                 return nb;
             };
 
+            // the first batch is staged while v's parent loads are in flight
+            int nb_first = 0;
+            if (sv.e0 < sv.e1) nb_first = stage_rows(sv.e0);
+            for (int q0 = 0; q0 < (int)sv.dn; q0 += 16) {  // uniform within the group
+                uint32_t h = par_h;
+                float sg = par_s;
+                if (q0 > 0) {  // rare: more than 16 completed parents
+                    h = 0u;
+                    sg = 0.0f;
+                    if (q0 + lane < (int)sv.dn) {
+                        const DoneParent pu = a.done[sv.dbeg + q0 + lane];
+                        h = (uint32_t)pu.holders;
+                        sg = pu.sigma;
+                    }
+                }
+                add_parents16(h, sg, min(16, (int)sv.dn - q0));
+            }
+            imm_terms(a_imm, b_imm);
+
+            // ---- candidates: the single {lane} on its own lane; the window of
+            // size k = s + 2 starting at device i on lane i of slot s (windows
+            // are ordered by size, then start: slot s writes one contiguous run)
+            const uint32_t c0 = sv.c0;
+            int nk = 0;  // window sizes present: 2 .. nk + 1
+            for (int rem = (int)sv.nc - D; rem > 0; rem -= D - nk) ++nk;
+            const float j0_single = a_imm + b_imm;
+            const uint32_t fm = (uint32_t)feas_mask;
+            float w_j0[3] = {0.0f, 0.0f, 0.0f};
+            bool w_ok[3] = {false, false, false};
+            if (__ballot(nk != 0) != 0ull) {  // uniform over the wave: some stage of it has windows
+#pragma unroll
+                for (int s = 0; s < 3; ++s) {
+                    const int k = s + 2;
+                    const float y = a_imm + b_imm * (1.0f / (float)k);  // k is a constant here
+                    // maximum over devices i..i+k-1 (a lane whose source is past the row holds no window)
+                    float m = fmaxf(y, dpp_b0<0x101>(y));
+                    if (k >= 3) m = fmaxf(m, dpp_b0<0x102>(y));
+                    if (k >= 4) m = fmaxf(m, dpp_b0<0x103>(y));
+                    const uint32_t wm = (1u << k) - 1u;
+                    w_ok[s] = windows_on && s < nk && lane <= D - k && ((fm >> lane) & wm) == wm;
+                    // gather with uniform beta: each of the k-1 other devices sends sigma/k
+                    w_j0[s] = m + lam_tr * ((float)(k - 1) * a.beta0 * sv.sigma * (1.0f / (float)k));
+                }
+            }
+
+
             // ---- horizon rows.  Outside S the row is scanned as order-reversing
             // integer keys (prefix and suffix minima, one DPP op per step); the
             // minimum outside a window {i..i+k-1} is min(prefix(i-1), suffix(i+k)).
@@ -1062,7 +1142,7 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
             // lane per size.  A batch's terms are summed in fp32, batches in fp64.
             double acc0 = 0.0, w_acc[3] = {0.0, 0.0, 0.0};
             for (uint32_t base = sv.e0; base < sv.e1; base += G) {  // uniform
-                const int nb = stage_rows(base);
+                const int nb = base == sv.e0 ? nb_first : stage_rows(base);
                 float f0 = 0.0f, f1 = 0.0f, f2 = 0.0f, f3 = 0.0f;
                 // staged row jj: the key outside S, the value inside S, and gamma^depth.
                 // Branch-free: a bit of a device mask selects a value by masking its bits.
@@ -1080,9 +1160,21 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
                         X -= bit_sel(q2.y, dlane + 16u, __uint_as_float(q2.w));
                         X -= bit_sel(q0.z, dlane + 16u, q3.x);
                         const uint32_t dn = q0.w >> 8;
-                        for (uint32_t q = kCap; q < dn; ++q) {  // rare: more completed parents than staged
-                            const DoneParent pu = a.done[q2.x + q];
-                            X -= ((uint32_t)pu.holders & bit_lo) ? lam_tr * a.beta0 * pu.sigma + q3.y : 0.0f;
+                        for (uint32_t p0 = kCap; p0 < dn; p0 += kMore) {  // rare: more completed parents than staged
+                            uint32_t hq[kMore];  // loads issued together, subtracted in parent order
+                            float sq[kMore];
+#pragma unroll
+                            for (int i = 0; i < kMore; ++i) {
+                                hq[i] = 0u;
+                                sq[i] = 0.0f;
+                                if (p0 + i < dn) {
+                                    hq[i] = (uint32_t)a.done[q2.x + p0 + i].holders;
+                                    sq[i] = a.done[q2.x + p0 + i].sigma;
+                                }
+                            }
+#pragma unroll
+                            for (int i = 0; i < kMore; ++i)
+                                if (p0 + i < dn) X -= (hq[i] & bit_lo) ? lam_tr * a.beta0 * sq[i] + q3.y : 0.0f;
                         }
                     }
                     X -= bit_sel(q0.y, dlane + 16u, q1.w);  // grp(w) already cached on this device
@@ -1178,6 +1270,16 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
                 const int64_t f = (int64_t)f0 + si;
                 int32_t *ti = a.tk_idx + f * a.topk;
                 float *tv = a.tk_val + f * a.topk;
+                // the stage's record slot in LDS is dead once its group holds it
+                // in registers: it takes the stage's score bits (one word per
+                // device, 0 for none), ranked after the loop one lane per stage;
+                // a stage ranked here marks the slot instead
+                uint32_t *ranked = reinterpret_cast<uint32_t *>(L.stages + si);
+                if (a.topk <= kLaneTopk && __ballot(nk != 0) == 0ull) {  // uniform over the wave
+                    ranked[lane] = live ? topk_bits(psi0) : 0u;
+                    continue;
+                }
+                if (lane == 0) ranked[0] = kRankedInLoop;
                 if (__ballot(nk != 0) == 0ull) {  // uniform over the wave: singletons only
                     uint32_t sb[1] = {live ? topk_bits(psi0) : 0u};
                     const uint32_t ci[1] = {(uint32_t)lane};
@@ -1351,6 +1453,24 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
             if (s >= wslots) continue;  // uniform
             const int t = lane + s * G;
             if (t < nwin) scores[c0 + D + t] = w_ok[s] ? (float)(-((double)w_j0[s] + w_acc[s])) : -inf_f();
+        }
+    }
+
+    // ---- slot layout: the singletons-only stages' top-k, one lane per stage,
+    // from the score bits their groups left in the stages' LDS slots
+    if (kSlots && a.topk > 0 && a.topk <= kLaneTopk) {  // uniform over the block
+        __syncthreads();  // every stage of the slice is scored
+        for (int i = tid; i < nF; i += kBlock) {
+            const uint4 *slot = reinterpret_cast<const uint4 *>(L.stages + i);
+            uint32_t x[16];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint4 v = slot[q];
+                x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+            }
+            if (x[0] == kRankedInLoop) continue;
+            const int64_t f = (int64_t)f0 + i;
+            lane_topk16(x, a.topk, a.tk_idx + f * a.topk, a.tk_val + f * a.topk);
         }
     }
 
