@@ -415,22 +415,33 @@ def record_fate_plan(w, params, k, log, max_waves=2000):
 
 def sim_compare(w, params, k, log):
     """Execute the FATE plan and the round-robin and HEFT-style placements of
-    the same batch (running / committed stages made pending) and report the
-    App. C.2 metrics, normalised by round robin as the paper does."""
+    the same batch (running / committed stages made pending) on the device
+    and report the App. C.2 metrics, normalised by round robin as the paper
+    does.  The baselines are built on the device too."""
     import dataclasses
+    import torch
     from paper_2605_07238_amd import fate
     ws = dataclasses.replace(w, status=np.where(w.status == 1, 1, 0).astype(np.uint8))
+    kpf = float(ws.params["kappa_prefix"])
     plans = {}
-    plans["FATE"] = record_fate_plan(ws, params, k, log)[:2]
+    fdev, ford = record_fate_plan(ws, params, k, log)[:2]
+    pk = fate.fate_pack_dags(ws)
+    st = fate.fate_pack_state(pk, ws)
+    work = torch.empty(max(1, fate.fate_sim_ws_size(pk)), dtype=torch.uint8, device="cuda")
+    plans["FATE"] = (torch.from_numpy(np.ascontiguousarray(fdev, np.uint64).view(np.int64)).cuda(),
+                     torch.from_numpy(np.ascontiguousarray(ford, np.int64)).cuda())
     t = {}
     for name, pol in (("RoundRobin", fate.FATE_PLACE_ROUND_ROBIN), ("HEFT", fate.FATE_PLACE_HEFT)):
+        torch.cuda.synchronize()
         t0 = time.perf_counter()
-        plans[name] = fate.fate_place_baseline(ws, pol)
+        plans[name] = fate.fate_place_baseline_device(pk, st, pol, kpf, ws=work)
+        torch.cuda.synchronize()
         t[name] = time.perf_counter() - t0
     res, sim_s = {}, {}
     for name, (dev, order) in plans.items():
+        torch.cuda.synchronize()
         t0 = time.perf_counter()
-        res[name] = fate.fate_simulate(ws, dev, order)
+        res[name] = fate.fate_simulate_device(pk, st, dev, order, kpf, ws=work)
         sim_s[name] = time.perf_counter() - t0
     rr = res["RoundRobin"]
     ok = rr["makespan"] > 0
@@ -449,7 +460,8 @@ def sim_compare(w, params, k, log):
         log("%-10s NormMS %.3f NormP95 %.3f XDevEdge %.3f CacheScore %.3f ModelCont %.3f (%d tasks)"
             % (name, out[name]["NormMS"], out[name]["NormP95"], out[name]["XDevEdge"], out[name]["CacheScore"],
                out[name]["ModelCont"], out[name]["tasks"]))
-    out["note"] = ("synthetic execution model (fate_simulate); running / committed stages made pending; "
+    out["note"] = ("synthetic execution model (fate_simulate_device, placements by fate_place_baseline_device); "
+                   "running / committed stages made pending; "
                    "FATE = device planning loop with top-%d choices per stage" % k)
     return out
 

@@ -494,6 +494,40 @@ fate_status_t fate_place_baseline(const fate_cluster_t *cluster, const fate_dag_
                                   const fate_state_t *state, int32_t policy, float kappa_prefix, uint64_t *devices,
                                   int64_t *order);
 
+/* Plan execution and baseline placements on the device (App. C.2 metrics,
+ * App. B baselines): the rules of fate_simulate and fate_place_baseline,
+ * computed in fp64 by one 64-lane wave per instance, on the packed DAGs and
+ * a packed state instead of host arrays.  A stage is completed when its
+ * holders in the packed state are non-zero, pending otherwise (so running and
+ * committed stages count as pending).
+ *
+ * fate_sim_ws_size: bytes of device workspace the two calls below need
+ * (about 50 bytes per stage of the batch).  Errors: EINVAL. */
+fate_status_t fate_sim_ws_size(const fate_dags_t *dags, size_t *bytes);
+
+/* fate_simulate_device: fate_simulate for d_devices[N] / d_order[N] (device
+ * arrays, flat stage ids) from the packed state; writes d_out[B]
+ * (fate_sim_metrics_t) and d_status[B] (device memory), and is enqueued on
+ * `stream`.  Errors found in the device arrays are reported per instance in
+ * d_status (FATE_OK, FATE_EINVAL for a device bit >= D, FATE_ESTATE for an
+ * order that runs a placed stage before a parent that is neither completed
+ * nor run earlier); such an instance's metrics are all zero.  The times
+ * equal fate_simulate's bit for bit (the same fp64 operations in the same
+ * order); d_ws is caller memory of fate_sim_ws_size bytes, overwritten.
+ * Errors: EINVAL (null pointers, kappa_prefix negative or not finite),
+ * ESTATE (handles of different batches), ESIZE (workspace), EHIP. */
+fate_status_t fate_simulate_device(const fate_dags_t *dags, const fate_state_h *state, const uint64_t *d_devices,
+                                   const int64_t *d_order, float kappa_prefix, fate_sim_metrics_t *d_out,
+                                   int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream);
+
+/* fate_place_baseline_device: fate_place_baseline on the device; writes
+ * d_devices[N] and d_order[N] (0 for completed stages) and d_status[B]
+ * (FATE_OK, or FATE_ESTATE if a stage's parent would run after it).
+ * Errors: as fate_simulate_device, plus EINVAL for an unknown policy. */
+fate_status_t fate_place_baseline_device(const fate_dags_t *dags, const fate_state_h *state, int32_t policy,
+                                         float kappa_prefix, uint64_t *d_devices, int64_t *d_order,
+                                         int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libfate.so")
 SOURCES = [os.path.join(CSRC, "fate_host.cpp"), os.path.join(CSRC, "fate_kernels.hip"),
            os.path.join(CSRC, "fate_commit.hip"), os.path.join(CSRC, "fate_plan.hip"),
-           os.path.join(CSRC, "fate_sim.cpp")]
+           os.path.join(CSRC, "fate_sim.cpp"), os.path.join(CSRC, "fate_simdev.hip")]
 ARCH = os.environ.get("FATE_OFFLOAD_ARCH", "gfx950")
 
 
@@ -45,6 +45,7 @@ def commands(out: str = LIB, objdir: str = None) -> list:
     commit_o = os.path.join(objdir, "fate_commit.o")
     plan_o = os.path.join(objdir, "fate_plan.o")
     sim_o = os.path.join(objdir, "fate_sim.o")
+    simdev_o = os.path.join(objdir, "fate_simdev.o")
     inc = ["-I", INCLUDE, "-I", CSRC]
     return [
         [hipcc(), *COMMON, *inc, "-c", SOURCES[0], "-o", host_o],
@@ -52,8 +53,9 @@ def commands(out: str = LIB, objdir: str = None) -> list:
         [hipcc(), *COMMON, *KERNEL_FLAGS, *inc, "-c", SOURCES[2], "-o", commit_o],
         [hipcc(), *COMMON, *KERNEL_FLAGS, *inc, "-c", SOURCES[3], "-o", plan_o],
         [hipcc(), *COMMON, *inc, "-c", SOURCES[4], "-o", sim_o],
-        [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", host_o, kern_o, commit_o, plan_o, sim_o, "-o", out,
-         "-lpthread"],
+        [hipcc(), *COMMON, *KERNEL_FLAGS, *inc, "-c", SOURCES[5], "-o", simdev_o],
+        [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", host_o, kern_o, commit_o, plan_o, sim_o, simdev_o,
+         "-o", out, "-lpthread"],
     ]
 
 

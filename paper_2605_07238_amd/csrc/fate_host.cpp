@@ -970,3 +970,97 @@ fate_status_t fate_plan_wave(const fate_state_h *state, const int32_t *d_idx, co
 }
 
 }  // extern "C"
+
+// ---- plan execution and baseline placements on the device ------------------
+
+static fate_status_t sim_check(const fate_dags_t *dags, const fate_state_h *state, float kappa_prefix,
+                               int32_t *d_status, void *d_ws, size_t ws_bytes) {
+    fate_status_t st = check_pair(dags, state);
+    if (st != FATE_OK) return st;
+    if (!finite_nonneg(kappa_prefix)) return FATE_EINVAL;
+    if (state->B > 0 && (!d_status || !state->resident || !state->tau_free || !state->t_now || !dags->stage_off))
+        return FATE_EINVAL;
+    if (state->K > 0 && state->B > 0 && !state->prefix_cache) return FATE_EINVAL;
+    if (state->N > 0 && !state->holders) return FATE_EINVAL;
+    const fate::SimWs W = fate::sim_ws_layout(state->N);
+    if (ws_bytes < W.total) return FATE_ESIZE;
+    if (W.total > 0 && !d_ws) return FATE_EINVAL;
+    return FATE_OK;
+}
+
+static void sim_fill(const fate_dags_t *dags, const fate_state_h *state, float kappa_prefix, int32_t *d_status,
+                     void *d_ws, fate::SimLaunch &a) {
+    const fate::SimWs W = fate::sim_ws_layout(state->N);
+    uint8_t *ws = static_cast<uint8_t *>(d_ws);
+    a.rec = static_cast<const StageRec *>(dags->records);
+    a.par_idx = dags->par_idx;
+    a.stage_off = dags->stage_off;
+    a.exec = dags->exec;
+    a.ksw = dags->switch_s;
+    a.beta = dags->beta;
+    a.weight = dags->weight;
+    a.cap = dags->cap;
+    a.fits = dags->fits;
+    a.resident = state->resident;
+    a.pcache = state->prefix_cache;
+    a.holders = state->holders;
+    a.tau = state->tau_free;
+    a.tnow = state->t_now;
+    a.devices = nullptr;
+    a.order = nullptr;
+    a.dev_out = nullptr;
+    a.ord_out = nullptr;
+    a.out = nullptr;
+    a.status = d_status;
+    a.fin = reinterpret_cast<double *>(ws + W.fin);
+    a.aux = reinterpret_cast<double *>(ws + W.aux);
+    a.tail = reinterpret_cast<double *>(ws + W.tail);
+    a.hold = reinterpret_cast<uint64_t *>(ws + W.hold);
+    a.keys = reinterpret_cast<uint64_t *>(ws + W.keys);
+    a.ids = reinterpret_cast<uint32_t *>(ws + W.ids);
+    a.todo = reinterpret_cast<uint32_t *>(ws + W.todo);
+    a.flags = ws + W.flags;
+    a.kpf = (double)kappa_prefix;
+    a.B = state->B;
+    a.D = dags->D;
+    a.K = state->K;
+}
+
+extern "C" {
+
+fate_status_t fate_sim_ws_size(const fate_dags_t *dags, size_t *bytes) {
+    if (!dags || !bytes) return FATE_EINVAL;
+    *bytes = fate::sim_ws_layout(dags->N).total;
+    return FATE_OK;
+}
+
+fate_status_t fate_simulate_device(const fate_dags_t *dags, const fate_state_h *state, const uint64_t *d_devices,
+                                   const int64_t *d_order, float kappa_prefix, fate_sim_metrics_t *d_out,
+                                   int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream) {
+    fate_status_t st = sim_check(dags, state, kappa_prefix, d_status, d_ws, ws_bytes);
+    if (st != FATE_OK) return st;
+    if (state->B > 0 && !d_out) return FATE_EINVAL;
+    if (state->N > 0 && (!d_devices || !d_order)) return FATE_EINVAL;
+    fate::SimLaunch a;
+    sim_fill(dags, state, kappa_prefix, d_status, d_ws, a);
+    a.devices = d_devices;
+    a.order = d_order;
+    a.out = d_out;
+    return fate::launch_sim(a, 0, stream) == 0 ? FATE_OK : FATE_EHIP;
+}
+
+fate_status_t fate_place_baseline_device(const fate_dags_t *dags, const fate_state_h *state, int32_t policy,
+                                         float kappa_prefix, uint64_t *d_devices, int64_t *d_order,
+                                         int32_t *d_status, void *d_ws, size_t ws_bytes, void *stream) {
+    if (policy != FATE_PLACE_ROUND_ROBIN && policy != FATE_PLACE_HEFT) return FATE_EINVAL;
+    fate_status_t st = sim_check(dags, state, kappa_prefix, d_status, d_ws, ws_bytes);
+    if (st != FATE_OK) return st;
+    if (state->N > 0 && (!d_devices || !d_order)) return FATE_EINVAL;
+    fate::SimLaunch a;
+    sim_fill(dags, state, kappa_prefix, d_status, d_ws, a);
+    a.dev_out = d_devices;
+    a.ord_out = d_order;
+    return fate::launch_sim(a, policy == FATE_PLACE_ROUND_ROBIN ? 1 : 2, stream) == 0 ? FATE_OK : FATE_EHIP;
+}
+
+}  // extern "C"

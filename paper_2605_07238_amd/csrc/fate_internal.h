@@ -192,4 +192,51 @@ struct PlanLaunch {
 };
 int launch_plan(const PlanLaunch &a, void *stream);
 
+// Plan execution and baseline placements on the device (fate_simdev.hip).
+struct SimLaunch {
+    // packed DAGs
+    const StageRec *rec;
+    const uint32_t *par_idx;
+    const int64_t *stage_off;
+    const float *exec, *ksw, *beta;
+    const uint64_t *weight, *cap, *fits;
+    // packed state (completed stages: holders != 0)
+    const uint64_t *resident, *pcache, *holders;
+    const float *tau, *tnow;
+    // plan to execute, or the placement written
+    const uint64_t *devices;
+    const int64_t *order;
+    uint64_t *dev_out;
+    int64_t *ord_out;
+    fate_sim_metrics_t *out;
+    int32_t *status;
+    // workspace (sim_ws_layout), per flat stage
+    double *fin, *aux, *tail;
+    uint64_t *hold, *keys;
+    uint32_t *ids, *todo;
+    uint8_t *flags;
+    double kpf;
+    int32_t B, D, K;
+};
+struct SimWs {
+    size_t fin, aux, tail, hold, keys, ids, todo, flags, total;
+};
+inline SimWs sim_ws_layout(int64_t N) {
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    SimWs w;
+    size_t o = 0;
+    w.fin = o; o = up(o + 8 * (size_t)N);
+    w.aux = o; o = up(o + 8 * (size_t)N);
+    w.tail = o; o = up(o + 8 * (size_t)N);
+    w.hold = o; o = up(o + 8 * (size_t)N);
+    w.keys = o; o = up(o + 8 * (size_t)N);
+    w.ids = o; o = up(o + 4 * (size_t)N);
+    w.todo = o; o = up(o + 4 * (size_t)N);
+    w.flags = o; o = up(o + (size_t)N);
+    w.total = o;
+    return w;
+}
+// mode 0: execute the plan; 1: round-robin placement; 2: HEFT-style placement
+int launch_sim(const SimLaunch &a, int mode, void *stream);
+
 }  // namespace fate

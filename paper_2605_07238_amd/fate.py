@@ -34,7 +34,8 @@ EXPORTS = ["fate_version", "fate_strerror", "fate_pack_dags_size", "fate_pack_da
            "fate_pack_state_advance", "fate_commit_ws_size", "fate_commit_advance", "fate_commit_advance_noalloc",
            "fate_pack_dags_opt_size",
            "fate_pack_dags_opt", "fate_layout_dags_opt", "fate_score_sweep", "fate_topk_sweep", "fate_plan_wave",
-           "fate_simulate", "fate_place_baseline"]
+           "fate_simulate", "fate_place_baseline", "fate_sim_ws_size", "fate_simulate_device",
+           "fate_place_baseline_device"]
 
 # Scoring variants and packing options (fate_params_t.flags, fate_pack_opts_t.levels).
 FATE_MEAN_PER_LEVEL, FATE_NO_WINDOWS = 1, 2
@@ -157,6 +158,11 @@ def load(path: Optional[str] = None):
                                   P(SimMetrics)]
     lib.fate_place_baseline.argtypes = [P(Cluster), P(DagBatch), P(State), C.c_int32, C.c_float, C.c_void_p,
                                         C.c_void_p]
+    lib.fate_sim_ws_size.argtypes = [P(Dags), P(C.c_size_t)]
+    lib.fate_simulate_device.argtypes = [P(Dags), P(StateH), C.c_void_p, C.c_void_p, C.c_float, C.c_void_p,
+                                         C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.fate_place_baseline_device.argtypes = [P(Dags), P(StateH), C.c_int32, C.c_float, C.c_void_p, C.c_void_p,
+                                               C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
     for name in EXPORTS[2:]:
         getattr(lib, name).restype = st
     if path is None:
@@ -536,6 +542,71 @@ def fate_commit_advance_noalloc(packed: PackedDags, state: PackedState, sel, str
     _check(load().fate_commit_advance_noalloc(C.byref(packed.handle), C.byref(state.handle),
                                               C.c_void_p(sel.data_ptr()), stride, C.c_void_p(_stream_ptr(stream))),
            "fate_commit_advance_noalloc")
+
+
+def fate_sim_ws_size(packed: PackedDags) -> int:
+    n = C.c_size_t(0)
+    _check(load().fate_sim_ws_size(C.byref(packed.handle), C.byref(n)), "fate_sim_ws_size")
+    return int(n.value)
+
+
+def _sim_status(status, what: str):
+    bad = status.cpu().numpy()
+    nz = np.nonzero(bad != FATE_OK)[0]
+    if len(nz):
+        raise FateError(int(bad[nz[0]]), "%s (instance %d)" % (what, int(nz[0])))
+
+
+def fate_simulate_device(packed: PackedDags, state: PackedState, devices, order, kappa_prefix: float,
+                         ws=None, stream=None) -> dict:
+    """Execute a placement on the device: ``devices`` uint64 (as int64) and
+    ``order`` int64 device tensors [N] over flat stage ids.  Returns the
+    per-instance metrics as numpy arrays (tasks, makespan, p95, xdev_edges,
+    cache_hits, model_cont); raises on a per-instance error status."""
+    import torch
+    lib = load()
+    dev = packed.buf.device
+    for t, nm in ((devices, "devices"), (order, "order")):
+        if t.dtype != torch.int64 or not t.is_contiguous() or t.numel() < packed.handle.N:
+            raise ValueError("%s must be a contiguous int64 tensor of N elements" % nm)
+    nbytes = fate_sim_ws_size(packed)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
+    B = int(packed.handle.B)
+    out = torch.empty((max(1, B), C.sizeof(SimMetrics)), dtype=torch.uint8, device=dev)
+    status = torch.empty(max(1, B), dtype=torch.int32, device=dev)
+    _check(lib.fate_simulate_device(C.byref(packed.handle), C.byref(state.handle), C.c_void_p(devices.data_ptr()),
+                                    C.c_void_p(order.data_ptr()), float(kappa_prefix), C.c_void_p(out.data_ptr()),
+                                    C.c_void_p(status.data_ptr()), C.c_void_p(ws.data_ptr()), nbytes,
+                                    C.c_void_p(_stream_ptr(stream))), "fate_simulate_device")
+    _sim_status(status[:B], "fate_simulate_device")
+    raw = out[:B].cpu().numpy()
+    rec = np.frombuffer(raw.tobytes(), dtype=np.dtype([(name, np.float64 if name in ("makespan", "p95") else np.int64)
+                                                       for name, _ in SimMetrics._fields_]), count=B)
+    return {name: np.array(rec[name]) for name, _ in SimMetrics._fields_}
+
+
+def fate_place_baseline_device(packed: PackedDags, state: PackedState, policy: int, kappa_prefix: float,
+                               ws=None, stream=None):
+    """Round-robin or HEFT-style placement built on the device: (devices,
+    order) int64 device tensors [N] (devices holds the uint64 masks)."""
+    import torch
+    lib = load()
+    dev = packed.buf.device
+    N, B = int(packed.handle.N), int(packed.handle.B)
+    nbytes = fate_sim_ws_size(packed)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
+    devices = torch.empty(max(1, N), dtype=torch.int64, device=dev)
+    order = torch.empty(max(1, N), dtype=torch.int64, device=dev)
+    status = torch.empty(max(1, B), dtype=torch.int32, device=dev)
+    _check(lib.fate_place_baseline_device(C.byref(packed.handle), C.byref(state.handle), int(policy),
+                                          float(kappa_prefix), C.c_void_p(devices.data_ptr()),
+                                          C.c_void_p(order.data_ptr()), C.c_void_p(status.data_ptr()),
+                                          C.c_void_p(ws.data_ptr()), nbytes, C.c_void_p(_stream_ptr(stream))),
+           "fate_place_baseline_device")
+    _sim_status(status[:B], "fate_place_baseline_device")
+    return devices[:N], order[:N]
 
 
 def state_arrays(state: PackedState):
