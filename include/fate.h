@@ -196,6 +196,7 @@ typedef struct {
     const int64_t *stage_off;             /* [B+1] */
     int32_t levels;                       /* FATE_LEVELS_HOP or FATE_LEVELS_TOPO */
     const float *desc_w;                  /* [n_desc] level weights, or null */
+    int32_t max_r;                        /* largest shard degree R(v) of the batch */
 } fate_dags_t;
 
 /* Packed state of one planning step: plain data pointing into the caller's

@@ -201,6 +201,9 @@ void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
         }
     out->beta_uniform = uniform;
     out->beta0 = b0;
+    int32_t max_r = 1;
+    for (int64_t i = 0; i < p.N; ++i) max_r = std::max(max_r, (int32_t)g->shard_max[i]);
+    out->max_r = max_r;
     out->base = base;
     out->bytes = bytes;
     out->exec = reinterpret_cast<const float *>(base + L.exec);
@@ -866,6 +869,9 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.slice = fate::slice_len(dags->D);
     a.beta0 = dags->beta0;
     a.topo = dags->levels == FATE_LEVELS_TOPO ? 1 : 0;
+    a.Hpack = dags->H;
+    // a window needs a stage with R(v) > 1, a shard cap above 1 and two devices
+    a.singles = std::min(std::min(dags->max_r, state->max_shard), dags->D) <= 1 ? 1 : 0;
     a.nsets = P;
     for (int p = 0; p < fate::kMaxSets; ++p) {
         const fate_params_t &q = params[p < P ? p : 0];
@@ -880,6 +886,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
         ps.lam_m = q.lam_m;
         ps.H = q.H;
         ps.flags = q.flags;
+        a.set_of[p] = p;
     }
     return fate::launch_score(a, stream) == 0 ? FATE_OK : FATE_EHIP;
 }

@@ -74,8 +74,11 @@ struct ScoreLaunch {
     int32_t D, M, K, max_shard, beta_uniform, slice;
     float beta0;
     int32_t topo;  // descendant lists by topological level (FATE_LEVELS_TOPO)
+    int32_t Hpack;      // horizon the descendant lists were packed with
+    int32_t singles;    // every frontier stage has only single-device candidates
     int32_t nsets;
     ParamSet ps[kMaxSets];
+    int32_t set_of[kMaxSets];  // grid row y scores parameter set set_of[y] (its place in the output)
 };
 
 struct TopkLaunch {

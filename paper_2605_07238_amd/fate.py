@@ -91,7 +91,8 @@ class Dags(C.Structure):
                 ("exec", C.c_void_p), ("switch_s", C.c_void_p), ("beta", C.c_void_p),
                 ("weight", C.c_void_p), ("cap", C.c_void_p), ("fits", C.c_void_p),
                 ("records", C.c_void_p), ("par_idx", C.c_void_p), ("desc_off", C.c_void_p),
-                ("desc", C.c_void_p), ("stage_off", C.c_void_p), ("levels", C.c_int32), ("desc_w", C.c_void_p)]
+                ("desc", C.c_void_p), ("stage_off", C.c_void_p), ("levels", C.c_int32), ("desc_w", C.c_void_p),
+                ("max_r", C.c_int32)]
 
 
 class StateH(C.Structure):
