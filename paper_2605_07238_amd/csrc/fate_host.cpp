@@ -861,6 +861,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.tk_val = d_val;
     a.nF = state->n_frontier;
     a.n_slices = state->n_slices;
+    a.B = dags->B;
     a.D = dags->D;
     a.M = dags->M;
     a.K = state->K;

@@ -71,7 +71,7 @@ struct ScoreLaunch {
     float *tk_val;
     int32_t topk;
     int64_t nF, n_slices;
-    int32_t D, M, K, max_shard, beta_uniform, slice;
+    int32_t B, D, M, K, max_shard, beta_uniform, slice;
     float beta0;
     int32_t topo;  // descendant lists by topological level (FATE_LEVELS_TOPO)
     int32_t Hpack;      // horizon the descendant lists were packed with

@@ -1529,11 +1529,12 @@ __global__ __launch_bounds__(kBlock) void k_topk(TopkLaunch a) {
 
 // ---- k_rows: one horizon row per lane ---------------------------------------
 // For frontiers whose stages have single-device candidates only, with a
-// uniform off-diagonal beta, D <= 16 and no scoring variant.  A workgroup
-// takes one slice of an instance's frontier, as k_score does, and stages the
-// same instance tables in LDS (prefix-group table, per-(model, device) cost
-// terms, residency after each Load).  Then:
-//   rows     the slice's (frontier stage v, horizon row w) pairs are cut into
+// uniform off-diagonal beta, D <= 16 and no scoring variant.  One workgroup
+// per instance: it stages the instance's tables in LDS once (prefix-group
+// table, per-(model, device) cost terms, and, per pair of models, the devices
+// where loading the first flips the residency of the second), then takes the
+// instance's frontier in chunks of kRowsChunk stages:
+//   rows     the chunk's (frontier stage v, horizon row w) pairs are cut into
 //            tasks of at most L consecutive rows of one stage, one task per
 //            lane.  For each row the lane walks the devices d' in registers:
 //            B(d') = c_hat(w, d' | s) (+infinity where w is infeasible), and,
@@ -1559,26 +1560,32 @@ struct alignas(16) StageR {
     uint32_t q0, nq;     // first task of the stage and number of tasks
     uint16_t dn, npar;
     uint8_t model, pad0;
-    uint16_t pad1;
-    uint32_t pfm, pad2;  // devices caching grp(v)
+    uint16_t h0;         // devices holding the first completed parent's output (D <= 16)
+    float s0;            // its output size
+    uint32_t pfm;        // devices caching grp(v)
 };
 static_assert(sizeof(StageR) == 64, "StageR");
 
+constexpr int kRowsChunk = 128;  // frontier stages per chunk of an instance
+
 // floats per model row of the rows' cost table: (exec + switch term, switch
-// magnitude) per device, padded to a multiple of four floats plus four
+// magnitude) per device, plus four (rows of different models start on
+// different LDS banks)
 __host__ __device__ constexpr int rows_stride(int nd) { return 2 * nd + 4; }
 
 struct RowsPlan {
-    uint32_t pkey, pmask, rho, cap, wt, fits, wait, gpow, cst, rtab, rnew, fl, stages, tasks, part, misc, total;
+    uint32_t pkey, pmask, rho, cap, wt, fits, wait, gpow, cst, rtab, fl, stages, tasks, part, misc, total;
+    uint32_t ntask;  // task capacity
 };
 
-// tasks of a slice: at most max(threads, slice length)
-__host__ __device__ inline int rows_task_cap(int slice, int blk) { return slice > blk ? slice : blk; }
-
-__host__ __device__ inline RowsPlan rows_plan(int D, int K, int M, int slice, int nd, int blk) {
+// The task sums are stored as float4 columns: column j of task t at
+// part4[j * (ntask + 1) + t], so that lanes of consecutive tasks store to
+// consecutive 16-byte slots, and the group reading a task's columns reads
+// different banks.
+__host__ __device__ inline RowsPlan rows_plan(int D, int K, int M, int nd, int blk) {
     RowsPlan q;
     const uint32_t T = 1u << table_log2(D, K);
-    const uint32_t cap = (uint32_t)rows_task_cap(slice, blk);
+    q.ntask = (uint32_t)(kRowsChunk > blk ? kRowsChunk : blk);
     uint32_t o = 0;
     q.pkey = o; o += 8 * T;
     q.pmask = o; o += 4 * T;
@@ -1592,59 +1599,42 @@ __host__ __device__ inline RowsPlan rows_plan(int D, int K, int M, int slice, in
     o = (o + 15u) & ~15u;
     q.cst = o; o += (uint32_t)sizeof(CostS) * (uint32_t)(M * D);
     q.rtab = o; o += 4 * (uint32_t)(M * rows_stride(nd));
-    q.rnew = o; o += 4 * (uint32_t)(M * D);
     q.fl = o; o += 4 * (uint32_t)(M * M);
     o = (o + 15u) & ~15u;
-    q.stages = o; o += (uint32_t)sizeof(StageR) * (uint32_t)slice;
-    q.tasks = o; o += 4 * cap;
+    q.stages = o; o += (uint32_t)sizeof(StageR) * (uint32_t)kRowsChunk;
+    q.tasks = o; o += 4 * q.ntask;
     o = (o + 15u) & ~15u;
-    q.part = o; o += 4 * (uint32_t)nd * cap;
-    q.misc = o; o += 4 * 32;
+    q.part = o; o += 16 * (uint32_t)(nd / 4) * (q.ntask + 1);
+    q.misc = o; o += 4 * 16;
     q.total = (o + 15u) & ~15u;
     return q;
 }
 
-// Exclusive prefix sum over the workgroup of one value per thread; total
-// receives the sum.  sh holds BLK / 64 words; two barriers.
-template <int BLK>
-__device__ __forceinline__ uint32_t block_exscan1(uint32_t x, uint32_t *sh, uint32_t &total) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+// Sum and exclusive prefix sum over the 64 lanes of a wave (all active).
+__device__ __forceinline__ uint32_t wave_exscan_u32(uint32_t x, uint32_t &total) {
+    const int lane = threadIdx.x & 63;
     uint32_t v = x;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
         const uint32_t y = __shfl_up(v, off, 64);
         if (lane >= off) v += y;
     }
-    if (lane == 63) sh[wid] = v;
-    __syncthreads();
-    uint32_t before = 0, all = 0;
-#pragma unroll
-    for (int w = 0; w < BLK / 64; ++w) {
-        const uint32_t t = sh[w];
-        before += w < wid ? t : 0u;
-        all += t;
-    }
-    __syncthreads();
-    total = all;
-    return before + v - x;
+    total = __shfl(v, 63, 64);
+    return v - x;
 }
 
 template <int ND, int BLK>
 __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
-    const uint32_t slice = blockIdx.x;
-    if (a.dcounts && slice >= a.dcounts[2]) return;
+    static_assert(BLK >= kRowsChunk && BLK % 64 == 0, "one thread per stage of a chunk");
+    const int b = (int)blockIdx.x;
     const ParamSet ps = a.ps[blockIdx.y];
     float *const scores = a.scores + (int64_t)a.set_of[blockIdx.y] * a.score_stride;
     extern __shared__ uint64_t smem[];
     uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
     const int tid = threadIdx.x;
     const int D = a.D, K = a.K, M = a.M;
-    const uint32_t b = a.slices[3 * slice];
-    const uint32_t f0 = a.slices[3 * slice + 1];
-    const int nF = min((int)(a.slices[3 * slice + 2] - f0), a.slice);
-    const RowsPlan plan = rows_plan(D, K, M, a.slice, ND, BLK);
-    const int cap_tasks = rows_task_cap(a.slice, BLK);
-    constexpr int CS = rows_stride(ND);
+    const RowsPlan plan = rows_plan(D, K, M, ND, BLK);
+    constexpr int CS = rows_stride(ND), NJ = ND / 4;
     Lds L;
     L.logT = table_log2(D, K);
     L.pkey = reinterpret_cast<uint64_t *>(sb + plan.pkey);
@@ -1658,16 +1648,18 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
     float *gpow = reinterpret_cast<float *>(sb + plan.gpow);
     CostS *cst = reinterpret_cast<CostS *>(sb + plan.cst);
     float *rtab = reinterpret_cast<float *>(sb + plan.rtab);
-    uint32_t *rnew = reinterpret_cast<uint32_t *>(sb + plan.rnew);
     uint32_t *fl = reinterpret_cast<uint32_t *>(sb + plan.fl);
     StageR *stg = reinterpret_cast<StageR *>(sb + plan.stages);
     uint32_t *tasks = reinterpret_cast<uint32_t *>(sb + plan.tasks);
-    float *part = reinterpret_cast<float *>(sb + plan.part);
+    float4 *part4 = reinterpret_cast<float4 *>(sb + plan.part);
+    float *partf = reinterpret_cast<float *>(sb + plan.part);
     uint32_t *misc = reinterpret_cast<uint32_t *>(sb + plan.misc);
+    const uint32_t pcol = plan.ntask + 1;  // float4 slots per column of task sums
 
-    // ---- prologue: instance tables and the slice's stages
+    // ---- prologue: the instance's frontier range and tables
     const int T = 1 << L.logT;
     for (int i = tid; i < T; i += BLK) { L.pkey[i] = 0; pmask[i] = 0u; }
+    for (int i = tid; i < M * M; i += BLK) fl[i] = 0u;
     if (tid < D) {
         rho[tid] = a.resident[(int64_t)b * D + tid];
         wait[tid] = fmaxf(0.0f, a.tau[(int64_t)b * D + tid] - a.tnow[b]);
@@ -1696,38 +1688,6 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
         rtab[m * CS + 2 * d] = sw0;  // devices past D: never feasible
         rtab[m * CS + 2 * d + 1] = ks;
     }
-    for (int i = tid; i < nF; i += BLK) {
-        const uint32_t v = a.frontier[2 * (f0 + i)];
-        const StageRec r = a.rec[v];
-        StageR s;
-        s.elig = r.elig;
-        s.hash = r.hash;
-        s.tokens = r.tokens;
-        s.sigma = r.sigma;
-        s.e0 = a.desc_off[v];
-        uint32_t n = a.desc_off[v + 1] - s.e0;
-        if (ps.H < a.Hpack && n > 0) {  // entries are ordered by depth: those within H form a prefix
-            uint32_t lo = 0, hi = n;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi) >> 1;
-                if ((int)(a.desc[s.e0 + mid] >> kDescDepthShift) <= ps.H) lo = mid + 1;
-                else hi = mid;
-            }
-            n = lo;
-        }
-        s.n = n;
-        s.c0 = a.cand_off[f0 + i];
-        s.dbeg = a.done_off[v];
-        s.dn = (uint16_t)(a.done_off[v + 1] - s.dbeg);
-        s.npar = r.npar;
-        s.model = r.model;
-        s.pad0 = 0;
-        s.pad1 = 0;
-        s.q0 = s.nq = 0;
-        s.pfm = 0;
-        s.pad2 = 0;
-        stg[i] = s;
-    }
     constexpr int kPre = 4;  // prefix-cache entries fetched before the barrier
     uint64_t pre[kPre];
 #pragma unroll
@@ -1735,7 +1695,19 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
         const int i = tid + r * BLK;
         pre[r] = i < D * K ? a.pcache[(int64_t)b * D * K + i] : 0ull;
     }
+    if (tid < 64) {  // the instance's frontier range (the frontier is ordered by instance)
+        const int64_t nFc = a.dcounts ? (int64_t)a.dcounts[0] : a.nF;
+        const int64_t lo = first_slot_of_wave(a.frontier, nFc, (uint32_t)b);
+        const int64_t hi = first_slot_of_wave(a.frontier, nFc, (uint32_t)b + 1u);
+        if (tid == 0) {
+            misc[0] = (uint32_t)lo;
+            misc[1] = (uint32_t)(hi - lo);
+        }
+    }
     __syncthreads();
+    const int64_t lo = misc[0];
+    const int nFi = (int)misc[1];
+    if (nFi == 0) return;  // uniform
 #pragma unroll
     for (int r = 0; r < kPre; ++r)
         if (pre[r] != 0) table_insert<uint32_t>(L, pre[r], (tid + r * BLK) / K);
@@ -1743,216 +1715,256 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
         const uint64_t h = a.pcache[(int64_t)b * D * K + i];
         if (h != 0) table_insert<uint32_t>(L, h, i / K);
     }
-    for (int i = tid; i < M * D; i += BLK) {  // residency of d after loading m
-        const int m = i / D, d = i - m * D;
-        rnew[i] = (uint32_t)load_model(rho[d], m, capd[d], wt);
-    }
-    // tasks: rows per task L = ceil(R / max(1, cap - S)) over the slice's R
-    // rows in S stages with rows, so that at most cap tasks cover them
-    constexpr int kSpt = 2;  // stages per thread (slices hold at most 2 * BLK stages)
-    uint32_t nrow[kSpt], rsum = 0, ssum = 0;
-#pragma unroll
-    for (int j = 0; j < kSpt; ++j) {
-        const int i = tid * kSpt + j;
-        nrow[j] = i < nF ? stg[i].n : 0u;
-        rsum += nrow[j];
-        ssum += nrow[j] ? 1u : 0u;
-    }
-    uint32_t R = 0, S = 0;
-    (void)block_exscan1<BLK>(rsum, misc, R);
-    (void)block_exscan1<BLK>(ssum, misc + 8, S);
-    const uint32_t room = (uint32_t)cap_tasks > S ? (uint32_t)cap_tasks - S : 1u;
-    const uint32_t Lr = R > 0 ? max(1u, (R + room - 1u) / room) : 1u;
-    uint32_t nq[kSpt], qsum = 0;
-#pragma unroll
-    for (int j = 0; j < kSpt; ++j) {
-        nq[j] = (nrow[j] + Lr - 1u) / Lr;
-        qsum += nq[j];
-    }
-    uint32_t ntask = 0;
-    uint32_t q0 = block_exscan1<BLK>(qsum, misc + 16, ntask);
-#pragma unroll
-    for (int j = 0; j < kSpt; ++j) {
-        const int i = tid * kSpt + j;
-        if (i < nF) {
-            stg[i].q0 = q0;
-            stg[i].nq = nq[j];
-            stg[i].pfm = table_find<uint32_t>(L, stg[i].hash);
-            for (uint32_t p = 0; p < nq[j]; ++p) tasks[q0 + p] = (uint32_t)i | (p << 16);
-        }
-        q0 += nq[j];
-    }
-    // Load's effect on m(w)'s residency: per (m(v), m(w)), the devices where
+    // Load's effect on m(w)'s residency, per (m(v), m(w)): the devices where
     // it flips (high half) and where m(w) becomes resident (low half)
-    for (int i = tid; i < M * M; i += BLK) {
-        const int mv = i / M, mw = i - mv * M;
-        uint32_t ld = 0, fp = 0;
-        for (int d = 0; d < D; ++d) {
-            const uint64_t r0 = rho[d], r1 = rnew[mv * D + d];
-            fp |= (uint32_t)((r0 ^ r1) >> mw & 1ull) << d;
-            ld |= (uint32_t)((r1 & ~r0) >> mw & 1ull) << d;
+    for (int i = tid; i < M * D; i += BLK) {
+        const int m = i / D, d = i - m * D;
+        const uint64_t r0 = rho[d], r1 = load_model(r0, m, capd[d], wt);
+        const uint64_t ldm = r1 & ~r0;
+        for (uint64_t x = r0 ^ r1; x; x &= x - 1) {
+            const int mw = __builtin_ctzll(x);
+            atomicOr(&fl[m * M + mw], (1u << (16 + d)) | ((uint32_t)((ldm >> mw) & 1ull) << d));
         }
-        fl[i] = ld | (fp << 16);
     }
     __syncthreads();
 
-    // ---- rows
     const float lam_tr = ps.lam_tr, lam_c = ps.lam_c, lam_p = ps.lam_p, b0 = a.beta0;
     const uint32_t dmask = (1u << D) - 1u;  // D <= 16
-    for (int t = tid; t < (int)ntask; t += BLK) {
-        const uint32_t tk = tasks[t];
-        const int si = (int)(tk & 0xffffu);
-        const uint32_t pt = tk >> 16;
-        const StageR s = stg[si];
-        const uint32_t r0 = pt * Lr, r1 = min(s.n, r0 + Lr);
-        const uint64_t hv = s.hash;
-        const float t0 = lam_tr * s.sigma * b0;  // v's output to one more device
-        const uint32_t *flr = fl + (uint32_t)s.model * (uint32_t)M;
-        float *scr = part + (size_t)t * ND;  // the task's row copy, then its sums
-        float f[ND];
-#pragma unroll
-        for (int d = 0; d < ND; ++d) f[d] = 0.0f;
-        for (uint32_t r = r0; r < r1; ++r) {
-            const uint32_t ent = a.desc[s.e0 + r];
-            const uint32_t w = ent & kDescIdMask;
-            const int depth = (int)(ent >> kDescDepthShift);
-            const StageRec rw = a.rec[w];
-            const uint32_t db = a.done_off[w];
-            const uint32_t dn = a.done_off[w + 1] - db;
-            const uint32_t mw = rw.model;
-            const uint32_t feas = (uint32_t)(rw.elig & fits[mw]) & dmask;
-            const uint32_t pfo = table_find<uint32_t>(L, rw.hash);
-            const bool same = rw.hash != 0 && rw.hash == hv;
-            const float gh = gpow[depth];
-            const float pfp = lam_p * ps.kpf * rw.tokens;
-            const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
-            const uint32_t flw = flr[mw];
-            const uint32_t ld = flw & 0xffffu, flip = flw >> 16;
-            const float *crow = rtab + mw * CS;
-            // B without the completed parents: cost with the switch term, less the prefix benefit
-            float B[ND];
-#pragma unroll
-            for (int j = 0; j < ND / 2; ++j) {
-                const float4 c = *reinterpret_cast<const float4 *>(crow + 4 * j);
-                B[2 * j] = c.x - __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)pfo, 2 * j, 1u));
-                B[2 * j + 1] = c.z - __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)pfo, 2 * j + 1, 1u));
-            }
-            // completed parents: every one's transfer (all remote), and on the
-            // devices holding one its transfer saved and the colocation share
-            float xb = 0.0f;
-            if (dn > 0) {
-#pragma unroll
-                for (int j = 0; j < ND / 4; ++j)
-                    *reinterpret_cast<float4 *>(scr + 4 * j) = make_float4(B[4 * j], B[4 * j + 1], B[4 * j + 2], B[4 * j + 3]);
-                for (uint32_t q = 0; q < dn; ++q) {
-                    const DoneParent pu = a.done[db + q];
-                    const float tq = lam_tr * b0 * pu.sigma;
-                    xb += tq;
-                    const float pw = tq + cw;
-                    for (uint32_t h = (uint32_t)pu.holders & dmask; h; h &= h - 1u) scr[__builtin_ctz(h)] -= pw;
-                }
-#pragma unroll
-                for (int j = 0; j < ND / 4; ++j) {
-                    const float4 c = *reinterpret_cast<const float4 *>(scr + 4 * j);
-                    B[4 * j] = c.x; B[4 * j + 1] = c.y; B[4 * j + 2] = c.z; B[4 * j + 3] = c.w;
-                }
-            }
-            // feasibility, and the two smallest values of the row
-            float m1 = inf_f(), m2 = inf_f();
-#pragma unroll
-            for (int d = 0; d < ND; ++d) {
-                const uint32_t fm = (uint32_t)__builtin_amdgcn_sbfe((int)feas, d, 1u);
-                const float x = __uint_as_float((fm & __float_as_uint(B[d] + xb)) | (~fm & __float_as_uint(inf_f())));
-                B[d] = x;
-                m2 = __builtin_amdgcn_fmed3f(m1, x, m2);
-                m1 = fminf(m1, x);
-            }
-            const bool child = depth == 1;
-            const float m1c = child ? m1 + t0 : m1, m2c = child ? m2 + t0 : m2;
-            const float cwc = child ? cw : 0.0f;
-            // devices that gain grp(w) once v runs there
-            const uint32_t gain = same ? (~pfo & dmask) : 0u;
-#pragma unroll
-            for (int j = 0; j < ND / 2; ++j) {
-                const float4 c = *reinterpret_cast<const float4 *>(crow + 4 * j);
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int d = 2 * j + u;
-                    const float ksr = u == 0 ? c.y : c.w;
-                    // m(w)'s switch term on d flips when v's Load changes its
-                    // residency there: down by the magnitude when loaded, up when evicted
-                    const float dsw = __uint_as_float((__builtin_amdgcn_ubfe(ld, d, 1u) << 31) |
-                                                      (__float_as_uint(ksr) & (uint32_t)__builtin_amdgcn_sbfe((int)flip, d, 1u)));
-                    const float gp = __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)gain, d, 1u));
-                    const float C = ((B[d] - cwc) + dsw) - gp;
-                    const float o = B[d] == m1 ? m2c : m1c;
-                    f[d] += gh * fminf(o, C);
-                }
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < ND / 4; ++j)
-            *reinterpret_cast<float4 *>(scr + 4 * j) = make_float4(f[4 * j], f[4 * j + 1], f[4 * j + 2], f[4 * j + 3]);
-    }
-    __syncthreads();
-
-    // ---- combine: immediate cost plus the stage's task sums; scores
     constexpr int G = ND, kGroups = BLK / G;
     const int lane = tid & (G - 1);
     const bool live = lane < D;
     const int dl = live ? lane : D - 1;
     const bool lane_rank = a.topk > 0 && a.topk <= kLaneTopk;
-    for (int i = tid / G; i < nF; i += kGroups) {  // uniform within the group
-        const StageR s = stg[i];
-        float tr = 0.0f, cnt = 0.0f;
-        for (int q0 = 0; q0 < (int)s.dn; q0 += G) {  // each completed parent to the whole group, in order
-            uint32_t h = 0u;
-            float sg = 0.0f;
-            if (q0 + lane < (int)s.dn) {
-                const DoneParent pu = a.done[s.dbeg + q0 + lane];
-                h = (uint32_t)pu.holders;
-                sg = pu.sigma;
+
+    for (int c0 = 0; c0 < nFi; c0 += kRowsChunk) {  // uniform: chunks of the instance's frontier
+        const int nC = min(kRowsChunk, nFi - c0);
+        const int64_t fc = lo + c0;  // frontier slot of the chunk's first stage
+        if (tid < nC) {  // stage records, descendant ranges, v's first completed parent
+            const uint32_t v = a.frontier[2 * (fc + tid)];
+            const StageRec r = a.rec[v];
+            StageR s;
+            s.elig = r.elig;
+            s.hash = r.hash;
+            s.tokens = r.tokens;
+            s.sigma = r.sigma;
+            s.e0 = a.desc_off[v];
+            uint32_t n = a.desc_off[v + 1] - s.e0;
+            if (ps.H < a.Hpack && n > 0) {  // entries are ordered by depth: those within H form a prefix
+                uint32_t l0 = 0, l1 = n;
+                while (l0 < l1) {
+                    const uint32_t mid = (l0 + l1) >> 1;
+                    if ((int)(a.desc[s.e0 + mid] >> kDescDepthShift) <= ps.H) l0 = mid + 1;
+                    else l1 = mid;
+                }
+                n = l0;
             }
-            const int nq = min(G, (int)s.dn - q0);
-            for (int j = 0; j < nq; ++j) {
-                const uint32_t hj = (uint32_t)__shfl((int)h, j, G);
-                const float sj = __shfl(sg, j, G);
-                const bool local = ((hj >> dl) & 1u) != 0;
-                cnt += local ? 1.0f : 0.0f;
-                tr += local ? 0.0f : sj * b0;
+            s.n = n;
+            s.c0 = a.cand_off[fc + tid];
+            s.dbeg = a.done_off[v];
+            s.dn = (uint16_t)(a.done_off[v + 1] - s.dbeg);
+            s.npar = r.npar;
+            s.model = r.model;
+            s.pad0 = 0;
+            s.h0 = 0;
+            s.s0 = 0.0f;
+            if (s.dn > 0) {
+                const DoneParent pu = a.done[s.dbeg];
+                s.h0 = (uint16_t)pu.holders;
+                s.s0 = pu.sigma;
             }
+            s.q0 = s.nq = 0;
+            s.pfm = table_find<uint32_t>(L, r.hash);
+            stg[tid] = s;
         }
-        const CostS c = cst[s.model * D + dl];
-        const float pf_v = ((s.pfm >> dl) & 1u) ? ps.kpf * s.tokens : 0.0f;
-        const float colo = s.npar ? cnt * fast_rcp((float)s.npar) : 0.0f;
-        const float a_imm = ps.lam_q * wait[dl] + c.swo - lam_c * colo;
-        const float b_imm = c.exec + lam_tr * tr - lam_p * pf_v;
-        double acc = 0.0;
-        for (uint32_t t = 0; t < s.nq; ++t) acc += (double)part[(size_t)(s.q0 + t) * ND + lane];
-        const bool feas_v = live && bit(s.elig, lane) && bit(fits[s.model], lane);
-        const float psi = feas_v ? (float)(-((double)(a_imm + b_imm) + acc)) : -inf_f();
-        if (live) scores[s.c0 + lane] = psi;
-        if (a.topk > 0) {
-            if (lane_rank) {  // the stage's record slot takes its score bits
-                reinterpret_cast<uint32_t *>(stg + i)[lane] = live ? topk_bits(psi) : 0u;
-            } else {
-                const int64_t f = (int64_t)f0 + i;
-                uint32_t sbits[1] = {live ? topk_bits(psi) : 0u};
-                const uint32_t ci[1] = {(uint32_t)lane};
-                group_topk_at<G, 1>(sbits, ci, lane, a.topk, a.tk_idx + f * a.topk, a.tk_val + f * a.topk);
-            }
-        }
-    }
-    if (lane_rank) {  // uniform over the block
         __syncthreads();
-        for (int i = tid; i < nF; i += BLK) {
-            const uint32_t *slot = reinterpret_cast<const uint32_t *>(stg + i);
-            uint32_t x[16];
-#pragma unroll
-            for (int q = 0; q < 16; ++q) x[q] = q < ND ? slot[q] : 0u;
-            const int64_t f = (int64_t)f0 + i;
-            lane_topk16(x, a.topk, a.tk_idx + f * a.topk, a.tk_val + f * a.topk);
+        if (tid < 64) {  // tasks: L = ceil(R / max(1, cap - S)) rows each over the chunk's R rows in S stages
+            const int i0 = 2 * tid, i1 = 2 * tid + 1;
+            const uint32_t n0 = i0 < nC ? stg[i0].n : 0u, n1 = i1 < nC ? stg[i1].n : 0u;
+            uint32_t R = 0, S = 0;
+            (void)wave_exscan_u32(n0 + n1, R);
+            (void)wave_exscan_u32((n0 ? 1u : 0u) + (n1 ? 1u : 0u), S);
+            const uint32_t room = plan.ntask > S ? plan.ntask - S : 1u;
+            const uint32_t Lr = R > 0 ? max(1u, (R + room - 1u) / room) : 1u;
+            const uint32_t q0n = (n0 + Lr - 1u) / Lr, q1n = (n1 + Lr - 1u) / Lr;
+            uint32_t ntask = 0;
+            const uint32_t off = wave_exscan_u32(q0n + q1n, ntask);
+            if (i0 < nC) { stg[i0].q0 = off; stg[i0].nq = q0n; }
+            if (i1 < nC) { stg[i1].q0 = off + q0n; stg[i1].nq = q1n; }
+            for (uint32_t p = 0; p < q0n; ++p) tasks[off + p] = (uint32_t)i0 | (p << 16);
+            for (uint32_t p = 0; p < q1n; ++p) tasks[off + q0n + p] = (uint32_t)i1 | (p << 16);
+            if (tid == 0) {
+                misc[2] = ntask;
+                misc[3] = Lr;
+            }
         }
+        __syncthreads();
+        const int ntask = (int)misc[2];
+        const uint32_t Lr = misc[3];
+
+        // ---- rows
+        for (int t = tid; t < ntask; t += BLK) {
+            const uint32_t tk = tasks[t];
+            const int si = (int)(tk & 0xffffu);
+            const uint32_t pt = tk >> 16;
+            const StageR s = stg[si];
+            const uint32_t r0 = pt * Lr, r1 = min(s.n, r0 + Lr);
+            const uint64_t hv = s.hash;
+            const float t0 = lam_tr * s.sigma * b0;  // v's output to one more device
+            const uint32_t *flr = fl + (uint32_t)s.model * (uint32_t)M;
+            float f[ND];
+#pragma unroll
+            for (int d = 0; d < ND; ++d) f[d] = 0.0f;
+            auto row = [&](uint32_t ent, const StageRec &rw, uint32_t db, uint32_t dn) {
+                const int depth = (int)(ent >> kDescDepthShift);
+                const uint32_t mw = rw.model;
+                const uint32_t feas = (uint32_t)(rw.elig & fits[mw]) & dmask;
+                const uint32_t pfo = table_find<uint32_t>(L, rw.hash);
+                const bool same = rw.hash != 0 && rw.hash == hv;
+                const float gh = gpow[depth];
+                const float pfp = lam_p * ps.kpf * rw.tokens;
+                const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
+                const uint32_t flw = flr[mw];
+                const uint32_t ld = flw & 0xffffu, flip = flw >> 16;
+                const float *crow = rtab + mw * CS;
+                // B without the completed parents: cost with the switch term, less the prefix benefit
+                float B[ND];
+#pragma unroll
+                for (int j = 0; j < ND / 2; ++j) {
+                    const float4 c = *reinterpret_cast<const float4 *>(crow + 4 * j);
+                    B[2 * j] = c.x - __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)pfo, 2 * j, 1u));
+                    B[2 * j + 1] = c.z - __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)pfo, 2 * j + 1, 1u));
+                }
+                // completed parents: every one's transfer (all remote), and on the
+                // devices holding one its transfer saved and the colocation share
+                float xb = 0.0f;
+                if (dn > 0) {  // the row goes through the task's sum slots, indexed by device
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) part4[j * pcol + t] = make_float4(B[4 * j], B[4 * j + 1], B[4 * j + 2], B[4 * j + 3]);
+                    for (uint32_t q = 0; q < dn; ++q) {
+                        const DoneParent pu = a.done[db + q];
+                        const float tq = lam_tr * b0 * pu.sigma;
+                        xb += tq;
+                        const float pw = tq + cw;
+                        for (uint32_t h = (uint32_t)pu.holders & dmask; h; h &= h - 1u) {
+                            const int d = __builtin_ctz(h);
+                            partf[((d >> 2) * pcol + t) * 4 + (d & 3)] -= pw;
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+                        const float4 c = part4[j * pcol + t];
+                        B[4 * j] = c.x; B[4 * j + 1] = c.y; B[4 * j + 2] = c.z; B[4 * j + 3] = c.w;
+                    }
+                }
+                // feasibility, and the two smallest values of the row
+                float m1 = inf_f(), m2 = inf_f();
+#pragma unroll
+                for (int d = 0; d < ND; ++d) {
+                    const uint32_t fm = (uint32_t)__builtin_amdgcn_sbfe((int)feas, d, 1u);
+                    const float x = __uint_as_float((fm & __float_as_uint(B[d] + xb)) | (~fm & __float_as_uint(inf_f())));
+                    B[d] = x;
+                    m2 = __builtin_amdgcn_fmed3f(m1, x, m2);
+                    m1 = fminf(m1, x);
+                }
+                const bool child = depth == 1;
+                const float m1c = child ? m1 + t0 : m1, m2c = child ? m2 + t0 : m2;
+                const float cwc = child ? cw : 0.0f;
+                // devices that gain grp(w) once v runs there
+                const uint32_t gain = same ? (~pfo & dmask) : 0u;
+#pragma unroll
+                for (int j = 0; j < ND / 2; ++j) {
+                    const float4 c = *reinterpret_cast<const float4 *>(crow + 4 * j);
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const int d = 2 * j + u;
+                        const float ksr = u == 0 ? c.y : c.w;
+                        // m(w)'s switch term on d flips when v's Load changes its
+                        // residency there: down by the magnitude when loaded, up when evicted
+                        const float dsw = __uint_as_float((__builtin_amdgcn_ubfe(ld, d, 1u) << 31) |
+                                                          (__float_as_uint(ksr) & (uint32_t)__builtin_amdgcn_sbfe((int)flip, d, 1u)));
+                        const float gp = __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)gain, d, 1u));
+                        const float C = ((B[d] - cwc) + dsw) - gp;
+                        const float o = B[d] == m1 ? m2c : m1c;
+                        f[d] += gh * fminf(o, C);
+                    }
+                }
+            };
+            for (uint32_t r = r0; r < r1; r += 2) {  // two rows' loads in flight together
+                const bool two = r + 1 < r1;
+                const uint32_t e0 = a.desc[s.e0 + r];
+                const uint32_t e1 = two ? a.desc[s.e0 + r + 1] : e0;
+                const StageRec w0 = a.rec[e0 & kDescIdMask];
+                const StageRec w1 = a.rec[e1 & kDescIdMask];
+                const uint32_t db0 = a.done_off[e0 & kDescIdMask], de0 = a.done_off[(e0 & kDescIdMask) + 1];
+                const uint32_t db1 = a.done_off[e1 & kDescIdMask], de1 = a.done_off[(e1 & kDescIdMask) + 1];
+                row(e0, w0, db0, de0 - db0);
+                if (two) row(e1, w1, db1, de1 - db1);
+            }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) part4[j * pcol + t] = make_float4(f[4 * j], f[4 * j + 1], f[4 * j + 2], f[4 * j + 3]);
+        }
+        __syncthreads();
+
+        // ---- combine: immediate cost plus the stage's task sums; scores
+        for (int i = tid / G; i < nC; i += kGroups) {  // uniform within the group
+            const StageR s = stg[i];
+            // completed parents of v, each to the whole group in order; the first was staged
+            float tr = 0.0f, cnt = 0.0f;
+            if (s.dn > 0) {
+                const bool local = ((s.h0 >> dl) & 1u) != 0;
+                cnt += local ? 1.0f : 0.0f;
+                tr += local ? 0.0f : s.s0 * b0;
+            }
+            for (int q0 = 1; q0 < (int)s.dn; q0 += G) {
+                uint32_t h = 0u;
+                float sg = 0.0f;
+                if (q0 + lane < (int)s.dn) {
+                    const DoneParent pu = a.done[s.dbeg + q0 + lane];
+                    h = (uint32_t)pu.holders;
+                    sg = pu.sigma;
+                }
+                const int nq = min(G, (int)s.dn - q0);
+                for (int j = 0; j < nq; ++j) {
+                    const uint32_t hj = (uint32_t)__shfl((int)h, j, G);
+                    const float sj = __shfl(sg, j, G);
+                    const bool local = ((hj >> dl) & 1u) != 0;
+                    cnt += local ? 1.0f : 0.0f;
+                    tr += local ? 0.0f : sj * b0;
+                }
+            }
+            const CostS c = cst[s.model * D + dl];
+            const float pf_v = ((s.pfm >> dl) & 1u) ? ps.kpf * s.tokens : 0.0f;
+            const float colo = s.npar ? cnt * fast_rcp((float)s.npar) : 0.0f;
+            const float a_imm = ps.lam_q * wait[dl] + c.swo - lam_c * colo;
+            const float b_imm = c.exec + lam_tr * tr - lam_p * pf_v;
+            double acc = 0.0;
+            for (uint32_t t = 0; t < s.nq; ++t) acc += (double)partf[((lane >> 2) * pcol + s.q0 + t) * 4 + (lane & 3)];
+            const bool feas_v = live && bit(s.elig, lane) && bit(fits[s.model], lane);
+            const float psi = feas_v ? (float)(-((double)(a_imm + b_imm) + acc)) : -inf_f();
+            if (live) scores[s.c0 + lane] = psi;
+            if (a.topk > 0) {
+                if (lane_rank) {  // the stage's record slot takes its score bits
+                    reinterpret_cast<uint32_t *>(stg + i)[lane] = live ? topk_bits(psi) : 0u;
+                } else {
+                    const int64_t f = fc + i;
+                    uint32_t sbits[1] = {live ? topk_bits(psi) : 0u};
+                    const uint32_t ci[1] = {(uint32_t)lane};
+                    group_topk_at<G, 1>(sbits, ci, lane, a.topk, a.tk_idx + f * a.topk, a.tk_val + f * a.topk);
+                }
+            }
+        }
+        if (lane_rank) {  // uniform over the block
+            __syncthreads();
+            if (tid < nC) {
+                const uint32_t *slot = reinterpret_cast<const uint32_t *>(stg + tid);
+                uint32_t x[16];
+#pragma unroll
+                for (int q = 0; q < 16; ++q) x[q] = q < ND ? slot[q] : 0u;
+                const int64_t f = fc + tid;
+                lane_topk16(x, a.topk, a.tk_idx + f * a.topk, a.tk_val + f * a.topk);
+            }
+        }
+        __syncthreads();  // the next chunk reuses the stage slots and task sums
     }
 }
 
@@ -2007,22 +2019,22 @@ bool score_fits(int D, int K, int M, int beta_uniform) {
     return score_shape(D, K, M, slice_len(D), beta_uniform != 0, sh);
 }
 
-// Threads of a k_rows workgroup (a slice holds at most twice as many stages).
+// Threads of a k_rows workgroup.
 constexpr int kRowsBlock = 256;
 
 // k_rows takes frontiers with single-device candidates only, uniform beta,
 // D <= 16, at most 32 models and parameter sets without a scoring variant,
 // when its LDS fits.
 static bool rows_fit(const ScoreLaunch &a) {
-    if (!a.beta_uniform || !a.singles || a.topo || a.D > 16 || a.M > 32 || a.slice > 2 * kRowsBlock) return false;
+    if (!a.beta_uniform || !a.singles || a.topo || a.D > 16 || a.M > 32) return false;
     const int nd = a.D <= 4 ? 4 : a.D <= 8 ? 8 : 16;
-    return rows_plan(a.D, a.K, a.M, a.slice, nd, kRowsBlock).total <= kLdsLimit;
+    return rows_plan(a.D, a.K, a.M, nd, kRowsBlock).total <= kLdsLimit;
 }
 
 static void launch_rows(const ScoreLaunch &a, hipStream_t s) {
     const int nd = a.D <= 4 ? 4 : a.D <= 8 ? 8 : 16;
-    const size_t lds = rows_plan(a.D, a.K, a.M, a.slice, nd, kRowsBlock).total;
-    const dim3 grid((unsigned)a.n_slices, (unsigned)a.nsets), block((unsigned)kRowsBlock);
+    const size_t lds = rows_plan(a.D, a.K, a.M, nd, kRowsBlock).total;
+    const dim3 grid((unsigned)a.B, (unsigned)a.nsets), block((unsigned)kRowsBlock);
     switch (nd) {
         case 4: hipLaunchKernelGGL((k_rows<4, kRowsBlock>), grid, block, lds, s, a); break;
         case 8: hipLaunchKernelGGL((k_rows<8, kRowsBlock>), grid, block, lds, s, a); break;
