@@ -1557,7 +1557,7 @@ struct alignas(16) StageR {
     float tokens, sigma;
     uint32_t e0, n;      // first descendant entry; rows within the horizon
     uint32_t c0, dbeg;   // first score; first completed parent
-    uint32_t q0, nq;     // first task of the stage and number of tasks
+    uint32_t q0, nq;     // first full-length task and their number; the tail task (or 0xffffffff)
     uint16_t dn, npar;
     uint8_t model, pad0;
     uint16_t h0;         // devices holding the first completed parent's output (D <= 16)
@@ -1777,7 +1777,12 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             stg[tid] = s;
         }
         __syncthreads();
-        if (tid < 64) {  // tasks: L = ceil(R / max(1, cap - S)) rows each over the chunk's R rows in S stages
+        if (tid < 64) {
+            // tasks of L = ceil(R / max(1, cap - S)) rows over the chunk's R rows
+            // in S stages (at most cap tasks): every stage's full-length tasks
+            // first, then its shorter tail task; the tail tasks ordered by
+            // length, longest first (ties by stage), so that the lanes of a
+            // wave run the same number of rows
             const int i0 = 2 * tid, i1 = 2 * tid + 1;
             const uint32_t n0 = i0 < nC ? stg[i0].n : 0u, n1 = i1 < nC ? stg[i1].n : 0u;
             uint32_t R = 0, S = 0;
@@ -1785,15 +1790,51 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             (void)wave_exscan_u32((n0 ? 1u : 0u) + (n1 ? 1u : 0u), S);
             const uint32_t room = plan.ntask > S ? plan.ntask - S : 1u;
             const uint32_t Lr = R > 0 ? max(1u, (R + room - 1u) / room) : 1u;
-            const uint32_t q0n = (n0 + Lr - 1u) / Lr, q1n = (n1 + Lr - 1u) / Lr;
-            uint32_t ntask = 0;
-            const uint32_t off = wave_exscan_u32(q0n + q1n, ntask);
-            if (i0 < nC) { stg[i0].q0 = off; stg[i0].nq = q0n; }
-            if (i1 < nC) { stg[i1].q0 = off + q0n; stg[i1].nq = q1n; }
-            for (uint32_t p = 0; p < q0n; ++p) tasks[off + p] = (uint32_t)i0 | (p << 16);
-            for (uint32_t p = 0; p < q1n; ++p) tasks[off + q0n + p] = (uint32_t)i1 | (p << 16);
+            const uint32_t f0n = n0 / Lr, f1n = n1 / Lr, t0n = n0 - f0n * Lr, t1n = n1 - f1n * Lr;
+            uint32_t nfull = 0;
+            const uint32_t off = wave_exscan_u32(f0n + f1n, nfull);
+            // tail tasks by length buckets, longest first: a count per bucket,
+            // then each tail takes the next slot of its bucket (which lane
+            // runs which task does not change any sum: a stage adds its full
+            // tasks, then its tail)
+            uint32_t *bkt = reinterpret_cast<uint32_t *>(partf);  // scratch until the rows write their sums
+            constexpr uint32_t kBuckets = 32;
+            auto bucket = [&](uint32_t len) { return len >= kBuckets ? kBuckets - 1u : len; };
+            if (tid < (int)kBuckets) bkt[tid] = 0u;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (i0 < nC && t0n) atomicAdd(&bkt[bucket(t0n)], 1u);
+            if (i1 < nC && t1n) atomicAdd(&bkt[bucket(t1n)], 1u);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const uint32_t cb = tid < (int)kBuckets ? bkt[kBuckets - 1u - (uint32_t)tid] : 0u;  // longest first
+            uint32_t ntail = 0;
+            const uint32_t start = nfull + wave_exscan_u32(cb, ntail);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (tid < (int)kBuckets) bkt[kBuckets - 1u - (uint32_t)tid] = start;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const uint32_t k0 = (i0 < nC && t0n) ? atomicAdd(&bkt[bucket(t0n)], 1u) : 0u;
+            const uint32_t k1 = (i1 < nC && t1n) ? atomicAdd(&bkt[bucket(t1n)], 1u) : 0u;
+            if (i0 < nC) {
+                stg[i0].q0 = off | (f0n << 16);
+                stg[i0].nq = t0n ? k0 : 0xffffffffu;
+                if (t0n) tasks[k0] = (uint32_t)i0 | (f0n << 16);
+            }
+            if (i1 < nC) {
+                stg[i1].q0 = (off + f0n) | (f1n << 16);
+                stg[i1].nq = t1n ? k1 : 0xffffffffu;
+                if (t1n) tasks[k1] = (uint32_t)i1 | (f1n << 16);
+            }
+            for (uint32_t p = 0; p < f0n; ++p) tasks[off + p] = (uint32_t)i0 | (p << 16);
+            for (uint32_t p = 0; p < f1n; ++p) tasks[off + f0n + p] = (uint32_t)i1 | (p << 16);
             if (tid == 0) {
-                misc[2] = ntask;
+                misc[2] = nfull + ntail;
                 misc[3] = Lr;
             }
         }
@@ -1937,8 +1978,10 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             const float colo = s.npar ? cnt * fast_rcp((float)s.npar) : 0.0f;
             const float a_imm = ps.lam_q * wait[dl] + c.swo - lam_c * colo;
             const float b_imm = c.exec + lam_tr * tr - lam_p * pf_v;
-            double acc = 0.0;
-            for (uint32_t t = 0; t < s.nq; ++t) acc += (double)partf[((lane >> 2) * pcol + s.q0 + t) * 4 + (lane & 3)];
+            double acc = 0.0;  // full-length tasks in row order, then the tail
+            const uint32_t qf = s.q0 & 0xffffu, nf = s.q0 >> 16;
+            for (uint32_t t = 0; t < nf; ++t) acc += (double)partf[((lane >> 2) * pcol + qf + t) * 4 + (lane & 3)];
+            if (s.nq != 0xffffffffu) acc += (double)partf[((lane >> 2) * pcol + s.nq) * 4 + (lane & 3)];
             const bool feas_v = live && bit(s.elig, lane) && bit(fits[s.model], lane);
             const float psi = feas_v ? (float)(-((double)(a_imm + b_imm) + acc)) : -inf_f();
             if (live) scores[s.c0 + lane] = psi;
