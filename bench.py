@@ -115,11 +115,30 @@ def counted_work(w, pk, st, scores_host, H):
                                                             per_stage=per_stage, stage_inst=fb)
 
 
+def score_kernel(w, params) -> str:
+    """Which scoring kernel the library launches for this batch (a label for
+    the report): k_rows for frontiers of single-device candidates with a
+    uniform off-diagonal beta, D <= 16, at most 32 models and no scoring
+    variant; k_score otherwise."""
+    off = w.beta[~np.eye(w.D, dtype=bool)]
+    uniform = off.size == 0 or bool(np.all(off == off[0]))
+    singles = min(int(np.max(w.shard_max)) if w.N else 1, int(w.max_shard), int(w.D)) <= 1
+    variant = bool(w.params.get("topo_levels")) or params.lam_m != 0.0 or params.flags != 0
+    return "k_rows" if uniform and singles and w.D <= 16 and w.M <= 32 and not variant else "k_score"
+
+
 def read_counters(workload: str):
     """HBM traffic and VALU instructions per launch of the score kernel from
     the committed rocprofv3 counter runs, if they were taken on the current
     kernel source: (hbm bytes or None, SQ_INSTS_VALU or None)."""
-    path = os.path.join(ROOT, "profiles", "k_score_%s_counters.txt" % workload)
+    for kern in ("k_rows", "k_score"):
+        hbm, valu = read_counter_file(os.path.join(ROOT, "profiles", "%s_%s_counters.txt" % (kern, workload)))
+        if hbm is not None or valu is not None:
+            return hbm, valu
+    return None, None
+
+
+def read_counter_file(path: str):
     if not os.path.exists(path):
         return None, None
     vals = {}
@@ -700,7 +719,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-            "kernel": "k_score (with top-k epilogue)" if args.fused else "k_score",
+            "kernel": score_kernel(w, params) + (" with the fused top-k" if args.fused else ""),
             "kernel_ms": kern_ms, "copies_rotated": R,
         },
     }

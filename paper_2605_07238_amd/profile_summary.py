@@ -13,6 +13,7 @@ import collections
 import csv
 import hashlib
 import os
+import re
 import sqlite3
 import sys
 
@@ -38,7 +39,8 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace-db")
     ap.add_argument("--pmc", nargs="*", default=[])
-    ap.add_argument("--kernel", default="k_score")
+    ap.add_argument("--kernel", default="k_rows|k_score",
+                    help="regular expression naming the kernel whose counters are summarised")
     ap.add_argument("--copy-bytes", type=int, default=512 << 20)
     ap.add_argument("--kernel-source", nargs="*",
                     help="source files whose joint SHA-256 identifies the profiled kernel and its launch geometry")
@@ -57,7 +59,7 @@ def main():
     for path in args.pmc:
         for kname, cs in counters(path).items():
             for cname, v in cs.items():
-                if args.kernel in kname:
+                if re.search(args.kernel, kname):
                     avg = sum(v) / len(v)
                     kavg[cname] = avg
                     out.append("counter %-20s %-60s avg over %d dispatches: %.1f" % (cname, kname[:60], len(v), avg))
