@@ -731,7 +731,8 @@ def main():
         "frac": valu_g / VALU_PEAK_GIPS if valu_g else None,
         "valu_insts_per_launch": valu_insts,
         "note": "peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per wave64 VALU instruction; instructions from "
-                "profiles/k_score_%s_counters.txt when its kernel source hash matches, else null" % args.workload,
+                "profiles/%s_%s_counters.txt when its kernel source hash matches, else null"
+                % (score_kernel(w, params), args.workload),
     }
     if args.planning_steps > 0:
         out["planning_loop"] = planning_loop(w, pk, params, args.topk, args.planning_steps, log)
