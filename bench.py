@@ -184,11 +184,24 @@ def cpu_per_core(w, H, counts, n_inst=64):
     return evals / (time.perf_counter() - t), n_inst
 
 
+def host_threads() -> int:
+    """Host cores the oracle may use: OMP_NUM_THREADS when the environment
+    sets it (the share of the host given to this process), else every core
+    this process may run on."""
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        return int(env)
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:
+        return max(1, os.cpu_count() or 1)
+
+
 def cpu_baseline(w, H, min_seconds=10.0, max_passes=50):
     """Time the fp64 oracle over the whole batch, repeating passes until at
     least ``min_seconds`` of host work; returns (seconds per pass, passes, threads)."""
     from oracle import oracle
-    threads = min(16, os.cpu_count() or 1)
+    threads = host_threads()
     passes, total = 0, 0.0
     while passes < max_passes and (total < min_seconds or passes == 0):
         t = time.perf_counter()

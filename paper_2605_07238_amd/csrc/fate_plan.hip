@@ -23,7 +23,11 @@
 namespace fate {
 namespace {
 
-constexpr int kPlanCap = 2048;  // choices of one instance staged in LDS
+// Choices of one instance staged in LDS: 16 KB, so that ten one-wave
+// workgroups share a compute unit (2,048 choices, 32 KB, left room for five:
+// 0.083 against 0.055 ms per fork-join wave).  Fork-join instances hold about
+// 460 choices at k = 4.
+constexpr int kPlanCap = 1024;
 
 // Order-preserving map of a finite or +infinite score to a nonzero 32-bit key
 // (a larger score gives a larger key, -0 and +0 the same one); 0 marks "no
