@@ -322,7 +322,8 @@ def sweep_bench(w, k, reps, log):
         % (P, t["sweep"], t["single_calls"]))
     return dict(sets=names, H_packed=H_max, ms=t["sweep"], single_calls_ms=t["single_calls"],
                 evals=evals, evals_per_s=evals / (t["sweep"] * 1e-3), bitwise_equal_to_single_calls=bool(same),
-                kernels="k_score (grid rows = parameter sets) + k_topk")
+                kernels="k_rows for the sets without a variant and k_score for the others (grid rows = "
+                        "parameter sets), then k_topk")
 
 
 def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
