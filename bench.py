@@ -211,29 +211,41 @@ def cpu_baseline(w, H, min_seconds=10.0, max_passes=50):
     return total / passes, passes, threads
 
 
-def commit_bytes(pk, st, w):
-    """Algorithmic bytes of one commit-and-advance on the device, counted from
-    the planning state it produced: every stage's status is read, and a
-    pending stage's record and its parents' statuses; the completed-parent
-    lists, frontier, candidate offsets and slices are written; each
-    (instance, device) state word, free time and prefix slots are read and
-    written; each frontier slot and its selection are read once."""
-    import torch
-    from paper_2605_07238_amd import fate
-    h = st.handle
-    N, B, D, K = int(h.N), int(h.B), int(h.D), int(h.K)
-    nF, nC, nS, _ = st.counts()
-    base = st.buf.data_ptr()
-    off = h.done_off - base
-    n_done = int(st.buf[off + 4 * N:off + 4 * N + 4].view(torch.int32).cpu().item())
-    status = fate.state_arrays(st)["status"]
-    pend = status == 0
-    e_pend = int(np.diff(w.par_off)[pend].sum())
-    return (N + int(pend.sum()) * 32 + e_pend * (4 + 1)  # statuses; pending records, parent ids and statuses
-            + 4 * (N + 1) + 16 * n_done                  # completed-parent offsets and entries
-            + 12 * (nF + 1) + 12 * nS                    # frontier, candidate offsets, slices
-            + 2 * B * D * (8 + 4 + 8 * K)                # resident models, free times, prefix slots
-            + 4 * B + 16)
+def edge_table(w):
+    """Flat parent and child id of every edge of the batch."""
+    npar = np.diff(w.par_off)
+    child = np.repeat(np.arange(w.N, dtype=np.int64), npar)
+    inst = np.repeat(np.arange(w.B, dtype=np.int64), np.diff(w.stage_off))
+    parent = w.stage_off[inst[child]] + w.par_idx.astype(np.int64)
+    return parent, child, npar
+
+
+def commit_bytes(w, edges, front_v, sel, status, nF1, nS1, K, max_shard):
+    """Algorithmic bytes of one commit-and-advance on the device, from the
+    frontier it started from (front_v, its selections sel) and the statuses
+    it left: each frontier slot's id, selection, record and children range
+    are read; a completed stage's holders, status and finish are written and
+    its parents' ids, holders, finish times and sizes read; for each child of
+    a completed stage its id and record, its parents' ids, statuses, holders
+    and sizes are read and its completed-parent entries and count written;
+    each (instance, device) state word, free time and prefix slots are read
+    and written; the new frontier goes through the workspace list (written,
+    read) into its slots and candidate offsets, the slices are written, and
+    the per-instance totals and offsets are written and read."""
+    parent, child, npar = edges
+    B, D = w.B, w.D
+    done = np.zeros(w.N, bool)
+    done[front_v[(sel >= 0) & (status[front_v] == 1)]] = True
+    from_done = done[parent]
+    kids = child[from_done]
+    ndone = np.bincount(child[status[parent] == 1], minlength=w.N)
+    nb = (len(front_v) * (8 + 4 + 32 + 8)
+          + int(done.sum()) * (8 + 1 + 4) + int(npar[done].sum()) * (4 + 8 + 4 + 4)
+          + len(kids) * (4 + 32 + 4) + int(npar[kids].sum()) * (4 + 1 + 8 + 4) + int(ndone[kids].sum()) * 16
+          + 2 * B * D * (8 + 4 + 8 * K)
+          + nF1 * (8 + 4 + 8 + 8 + (32 if max_shard > 1 and D > 1 else 0)) + 12 * nS1
+          + B * (16 + 16 + 8 + 8 + 4 + 4) + 16)
+    return nb
 
 
 def sweep_grid(w, H_max=4):
@@ -344,6 +356,7 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
     sel = torch.empty(cap, dtype=torch.int32, device="cuda")
     ws = torch.empty(max(1, fate.fate_commit_ws_size(pk, st)), dtype=torch.uint8, device="cuda")
     mk = lambda: torch.cuda.Event(enable_timing=True)
+    edges = edge_table(w)
 
     def step():
         fate.fate_score_topk(pk, st, params, k, out=scores, idx=idx, val=val)
@@ -355,6 +368,7 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         nF0 = st.counts()[0]
         if nF0 == 0:
             break
+        front_v = fate.frontier_table(st)[0]  # the frontier the step starts from
         e = [mk() for _ in range(4)]
         # keep the device busy while the host enqueues the step, so that the
         # first event does not also time the host's call overhead
@@ -367,9 +381,11 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         fate.fate_commit_advance(pk, st, sel, ws=ws)
         e[3].record()
         torch.cuda.synchronize()
-        nF1 = st.counts()[0]
-        cb = commit_bytes(pk, st, w)
-        placed = int(torch.count_nonzero(sel[:nF0] >= 0).item())
+        nF1, _, nS1, _ = st.counts()
+        sel_h = sel[:nF0].cpu().numpy()
+        cb = commit_bytes(w, edges, front_v, sel_h, fate.state_arrays(st)["status"], nF1, nS1, int(st.handle.K),
+                          int(st.handle.max_shard))
+        placed = int(np.count_nonzero(sel_h >= 0))
         row = dict(frontier=nF0, placed=placed, next_frontier=nF1, score_topk_ms=e[0].elapsed_time(e[1]),
                    plan_ms=e[1].elapsed_time(e[2]), commit_ms=e[2].elapsed_time(e[3]), commit_bytes=cb)
         rows.append(row)
@@ -384,7 +400,7 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         out.update(commit_ms_mean=float(np.mean(cms)), plan_ms_mean=float(np.mean([r["plan_ms"] for r in timed])),
                    step_ms_mean=float(np.mean([r["score_topk_ms"] + r["plan_ms"] + r["commit_ms"] for r in timed])),
                    commit_roofline={"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                    "frac": achieved / HBM_PEAK_GBS, "kernels": "fate_commit_advance (6 launches)"})
+                                    "frac": achieved / HBM_PEAK_GBS, "kernels": "fate_commit_advance (3 launches)"})
     if full_plan:
         # the rest of the plan, untimed per launch: one event pair around the whole loop
         n = len(rows)

@@ -197,6 +197,9 @@ typedef struct {
     int32_t levels;                       /* FATE_LEVELS_HOP or FATE_LEVELS_TOPO */
     const float *desc_w;                  /* [n_desc] level weights, or null */
     int32_t max_r;                        /* largest shard degree R(v) of the batch */
+    const uint32_t *ch_off;               /* [N+1]: children of flat stage g are */
+    const uint32_t *ch_idx;               /* ch_idx[ch_off[g] .. ch_off[g+1]), ascending flat ids */
+    int64_t max_stages;                   /* stages of the largest instance */
 } fate_dags_t;
 
 /* Packed state of one planning step: plain data pointing into the caller's
@@ -213,11 +216,12 @@ typedef struct {
     int64_t n_slices;
     const uint32_t *slices;   /* [n_slices][3]: instance, first and end frontier slot; the
                                  scoring kernel runs one workgroup per slice */
-    int64_t n_done_edges;
-    const uint32_t *done_off; /* [N+1]: completed parents of pending flat stage g
-                                 are done[done_off[g] .. done_off[g+1]); other
-                                 stages have empty lists */
-    const void *done;         /* 16-byte entries {uint64 holders; float out_bytes; pad} */
+    int64_t n_done_edges;     /* E: every stage has a slot per parent */
+    const uint32_t *done_n;   /* [N]: the completed parents of pending flat stage g,
+                                 in parent order, are done[p .. p + done_n[g]) with
+                                 p = par_off[g], the first of g's |Pa(g)| slots;
+                                 the counts and slots of other stages are stale */
+    const void *done;         /* [E] 16-byte entries {uint64 holders; float out_bytes; pad} */
     /* Planning state (fate_pack_state_advance; all zero otherwise).  Its
      * sections are sized for any later planning step, so n_frontier,
      * n_cand and n_slices above hold those capacities, and the current
@@ -232,6 +236,8 @@ typedef struct {
     int32_t slice;            /* frontier stages per slice the state was cut into;
                                  scoring rejects a state whose slice length differs
                                  from this build's for the DAGs' device count (ESTATE) */
+    const uint32_t *fr_off;   /* [B+1]: instance b's frontier slots are
+                                 fr_off[b] .. fr_off[b+1] (current counts) */
 } fate_state_h;
 
 const char *fate_version(void);
@@ -312,7 +318,7 @@ fate_status_t fate_pack_state_advance(const fate_dags_t *packed, const fate_dag_
                                       void *stream, fate_state_h *out);
 
 /* fate_commit_ws_size: device workspace bytes fate_commit_advance needs
- * (about 16 bytes per stage).  Errors: EINVAL, ESTATE. */
+ * (about 8 bytes per stage).  Errors: EINVAL, ESTATE. */
 fate_status_t fate_commit_ws_size(const fate_dags_t *dags, const fate_state_h *state, size_t *bytes);
 
 /* fate_commit_advance: commit one planning step on the device and advance
@@ -339,8 +345,10 @@ fate_status_t fate_commit_ws_size(const fate_dags_t *dags, const fate_state_h *s
  * A selection past the stage's candidates, or whose candidate has a device
  * that is not eligible or cannot hold the model, is skipped and counted in
  * counts[3].  Afterwards the frontier (pending stages whose parents are all
- * completed), candidate offsets, workgroup slices and completed-parent lists
- * are rebuilt on the device.  t_now is unchanged.
+ * completed), its per-instance offsets, the candidate offsets and the
+ * workgroup slices are rebuilt on the device, and so are the completed-parent
+ * lists of the children of the stages just completed (no other list
+ * changes).  t_now is unchanged.
  * `state` must come from fate_pack_state_advance; its buffer is updated in
  * place.  d_ws: at least fate_commit_ws_size bytes.  Enqueued on `stream`;
  * does not synchronise.

@@ -1,33 +1,33 @@
 // Commit-and-advance of a planning state on the device (Alg. 1: materialise
 // the selected placements, then advance the planning frontier and update the
 // planning state; Alg. 2: commit into the action pool and update the state
-// as the stages complete).  Six launches on the caller's stream:
+// as the stages complete).  Three launches on the caller's stream; only the
+// instances' own frontiers and the children of the stages completed are
+// visited, never the whole batch:
 //
 //   k_commit_apply  one wave per instance.  The wave keeps the instance's
-//                   prefix slots, the exec and switch tables and the model
-//                   weights in LDS.  It takes the frontier slots 64 at a
-//                   time: lane q checks slot q's selection and marks the
-//                   stage completed with its output on the candidate's
-//                   devices; then lane d (device d) applies, in ascending
-//                   stage id, every placement whose candidate contains d:
-//                   start at max(tau, t), switch time if the model was
-//                   absent, Load, prefix slots, free time (summed in fp64
-//                   over the step, stored as fp32).
-//   k_plan_count    per stage (kPlanItems consecutive stages per thread): for
-//                   a pending stage its completed parents, and its candidate
-//                   count when it is now in the frontier (every parent
-//                   completed); workgroup totals.
-//   k_plan_segscan  one workgroup per segment of kPlanSeg workgroup totals:
-//                   offsets within the segment, segment totals.
-//   k_plan_offsets  one workgroup: exclusive scan of the segment totals;
-//                   frontier and candidate totals.  (One workgroup reading
-//                   all the workgroup totals took 31 us: a single compute
-//                   unit keeps too few loads in flight.)
-//   k_plan_fill     per stage: offset and entries of its completed-parent
-//                   list, its frontier slot, instance and first candidate.
-//   k_plan_slices   one workgroup: each instance's frontier range cut into
-//                   workgroup slices for the scoring kernel; the counts the
-//                   scoring and top-k launches read.
+//                   prefix slots, the exec and switch tables, the model
+//                   weights and a bitmap over its stages in LDS.  It takes
+//                   the instance's frontier slots 64 at a time: lane q
+//                   checks slot q's selection and marks the stage completed
+//                   with its output on the candidate's devices, or sets the
+//                   stage's bit (it stays in the frontier); lane d (device d)
+//                   applies, in ascending stage id, every placement whose
+//                   candidate contains d: start at max(tau, t), switch time
+//                   if the model was absent, Load, prefix slots, free time
+//                   (summed in fp64 over the step, stored as fp32).  Then the
+//                   children of the stages just completed, one (stage, child)
+//                   pair per lane: the child's completed-parent list is
+//                   rewritten in its parent slots, and a child whose parents
+//                   are now all completed sets its bit.  The set bits, read
+//                   in order, are the instance's new frontier: stage ids and
+//                   candidate offsets within the instance, and its totals.
+//   k_commit_scan   one workgroup: exclusive scan of the instances' totals
+//                   (frontier stages, candidates, slices, rejected
+//                   selections): frontier offsets per instance and the
+//                   counters the scoring and top-k launches read.
+//   k_commit_fill   one wave per instance: its frontier slots, candidate
+//                   offsets and scoring slices at the scanned offsets.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -39,7 +39,7 @@
 namespace fate {
 namespace {
 
-constexpr uint8_t kPending = FATE_PENDING, kCompleted = FATE_COMPLETED;
+constexpr uint8_t kCompleted = FATE_COMPLETED;
 
 // Exclusive scan over the workgroup (NT threads, a multiple of 64) of F
 // fields at once; total[] receives the sums.  sh holds F * NT / 64 words.
@@ -80,47 +80,8 @@ __device__ void block_exscan(const uint32_t (&x)[F], uint32_t *sh, uint32_t (&ex
     __syncthreads();  // sh may be reused
 }
 
-// Parents whose loads one thread issues together in the planning scans.
+// Parents whose loads one lane issues together.
 constexpr int kParBatch = 8;
-
-// Instance of flat stage s: the last b with stage_off[b] <= s.
-__device__ int instance_of(const int64_t *stage_off, int B, int64_t s) {
-    int lo = 0, hi = B;  // stage_off[lo] <= s < stage_off[hi]
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (stage_off[mid] <= s) lo = mid;
-        else hi = mid;
-    }
-    return lo;
-}
-
-// Instance of each lane's stage sw + lane, for a wave whose 64 lanes hold
-// consecutive stages from sw < N (all lanes active).  A 64-way search finds
-// the instance of sw (each round of parallel loads narrows the range
-// 64-fold), then the instance starts inside the wave's range, which form a
-// prefix of the following instances, move each lane past the starts at or
-// before its stage.  Many empty instances can put more than 63 starts in
-// the range; those waves search per lane.
-__device__ int instance_of_wave(const int64_t *stage_off, int B, int64_t sw) {
-    const int lane = threadIdx.x & 63;
-    int lo = 0, hi = B;  // stage_off[lo] <= sw < stage_off[hi] (stage_off[B] = N)
-    while (hi - lo > 1) {  // uniform
-        const int64_t n = hi - lo;
-        auto probe = [&](int l) { return lo + 1 + (int)(((int64_t)l * (n - 1)) / 64); };  // in [lo + 1, hi - 1]
-        const int cnt = __popcll(__ballot(stage_off[probe(lane)] <= sw));  // the probes at or below sw form a prefix
-        const int nlo = cnt > 0 ? probe(cnt - 1) : lo;
-        const int nhi = cnt < 64 ? probe(cnt) : hi;
-        lo = nlo;
-        hi = nhi;
-    }
-    const int64_t s = sw + lane;
-    const int64_t st = stage_off[min(lo + 1 + lane, B)];  // starts after the instance of sw, ascending
-    const int k = __popcll(__ballot(st <= sw + 63));
-    if (k == 64) return instance_of(stage_off, B, s);
-    int inst = lo;
-    for (int j = 0; j < k; ++j) inst += s >= __shfl(st, j) ? 1 : 0;  // uniform trip count
-    return inst;
-}
 
 // One frontier slot of the instance, staged for the lanes of its wave:
 // the devices of its selected candidate (0 when none or rejected), the
@@ -138,10 +99,11 @@ __host__ __device__ inline int padded_slots(int K) { return (K + 7) & ~7; }
 
 // LDS of k_commit_apply: the staged slots and their shards' finish times,
 // the exec and switch tables, the model weights and fit masks, the instance's
-// prefix-slot rows and each row's ring head.
-__host__ __device__ inline size_t apply_lds_bytes(int D, int M, int K) {
+// prefix-slot rows and each row's ring head, then the instance's bitmap when
+// it is kept in LDS (bm_words words).
+__host__ __device__ inline size_t apply_lds_bytes(int D, int M, int K, int bm_words) {
     return 64 * sizeof(SlotL) + 64 * 8 * FATE_MAX_SHARD + 8 * (size_t)M * D + 16 * (size_t)M +
-           8 * (size_t)D * padded_slots(K) + 4 * (size_t)D;
+           8 * (size_t)D * padded_slots(K) + 4 * (size_t)D + 4 * (size_t)bm_words;
 }
 
 // When the outputs of stage s's parents are on device d for a k-shard
@@ -198,6 +160,17 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
     float *ex = reinterpret_cast<float *>(pslots + (size_t)D * Kp);
     float *ks = ex + (size_t)M * D;
     int *heads = reinterpret_cast<int *>(ks + (size_t)M * D);
+    // the instance's bitmap: bit bo + i for its stage i (frontier membership
+    // after this step), in LDS or in its workspace region
+    const int64_t sb = a.stage_off[b], nst = a.stage_off[b + 1] - sb;
+    const uint32_t bo = a.bm_lds ? 0u : (uint32_t)(sb & 31);
+    uint32_t *bm = a.bm_lds ? reinterpret_cast<uint32_t *>(heads + D) : a.gbm + (sb >> 5) + b;
+    const uint32_t words = (uint32_t)((bo + nst + 31) / 32);
+    auto mark = [&](int64_t s) {
+        const uint32_t i = bo + (uint32_t)(s - sb);
+        atomicOr(bm + (i >> 5), 1u << (i & 31));
+    };
+    for (uint32_t i = lane; i < words; i += 64) bm[i] = 0u;
     for (int i = lane; i < M * D; i += 64) {
         ex[i] = a.exec[i];
         ks[i] = a.ksw[i];
@@ -210,9 +183,7 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
         const int dd = i / Kp, e = i - dd * Kp;
         pslots[i] = e < K ? a.pcache[((int64_t)b * D + dd) * K + e] : 0ull;
     }
-    const int64_t nF = a.counts[0];
-    const int64_t lo = first_slot_of_wave(a.frontier, nF, (uint32_t)b);
-    const int64_t hi = first_slot_of_wave(a.frontier, nF, (uint32_t)b + 1u);
+    const int64_t lo = a.fr_off[b], hi = a.fr_off[b + 1];
     const bool live = lane < D;
     const int d = live ? lane : 0;
     const int64_t t = (int64_t)b * D + d;
@@ -240,12 +211,14 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
         const int64_t f = c0 + lane;
         uint64_t win = 0;
         bool rej = false;
-        uint32_t s = 0;
+        uint32_t s = 0, cb = 0, cn = 0;
         int kq = 0;
         if (f < hi) {
             s = a.frontier[2 * f];
             const int j = a.sel[f * a.sel_stride];
             const StageRec r = a.rec[s];
+            cb = a.ch_off[s];
+            cn = a.ch_off[s + 1] - cb;
             SlotL x;
             x.hash = r.hash;
             x.model = r.model;
@@ -276,6 +249,7 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
             }
             x.win = win;
             sl[lane] = x;
+            if (win == 0) mark(s);  // still pending: it stays in the frontier
         }
         rejected += (uint32_t)__popcll(__ballot(rej));
         // lane d collects the slots whose candidate contains device d
@@ -333,6 +307,51 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
             }
             a.fin[s] = (float)fs;
         }
+        // Children of the stages this chunk completed, one (stage, child)
+        // pair per lane.  Every parent status and holder set so far is
+        // visible to the wave (the barriers above).  A child with several
+        // parents completed in this step is rewritten once per such parent,
+        // each time from the statuses then settled: a later rewrite sees
+        // more completed parents, and the last one sees them all (parents in
+        // the same chunk write the same list).  No child of a stage pending
+        // before this step is in the frontier, so its bit is new.
+        uint32_t npairs = 0;
+        const uint32_t first = wave_exscan_u32(kq > 0 ? cn : 0u, npairs);
+        for (uint32_t p0 = 0; p0 < npairs; p0 += 64) {  // uniform
+            const uint32_t pr = p0 + (uint32_t)lane;
+            // the pair's stage: the last lane whose first pair is at or before it
+            int q = 0;
+#pragma unroll
+            for (int step = 32; step >= 1; step >>= 1)
+                if ((uint32_t)__shfl((int)first, q + step) <= pr) q += step;
+            const uint32_t qb = (uint32_t)__shfl((int)cb, q), qf = (uint32_t)__shfl((int)first, q);
+            if (pr < npairs) {
+                const uint32_t w = a.ch_idx[qb + (pr - qf)];
+                const StageRec rw = a.rec[w];
+                uint32_t nd = 0;
+                for (uint32_t q0 = 0; q0 < rw.npar; q0 += kParBatch) {  // the batch's loads are issued together
+                    uint32_t u[kParBatch];
+#pragma unroll
+                    for (int j = 0; j < kParBatch; ++j) u[j] = q0 + j < rw.npar ? a.par_idx[rw.par_begin + q0 + j] : 0u;
+                    bool dn[kParBatch];
+#pragma unroll
+                    for (int j = 0; j < kParBatch; ++j) dn[j] = q0 + j < rw.npar && a.status[u[j]] == kCompleted;
+                    DoneParent e[kParBatch];
+#pragma unroll
+                    for (int j = 0; j < kParBatch; ++j) {
+                        e[j].holders = dn[j] ? a.holders[u[j]] : 0ull;
+                        e[j].sigma = dn[j] ? a.rec[u[j]].sigma : 0.0f;
+                        e[j].pad = 0u;
+                    }
+#pragma unroll
+                    for (int j = 0; j < kParBatch; ++j)
+                        if (dn[j]) a.done[rw.par_begin + nd++] = e[j];
+                }
+                a.done_n[w] = nd;
+                if (nd == rw.npar) mark(w);
+            }
+        }
+        __syncthreads();
     }
     if (live) {
         a.resident[t] = res;
@@ -346,212 +365,104 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
         p = p >= K ? p - K : p;
         a.pcache[(int64_t)b * D * K + i] = pslots[dd * Kp + p];
     }
-    if (lane == 0) a.rej[b] = rejected;
-}
-
-__global__ __launch_bounds__(kPlanBlock) void k_plan_count(CommitLaunch a) {
-    __shared__ uint32_t sh[3 * (kPlanBlock / 64)];
-    const int64_t s0 = (int64_t)blockIdx.x * kPlanStages + (int64_t)threadIdx.x * kPlanItems;
-    uint32_t tcp = 0, tfr = 0, tnc = 0;
-    for (int i = 0; i < kPlanItems; ++i) {
-        const int64_t s = s0 + i;
-        if (s >= a.N) break;
-        // only pending stages can be scored (in the frontier or a horizon),
-        // so only they carry completed-parent lists
-        bool ready = a.status[s] == kPending;
-        uint32_t cp = 0, nc = 0;
-        if (ready) {
-            const StageRec r = a.rec[s];
-            for (uint32_t q0 = 0; q0 < r.npar; q0 += kParBatch) {  // the batch's loads are issued together
-                uint32_t u[kParBatch];
-#pragma unroll
-                for (int j = 0; j < kParBatch; ++j) u[j] = q0 + j < r.npar ? a.par_idx[r.par_begin + q0 + j] : 0u;
-                uint8_t st[kParBatch];
-#pragma unroll
-                for (int j = 0; j < kParBatch; ++j) st[j] = q0 + j < r.npar ? a.status[u[j]] : kCompleted;
-#pragma unroll
-                for (int j = 0; j < kParBatch; ++j) {
-                    if (q0 + j >= r.npar) break;
-                    if (st[j] == kCompleted) ++cp;
-                    else ready = false;
-                }
+    // the new frontier in stage order: the set bits, 64 words at a time
+    uint2 *lst = reinterpret_cast<uint2 *>(a.list) + sb;
+    const bool singles = a.max_shard == 1 || D == 1;  // every stage has D candidates
+    uint32_t nf = 0;
+    for (uint32_t c = 0; c < words; c += 64) {  // uniform
+        uint32_t x = c + lane < words ? bm[c + lane] : 0u;
+        uint32_t cnt = 0;
+        uint32_t pos = nf + wave_exscan_u32((uint32_t)__popc(x), cnt);
+        while (x) {
+            const uint32_t i = 32u * (c + lane) + (uint32_t)__builtin_ctz(x) - bo;
+            x &= x - 1u;
+            lst[pos] = make_uint2((uint32_t)sb + i, singles ? pos * (uint32_t)D : 0u);
+            ++pos;
+        }
+        nf += cnt;
+    }
+    uint32_t ncand = nf * (uint32_t)D;
+    if (!singles) {  // candidate offsets within the instance from the stages' shard caps
+        __syncthreads();
+        ncand = 0;
+        for (uint32_t i0 = 0; i0 < nf; i0 += 64) {  // uniform
+            const uint32_t i = i0 + lane;
+            uint32_t s = 0, nc = 0;
+            if (i < nf) {
+                s = lst[i].x;
+                nc = (uint32_t)candidates_of(shard_cap_of(a.rec[s].shard, a.max_shard, D), D);
             }
-            nc = ready ? (uint32_t)candidates_of(shard_cap_of(r.shard, a.max_shard, a.D), a.D) : 0u;
+            uint32_t cnt = 0;
+            const uint32_t off = ncand + wave_exscan_u32(nc, cnt);
+            if (i < nf) lst[i] = make_uint2(s, off);
+            ncand += cnt;
         }
-        a.cp[s] = cp;
-        a.nc[s] = nc;
-        tcp += cp;
-        tfr += ready ? 1u : 0u;
-        tnc += nc;
     }
-    const uint32_t x[3] = {tcp, tfr, tnc};
-    uint32_t ex[3], tot[3];
-    block_exscan<kPlanBlock, 3>(x, sh, ex, tot);
-    if (threadIdx.x == 0) {
-        a.bsum[3 * blockIdx.x] = tot[0];
-        a.bsum[3 * blockIdx.x + 1] = tot[1];
-        a.bsum[3 * blockIdx.x + 2] = tot[2];
+    if (lane == 0) {
+        const uint32_t slice = (uint32_t)a.slice;
+        reinterpret_cast<uint4 *>(a.tot)[b] = make_uint4(nf, ncand, (nf + slice - 1u) / slice, rejected);
     }
 }
 
-// One workgroup per segment of kPlanSeg workgroup totals: the totals become
-// offsets within the segment (in place), and the segment total is recorded.
-__global__ __launch_bounds__(kPlanBlock) void k_plan_segscan(CommitLaunch a) {
-    static_assert(kPlanSeg == kPlanBlock, "one workgroup total per thread");
-    __shared__ uint32_t sh[3 * (kPlanBlock / 64)];
-    const int seg = (int)blockIdx.x, i = seg * kPlanSeg + (int)threadIdx.x;
-    uint32_t x[3] = {0u, 0u, 0u};
-    if (i < a.nblk) {
-#pragma unroll
-        for (int c = 0; c < 3; ++c) x[c] = a.bsum[3 * i + c];
-    }
-    uint32_t ex[3], tot[3];
-    block_exscan<kPlanBlock, 3>(x, sh, ex, tot);
-    if (i < a.nblk) {
-#pragma unroll
-        for (int c = 0; c < 3; ++c) a.bsum[3 * i + c] = ex[c];
-    }
-    if (threadIdx.x == 0) {
-#pragma unroll
-        for (int c = 0; c < 3; ++c) a.segsum[3 * seg + c] = tot[c];
-    }
-}
+// Instances per thread of k_commit_scan: 4 K instances take one workgroup scan.
+constexpr int kScanItems = 4;
 
-__global__ __launch_bounds__(1024) void k_plan_offsets(CommitLaunch a) {
-    // exclusive scan of the segment totals, 1024 at a time, in place
-    __shared__ uint32_t sh[3 * (1024 / 64)];
-    uint32_t run[3] = {0u, 0u, 0u};
-    for (int batch = 0; batch < a.nseg; batch += 1024) {  // uniform
-        const int i = batch + (int)threadIdx.x;
-        uint32_t x[3];
+__global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
+    __shared__ uint32_t sh[4 * (1024 / 64)];
+    uint32_t run[4] = {0u, 0u, 0u, 0u};
+    const uint4 *tot = reinterpret_cast<const uint4 *>(a.tot);
+    for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // uniform
+        const int b0 = batch + (int)threadIdx.x * kScanItems;
+        uint4 t[kScanItems];
+        uint32_t x[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int c = 0; c < 3; ++c) x[c] = i < a.nseg ? a.segsum[3 * i + c] : 0u;
-        uint32_t ex[3], tot[3];
-        block_exscan<1024, 3>(x, sh, ex, tot);
-        if (i < a.nseg) {
-#pragma unroll
-            for (int c = 0; c < 3; ++c) a.segsum[3 * i + c] = run[c] + ex[c];
+        for (int j = 0; j < kScanItems; ++j) {
+            t[j] = b0 + j < a.B ? tot[b0 + j] : make_uint4(0u, 0u, 0u, 0u);
+            x[0] += t[j].x;
+            x[1] += t[j].y;
+            x[2] += t[j].z;
+            x[3] += t[j].w;
         }
+        uint32_t ex[4], all[4];
+        block_exscan<1024, 4>(x, sh, ex, all);
+        uint32_t f = run[0] + ex[0], c = run[1] + ex[1], sl = run[2] + ex[2];
 #pragma unroll
-        for (int c = 0; c < 3; ++c) run[c] += tot[c];
-    }
-    if (threadIdx.x == 0) {
-        a.done_off[a.N] = run[0];
-        a.fidx[a.N] = run[1];
-        a.cand_off[run[1]] = run[2];
-        a.counts[0] = run[1];
-        a.counts[1] = run[2];
-    }
-}
-
-__global__ __launch_bounds__(kPlanBlock) void k_plan_fill(CommitLaunch a) {
-    __shared__ uint32_t sh[3 * (kPlanBlock / 64)];
-    const int64_t s0 = (int64_t)blockIdx.x * kPlanStages + (int64_t)threadIdx.x * kPlanItems;
-    uint32_t cp[kPlanItems], nc[kPlanItems];
-    uint32_t tcp = 0, tfr = 0, tnc = 0;
-#pragma unroll
-    for (int i = 0; i < kPlanItems; ++i) {
-        const int64_t s = s0 + i;
-        cp[i] = s < a.N ? a.cp[s] : 0u;
-        nc[i] = s < a.N ? a.nc[s] : 0u;
-        tcp += cp[i];
-        tfr += nc[i] ? 1u : 0u;
-        tnc += nc[i];
-    }
-    const uint32_t x[3] = {tcp, tfr, tnc};
-    uint32_t ex[3], tot[3];
-    block_exscan<kPlanBlock, 3>(x, sh, ex, tot);
-    const int seg = (int)blockIdx.x / kPlanSeg;  // segment offset + offset within the segment + within the workgroup
-    uint32_t dpos = a.segsum[3 * seg] + a.bsum[3 * blockIdx.x] + ex[0];
-    uint32_t fpos = a.segsum[3 * seg + 1] + a.bsum[3 * blockIdx.x + 1] + ex[1];
-    uint32_t cpos = a.segsum[3 * seg + 2] + a.bsum[3 * blockIdx.x + 2] + ex[2];
-    static_assert(kPlanItems == 1, "the wave's stages are consecutive, one per lane");
-    const int64_t sw = s0 - (threadIdx.x & 63);  // first stage of the wave
-    const int inst = sw < a.N ? instance_of_wave(a.stage_off, a.B, sw) : 0;  // uniform condition
-    for (int i = 0; i < kPlanItems; ++i) {
-        const int64_t s = s0 + i;
-        if (s >= a.N) break;
-        a.done_off[s] = dpos;
-        a.fidx[s] = fpos;
-        if (nc[i]) {
-            a.frontier[2 * (int64_t)fpos] = (uint32_t)s;
-            a.frontier[2 * (int64_t)fpos + 1] = (uint32_t)inst;
-            a.cand_off[fpos] = cpos;
-            ++fpos;
-            cpos += nc[i];
-        }
-        if (cp[i]) {
-            const StageRec r = a.rec[s];
-            uint32_t e = dpos;
-            for (uint32_t q0 = 0; q0 < r.npar; q0 += kParBatch) {  // the batch's loads are issued together
-                uint32_t u[kParBatch];
-#pragma unroll
-                for (int j = 0; j < kParBatch; ++j) u[j] = q0 + j < r.npar ? a.par_idx[r.par_begin + q0 + j] : 0u;
-                bool done[kParBatch];
-#pragma unroll
-                for (int j = 0; j < kParBatch; ++j) done[j] = q0 + j < r.npar && a.status[u[j]] == kCompleted;
-                DoneParent p[kParBatch];
-#pragma unroll
-                for (int j = 0; j < kParBatch; ++j) {
-                    p[j].holders = done[j] ? a.holders[u[j]] : 0ull;
-                    p[j].sigma = done[j] ? a.rec[u[j]].sigma : 0.0f;
-                    p[j].pad = 0u;
-                }
-#pragma unroll
-                for (int j = 0; j < kParBatch; ++j)
-                    if (done[j]) a.done[e++] = p[j];
-            }
-            dpos += cp[i];
-        }
-    }
-}
-
-// Instances per thread of k_plan_slices: 4 K instances take one workgroup scan.
-constexpr int kSliceItems = 4;
-
-__global__ __launch_bounds__(1024) void k_plan_slices(CommitLaunch a) {
-    // each thread takes kSliceItems consecutive instances: their frontier
-    // ranges, slice and rejection counts; one workgroup scan places them
-    __shared__ uint32_t sh[2 * (1024 / 64)];
-    const uint32_t slice = (uint32_t)a.slice;
-    uint32_t run[2] = {0u, 0u};
-    for (int batch = 0; batch < a.B; batch += kSliceItems * 1024) {  // uniform
-        const int b0 = batch + (int)threadIdx.x * kSliceItems;
-        int64_t so[kSliceItems + 1];
-#pragma unroll
-        for (int j = 0; j <= kSliceItems; ++j) so[j] = b0 + j <= a.B ? a.stage_off[b0 + j] : 0;
-        uint32_t f[kSliceItems + 1], r[kSliceItems];
-#pragma unroll
-        for (int j = 0; j <= kSliceItems; ++j) f[j] = b0 + j <= a.B ? a.fidx[so[j]] : 0u;
-#pragma unroll
-        for (int j = 0; j < kSliceItems; ++j) r[j] = b0 + j < a.B ? a.rej[b0 + j] : 0u;
-        uint32_t ns[kSliceItems], t[2] = {0u, 0u};
-#pragma unroll
-        for (int j = 0; j < kSliceItems; ++j) {
-            ns[j] = b0 + j < a.B ? (f[j + 1] - f[j] + slice - 1) / slice : 0u;
-            t[0] += ns[j];
-            t[1] += r[j];
-        }
-        uint32_t ex[2], tot[2];
-        block_exscan<1024, 2>(t, sh, ex, tot);
-        uint32_t off = run[0] + ex[0];
-#pragma unroll
-        for (int j = 0; j < kSliceItems; ++j) {
+        for (int j = 0; j < kScanItems; ++j) {
             if (b0 + j >= a.B) break;
-            for (uint32_t q = 0; q < ns[j]; ++q, ++off) {
-                const uint32_t fs = f[j] + q * slice;
-                const int64_t o = 3 * (int64_t)off;
-                a.slices[o] = (uint32_t)(b0 + j);
-                a.slices[o + 1] = fs;
-                a.slices[o + 2] = min(fs + slice, f[j + 1]);
-            }
+            a.fr_off[b0 + j] = f;
+            reinterpret_cast<uint2 *>(a.base)[b0 + j] = make_uint2(c, sl);
+            f += t[j].x;
+            c += t[j].y;
+            sl += t[j].z;
         }
-        run[0] += tot[0];
-        run[1] += tot[1];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) run[q] += all[q];
     }
     if (threadIdx.x == 0) {
-        a.counts[2] = run[0];
-        a.counts[3] = run[1];
+        a.fr_off[a.B] = run[0];
+        a.cand_off[run[0]] = run[1];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) a.counts[q] = run[q];
+    }
+}
+
+__global__ __launch_bounds__(64) void k_commit_fill(CommitLaunch a) {
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const uint32_t F = a.fr_off[b], n = a.fr_off[b + 1] - F;
+    const uint2 cs = reinterpret_cast<const uint2 *>(a.base)[b];
+    const uint2 *lst = reinterpret_cast<const uint2 *>(a.list) + a.stage_off[b];
+    uint2 *fr = reinterpret_cast<uint2 *>(a.frontier);
+    for (uint32_t i = lane; i < n; i += 64) {
+        const uint2 e = lst[i];
+        fr[F + i] = make_uint2(e.x, (uint32_t)b);
+        a.cand_off[F + i] = cs.x + e.y;
+    }
+    const uint32_t slice = (uint32_t)a.slice, ns = (n + slice - 1u) / slice;
+    for (uint32_t q = lane; q < ns; q += 64) {
+        const int64_t o = 3 * (int64_t)(cs.y + q);
+        a.slices[o] = (uint32_t)b;
+        a.slices[o + 1] = F + q * slice;
+        a.slices[o + 2] = F + min(n, (q + 1u) * slice);
     }
 }
 
@@ -559,13 +470,10 @@ __global__ __launch_bounds__(1024) void k_plan_slices(CommitLaunch a) {
 
 int launch_commit(const CommitLaunch &a, void *stream) {
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (a.B > 0)
-        hipLaunchKernelGGL(k_commit_apply, dim3((unsigned)a.B), dim3(64), apply_lds_bytes(a.D, a.M, a.K), s, a);
-    if (a.nblk > 0) hipLaunchKernelGGL(k_plan_count, dim3((unsigned)a.nblk), dim3(kPlanBlock), 0, s, a);
-    if (a.nseg > 0) hipLaunchKernelGGL(k_plan_segscan, dim3((unsigned)a.nseg), dim3(kPlanBlock), 0, s, a);
-    hipLaunchKernelGGL(k_plan_offsets, dim3(1), dim3(1024), 0, s, a);
-    if (a.nblk > 0) hipLaunchKernelGGL(k_plan_fill, dim3((unsigned)a.nblk), dim3(kPlanBlock), 0, s, a);
-    hipLaunchKernelGGL(k_plan_slices, dim3(1), dim3(1024), 0, s, a);
+    const size_t lds = apply_lds_bytes(a.D, a.M, a.K, a.bm_lds ? a.bm_words : 0);
+    if (a.B > 0) hipLaunchKernelGGL(k_commit_apply, dim3((unsigned)a.B), dim3(64), lds, s, a);
+    hipLaunchKernelGGL(k_commit_scan, dim3(1), dim3(1024), 0, s, a);
+    if (a.B > 0) hipLaunchKernelGGL(k_commit_fill, dim3((unsigned)a.B), dim3(64), 0, s, a);
     return (int)hipGetLastError();
 }
 

@@ -1,6 +1,7 @@
 // Device helpers shared by the scoring, commit-and-advance and planning
 // kernels of libfate: bit tests, +infinity, the Load rule, the candidate
-// numbering of a frontier stage and the frontier range of an instance.
+// numbering of a frontier stage, a wave prefix sum and the frontier range of
+// an instance.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -55,6 +56,19 @@ __device__ __forceinline__ void candidate_window(int j, int D, int &i, int &k) {
         ++k;
     }
     i = j;
+}
+
+// Sum and exclusive prefix sum over the 64 lanes of a wave (all active).
+__device__ __forceinline__ uint32_t wave_exscan_u32(uint32_t x, uint32_t &total) {
+    const int lane = threadIdx.x & 63;
+    uint32_t v = x;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(v, off, 64);
+        if (lane >= off) v += y;
+    }
+    total = __shfl(v, 63, 64);
+    return v - x;
 }
 
 // First frontier slot whose instance is >= b (the frontier is ordered by

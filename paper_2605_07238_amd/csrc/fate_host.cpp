@@ -123,7 +123,7 @@ void instance_horizons(const fate_dag_batch_t *g, int b, int H, int levels, uint
 }
 
 struct DagLayout {
-    size_t exec, ksw, beta, weight, cap, fits, stage_off, rec, par, desc_off, desc, desc_w, total;
+    size_t exec, ksw, beta, weight, cap, fits, stage_off, rec, par, desc_off, desc, desc_w, ch_off, ch_idx, total;
 };
 
 // desc_w (one float per horizon entry) only with level weights
@@ -142,6 +142,8 @@ DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc, b
     L.desc_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
     L.desc = o; o = align_up(o + sizeof(uint32_t) * ndesc);
     L.desc_w = o; o = align_up(o + (level_weights ? sizeof(float) * ndesc : 0));
+    L.ch_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
+    L.ch_idx = o; o = align_up(o + sizeof(uint32_t) * E);
     L.total = o;
     return L;
 }
@@ -204,6 +206,9 @@ void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
     int32_t max_r = 1;
     for (int64_t i = 0; i < p.N; ++i) max_r = std::max(max_r, (int32_t)g->shard_max[i]);
     out->max_r = max_r;
+    int64_t max_stages = 0;
+    for (int b = 0; b < g->B; ++b) max_stages = std::max(max_stages, g->stage_off[b + 1] - g->stage_off[b]);
+    out->max_stages = max_stages;
     out->base = base;
     out->bytes = bytes;
     out->exec = reinterpret_cast<const float *>(base + L.exec);
@@ -217,6 +222,8 @@ void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
     out->par_idx = reinterpret_cast<const uint32_t *>(base + L.par);
     out->desc_off = reinterpret_cast<const uint32_t *>(base + L.desc_off);
     out->desc = reinterpret_cast<const uint32_t *>(base + L.desc);
+    out->ch_off = reinterpret_cast<const uint32_t *>(base + L.ch_off);
+    out->ch_idx = reinterpret_cast<const uint32_t *>(base + L.ch_idx);
 }
 
 void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const DagsPlan &p,
@@ -260,6 +267,24 @@ void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
         if (n > 0 && !p.lists[b].empty())
             copy_bytes(desc + doff[base], p.lists[b].data(), sizeof(uint32_t) * p.lists[b].size());
     });
+    // children lists: stages visited in ascending id append themselves to
+    // their parents' lists, so every list ascends
+    uint32_t *choff = reinterpret_cast<uint32_t *>(img + L.ch_off);
+    uint32_t *chidx = reinterpret_cast<uint32_t *>(img + L.ch_idx);
+    for (int b = 0; b < g->B; ++b)
+        for (int64_t s = g->stage_off[b]; s < g->stage_off[b + 1]; ++s)
+            for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) ++choff[g->stage_off[b] + g->par_idx[q]];
+    uint32_t run = 0;
+    for (int64_t s = 0; s <= p.N; ++s) {
+        const uint32_t c = s < p.N ? choff[s] : 0u;
+        choff[s] = run;
+        run += c;
+    }
+    std::vector<uint32_t> fillc(choff, choff + p.N);
+    for (int b = 0; b < g->B; ++b)
+        for (int64_t s = g->stage_off[b]; s < g->stage_off[b + 1]; ++s)
+            for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q)
+                chidx[fillc[g->stage_off[b] + g->par_idx[q]]++] = (uint32_t)s;
     if (!wts) return;
     // level weights: 1 / (number of v's horizon stages at that depth), for
     // the mean-per-level tail; the entries of a stage are ordered by depth
@@ -290,8 +315,9 @@ struct StatePlan {
     std::vector<uint32_t> frontier;  // pairs
     std::vector<uint32_t> cand_off;
     std::vector<uint32_t> slices;    // triples
-    std::vector<uint32_t> done_off;  // [N+1]
-    std::vector<fate::DoneParent> done;
+    std::vector<uint32_t> fr_off;    // [B+1]
+    std::vector<uint32_t> done_n;    // [N]
+    std::vector<fate::DoneParent> done;  // [E]: stage s's slots from par_off[s]
     int64_t nF = 0, nC = 0, nS = 0;
 };
 
@@ -319,12 +345,14 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
     p->cand_off.clear();
     p->frontier.clear();
     p->slices.clear();
+    p->fr_off.assign(B + 1, 0);
     const int64_t slice = fate::slice_len(D);
     int64_t nc = 0;
     for (int b = 0; b < B; ++b) {
         const int64_t base = g->stage_off[b];
         const int64_t n = g->stage_off[b + 1] - base;
         const int64_t first = (int64_t)p->frontier.size() / 2;
+        p->fr_off[b] = (uint32_t)first;
         for (int64_t v = 0; v < n; ++v) {
             const int64_t s = base + v;
             const uint8_t status = st->status[s];
@@ -355,32 +383,30 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
         }
     }
     p->nS = (int64_t)p->slices.size() / 3;
+    p->fr_off[B] = (uint32_t)(p->frontier.size() / 2);
     // completed parents of every pending stage (only pending stages are
-    // scored, in the frontier or in a horizon), with their holders and sizes
-    p->done_off.assign(N + 1, 0);
-    p->done.clear();
-    {
-        int64_t acc = 0;
-        for (int b = 0; b < B; ++b) {
-            const int64_t base = g->stage_off[b];
-            const int64_t n = g->stage_off[b + 1] - base;
-            for (int64_t v = 0; v < n; ++v) {
-                const int64_t s = base + v;
-                p->done_off[s] = (uint32_t)acc;
-                if (st->status[s] != FATE_PENDING) continue;
-                for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) {
-                    const int64_t u = base + g->par_idx[q];
-                    if (st->holders[u] == 0) continue;
-                    fate::DoneParent e;
-                    e.holders = st->holders[u];
-                    e.sigma = g->out_bytes[u];
-                    e.pad = 0;
-                    p->done.push_back(e);
-                    ++acc;
-                }
+    // scored, in the frontier or in a horizon), with their holders and
+    // sizes, in the first of the stage's parent slots
+    p->done_n.assign(N, 0);
+    fate::DoneParent zero;
+    zero.holders = 0;
+    zero.sigma = 0.0f;
+    zero.pad = 0;
+    p->done.assign(pk->E, zero);
+    for (int b = 0; b < B; ++b) {
+        const int64_t base = g->stage_off[b];
+        for (int64_t s = base; s < g->stage_off[b + 1]; ++s) {
+            if (st->status[s] != FATE_PENDING) continue;
+            uint32_t k = 0;
+            for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) {
+                const int64_t u = base + g->par_idx[q];
+                if (st->holders[u] == 0) continue;
+                fate::DoneParent &e = p->done[g->par_off[s] + k++];
+                e.holders = st->holders[u];
+                e.sigma = g->out_bytes[u];
             }
+            p->done_n[s] = k;
         }
-        p->done_off[N] = (uint32_t)acc;
     }
     p->cand_off.push_back((uint32_t)nc);
     p->nF = (int64_t)p->frontier.size() / 2;
@@ -389,13 +415,13 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
 }
 
 struct StateLayout {
-    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_off, done, status, finish, counts,
-        total;
+    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_n, done, fr_off, status, finish,
+        counts, total;
 };
 
-// Section sizes: nF frontier slots, nS slices, nDone completed-parent entries
-// (the exact counts, or the capacities of a planning state, which also
-// carries the stage statuses and the device counters).
+// Section sizes: nF frontier slots, nS slices (the exact counts, or the
+// capacities of a planning state, which also carries the stage statuses and
+// the device counters), nDone = E completed-parent slots.
 StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS, int64_t nDone,
                          bool advance = false) {
     StateLayout L;
@@ -408,8 +434,9 @@ StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS,
     L.frontier = o; o = align_up(o + sizeof(uint32_t) * 2 * nF);
     L.cand_off = o; o = align_up(o + sizeof(uint32_t) * (nF + 1));
     L.slices = o; o = align_up(o + sizeof(uint32_t) * 3 * nS);
-    L.done_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
+    L.done_n = o; o = align_up(o + sizeof(uint32_t) * N);
     L.done = o; o = align_up(o + sizeof(fate::DoneParent) * nDone);
+    L.fr_off = o; o = align_up(o + sizeof(uint32_t) * (B + 1));
     L.status = o;
     if (advance) o = align_up(o + (size_t)N);
     L.finish = o;
@@ -454,8 +481,9 @@ void write_state_image(const fate_dags_t *pk, const fate_dag_batch_t *g, const f
     copy_bytes(img + L.frontier, p.frontier.data(), sizeof(uint32_t) * p.frontier.size());
     copy_bytes(img + L.cand_off, p.cand_off.data(), sizeof(uint32_t) * p.cand_off.size());
     copy_bytes(img + L.slices, p.slices.data(), sizeof(uint32_t) * p.slices.size());
-    copy_bytes(img + L.done_off, p.done_off.data(), sizeof(uint32_t) * p.done_off.size());
+    copy_bytes(img + L.done_n, p.done_n.data(), sizeof(uint32_t) * p.done_n.size());
     copy_bytes(img + L.done, p.done.data(), sizeof(fate::DoneParent) * p.done.size());
+    copy_bytes(img + L.fr_off, p.fr_off.data(), sizeof(uint32_t) * p.fr_off.size());
     if (L.counts > L.status) {  // planning state
         copy_bytes(img + L.status, st->status, (size_t)pk->N);
         // planned finish: t for the stages completed when planning begins
@@ -490,8 +518,9 @@ void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_sh
     out->n_slices = p.nS;
     out->slices = reinterpret_cast<const uint32_t *>(base + L.slices);
     out->n_done_edges = (int64_t)p.done.size();
-    out->done_off = reinterpret_cast<const uint32_t *>(base + L.done_off);
+    out->done_n = reinterpret_cast<const uint32_t *>(base + L.done_n);
     out->done = base + L.done;
+    out->fr_off = reinterpret_cast<const uint32_t *>(base + L.fr_off);
     out->slice = (int32_t)fate::slice_len(pk->D);
 }
 
@@ -627,7 +656,7 @@ fate_status_t fate_pack_state_size(const fate_dags_t *packed, const fate_dag_bat
     StatePlan p;
     fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
     if (st != FATE_OK) return st;
-    *bytes = state_layout(packed->B, packed->D, state->K, packed->N, p.nF, p.nS, (int64_t)p.done.size()).total;
+    *bytes = state_layout(packed->B, packed->D, state->K, packed->N, p.nF, p.nS, packed->E).total;
     if (n_frontier) *n_frontier = p.nF;
     if (n_cand) *n_cand = p.nC;
     return FATE_OK;
@@ -638,7 +667,7 @@ static fate_status_t build_state(const fate_dags_t *packed, const fate_dag_batch
                                  std::vector<uint8_t> &img, StatePlan &p, StateLayout &L) {
     fate_status_t st = plan_state(packed, dags, state, max_shard, &p);
     if (st != FATE_OK) return st;
-    L = state_layout(packed->B, packed->D, state->K, packed->N, p.nF, p.nS, (int64_t)p.done.size());
+    L = state_layout(packed->B, packed->D, state->K, packed->N, p.nF, p.nS, packed->E);
     if (bytes < L.total) return FATE_ESIZE;
     img.assign(L.total, 0);
     write_state_image(packed, dags, state, p, L, img.data());
@@ -713,7 +742,8 @@ static fate_status_t check_pair(const fate_dags_t *dags, const fate_state_h *sta
     if (dags->B != state->B || dags->D != state->D || dags->N != state->N) return FATE_ESTATE;
     // the scoring kernel's LDS holds one slice of this build's length
     if (state->slice != fate::slice_len(dags->D)) return FATE_ESTATE;
-    if (!dags->records || !state->frontier || !state->cand_off || !state->slices || !state->done_off)
+    if (!dags->records || !state->frontier || !state->cand_off || !state->slices || !state->done_n ||
+        !state->fr_off)
         return FATE_EINVAL;
     return FATE_OK;
 }
@@ -742,6 +772,7 @@ fate_status_t commit_check(const fate_dags_t *dags, const fate_state_h *state, c
     if (st != FATE_OK) return st;
     if (!state->advance || !state->status || !state->counts || sel_stride < 1) return FATE_EINVAL;
     if (state->n_frontier > 0 && !d_sel) return FATE_EINVAL;
+    if (!dags->ch_off || (dags->E > 0 && !dags->ch_idx)) return FATE_EINVAL;
     *ws_total = fate::commit_ws_layout(state->N, state->B).total;
     return FATE_OK;
 }
@@ -752,6 +783,7 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     if (st != FATE_OK) return st;
     if (!state->advance || !state->status || !state->counts || sel_stride < 1) return FATE_EINVAL;
     if (state->n_frontier > 0 && !d_sel) return FATE_EINVAL;
+    if (!dags->ch_off || (dags->E > 0 && !dags->ch_idx)) return FATE_EINVAL;
     const fate::CommitWs W = fate::commit_ws_layout(state->N, state->B);
     if (ws_bytes < W.total) return FATE_ESIZE;
     if (W.total > 0 && !d_ws) return FATE_EINVAL;
@@ -777,17 +809,22 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     a.frontier = const_cast<uint32_t *>(state->frontier);
     a.cand_off = const_cast<uint32_t *>(state->cand_off);
     a.slices = const_cast<uint32_t *>(state->slices);
-    a.done_off = const_cast<uint32_t *>(state->done_off);
+    a.done_n = const_cast<uint32_t *>(state->done_n);
+    a.fr_off = const_cast<uint32_t *>(state->fr_off);
     a.done = static_cast<fate::DoneParent *>(const_cast<void *>(state->done));
     a.counts = const_cast<uint32_t *>(state->counts);
     a.sel = d_sel;
     a.sel_stride = sel_stride;
-    a.cp = reinterpret_cast<uint32_t *>(ws + W.cp);
-    a.nc = reinterpret_cast<uint32_t *>(ws + W.nc);
-    a.fidx = reinterpret_cast<uint32_t *>(ws + W.fidx);
-    a.bsum = reinterpret_cast<uint32_t *>(ws + W.bsum);
-    a.rej = reinterpret_cast<uint32_t *>(ws + W.rej);
-    a.segsum = reinterpret_cast<uint32_t *>(ws + W.segsum);
+    a.ch_off = dags->ch_off;
+    a.ch_idx = dags->ch_idx;
+    a.list = reinterpret_cast<uint32_t *>(ws + W.list);
+    a.tot = reinterpret_cast<uint32_t *>(ws + W.tot);
+    a.base = reinterpret_cast<uint32_t *>(ws + W.base);
+    a.gbm = reinterpret_cast<uint32_t *>(ws + W.gbm);
+    // the largest instance's bitmap, with the slack of an unaligned start in
+    // the workspace
+    a.bm_words = (int32_t)((dags->max_stages + 31 + 31) / 32);
+    a.bm_lds = a.bm_words <= fate::kCommitLdsBitmapWords ? 1 : 0;
     a.N = state->N;
     a.B = state->B;
     a.D = dags->D;
@@ -795,8 +832,6 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     a.K = state->K;
     a.max_shard = state->max_shard;
     a.slice = fate::slice_len(dags->D);
-    a.nblk = (int32_t)((state->N + fate::kPlanStages - 1) / fate::kPlanStages);
-    a.nseg = (a.nblk + fate::kPlanSeg - 1) / fate::kPlanSeg;
     return fate::launch_commit(a, stream) == 0 ? FATE_OK : FATE_EHIP;
 }
 
@@ -851,7 +886,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.frontier = state->frontier;
     a.cand_off = state->cand_off;
     a.slices = state->slices;
-    a.done_off = state->done_off;
+    a.done_n = state->done_n;
     a.done = static_cast<const fate::DoneParent *>(state->done);
     a.scores = d_scores;
     a.score_stride = stride;

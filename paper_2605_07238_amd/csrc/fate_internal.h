@@ -62,7 +62,7 @@ struct ScoreLaunch {
     const uint32_t *frontier;
     const uint32_t *cand_off;
     const uint32_t *slices;
-    const uint32_t *done_off;
+    const uint32_t *done_n;  // completed parents of stage g: done[rec[g].par_begin ..] (done_n[g] of them)
     const DoneParent *done;
     float *scores;            // parameter set p (blockIdx.y) writes scores + p * score_stride
     int64_t score_stride;
@@ -107,39 +107,45 @@ struct CommitLaunch {
     float *tau, *fin;
     const float *tnow;
     uint8_t *status;
-    uint32_t *frontier, *cand_off, *slices, *done_off;
+    uint32_t *frontier, *cand_off, *slices, *done_n, *fr_off;
     DoneParent *done;
     uint32_t *counts;
     // selections: sel[f * sel_stride] for frontier slot f
     const int32_t *sel;
     int32_t sel_stride;
+    // packed DAGs: children lists
+    const uint32_t *ch_off, *ch_idx;
     // workspace (commit_ws_layout)
-    uint32_t *cp, *nc, *fidx, *bsum, *rej;
-    uint32_t *segsum;  // per segment of kPlanSeg workgroups: totals, then offsets
-    int32_t nseg;
+    uint32_t *list;  // [N][2]: instance b's new frontier (stage, first candidate
+                     // relative to the instance) from stage_off[b] on
+    uint32_t *tot;   // [B][4]: new frontier stages, candidates, slices, rejected selections
+    uint32_t *base;  // [B][2]: the instance's first candidate and first slice
+    uint32_t *gbm;   // frontier bitmaps of instances too large for LDS
+    int32_t bm_lds;  // 1: every instance's bitmap fits the apply kernel's LDS
+    int32_t bm_words;  // bitmap words of the largest instance
     int64_t N;
-    int32_t B, D, M, K, max_shard, slice, nblk;
+    int32_t B, D, M, K, max_shard, slice;
 };
 
-// Stages per workgroup of the planning scans, workgroups per segment of the
-// two-level offset scan, and the workspace layout.
-constexpr int kPlanBlock = 256, kPlanItems = 1, kPlanStages = kPlanBlock * kPlanItems;
-constexpr int kPlanSeg = kPlanBlock;
+// Bitmap words past which an instance's frontier bitmap moves from LDS to
+// the workspace (instances of more than 32,768 stages).
+constexpr int kCommitLdsBitmapWords = 1024;
+
+// Workspace of the commit: the new frontier lists (one slot per stage), the
+// per-instance totals and bases, and the frontier bitmaps of large instances
+// (instance b's from word (stage_off[b] >> 5) + b, covering bit
+// (stage_off[b] & 31) + i for its stage i).
 struct CommitWs {
-    size_t cp, nc, fidx, bsum, rej, segsum, total;
+    size_t list, tot, base, gbm, total;
 };
 inline CommitWs commit_ws_layout(int64_t N, int B) {
     auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-    const int64_t nblk = (N + kPlanStages - 1) / kPlanStages;
     CommitWs w;
     size_t o = 0;
-    w.cp = o; o = up(o + 4 * (size_t)N);
-    w.nc = o; o = up(o + 4 * (size_t)N);
-    w.fidx = o; o = up(o + 4 * ((size_t)N + 1));
-    w.bsum = o; o = up(o + 12 * (size_t)nblk);
-    w.rej = o; o = up(o + 4 * ((size_t)B + 1));
-    const int64_t nseg = (nblk + kPlanSeg - 1) / kPlanSeg;
-    w.segsum = o; o = up(o + 12 * (size_t)nseg);
+    w.list = o; o = up(o + 8 * (size_t)N);
+    w.tot = o; o = up(o + 16 * (size_t)B);
+    w.base = o; o = up(o + 8 * (size_t)B);
+    w.gbm = o; o = up(o + 4 * ((size_t)N / 32 + (size_t)B + 1));
     w.total = o;
     return w;
 }
@@ -175,7 +181,7 @@ int launch_topk(const TopkLaunch &a, void *stream);
 int launch_commit(const CommitLaunch &a, void *stream);  // fate_commit.hip
 
 // Commit-and-advance behind both entry points (fate_host.cpp): validation,
-// then the six launches with the workspace d_ws of ws_bytes.  commit_check
+// then the three launches with the workspace d_ws of ws_bytes.  commit_check
 // runs the validation alone and returns the workspace bytes needed.
 fate_status_t commit_check(const fate_dags_t *dags, const fate_state_h *state, const int32_t *d_sel,
                            int32_t sel_stride, size_t *ws_total);

@@ -745,8 +745,8 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
             st.v = v;
             st.e0 = a.desc_off[v];
             st.e1 = a.desc_off[v + 1];
-            st.dbeg = a.done_off[v];
-            st.dn = (uint16_t)(a.done_off[v + 1] - st.dbeg);
+            st.dbeg = r.par_begin;
+            st.dn = (uint16_t)a.done_n[v];
             st.c0 = a.cand_off[f0 + i];
             st.nc = a.cand_off[f0 + i + 1] - st.c0;
             st.npar = r.npar;
@@ -938,8 +938,8 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
                 const uint32_t w = ent & kDescIdMask;
                 const int depth = (int)(ent >> kDescDepthShift);
                 const StageRec rw = a.rec[w];
-                const uint32_t db = a.done_off[w];
-                const uint32_t dn = a.done_off[w + 1] - db;
+                const uint32_t db = rw.par_begin;
+                const uint32_t dn = a.done_n[w];
                 Entry &E = area[lane];
                 E.feas = (Mask)(rw.elig & L.fits[rw.model]);
                 E.pfdevs = table_find<Mask>(L, rw.hash);
@@ -1033,8 +1033,8 @@ __global__ __launch_bounds__(BLK) void k_score(ScoreLaunch a) {
                     const uint32_t w = ent & kDescIdMask;
                     const int depth = (int)(ent >> kDescDepthShift);
                     const StageRec rw = a.rec[w];
-                    const uint32_t db = a.done_off[w];
-                    const uint32_t dn = a.done_off[w + 1] - db;
+                    const uint32_t db = rw.par_begin;
+                    const uint32_t dn = a.done_n[w];
                     const uint32_t feas = (uint32_t)(rw.elig & L.fits[rw.model]);
                     const uint32_t pfo = table_find<uint32_t>(L, rw.hash);
                     const bool same = rw.hash != 0 && rw.hash == sv.hash;
@@ -1610,19 +1610,6 @@ __host__ __device__ inline RowsPlan rows_plan(int D, int K, int M, int nd, int b
     return q;
 }
 
-// Sum and exclusive prefix sum over the 64 lanes of a wave (all active).
-__device__ __forceinline__ uint32_t wave_exscan_u32(uint32_t x, uint32_t &total) {
-    const int lane = threadIdx.x & 63;
-    uint32_t v = x;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(v, off, 64);
-        if (lane >= off) v += y;
-    }
-    total = __shfl(v, 63, 64);
-    return v - x;
-}
-
 template <int ND, int BLK>
 __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
     static_assert(BLK >= kRowsChunk && BLK % 64 == 0, "one thread per stage of a chunk");
@@ -1760,8 +1747,8 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             }
             s.n = n;
             s.c0 = a.cand_off[fc + tid];
-            s.dbeg = a.done_off[v];
-            s.dn = (uint16_t)(a.done_off[v + 1] - s.dbeg);
+            s.dbeg = r.par_begin;
+            s.dn = (uint16_t)a.done_n[v];
             s.npar = r.npar;
             s.model = r.model;
             s.pad0 = 0;
@@ -1936,10 +1923,10 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                 const uint32_t e1 = two ? a.desc[s.e0 + r + 1] : e0;
                 const StageRec w0 = a.rec[e0 & kDescIdMask];
                 const StageRec w1 = a.rec[e1 & kDescIdMask];
-                const uint32_t db0 = a.done_off[e0 & kDescIdMask], de0 = a.done_off[(e0 & kDescIdMask) + 1];
-                const uint32_t db1 = a.done_off[e1 & kDescIdMask], de1 = a.done_off[(e1 & kDescIdMask) + 1];
-                row(e0, w0, db0, de0 - db0);
-                if (two) row(e1, w1, db1, de1 - db1);
+                const uint32_t dn0 = a.done_n[e0 & kDescIdMask];
+                const uint32_t dn1 = a.done_n[e1 & kDescIdMask];
+                row(e0, w0, w0.par_begin, dn0);
+                if (two) row(e1, w1, w1.par_begin, dn1);
             }
 #pragma unroll
             for (int j = 0; j < NJ; ++j) part4[j * pcol + t] = make_float4(f[4 * j], f[4 * j + 1], f[4 * j + 2], f[4 * j + 3]);

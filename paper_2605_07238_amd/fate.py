@@ -92,7 +92,8 @@ class Dags(C.Structure):
                 ("weight", C.c_void_p), ("cap", C.c_void_p), ("fits", C.c_void_p),
                 ("records", C.c_void_p), ("par_idx", C.c_void_p), ("desc_off", C.c_void_p),
                 ("desc", C.c_void_p), ("stage_off", C.c_void_p), ("levels", C.c_int32), ("desc_w", C.c_void_p),
-                ("max_r", C.c_int32)]
+                ("max_r", C.c_int32), ("ch_off", C.c_void_p), ("ch_idx", C.c_void_p),
+                ("max_stages", C.c_int64)]
 
 
 class StateH(C.Structure):
@@ -103,9 +104,9 @@ class StateH(C.Structure):
                 ("tau_free", C.c_void_p), ("t_now", C.c_void_p),
                 ("frontier", C.c_void_p), ("cand_off", C.c_void_p),
                 ("n_slices", C.c_int64), ("slices", C.c_void_p),
-                ("n_done_edges", C.c_int64), ("done_off", C.c_void_p), ("done", C.c_void_p),
+                ("n_done_edges", C.c_int64), ("done_n", C.c_void_p), ("done", C.c_void_p),
                 ("advance", C.c_int32), ("status", C.c_void_p), ("counts", C.c_void_p), ("finish", C.c_void_p),
-                ("slice", C.c_int32)]
+                ("slice", C.c_int32), ("fr_off", C.c_void_p)]
 
 
 _lib = None

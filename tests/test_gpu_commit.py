@@ -31,12 +31,10 @@ def _sections(st):
         nb = n * np.dtype(dt).itemsize
         return st.buf[off:off + nb].cpu().numpy().view(dt).copy() if n else np.zeros(0, dt)
 
-    N = int(h.N)
-    done_off = take(h.done_off, N + 1)
-    done = take(h.done, 4 * int(done_off[-1])).reshape(-1, 4)
+    N, B, E = int(h.N), int(h.B), int(h.n_done_edges)
     return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
-                slices=take(h.slices, 3 * nS).reshape(nS, 3), done_off=done_off, done=done,
-                counts=(nF, nC, nS, rej))
+                slices=take(h.slices, 3 * nS).reshape(nS, 3), done_n=take(h.done_n, N),
+                done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), counts=(nF, nC, nS, rej))
 
 
 def _host_sections(pk, w):
@@ -48,10 +46,21 @@ def _host_sections(pk, w):
     def take(ptr, n, dt=np.uint32):
         return np.frombuffer(buf, dt, n, ptr - base).copy() if n else np.zeros(0, dt)
 
-    done_off = take(h.done_off, N + 1)
+    B, E = int(h.B), int(h.n_done_edges)
     return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
-                slices=take(h.slices, 3 * nS).reshape(nS, 3), done_off=done_off,
-                done=take(h.done, 4 * int(done_off[-1])).reshape(-1, 4), n_cand=int(h.n_cand))
+                slices=take(h.slices, 3 * nS).reshape(nS, 3), done_n=take(h.done_n, N),
+                done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), n_cand=int(h.n_cand))
+
+
+def pending_lists(sec, par_off, status):
+    """Completed-parent counts of the pending stages, and their entries
+    (holders, size) concatenated in stage order: each pending stage's list
+    is the first done_n of its parent slots."""
+    pend = np.flatnonzero(status == 0)
+    cnt = sec["done_n"][pend].astype(np.int64)
+    first = np.repeat(np.asarray(par_off, np.int64)[pend], cnt)
+    within = np.arange(int(cnt.sum())) - np.repeat(np.cumsum(cnt) - cnt, cnt)
+    return cnt, sec["done"][first + within, :3]
 
 
 def _compare_state(st, w_ref, tau_ref, fin_ref=None):
@@ -79,8 +88,11 @@ def _compare_sections(pk, st, w_ref):
     assert np.array_equal(dev["cand_off"], host["cand_off"]), "candidate offsets"
     assert nC == host["n_cand"]
     assert np.array_equal(dev["slices"], host["slices"]), "slices"
-    assert np.array_equal(dev["done_off"], host["done_off"]), "completed-parent offsets"
-    assert np.array_equal(dev["done"][:, :3], host["done"][:, :3]), "completed-parent entries"
+    assert np.array_equal(dev["fr_off"], host["fr_off"]), "frontier offsets per instance"
+    dn, de = pending_lists(dev, w_ref.par_off, w_ref.status)
+    hn, he = pending_lists(host, w_ref.par_off, w_ref.status)
+    assert np.array_equal(dn, hn), "completed-parent counts"
+    assert np.array_equal(de, he), "completed-parent entries"
 
 
 def _score_and_check(pk, st, w, params=None):
@@ -221,7 +233,7 @@ def test_commit_nothing_keeps_everything():
     fate.fate_commit_advance(pk, st, sel)
     torch.cuda.synchronize()
     after = _sections(st)
-    for k in ("frontier", "cand_off", "slices", "done_off", "done"):
+    for k in ("frontier", "cand_off", "slices", "done_n", "done", "fr_off"):
         assert np.array_equal(before[k], after[k]), k
     now = fate.state_arrays(st)
     for k, v in arrays.items():

@@ -85,11 +85,21 @@ def test_host_layouts_match_independent_derivations(case):
         got = [(int(e >> 28), int(e & ((1 << 28) - 1))) for e in ent]
         want = sorted((h, x) for x, h in inst.horizon(v, H))
         assert got == want, (v, got, want)
-    # completed-parent lists of pending stages, in parent order
-    done_off = take(sbuf, hs.done_off, N + 1)
-    done = np.frombuffer(sbuf, np.uint32, 4 * int(done_off[-1]), hs.done - sbase).reshape(-1, 4)
+    # children lists: every stage that names v as a parent, ascending
+    E = int(hd.E)
+    ch_off = take(buf, hd.ch_off, N + 1)
+    ch_idx = take(buf, hd.ch_idx, E)
     for v in range(N):
-        rows = done[done_off[v]:done_off[v + 1]]
+        assert ch_idx[ch_off[v]:ch_off[v + 1]].tolist() == [c for c in range(N) if v in inst.parents[c]], v
+    # frontier offsets per instance
+    assert take(sbuf, hs.fr_off, w.B + 1).tolist() == [0, nF]
+    # completed-parent lists of pending stages, in parent order, in the
+    # first of each stage's parent slots
+    done_n = take(sbuf, hs.done_n, N)
+    done = np.frombuffer(sbuf, np.uint32, 4 * E, hs.done - sbase).reshape(-1, 4)
+    for v in range(N):
+        rows = done[w.par_off[v]:w.par_off[v] + done_n[v]]
+        assert done_n[v] <= w.par_off[v + 1] - w.par_off[v]
         want = [u for u in inst.parents[v] if inst.status[u] == 1] if inst.status[v] == 0 else []
         hold = [int(r[0]) | (int(r[1]) << 32) for r in rows]
         assert hold == [int(w.holders[u]) for u in want], (v, hold, want)

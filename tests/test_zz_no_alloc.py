@@ -30,11 +30,10 @@ def _snapshot(st):
         nb = n * np.dtype(dt).itemsize
         return st.buf[off:off + nb].cpu().numpy().view(dt).copy() if n else np.zeros(0, dt)
 
-    done_off = take(h.done_off, N + 1)
     out = {k: np.asarray(v).view(np.uint8) for k, v in fate.state_arrays(st).items()}
     out.update(frontier=take(h.frontier, 2 * nF), cand_off=take(h.cand_off, nF + 1), slices=take(h.slices, 3 * nS),
-               done_off=done_off, done=take(h.done, 4 * int(done_off[-1])),
-               counts=np.array([nF, nC, nS, rej], np.int64))
+               done_n=take(h.done_n, N), done=take(h.done, 4 * int(h.n_done_edges)),
+               fr_off=take(h.fr_off, int(h.B) + 1), counts=np.array([nF, nC, nS, rej], np.int64))
     return out
 
 
@@ -76,7 +75,7 @@ def test_noalloc_commit_matches_workspace_commit():
 def test_noalloc_commit_rejects_a_state_beyond_its_workspace():
     import torch
     torch.cuda.set_device(0)
-    w = synth.make_workload("forkjoin-4096x1000-d16", B=3000, workers=16)
+    w = synth.make_workload("forkjoin-4096x1000-d16", B=4400, workers=16)  # 4.4 M stages: about 36 MB
     pk = fate.fate_pack_dags(w)
     st = fate.fate_pack_state(pk, w, advance=True)
     need = fate.fate_commit_ws_size(pk, st)
