@@ -1,6 +1,6 @@
 #!/bin/bash
 # Kernel-trace profile of the benchmark's planning loop (score, top-k, then
-# commit-and-advance, repeated): per-kernel durations of the five commit
+# commit-and-advance, repeated): per-kernel durations of the three commit
 # kernels next to the scoring kernels.  Raw output under
 # gpurun_out/prof_commit_<workload>/; prints the summary.
 #   usage: paper_2605_07238_amd/profile_commit.sh <workload> [planning steps]

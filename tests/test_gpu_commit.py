@@ -12,6 +12,7 @@ state), and the next step's scores (within the scoring tolerance).
 import numpy as np
 import pytest
 
+import builders
 from gpu_util import RTOL
 from oracle import oracle
 from paper_2605_07238_amd import fate, parity, synth
@@ -178,12 +179,66 @@ def test_commit_recipes(name):
     _run_steps(w, 3)
 
 
-def test_commit_several_scan_segments():
-    """More than 65,536 stages: the workgroup totals span two segments of the
-    two-level offset scan (the second one ragged), and frontier slots near
-    instance starts fall inside one wave of the fill."""
+def test_commit_several_chunks_per_instance():
+    """80 fork-join instances of 1,000 stages: frontiers of more than 64
+    slots (several apply chunks per instance) and instance starts at every
+    alignment of the bitmap words."""
     w = synth.make_workload("forkjoin-4096x1000-d16", B=80)
-    assert w.N > 256 * 256 and (w.N + 255) // 256 % 256 != 0
+    fb, _, _ = oracle.frontier(w)
+    assert np.bincount(fb, minlength=w.B).max() > 64
+    _run_steps(w, 2)
+
+
+def _sized_workload(name, sizes, seed=5):
+    """Instances of the recipe with the given stage counts."""
+    rc = synth.RECIPES[name]
+    cluster = synth.make_cluster(rc, seed)
+    K, ms = synth.COMMON["K"], synth.COMMON["max_shard"]
+    insts = [synth._gen_instance(dict(rc, n=n), cluster, seed, b, K, ms) for b, n in enumerate(sizes)]
+    return synth._assemble(name + "+sizes", rc, cluster, insts, K, ms)
+
+
+def test_commit_large_instance_bitmap_in_workspace():
+    """An instance of more than 32,768 stages moves every instance's frontier
+    bitmap from LDS to the workspace; the next instances start at offsets
+    that are not multiples of 32."""
+    w = _sized_workload("forkjoin-4096x1000-d16", [33005, 997, 1003])
+    pk = fate.fate_pack_dags(w)
+    assert pk.handle.max_stages == 33005 and w.stage_off[1] % 32 != 0
+    _run_steps(w, 3)
+
+
+def _join_spec():
+    """100 roots (two apply chunks), joins whose parents sit in both chunks,
+    a stage with 20 parents (three batches of parent loads), a child of a
+    root and a join, and an empty instance in between."""
+    D, M = 4, 2
+    parents = [[] for _ in range(100)]
+    parents += [[3, 70, 99], list(range(20, 40)), [5, 100], [64], [0, 63, 64, 65]]
+    n = len(parents)
+    big = dict(parents=parents, model=[v % M for v in range(n)], elig=[(1 << D) - 1] * n,
+               prefix_hash=[0 if v % 3 else 17 + v % 2 for v in range(n)], prefix_tokens=[200.0] * n,
+               out_bytes=[1e6 * (1 + v % 7) for v in range(n)], status=[0] * n, holders=[0] * n,
+               resident=[1, 2, 0, 3], tau_free=[0.0, 0.5, 1.0, 0.25], t_now=0.0)
+    empty = dict(parents=[], model=[], elig=[], out_bytes=[], status=[], holders=[],
+                 resident=[0] * D, tau_free=[0.0] * D, t_now=0.0)
+    small = dict(parents=[[], [0], [0, 1]], model=[0, 1, 0], elig=[15, 15, 15], out_bytes=[1e6, 2e6, 3e6],
+                 status=[1, 0, 0], holders=[2, 0, 0], resident=[1, 0, 0, 2], tau_free=[0.0] * D, t_now=0.0)
+    return dict(D=D, M=M, K=2, exec=[[1.0, 1.5, 2.0, 0.5]] * M, switch_s=[[0.3] * D] * M, weight_gb=[10, 20],
+                cap_gb=[40, 40, 25, 40], beta=[[0.0 if i == j else 2e-10 for j in range(D)] for i in range(D)],
+                max_shard=1, instances=[big, empty, small])
+
+
+def test_commit_joins_across_chunks():
+    w = builders.from_spec(_join_spec(), H=2)
+    pk, st, cur = _run_steps(w, 4)
+    # the joins joined the frontier once all their parents completed
+    assert (cur.status[100:105] == 1).sum() > 0
+
+
+def test_commit_more_instances_than_one_scan_batch():
+    """4,100 instances: the one-workgroup scan takes two batches of 4,096."""
+    w = synth.make_random_small(31, B=4100, n=6, D=4, M=3, max_shard=2, shard_frac=0.3, p_edge=0.4)
     _run_steps(w, 2)
 
 
