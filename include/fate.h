@@ -238,6 +238,10 @@ typedef struct {
                                  from this build's for the DAGs' device count (ESTATE) */
     const uint32_t *fr_off;   /* [B+1]: instance b's frontier slots are
                                  fr_off[b] .. fr_off[b+1] (current counts) */
+    const uint32_t *order;    /* [B]: the instances by decreasing frontier size, the
+                                 order in which per-instance launches take them (a
+                                 dispatch order only: no result depends on it; a
+                                 commit re-sorts it, ties in any order) */
 } fate_state_h;
 
 const char *fate_version(void);

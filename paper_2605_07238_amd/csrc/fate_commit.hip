@@ -151,7 +151,8 @@ __device__ __forceinline__ int row_first_empty(const uint64_t *row, int K) {
 
 __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
     extern __shared__ uint64_t smem[];
-    const int b = blockIdx.x, lane = threadIdx.x, D = a.D, K = a.K, M = a.M, Kp = padded_slots(K);
+    // largest frontiers first, so that the last waves to start are short
+    const int b = (int)a.order[blockIdx.x], lane = threadIdx.x, D = a.D, K = a.K, M = a.M, Kp = padded_slots(K);
     SlotL *sl = reinterpret_cast<SlotL *>(smem);
     double *sfin = reinterpret_cast<double *>(smem + (64 * sizeof(SlotL)) / 8);  // [64][FATE_MAX_SHARD]
     uint64_t *wt = reinterpret_cast<uint64_t *>(sfin + 64 * FATE_MAX_SHARD);
@@ -406,11 +407,18 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
 
 // Instances per thread of k_commit_scan: 4 K instances take one workgroup scan.
 constexpr int kScanItems = 4;
+// Frontier sizes the dispatch order distinguishes (larger ones tie).
+constexpr int kOrderBuckets = 1024;
+static_assert(kOrderBuckets == 1024, "one bucket per thread of k_commit_scan");
 
 __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
     __shared__ uint32_t sh[4 * (1024 / 64)];
+    __shared__ uint32_t hist[kOrderBuckets];  // instances per frontier size, largest first
     uint32_t run[4] = {0u, 0u, 0u, 0u};
     const uint4 *tot = reinterpret_cast<const uint4 *>(a.tot);
+    auto bucket = [](uint32_t n) { return (uint32_t)kOrderBuckets - 1u - min(n, (uint32_t)kOrderBuckets - 1u); };
+    hist[threadIdx.x] = 0u;
+    __syncthreads();
     for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // uniform
         const int b0 = batch + (int)threadIdx.x * kScanItems;
         uint4 t[kScanItems];
@@ -422,6 +430,7 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
             x[1] += t[j].y;
             x[2] += t[j].z;
             x[3] += t[j].w;
+            if (b0 + j < a.B) atomicAdd(&hist[bucket(t[j].x)], 1u);
         }
         uint32_t ex[4], all[4];
         block_exscan<1024, 4>(x, sh, ex, all);
@@ -444,10 +453,20 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) a.counts[q] = run[q];
     }
+    // the dispatch order of the next per-instance launches: a counting sort
+    // by new frontier size, largest first (ties in any order)
+    {
+        const uint32_t hx[1] = {hist[threadIdx.x]};
+        uint32_t ex[1], all[1];
+        block_exscan<1024, 1>(hx, sh, ex, all);
+        hist[threadIdx.x] = ex[0];
+        __syncthreads();
+    }
+    for (int b0 = (int)threadIdx.x; b0 < a.B; b0 += 1024) a.order[atomicAdd(&hist[bucket(tot[b0].x)], 1u)] = (uint32_t)b0;
 }
 
 __global__ __launch_bounds__(64) void k_commit_fill(CommitLaunch a) {
-    const int b = blockIdx.x, lane = threadIdx.x;
+    const int b = (int)a.order[blockIdx.x], lane = threadIdx.x;
     const uint32_t F = a.fr_off[b], n = a.fr_off[b + 1] - F;
     const uint2 cs = reinterpret_cast<const uint2 *>(a.base)[b];
     const uint2 *lst = reinterpret_cast<const uint2 *>(a.list) + a.stage_off[b];

@@ -316,6 +316,7 @@ struct StatePlan {
     std::vector<uint32_t> cand_off;
     std::vector<uint32_t> slices;    // triples
     std::vector<uint32_t> fr_off;    // [B+1]
+    std::vector<uint32_t> order;     // [B]: by decreasing frontier size, ties by instance
     std::vector<uint32_t> done_n;    // [N]
     std::vector<fate::DoneParent> done;  // [E]: stage s's slots from par_off[s]
     int64_t nF = 0, nC = 0, nS = 0;
@@ -384,6 +385,13 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
     }
     p->nS = (int64_t)p->slices.size() / 3;
     p->fr_off[B] = (uint32_t)(p->frontier.size() / 2);
+    // per-instance launches take the largest frontiers first, so that the
+    // last workgroups to start are short ones
+    p->order.resize(B);
+    for (int b = 0; b < B; ++b) p->order[b] = (uint32_t)b;
+    std::stable_sort(p->order.begin(), p->order.end(), [&](uint32_t x, uint32_t y) {
+        return p->fr_off[x + 1] - p->fr_off[x] > p->fr_off[y + 1] - p->fr_off[y];
+    });
     // completed parents of every pending stage (only pending stages are
     // scored, in the frontier or in a horizon), with their holders and
     // sizes, in the first of the stage's parent slots
@@ -415,8 +423,8 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
 }
 
 struct StateLayout {
-    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_n, done, fr_off, status, finish,
-        counts, total;
+    size_t resident, pcache, holders, tau, tnow, frontier, cand_off, slices, done_n, done, fr_off, order, status,
+        finish, counts, total;
 };
 
 // Section sizes: nF frontier slots, nS slices (the exact counts, or the
@@ -437,6 +445,7 @@ StateLayout state_layout(int B, int D, int K, int64_t N, int64_t nF, int64_t nS,
     L.done_n = o; o = align_up(o + sizeof(uint32_t) * N);
     L.done = o; o = align_up(o + sizeof(fate::DoneParent) * nDone);
     L.fr_off = o; o = align_up(o + sizeof(uint32_t) * (B + 1));
+    L.order = o; o = align_up(o + sizeof(uint32_t) * B);
     L.status = o;
     if (advance) o = align_up(o + (size_t)N);
     L.finish = o;
@@ -484,6 +493,7 @@ void write_state_image(const fate_dags_t *pk, const fate_dag_batch_t *g, const f
     copy_bytes(img + L.done_n, p.done_n.data(), sizeof(uint32_t) * p.done_n.size());
     copy_bytes(img + L.done, p.done.data(), sizeof(fate::DoneParent) * p.done.size());
     copy_bytes(img + L.fr_off, p.fr_off.data(), sizeof(uint32_t) * p.fr_off.size());
+    copy_bytes(img + L.order, p.order.data(), sizeof(uint32_t) * p.order.size());
     if (L.counts > L.status) {  // planning state
         copy_bytes(img + L.status, st->status, (size_t)pk->N);
         // planned finish: t for the stages completed when planning begins
@@ -521,6 +531,7 @@ void fill_state_handle(const fate_dags_t *pk, const fate_state_t *st, int max_sh
     out->done_n = reinterpret_cast<const uint32_t *>(base + L.done_n);
     out->done = base + L.done;
     out->fr_off = reinterpret_cast<const uint32_t *>(base + L.fr_off);
+    out->order = reinterpret_cast<const uint32_t *>(base + L.order);
     out->slice = (int32_t)fate::slice_len(pk->D);
 }
 
@@ -743,7 +754,7 @@ static fate_status_t check_pair(const fate_dags_t *dags, const fate_state_h *sta
     // the scoring kernel's LDS holds one slice of this build's length
     if (state->slice != fate::slice_len(dags->D)) return FATE_ESTATE;
     if (!dags->records || !state->frontier || !state->cand_off || !state->slices || !state->done_n ||
-        !state->fr_off)
+        !state->fr_off || !state->order)
         return FATE_EINVAL;
     return FATE_OK;
 }
@@ -811,6 +822,7 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     a.slices = const_cast<uint32_t *>(state->slices);
     a.done_n = const_cast<uint32_t *>(state->done_n);
     a.fr_off = const_cast<uint32_t *>(state->fr_off);
+    a.order = const_cast<uint32_t *>(state->order);
     a.done = static_cast<fate::DoneParent *>(const_cast<void *>(state->done));
     a.counts = const_cast<uint32_t *>(state->counts);
     a.sel = d_sel;
@@ -888,6 +900,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.slices = state->slices;
     a.done_n = state->done_n;
     a.done = static_cast<const fate::DoneParent *>(state->done);
+    a.order = state->order;
     a.scores = d_scores;
     a.score_stride = stride;
     a.dcounts = state->advance ? state->counts : nullptr;
@@ -996,15 +1009,17 @@ fate_status_t fate_plan_wave(const fate_state_h *state, const int32_t *d_idx, co
     if (!state) return FATE_EINVAL;
     if (k < 1 || k > FATE_MAX_TOPK) return FATE_ERANGE;
     if (state->n_frontier == 0) return FATE_OK;
-    if (!d_idx || !d_val || !d_sel || !state->frontier || !state->cand_off) return FATE_EINVAL;
+    if (!d_idx || !d_val || !d_sel || !state->frontier || !state->cand_off || !state->fr_off || !state->order)
+        return FATE_EINVAL;
     if (state->n_frontier * (int64_t)k >= (int64_t(1) << 32)) return FATE_ERANGE;
     fate::PlanLaunch a;
     a.frontier = state->frontier;
     a.cand_off = state->cand_off;
-    a.dcounts = state->advance ? state->counts : nullptr;
     a.idx = d_idx;
     a.val = d_val;
     a.sel = d_sel;
+    a.fr_off = state->fr_off;
+    a.order = state->order;
     a.nF = state->n_frontier;
     a.B = state->B;
     a.D = state->D;

@@ -64,6 +64,7 @@ struct ScoreLaunch {
     const uint32_t *slices;
     const uint32_t *done_n;  // completed parents of stage g: done[rec[g].par_begin ..] (done_n[g] of them)
     const DoneParent *done;
+    const uint32_t *order;   // instances by decreasing frontier size (grid row x takes order[x])
     float *scores;            // parameter set p (blockIdx.y) writes scores + p * score_stride
     int64_t score_stride;
     const uint32_t *dcounts;  // planning state: counts[2] = current slices, else null
@@ -108,6 +109,7 @@ struct CommitLaunch {
     const float *tnow;
     uint8_t *status;
     uint32_t *frontier, *cand_off, *slices, *done_n, *fr_off;
+    uint32_t *order;  // read by the apply kernel, re-sorted by the scan for the fill and the next step
     DoneParent *done;
     uint32_t *counts;
     // selections: sel[f * sel_stride] for frontier slot f
@@ -192,10 +194,11 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
 struct PlanLaunch {
     const uint32_t *frontier;  // [nF][2]: flat stage id, instance
     const uint32_t *cand_off;  // [nF + 1]: a stage's candidates are its choices' valid range
-    const uint32_t *dcounts;   // planning state: counts[0] = current frontier size, else null
     const int32_t *idx;        // [nF][k] choices (local candidate indices, -1 = none)
     const float *val;          // [nF][k] their scores
     int32_t *sel;              // [nF] chosen candidate or -1
+    const uint32_t *fr_off;    // [B+1] instance b's frontier slots
+    const uint32_t *order;     // [B] instances by decreasing frontier size
     int64_t nF;                // frontier size, or its capacity with dcounts
     int32_t B, D, k;
 };

@@ -1613,7 +1613,7 @@ __host__ __device__ inline RowsPlan rows_plan(int D, int K, int M, int nd, int b
 template <int ND, int BLK>
 __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
     static_assert(BLK >= kRowsChunk && BLK % 64 == 0, "one thread per stage of a chunk");
-    const int b = (int)blockIdx.x;
+    const int b = (int)a.order[blockIdx.x];  // largest frontiers first: the last workgroups to start are short
     const ParamSet ps = a.ps[blockIdx.y];
     float *const scores = a.scores + (int64_t)a.set_of[blockIdx.y] * a.score_stride;
     extern __shared__ uint64_t smem[];

@@ -78,10 +78,8 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
 __global__ __launch_bounds__(64) void k_plan_wave(PlanLaunch a) {
     __shared__ ChoiceL ch[kPlanCap];
     __shared__ uint32_t taken[64];  // local stages assigned so far (one device each at least)
-    const int b = blockIdx.x, lane = threadIdx.x, k = a.k;
-    const int64_t nF = a.dcounts ? (int64_t)a.dcounts[0] : a.nF;
-    const int64_t lo = first_slot_of_wave(a.frontier, nF, (uint32_t)b);
-    const int64_t hi = first_slot_of_wave(a.frontier, nF, (uint32_t)b + 1u);
+    const int b = (int)a.order[blockIdx.x], lane = threadIdx.x, k = a.k;  // largest frontiers first
+    const int64_t lo = a.fr_off[b], hi = a.fr_off[b + 1];
     const int64_t base = lo * k;
     const uint32_t n = (uint32_t)((hi - lo) * k);
     const uint32_t nl = n < (uint32_t)kPlanCap ? n : (uint32_t)kPlanCap;

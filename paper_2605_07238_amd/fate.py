@@ -106,7 +106,7 @@ class StateH(C.Structure):
                 ("n_slices", C.c_int64), ("slices", C.c_void_p),
                 ("n_done_edges", C.c_int64), ("done_n", C.c_void_p), ("done", C.c_void_p),
                 ("advance", C.c_int32), ("status", C.c_void_p), ("counts", C.c_void_p), ("finish", C.c_void_p),
-                ("slice", C.c_int32), ("fr_off", C.c_void_p)]
+                ("slice", C.c_int32), ("fr_off", C.c_void_p), ("order", C.c_void_p)]
 
 
 _lib = None

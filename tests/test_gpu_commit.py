@@ -35,7 +35,8 @@ def _sections(st):
     N, B, E = int(h.N), int(h.B), int(h.n_done_edges)
     return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
                 slices=take(h.slices, 3 * nS).reshape(nS, 3), done_n=take(h.done_n, N),
-                done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), counts=(nF, nC, nS, rej))
+                done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), order=take(h.order, B),
+                counts=(nF, nC, nS, rej))
 
 
 def _host_sections(pk, w):
@@ -50,7 +51,17 @@ def _host_sections(pk, w):
     B, E = int(h.B), int(h.n_done_edges)
     return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
                 slices=take(h.slices, 3 * nS).reshape(nS, 3), done_n=take(h.done_n, N),
-                done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), n_cand=int(h.n_cand))
+                done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), order=take(h.order, B),
+                n_cand=int(h.n_cand))
+
+
+def check_order(order, fr_off):
+    """The dispatch order is a permutation of the instances by decreasing
+    frontier size (sizes from 1,023 on tie)."""
+    B = len(order)
+    assert np.array_equal(np.sort(order), np.arange(B)), "order is not a permutation"
+    size = np.minimum(np.diff(np.asarray(fr_off, np.int64))[order], 1023)
+    assert np.all(np.diff(size) <= 0), "order is not by decreasing frontier size"
 
 
 def pending_lists(sec, par_off, status):
@@ -90,6 +101,8 @@ def _compare_sections(pk, st, w_ref):
     assert nC == host["n_cand"]
     assert np.array_equal(dev["slices"], host["slices"]), "slices"
     assert np.array_equal(dev["fr_off"], host["fr_off"]), "frontier offsets per instance"
+    check_order(dev["order"], dev["fr_off"])
+    check_order(host["order"], host["fr_off"])
     dn, de = pending_lists(dev, w_ref.par_off, w_ref.status)
     hn, he = pending_lists(host, w_ref.par_off, w_ref.status)
     assert np.array_equal(dn, hn), "completed-parent counts"

@@ -91,8 +91,9 @@ def test_host_layouts_match_independent_derivations(case):
     ch_idx = take(buf, hd.ch_idx, E)
     for v in range(N):
         assert ch_idx[ch_off[v]:ch_off[v + 1]].tolist() == [c for c in range(N) if v in inst.parents[c]], v
-    # frontier offsets per instance
+    # frontier offsets per instance, and the dispatch order
     assert take(sbuf, hs.fr_off, w.B + 1).tolist() == [0, nF]
+    assert take(sbuf, hs.order, w.B).tolist() == [0]
     # completed-parent lists of pending stages, in parent order, in the
     # first of each stage's parent slots
     done_n = take(sbuf, hs.done_n, N)
