@@ -1,7 +1,6 @@
 // Device helpers shared by the scoring, commit-and-advance and planning
 // kernels of libfate: bit tests, +infinity, the Load rule, the candidate
-// numbering of a frontier stage, a wave prefix sum and the frontier range of
-// an instance.
+// numbering of a frontier stage and a wave prefix sum.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -69,29 +68,6 @@ __device__ __forceinline__ uint32_t wave_exscan_u32(uint32_t x, uint32_t &total)
     }
     total = __shfl(v, 63, 64);
     return v - x;
-}
-
-// First frontier slot whose instance is >= b (the frontier is ordered by
-// instance), found by the whole wave (all 64 lanes active): each lane probes
-// one position, so every round of parallel loads shrinks the range 64-fold.
-__device__ inline int64_t first_slot_of_wave(const uint32_t *frontier, int64_t nF, uint32_t b) {
-    const int lane = threadIdx.x & 63;
-    int64_t lo = 0, hi = nF;  // the answer lies in [lo, hi]
-    for (;;) {  // uniform
-        const int64_t n = hi - lo;
-        if (n <= 64) {  // probe every position
-            const bool below = lane < n && frontier[2 * (lo + lane) + 1] < b;
-            return lo + __popcll(__ballot(below));
-        }
-        // probes p_l = lo + floor((l + 1) n / 64) - 1 rise strictly and end at hi - 1;
-        // those below b form a prefix of cnt probes
-        const int64_t p = lo + ((int64_t)(lane + 1) * n) / 64 - 1;
-        const int cnt = __popcll(__ballot(frontier[2 * p + 1] < b));
-        const int64_t nlo = cnt > 0 ? lo + ((int64_t)cnt * n) / 64 : lo;              // p_{cnt-1} + 1
-        const int64_t nhi = cnt < 64 ? lo + ((int64_t)(cnt + 1) * n) / 64 - 1 : hi;   // p_cnt
-        lo = nlo;
-        hi = nhi;
-    }
 }
 
 }  // namespace fate

@@ -901,6 +901,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     a.done_n = state->done_n;
     a.done = static_cast<const fate::DoneParent *>(state->done);
     a.order = state->order;
+    a.fr_off = state->fr_off;
     a.scores = d_scores;
     a.score_stride = stride;
     a.dcounts = state->advance ? state->counts : nullptr;

@@ -65,6 +65,7 @@ struct ScoreLaunch {
     const uint32_t *done_n;  // completed parents of stage g: done[rec[g].par_begin ..] (done_n[g] of them)
     const DoneParent *done;
     const uint32_t *order;   // instances by decreasing frontier size (grid row x takes order[x])
+    const uint32_t *fr_off;  // [B+1] instance b's frontier slots
     float *scores;            // parameter set p (blockIdx.y) writes scores + p * score_stride
     int64_t score_stride;
     const uint32_t *dcounts;  // planning state: counts[2] = current slices, else null

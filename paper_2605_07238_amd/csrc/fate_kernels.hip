@@ -1682,14 +1682,10 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
         const int i = tid + r * BLK;
         pre[r] = i < D * K ? a.pcache[(int64_t)b * D * K + i] : 0ull;
     }
-    if (tid < 64) {  // the instance's frontier range (the frontier is ordered by instance)
-        const int64_t nFc = a.dcounts ? (int64_t)a.dcounts[0] : a.nF;
-        const int64_t lo = first_slot_of_wave(a.frontier, nFc, (uint32_t)b);
-        const int64_t hi = first_slot_of_wave(a.frontier, nFc, (uint32_t)b + 1u);
-        if (tid == 0) {
-            misc[0] = (uint32_t)lo;
-            misc[1] = (uint32_t)(hi - lo);
-        }
+    if (tid == 0) {  // the instance's frontier range
+        const uint32_t lo = a.fr_off[b], hi = a.fr_off[b + 1];
+        misc[0] = lo;
+        misc[1] = hi - lo;
     }
     __syncthreads();
     const int64_t lo = misc[0];
