@@ -25,7 +25,9 @@
 //   k_commit_scan   one workgroup: exclusive scan of the instances' totals
 //                   (frontier stages, candidates, slices, rejected
 //                   selections): frontier offsets per instance and the
-//                   counters the scoring and top-k launches read.
+//                   counters the scoring and top-k launches read; then the
+//                   dispatch order (instances by decreasing frontier size)
+//                   and the instances' slices placed in that order.
 //   k_commit_fill   one wave per instance: its frontier slots, candidate
 //                   offsets and scoring slices at the scanned offsets.
 #include <hip/hip_runtime.h>
@@ -434,15 +436,14 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
         }
         uint32_t ex[4], all[4];
         block_exscan<1024, 4>(x, sh, ex, all);
-        uint32_t f = run[0] + ex[0], c = run[1] + ex[1], sl = run[2] + ex[2];
+        uint32_t f = run[0] + ex[0], c = run[1] + ex[1];
 #pragma unroll
         for (int j = 0; j < kScanItems; ++j) {
             if (b0 + j >= a.B) break;
             a.fr_off[b0 + j] = f;
-            reinterpret_cast<uint2 *>(a.base)[b0 + j] = make_uint2(c, sl);
+            a.base[2 * (b0 + j)] = c;
             f += t[j].x;
             c += t[j].y;
-            sl += t[j].z;
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) run[q] += all[q];
@@ -462,7 +463,35 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
         hist[threadIdx.x] = ex[0];
         __syncthreads();
     }
-    for (int b0 = (int)threadIdx.x; b0 < a.B; b0 += 1024) a.order[atomicAdd(&hist[bucket(tot[b0].x)], 1u)] = (uint32_t)b0;
+    for (int b0 = (int)threadIdx.x; b0 < a.B; b0 += 1024) {
+        const uint4 t = tot[b0];
+        const uint32_t pos = atomicAdd(&hist[bucket(t.x)], 1u);
+        a.order[pos] = (uint32_t)b0;
+        a.nsp[pos] = t.z;
+    }
+    __syncthreads();  // the order and the slice counts by position are complete
+    // the instances' first slices, in the dispatch order: the scoring
+    // launch's workgroups then take the largest frontiers first too
+    uint32_t srun = 0;
+    for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // uniform
+        const int i0 = batch + (int)threadIdx.x * kScanItems;
+        uint32_t n[kScanItems], bq[kScanItems], x[1] = {0u};
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            n[j] = i0 + j < a.B ? a.nsp[i0 + j] : 0u;
+            bq[j] = i0 + j < a.B ? a.order[i0 + j] : 0u;
+            x[0] += n[j];
+        }
+        uint32_t ex[1], all[1];
+        block_exscan<1024, 1>(x, sh, ex, all);
+        uint32_t sp = srun + ex[0];
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            if (i0 + j < a.B) a.base[2 * bq[j] + 1] = sp;
+            sp += n[j];
+        }
+        srun += all[0];
+    }
 }
 
 __global__ __launch_bounds__(64) void k_commit_fill(CommitLaunch a) {

@@ -376,22 +376,25 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
                 if (nc >= (int64_t(1) << 32)) return FATE_ERANGE;
             }
         }
-        const int64_t last = (int64_t)p->frontier.size() / 2;
-        for (int64_t f = first; f < last; f += slice) {
-            p->slices.push_back((uint32_t)b);
-            p->slices.push_back((uint32_t)f);
-            p->slices.push_back((uint32_t)std::min(last, f + slice));
-        }
     }
-    p->nS = (int64_t)p->slices.size() / 3;
     p->fr_off[B] = (uint32_t)(p->frontier.size() / 2);
     // per-instance launches take the largest frontiers first, so that the
-    // last workgroups to start are short ones
+    // last workgroups to start are short ones; the scoring slices follow the
+    // same order
     p->order.resize(B);
     for (int b = 0; b < B; ++b) p->order[b] = (uint32_t)b;
     std::stable_sort(p->order.begin(), p->order.end(), [&](uint32_t x, uint32_t y) {
         return p->fr_off[x + 1] - p->fr_off[x] > p->fr_off[y + 1] - p->fr_off[y];
     });
+    for (uint32_t b : p->order) {
+        const int64_t first = p->fr_off[b], last = p->fr_off[b + 1];
+        for (int64_t f = first; f < last; f += slice) {
+            p->slices.push_back(b);
+            p->slices.push_back((uint32_t)f);
+            p->slices.push_back((uint32_t)std::min(last, f + slice));
+        }
+    }
+    p->nS = (int64_t)p->slices.size() / 3;
     // completed parents of every pending stage (only pending stages are
     // scored, in the frontier or in a horizon), with their holders and
     // sizes, in the first of the stage's parent slots
@@ -832,6 +835,7 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     a.list = reinterpret_cast<uint32_t *>(ws + W.list);
     a.tot = reinterpret_cast<uint32_t *>(ws + W.tot);
     a.base = reinterpret_cast<uint32_t *>(ws + W.base);
+    a.nsp = reinterpret_cast<uint32_t *>(ws + W.nsp);
     a.gbm = reinterpret_cast<uint32_t *>(ws + W.gbm);
     // the largest instance's bitmap, with the slack of an unaligned start in
     // the workspace

@@ -123,6 +123,7 @@ struct CommitLaunch {
                      // relative to the instance) from stage_off[b] on
     uint32_t *tot;   // [B][4]: new frontier stages, candidates, slices, rejected selections
     uint32_t *base;  // [B][2]: the instance's first candidate and first slice
+    uint32_t *nsp;   // [B]: slices of the instance at each dispatch position
     uint32_t *gbm;   // frontier bitmaps of instances too large for LDS
     int32_t bm_lds;  // 1: every instance's bitmap fits the apply kernel's LDS
     int32_t bm_words;  // bitmap words of the largest instance
@@ -135,11 +136,12 @@ struct CommitLaunch {
 constexpr int kCommitLdsBitmapWords = 1024;
 
 // Workspace of the commit: the new frontier lists (one slot per stage), the
-// per-instance totals and bases, and the frontier bitmaps of large instances
+// per-instance totals, bases and slice counts by dispatch position, and the
+// frontier bitmaps of large instances
 // (instance b's from word (stage_off[b] >> 5) + b, covering bit
 // (stage_off[b] & 31) + i for its stage i).
 struct CommitWs {
-    size_t list, tot, base, gbm, total;
+    size_t list, tot, base, nsp, gbm, total;
 };
 inline CommitWs commit_ws_layout(int64_t N, int B) {
     auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
@@ -148,6 +150,7 @@ inline CommitWs commit_ws_layout(int64_t N, int B) {
     w.list = o; o = up(o + 8 * (size_t)N);
     w.tot = o; o = up(o + 16 * (size_t)B);
     w.base = o; o = up(o + 8 * (size_t)B);
+    w.nsp = o; o = up(o + 4 * (size_t)B);
     w.gbm = o; o = up(o + 4 * ((size_t)N / 32 + (size_t)B + 1));
     w.total = o;
     return w;

@@ -36,7 +36,7 @@ def _sections(st):
     return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
                 slices=take(h.slices, 3 * nS).reshape(nS, 3), done_n=take(h.done_n, N),
                 done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), order=take(h.order, B),
-                counts=(nF, nC, nS, rej))
+                slice=int(h.slice), counts=(nF, nC, nS, rej))
 
 
 def _host_sections(pk, w):
@@ -52,7 +52,7 @@ def _host_sections(pk, w):
     return dict(frontier=take(h.frontier, 2 * nF).reshape(nF, 2), cand_off=take(h.cand_off, nF + 1),
                 slices=take(h.slices, 3 * nS).reshape(nS, 3), done_n=take(h.done_n, N),
                 done=take(h.done, 4 * E).reshape(-1, 4), fr_off=take(h.fr_off, B + 1), order=take(h.order, B),
-                n_cand=int(h.n_cand))
+                slice=int(h.slice), n_cand=int(h.n_cand))
 
 
 def check_order(order, fr_off):
@@ -62,6 +62,14 @@ def check_order(order, fr_off):
     assert np.array_equal(np.sort(order), np.arange(B)), "order is not a permutation"
     size = np.minimum(np.diff(np.asarray(fr_off, np.int64))[order], 1023)
     assert np.all(np.diff(size) <= 0), "order is not by decreasing frontier size"
+
+
+def check_slices(sec):
+    """Each instance's frontier range cut into pieces of the state's slice
+    length, the instances in the dispatch order."""
+    fr, L = sec["fr_off"], sec["slice"]
+    want = [(b, f, min(int(fr[b + 1]), f + L)) for b in sec["order"] for f in range(int(fr[b]), int(fr[b + 1]), L)]
+    assert np.array_equal(sec["slices"], np.array(want, np.uint32).reshape(-1, 3)), "slices"
 
 
 def pending_lists(sec, par_off, status):
@@ -99,10 +107,13 @@ def _compare_sections(pk, st, w_ref):
     assert np.array_equal(dev["frontier"], host["frontier"]), "frontier"
     assert np.array_equal(dev["cand_off"], host["cand_off"]), "candidate offsets"
     assert nC == host["n_cand"]
-    assert np.array_equal(dev["slices"], host["slices"]), "slices"
     assert np.array_equal(dev["fr_off"], host["fr_off"]), "frontier offsets per instance"
-    check_order(dev["order"], dev["fr_off"])
-    check_order(host["order"], host["fr_off"])
+    for sec in (dev, host):
+        check_order(sec["order"], sec["fr_off"])
+        check_slices(sec)
+    # the same slices (their order follows each side's dispatch order, whose ties may differ)
+    key = lambda sl: sl[np.lexsort((sl[:, 1], sl[:, 0]))]
+    assert np.array_equal(key(dev["slices"]), key(host["slices"])), "slices"
     dn, de = pending_lists(dev, w_ref.par_off, w_ref.status)
     hn, he = pending_lists(host, w_ref.par_off, w_ref.status)
     assert np.array_equal(dn, hn), "completed-parent counts"
