@@ -27,7 +27,8 @@
 //                   selections): frontier offsets per instance and the
 //                   counters the scoring and top-k launches read; then the
 //                   dispatch order (instances by decreasing frontier size)
-//                   and the instances' slices placed in that order.
+//                   and, for batches the general scoring kernel takes, the
+//                   instances' slices placed in that order.
 //   k_commit_fill   one wave per instance: its frontier slots, candidate
 //                   offsets and scoring slices at the scanned offsets.
 #include <hip/hip_runtime.h>
@@ -413,6 +414,9 @@ constexpr int kScanItems = 4;
 constexpr int kOrderBuckets = 1024;
 static_assert(kOrderBuckets == 1024, "one bucket per thread of k_commit_scan");
 
+// SLICES: the batch's slices follow the dispatch order (the general scoring
+// kernel uses them); otherwise they stay in instance order.
+template <bool SLICES>
 __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
     __shared__ uint32_t sh[4 * (1024 / 64)];
     __shared__ uint32_t hist[kOrderBuckets];  // instances per frontier size, largest first
@@ -436,14 +440,16 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
         }
         uint32_t ex[4], all[4];
         block_exscan<1024, 4>(x, sh, ex, all);
-        uint32_t f = run[0] + ex[0], c = run[1] + ex[1];
+        uint32_t f = run[0] + ex[0], c = run[1] + ex[1], sl = run[2] + ex[2];
 #pragma unroll
         for (int j = 0; j < kScanItems; ++j) {
             if (b0 + j >= a.B) break;
             a.fr_off[b0 + j] = f;
             a.base[2 * (b0 + j)] = c;
+            if (!SLICES) a.base[2 * (b0 + j) + 1] = sl;  // slices in instance order
             f += t[j].x;
             c += t[j].y;
+            sl += t[j].z;
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) run[q] += all[q];
@@ -463,15 +469,26 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
         hist[threadIdx.x] = ex[0];
         __syncthreads();
     }
-    for (int b0 = (int)threadIdx.x; b0 < a.B; b0 += 1024) {
-        const uint4 t = tot[b0];
-        const uint32_t pos = atomicAdd(&hist[bucket(t.x)], 1u);
-        a.order[pos] = (uint32_t)b0;
-        a.nsp[pos] = t.z;
+    for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // the items' loads issued together
+        const int b0 = batch + (int)threadIdx.x * kScanItems;
+        uint2 t[kScanItems];
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const uint4 q = b0 + j < a.B ? tot[b0 + j] : make_uint4(0u, 0u, 0u, 0u);
+            t[j] = make_uint2(q.x, q.z);
+        }
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            if (b0 + j >= a.B) break;
+            const uint32_t pos = atomicAdd(&hist[bucket(t[j].x)], 1u);
+            a.order[pos] = (uint32_t)(b0 + j);
+            a.nsp[pos] = t[j].y;
+        }
     }
+    if (!SLICES) return;
     __syncthreads();  // the order and the slice counts by position are complete
-    // the instances' first slices, in the dispatch order: the scoring
-    // launch's workgroups then take the largest frontiers first too
+    // the instances' first slices, in the dispatch order: the general scoring
+    // kernel's workgroups then take the largest frontiers first too
     uint32_t srun = 0;
     for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // uniform
         const int i0 = batch + (int)threadIdx.x * kScanItems;
@@ -520,7 +537,8 @@ int launch_commit(const CommitLaunch &a, void *stream) {
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const size_t lds = apply_lds_bytes(a.D, a.M, a.K, a.bm_lds ? a.bm_words : 0);
     if (a.B > 0) hipLaunchKernelGGL(k_commit_apply, dim3((unsigned)a.B), dim3(64), lds, s, a);
-    hipLaunchKernelGGL(k_commit_scan, dim3(1), dim3(1024), 0, s, a);
+    if (a.slice_order) hipLaunchKernelGGL(k_commit_scan<true>, dim3(1), dim3(1024), 0, s, a);
+    else hipLaunchKernelGGL(k_commit_scan<false>, dim3(1), dim3(1024), 0, s, a);
     if (a.B > 0) hipLaunchKernelGGL(k_commit_fill, dim3((unsigned)a.B), dim3(64), 0, s, a);
     return (int)hipGetLastError();
 }

@@ -380,13 +380,15 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
     p->fr_off[B] = (uint32_t)(p->frontier.size() / 2);
     // per-instance launches take the largest frontiers first, so that the
     // last workgroups to start are short ones; the scoring slices follow the
-    // same order
+    // same order where the general scoring kernel uses them
     p->order.resize(B);
     for (int b = 0; b < B; ++b) p->order[b] = (uint32_t)b;
     std::stable_sort(p->order.begin(), p->order.end(), [&](uint32_t x, uint32_t y) {
         return p->fr_off[x + 1] - p->fr_off[x] > p->fr_off[y + 1] - p->fr_off[y];
     });
-    for (uint32_t b : p->order) {
+    const bool in_order = !fate::rows_batch(pk, max_shard);
+    for (int i = 0; i < B; ++i) {
+        const uint32_t b = in_order ? p->order[i] : (uint32_t)i;
         const int64_t first = p->fr_off[b], last = p->fr_off[b + 1];
         for (int64_t f = first; f < last; f += slice) {
             p->slices.push_back(b);
@@ -841,6 +843,7 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     // the workspace
     a.bm_words = (int32_t)((dags->max_stages + 31 + 31) / 32);
     a.bm_lds = a.bm_words <= fate::kCommitLdsBitmapWords ? 1 : 0;
+    a.slice_order = fate::rows_batch(dags, state->max_shard) ? 0 : 1;
     a.N = state->N;
     a.B = state->B;
     a.D = dags->D;

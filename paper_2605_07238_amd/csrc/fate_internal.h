@@ -125,11 +125,23 @@ struct CommitLaunch {
     uint32_t *base;  // [B][2]: the instance's first candidate and first slice
     uint32_t *nsp;   // [B]: slices of the instance at each dispatch position
     uint32_t *gbm;   // frontier bitmaps of instances too large for LDS
+    int32_t slice_order;  // 1: the slices follow the dispatch order (rows_batch false)
     int32_t bm_lds;  // 1: every instance's bitmap fits the apply kernel's LDS
     int32_t bm_words;  // bitmap words of the largest instance
     int64_t N;
     int32_t B, D, M, K, max_shard, slice;
 };
+
+// Whether scoring on this batch takes the row kernel (k_rows) for parameter
+// sets without a variant: single-device candidates only, uniform beta, hop
+// levels, D <= 16, M <= 32.  Its scoring slices then go unused, and the
+// packer and the commit leave them in instance order; otherwise they follow
+// the dispatch order (largest frontiers first).
+inline bool rows_batch(const fate_dags_t *dags, int max_shard) {
+    const int r = dags->max_r < max_shard ? dags->max_r : max_shard;
+    return dags->beta_uniform && (r < dags->D ? r : dags->D) <= 1 && dags->levels != FATE_LEVELS_TOPO &&
+           dags->D <= 16 && dags->M <= 32;
+}
 
 // Bitmap words past which an instance's frontier bitmap moves from LDS to
 // the workspace (instances of more than 32,768 stages).

@@ -64,11 +64,21 @@ def check_order(order, fr_off):
     assert np.all(np.diff(size) <= 0), "order is not by decreasing frontier size"
 
 
-def check_slices(sec):
+def rows_batch(pk, st):
+    """Whether variant-free scoring of this batch takes the row kernel, which
+    does not use the slices (single-device candidates, uniform beta, hop
+    levels, D <= 16, M <= 32)."""
+    h = pk.handle
+    r = min(int(h.max_r), int(st.handle.max_shard), int(h.D))
+    return bool(h.beta_uniform) and r <= 1 and h.levels != fate.FATE_LEVELS_TOPO and h.D <= 16 and h.M <= 32
+
+
+def check_slices(sec, in_order):
     """Each instance's frontier range cut into pieces of the state's slice
-    length, the instances in the dispatch order."""
+    length, the instances in the dispatch order (in_order) or by id."""
     fr, L = sec["fr_off"], sec["slice"]
-    want = [(b, f, min(int(fr[b + 1]), f + L)) for b in sec["order"] for f in range(int(fr[b]), int(fr[b + 1]), L)]
+    insts = sec["order"] if in_order else range(len(sec["order"]))
+    want = [(b, f, min(int(fr[b + 1]), f + L)) for b in insts for f in range(int(fr[b]), int(fr[b + 1]), L)]
     assert np.array_equal(sec["slices"], np.array(want, np.uint32).reshape(-1, 3)), "slices"
 
 
@@ -110,7 +120,7 @@ def _compare_sections(pk, st, w_ref):
     assert np.array_equal(dev["fr_off"], host["fr_off"]), "frontier offsets per instance"
     for sec in (dev, host):
         check_order(sec["order"], sec["fr_off"])
-        check_slices(sec)
+        check_slices(sec, not rows_batch(pk, st))
     # the same slices (their order follows each side's dispatch order, whose ties may differ)
     key = lambda sl: sl[np.lexsort((sl[:, 1], sl[:, 0]))]
     assert np.array_equal(key(dev["slices"]), key(host["slices"])), "slices"
