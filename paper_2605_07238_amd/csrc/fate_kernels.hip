@@ -1864,14 +1864,21 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                 if (dn > 0) {  // the row goes through the task's sum slots, indexed by device
 #pragma unroll
                     for (int j = 0; j < NJ; ++j) part4[j * pcol + t] = make_float4(B[4 * j], B[4 * j + 1], B[4 * j + 2], B[4 * j + 3]);
-                    for (uint32_t q = 0; q < dn; ++q) {
-                        const DoneParent pu = a.done[db + q];
-                        const float tq = lam_tr * b0 * pu.sigma;
-                        xb += tq;
-                        const float pw = tq + cw;
-                        for (uint32_t h = (uint32_t)pu.holders & dmask; h; h &= h - 1u) {
-                            const int d = __builtin_ctz(h);
-                            partf[((d >> 2) * pcol + t) * 4 + (d & 3)] -= pw;
+                    for (uint32_t q0 = 0; q0 < dn; q0 += 4) {  // the batch's loads are issued together
+                        DoneParent pb[4];
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            if (q0 + j < dn) pb[j] = a.done[db + q0 + j];
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            if (q0 + j >= dn) break;
+                            const float tq = lam_tr * b0 * pb[j].sigma;
+                            xb += tq;
+                            const float pw = tq + cw;
+                            for (uint32_t h = (uint32_t)pb[j].holders & dmask; h; h &= h - 1u) {
+                                const int d = __builtin_ctz(h);
+                                partf[((d >> 2) * pcol + t) * 4 + (d & 3)] -= pw;
+                            }
                         }
                     }
 #pragma unroll
