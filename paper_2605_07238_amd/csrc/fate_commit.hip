@@ -109,26 +109,47 @@ __host__ __device__ inline size_t apply_lds_bytes(int D, int M, int K, int bm_wo
            8 * (size_t)D * padded_slots(K) + 4 * (size_t)D + 4 * (size_t)bm_words;
 }
 
-// When the outputs of stage s's parents are on device d for a k-shard
-// placement: the latest parent finish plus, for a parent whose output d does
-// not hold, its size times the cheapest transfer coefficient into d over k.
-__device__ double inputs_ready(const CommitLaunch &a, const StageRec &r, int d, int k) {
-    double ready = -__builtin_inf();
-    for (uint32_t q = 0; q < r.npar; ++q) {
-        const uint32_t u = a.par_idx[r.par_begin + q];
-        const uint64_t hu = a.holders[u];
-        double arr = (double)a.fin[u];
-        if (!bit(hu, d)) {
-            double bmin = __builtin_inf();
-            for (uint64_t t = hu; t; t &= t - 1) {
-                const double bt = (double)a.beta[__builtin_ctzll(t) * a.D + d];
-                bmin = bt < bmin ? bt : bmin;
-            }
-            arr = (double)a.fin[u] + (double)a.rec[u].sigma * bmin / (double)k;
+// When the outputs of stage s's parents are on each device i0 + p (p < k) of
+// a k-shard window: the latest parent finish plus, for a parent whose output
+// that device does not hold, its size times the cheapest transfer coefficient
+// into the device over k.  The parents' ids, then their holders, finish
+// times and sizes, are loaded kParBatch at a time.
+__device__ void inputs_ready(const CommitLaunch &a, const StageRec &r, int i0, int k, double (&ready)[FATE_MAX_SHARD]) {
+#pragma unroll
+    for (int p = 0; p < FATE_MAX_SHARD; ++p) ready[p] = -__builtin_inf();
+    for (uint32_t q0 = 0; q0 < r.npar; q0 += kParBatch) {
+        uint32_t u[kParBatch];
+#pragma unroll
+        for (int j = 0; j < kParBatch; ++j) u[j] = q0 + j < r.npar ? a.par_idx[r.par_begin + q0 + j] : 0u;
+        uint64_t hu[kParBatch];
+        float fu[kParBatch], su[kParBatch];
+#pragma unroll
+        for (int j = 0; j < kParBatch; ++j) {
+            const bool in = q0 + j < r.npar;
+            hu[j] = in ? a.holders[u[j]] : 0ull;
+            fu[j] = in ? a.fin[u[j]] : 0.0f;
+            su[j] = in ? a.rec[u[j]].sigma : 0.0f;
         }
-        ready = arr > ready ? arr : ready;
+        for (int j = 0; j < kParBatch && q0 + j < r.npar; ++j) {
+            for (int p = 0; p < k; ++p) {
+                const int d = i0 + p;
+                double arr = (double)fu[j];
+                if (!bit(hu[j], d)) {
+                    double bmin = __builtin_inf();
+                    if (a.beta_uniform) {
+                        bmin = (double)a.beta0;  // every off-diagonal coefficient
+                    } else {
+                        for (uint64_t t = hu[j]; t; t &= t - 1) {
+                            const double bt = (double)a.beta[__builtin_ctzll(t) * a.D + d];
+                            bmin = bt < bmin ? bt : bmin;
+                        }
+                    }
+                    arr = (double)fu[j] + (double)su[j] * bmin / (double)k;
+                }
+                ready[p] = arr > ready[p] ? arr : ready[p];
+            }
+        }
     }
-    return ready;
 }
 
 // Is the nonzero group h in the padded row?  Empty and padding entries
@@ -245,7 +266,7 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
                         x.i0 = i0;
                         // parents completed in earlier steps: their finish
                         // times and holders are settled
-                        for (int p = 0; p < k; ++p) x.ready[p] = inputs_ready(a, r, i0 + p, k);
+                        inputs_ready(a, r, i0, k, x.ready);
                         a.holders[s] = w;
                         a.status[s] = kCompleted;
                     }

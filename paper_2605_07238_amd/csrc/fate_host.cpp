@@ -844,6 +844,8 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     a.bm_words = (int32_t)((dags->max_stages + 31 + 31) / 32);
     a.bm_lds = a.bm_words <= fate::kCommitLdsBitmapWords ? 1 : 0;
     a.slice_order = fate::rows_batch(dags, state->max_shard) ? 0 : 1;
+    a.beta_uniform = dags->beta_uniform;
+    a.beta0 = dags->beta0;
     a.N = state->N;
     a.B = state->B;
     a.D = dags->D;

@@ -130,6 +130,8 @@ struct CommitLaunch {
     int32_t bm_words;  // bitmap words of the largest instance
     int64_t N;
     int32_t B, D, M, K, max_shard, slice;
+    int32_t beta_uniform;  // every off-diagonal beta equals beta0
+    float beta0;
 };
 
 // Whether scoring on this batch takes the row kernel (k_rows) for parameter
