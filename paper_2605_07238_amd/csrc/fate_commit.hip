@@ -231,6 +231,8 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
     // empty slot filled, so head stays 0 while any slot is empty.
     int head = 0, nempty = 0;
     for (int e = 0; e < K; ++e) nempty += row[e] == 0ull ? 1 : 0;
+    bool held = false;         // uniform: a chunk's children wait for the next pass
+    uint32_t hcb = 0, hcn = 0;  // the held chunk's lane: its stage's first child, its pair count
     for (int64_t c0 = lo; c0 < hi; c0 += 64) {  // uniform: chunks of 64 slots
         // lane q checks slot c0 + q and records its stage as completed
         const int64_t f = c0 + lane;
@@ -332,26 +334,44 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
             }
             a.fin[s] = (float)fs;
         }
-        // Children of the stages this chunk completed, one (stage, child)
-        // pair per lane.  Every parent status and holder set so far is
-        // visible to the wave (the barriers above).  A child with several
-        // parents completed in this step is rewritten once per such parent,
-        // each time from the statuses then settled: a later rewrite sees
-        // more completed parents, and the last one sees them all (parents in
-        // the same chunk write the same list).  No child of a stage pending
-        // before this step is in the frontier, so its bit is new.
-        uint32_t npairs = 0;
-        const uint32_t first = wave_exscan_u32(kq > 0 ? cn : 0u, npairs);
+        // Children of the stages completed in this chunk and, every other
+        // chunk, in the one before it (its pair counts wait in registers), one
+        // (stage, child) pair per lane.  Every parent status and holder set so
+        // far is visible to the wave (the barriers above).  A child with
+        // several parents completed in this step is rewritten once per such
+        // parent, each time from the statuses then settled: a later rewrite
+        // sees more completed parents, and the last one sees them all
+        // (parents in the same pass write the same list).  No child of a
+        // stage pending before this step is in the frontier, so its bit is new.
+        const uint32_t ncur = kq > 0 ? cn : 0u;
+        if (!held && c0 + 64 < hi) {  // uniform: hold this chunk's children for the next pass
+            held = true;
+            hcb = cb;
+            hcn = ncur;
+            __syncthreads();
+            continue;
+        }
+        uint32_t n0 = 0, n1 = 0;
+        const uint32_t first0 = wave_exscan_u32(held ? hcn : 0u, n0);  // the held chunk's pairs, then this one's
+        const uint32_t first1 = wave_exscan_u32(ncur, n1);
+        const uint32_t cb0 = held ? hcb : 0u;
+        held = false;
+        const uint32_t npairs = n0 + n1;
         for (uint32_t p0 = 0; p0 < npairs; p0 += 64) {  // uniform
             const uint32_t pr = p0 + (uint32_t)lane;
-            // the pair's stage: the last lane whose first pair is at or before it
+            const bool in1 = pr >= n0;
+            const uint32_t pl = in1 ? pr - n0 : pr;  // the pair within its chunk
+            // the pair's stage: the last lane of its chunk whose first pair is at or before it
             int q = 0;
 #pragma unroll
-            for (int step = 32; step >= 1; step >>= 1)
-                if ((uint32_t)__shfl((int)first, q + step) <= pr) q += step;
-            const uint32_t qb = (uint32_t)__shfl((int)cb, q), qf = (uint32_t)__shfl((int)first, q);
+            for (int step = 32; step >= 1; step >>= 1) {
+                const uint32_t f0 = (uint32_t)__shfl((int)first0, q + step), f1 = (uint32_t)__shfl((int)first1, q + step);
+                if ((in1 ? f1 : f0) <= pl) q += step;
+            }
+            const uint32_t qb0 = (uint32_t)__shfl((int)cb0, q), qb1 = (uint32_t)__shfl((int)cb, q);
+            const uint32_t qf0 = (uint32_t)__shfl((int)first0, q), qf1 = (uint32_t)__shfl((int)first1, q);
             if (pr < npairs) {
-                const uint32_t w = a.ch_idx[qb + (pr - qf)];
+                const uint32_t w = a.ch_idx[in1 ? qb1 + (pl - qf1) : qb0 + (pl - qf0)];
                 const StageRec rw = a.rec[w];
                 uint32_t nd = 0;
                 for (uint32_t q0 = 0; q0 < rw.npar; q0 += kParBatch) {  // the batch's loads are issued together
