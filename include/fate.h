@@ -238,10 +238,12 @@ typedef struct {
                                  from this build's for the DAGs' device count (ESTATE) */
     const uint32_t *fr_off;   /* [B+1]: instance b's frontier slots are
                                  fr_off[b] .. fr_off[b+1] (current counts) */
-    const uint32_t *order;    /* [B]: the instances by decreasing frontier size, the
-                                 order in which per-instance launches take them (a
-                                 dispatch order only: no result depends on it; a
-                                 commit re-sorts it, ties in any order) */
+    const uint32_t *order;    /* [B]: the order in which per-instance launches take
+                                 the instances, largest frontiers first: instance b
+                                 with a frontier of n stages, mx the largest, is in
+                                 class 7 - min(7, 8 n / (mx + 1)), classes ascending,
+                                 each in instance order (a dispatch order only: no
+                                 result depends on it; a commit recomputes it) */
 } fate_state_h;
 
 const char *fate_version(void);

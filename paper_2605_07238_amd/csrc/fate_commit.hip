@@ -26,9 +26,10 @@
 //                   (frontier stages, candidates, slices, rejected
 //                   selections): frontier offsets per instance and the
 //                   counters the scoring and top-k launches read; then the
-//                   dispatch order (instances by decreasing frontier size)
-//                   and, for batches the general scoring kernel takes, the
-//                   instances' slices placed in that order.
+//                   dispatch order (instances by size class of their
+//                   frontier, largest first) and, for batches the general
+//                   scoring kernel takes, the instances' slices placed in
+//                   that order.
 //   k_commit_fill   one wave per instance: its frontier slots, candidate
 //                   offsets and scoring slices at the scanned offsets.
 #include <hip/hip_runtime.h>
@@ -451,21 +452,23 @@ __global__ __launch_bounds__(64) void k_commit_apply(CommitLaunch a) {
 
 // Instances per thread of k_commit_scan: 4 K instances take one workgroup scan.
 constexpr int kScanItems = 4;
-// Frontier sizes the dispatch order distinguishes (larger ones tie).
-constexpr int kOrderBuckets = 1024;
-static_assert(kOrderBuckets == 1024, "one bucket per thread of k_commit_scan");
 
 // SLICES: the batch's slices follow the dispatch order (the general scoring
 // kernel uses them); otherwise they stay in instance order.
 template <bool SLICES>
 __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
+    constexpr int C = kOrderClasses;
+    static_assert(C * kScanItems * 16 < 1024, "one (class, item, wave) count per thread");
     __shared__ uint32_t sh[4 * (1024 / 64)];
-    __shared__ uint32_t hist[kOrderBuckets];  // instances per frontier size, largest first
+    __shared__ uint32_t smax;
+    __shared__ uint32_t gcnt[C * kScanItems * 16];      // per (class, item, wave): items
+    __shared__ uint32_t gbase[C * kScanItems * 16 + 1];  // their first positions in the batch
+    __shared__ uint32_t cstart[C + 1];                   // first position of each class (several batches)
     uint32_t run[4] = {0u, 0u, 0u, 0u};
     const uint4 *tot = reinterpret_cast<const uint4 *>(a.tot);
-    auto bucket = [](uint32_t n) { return (uint32_t)kOrderBuckets - 1u - min(n, (uint32_t)kOrderBuckets - 1u); };
-    hist[threadIdx.x] = 0u;
+    if (threadIdx.x == 0) smax = 0u;
     __syncthreads();
+    uint32_t mx = 0;  // the largest new frontier
     for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // uniform
         const int b0 = batch + (int)threadIdx.x * kScanItems;
         uint4 t[kScanItems];
@@ -477,7 +480,7 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
             x[1] += t[j].y;
             x[2] += t[j].z;
             x[3] += t[j].w;
-            if (b0 + j < a.B) atomicAdd(&hist[bucket(t[j].x)], 1u);
+            mx = max(mx, t[j].x);
         }
         uint32_t ex[4], all[4];
         block_exscan<1024, 4>(x, sh, ex, all);
@@ -501,30 +504,83 @@ __global__ __launch_bounds__(1024) void k_commit_scan(CommitLaunch a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) a.counts[q] = run[q];
     }
-    // the dispatch order of the next per-instance launches: a counting sort
-    // by new frontier size, largest first (ties in any order)
-    {
-        const uint32_t hx[1] = {hist[threadIdx.x]};
+    // The dispatch order of the next per-instance launches: the instances by
+    // size class of their new frontier, largest class first, each class in
+    // instance order (a stable partition; no atomics, so the order is the
+    // same on every run and equals the host packer's).  Per batch of 4,096
+    // instances, item j of thread t is instance batch + 1024 j + t, so that
+    // instance order is (j, wave, lane): ballots count each (class, j, wave),
+    // one prefix sum over those counts in class-major order places every
+    // (class, j, wave) group, and a lane's rank inside its wave's ballot
+    // places the item.  Batches before this one put their items of each
+    // class first.
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
+    if ((threadIdx.x & 63) == 0) atomicMax(&smax, mx);
+    __syncthreads();
+    mx = smax;
+    const int wv = (int)threadIdx.x >> 6, ln = (int)threadIdx.x & 63;
+    const uint64_t below = ln ? (~0ull >> (64 - ln)) : 0ull;  // the lanes before this one
+    // one batch: ballot counts, their class-major prefix sum into gbase, each
+    // item's rank in its wave's ballot
+    auto place = [&](int batch, uint32_t (&cl)[kScanItems], uint32_t (&rank)[kScanItems]) {
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const int b = batch + j * 1024 + (int)threadIdx.x;
+            cl[j] = b < a.B ? order_class(tot[b].x, mx) : (uint32_t)C;
+        }
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                const uint64_t m = __ballot(cl[j] == (uint32_t)q);
+                if (cl[j] == (uint32_t)q) rank[j] = (uint32_t)__popcll(m & below);
+                if (ln == 0) gcnt[(q * kScanItems + j) * 16 + wv] = (uint32_t)__popcll(m);
+            }
+        }
+        __syncthreads();
+        const uint32_t x[1] = {threadIdx.x < C * kScanItems * 16 ? gcnt[threadIdx.x] : 0u};
         uint32_t ex[1], all[1];
-        block_exscan<1024, 1>(hx, sh, ex, all);
-        hist[threadIdx.x] = ex[0];
+        block_exscan<1024, 1>(x, sh, ex, all);
+        if (threadIdx.x < C * kScanItems * 16) gbase[threadIdx.x] = ex[0];
+        if (threadIdx.x == 0) gbase[C * kScanItems * 16] = all[0];
+        __syncthreads();
+    };
+    // the classes' starts over the whole batch of instances
+    if (threadIdx.x <= C) cstart[threadIdx.x] = 0u;
+    __syncthreads();
+    const bool one = a.B <= kScanItems * 1024;  // uniform
+    if (!one) {
+        for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // uniform
+            uint32_t cl[kScanItems], rank[kScanItems];
+            place(batch, cl, rank);
+            if (threadIdx.x < C)
+                cstart[threadIdx.x + 1] += gbase[(threadIdx.x + 1) * kScanItems * 16] - gbase[threadIdx.x * kScanItems * 16];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0)
+            for (int q = 1; q <= C; ++q) cstart[q] += cstart[q - 1];
         __syncthreads();
     }
-    for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // the items' loads issued together
-        const int b0 = batch + (int)threadIdx.x * kScanItems;
-        uint2 t[kScanItems];
+    for (int batch = 0; batch < a.B; batch += kScanItems * 1024) {  // uniform: positions
+        uint32_t cl[kScanItems], rank[kScanItems];
+        place(batch, cl, rank);
 #pragma unroll
         for (int j = 0; j < kScanItems; ++j) {
-            const uint4 q = b0 + j < a.B ? tot[b0 + j] : make_uint4(0u, 0u, 0u, 0u);
-            t[j] = make_uint2(q.x, q.z);
+            const int b = batch + j * 1024 + (int)threadIdx.x;
+            if (b >= a.B) continue;
+            const uint32_t g = (cl[j] * kScanItems + j) * 16 + wv;
+            // the class's start over all batches, then this batch's items of
+            // the class before this (j, wave) group
+            const uint32_t pos = one ? gbase[g] + rank[j]
+                                     : cstart[cl[j]] + gbase[g] - gbase[cl[j] * kScanItems * 16] + rank[j];
+            a.order[pos] = (uint32_t)b;
+            if (SLICES) a.nsp[pos] = tot[b].z;
         }
-#pragma unroll
-        for (int j = 0; j < kScanItems; ++j) {
-            if (b0 + j >= a.B) break;
-            const uint32_t pos = atomicAdd(&hist[bucket(t[j].x)], 1u);
-            a.order[pos] = (uint32_t)(b0 + j);
-            a.nsp[pos] = t[j].y;
-        }
+        __syncthreads();  // gbase is rewritten by the next batch
+        if (!one && threadIdx.x < C)  // the next batch's items of a class follow this batch's
+            cstart[threadIdx.x] += gbase[(threadIdx.x + 1) * kScanItems * 16] - gbase[threadIdx.x * kScanItems * 16];
+        __syncthreads();
     }
     if (!SLICES) return;
     __syncthreads();  // the order and the slice counts by position are complete

@@ -382,9 +382,14 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
     // last workgroups to start are short ones; the scoring slices follow the
     // same order where the general scoring kernel uses them
     p->order.resize(B);
-    for (int b = 0; b < B; ++b) p->order[b] = (uint32_t)b;
+    uint32_t mx = 0;
+    for (int b = 0; b < B; ++b) {
+        p->order[b] = (uint32_t)b;
+        mx = std::max(mx, p->fr_off[b + 1] - p->fr_off[b]);
+    }
     std::stable_sort(p->order.begin(), p->order.end(), [&](uint32_t x, uint32_t y) {
-        return p->fr_off[x + 1] - p->fr_off[x] > p->fr_off[y + 1] - p->fr_off[y];
+        return fate::order_class(p->fr_off[x + 1] - p->fr_off[x], mx) <
+               fate::order_class(p->fr_off[y + 1] - p->fr_off[y], mx);
     });
     const bool in_order = !fate::rows_batch(pk, max_shard);
     for (int i = 0; i < B; ++i) {

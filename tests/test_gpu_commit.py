@@ -56,12 +56,13 @@ def _host_sections(pk, w):
 
 
 def check_order(order, fr_off):
-    """The dispatch order is a permutation of the instances by decreasing
-    frontier size (sizes from 1,023 on tie)."""
-    B = len(order)
-    assert np.array_equal(np.sort(order), np.arange(B)), "order is not a permutation"
-    size = np.minimum(np.diff(np.asarray(fr_off, np.int64))[order], 1023)
-    assert np.all(np.diff(size) <= 0), "order is not by decreasing frontier size"
+    """The dispatch order: instances by size class of their frontier (eight
+    classes in proportion to the largest frontier, largest first), each class
+    in instance order."""
+    n = np.diff(np.asarray(fr_off, np.int64))
+    mx = int(n.max()) if len(n) else 0
+    cls = 7 - np.minimum(7, n * 8 // (mx + 1))
+    assert np.array_equal(order, np.argsort(cls, kind="stable")), "dispatch order"
 
 
 def rows_batch(pk, st):
@@ -121,9 +122,8 @@ def _compare_sections(pk, st, w_ref):
     for sec in (dev, host):
         check_order(sec["order"], sec["fr_off"])
         check_slices(sec, not rows_batch(pk, st))
-    # the same slices (their order follows each side's dispatch order, whose ties may differ)
-    key = lambda sl: sl[np.lexsort((sl[:, 1], sl[:, 0]))]
-    assert np.array_equal(key(dev["slices"]), key(host["slices"])), "slices"
+    assert np.array_equal(dev["order"], host["order"]), "dispatch order"
+    assert np.array_equal(dev["slices"], host["slices"]), "slices"
     dn, de = pending_lists(dev, w_ref.par_off, w_ref.status)
     hn, he = pending_lists(host, w_ref.par_off, w_ref.status)
     assert np.array_equal(dn, hn), "completed-parent counts"

@@ -31,11 +31,10 @@ def _snapshot(st):
         return st.buf[off:off + nb].cpu().numpy().view(dt).copy() if n else np.zeros(0, dt)
 
     out = {k: np.asarray(v).view(np.uint8) for k, v in fate.state_arrays(st).items()}
-    sl = take(h.slices, 3 * nS).reshape(-1, 3)
-    sl = sl[np.lexsort((sl[:, 1], sl[:, 0]))]  # listed in the dispatch order, whose ties fall in any order
-    out.update(frontier=take(h.frontier, 2 * nF), cand_off=take(h.cand_off, nF + 1), slices=sl,
+    out.update(frontier=take(h.frontier, 2 * nF), cand_off=take(h.cand_off, nF + 1), slices=take(h.slices, 3 * nS),
                done_n=take(h.done_n, N), done=take(h.done, 4 * int(h.n_done_edges)),
-               fr_off=take(h.fr_off, int(h.B) + 1), counts=np.array([nF, nC, nS, rej], np.int64))
+               fr_off=take(h.fr_off, int(h.B) + 1), order=take(h.order, int(h.B)),
+               counts=np.array([nF, nC, nS, rej], np.int64))
     return out
 
 
