@@ -1761,18 +1761,30 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
         }
         __syncthreads();
         if (tid < 64) {
-            // tasks of L = ceil(R / max(1, cap - S)) rows over the chunk's R rows
-            // in S stages (at most cap tasks): every stage's full-length tasks
-            // first, then its shorter tail task; the tail tasks ordered by
-            // length, longest first (ties by stage), so that the lanes of a
-            // wave run the same number of rows
+            // tasks of L rows over the chunk's R rows in S stages, L the
+            // shortest length whose tasks (ceil(n / L) per stage of n rows) fit
+            // the cap task slots: every stage's full-length tasks first, then
+            // its shorter tail task; the tail tasks ordered by length, longest
+            // first (ties by stage), so that the lanes of a wave run the same
+            // number of rows
             const int i0 = 2 * tid, i1 = 2 * tid + 1;
             const uint32_t n0 = i0 < nC ? stg[i0].n : 0u, n1 = i1 < nC ? stg[i1].n : 0u;
             uint32_t R = 0, S = 0;
             (void)wave_exscan_u32(n0 + n1, R);
             (void)wave_exscan_u32((n0 ? 1u : 0u) + (n1 ? 1u : 0u), S);
-            const uint32_t room = plan.ntask > S ? plan.ntask - S : 1u;
-            const uint32_t Lr = R > 0 ? max(1u, (R + room - 1u) / room) : 1u;
+            // binary search between ceil(R / cap), below which the full tasks
+            // alone overflow, and ceil(R / (cap - S)), where even one tail per
+            // stage fits (S <= kRowsChunk < cap)
+            uint32_t lo = R > 0 ? max(1u, (R + plan.ntask - 1u) / plan.ntask) : 1u;
+            uint32_t hi = R > 0 ? max(1u, (R + plan.ntask - S - 1u) / (plan.ntask - S)) : 1u;
+            while (lo < hi) {  // uniform
+                const uint32_t mid = (lo + hi) >> 1;
+                uint32_t cnt = 0;
+                (void)wave_exscan_u32((n0 + mid - 1u) / mid + (n1 + mid - 1u) / mid, cnt);
+                if (cnt <= plan.ntask) hi = mid;
+                else lo = mid + 1u;
+            }
+            const uint32_t Lr = lo;
             const uint32_t f0n = n0 / Lr, f1n = n1 / Lr, t0n = n0 - f0n * Lr, t1n = n1 - f1n * Lr;
             uint32_t nfull = 0;
             const uint32_t off = wave_exscan_u32(f0n + f1n, nfull);
