@@ -107,6 +107,35 @@ def test_state_image_frontier(seed):
     assert np.array_equal(_view(sbuf, base, sh.holders, np.uint64, w.N), w.holders)
 
 
+@pytest.mark.parametrize("seed,uniform", [(0, False), (1, True), (2, False), (3, True)])
+def test_state_offsets_order_and_slices(seed, uniform):
+    """Per-instance frontier offsets; the dispatch order (eight size classes
+    in proportion to the largest frontier, largest first, each class in
+    instance order); the slices cut each instance's range into pieces of the
+    slice length, in the dispatch order unless the row kernel scores the
+    batch (single-device candidates, uniform beta, D <= 16, M <= 32), which
+    does not use them and keeps instance order."""
+    w = synth.make_random_small(seed, B=23, n=12 + seed, D=6, max_shard=1 if uniform else 3,
+                                shard_frac=0.0 if uniform else 0.4, uniform_beta=uniform)
+    buf, h, _ = fate.fate_layout_dags(w)
+    sbuf, sh, _ = fate.fate_layout_state(h, w)
+    base = sbuf.ctypes.data
+    F, S = int(sh.n_frontier), int(sh.n_slices)
+    fr = _view(sbuf, base, sh.frontier, np.uint32, 2 * F).reshape(F, 2)
+    fr_off = _view(sbuf, base, sh.fr_off, np.uint32, w.B + 1).astype(np.int64)
+    assert fr_off.tolist() == np.searchsorted(fr[:, 1], np.arange(w.B + 1), side="left").tolist()
+    n = np.diff(fr_off)
+    cls = 7 - np.minimum(7, n * 8 // (n.max() + 1))
+    order = _view(sbuf, base, sh.order, np.uint32, w.B)
+    assert order.tolist() == sorted(range(w.B), key=lambda b: (cls[b], b))
+    rows_batch = bool(h.beta_uniform) and min(int(h.max_r), w.max_shard, w.D) <= 1 and w.D <= 16 and w.M <= 32
+    assert rows_batch == uniform
+    L = int(sh.slice)
+    insts = range(w.B) if rows_batch else order
+    want = [(b, f, min(int(fr_off[b + 1]), f + L)) for b in insts for f in range(int(fr_off[b]), int(fr_off[b + 1]), L)]
+    assert _view(sbuf, base, sh.slices, np.uint32, 3 * S).reshape(S, 3).tolist() == [list(x) for x in want]
+
+
 def _status(fn, w, H=None):
     try:
         fn(w, H)
