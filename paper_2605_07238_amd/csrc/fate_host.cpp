@@ -391,7 +391,7 @@ fate_status_t plan_state(const fate_dags_t *pk, const fate_dag_batch_t *g, const
         return fate::order_class(p->fr_off[x + 1] - p->fr_off[x], mx) <
                fate::order_class(p->fr_off[y + 1] - p->fr_off[y], mx);
     });
-    const bool in_order = !fate::rows_batch(pk, max_shard);
+    const bool in_order = !fate::rows_batch(pk, max_shard, K);
     for (int i = 0; i < B; ++i) {
         const uint32_t b = in_order ? p->order[i] : (uint32_t)i;
         const int64_t first = p->fr_off[b], last = p->fr_off[b + 1];
@@ -848,7 +848,7 @@ fate_status_t commit_impl(const fate_dags_t *dags, const fate_state_h *state, co
     // the workspace
     a.bm_words = (int32_t)((dags->max_stages + 31 + 31) / 32);
     a.bm_lds = a.bm_words <= fate::kCommitLdsBitmapWords ? 1 : 0;
-    a.slice_order = fate::rows_batch(dags, state->max_shard) ? 0 : 1;
+    a.slice_order = fate::rows_batch(dags, state->max_shard, state->K) ? 0 : 1;
     a.beta_uniform = dags->beta_uniform;
     a.beta0 = dags->beta0;
     a.N = state->N;

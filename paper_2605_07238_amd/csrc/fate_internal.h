@@ -134,15 +134,19 @@ struct CommitLaunch {
     float beta0;
 };
 
-// Whether scoring on this batch takes the row kernel (k_rows) for parameter
-// sets without a variant: single-device candidates only, uniform beta, hop
-// levels, D <= 16, M <= 32.  Its scoring slices then go unused, and the
-// packer and the commit leave them in instance order; otherwise they follow
-// the dispatch order (largest frontiers first).
-inline bool rows_batch(const fate_dags_t *dags, int max_shard) {
+// Whether a row kernel's LDS plan fits for D devices, K prefix slots and M
+// models (fate_kernels.hip).
+bool rows_kernel_fits(int D, int K, int M);
+
+// Whether scoring on this batch takes a row kernel (k_rows, k_rows4) for
+// parameter sets without a variant: single-device candidates only, uniform
+// beta, hop levels, and tables that fit.  Its scoring slices then go unused,
+// and the packer and the commit leave them in instance order; otherwise they
+// follow the dispatch order (largest frontiers first).
+inline bool rows_batch(const fate_dags_t *dags, int max_shard, int K) {
     const int r = dags->max_r < max_shard ? dags->max_r : max_shard;
     return dags->beta_uniform && (r < dags->D ? r : dags->D) <= 1 && dags->levels != FATE_LEVELS_TOPO &&
-           dags->D <= 16 && dags->M <= 32;
+           rows_kernel_fits(dags->D, K, dags->M);
 }
 
 // The dispatch order of per-instance launches: instances by size class of

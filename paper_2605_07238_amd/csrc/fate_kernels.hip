@@ -2013,6 +2013,465 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
     }
 }
 
+// ---- k_rows4: one horizon row per four lanes (17 to 64 devices) -----------
+// The rows kernel for wider clusters: a row's devices are split over the
+// four lanes of a quad, lane ql of the quad holding devices 16 ql .. 16 ql +
+// 15.  Each lane keeps the two smallest B of its sixteen, two exchanges
+// within the quad give the row's two smallest, and each lane adds its
+// devices' terms to its part of the task's sums (a task belongs to a quad).
+// Device masks are 64-bit.  The combine gives each stage a whole wave (lane
+// d = device d), which also ranks the stage's top-k.
+struct alignas(16) StageR4 {
+    uint64_t elig, hash;
+    uint64_t pfm;        // devices caching grp(v)
+    uint64_t h0;         // devices holding the first completed parent's output
+    float tokens, sigma;
+    uint32_t e0, n;      // first descendant entry; rows within the horizon
+    uint32_t c0, dbeg;   // first score; first completed parent
+    uint32_t q0, nq;     // first full-length task and their number; the tail task (or 0xffffffff)
+    float s0;            // the first completed parent's output size
+    uint16_t dn, npar;
+    uint8_t model, pad0, pad1, pad2;
+    uint32_t pad3;
+};
+static_assert(sizeof(StageR4) == 80, "StageR4");
+
+constexpr int kRows4Devs = 64;                       // devices a row can span
+constexpr int kRows4Stride = 2 * kRows4Devs + 4;     // floats per model row of the cost table
+
+struct Rows4Plan {
+    uint32_t pkey, pmask, rho, cap, wt, fits, wait, gpow, rtab, flf, fll, stages, tasks, part, misc, total;
+    uint32_t ntask;  // task slots: one per quad
+};
+
+// Task sums as float4 columns (16 of them: devices 4 j .. 4 j + 3), column j
+// of task t at part4[j * (ntask + 1) + t].
+__host__ __device__ inline Rows4Plan rows4_plan(int D, int K, int M, int blk) {
+    Rows4Plan q;
+    const uint32_t T = 1u << table_log2(D, K);
+    q.ntask = (uint32_t)(blk / 4);
+    uint32_t o = 0;
+    q.pkey = o; o += 8 * T;
+    q.pmask = o; o += 8 * T;
+    q.rho = o; o += 8 * kRows4Devs;
+    q.cap = o; o += 8 * kRows4Devs;
+    q.wt = o; o += 8 * (uint32_t)M;
+    q.fits = o; o += 8 * (uint32_t)M;
+    q.wait = o; o += 4 * kRows4Devs;
+    q.gpow = o; o += 4 * 16;
+    o = (o + 15u) & ~15u;
+    q.rtab = o; o += 4 * (uint32_t)(M * kRows4Stride);
+    o = (o + 7u) & ~7u;
+    q.flf = o; o += 8 * (uint32_t)(M * M);
+    q.fll = o; o += 8 * (uint32_t)(M * M);
+    o = (o + 15u) & ~15u;
+    q.stages = o; o += (uint32_t)sizeof(StageR4) * (uint32_t)kRowsChunk;
+    q.tasks = o; o += 4 * q.ntask;
+    o = (o + 15u) & ~15u;
+    q.part = o; o += 16 * (uint32_t)(kRows4Devs / 4) * (q.ntask + 1);
+    q.misc = o; o += 4 * 16;
+    q.total = (o + 15u) & ~15u;
+    return q;
+}
+
+// The two smallest of a quad's (m1, m2) pairs, on every lane of the quad.
+template <int CTRL>
+__device__ __forceinline__ float quad_move(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ void quad_two_smallest(float &m1, float &m2) {
+    float x1 = quad_move<0xB1>(m1), x2 = quad_move<0xB1>(m2);  // quad_perm [1, 0, 3, 2]
+    float lo = fminf(m1, x1);
+    m2 = fminf(fmaxf(m1, x1), fminf(m2, x2));
+    m1 = lo;
+    x1 = quad_move<0x4E>(m1);  // quad_perm [2, 3, 0, 1]
+    x2 = quad_move<0x4E>(m2);
+    lo = fminf(m1, x1);
+    m2 = fminf(fmaxf(m1, x1), fminf(m2, x2));
+    m1 = lo;
+}
+
+template <int BLK>
+__global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
+    constexpr int ND = 16, NJ = ND / 4;  // devices per lane, float4 columns per lane
+    constexpr int CS = kRows4Stride;
+    static_assert(BLK / 4 >= kRowsChunk && BLK % 64 == 0, "a task slot per stage of a chunk, one thread per stage");
+    const int b = (int)a.order[blockIdx.x];  // largest frontiers first: the last workgroups to start are short
+    const ParamSet ps = a.ps[blockIdx.y];
+    float *const scores = a.scores + (int64_t)a.set_of[blockIdx.y] * a.score_stride;
+    extern __shared__ uint64_t smem[];
+    uint8_t *sb = reinterpret_cast<uint8_t *>(smem);
+    const int tid = threadIdx.x;
+    const int D = a.D, K = a.K, M = a.M;
+    const Rows4Plan plan = rows4_plan(D, K, M, BLK);
+    Lds L;
+    L.logT = table_log2(D, K);
+    L.pkey = reinterpret_cast<uint64_t *>(sb + plan.pkey);
+    L.pmask = sb + plan.pmask;
+    uint64_t *pmask = reinterpret_cast<uint64_t *>(sb + plan.pmask);
+    uint64_t *rho = reinterpret_cast<uint64_t *>(sb + plan.rho);
+    uint64_t *capd = reinterpret_cast<uint64_t *>(sb + plan.cap);
+    uint64_t *wt = reinterpret_cast<uint64_t *>(sb + plan.wt);
+    uint64_t *fits = reinterpret_cast<uint64_t *>(sb + plan.fits);
+    float *wait = reinterpret_cast<float *>(sb + plan.wait);
+    float *gpow = reinterpret_cast<float *>(sb + plan.gpow);
+    float *rtab = reinterpret_cast<float *>(sb + plan.rtab);
+    uint64_t *flf = reinterpret_cast<uint64_t *>(sb + plan.flf);  // per (m(v), m(w)): devices where Load flips m(w)
+    uint64_t *fll = reinterpret_cast<uint64_t *>(sb + plan.fll);  // ... and where m(w) becomes resident
+    StageR4 *stg = reinterpret_cast<StageR4 *>(sb + plan.stages);
+    uint32_t *tasks = reinterpret_cast<uint32_t *>(sb + plan.tasks);
+    float4 *part4 = reinterpret_cast<float4 *>(sb + plan.part);
+    float *partf = reinterpret_cast<float *>(sb + plan.part);
+    uint32_t *misc = reinterpret_cast<uint32_t *>(sb + plan.misc);
+    const uint32_t pcol = plan.ntask + 1;  // float4 slots per column of task sums
+
+    // ---- prologue: the instance's frontier range and tables
+    const int64_t lo = a.fr_off[b];
+    const int nFi = (int)(a.fr_off[b + 1] - (uint32_t)lo);
+    if (nFi == 0) return;  // uniform
+    const int T = 1 << L.logT;
+    for (int i = tid; i < T; i += BLK) { L.pkey[i] = 0; pmask[i] = 0ull; }
+    for (int i = tid; i < M * M; i += BLK) { flf[i] = 0ull; fll[i] = 0ull; }
+    if (tid < D) {
+        rho[tid] = a.resident[(int64_t)b * D + tid];
+        wait[tid] = fmaxf(0.0f, a.tau[(int64_t)b * D + tid] - a.tnow[b]);
+        capd[tid] = a.cap[tid];
+    }
+    if (tid < M) { fits[tid] = a.fits[tid]; wt[tid] = a.weight[tid]; }
+    if (tid == 0) {
+        float g = 1.0f;
+        for (int h = 0; h < 16; ++h) { gpow[h] = g; g *= ps.gamma; }
+    }
+    for (int i = tid; i < M * kRows4Devs; i += BLK) {  // cost terms under the instance's residency
+        const int m = i / kRows4Devs, d = i - m * kRows4Devs;
+        float sw0 = 0.0f, ks = 0.0f;
+        if (d < D) {
+            const int j = m * D + d;
+            ks = ps.lam_s * a.ksw[j];
+            const float swo = bit(a.resident[(int64_t)b * D + d], m) ? 0.0f : ks;
+            sw0 = a.exec[j] + swo;
+        }
+        rtab[m * CS + 2 * d] = sw0;  // devices past D: never feasible
+        rtab[m * CS + 2 * d + 1] = ks;
+    }
+    constexpr int kPre = 4;  // prefix-cache entries fetched before the barrier
+    uint64_t pre[kPre];
+#pragma unroll
+    for (int r = 0; r < kPre; ++r) {
+        const int i = tid + r * BLK;
+        pre[r] = i < D * K ? a.pcache[(int64_t)b * D * K + i] : 0ull;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kPre; ++r)
+        if (pre[r] != 0) table_insert<uint64_t>(L, pre[r], (tid + r * BLK) / K);
+    for (int i = tid + kPre * BLK; i < D * K; i += BLK) {
+        const uint64_t h = a.pcache[(int64_t)b * D * K + i];
+        if (h != 0) table_insert<uint64_t>(L, h, i / K);
+    }
+    // Load's effect on m(w)'s residency, per (m(v), m(w))
+    for (int i = tid; i < M * D; i += BLK) {
+        const int m = i / D, d = i - m * D;
+        const uint64_t r0 = rho[d], r1 = load_model(r0, m, capd[d], wt);
+        const uint64_t ldm = r1 & ~r0;
+        for (uint64_t x = r0 ^ r1; x; x &= x - 1) {
+            const int mw = __builtin_ctzll(x);
+            atomicOr((unsigned long long *)&flf[m * M + mw], 1ull << d);
+            if ((ldm >> mw) & 1ull) atomicOr((unsigned long long *)&fll[m * M + mw], 1ull << d);
+        }
+    }
+    __syncthreads();
+
+    const float lam_tr = ps.lam_tr, lam_c = ps.lam_c, lam_p = ps.lam_p, b0 = a.beta0;
+    const uint64_t dmask = D >= 64 ? ~0ull : ((1ull << D) - 1ull);
+    constexpr int G = 64, kGroups = BLK / G;  // the combine: a wave per stage
+    const int lane = tid & 63;
+    const bool live = lane < D;
+    const int dl = live ? lane : D - 1;
+    const int ql = tid & 3, dq = ND * ql;  // this lane's devices within its quad's row
+    const uint32_t qmask = (uint32_t)((dmask >> dq) & 0xffffull);
+
+    for (int c0 = 0; c0 < nFi; c0 += kRowsChunk) {  // uniform: chunks of the instance's frontier
+        const int nC = min(kRowsChunk, nFi - c0);
+        const int64_t fc = lo + c0;  // frontier slot of the chunk's first stage
+        if (tid < nC) {  // stage records, descendant ranges, v's first completed parent
+            const uint32_t v = a.frontier[2 * (fc + tid)];
+            const StageRec r = a.rec[v];
+            StageR4 s;
+            s.elig = r.elig;
+            s.hash = r.hash;
+            s.tokens = r.tokens;
+            s.sigma = r.sigma;
+            s.e0 = a.desc_off[v];
+            uint32_t n = a.desc_off[v + 1] - s.e0;
+            if (ps.H < a.Hpack && n > 0) {  // entries are ordered by depth: those within H form a prefix
+                uint32_t l0 = 0, l1 = n;
+                while (l0 < l1) {
+                    const uint32_t mid = (l0 + l1) >> 1;
+                    if ((int)(a.desc[s.e0 + mid] >> kDescDepthShift) <= ps.H) l0 = mid + 1;
+                    else l1 = mid;
+                }
+                n = l0;
+            }
+            s.n = n;
+            s.c0 = a.cand_off[fc + tid];
+            s.dbeg = r.par_begin;
+            s.dn = (uint16_t)a.done_n[v];
+            s.npar = r.npar;
+            s.model = r.model;
+            s.pad0 = s.pad1 = s.pad2 = 0;
+            s.pad3 = 0;
+            s.h0 = 0;
+            s.s0 = 0.0f;
+            if (s.dn > 0) {
+                const DoneParent pu = a.done[s.dbeg];
+                s.h0 = pu.holders;
+                s.s0 = pu.sigma;
+            }
+            s.q0 = s.nq = 0;
+            s.pfm = table_find<uint64_t>(L, r.hash);
+            stg[tid] = s;
+        }
+        __syncthreads();
+        if (tid < 64) {
+            // tasks of L rows over the chunk's R rows in S stages, L the
+            // shortest length whose tasks (ceil(n / L) per stage of n rows) fit
+            // the task slots: every stage's full-length tasks first, then its
+            // shorter tail task; the tail tasks ordered by length, longest
+            // first (ties by stage), so that the quads of a wave run the same
+            // number of rows
+            const int i0 = 2 * tid, i1 = 2 * tid + 1;
+            const uint32_t n0 = i0 < nC ? stg[i0].n : 0u, n1 = i1 < nC ? stg[i1].n : 0u;
+            uint32_t R = 0, S = 0;
+            (void)wave_exscan_u32(n0 + n1, R);
+            (void)wave_exscan_u32((n0 ? 1u : 0u) + (n1 ? 1u : 0u), S);
+            uint32_t tlo = R > 0 ? max(1u, (R + plan.ntask - 1u) / plan.ntask) : 1u;
+            uint32_t thi = R > 0 ? max(1u, (R + plan.ntask - S - 1u) / (plan.ntask - S)) : 1u;
+            while (tlo < thi) {  // uniform
+                const uint32_t mid = (tlo + thi) >> 1;
+                uint32_t cnt = 0;
+                (void)wave_exscan_u32((n0 + mid - 1u) / mid + (n1 + mid - 1u) / mid, cnt);
+                if (cnt <= plan.ntask) thi = mid;
+                else tlo = mid + 1u;
+            }
+            const uint32_t Lr = tlo;
+            const uint32_t f0n = n0 / Lr, f1n = n1 / Lr, t0n = n0 - f0n * Lr, t1n = n1 - f1n * Lr;
+            uint32_t nfull = 0;
+            const uint32_t off = wave_exscan_u32(f0n + f1n, nfull);
+            uint32_t *bkt = reinterpret_cast<uint32_t *>(partf);  // scratch until the rows write their sums
+            constexpr uint32_t kBuckets = 32;
+            auto bucket = [&](uint32_t len) { return len >= kBuckets ? kBuckets - 1u : len; };
+            if (tid < (int)kBuckets) bkt[tid] = 0u;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (i0 < nC && t0n) atomicAdd(&bkt[bucket(t0n)], 1u);
+            if (i1 < nC && t1n) atomicAdd(&bkt[bucket(t1n)], 1u);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const uint32_t cb = tid < (int)kBuckets ? bkt[kBuckets - 1u - (uint32_t)tid] : 0u;  // longest first
+            uint32_t ntail = 0;
+            const uint32_t start = nfull + wave_exscan_u32(cb, ntail);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (tid < (int)kBuckets) bkt[kBuckets - 1u - (uint32_t)tid] = start;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const uint32_t k0 = (i0 < nC && t0n) ? atomicAdd(&bkt[bucket(t0n)], 1u) : 0u;
+            const uint32_t k1 = (i1 < nC && t1n) ? atomicAdd(&bkt[bucket(t1n)], 1u) : 0u;
+            if (i0 < nC) {
+                stg[i0].q0 = off | (f0n << 16);
+                stg[i0].nq = t0n ? k0 : 0xffffffffu;
+                if (t0n) tasks[k0] = (uint32_t)i0 | (f0n << 16);
+            }
+            if (i1 < nC) {
+                stg[i1].q0 = (off + f0n) | (f1n << 16);
+                stg[i1].nq = t1n ? k1 : 0xffffffffu;
+                if (t1n) tasks[k1] = (uint32_t)i1 | (f1n << 16);
+            }
+            for (uint32_t p = 0; p < f0n; ++p) tasks[off + p] = (uint32_t)i0 | (p << 16);
+            for (uint32_t p = 0; p < f1n; ++p) tasks[off + f0n + p] = (uint32_t)i1 | (p << 16);
+            if (tid == 0) {
+                misc[2] = nfull + ntail;
+                misc[3] = Lr;
+            }
+        }
+        __syncthreads();
+        const int ntask = (int)misc[2];
+        const uint32_t Lr = misc[3];
+
+        // ---- rows: task t on quad t, lane ql taking devices dq .. dq + 15
+        for (int t = tid >> 2; t < ntask; t += BLK / 4) {  // uniform within the quad
+            const uint32_t tk = tasks[t];
+            const int si = (int)(tk & 0xffffu);
+            const uint32_t pt = tk >> 16;
+            const StageR4 &s = stg[si];
+            const uint32_t se0 = s.e0, sn = s.n;
+            const uint32_t r0 = pt * Lr, r1 = min(sn, r0 + Lr);
+            const uint64_t hv = s.hash;
+            const float t0 = lam_tr * s.sigma * b0;  // v's output to one more device
+            const uint32_t mrow = (uint32_t)s.model * (uint32_t)M;
+            float f[ND];
+#pragma unroll
+            for (int d = 0; d < ND; ++d) f[d] = 0.0f;
+            auto row = [&](uint32_t ent, const StageRec &rw, uint32_t db, uint32_t dn) {
+                const int depth = (int)(ent >> kDescDepthShift);
+                const uint32_t mw = rw.model;
+                const uint32_t feas = (uint32_t)(((rw.elig & fits[mw]) >> dq) & 0xffffull) & qmask;
+                const uint64_t pfo64 = table_find<uint64_t>(L, rw.hash);
+                const uint32_t pfo = (uint32_t)((pfo64 >> dq) & 0xffffull);
+                const bool same = rw.hash != 0 && rw.hash == hv;
+                const float gh = gpow[depth];
+                const float pfp = lam_p * ps.kpf * rw.tokens;
+                const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
+                const uint32_t flip = (uint32_t)((flf[mrow + mw] >> dq) & 0xffffull);
+                const uint32_t ld = (uint32_t)((fll[mrow + mw] >> dq) & 0xffffull);
+                const float *crow = rtab + mw * CS + 2 * dq;
+                // B without the completed parents: cost with the switch term, less the prefix benefit
+                float B[ND];
+#pragma unroll
+                for (int j = 0; j < ND / 2; ++j) {
+                    const float4 c = *reinterpret_cast<const float4 *>(crow + 4 * j);
+                    B[2 * j] = c.x - __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)pfo, 2 * j, 1u));
+                    B[2 * j + 1] = c.z - __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)pfo, 2 * j + 1, 1u));
+                }
+                // completed parents: every one's transfer (all remote), and on the
+                // devices holding one its transfer saved and the colocation share
+                float xb = 0.0f;
+                if (dn > 0) {  // the lane's devices go through its task sum slots, indexed by device
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j)
+                        part4[(dq / 4 + j) * pcol + t] = make_float4(B[4 * j], B[4 * j + 1], B[4 * j + 2], B[4 * j + 3]);
+                    for (uint32_t q0 = 0; q0 < dn; q0 += 4) {  // the batch's loads are issued together
+                        DoneParent pb[4];
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            if (q0 + j < dn) pb[j] = a.done[db + q0 + j];
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            if (q0 + j >= dn) break;
+                            const float tq = lam_tr * b0 * pb[j].sigma;
+                            xb += tq;
+                            const float pw = tq + cw;
+                            for (uint32_t h = (uint32_t)((pb[j].holders >> dq) & 0xffffull) & qmask; h; h &= h - 1u) {
+                                const int d = dq + __builtin_ctz(h);
+                                partf[((d >> 2) * pcol + t) * 4 + (d & 3)] -= pw;
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+                        const float4 c = part4[(dq / 4 + j) * pcol + t];
+                        B[4 * j] = c.x; B[4 * j + 1] = c.y; B[4 * j + 2] = c.z; B[4 * j + 3] = c.w;
+                    }
+                }
+                // feasibility, and the two smallest values of the row
+                float m1 = inf_f(), m2 = inf_f();
+#pragma unroll
+                for (int d = 0; d < ND; ++d) {
+                    const uint32_t fm = (uint32_t)__builtin_amdgcn_sbfe((int)feas, d, 1u);
+                    const float x = __uint_as_float((fm & __float_as_uint(B[d] + xb)) | (~fm & __float_as_uint(inf_f())));
+                    B[d] = x;
+                    m2 = __builtin_amdgcn_fmed3f(m1, x, m2);
+                    m1 = fminf(m1, x);
+                }
+                quad_two_smallest(m1, m2);
+                const bool child = depth == 1;
+                const float m1c = child ? m1 + t0 : m1, m2c = child ? m2 + t0 : m2;
+                const float cwc = child ? cw : 0.0f;
+                // devices that gain grp(w) once v runs there
+                const uint32_t gain = same ? (~pfo & qmask) : 0u;
+#pragma unroll
+                for (int j = 0; j < ND / 2; ++j) {
+                    const float4 c = *reinterpret_cast<const float4 *>(crow + 4 * j);
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const int d = 2 * j + u;
+                        const float ksr = u == 0 ? c.y : c.w;
+                        // m(w)'s switch term on d flips when v's Load changes its
+                        // residency there: down by the magnitude when loaded, up when evicted
+                        const float dsw = __uint_as_float((__builtin_amdgcn_ubfe(ld, d, 1u) << 31) |
+                                                          (__float_as_uint(ksr) & (uint32_t)__builtin_amdgcn_sbfe((int)flip, d, 1u)));
+                        const float gp = __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)gain, d, 1u));
+                        const float C = ((B[d] - cwc) + dsw) - gp;
+                        const float o = B[d] == m1 ? m2c : m1c;
+                        f[d] += gh * fminf(o, C);
+                    }
+                }
+            };
+            for (uint32_t r = r0; r < r1; r += 2) {  // two rows' loads in flight together
+                const bool two = r + 1 < r1;
+                const uint32_t e0 = a.desc[se0 + r];
+                const uint32_t e1 = two ? a.desc[se0 + r + 1] : e0;
+                const StageRec w0 = a.rec[e0 & kDescIdMask];
+                const StageRec w1 = a.rec[e1 & kDescIdMask];
+                const uint32_t dn0 = a.done_n[e0 & kDescIdMask];
+                const uint32_t dn1 = a.done_n[e1 & kDescIdMask];
+                row(e0, w0, w0.par_begin, dn0);
+                if (two) row(e1, w1, w1.par_begin, dn1);
+            }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                part4[(dq / 4 + j) * pcol + t] = make_float4(f[4 * j], f[4 * j + 1], f[4 * j + 2], f[4 * j + 3]);
+        }
+        __syncthreads();
+
+        // ---- combine: immediate cost plus the stage's task sums; scores and top-k
+        for (int i = tid / G; i < nC; i += kGroups) {  // uniform within the wave
+            const StageR4 s = stg[i];
+            // completed parents of v, each to the whole wave in order; the first was staged
+            float tr = 0.0f, cnt = 0.0f;
+            if (s.dn > 0) {
+                const bool local = ((s.h0 >> dl) & 1ull) != 0;
+                cnt += local ? 1.0f : 0.0f;
+                tr += local ? 0.0f : s.s0 * b0;
+            }
+            for (int q0 = 1; q0 < (int)s.dn; q0 += G) {
+                uint64_t h = 0ull;
+                float sg = 0.0f;
+                if (q0 + lane < (int)s.dn) {
+                    const DoneParent pu = a.done[s.dbeg + q0 + lane];
+                    h = pu.holders;
+                    sg = pu.sigma;
+                }
+                const int nq = min(G, (int)s.dn - q0);
+                for (int j = 0; j < nq; ++j) {
+                    const uint64_t hj = ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(h >> 32), j, G) << 32) |
+                                        (uint64_t)(uint32_t)__shfl((int)(uint32_t)h, j, G);
+                    const float sj = __shfl(sg, j, G);
+                    const bool local = ((hj >> dl) & 1ull) != 0;
+                    cnt += local ? 1.0f : 0.0f;
+                    tr += local ? 0.0f : sj * b0;
+                }
+            }
+            const float ks = rtab[s.model * CS + 2 * dl + 1];
+            const float swo = bit(rho[dl], s.model) ? 0.0f : ks;
+            const float ex = a.exec[s.model * D + dl];
+            const float pf_v = ((s.pfm >> dl) & 1ull) ? ps.kpf * s.tokens : 0.0f;
+            const float colo = s.npar ? cnt * fast_rcp((float)s.npar) : 0.0f;
+            const float a_imm = ps.lam_q * wait[dl] + swo - lam_c * colo;
+            const float b_imm = ex + lam_tr * tr - lam_p * pf_v;
+            double acc = 0.0;  // full-length tasks in row order, then the tail
+            const uint32_t qf = s.q0 & 0xffffu, nf = s.q0 >> 16;
+            for (uint32_t t = 0; t < nf; ++t) acc += (double)partf[((lane >> 2) * pcol + qf + t) * 4 + (lane & 3)];
+            if (s.nq != 0xffffffffu) acc += (double)partf[((lane >> 2) * pcol + s.nq) * 4 + (lane & 3)];
+            const bool feas_v = live && bit(s.elig, lane) && bit(fits[s.model], lane);
+            const float psi = feas_v ? (float)(-((double)(a_imm + b_imm) + acc)) : -inf_f();
+            if (live) scores[s.c0 + lane] = psi;
+            if (a.topk > 0) {
+                const int64_t f = fc + i;
+                uint32_t sbits[1] = {live ? topk_bits(psi) : 0u};
+                const uint32_t ci[1] = {(uint32_t)lane};
+                group_topk_at<G, 1>(sbits, ci, lane, a.topk, a.tk_idx + f * a.topk, a.tk_val + f * a.topk);
+            }
+        }
+        __syncthreads();  // the next chunk reuses the stage slots and task sums
+    }
+}
+
 // Most workgroups of one top-k launch (sixteen per compute unit); larger
 // frontiers loop over their tiles.
 constexpr int64_t kTopkMaxBlocks = 4096;
@@ -2064,19 +2523,33 @@ bool score_fits(int D, int K, int M, int beta_uniform) {
     return score_shape(D, K, M, slice_len(D), beta_uniform != 0, sh);
 }
 
-// Threads of a k_rows workgroup.
+// Threads of a k_rows workgroup, and of a k_rows4 one (256 quads).
 constexpr int kRowsBlock = 256;
+constexpr int kRows4Block = 1024;
 
-// k_rows takes frontiers with single-device candidates only, uniform beta,
-// D <= 16, at most 32 models and parameter sets without a scoring variant,
-// when its LDS fits.
+// The row kernels take frontiers with single-device candidates only, uniform
+// beta, hop levels and parameter sets without a scoring variant: k_rows up
+// to 16 devices and 32 models, k_rows4 up to 64 devices and 64 models, when
+// their LDS fits.
+bool rows_kernel_fits(int D, int K, int M) {
+    if (D <= 16) {
+        const int nd = D <= 4 ? 4 : D <= 8 ? 8 : 16;
+        return M <= 32 && rows_plan(D, K, M, nd, kRowsBlock).total <= kLdsLimit;
+    }
+    return D <= kRows4Devs && M <= 64 && rows4_plan(D, K, M, kRows4Block).total <= kLdsLimit;
+}
+
 static bool rows_fit(const ScoreLaunch &a) {
-    if (!a.beta_uniform || !a.singles || a.topo || a.D > 16 || a.M > 32) return false;
-    const int nd = a.D <= 4 ? 4 : a.D <= 8 ? 8 : 16;
-    return rows_plan(a.D, a.K, a.M, nd, kRowsBlock).total <= kLdsLimit;
+    if (!a.beta_uniform || !a.singles || a.topo) return false;
+    return rows_kernel_fits(a.D, a.K, a.M);
 }
 
 static void launch_rows(const ScoreLaunch &a, hipStream_t s) {
+    if (a.D > 16) {
+        const size_t lds = rows4_plan(a.D, a.K, a.M, kRows4Block).total;
+        hipLaunchKernelGGL((k_rows4<kRows4Block>), dim3((unsigned)a.B, (unsigned)a.nsets), dim3(kRows4Block), lds, s, a);
+        return;
+    }
     const int nd = a.D <= 4 ? 4 : a.D <= 8 ? 8 : 16;
     const size_t lds = rows_plan(a.D, a.K, a.M, nd, kRowsBlock).total;
     const dim3 grid((unsigned)a.B, (unsigned)a.nsets), block((unsigned)kRowsBlock);
