@@ -1659,11 +1659,12 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
     }
     for (int i = tid; i < M * ND; i += BLK) {  // cost terms under the instance's residency
         const int m = i / ND, d = i - m * ND;
-        float sw0 = 0.0f, ks = 0.0f;
+        float sw0 = 0.0f, sks = 0.0f;
         if (d < D) {
             const int j = m * D + d;
-            ks = ps.lam_s * a.ksw[j];
-            const float swo = bit(a.resident[(int64_t)b * D + d], m) ? 0.0f : ks;
+            const float ks = ps.lam_s * a.ksw[j];
+            const bool res = bit(a.resident[(int64_t)b * D + d], m);
+            const float swo = res ? 0.0f : ks;
             sw0 = a.exec[j] + swo;
             CostS c;
             c.sw0 = sw0;
@@ -1671,9 +1672,15 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             c.exec = a.exec[j];
             c.swo = swo;
             cst[j] = c;
+            // a row's cost is +infinity where the model does not fit (its
+            // feasibility then only needs A(w)); the magnitude carries the
+            // sign of the change a flip of the residency makes: up where m is
+            // resident now (evicted), down where it is not (loaded)
+            if (!bit(a.fits[m], d)) sw0 = inf_f();
+            sks = res ? ks : -ks;
         }
         rtab[m * CS + 2 * d] = sw0;  // devices past D: never feasible
-        rtab[m * CS + 2 * d + 1] = ks;
+        rtab[m * CS + 2 * d + 1] = sks;
     }
     constexpr int kPre = 4;  // prefix-cache entries fetched before the barrier
     uint64_t pre[kPre];
@@ -1847,20 +1854,21 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             const uint64_t hv = s.hash;
             const float t0 = lam_tr * s.sigma * b0;  // v's output to one more device
             const uint32_t *flr = fl + (uint32_t)s.model * (uint32_t)M;
-            float f[ND];
+            // f[d]: the task's sums of gamma^depth * min(outside, C(d)) less
+            // the row terms common to every device, which go to fx
+            float f[ND], fx = 0.0f;
 #pragma unroll
             for (int d = 0; d < ND; ++d) f[d] = 0.0f;
             auto row = [&](uint32_t ent, const StageRec &rw, uint32_t db, uint32_t dn) {
                 const int depth = (int)(ent >> kDescDepthShift);
                 const uint32_t mw = rw.model;
-                const uint32_t feas = (uint32_t)(rw.elig & fits[mw]) & dmask;
+                const uint32_t feas = (uint32_t)rw.elig & dmask;  // the row table is +infinity where m(w) does not fit
                 const uint32_t pfo = table_find<uint32_t>(L, rw.hash);
                 const bool same = rw.hash != 0 && rw.hash == hv;
                 const float gh = gpow[depth];
                 const float pfp = lam_p * ps.kpf * rw.tokens;
                 const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
-                const uint32_t flw = flr[mw];
-                const uint32_t ld = flw & 0xffffu, flip = flw >> 16;
+                const uint32_t flip = flr[mw] >> 16;
                 const float *crow = rtab + mw * CS;
                 // B without the completed parents: cost with the switch term, less the prefix benefit
                 float B[ND];
@@ -1899,19 +1907,25 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                         B[4 * j] = c.x; B[4 * j + 1] = c.y; B[4 * j + 2] = c.z; B[4 * j + 3] = c.w;
                     }
                 }
-                // feasibility, and the two smallest values of the row
+                // feasibility, and the two smallest values of the row.  The
+                // parents' transfer xb is common to every device of the row
+                // (B, the outside minimum and C all carry it), and so is a
+                // child's colocation share once it is moved to the outside
+                // side: min(o, B - cw + ...) = min(o + cw, B + ...) - cw.
+                // Both go to fx, once per row.
                 float m1 = inf_f(), m2 = inf_f();
 #pragma unroll
                 for (int d = 0; d < ND; ++d) {
                     const uint32_t fm = (uint32_t)__builtin_amdgcn_sbfe((int)feas, d, 1u);
-                    const float x = __uint_as_float((fm & __float_as_uint(B[d] + xb)) | (~fm & __float_as_uint(inf_f())));
+                    const float x = __uint_as_float((fm & __float_as_uint(B[d])) | (~fm & __float_as_uint(inf_f())));
                     B[d] = x;
                     m2 = __builtin_amdgcn_fmed3f(m1, x, m2);
                     m1 = fminf(m1, x);
                 }
                 const bool child = depth == 1;
-                const float m1c = child ? m1 + t0 : m1, m2c = child ? m2 + t0 : m2;
                 const float cwc = child ? cw : 0.0f;
+                const float m1c = child ? (m1 + t0) + cw : m1, m2c = child ? (m2 + t0) + cw : m2;
+                fx += gh * (xb - cwc);
                 // devices that gain grp(w) once v runs there
                 const uint32_t gain = same ? (~pfo & dmask) : 0u;
 #pragma unroll
@@ -1920,13 +1934,11 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
 #pragma unroll
                     for (int u = 0; u < 2; ++u) {
                         const int d = 2 * j + u;
-                        const float ksr = u == 0 ? c.y : c.w;
-                        // m(w)'s switch term on d flips when v's Load changes its
-                        // residency there: down by the magnitude when loaded, up when evicted
-                        const float dsw = __uint_as_float((__builtin_amdgcn_ubfe(ld, d, 1u) << 31) |
-                                                          (__float_as_uint(ksr) & (uint32_t)__builtin_amdgcn_sbfe((int)flip, d, 1u)));
+                        // m(w)'s switch term on d changes by the signed magnitude
+                        // where v's Load flips m(w)'s residency there
+                        const float dsw = __uint_as_float(__float_as_uint(u == 0 ? c.y : c.w) & (uint32_t)__builtin_amdgcn_sbfe((int)flip, d, 1u));
                         const float gp = __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)gain, d, 1u));
-                        const float C = ((B[d] - cwc) + dsw) - gp;
+                        const float C = (B[d] + dsw) - gp;
                         const float o = B[d] == m1 ? m2c : m1c;
                         f[d] += gh * fminf(o, C);
                     }
@@ -1944,7 +1956,8 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                 if (two) row(e1, w1, w1.par_begin, dn1);
             }
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) part4[j * pcol + t] = make_float4(f[4 * j], f[4 * j + 1], f[4 * j + 2], f[4 * j + 3]);
+            for (int j = 0; j < NJ; ++j)
+                part4[j * pcol + t] = make_float4(f[4 * j] + fx, f[4 * j + 1] + fx, f[4 * j + 2] + fx, f[4 * j + 3] + fx);
         }
         __syncthreads();
 
