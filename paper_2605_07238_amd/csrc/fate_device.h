@@ -57,16 +57,20 @@ __device__ __forceinline__ void candidate_window(int j, int D, int &i, int &k) {
     i = j;
 }
 
-// Sum and exclusive prefix sum over the 64 lanes of a wave (all active).
+// Sum and exclusive prefix sum over the 64 lanes of a wave (all active), in
+// DPP moves only: shifts right by 1, 2, 4 and 8 within each row of 16 lanes
+// (lanes shifted in from outside the row read 0), then the last lane of row
+// 0 and of row 2 added to rows 1 and 3 (row_bcast:15), then the last lane
+// of row 1 to rows 2 and 3 (row_bcast:31); the total is lane 63's.
 __device__ __forceinline__ uint32_t wave_exscan_u32(uint32_t x, uint32_t &total) {
-    const int lane = threadIdx.x & 63;
     uint32_t v = x;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(v, off, 64);
-        if (lane >= off) v += y;
-    }
-    total = __shfl(v, 63, 64);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+    total = (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
     return v - x;
 }
 
