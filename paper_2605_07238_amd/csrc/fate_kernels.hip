@@ -1971,21 +1971,17 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                 cnt += local ? 1.0f : 0.0f;
                 tr += local ? 0.0f : s.s0 * b0;
             }
-            for (int q0 = 1; q0 < (int)s.dn; q0 += G) {
-                uint32_t h = 0u;
-                float sg = 0.0f;
-                if (q0 + lane < (int)s.dn) {
-                    const DoneParent pu = a.done[s.dbeg + q0 + lane];
-                    h = (uint32_t)pu.holders;
-                    sg = pu.sigma;
-                }
-                const int nq = min(G, (int)s.dn - q0);
-                for (int j = 0; j < nq; ++j) {
-                    const uint32_t hj = (uint32_t)__shfl((int)h, j, G);
-                    const float sj = __shfl(sg, j, G);
-                    const bool local = ((hj >> dl) & 1u) != 0;
+            for (int q0 = 1; q0 < (int)s.dn; q0 += 4) {  // every lane loads the batch (one address per group), in order
+                DoneParent pb[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (q0 + j < (int)s.dn) pb[j] = a.done[s.dbeg + q0 + j];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (q0 + j >= (int)s.dn) break;
+                    const bool local = (((uint32_t)pb[j].holders >> dl) & 1u) != 0;
                     cnt += local ? 1.0f : 0.0f;
-                    tr += local ? 0.0f : sj * b0;
+                    tr += local ? 0.0f : pb[j].sigma * b0;
                 }
             }
             const CostS c = cst[s.model * D + dl];
