@@ -1989,10 +1989,22 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             const float colo = s.npar ? cnt * fast_rcp((float)s.npar) : 0.0f;
             const float a_imm = ps.lam_q * wait[dl] + c.swo - lam_c * colo;
             const float b_imm = c.exec + lam_tr * tr - lam_p * pf_v;
-            double acc = 0.0;  // full-length tasks in row order, then the tail
+            // full-length tasks in row order, then the tail; task t's sum for
+            // this lane's device at pc[4 t], four loads in flight per batch
             const uint32_t qf = s.q0 & 0xffffu, nf = s.q0 >> 16;
-            for (uint32_t t = 0; t < nf; ++t) acc += (double)partf[((lane >> 2) * pcol + qf + t) * 4 + (lane & 3)];
-            if (s.nq != 0xffffffffu) acc += (double)partf[((lane >> 2) * pcol + s.nq) * 4 + (lane & 3)];
+            const float *pc = partf + ((lane >> 2) * pcol + qf) * 4 + (lane & 3);
+            const float xt = s.nq != 0xffffffffu ? partf[((lane >> 2) * pcol + s.nq) * 4 + (lane & 3)] : 0.0f;
+            double acc = 0.0;
+            uint32_t t = 0;
+            for (; t + 4 <= nf; t += 4) {
+                const float x0 = pc[4 * t], x1 = pc[4 * t + 4], x2 = pc[4 * t + 8], x3 = pc[4 * t + 12];
+                acc += (double)x0;
+                acc += (double)x1;
+                acc += (double)x2;
+                acc += (double)x3;
+            }
+            for (; t < nf; ++t) acc += (double)pc[4 * t];
+            if (s.nq != 0xffffffffu) acc += (double)xt;
             const bool feas_v = live && bit(s.elig, lane) && bit(fits[s.model], lane);
             const float psi = feas_v ? (float)(-((double)(a_imm + b_imm) + acc)) : -inf_f();
             if (live) scores[s.c0 + lane] = psi;
@@ -2463,10 +2475,22 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
             const float colo = s.npar ? cnt * fast_rcp((float)s.npar) : 0.0f;
             const float a_imm = ps.lam_q * wait[dl] + swo - lam_c * colo;
             const float b_imm = ex + lam_tr * tr - lam_p * pf_v;
-            double acc = 0.0;  // full-length tasks in row order, then the tail
+            // full-length tasks in row order, then the tail; task t's sum for
+            // this lane's device at pc[4 t], four loads in flight per batch
             const uint32_t qf = s.q0 & 0xffffu, nf = s.q0 >> 16;
-            for (uint32_t t = 0; t < nf; ++t) acc += (double)partf[((lane >> 2) * pcol + qf + t) * 4 + (lane & 3)];
-            if (s.nq != 0xffffffffu) acc += (double)partf[((lane >> 2) * pcol + s.nq) * 4 + (lane & 3)];
+            const float *pc = partf + ((lane >> 2) * pcol + qf) * 4 + (lane & 3);
+            const float xt = s.nq != 0xffffffffu ? partf[((lane >> 2) * pcol + s.nq) * 4 + (lane & 3)] : 0.0f;
+            double acc = 0.0;
+            uint32_t t = 0;
+            for (; t + 4 <= nf; t += 4) {
+                const float x0 = pc[4 * t], x1 = pc[4 * t + 4], x2 = pc[4 * t + 8], x3 = pc[4 * t + 12];
+                acc += (double)x0;
+                acc += (double)x1;
+                acc += (double)x2;
+                acc += (double)x3;
+            }
+            for (; t < nf; ++t) acc += (double)pc[4 * t];
+            if (s.nq != 0xffffffffu) acc += (double)xt;
             const bool feas_v = live && bit(s.elig, lane) && bit(fits[s.model], lane);
             const float psi = feas_v ? (float)(-((double)(a_imm + b_imm) + acc)) : -inf_f();
             if (live) scores[s.c0 + lane] = psi;
