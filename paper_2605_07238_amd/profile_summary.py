@@ -91,6 +91,25 @@ def main():
         busy = kavg["SQ_INSTS_VALU"] * 4.0 / (args.cus * 4 * cycles)
         out.append("gpu_cycles_per_dispatch: %.0f" % cycles)
         out.append("valu_issue_busy_frac: %.3f  (SQ_INSTS_VALU x 4 / (%d CUs x 4 SIMDs x cycles))" % (busy, args.cus))
+    if "GRBM_GUI_ACTIVE" in kavg:
+        # memory-pipeline readings (present when those counters were taken)
+        cycles = kavg["GRBM_GUI_ACTIVE"] / args.xcds
+        if "TCC_HIT_sum" in kavg and "TCC_MISS_sum" in kavg:
+            h, m = kavg["TCC_HIT_sum"], kavg["TCC_MISS_sum"]
+            out.append("l2_hit_frac: %.3f  (TCC_HIT / (TCC_HIT + TCC_MISS))" % (h / max(1.0, h + m)))
+        if "TCP_TCC_READ_REQ_LATENCY_sum" in kavg and "TCP_TCC_READ_REQ_sum" in kavg:
+            lat, req = kavg["TCP_TCC_READ_REQ_LATENCY_sum"], kavg["TCP_TCC_READ_REQ_sum"]
+            out.append("l1_to_l2_read_latency_cycles: %.0f  (TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ)"
+                       % (lat / max(1.0, req)))
+            out.append("l2_reads_in_flight_per_cu: %.1f  (TCP_TCC_READ_REQ_LATENCY / (CUs x cycles))"
+                       % (lat / (args.cus * cycles)))
+        if "TCP_PENDING_STALL_CYCLES_sum" in kavg:
+            out.append("l1_pending_stall_frac: %.3f  (TCP_PENDING_STALL_CYCLES / (CUs x cycles))"
+                       % (kavg["TCP_PENDING_STALL_CYCLES_sum"] / (args.cus * cycles)))
+        if "TA_BUSY_avr" in kavg:
+            out.append("ta_busy_frac: %.3f  (TA_BUSY_avr / cycles)" % (kavg["TA_BUSY_avr"] / cycles))
+        if "SQ_WAIT_ANY" in kavg and "SQ_WAVE_CYCLES" in kavg:
+            out.append("wave_wait_frac: %.3f  (SQ_WAIT_ANY / SQ_WAVE_CYCLES)" % (kavg["SQ_WAIT_ANY"] / kavg["SQ_WAVE_CYCLES"]))
     if args.kernel_source:
         h = hashlib.sha256()
         for path in args.kernel_source:
