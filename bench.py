@@ -388,9 +388,12 @@ def planning_loop(w, pk, params, k, steps, log, full_plan=True, max_waves=2000):
         placed = int(np.count_nonzero(sel_h >= 0))
         row = dict(frontier=nF0, placed=placed, next_frontier=nF1, score_topk_ms=e[0].elapsed_time(e[1]),
                    plan_ms=e[1].elapsed_time(e[2]), commit_ms=e[2].elapsed_time(e[3]), commit_bytes=cb)
+        if i == 0:
+            row["warmup"] = True  # first launch of the plan and commit kernels (code loading); not in the means
         rows.append(row)
-        log("planning step %d: frontier %d, placed %d -> %d; score + top-k %.4f, plan %.4f, commit %.4f ms"
-            % (i, nF0, placed, nF1, row["score_topk_ms"], row["plan_ms"], row["commit_ms"]))
+        log("planning step %d: frontier %d, placed %d -> %d; score + top-k %.4f, plan %.4f, commit %.4f ms%s"
+            % (i, nF0, placed, nF1, row["score_topk_ms"], row["plan_ms"], row["commit_ms"],
+               " (first launches: warm-up, not in the means)" if i == 0 else ""))
     out = dict(steps=rows, planner="fate_plan_wave (greedy wave, top-%d choices)" % k)
     timed = rows[1:] or rows  # the first launch of each kernel warms up
     if timed:
