@@ -2061,7 +2061,7 @@ constexpr int kRows4Devs = 64;                       // devices a row can span
 constexpr int kRows4Stride = 2 * kRows4Devs + 4;     // floats per model row of the cost table
 
 struct Rows4Plan {
-    uint32_t pkey, pmask, rho, cap, wt, fits, wait, gpow, rtab, flf, fll, stages, tasks, part, misc, total;
+    uint32_t pkey, pmask, rho, cap, wt, fits, wait, gpow, rtab, flf, stages, tasks, part, misc, total;
     uint32_t ntask;  // task slots: one per quad
 };
 
@@ -2084,7 +2084,6 @@ __host__ __device__ inline Rows4Plan rows4_plan(int D, int K, int M, int blk) {
     q.rtab = o; o += 4 * (uint32_t)(M * kRows4Stride);
     o = (o + 7u) & ~7u;
     q.flf = o; o += 8 * (uint32_t)(M * M);
-    q.fll = o; o += 8 * (uint32_t)(M * M);
     o = (o + 15u) & ~15u;
     q.stages = o; o += (uint32_t)sizeof(StageR4) * (uint32_t)kRowsChunk;
     q.tasks = o; o += 4 * q.ntask;
@@ -2138,7 +2137,6 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
     float *gpow = reinterpret_cast<float *>(sb + plan.gpow);
     float *rtab = reinterpret_cast<float *>(sb + plan.rtab);
     uint64_t *flf = reinterpret_cast<uint64_t *>(sb + plan.flf);  // per (m(v), m(w)): devices where Load flips m(w)
-    uint64_t *fll = reinterpret_cast<uint64_t *>(sb + plan.fll);  // ... and where m(w) becomes resident
     StageR4 *stg = reinterpret_cast<StageR4 *>(sb + plan.stages);
     uint32_t *tasks = reinterpret_cast<uint32_t *>(sb + plan.tasks);
     float4 *part4 = reinterpret_cast<float4 *>(sb + plan.part);
@@ -2152,7 +2150,7 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
     if (nFi == 0) return;  // uniform
     const int T = 1 << L.logT;
     for (int i = tid; i < T; i += BLK) { L.pkey[i] = 0; pmask[i] = 0ull; }
-    for (int i = tid; i < M * M; i += BLK) { flf[i] = 0ull; fll[i] = 0ull; }
+    for (int i = tid; i < M * M; i += BLK) flf[i] = 0ull;
     if (tid < D) {
         rho[tid] = a.resident[(int64_t)b * D + tid];
         wait[tid] = fmaxf(0.0f, a.tau[(int64_t)b * D + tid] - a.tnow[b]);
@@ -2165,15 +2163,19 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
     }
     for (int i = tid; i < M * kRows4Devs; i += BLK) {  // cost terms under the instance's residency
         const int m = i / kRows4Devs, d = i - m * kRows4Devs;
-        float sw0 = 0.0f, ks = 0.0f;
+        float sw0 = 0.0f, sks = 0.0f;
         if (d < D) {
             const int j = m * D + d;
-            ks = ps.lam_s * a.ksw[j];
-            const float swo = bit(a.resident[(int64_t)b * D + d], m) ? 0.0f : ks;
-            sw0 = a.exec[j] + swo;
+            const float ks = ps.lam_s * a.ksw[j];
+            const bool res = bit(a.resident[(int64_t)b * D + d], m);
+            sw0 = a.exec[j] + (res ? 0.0f : ks);
+            // +infinity where the model does not fit; the magnitude signed by
+            // the change a flip of the residency makes (up where resident now)
+            if (!bit(a.fits[m], d)) sw0 = inf_f();
+            sks = res ? ks : -ks;
         }
         rtab[m * CS + 2 * d] = sw0;  // devices past D: never feasible
-        rtab[m * CS + 2 * d + 1] = ks;
+        rtab[m * CS + 2 * d + 1] = sks;
     }
     constexpr int kPre = 4;  // prefix-cache entries fetched before the barrier
     uint64_t pre[kPre];
@@ -2194,11 +2196,9 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
     for (int i = tid; i < M * D; i += BLK) {
         const int m = i / D, d = i - m * D;
         const uint64_t r0 = rho[d], r1 = load_model(r0, m, capd[d], wt);
-        const uint64_t ldm = r1 & ~r0;
         for (uint64_t x = r0 ^ r1; x; x &= x - 1) {
             const int mw = __builtin_ctzll(x);
             atomicOr((unsigned long long *)&flf[m * M + mw], 1ull << d);
-            if ((ldm >> mw) & 1ull) atomicOr((unsigned long long *)&fll[m * M + mw], 1ull << d);
         }
     }
     __syncthreads();
@@ -2335,13 +2335,14 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
             const uint64_t hv = s.hash;
             const float t0 = lam_tr * s.sigma * b0;  // v's output to one more device
             const uint32_t mrow = (uint32_t)s.model * (uint32_t)M;
-            float f[ND];
+            // f[d]: the task's sums less the row terms common to every device (fx)
+            float f[ND], fx = 0.0f;
 #pragma unroll
             for (int d = 0; d < ND; ++d) f[d] = 0.0f;
             auto row = [&](uint32_t ent, const StageRec &rw, uint32_t db, uint32_t dn) {
                 const int depth = (int)(ent >> kDescDepthShift);
                 const uint32_t mw = rw.model;
-                const uint32_t feas = (uint32_t)(((rw.elig & fits[mw]) >> dq) & 0xffffull) & qmask;
+                const uint32_t feas = (uint32_t)((rw.elig >> dq) & 0xffffull) & qmask;  // +infinity in the row table where m(w) does not fit
                 const uint64_t pfo64 = table_find<uint64_t>(L, rw.hash);
                 const uint32_t pfo = (uint32_t)((pfo64 >> dq) & 0xffffull);
                 const bool same = rw.hash != 0 && rw.hash == hv;
@@ -2349,7 +2350,6 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
                 const float pfp = lam_p * ps.kpf * rw.tokens;
                 const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
                 const uint32_t flip = (uint32_t)((flf[mrow + mw] >> dq) & 0xffffull);
-                const uint32_t ld = (uint32_t)((fll[mrow + mw] >> dq) & 0xffffull);
                 const float *crow = rtab + mw * CS + 2 * dq;
                 // B without the completed parents: cost with the switch term, less the prefix benefit
                 float B[ND];
@@ -2394,15 +2394,18 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
 #pragma unroll
                 for (int d = 0; d < ND; ++d) {
                     const uint32_t fm = (uint32_t)__builtin_amdgcn_sbfe((int)feas, d, 1u);
-                    const float x = __uint_as_float((fm & __float_as_uint(B[d] + xb)) | (~fm & __float_as_uint(inf_f())));
+                    const float x = __uint_as_float((fm & __float_as_uint(B[d])) | (~fm & __float_as_uint(inf_f())));
                     B[d] = x;
                     m2 = __builtin_amdgcn_fmed3f(m1, x, m2);
                     m1 = fminf(m1, x);
                 }
                 quad_two_smallest(m1, m2);
+                // the parents' transfer xb and a child's colocation share (moved
+                // to the outside side) are common to every device: once per row
                 const bool child = depth == 1;
-                const float m1c = child ? m1 + t0 : m1, m2c = child ? m2 + t0 : m2;
                 const float cwc = child ? cw : 0.0f;
+                const float m1c = child ? (m1 + t0) + cw : m1, m2c = child ? (m2 + t0) + cw : m2;
+                fx += gh * (xb - cwc);
                 // devices that gain grp(w) once v runs there
                 const uint32_t gain = same ? (~pfo & qmask) : 0u;
 #pragma unroll
@@ -2411,13 +2414,11 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
 #pragma unroll
                     for (int u = 0; u < 2; ++u) {
                         const int d = 2 * j + u;
-                        const float ksr = u == 0 ? c.y : c.w;
-                        // m(w)'s switch term on d flips when v's Load changes its
-                        // residency there: down by the magnitude when loaded, up when evicted
-                        const float dsw = __uint_as_float((__builtin_amdgcn_ubfe(ld, d, 1u) << 31) |
-                                                          (__float_as_uint(ksr) & (uint32_t)__builtin_amdgcn_sbfe((int)flip, d, 1u)));
+                        // m(w)'s switch term on d changes by the signed magnitude
+                        // where v's Load flips m(w)'s residency there
+                        const float dsw = __uint_as_float(__float_as_uint(u == 0 ? c.y : c.w) & (uint32_t)__builtin_amdgcn_sbfe((int)flip, d, 1u));
                         const float gp = __uint_as_float(__float_as_uint(pfp) & (uint32_t)__builtin_amdgcn_sbfe((int)gain, d, 1u));
-                        const float C = ((B[d] - cwc) + dsw) - gp;
+                        const float C = (B[d] + dsw) - gp;
                         const float o = B[d] == m1 ? m2c : m1c;
                         f[d] += gh * fminf(o, C);
                     }
@@ -2436,7 +2437,7 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
             }
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
-                part4[(dq / 4 + j) * pcol + t] = make_float4(f[4 * j], f[4 * j + 1], f[4 * j + 2], f[4 * j + 3]);
+                part4[(dq / 4 + j) * pcol + t] = make_float4(f[4 * j] + fx, f[4 * j + 1] + fx, f[4 * j + 2] + fx, f[4 * j + 3] + fx);
         }
         __syncthreads();
 
@@ -2450,26 +2451,22 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
                 cnt += local ? 1.0f : 0.0f;
                 tr += local ? 0.0f : s.s0 * b0;
             }
-            for (int q0 = 1; q0 < (int)s.dn; q0 += G) {
-                uint64_t h = 0ull;
-                float sg = 0.0f;
-                if (q0 + lane < (int)s.dn) {
-                    const DoneParent pu = a.done[s.dbeg + q0 + lane];
-                    h = pu.holders;
-                    sg = pu.sigma;
-                }
-                const int nq = min(G, (int)s.dn - q0);
-                for (int j = 0; j < nq; ++j) {
-                    const uint64_t hj = ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(h >> 32), j, G) << 32) |
-                                        (uint64_t)(uint32_t)__shfl((int)(uint32_t)h, j, G);
-                    const float sj = __shfl(sg, j, G);
-                    const bool local = ((hj >> dl) & 1ull) != 0;
+            for (int q0 = 1; q0 < (int)s.dn; q0 += 4) {  // every lane loads the batch (one address per wave), in order
+                DoneParent pb[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (q0 + j < (int)s.dn) pb[j] = a.done[s.dbeg + q0 + j];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (q0 + j >= (int)s.dn) break;
+                    const bool local = ((pb[j].holders >> dl) & 1ull) != 0;
                     cnt += local ? 1.0f : 0.0f;
-                    tr += local ? 0.0f : sj * b0;
+                    tr += local ? 0.0f : pb[j].sigma * b0;
                 }
             }
-            const float ks = rtab[s.model * CS + 2 * dl + 1];
-            const float swo = bit(rho[dl], s.model) ? 0.0f : ks;
+            // the switch term where m(v) is not resident (the row table's
+            // magnitude is negative there)
+            const float swo = bit(rho[dl], s.model) ? 0.0f : -rtab[s.model * CS + 2 * dl + 1];
             const float ex = a.exec[s.model * D + dl];
             const float pf_v = ((s.pfm >> dl) & 1ull) ? ps.kpf * s.tokens : 0.0f;
             const float colo = s.npar ? cnt * fast_rcp((float)s.npar) : 0.0f;
