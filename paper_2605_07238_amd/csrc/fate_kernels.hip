@@ -2424,16 +2424,24 @@ __global__ __launch_bounds__(BLK) void k_rows4(ScoreLaunch a) {
                     }
                 }
             };
-            for (uint32_t r = r0; r < r1; r += 2) {  // two rows' loads in flight together
-                const bool two = r + 1 < r1;
-                const uint32_t e0 = a.desc[se0 + r];
-                const uint32_t e1 = two ? a.desc[se0 + r + 1] : e0;
-                const StageRec w0 = a.rec[e0 & kDescIdMask];
-                const StageRec w1 = a.rec[e1 & kDescIdMask];
-                const uint32_t dn0 = a.done_n[e0 & kDescIdMask];
-                const uint32_t dn1 = a.done_n[e1 & kDescIdMask];
-                row(e0, w0, w0.par_begin, dn0);
-                if (two) row(e1, w1, w1.par_begin, dn1);
+            // one row at a time with the next row's record and completed-parent
+            // count in flight, and the descendant entry after it (a workgroup
+            // has the compute unit to itself, so the lane's own rows hide the
+            // loads' latency)
+            uint32_t e = r0 < r1 ? a.desc[se0 + r0] : 0u;
+            uint32_t en = r0 + 1 < r1 ? a.desc[se0 + r0 + 1] : 0u;
+            StageRec w = a.rec[e & kDescIdMask];
+            uint32_t dn = a.done_n[e & kDescIdMask];
+            for (uint32_t r = r0; r < r1; ++r) {
+                const uint32_t ec = e, dc = dn;
+                const StageRec wc = w;
+                if (r + 1 < r1) {
+                    w = a.rec[en & kDescIdMask];
+                    dn = a.done_n[en & kDescIdMask];
+                    e = en;
+                }
+                if (r + 2 < r1) en = a.desc[se0 + r + 2];
+                row(ec, wc, wc.par_begin, dc);
             }
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
