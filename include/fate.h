@@ -200,6 +200,9 @@ typedef struct {
     const uint32_t *ch_off;               /* [N+1]: children of flat stage g are */
     const uint32_t *ch_idx;               /* ch_idx[ch_off[g] .. ch_off[g+1]), ascending flat ids */
     int64_t max_stages;                   /* stages of the largest instance */
+    const void *row_records;              /* 16-byte row records [N] (group hash, L(v), then A(v) as 16 bits
+                                             | m(v) << 16 | |Pa(v)| << 21), when D <= 16, M <= 32 and no
+                                             stage has more than 2047 parents; else null */
 } fate_dags_t;
 
 /* Packed state of one planning step: plain data pointing into the caller's

@@ -123,11 +123,17 @@ void instance_horizons(const fate_dag_batch_t *g, int b, int H, int levels, uint
 }
 
 struct DagLayout {
-    size_t exec, ksw, beta, weight, cap, fits, stage_off, rec, par, desc_off, desc, desc_w, ch_off, ch_idx, total;
+    size_t exec, ksw, beta, weight, cap, fits, stage_off, rec, rowrec, par, desc_off, desc, desc_w, ch_off, ch_idx, total;
 };
 
+// Whether the batch gets 16-byte row records: the row kernel for at most 16
+// devices and 32 models reads them, and their packed word holds |Pa(v)| in 11 bits.
+inline bool row_records_fit(int D, int M, int64_t max_npar) {
+    return D <= 16 && M <= 32 && max_npar <= fate::kRowRecMaxNpar;
+}
+
 // desc_w (one float per horizon entry) only with level weights
-DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc, bool level_weights) {
+DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc, bool level_weights, bool rows) {
     DagLayout L;
     size_t o = 0;
     L.exec = o; o = align_up(o + sizeof(float) * M * D);
@@ -138,6 +144,7 @@ DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc, b
     L.fits = o; o = align_up(o + sizeof(uint64_t) * M);
     L.stage_off = o; o = align_up(o + sizeof(int64_t) * (B + 1));
     L.rec = o; o = align_up(o + sizeof(StageRec) * N);
+    L.rowrec = o; o = align_up(o + (rows ? sizeof(fate::RowRec) * N : 0));
     L.par = o; o = align_up(o + sizeof(uint32_t) * E);
     L.desc_off = o; o = align_up(o + sizeof(uint32_t) * (N + 1));
     L.desc = o; o = align_up(o + sizeof(uint32_t) * ndesc);
@@ -149,7 +156,8 @@ DagLayout dag_layout(int B, int D, int M, int64_t N, int64_t E, int64_t ndesc, b
 }
 
 struct DagsPlan {
-    int64_t N = 0, E = 0, ndesc = 0;
+    int64_t N = 0, E = 0, ndesc = 0, max_npar = 0;
+    bool rows = false;  // row records (row_records_fit)
     std::vector<uint32_t> count;
     std::vector<std::vector<uint32_t>> lists;  // per instance, when building
 };
@@ -167,6 +175,8 @@ fate_status_t plan_dags(const fate_cluster_t *c, const fate_dag_batch_t *g, cons
     if (H < 0 || H > FATE_MAX_HORIZON) return FATE_ERANGE;
     st = validate_batch(c, g, &p->N, &p->E);
     if (st != FATE_OK) return st;
+    for (int64_t s = 0; s < p->N; ++s) p->max_npar = std::max(p->max_npar, g->par_off[s + 1] - g->par_off[s]);
+    p->rows = row_records_fit(c->D, c->M, p->max_npar);
     p->count.assign(p->N, 0);
     if (keep) p->lists.assign(g->B, {});
     parallel_for(g->B, [&](int64_t b) {
@@ -224,6 +234,7 @@ void fill_dags_handle(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
     out->desc = reinterpret_cast<const uint32_t *>(base + L.desc);
     out->ch_off = reinterpret_cast<const uint32_t *>(base + L.ch_off);
     out->ch_idx = reinterpret_cast<const uint32_t *>(base + L.ch_idx);
+    out->row_records = p.rows ? base + L.rowrec : nullptr;
 }
 
 void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const DagsPlan &p,
@@ -262,6 +273,13 @@ void write_dags_image(const fate_cluster_t *c, const fate_dag_batch_t *g, const 
             r.shard = (uint8_t)g->shard_max[s];
             r.npar = (uint16_t)(g->par_off[s + 1] - g->par_off[s]);
             rec[s] = r;
+            if (p.rows) {
+                fate::RowRec rr;
+                rr.hash = r.hash;
+                rr.tokens = r.tokens;
+                rr.meta = (uint32_t)(r.elig & 0xffffull) | ((uint32_t)r.model << 16) | ((uint32_t)r.npar << 21);
+                reinterpret_cast<fate::RowRec *>(img + L.rowrec)[s] = rr;
+            }
             for (int64_t q = g->par_off[s]; q < g->par_off[s + 1]; ++q) par[q] = (uint32_t)(base + g->par_idx[q]);
         }
         if (n > 0 && !p.lists[b].empty())
@@ -600,7 +618,7 @@ fate_status_t fate_pack_dags_opt_size(const fate_cluster_t *cluster, const fate_
     DagsPlan p;
     fate_status_t st = plan_dags(cluster, dags, *opts, false, &p);
     if (st != FATE_OK) return st;
-    *bytes = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc, opts->level_weights != 0).total;
+    *bytes = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc, opts->level_weights != 0, p.rows).total;
     return FATE_OK;
 }
 
@@ -609,7 +627,7 @@ static fate_status_t build_dags(const fate_cluster_t *cluster, const fate_dag_ba
                                 DagLayout &L) {
     fate_status_t st = plan_dags(cluster, dags, o, true, &p);
     if (st != FATE_OK) return st;
-    L = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc, o.level_weights != 0);
+    L = dag_layout(dags->B, cluster->D, cluster->M, p.N, p.E, p.ndesc, o.level_weights != 0, p.rows);
     if (bytes < L.total) return FATE_ESIZE;
     img.assign(L.total, 0);
     write_dags_image(cluster, dags, p, L, o.level_weights != 0, img.data());
@@ -894,6 +912,7 @@ static fate_status_t score_impl(const fate_dags_t *dags, const fate_state_h *sta
     if (!d_scores) return FATE_EINVAL;
     fate::ScoreLaunch a;
     a.rec = static_cast<const StageRec *>(dags->records);
+    a.rowrec = static_cast<const fate::RowRec *>(dags->row_records);
     a.par_idx = dags->par_idx;
     a.desc_off = dags->desc_off;
     a.desc = dags->desc;

@@ -23,6 +23,17 @@ static_assert(sizeof(StageRec) == 32, "stage record must be 32 bytes");
 
 // A completed parent of a stage as packed per planning step: the devices
 // holding its output and its output size.
+// The fields of a stage that a horizon row reads in the row kernel for at
+// most 16 devices and 32 models, half a stage record: the group hash, L(v),
+// and A(v) (16 bits) | m(v) << 16 (5 bits) | |Pa(v)| << 21 (11 bits).
+struct alignas(16) RowRec {
+    uint64_t hash;
+    float tokens;
+    uint32_t meta;
+};
+static_assert(sizeof(RowRec) == 16, "row record must be 16 bytes");
+constexpr int kRowRecMaxNpar = 2047;
+
 struct alignas(16) DoneParent {
     uint64_t holders;
     float sigma;
@@ -44,6 +55,7 @@ constexpr int kMaxSets = FATE_MAX_SWEEP;
 
 struct ScoreLaunch {
     const StageRec *rec;
+    const RowRec *rowrec;  // row records (null unless D <= 16, M <= 32, |Pa| <= 2047)
     const uint32_t *par_idx;
     const uint32_t *desc_off;
     const uint32_t *desc;
@@ -146,7 +158,7 @@ bool rows_kernel_fits(int D, int K, int M);
 inline bool rows_batch(const fate_dags_t *dags, int max_shard, int K) {
     const int r = dags->max_r < max_shard ? dags->max_r : max_shard;
     return dags->beta_uniform && (r < dags->D ? r : dags->D) <= 1 && dags->levels != FATE_LEVELS_TOPO &&
-           rows_kernel_fits(dags->D, K, dags->M);
+           rows_kernel_fits(dags->D, K, dags->M) && (dags->D > 16 || dags->row_records);
 }
 
 // The dispatch order of per-instance launches: instances by size class of

@@ -1859,15 +1859,16 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
             float f[ND], fx = 0.0f;
 #pragma unroll
             for (int d = 0; d < ND; ++d) f[d] = 0.0f;
-            auto row = [&](uint32_t ent, const StageRec &rw, uint32_t db, uint32_t dn) {
+            // a row from w's row record: group hash, L(w), A(w) | m(w) << 16 | |Pa(w)| << 21
+            auto row = [&](uint32_t ent, const RowRec &rw, uint32_t dn) {
                 const int depth = (int)(ent >> kDescDepthShift);
-                const uint32_t mw = rw.model;
-                const uint32_t feas = (uint32_t)rw.elig & dmask;  // the row table is +infinity where m(w) does not fit
+                const uint32_t mw = (rw.meta >> 16) & 31u;
+                const uint32_t feas = rw.meta & dmask;  // the row table is +infinity where m(w) does not fit
                 const uint32_t pfo = table_find<uint32_t>(L, rw.hash);
                 const bool same = rw.hash != 0 && rw.hash == hv;
                 const float gh = gpow[depth];
                 const float pfp = lam_p * ps.kpf * rw.tokens;
-                const float cw = lam_c * fast_rcp((float)rw.npar);  // a descendant has at least one parent
+                const float cw = lam_c * fast_rcp((float)(rw.meta >> 21));  // a descendant has at least one parent
                 const uint32_t flip = flr[mw] >> 16;
                 const float *crow = rtab + mw * CS;
                 // B without the completed parents: cost with the switch term, less the prefix benefit
@@ -1882,6 +1883,7 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                 // devices holding one its transfer saved and the colocation share
                 float xb = 0.0f;
                 if (dn > 0) {  // the row goes through the task's sum slots, indexed by device
+                    const uint32_t db = a.rec[ent & kDescIdMask].par_begin;  // w's completed-parent slots
 #pragma unroll
                     for (int j = 0; j < NJ; ++j) part4[j * pcol + t] = make_float4(B[4 * j], B[4 * j + 1], B[4 * j + 2], B[4 * j + 3]);
                     for (uint32_t q0 = 0; q0 < dn; q0 += 4) {  // the batch's loads are issued together
@@ -1948,12 +1950,12 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                 const bool two = r + 1 < r1;
                 const uint32_t e0 = a.desc[s.e0 + r];
                 const uint32_t e1 = two ? a.desc[s.e0 + r + 1] : e0;
-                const StageRec w0 = a.rec[e0 & kDescIdMask];
-                const StageRec w1 = a.rec[e1 & kDescIdMask];
+                const RowRec w0 = a.rowrec[e0 & kDescIdMask];
+                const RowRec w1 = a.rowrec[e1 & kDescIdMask];
                 const uint32_t dn0 = a.done_n[e0 & kDescIdMask];
                 const uint32_t dn1 = a.done_n[e1 & kDescIdMask];
-                row(e0, w0, w0.par_begin, dn0);
-                if (two) row(e1, w1, w1.par_begin, dn1);
+                row(e0, w0, dn0);
+                if (two) row(e1, w1, dn1);
             }
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
@@ -2579,6 +2581,7 @@ bool rows_kernel_fits(int D, int K, int M) {
 
 static bool rows_fit(const ScoreLaunch &a) {
     if (!a.beta_uniform || !a.singles || a.topo) return false;
+    if (a.D <= 16 && !a.rowrec) return false;  // k_rows reads the row records
     return rows_kernel_fits(a.D, a.K, a.M);
 }
 

@@ -93,7 +93,7 @@ class Dags(C.Structure):
                 ("records", C.c_void_p), ("par_idx", C.c_void_p), ("desc_off", C.c_void_p),
                 ("desc", C.c_void_p), ("stage_off", C.c_void_p), ("levels", C.c_int32), ("desc_w", C.c_void_p),
                 ("max_r", C.c_int32), ("ch_off", C.c_void_p), ("ch_idx", C.c_void_p),
-                ("max_stages", C.c_int64)]
+                ("max_stages", C.c_int64), ("row_records", C.c_void_p)]
 
 
 class StateH(C.Structure):

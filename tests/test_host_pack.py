@@ -14,6 +14,7 @@ from paper_2605_07238_amd import fate, synth
 
 REC = np.dtype([("elig", "<u8"), ("hash", "<u8"), ("tokens", "<f4"), ("sigma", "<f4"),
                 ("par_begin", "<u4"), ("model", "u1"), ("shard", "u1"), ("npar", "<u2")])
+ROWREC = np.dtype([("hash", "<u8"), ("tokens", "<f4"), ("meta", "<u4")])
 
 
 def _view(buf, base, ptr, dtype, count):
@@ -58,6 +59,18 @@ def test_dags_image_roundtrip(maker):
     assert np.array_equal(u["par"], exp_par.astype(np.uint32))
     fits = [sum(1 << d for d in range(w.D) if w.weight_bytes[m] <= w.cap_bytes[d]) for m in range(w.M)]
     assert u["fits"].tolist() == fits
+    # 16-byte row records (the row kernel for D <= 16, M <= 32): present exactly then
+    npar = np.diff(w.par_off)
+    expect_rows = w.D <= 16 and w.M <= 32 and (len(npar) == 0 or npar.max() <= 2047)
+    assert bool(h.row_records) == expect_rows
+    if expect_rows:
+        rr = _view(buf, buf.ctypes.data, h.row_records, ROWREC, int(h.N))
+        assert np.array_equal(rr["hash"], w.prefix_hash)
+        assert np.array_equal(rr["tokens"], w.prefix_tokens)
+        meta = rr["meta"].astype(np.uint64)
+        assert np.array_equal(meta & 0xFFFF, w.elig & np.uint64(0xFFFF))
+        assert np.array_equal((meta >> 16) & 31, w.model.astype(np.uint64))
+        assert np.array_equal(meta >> 21, npar.astype(np.uint64))
     # descendant lists = breadth-first distances 1..H, ordered by (distance, id)
     for b in range(w.B):
         lo, hi = int(w.stage_off[b]), int(w.stage_off[b + 1])
