@@ -1946,16 +1946,20 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                     }
                 }
             };
-            for (uint32_t r = r0; r < r1; r += 2) {  // two rows' loads in flight together
-                const bool two = r + 1 < r1;
+            for (uint32_t r = r0; r < r1; r += 3) {  // three rows' loads in flight together
+                const bool two = r + 1 < r1, three = r + 2 < r1;
                 const uint32_t e0 = a.desc[s.e0 + r];
                 const uint32_t e1 = two ? a.desc[s.e0 + r + 1] : e0;
+                const uint32_t e2 = three ? a.desc[s.e0 + r + 2] : e0;
                 const RowRec w0 = a.rowrec[e0 & kDescIdMask];
                 const RowRec w1 = a.rowrec[e1 & kDescIdMask];
+                const RowRec w2 = a.rowrec[e2 & kDescIdMask];
                 const uint32_t dn0 = a.done_n[e0 & kDescIdMask];
                 const uint32_t dn1 = a.done_n[e1 & kDescIdMask];
+                const uint32_t dn2 = a.done_n[e2 & kDescIdMask];
                 row(e0, w0, dn0);
                 if (two) row(e1, w1, dn1);
+                if (three) row(e2, w2, dn2);
             }
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
