@@ -1610,8 +1610,10 @@ __host__ __device__ inline RowsPlan rows_plan(int D, int K, int M, int nd, int b
     return q;
 }
 
+// Four waves per SIMD (at most 128 VGPRs): four rows' loads in flight per lane
+// need 129 without the bound, which would leave three.
 template <int ND, int BLK>
-__global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
+__global__ __launch_bounds__(BLK) __attribute__((amdgpu_waves_per_eu(4))) void k_rows(ScoreLaunch a) {
     static_assert(BLK >= kRowsChunk && BLK % 64 == 0, "one thread per stage of a chunk");
     const int b = (int)a.order[blockIdx.x];  // largest frontiers first: the last workgroups to start are short
     const ParamSet ps = a.ps[blockIdx.y];
@@ -1946,20 +1948,20 @@ __global__ __launch_bounds__(BLK) void k_rows(ScoreLaunch a) {
                     }
                 }
             };
-            for (uint32_t r = r0; r < r1; r += 3) {  // three rows' loads in flight together
-                const bool two = r + 1 < r1, three = r + 2 < r1;
-                const uint32_t e0 = a.desc[s.e0 + r];
-                const uint32_t e1 = two ? a.desc[s.e0 + r + 1] : e0;
-                const uint32_t e2 = three ? a.desc[s.e0 + r + 2] : e0;
-                const RowRec w0 = a.rowrec[e0 & kDescIdMask];
-                const RowRec w1 = a.rowrec[e1 & kDescIdMask];
-                const RowRec w2 = a.rowrec[e2 & kDescIdMask];
-                const uint32_t dn0 = a.done_n[e0 & kDescIdMask];
-                const uint32_t dn1 = a.done_n[e1 & kDescIdMask];
-                const uint32_t dn2 = a.done_n[e2 & kDescIdMask];
-                row(e0, w0, dn0);
-                if (two) row(e1, w1, dn1);
-                if (three) row(e2, w2, dn2);
+            for (uint32_t r = r0; r < r1; r += 4) {  // four rows' loads in flight together
+                uint32_t e[4];
+                RowRec w[4];
+                uint32_t dn[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) e[j] = r + j < r1 ? a.desc[s.e0 + r + j] : 0u;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    w[j] = a.rowrec[e[j] & kDescIdMask];
+                    dn[j] = a.done_n[e[j] & kDescIdMask];
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (r + j < r1) row(e[j], w[j], dn[j]);
             }
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
