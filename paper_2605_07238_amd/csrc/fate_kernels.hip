@@ -2038,7 +2038,7 @@ __global__ __launch_bounds__(BLK) __attribute__((amdgpu_waves_per_eu(4))) void k
                 lane_topk16(x, a.topk, a.tk_idx + f * a.topk, a.tk_val + f * a.topk);
             }
         }
-        __syncthreads();  // the next chunk reuses the stage slots and task sums
+        if (c0 + kRowsChunk < nFi) __syncthreads();  // uniform: the next chunk reuses the stage slots and task sums
     }
 }
 
